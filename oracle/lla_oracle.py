@@ -1,0 +1,308 @@
+"""Plain float64 CPU oracle of Looped Latent Attention (LLA), arxiv 2607.15456.
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import this module.  The product path
+(the HIP library and its Python binding) never imports, links or calls it, and
+this module imports nothing from the product package.
+
+Every function is written straight from the paper's definitions, in float64,
+with no blocking, fusion or reordering beyond what the definition states, so
+that it can be checked against the paper by eye.  Notation follows the paper:
+
+* T recurrence steps (loops), D layers, H heads of width d = d_head;
+* per (layer, head, token, axis) the teacher emits T vectors x_1..x_T, stacked
+  loop-major as x = [x_1; ...; x_T] of length T*d            (Sec. 3, Eq. 1);
+* the codec stores c = (x - mu) W_down, c in R^r              (Sec. 3, Eq. 2);
+* loop t is reconstructed as x_hat_t = c W_up,t^T + mu_t      (Sec. 3, Eq. 3);
+* the exact compression ratio is rho = 2 T d / (r_k + r_v)   (Sec. 3, Eq. 4).
+
+Loop indices here are 0-based (l = 0..T-1); the paper's t is l + 1.
+
+Attention itself is the teacher's, unchanged (Sec. 1, caption of the
+architecture figure: reconstruction happens before attention, which is left
+unchanged): s_n = scale * <q, k_n>, a = softmax(s), o = sum_n a_n v_n.
+
+Readings where the paper is silent (all listed in the design doc):
+* the softmax scale is a parameter; the teacher's 1/sqrt(d_head) is the default;
+* no RoPE on this path (the NoPE content path of App. J, where absorption is
+  exact);
+* a decode query attends exactly the N cached latent entries [0, N);
+* a prefill query at absolute position p attends keys n <= p.
+
+Parity pins: see tests/test_oracle_pins.py.  Every function below is pinned
+there by something other than itself (printed values, closed forms, brute
+force in pure Python, special cases that reduce to textbook results).
+"""
+
+from __future__ import annotations
+
+import math
+from fractions import Fraction
+
+import numpy as np
+
+__all__ = [
+    "compression_ratio",
+    "teacher_scalars_per_token_layer",
+    "latent_scalars_per_token_layer",
+    "cache_bytes",
+    "stack_loops",
+    "encode",
+    "reconstruct",
+    "softmax",
+    "attention",
+    "default_scale",
+    "decode_attn",
+    "decode_attn_absorbed",
+    "prefill_attn",
+    "split_partial",
+    "split_merge",
+    "decode_attn_batched",
+    "prefill_attn_batched",
+    "encode_batched",
+]
+
+
+# ---------------------------------------------------------------------------
+# Sec. 3, Eq. 4 and the "Teacher cache" / "Cross-loop codec" paragraphs:
+# scalar accounting of the cache.
+# ---------------------------------------------------------------------------
+
+def compression_ratio(T: int, d_head: int, r_k: int, r_v: int) -> Fraction:
+    """Eq. 4: rho = 2 T H d / ((r_k + r_v) H) = 2 T d / (r_k + r_v), exact."""
+    for name, v in (("T", T), ("d_head", d_head), ("r_k", r_k), ("r_v", r_v)):
+        if int(v) != v or v <= 0:
+            raise ValueError(f"{name} must be a positive integer, got {v!r}")
+    return Fraction(2 * T * d_head, r_k + r_v)
+
+
+def teacher_scalars_per_token_layer(T: int, H: int, d_head: int) -> int:
+    """Sec. 3 "Teacher cache": K and V for every loop and head: 2 T H d scalars."""
+    return 2 * T * H * d_head
+
+
+def latent_scalars_per_token_layer(H: int, r_k: int, r_v: int) -> int:
+    """Sec. 3 "Cross-loop codec": (r_k + r_v) H latent scalars per token per layer."""
+    return (r_k + r_v) * H
+
+
+def cache_bytes(layers: int, heads: int, T: int, d_head: int, r_k: int, r_v: int,
+                tokens: int, elem_bytes: int, latent: bool) -> int:
+    """Bytes of a D-layer cache holding ``tokens`` tokens (Sec. 3; tab:memory)."""
+    per = (latent_scalars_per_token_layer(heads, r_k, r_v) if latent
+           else teacher_scalars_per_token_layer(T, heads, d_head))
+    return layers * per * elem_bytes * tokens
+
+
+# ---------------------------------------------------------------------------
+# Sec. 3, Eqs. 1-3: the codec.
+# ---------------------------------------------------------------------------
+
+def stack_loops(per_loop):
+    """Eq. 1: x = [x_1; ...; x_T], loop-major along the last axis."""
+    return np.concatenate([np.asarray(v, dtype=np.float64) for v in per_loop], axis=-1)
+
+
+def encode(x, mu, w_down):
+    """Eq. 2: c = (x - mu) W_down.
+
+    x: [..., T*d] loop-stacked vectors; mu: [T*d] or None (zero mean);
+    w_down: [T*d, r].  Returns c: [..., r].
+    """
+    x = np.asarray(x, dtype=np.float64)
+    w_down = np.asarray(w_down, dtype=np.float64)
+    if mu is not None:
+        x = x - np.asarray(mu, dtype=np.float64)
+    return x @ w_down
+
+
+def reconstruct(c, w_up_t, mu_t):
+    """Eq. 3: x_hat_t = c W_up,t^T + mu_t.
+
+    c: [..., r]; w_up_t: [d, r] (the loop-t up-projection); mu_t: [d] or None
+    (the loop-t slice of mu).  Returns x_hat_t: [..., d].
+    """
+    c = np.asarray(c, dtype=np.float64)
+    w_up_t = np.asarray(w_up_t, dtype=np.float64)
+    out = c @ w_up_t.T
+    if mu_t is not None:
+        out = out + np.asarray(mu_t, dtype=np.float64)
+    return out
+
+
+# ---------------------------------------------------------------------------
+# The teacher's attention (unchanged by LLA).
+# ---------------------------------------------------------------------------
+
+def default_scale(d_head: int) -> float:
+    """The teacher's softmax scale 1/sqrt(d_head) (reading: the paper leaves
+    attention unchanged and states no other scale)."""
+    return 1.0 / math.sqrt(d_head)
+
+
+def softmax(s):
+    """Softmax along the last axis, max-shifted."""
+    s = np.asarray(s, dtype=np.float64)
+    m = np.max(s, axis=-1, keepdims=True)
+    e = np.exp(s - m)
+    return e / np.sum(e, axis=-1, keepdims=True)
+
+
+def attention(q, K, V, scale):
+    """One query against N keys/values: o = softmax(scale K q)^T V.
+
+    q: [d]; K: [N, d]; V: [N, d_v].  Returns o: [d_v].
+    """
+    q = np.asarray(q, dtype=np.float64)
+    K = np.asarray(K, dtype=np.float64)
+    V = np.asarray(V, dtype=np.float64)
+    if K.shape[0] == 0:
+        raise ValueError("attention over an empty context is undefined")
+    a = softmax(scale * (K @ q))
+    return a @ V
+
+
+# ---------------------------------------------------------------------------
+# Loop-l decode over the latent cache.
+# ---------------------------------------------------------------------------
+
+def decode_attn(q, c_k, c_v, u_k, u_v, mu_k=None, mu_v=None, scale=None):
+    """Loop-l decode attention of one (batch, head) over N cached latents --
+    the plain definition: reconstruct K_l and V_l with Eq. 3 for every cached
+    token, then run the teacher's attention on them.
+
+    q: [d]; c_k: [N, r_k]; c_v: [N, r_v]; u_k: [d, r_k] = W^K_up,l;
+    u_v: [d, r_v] = W^V_up,l; mu_k, mu_v: [d] loop-l slices of the means, or
+    None.  Returns o: [d].
+    """
+    d = np.asarray(q).shape[-1]
+    if scale is None:
+        scale = default_scale(d)
+    K = reconstruct(c_k, u_k, mu_k)
+    V = reconstruct(c_v, u_v, mu_v)
+    return attention(q, K, V, scale)
+
+
+def decode_attn_absorbed(q, c_k, c_v, u_k, u_v, mu_k=None, mu_v=None, scale=None):
+    """The same result through the absorbed identities of App. J
+    ("Absorbed attention"): q^T (W_up c) = (W_up^T q)^T c for the score and
+    sum_i a_i W^V_up c_i = W^V_up sum_i a_i c_i for the value.  With means,
+    Eq. 3 adds q . mu_k to every score and mu_v to the output.
+    """
+    q = np.asarray(q, dtype=np.float64)
+    c_k = np.asarray(c_k, dtype=np.float64)
+    c_v = np.asarray(c_v, dtype=np.float64)
+    u_k = np.asarray(u_k, dtype=np.float64)
+    u_v = np.asarray(u_v, dtype=np.float64)
+    if scale is None:
+        scale = default_scale(q.shape[-1])
+    q_tilde = u_k.T @ q                       # absorbed query, [r_k]
+    s = c_k @ q_tilde
+    if mu_k is not None:
+        s = s + q @ np.asarray(mu_k, dtype=np.float64)
+    a = softmax(scale * s)
+    z = a @ c_v                               # attention-weighted latent, [r_v]
+    o = u_v @ z
+    if mu_v is not None:
+        o = o + np.asarray(mu_v, dtype=np.float64)
+    return o
+
+
+def prefill_attn(Q, c_k, c_v, u_k, u_v, mu_k=None, mu_v=None, scale=None, p0=0):
+    """Causal prefill of M queries at absolute positions p0..p0+M-1 over the
+    latent cache: query m attends keys n <= p0 + m (plain definition, row by
+    row).  Q: [M, d]; c_k: [>= p0+M, r_k]; c_v likewise.  Returns [M, d]."""
+    Q = np.asarray(Q, dtype=np.float64)
+    out = np.empty_like(Q)
+    for m in range(Q.shape[0]):
+        n = p0 + m + 1
+        out[m] = decode_attn(Q[m], c_k[:n], c_v[:n], u_k, u_v, mu_k, mu_v, scale)
+    return out
+
+
+# ---------------------------------------------------------------------------
+# Split-context partials and their merge (the softmax over a union of
+# disjoint key ranges, written as running max / sum / weighted latent).
+# ---------------------------------------------------------------------------
+
+def split_partial(q_tilde_scaled, c_k, c_v):
+    """Partial softmax state of one key range: (m, l, z) with
+    m = max_n s_n, l = sum_n exp(s_n - m), z = sum_n exp(s_n - m) c_v[n],
+    where s_n = <q_tilde_scaled, c_k[n]> (the scale already folded in)."""
+    s = np.asarray(c_k, dtype=np.float64) @ np.asarray(q_tilde_scaled, dtype=np.float64)
+    m = float(np.max(s))
+    e = np.exp(s - m)
+    return m, float(np.sum(e)), e @ np.asarray(c_v, dtype=np.float64)
+
+
+def split_merge(partials):
+    """Merge (m_s, l_s, z_s) partials: m = max m_s, weights w_s = exp(m_s - m),
+    l = sum w_s l_s, z = sum w_s z_s; returns the normalised latent z / l."""
+    m = max(p[0] for p in partials)
+    w = [math.exp(p[0] - m) for p in partials]
+    l_tot = sum(wi * p[1] for wi, p in zip(w, partials))
+    z = sum(wi * p[2] for wi, p in zip(w, partials))
+    return z / l_tot
+
+
+# ---------------------------------------------------------------------------
+# Batched wrappers: plain loops over (batch, head).  Layouts are the logical
+# ones (token-major latents); they say nothing about device layouts.
+# ---------------------------------------------------------------------------
+
+def encode_batched(x, mu, w_down_t):
+    """Eq. 2 for every (batch, token, head).
+
+    x: [B, M, H, T*d]; mu: [H, T*d] or None; w_down_t: [H, r, T*d]
+    (W_down transposed, one per head).  Returns c: [B, H, M, r]."""
+    x = np.asarray(x, dtype=np.float64)
+    w_down_t = np.asarray(w_down_t, dtype=np.float64)
+    B, M, H, _ = x.shape
+    r = w_down_t.shape[1]
+    c = np.empty((B, H, M, r))
+    for b in range(B):
+        for h in range(H):
+            c[b, h] = encode(x[b, :, h, :], None if mu is None else mu[h], w_down_t[h].T)
+    return c
+
+
+def decode_attn_batched(q, c_k, c_v, u_k, u_v, mu_k=None, mu_v=None, scale=None,
+                        ctx_len=None, units=None):
+    """decode_attn for every (b, h) (or only the (b, h) pairs in ``units``).
+
+    q: [B, H, d]; c_k: [B, H, >=N, r_k]; c_v: [B, H, >=N, r_v];
+    u_k: [H, d, r_k]; u_v: [H, d, r_v]; mu_k, mu_v: [H, d] or None;
+    ctx_len: int or per-batch sequence of ints.  Returns [B, H, d] (entries
+    not in ``units`` are NaN)."""
+    q = np.asarray(q, dtype=np.float64)
+    B, H, d = q.shape
+    if ctx_len is None:
+        ctx_len = c_k.shape[2]
+    lens = [int(ctx_len)] * B if np.ndim(ctx_len) == 0 else [int(v) for v in ctx_len]
+    out = np.full((B, H, d), np.nan)
+    todo = units if units is not None else [(b, h) for b in range(B) for h in range(H)]
+    for b, h in todo:
+        n = lens[b]
+        out[b, h] = decode_attn(q[b, h], c_k[b, h, :n], c_v[b, h, :n], u_k[h], u_v[h],
+                                None if mu_k is None else mu_k[h],
+                                None if mu_v is None else mu_v[h], scale)
+    return out
+
+
+def prefill_attn_batched(Q, c_k, c_v, u_k, u_v, mu_k=None, mu_v=None, scale=None, p0=0,
+                         units=None, rows=None):
+    """prefill_attn for every (b, h) (or the given units), optionally only for
+    the query rows in ``rows``.  Q: [B, H, M, d].  Returns [B, H, M, d]
+    (entries not computed are NaN)."""
+    Q = np.asarray(Q, dtype=np.float64)
+    B, H, M, d = Q.shape
+    out = np.full((B, H, M, d), np.nan)
+    todo = units if units is not None else [(b, h) for b in range(B) for h in range(H)]
+    row_list = range(M) if rows is None else rows
+    for b, h in todo:
+        for m in row_list:
+            n = p0 + m + 1
+            out[b, h, m] = decode_attn(Q[b, h, m], c_k[b, h, :n], c_v[b, h, :n], u_k[h], u_v[h],
+                                       None if mu_k is None else mu_k[h],
+                                       None if mu_v is None else mu_v[h], scale)
+    return out
