@@ -1,0 +1,206 @@
+/*
+ * lla.h -- C ABI of the Looped Latent Attention (LLA) latent-cache library for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * LLA (arxiv 2607.15456) stores the KV cache of a weight-tied looped
+ * transformer (T recurrence steps over one stack of D layers, H heads of width
+ * d_head) as one low-rank latent per (layer, head, token) and axis that
+ * jointly covers all T loops:
+ *
+ *   x   = [x_1; ...; x_T]            loop-stacked teacher K or V   (Sec. 3, Eq. 1)
+ *   c   = (x - mu) W_down            latent of rank r              (Sec. 3, Eq. 2)
+ *   x_t = c W_up,t^T + mu_t          loop-t reconstruction         (Sec. 3, Eq. 3)
+ *   rho = 2 T d_head / (r_k + r_v)   exact compression ratio       (Sec. 3, Eq. 4)
+ *
+ * The attention entry points never materialise K or V.  They use the absorbed
+ * form of App. J ("Absorbed attention"): scores q^T (W^K_up c) are computed as
+ * (W^K_up^T q)^T c, and the value path sum_n a_n W^V_up c_n as
+ * W^V_up (sum_n a_n c_n).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Loop indices are 0-based; the caller passes the loop-l parameters.
+ * - All tensor arguments are DEVICE pointers owned by the caller, row-major,
+ *   dense, and 16-byte aligned.  The library keeps no pointer after a call
+ *   returns, allocates no memory and never synchronises: it only enqueues
+ *   kernels on `stream` (a hipStream_t; NULL means the default stream).
+ *   Outputs are valid once the stream has reached that point.
+ * - Every entry point validates all scalar arguments and pointers on the host
+ *   before launching anything.  On any error nothing is launched and no
+ *   output is touched.  NaN/Inf in the data are propagated, not checked.
+ * - dtype arguments take lla_dtype values.  "dtype" is the element type of
+ *   every input tensor of the call (queries, latents, projections, means);
+ *   accumulation is always fp32.
+ * - Calls are stateless and reentrant.  Calls that share a workspace or write
+ *   the same cache region must be ordered by the caller (same stream).
+ *
+ * Latent cache layout (one buffer per layer and axis)
+ * ---------------------------------------------------
+ * A cache of capacity n_max tokens and rank r for B sequences and H heads
+ * holds B*H*n_max*r elements.  Tokens are grouped in pages of
+ * LLA_PAGE_TOKENS = 64 consecutive positions; inside a page the latent is
+ * stored feature-major, so that one feature of 64 consecutive tokens is
+ * contiguous:
+ *
+ *   element (b, h, token n, feature j) lives at index
+ *     ((b*H + h) * n_max + (n/64)*64) * r  +  j*64  +  (n % 64)
+ *
+ * i.e. logical c[b][h][n][j] is stored as c[b][h][n/64][j][n%64].  n_max must
+ * be a multiple of 64.  The stored scalar count is exactly (r_k + r_v) per
+ * (head, token) per layer, so Eq. 4 holds for the resident cache.
+ */
+#ifndef LLA_H_
+#define LLA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LLA_ABI_VERSION 1
+#define LLA_PAGE_TOKENS 64
+#define LLA_MAX_RANK 512
+#define LLA_MAX_SPLITS 64
+
+typedef enum lla_status {
+  LLA_OK = 0,
+  LLA_ERR_INVALID_ARG = 1, /* a size, pointer, alignment or value is invalid */
+  LLA_ERR_UNSUPPORTED = 2, /* valid in the paper's terms, not supported here */
+  LLA_ERR_WORKSPACE = 3,   /* the decode workspace is missing or too small  */
+  LLA_ERR_HIP = 4          /* the HIP runtime reported an error on launch    */
+} lla_status;
+
+typedef enum lla_dtype {
+  LLA_F32 = 0,  /* IEEE binary32 */
+  LLA_BF16 = 1  /* bfloat16 (round-to-nearest-even wherever the library rounds) */
+} lla_dtype;
+
+/* Static, NUL-terminated description of a status code (never NULL). */
+const char* lla_status_string(int status);
+
+/* LLA_ABI_VERSION of the built library. */
+int lla_abi_version(void);
+
+/*
+ * Exact compression ratio, Sec. 3 Eq. 4: rho = 2*T*d_head / (r_k + r_v),
+ * returned as the reduced fraction num/den.  Host only.
+ * Errors: LLA_ERR_INVALID_ARG if any size is <= 0 or an output pointer is NULL.
+ */
+lla_status lla_rho(int64_t T, int64_t d_head, int64_t r_k, int64_t r_v,
+                   int64_t* num, int64_t* den);
+
+/*
+ * Bytes of a `layers`-layer KV cache holding `tokens` tokens (Sec. 3, the
+ * "Teacher cache" and "Cross-loop codec" paragraphs; tab:memory):
+ *   latent == 0 (teacher): layers * 2*T*heads*d_head * elem_bytes * tokens
+ *   latent != 0 (LLA):     layers * (r_k + r_v)*heads * elem_bytes * tokens
+ * Host only.  Errors: LLA_ERR_INVALID_ARG for non-positive sizes (tokens may
+ * be 0), a NULL output, or a result that overflows int64.
+ */
+lla_status lla_cache_bytes(int64_t layers, int64_t heads, int64_t T, int64_t d_head,
+                           int64_t r_k, int64_t r_v, int64_t tokens, int64_t elem_bytes,
+                           int latent, int64_t* bytes);
+
+/*
+ * Encode / cache write, Sec. 3 Eq. 2 (with Eq. 1's loop-major stacking):
+ *   c[b][h][pos0+m][:] = (x[b][m][h][:] - mu[h][:]) W_down[h]
+ * for both axes (K with rank r_k, V with rank r_v), every sequence b < B,
+ * new token m < M and head h < H.
+ *
+ *   x_k, x_v   [B][M][H][T*d_head]  loop-stacked K/V of the new tokens
+ *                                    (element i = l*d_head + e is loop l,
+ *                                    channel e)
+ *   mu_k, mu_v [H][T*d_head] or NULL (NULL means a zero mean)
+ *   wdt_k      [H][r_k][T*d_head]   W_down^T for K, one per head
+ *   wdt_v      [H][r_v][T*d_head]   W_down^T for V
+ *   c_k, c_v   latent caches in the paged layout above, capacity n_max
+ *
+ * All inputs and both caches have element type `dtype`.  Results are rounded
+ * once, from the fp32 accumulator, to the cache type (RNE for bf16).  Cache
+ * slots outside [pos0, pos0+M) are not touched.
+ * Requires B, M, H, T >= 1; d_head a multiple of 32 in [32, 256];
+ * 1 <= r_k, r_v <= LLA_MAX_RANK; n_max a multiple of 64; pos0 >= 0 and
+ * pos0 + M <= n_max.
+ * Errors: LLA_ERR_INVALID_ARG, LLA_ERR_HIP.
+ */
+lla_status lla_encode(int dtype, int B, int M, int H, int T, int d_head, int r_k, int r_v,
+                      const void* x_k, const void* x_v, const void* mu_k, const void* mu_v,
+                      const void* wdt_k, const void* wdt_v, void* c_k, void* c_v,
+                      int n_max, int pos0, void* stream);
+
+/*
+ * Workspace bytes lla_decode_attn needs to split the context of every
+ * (b, h) across workgroups (split-K) for these sizes.  Depends only on the
+ * arguments.  Host only.  Errors: LLA_ERR_INVALID_ARG.
+ */
+lla_status lla_decode_workspace_bytes(int B, int H, int r_v, int n_ctx, size_t* bytes);
+
+/*
+ * Loop-l decode attention over the latent cache, absorbed form (App. J):
+ *   q~    = U_k^T q                                  [r_k]
+ *   s_n   = scale * (q~ . c_k[n] + q . mu_k)         n < N_b
+ *   a     = softmax(s)
+ *   out   = U_v (sum_n a_n c_v[n]) + mu_v            [d_head]
+ * which equals the teacher's attention over the Eq. 3 reconstructions
+ * K_l[n] = U_k c_k[n] + mu_k, V_l[n] = U_v c_v[n] + mu_v.  The q . mu_k term
+ * is the same for every n, so it cancels inside the softmax; the kernels do
+ * not compute it (the result is the same in exact arithmetic).
+ *
+ *   q          [B][H][d_head]       loop-l queries
+ *   c_k, c_v   latent caches (paged layout), ranks r_k / r_v, capacity n_max
+ *   u_k        [H][d_head][r_k]     W^K_up,l  (Eq. 3's W_up,t for this loop)
+ *   u_v        [H][d_head][r_v]     W^V_up,l
+ *   mu_k, mu_v [H][d_head] or NULL  loop-l slices mu_t of the means
+ *   ctx_len    device int32 [B] or NULL: N_b, the number of cached tokens
+ *              sequence b attends (positions [0, N_b)); NULL means N_b = n_ctx
+ *              for every b.  An entry outside [1, n_ctx] makes that
+ *              sequence's outputs NaN.
+ *   scale      softmax scale (the teacher's is 1/sqrt(d_head)); finite, > 0
+ *   out        [B][H][d_head] of out_dtype (LLA_F32 or LLA_BF16)
+ *   workspace  device buffer of ws_bytes >= lla_decode_workspace_bytes(), or
+ *              NULL with ws_bytes == 0 (the context is then not split across
+ *              workgroups).  Its first 4*B*H bytes are arrival counters that
+ *              must be zero before the first call (zero the buffer once after
+ *              allocating it); every call leaves them zero again.
+ *
+ * Requires 1 <= n_ctx <= n_max, n_max a multiple of 64, d_head a multiple of
+ * 32 in [32, 256], 1 <= r_k, r_v <= LLA_MAX_RANK.
+ * Errors: LLA_ERR_INVALID_ARG, LLA_ERR_WORKSPACE, LLA_ERR_HIP.
+ */
+lla_status lla_decode_attn(int dtype, int out_dtype, int B, int H, int d_head, int r_k, int r_v,
+                           int n_max, int n_ctx, const int32_t* ctx_len, const void* q,
+                           const void* c_k, const void* c_v, const void* u_k, const void* u_v,
+                           const void* mu_k, const void* mu_v, float scale, void* out,
+                           void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * Causal prefill attention at loop l over the latent cache (absorbed form,
+ * App. J; pass 2 of the two-pass decoder of App. A reads the cache this way):
+ * query m of sequence b sits at absolute position p0 + m and attends the
+ * cached tokens n <= p0 + m, i.e. row m equals lla_decode_attn with
+ * N = p0 + m + 1.  The cache must already hold positions [0, p0 + M) (write
+ * them with lla_encode first).
+ *
+ *   q    [B][H][M][d_head]   loop-l queries
+ *   out  [B][H][M][d_head]   of out_dtype
+ *   other arguments as for lla_decode_attn.
+ *
+ * Requires M >= 1, p0 >= 0, p0 + M <= n_max, and the decode size limits.
+ * With dtype LLA_BF16 the contractions run on bf16 MFMA: the absorbed query,
+ * the softmax weights and the normalised latent are rounded to bf16 before
+ * their products (fp32 accumulation throughout).
+ * Errors: LLA_ERR_INVALID_ARG, LLA_ERR_UNSUPPORTED (bf16 with r_k or r_v
+ * above 64), LLA_ERR_HIP.
+ */
+lla_status lla_prefill_attn(int dtype, int out_dtype, int B, int H, int M, int d_head, int r_k,
+                            int r_v, int n_max, int p0, const void* q, const void* c_k,
+                            const void* c_v, const void* u_k, const void* u_v, const void* mu_k,
+                            const void* mu_v, float scale, void* out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LLA_H_ */

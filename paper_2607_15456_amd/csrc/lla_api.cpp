@@ -1,0 +1,293 @@
+// C ABI of the LLA latent-cache library: host-side validation, split-K
+// heuristic and kernel dispatch.  Every check runs before any HIP call, so an
+// invalid call launches nothing and touches no output.
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstdlib>
+#include <limits>
+
+#include "../../include/lla.h"
+#include "lla_internal.h"
+
+namespace {
+
+constexpr double kLog2e = 1.4426950408889634;
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool ptr_ok(const void* p) { return p != nullptr && aligned16(p); }
+bool opt_ptr_ok(const void* p) { return p == nullptr || aligned16(p); }
+bool dtype_ok(int t) { return t == LLA_F32 || t == LLA_BF16; }
+bool head_ok(int d) { return d >= 32 && d <= 256 && d % 32 == 0; }
+bool rank_ok(int r) { return r >= 1 && r <= LLA_MAX_RANK; }
+bool cap_ok(int n_max) { return n_max >= LLA_PAGE_TOKENS && n_max % LLA_PAGE_TOKENS == 0; }
+
+int64_t gcd64(int64_t a, int64_t b) {
+  while (b) {
+    const int64_t t = a % b;
+    a = b;
+    b = t;
+  }
+  return a;
+}
+
+bool mul_ok(int64_t a, int64_t b, int64_t* out) {
+  if (a != 0 && b > std::numeric_limits<int64_t>::max() / a) return false;
+  *out = a * b;
+  return true;
+}
+
+int max_splits(int n_ctx) {
+  const int pages = (n_ctx + LLA_PAGE_TOKENS - 1) / LLA_PAGE_TOKENS;
+  return pages < LLA_MAX_SPLITS ? pages : LLA_MAX_SPLITS;
+}
+
+size_t workspace_bytes(int B, int H, int r_v, int n_ctx) {
+  const size_t units = (size_t)B * H;
+  const size_t counters = (units * sizeof(uint32_t) + 255) / 256 * 256;
+  return counters + units * (size_t)max_splits(n_ctx) * (size_t)(r_v + 2) * sizeof(float);
+}
+
+// Number of workgroups each (b, h) context is split over: enough workgroups
+// to give every compute unit several, while each wave still scans at least
+// two pages.  LLA_DECODE_SPLITS overrides it (for tuning sweeps).
+int choose_splits(int units, int n_ctx) {
+  static const int forced = [] {
+    const char* e = std::getenv("LLA_DECODE_SPLITS");
+    return e ? std::atoi(e) : 0;
+  }();
+  const int pages = (n_ctx + LLA_PAGE_TOKENS - 1) / LLA_PAGE_TOKENS;
+  int s;
+  if (forced > 0) {
+    s = forced;
+  } else {
+    const int target = 4 * lla::device_cu_count();
+    s = (target + units - 1) / units;
+    const int min_pages = 8;  // 4 waves x 2 pages
+    const int cap = pages / min_pages > 0 ? pages / min_pages : 1;
+    if (s > cap) s = cap;
+  }
+  if (s > max_splits(n_ctx)) s = max_splits(n_ctx);
+  if (s < 1) s = 1;
+  return s;
+}
+
+lla_status hip_status(hipError_t e) { return e == hipSuccess ? LLA_OK : LLA_ERR_HIP; }
+
+}  // namespace
+
+namespace lla {
+int device_cu_count() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
+}  // namespace lla
+
+extern "C" {
+
+const char* lla_status_string(int status) {
+  switch (status) {
+    case LLA_OK: return "LLA_OK: success";
+    case LLA_ERR_INVALID_ARG: return "LLA_ERR_INVALID_ARG: invalid size, pointer, alignment or value";
+    case LLA_ERR_UNSUPPORTED: return "LLA_ERR_UNSUPPORTED: valid arguments not supported by this build";
+    case LLA_ERR_WORKSPACE: return "LLA_ERR_WORKSPACE: decode workspace missing or too small";
+    case LLA_ERR_HIP: return "LLA_ERR_HIP: the HIP runtime reported an error";
+    default: return "unknown lla_status";
+  }
+}
+
+int lla_abi_version(void) { return LLA_ABI_VERSION; }
+
+lla_status lla_rho(int64_t T, int64_t d_head, int64_t r_k, int64_t r_v, int64_t* num,
+                   int64_t* den) {
+  if (T <= 0 || d_head <= 0 || r_k <= 0 || r_v <= 0 || !num || !den) return LLA_ERR_INVALID_ARG;
+  int64_t n;
+  if (!mul_ok(2 * T, d_head, &n) || r_k > std::numeric_limits<int64_t>::max() - r_v)
+    return LLA_ERR_INVALID_ARG;
+  const int64_t d = r_k + r_v;
+  const int64_t g = gcd64(n, d);
+  *num = n / g;
+  *den = d / g;
+  return LLA_OK;
+}
+
+lla_status lla_cache_bytes(int64_t layers, int64_t heads, int64_t T, int64_t d_head, int64_t r_k,
+                           int64_t r_v, int64_t tokens, int64_t elem_bytes, int latent,
+                           int64_t* bytes) {
+  if (layers <= 0 || heads <= 0 || T <= 0 || d_head <= 0 || r_k <= 0 || r_v <= 0 || tokens < 0 ||
+      elem_bytes <= 0 || !bytes)
+    return LLA_ERR_INVALID_ARG;
+  int64_t per = 0, v = 0;
+  if (latent) {
+    if (!mul_ok(r_k + r_v, heads, &per)) return LLA_ERR_INVALID_ARG;
+  } else {
+    if (!mul_ok(2 * T, heads, &per) || !mul_ok(per, d_head, &per)) return LLA_ERR_INVALID_ARG;
+  }
+  if (!mul_ok(layers, per, &v) || !mul_ok(v, elem_bytes, &v) || !mul_ok(v, tokens, &v))
+    return LLA_ERR_INVALID_ARG;
+  *bytes = v;
+  return LLA_OK;
+}
+
+lla_status lla_encode(int dtype, int B, int M, int H, int T, int d_head, int r_k, int r_v,
+                      const void* x_k, const void* x_v, const void* mu_k, const void* mu_v,
+                      const void* wdt_k, const void* wdt_v, void* c_k, void* c_v, int n_max,
+                      int pos0, void* stream) {
+  if (!dtype_ok(dtype) || B < 1 || M < 1 || H < 1 || T < 1 || !head_ok(d_head) || !rank_ok(r_k) ||
+      !rank_ok(r_v) || !cap_ok(n_max) || pos0 < 0 || (int64_t)pos0 + M > n_max)
+    return LLA_ERR_INVALID_ARG;
+  if ((int64_t)T * d_head > (1 << 20) || (int64_t)B * M > (1 << 30)) return LLA_ERR_INVALID_ARG;
+  if (!ptr_ok(x_k) || !ptr_ok(x_v) || !ptr_ok(wdt_k) || !ptr_ok(wdt_v) || !ptr_ok(c_k) ||
+      !ptr_ok(c_v) || !opt_ptr_ok(mu_k) || !opt_ptr_ok(mu_v))
+    return LLA_ERR_INVALID_ARG;
+  lla::EncodeArgs a{};
+  a.dtype = dtype;
+  a.B = B;
+  a.M = M;
+  a.H = H;
+  a.K = T * d_head;
+  a.r[0] = r_k;
+  a.r[1] = r_v;
+  a.x[0] = x_k;
+  a.x[1] = x_v;
+  a.mu[0] = mu_k;
+  a.mu[1] = mu_v;
+  a.wdt[0] = wdt_k;
+  a.wdt[1] = wdt_v;
+  a.c[0] = c_k;
+  a.c[1] = c_v;
+  a.n_max = n_max;
+  a.pos0 = pos0;
+  return hip_status(lla::launch_encode(a, static_cast<hipStream_t>(stream)));
+}
+
+lla_status lla_decode_workspace_bytes(int B, int H, int r_v, int n_ctx, size_t* bytes) {
+  if (B < 1 || H < 1 || !rank_ok(r_v) || n_ctx < 1 || !bytes) return LLA_ERR_INVALID_ARG;
+  *bytes = workspace_bytes(B, H, r_v, n_ctx);
+  return LLA_OK;
+}
+
+lla_status lla_decode_attn(int dtype, int out_dtype, int B, int H, int d_head, int r_k, int r_v,
+                           int n_max, int n_ctx, const int32_t* ctx_len, const void* q,
+                           const void* c_k, const void* c_v, const void* u_k, const void* u_v,
+                           const void* mu_k, const void* mu_v, float scale, void* out,
+                           void* workspace, size_t ws_bytes, void* stream) {
+  if (!dtype_ok(dtype) || !dtype_ok(out_dtype) || B < 1 || H < 1 || !head_ok(d_head) ||
+      !rank_ok(r_k) || !rank_ok(r_v) || !cap_ok(n_max) || n_ctx < 1 || n_ctx > n_max ||
+      !std::isfinite(scale) || !(scale > 0.f))
+    return LLA_ERR_INVALID_ARG;
+  if ((int64_t)B * H > (1 << 24)) return LLA_ERR_INVALID_ARG;
+  if (!ptr_ok(q) || !ptr_ok(c_k) || !ptr_ok(c_v) || !ptr_ok(u_k) || !ptr_ok(u_v) || !ptr_ok(out) ||
+      !opt_ptr_ok(mu_k) || !opt_ptr_ok(mu_v) ||
+      (ctx_len && (reinterpret_cast<uintptr_t>(ctx_len) & 3u)))
+    return LLA_ERR_INVALID_ARG;
+  if ((workspace == nullptr) != (ws_bytes == 0)) return LLA_ERR_WORKSPACE;
+  if (workspace && (!aligned16(workspace) || ws_bytes < workspace_bytes(B, H, r_v, n_ctx)))
+    return LLA_ERR_WORKSPACE;
+  (void)mu_k;  // q . mu_k is constant over the context: it cancels in the softmax
+
+  lla::DecodeArgs a{};
+  a.dtype = dtype;
+  a.out_dtype = out_dtype;
+  a.B = B;
+  a.H = H;
+  a.d = d_head;
+  a.rk = r_k;
+  a.rv = r_v;
+  a.n_max = n_max;
+  a.n_ctx = n_ctx;
+  a.M = 1;
+  a.p0 = 0;
+  a.causal = 0;
+  a.ctx_len = ctx_len;
+  a.q = q;
+  a.ck = c_k;
+  a.cv = c_v;
+  a.uk = u_k;
+  a.uv = u_v;
+  a.muv = mu_v;
+  a.qscale = (float)((double)scale * kLog2e);
+  a.out = out;
+  a.splits = workspace ? choose_splits(B * H, n_ctx) : 1;
+  if (a.splits > 1) {
+    const size_t units = (size_t)B * H;
+    const size_t counters = (units * sizeof(uint32_t) + 255) / 256 * 256;
+    a.cnt = static_cast<uint32_t*>(workspace);
+    a.part = reinterpret_cast<float*>(static_cast<char*>(workspace) + counters);
+  }
+  return hip_status(lla::launch_decode(a, static_cast<hipStream_t>(stream)));
+}
+
+lla_status lla_prefill_attn(int dtype, int out_dtype, int B, int H, int M, int d_head, int r_k,
+                            int r_v, int n_max, int p0, const void* q, const void* c_k,
+                            const void* c_v, const void* u_k, const void* u_v, const void* mu_k,
+                            const void* mu_v, float scale, void* out, void* stream) {
+  if (!dtype_ok(dtype) || !dtype_ok(out_dtype) || B < 1 || H < 1 || M < 1 || !head_ok(d_head) ||
+      !rank_ok(r_k) || !rank_ok(r_v) || !cap_ok(n_max) || p0 < 0 || (int64_t)p0 + M > n_max ||
+      !std::isfinite(scale) || !(scale > 0.f))
+    return LLA_ERR_INVALID_ARG;
+  if ((int64_t)B * H * M > (1 << 30)) return LLA_ERR_INVALID_ARG;
+  if (!ptr_ok(q) || !ptr_ok(c_k) || !ptr_ok(c_v) || !ptr_ok(u_k) || !ptr_ok(u_v) || !ptr_ok(out) ||
+      !opt_ptr_ok(mu_k) || !opt_ptr_ok(mu_v))
+    return LLA_ERR_INVALID_ARG;
+  (void)mu_k;  // q . mu_k is constant over the keys of a query: it cancels in the softmax
+  const float qscale = (float)((double)scale * kLog2e);
+  if (dtype == LLA_BF16) {
+    if (r_k > 64 || r_v > 64) return LLA_ERR_UNSUPPORTED;
+    lla::PrefillArgs a{};
+    a.out_dtype = out_dtype;
+    a.B = B;
+    a.H = H;
+    a.M = M;
+    a.d = d_head;
+    a.rk = r_k;
+    a.rv = r_v;
+    a.n_max = n_max;
+    a.p0 = p0;
+    a.q = q;
+    a.ck = c_k;
+    a.cv = c_v;
+    a.uk = u_k;
+    a.uv = u_v;
+    a.muv = mu_v;
+    a.qscale = qscale;
+    a.out = out;
+    return hip_status(lla::launch_prefill_bf16(a, static_cast<hipStream_t>(stream)));
+  }
+  // fp32: the decode scan, one workgroup per query, query m over [0, p0 + m].
+  lla::DecodeArgs a{};
+  a.dtype = dtype;
+  a.out_dtype = out_dtype;
+  a.B = B;
+  a.H = H;
+  a.d = d_head;
+  a.rk = r_k;
+  a.rv = r_v;
+  a.n_max = n_max;
+  a.n_ctx = p0 + M;
+  a.M = M;
+  a.p0 = p0;
+  a.causal = 1;
+  a.splits = 1;
+  a.q = q;
+  a.ck = c_k;
+  a.cv = c_v;
+  a.uk = u_k;
+  a.uv = u_v;
+  a.muv = mu_v;
+  a.qscale = qscale;
+  a.out = out;
+  return hip_status(lla::launch_decode(a, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

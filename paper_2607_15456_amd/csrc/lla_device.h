@@ -1,0 +1,65 @@
+// Device-side helpers shared by the LLA HIP kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace lla {
+
+constexpr int kPage = 64;      // tokens per cache page (feature-major inside a page)
+constexpr int kWave = 64;      // CDNA wavefront width
+constexpr int kMaxRank = 512;  // largest r_k / r_v accepted
+constexpr int kMaxHead = 256;  // largest d_head accepted
+
+typedef uint16_t bf16_t;  // bfloat16 storage
+
+// ---- bf16 <-> fp32 -------------------------------------------------------
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+__device__ __forceinline__ float bf16_to_f32(bf16_t h) { return __uint_as_float(uint32_t(h) << 16); }
+
+// Round-to-nearest-even fp32 -> bf16; NaN stays NaN (quiet bit set).
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return bf16_t((u >> 16) | 0x0040u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return bf16_t(u >> 16);
+}
+
+// Element access for the two input types.
+template <typename T> struct Elem;
+template <> struct Elem<float> {
+  static constexpr int kPer16B = 4;
+  __device__ __forceinline__ static float get(const float* p, size_t i) { return p[i]; }
+  __device__ __forceinline__ static void unpack(const uint4& v, float (&o)[4]) {
+    o[0] = __uint_as_float(v.x); o[1] = __uint_as_float(v.y);
+    o[2] = __uint_as_float(v.z); o[3] = __uint_as_float(v.w);
+  }
+};
+template <> struct Elem<bf16_t> {
+  static constexpr int kPer16B = 8;
+  __device__ __forceinline__ static float get(const bf16_t* p, size_t i) { return bf16_to_f32(p[i]); }
+  __device__ __forceinline__ static void unpack(const uint4& v, float (&o)[8]) {
+    o[0] = bf16_lo(v.x); o[1] = bf16_hi(v.x); o[2] = bf16_lo(v.y); o[3] = bf16_hi(v.y);
+    o[4] = bf16_lo(v.z); o[5] = bf16_hi(v.z); o[6] = bf16_lo(v.w); o[7] = bf16_hi(v.w);
+  }
+};
+
+template <typename T> __device__ __forceinline__ void store_out(T* p, size_t i, float v);
+template <> __device__ __forceinline__ void store_out<float>(float* p, size_t i, float v) { p[i] = v; }
+template <> __device__ __forceinline__ void store_out<bf16_t>(bf16_t* p, size_t i, float v) {
+  p[i] = f32_to_bf16(v);
+}
+
+__device__ __forceinline__ uint4 ld16(const void* p) {
+  return *reinterpret_cast<const uint4*>(p);
+}
+
+// ---- cross-lane ----------------------------------------------------------
+
+__device__ __forceinline__ float xor_shfl(float v, int mask) { return __shfl_xor(v, mask, kWave); }
+
+__device__ __forceinline__ float neg_inf() { return -__builtin_inff(); }
+
+}  // namespace lla

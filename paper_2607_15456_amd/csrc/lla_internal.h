@@ -1,0 +1,65 @@
+// Internal launch interface between the C ABI (lla_api.cpp) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace lla {
+
+// Decode (and the fp32 causal multi-query path used by prefill).
+struct DecodeArgs {
+  int dtype;      // LLA_F32 / LLA_BF16: element type of every input
+  int out_dtype;  // element type of out
+  int B, H, d, rk, rv, n_max, n_ctx;
+  int M;       // queries per (b, h): 1 for decode
+  int p0;      // causal mode: position of query 0
+  int causal;  // 0: decode (N_b from ctx_len / n_ctx); 1: query m attends [0, p0+m]
+  int splits;  // workgroups per (b, h, m) along the context
+  const int32_t* ctx_len;
+  const void* q;
+  const void* ck;
+  const void* cv;
+  const void* uk;
+  const void* uv;
+  const void* muv;
+  float qscale;  // softmax scale * log2(e)
+  void* out;
+  float* part;    // [units][splits][rv + 2] split partials (m, l, z)
+  uint32_t* cnt;  // [units] arrival counters
+};
+
+hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
+
+struct EncodeArgs {
+  int dtype;
+  int B, M, H, K;  // K = T * d_head
+  int r[2];
+  const void* x[2];
+  const void* mu[2];
+  const void* wdt[2];
+  void* c[2];
+  int n_max, pos0;
+};
+
+hipError_t launch_encode(const EncodeArgs& a, hipStream_t stream);
+
+struct PrefillArgs {
+  int out_dtype;
+  int B, H, M, d, rk, rv, n_max, p0;
+  const void* q;
+  const void* ck;
+  const void* cv;
+  const void* uk;
+  const void* uv;
+  const void* muv;
+  float qscale;
+  void* out;
+};
+
+// bf16 MFMA causal prefill.
+hipError_t launch_prefill_bf16(const PrefillArgs& a, hipStream_t stream);
+
+int device_cu_count();  // compute units of the current device (cached)
+
+}  // namespace lla

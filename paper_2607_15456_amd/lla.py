@@ -1,0 +1,264 @@
+"""Thin Python binding of liblla.so (argument marshalling only).
+
+Every entry point forwards torch tensors' device pointers and the current HIP
+stream to the C ABI declared in include/lla.h; all computation happens in the
+library's HIP kernels.  Torch provides device memory and streams only.
+
+Latent caches are torch tensors of shape [B, H, n_max // 64, r, 64] -- the
+paged, feature-major layout the kernels use (logical c[b][h][n][j] is
+element [b, h, n // 64, j, n % 64]).  ``to_paged`` / ``from_paged`` convert
+between that layout and a token-major [B, H, N, r] tensor (pure views and
+copies, no arithmetic).
+"""
+
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from fractions import Fraction
+
+import torch
+
+PAGE = 64
+MAX_RANK = 512
+MAX_SPLITS = 64
+
+LLA_OK, LLA_ERR_INVALID_ARG, LLA_ERR_UNSUPPORTED, LLA_ERR_WORKSPACE, LLA_ERR_HIP = range(5)
+LLA_F32, LLA_BF16 = 0, 1
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblla.so")
+
+_c_int, _c_i64, _c_vp, _c_f, _c_sz = (ctypes.c_int, ctypes.c_int64, ctypes.c_void_p,
+                                      ctypes.c_float, ctypes.c_size_t)
+
+_SIGS = {
+    "lla_status_string": (ctypes.c_char_p, [_c_int]),
+    "lla_abi_version": (_c_int, []),
+    "lla_rho": (_c_int, [_c_i64] * 4 + [ctypes.POINTER(_c_i64)] * 2),
+    "lla_cache_bytes": (_c_int, [_c_i64] * 8 + [_c_int, ctypes.POINTER(_c_i64)]),
+    "lla_encode": (_c_int, [_c_int] * 8 + [_c_vp] * 8 + [_c_int, _c_int, _c_vp]),
+    "lla_decode_workspace_bytes": (_c_int, [_c_int] * 4 + [ctypes.POINTER(_c_sz)]),
+    "lla_decode_attn": (_c_int, [_c_int] * 9 + [_c_vp] * 8 + [_c_f, _c_vp, _c_vp, _c_sz, _c_vp]),
+    "lla_prefill_attn": (_c_int, [_c_int] * 10 + [_c_vp] * 7 + [_c_f, _c_vp, _c_vp]),
+}
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load liblla.so (built in-tree by paper_2607_15456_amd.build)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2607_15456_amd.build`")
+        h = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            fn = getattr(h, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = h
+    return _lib
+
+
+class LLAError(RuntimeError):
+    def __init__(self, status: int):
+        self.status = status
+        super().__init__(status_string(status))
+
+
+def status_string(status: int) -> str:
+    return lib().lla_status_string(int(status)).decode()
+
+
+def _check(status: int) -> None:
+    if status != LLA_OK:
+        raise LLAError(status)
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return LLA_F32
+    if t.dtype == torch.bfloat16:
+        return LLA_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}; use float32 or bfloat16")
+
+
+def _out_code(dtype: torch.dtype) -> int:
+    return {torch.float32: LLA_F32, torch.bfloat16: LLA_BF16}[dtype]
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(t: torch.Tensor):
+    return torch.cuda.current_stream(t.device).cuda_stream
+
+
+def _need(t: torch.Tensor, name: str, dtype=None, device=None):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+
+
+# ---------------------------------------------------------------------------
+# Host-only helpers
+# ---------------------------------------------------------------------------
+
+def abi_version() -> int:
+    return lib().lla_abi_version()
+
+
+def rho(T: int, d_head: int, r_k: int, r_v: int) -> Fraction:
+    """Exact compression ratio (Sec. 3, Eq. 4) from the library."""
+    n, d = _c_i64(), _c_i64()
+    _check(lib().lla_rho(T, d_head, r_k, r_v, ctypes.byref(n), ctypes.byref(d)))
+    return Fraction(n.value, d.value)
+
+
+def cache_bytes(layers, heads, T, d_head, r_k, r_v, tokens, elem_bytes, latent) -> int:
+    out = _c_i64()
+    _check(lib().lla_cache_bytes(layers, heads, T, d_head, r_k, r_v, tokens, elem_bytes,
+                                 1 if latent else 0, ctypes.byref(out)))
+    return out.value
+
+
+def decode_workspace_bytes(B: int, H: int, r_v: int, n_ctx: int) -> int:
+    out = _c_sz()
+    _check(lib().lla_decode_workspace_bytes(B, H, r_v, n_ctx, ctypes.byref(out)))
+    return out.value
+
+
+# ---------------------------------------------------------------------------
+# Cache layout helpers (views and copies only)
+# ---------------------------------------------------------------------------
+
+def alloc_cache(B, H, n_max, r, dtype=torch.bfloat16, device="cuda", zero=False):
+    if n_max % PAGE:
+        raise ValueError("n_max must be a multiple of 64")
+    shape = (B, H, n_max // PAGE, r, PAGE)
+    return torch.zeros(shape, dtype=dtype, device=device) if zero else torch.empty(shape, dtype=dtype, device=device)
+
+
+def to_paged(c: torch.Tensor, n_max: int) -> torch.Tensor:
+    """[B, H, N, r] token-major -> [B, H, n_max/64, r, 64] paged (positions >= N are zero)."""
+    B, H, N, r = c.shape
+    if n_max % PAGE or N > n_max:
+        raise ValueError("n_max must be a multiple of 64 and >= N")
+    full = c.new_zeros((B, H, n_max, r))
+    full[:, :, :N] = c
+    return full.view(B, H, n_max // PAGE, PAGE, r).transpose(-1, -2).contiguous()
+
+
+def from_paged(pages: torch.Tensor, n: int | None = None) -> torch.Tensor:
+    """[B, H, n_max/64, r, 64] paged -> [B, H, n, r] token-major."""
+    B, H, P, r, _ = pages.shape
+    out = pages.transpose(-1, -2).reshape(B, H, P * PAGE, r)
+    return out if n is None else out[:, :, :n]
+
+
+def new_workspace(B: int, H: int, r_v: int, n_ctx: int, device="cuda") -> torch.Tensor:
+    """A zeroed decode workspace (its arrival counters must start at zero)."""
+    return torch.zeros(decode_workspace_bytes(B, H, r_v, n_ctx), dtype=torch.uint8, device=device)
+
+
+# ---------------------------------------------------------------------------
+# Device entry points
+# ---------------------------------------------------------------------------
+
+def encode(x_k, x_v, wdt_k, wdt_v, c_k, c_v, *, T: int, pos0: int, mu_k=None, mu_v=None):
+    """Write (x - mu) W_down for both axes into cache slots [pos0, pos0 + M) (Eq. 2).
+
+    x_k, x_v: [B, M, H, T*d]; wdt_k: [H, r_k, T*d]; wdt_v: [H, r_v, T*d];
+    mu_k, mu_v: [H, T*d] or None; c_k, c_v: paged caches [B, H, n_max/64, r, 64].
+    """
+    dev = x_k.device
+    for t, n in ((x_k, "x_k"), (x_v, "x_v"), (wdt_k, "wdt_k"), (wdt_v, "wdt_v"), (c_k, "c_k"), (c_v, "c_v")):
+        _need(t, n, x_k.dtype, dev)
+    for t, n in ((mu_k, "mu_k"), (mu_v, "mu_v")):
+        if t is not None:
+            _need(t, n, x_k.dtype, dev)
+    B, M, H, K = x_k.shape
+    if K % T:
+        raise ValueError("last dim of x must be T * d_head")
+    r_k, r_v = wdt_k.shape[1], wdt_v.shape[1]
+    n_max = c_k.shape[2] * PAGE
+    if (x_v.shape != x_k.shape or wdt_k.shape != (H, r_k, K) or wdt_v.shape != (H, r_v, K)
+            or c_k.shape != (B, H, n_max // PAGE, r_k, PAGE) or c_v.shape != (B, H, n_max // PAGE, r_v, PAGE)):
+        raise ValueError("inconsistent shapes")
+    _check(lib().lla_encode(_dt(x_k), B, M, H, T, K // T, r_k, r_v, _ptr(x_k), _ptr(x_v), _ptr(mu_k),
+                            _ptr(mu_v), _ptr(wdt_k), _ptr(wdt_v), _ptr(c_k), _ptr(c_v), n_max, pos0,
+                            _stream(x_k)))
+
+
+def decode_attn(q, c_k, c_v, u_k, u_v, *, n_ctx: int, ctx_len=None, mu_k=None, mu_v=None,
+                scale: float | None = None, out=None, out_dtype=torch.float32, workspace=None):
+    """Loop-l decode attention of q [B, H, d] over the paged latent cache.
+
+    u_k: [H, d, r_k], u_v: [H, d, r_v] (loop-l up-projections); mu_*: [H, d] or
+    None; ctx_len: int32 device tensor [B] or None (all sequences use n_ctx);
+    workspace: from new_workspace() or None (no split-K).  Returns out [B, H, d].
+    """
+    dev = q.device
+    B, H, d = q.shape
+    for t, n in ((q, "q"), (c_k, "c_k"), (c_v, "c_v"), (u_k, "u_k"), (u_v, "u_v")):
+        _need(t, n, q.dtype, dev)
+    for t, n in ((mu_k, "mu_k"), (mu_v, "mu_v")):
+        if t is not None:
+            _need(t, n, q.dtype, dev)
+    r_k, r_v = u_k.shape[2], u_v.shape[2]
+    n_max = c_k.shape[2] * PAGE
+    if (c_k.shape != (B, H, n_max // PAGE, r_k, PAGE) or c_v.shape != (B, H, n_max // PAGE, r_v, PAGE)
+            or u_k.shape != (H, d, r_k) or u_v.shape != (H, d, r_v)):
+        raise ValueError("inconsistent shapes")
+    if ctx_len is not None:
+        _need(ctx_len, "ctx_len", torch.int32, dev)
+        if ctx_len.shape != (B,):
+            raise ValueError("ctx_len must have shape [B]")
+    if out is None:
+        out = torch.empty((B, H, d), dtype=out_dtype, device=dev)
+    else:
+        _need(out, "out", None, dev)
+    if workspace is not None:
+        _need(workspace, "workspace", None, dev)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    _check(lib().lla_decode_attn(_dt(q), _out_code(out.dtype), B, H, d, r_k, r_v, n_max, n_ctx,
+                                 _ptr(ctx_len), _ptr(q), _ptr(c_k), _ptr(c_v), _ptr(u_k), _ptr(u_v),
+                                 _ptr(mu_k), _ptr(mu_v), float(scale), _ptr(out), _ptr(workspace),
+                                 ws_bytes, _stream(q)))
+    return out
+
+
+def prefill_attn(q, c_k, c_v, u_k, u_v, *, p0: int, mu_k=None, mu_v=None, scale: float | None = None,
+                 out=None, out_dtype=torch.float32):
+    """Causal loop-l prefill of q [B, H, M, d] at positions p0..p0+M-1 over the paged cache."""
+    dev = q.device
+    B, H, M, d = q.shape
+    for t, n in ((q, "q"), (c_k, "c_k"), (c_v, "c_v"), (u_k, "u_k"), (u_v, "u_v")):
+        _need(t, n, q.dtype, dev)
+    for t, n in ((mu_k, "mu_k"), (mu_v, "mu_v")):
+        if t is not None:
+            _need(t, n, q.dtype, dev)
+    r_k, r_v = u_k.shape[2], u_v.shape[2]
+    n_max = c_k.shape[2] * PAGE
+    if (c_k.shape != (B, H, n_max // PAGE, r_k, PAGE) or c_v.shape != (B, H, n_max // PAGE, r_v, PAGE)
+            or u_k.shape != (H, d, r_k) or u_v.shape != (H, d, r_v)):
+        raise ValueError("inconsistent shapes")
+    if out is None:
+        out = torch.empty((B, H, M, d), dtype=out_dtype, device=dev)
+    else:
+        _need(out, "out", None, dev)
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    _check(lib().lla_prefill_attn(_dt(q), _out_code(out.dtype), B, H, M, d, r_k, r_v, n_max, p0,
+                                  _ptr(q), _ptr(c_k), _ptr(c_v), _ptr(u_k), _ptr(u_v), _ptr(mu_k),
+                                  _ptr(mu_v), float(scale), _ptr(out), _stream(q)))
+    return out

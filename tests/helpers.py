@@ -1,0 +1,40 @@
+"""Shared helpers of the GPU parity tests."""
+
+import sys
+
+import numpy as np
+import torch
+
+# Tolerances: fp32 inputs, relative L2 <= 1e-5 per output tensor; bf16 inputs,
+# max-abs <= 2e-2 and relative L2 <= 1e-2 (both must hold).
+FP32_REL_L2 = 1e-5
+BF16_MAX_ABS = 2e-2
+BF16_REL_L2 = 1e-2
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def f64(t: torch.Tensor) -> np.ndarray:
+    """Exact host copy of a device tensor's values (bf16 -> float64 is exact)."""
+    return t.detach().to("cpu").to(torch.float64).numpy()
+
+
+def errors(got: np.ndarray, ref: np.ndarray):
+    err = got - ref
+    return float(np.max(np.abs(err))), float(np.linalg.norm(err) / np.linalg.norm(ref))
+
+
+def assert_close(got, ref, in_dtype, what=""):
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert got.shape == ref.shape, (got.shape, ref.shape)
+    assert np.all(np.isfinite(got)), f"{what}: non-finite output"
+    max_abs, rel = errors(got, ref)
+    log(f"  {what}: max_abs={max_abs:.3e} rel_l2={rel:.3e}")
+    if in_dtype == torch.float32:
+        assert rel <= FP32_REL_L2, (what, rel)
+    else:
+        assert max_abs <= BF16_MAX_ABS and rel <= BF16_REL_L2, (what, max_abs, rel)

@@ -1,0 +1,194 @@
+"""GPU parity of lla_decode_attn against the float64 oracle (plain definition:
+attention over the Eq. 3 reconstructions), called through the C ABI.
+
+Inputs are seeded (paper_2607_15456_amd.workloads); the oracle reads back the
+exact bytes the kernels consumed.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_15456_amd import lla, workloads as W
+from tests.helpers import assert_close, f64, log
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def _case(wl, r_k, r_v, B, N, n_max, layer, loop, means, dtype, device=DEV):
+    ck = W.latents(wl, r_k, "k", layer, B=B, N=N, device=device, dtype=dtype)
+    cv = W.latents(wl, r_v, "v", layer, B=B, N=N, device=device, dtype=dtype)
+    q = W.queries(wl, layer, loop, B=B, device=device, dtype=dtype)
+    uk, uv, muk, muv = W.codec_loop(wl, r_k, r_v, layer, loop, device, dtype, means=means)
+    return ck, cv, q, uk, uv, muk, muv, lla.to_paged(ck, n_max), lla.to_paged(cv, n_max)
+
+
+def _oracle(q, ck, cv, uk, uv, muk, muv, scale=None, ctx_len=None, units=None):
+    return oracle.decode_attn_batched(f64(q), f64(ck), f64(cv), f64(uk), f64(uv),
+                                      None if muk is None else f64(muk),
+                                      None if muv is None else f64(muv), scale,
+                                      ctx_len=ctx_len, units=units)
+
+
+# ---------------------------------------------------------------------------
+# Workload 1: the tiny fp32 case, every loop, every output checked.
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("split", [False, True])
+@pytest.mark.parametrize("means", [False, True])
+def test_tiny_fp32_every_loop(split, means):
+    wl = W.WORKLOADS["tiny_fp32"]
+    r_k, r_v = wl.ranks[0]
+    for loop in range(wl.T):
+        log(f"tiny_fp32 loop={loop} split={split} means={means}")
+        ck, cv, q, uk, uv, muk, muv, pk, pv = _case(wl, r_k, r_v, wl.B, wl.N, wl.N, 0, loop, means,
+                                                    torch.float32)
+        ws = lla.new_workspace(wl.B, wl.H, r_v, wl.N) if split else None
+        out = lla.decode_attn(q, pk, pv, uk, uv, n_ctx=wl.N, mu_k=muk, mu_v=muv, workspace=ws)
+        torch.cuda.synchronize()
+        assert_close(f64(out), _oracle(q, ck, cv, uk, uv, muk, muv), torch.float32, f"loop {loop}")
+
+
+def test_tiny_fp32_context_lengths():
+    """Shorter contexts over the same cache (fewer or no splits) still match."""
+    wl = W.WORKLOADS["tiny_fp32"]
+    r_k, r_v = wl.ranks[0]
+    ck, cv, q, uk, uv, muk, muv, pk, pv = _case(wl, r_k, r_v, wl.B, wl.N, wl.N, 0, 2, True, torch.float32)
+    ref = _oracle(q, ck, cv, uk, uv, muk, muv)
+    ws = lla.new_workspace(wl.B, wl.H, r_v, wl.N)
+    outs = []
+    # splits are chosen by the library; a 64-token context cannot split, a 512-token one can
+    for n in (64, 200, 512):
+        out = lla.decode_attn(q, pk, pv, uk, uv, n_ctx=n, mu_k=muk, mu_v=muv, workspace=ws)
+        torch.cuda.synchronize()
+        r = _oracle(q, ck[:, :, :n], cv[:, :, :n], uk, uv, muk, muv)
+        assert_close(f64(out), r, torch.float32, f"n_ctx={n}")
+        outs.append(out)
+    assert_close(f64(outs[-1]), ref, torch.float32, "full")
+
+
+# ---------------------------------------------------------------------------
+# bf16: ragged contexts, ranks that are not multiples of 8, per-sequence lengths.
+# ---------------------------------------------------------------------------
+
+SMALL = W.Workload("small_bf16", 1, 4, 128, 4, 3, 0, ((36, 60),), torch.bfloat16)
+
+
+@pytest.mark.parametrize("r_k,r_v", [(36, 60), (18, 30), (96, 160), (192, 320), (288, 480), (1, 512),
+                                     (512, 1), (7, 9)])
+@pytest.mark.parametrize("N", [1, 63, 64, 65, 777])
+def test_bf16_ragged(r_k, r_v, N):
+    n_max = ((N + 63) // 64) * 64 + 64
+    log(f"bf16 ragged r=({r_k},{r_v}) N={N}")
+    ck, cv, q, uk, uv, muk, muv, pk, pv = _case(SMALL, r_k, r_v, 3, N, n_max, 0, 1, True, torch.bfloat16)
+    ws = lla.new_workspace(3, SMALL.H, r_v, N)
+    for w in (None, ws):
+        out = lla.decode_attn(q, pk, pv, uk, uv, n_ctx=N, mu_k=muk, mu_v=muv, workspace=w)
+        torch.cuda.synchronize()
+        assert_close(f64(out), _oracle(q, ck, cv, uk, uv, muk, muv), torch.bfloat16,
+                     f"ws={'yes' if w is not None else 'no'}")
+
+
+def test_bf16_per_sequence_lengths_and_bf16_out():
+    B, N, n_max = 5, 1500, 1536
+    ck, cv, q, uk, uv, muk, muv, pk, pv = _case(SMALL, 36, 60, B, N, n_max, 0, 3, False, torch.bfloat16)
+    lens = [1, 64, 700, 1499, 1500]
+    ctx = torch.tensor(lens, dtype=torch.int32, device=DEV)
+    ws = lla.new_workspace(B, SMALL.H, 60, N)
+    ref = _oracle(q, ck, cv, uk, uv, muk, muv, ctx_len=lens)
+    for out_dtype in (torch.float32, torch.bfloat16):
+        out = lla.decode_attn(q, pk, pv, uk, uv, n_ctx=N, ctx_len=ctx, workspace=ws, out_dtype=out_dtype)
+        torch.cuda.synchronize()
+        assert out.dtype == out_dtype
+        assert_close(f64(out), ref, torch.bfloat16, f"ctx_len out={out_dtype}")
+
+
+def test_out_of_range_lengths_give_nan():
+    B, N, n_max = 3, 256, 256
+    ck, cv, q, uk, uv, muk, muv, pk, pv = _case(SMALL, 36, 60, B, N, n_max, 0, 0, False, torch.bfloat16)
+    ctx = torch.tensor([0, 100, 257], dtype=torch.int32, device=DEV)
+    ws = lla.new_workspace(B, SMALL.H, 60, N)
+    for w in (None, ws):
+        out = lla.decode_attn(q, pk, pv, uk, uv, n_ctx=N, ctx_len=ctx, workspace=w)
+        torch.cuda.synchronize()
+        o = f64(out)
+        assert np.all(np.isnan(o[0])) and np.all(np.isnan(o[2]))
+        assert_close(o[1:2], _oracle(q[1:2], ck[1:2], cv[1:2], uk, uv, None, None, ctx_len=[100]),
+                     torch.bfloat16, "valid row")
+    # the workspace counters are left at zero: a following call is still right
+    out = lla.decode_attn(q, pk, pv, uk, uv, n_ctx=N, workspace=ws)
+    torch.cuda.synchronize()
+    assert_close(f64(out), _oracle(q, ck, cv, uk, uv, None, None), torch.bfloat16, "after NaN call")
+
+
+def test_peaked_scores_and_custom_scale():
+    """Queries scaled x4 make the softmax peaked (a few keys dominate)."""
+    B, N, n_max = 2, 2048, 2048
+    ck, cv, q, uk, uv, muk, muv, pk, pv = _case(SMALL, 96, 160, B, N, n_max, 0, 2, True, torch.bfloat16)
+    q4 = (q.float() * 4).to(torch.bfloat16)
+    ws = lla.new_workspace(B, SMALL.H, 160, N)
+    for scale in (None, 0.05):
+        out = lla.decode_attn(q4, pk, pv, uk, uv, n_ctx=N, mu_k=muk, mu_v=muv, scale=scale, workspace=ws)
+        torch.cuda.synchronize()
+        assert_close(f64(out), _oracle(q4, ck, cv, uk, uv, muk, muv, scale=scale), torch.bfloat16,
+                     f"scale={scale}")
+
+
+def test_mu_k_cancels():
+    B, N = 2, 300
+    ck, cv, q, uk, uv, muk, muv, pk, pv = _case(SMALL, 36, 60, B, N, 320, 0, 1, True, torch.bfloat16)
+    a = lla.decode_attn(q, pk, pv, uk, uv, n_ctx=N, mu_k=muk, mu_v=muv)
+    b = lla.decode_attn(q, pk, pv, uk, uv, n_ctx=N, mu_k=None, mu_v=muv)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+    assert_close(f64(a), _oracle(q, ck, cv, uk, uv, muk, muv), torch.bfloat16, "with mu_k")
+
+
+# ---------------------------------------------------------------------------
+# Full-size workloads, in the launch configuration the benchmark times
+# (default split heuristic with a workspace); sampled (b, h) units.
+# ---------------------------------------------------------------------------
+
+def _full_size(wl, r_k, r_v, layer, loop, units):
+    n_max = wl.N + 64 if wl.name == "ouro14b_decode" else wl.N
+    log(f"{wl.name} r=({r_k},{r_v}) layer={layer} loop={loop} B={wl.B} N={wl.N}")
+    pk = lla.to_paged(W.latents(wl, r_k, "k", layer, device=DEV), n_max)
+    pv = lla.to_paged(W.latents(wl, r_v, "v", layer, device=DEV), n_max)
+    q = W.queries(wl, layer, loop, device=DEV)
+    uk, uv, _, _ = W.codec_loop(wl, r_k, r_v, layer, loop, DEV)
+    ws = lla.new_workspace(wl.B, wl.H, r_v, wl.N)
+    out = lla.decode_attn(q, pk, pv, uk, uv, n_ctx=wl.N, workspace=ws)
+    torch.cuda.synchronize()
+    o = f64(out)
+    for b, h in units:
+        ck = f64(lla.from_paged(pk[b:b + 1, h:h + 1], wl.N))[0, 0]
+        cv = f64(lla.from_paged(pv[b:b + 1, h:h + 1], wl.N))[0, 0]
+        ref = oracle.decode_attn(f64(q[b, h]), ck, cv, f64(uk[h]), f64(uv[h]))
+        assert_close(o[b, h], ref, torch.bfloat16, f"unit ({b},{h})")
+    del pk, pv
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.slow
+def test_full_ouro14b_decode():
+    wl = W.WORKLOADS["ouro14b_decode"]
+    units = [(0, 0), (7, 5), (16, 15), (31, 8), (31, 15)]
+    _full_size(wl, 192, 320, 0, 0, units)
+    _full_size(wl, 192, 320, 23, 3, units)
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("tier", range(6))
+def test_full_rank_sweep(tier):
+    wl = W.WORKLOADS["rank_sweep"]
+    r_k, r_v = wl.ranks[tier]
+    _full_size(wl, r_k, r_v, 0, tier % 4, [(0, 0), (33, 7), (63, 15)])
+
+
+@pytest.mark.slow
+def test_full_ouro26b_long():
+    wl = W.WORKLOADS["ouro26b_long"]
+    _full_size(wl, 36, 60, 47, 2, [(0, 0), (5, 11), (15, 15)])

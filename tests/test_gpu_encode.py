@@ -1,0 +1,123 @@
+"""GPU parity of lla_encode (Eq. 2 cache write) against the float64 oracle,
+called through the C ABI, plus an encode -> decode chain."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_15456_amd import lla, workloads as W
+from tests.helpers import assert_close, f64, log
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+SENTINEL = 7.0
+
+
+def _inputs(wl, r_k, r_v, B, M, means, dtype):
+    xk = W.stacked_kv(wl, "k", 0, B=B, M=M, device=DEV, dtype=dtype)
+    xv = W.stacked_kv(wl, "v", 0, B=B, M=M, device=DEV, dtype=dtype)
+    wk = W.down_projection(wl, r_k, "k", 0, DEV, dtype)
+    wv = W.down_projection(wl, r_v, "v", 0, DEV, dtype)
+    muk = W.stacked_mean(wl, "k", 0, DEV, dtype) if means else None
+    muv = W.stacked_mean(wl, "v", 0, DEV, dtype) if means else None
+    return xk, xv, wk, wv, muk, muv
+
+
+def _run(wl, r_k, r_v, B, M, pos0, n_max, means, dtype):
+    xk, xv, wk, wv, muk, muv = _inputs(wl, r_k, r_v, B, M, means, dtype)
+    ck = torch.full((B, wl.H, n_max // 64, r_k, 64), SENTINEL, dtype=dtype, device=DEV)
+    cv = torch.full((B, wl.H, n_max // 64, r_v, 64), SENTINEL, dtype=dtype, device=DEV)
+    lla.encode(xk, xv, wk, wv, ck, cv, T=wl.T, pos0=pos0, mu_k=muk, mu_v=muv)
+    torch.cuda.synchronize()
+    return (xk, xv, wk, wv, muk, muv), ck, cv
+
+
+def _check(wl, inputs, ck, cv, pos0, M, dtype, what):
+    xk, xv, wk, wv, muk, muv = inputs
+    for x, w, mu, c, name in ((xk, wk, muk, ck, "K"), (xv, wv, muv, cv, "V")):
+        ref = oracle.encode_batched(f64(x), None if mu is None else f64(mu), f64(w))
+        got = f64(lla.from_paged(c))
+        assert_close(got[:, :, pos0:pos0 + M], ref, dtype, f"{what} {name}")
+        untouched = np.concatenate([got[:, :, :pos0].ravel(), got[:, :, pos0 + M:].ravel()])
+        assert np.all(untouched == SENTINEL), f"{what} {name}: slots outside [pos0, pos0+M) changed"
+
+
+def test_tiny_fp32_encode():
+    wl = W.WORKLOADS["tiny_fp32"]
+    r_k, r_v = wl.ranks[0]
+    for means in (False, True):
+        log(f"tiny_fp32 encode means={means}")
+        inputs, ck, cv = _run(wl, r_k, r_v, wl.B, wl.N, 0, wl.N, means, torch.float32)
+        _check(wl, inputs, ck, cv, 0, wl.N, torch.float32, f"means={means}")
+
+
+SMALL = W.Workload("enc_small", 1, 3, 128, 4, 3, 0, ((18, 30),), torch.bfloat16)
+
+
+@pytest.mark.parametrize("r_k,r_v", [(18, 30), (36, 60), (96, 160), (192, 320), (7, 9), (1, 512)])
+@pytest.mark.parametrize("M,pos0", [(1, 0), (1, 63), (100, 37), (64, 64), (129, 0)])
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_encode_ragged(r_k, r_v, M, pos0, dtype):
+    n_max = 256
+    log(f"encode r=({r_k},{r_v}) M={M} pos0={pos0} {dtype}")
+    inputs, ck, cv = _run(SMALL, r_k, r_v, 3, M, pos0, n_max, True, dtype)
+    _check(SMALL, inputs, ck, cv, pos0, M, dtype, f"M={M} pos0={pos0}")
+
+
+def test_other_head_widths():
+    for d, T in ((64, 4), (96, 2), (256, 1)):
+        wl = W.Workload(f"enc_d{d}", 1, 2, d, T, 2, 0, ((18, 30),), torch.bfloat16)
+        log(f"encode d_head={d} T={T}")
+        inputs, ck, cv = _run(wl, 18, 30, 2, 70, 5, 128, True, torch.bfloat16)
+        _check(wl, inputs, ck, cv, 5, 70, torch.bfloat16, f"d={d}")
+
+
+def test_decode_time_write_ouro14b_shape():
+    """One new token per sequence at position 4096 (the decode step's cache write)."""
+    wl = W.WORKLOADS["ouro14b_decode"]
+    r_k, r_v = wl.ranks[0]
+    inputs, ck, cv = _run(wl, r_k, r_v, wl.B, 1, 4096, 4160, False, torch.bfloat16)
+    _check(wl, inputs, ck, cv, 4096, 1, torch.bfloat16, "M=1 at 4096")
+
+
+@pytest.mark.slow
+def test_full_prefill_write_encode():
+    """Workload 5's cache write at full size: 4 x 8192 tokens, sampled outputs."""
+    wl = W.WORKLOADS["prefill_write"]
+    r_k, r_v = wl.ranks[0]
+    log("prefill_write encode full size")
+    xk, xv, wk, wv, _, _ = _inputs(wl, r_k, r_v, wl.B, wl.N, False, torch.bfloat16)
+    ck = lla.alloc_cache(wl.B, wl.H, wl.N, r_k)
+    cv = lla.alloc_cache(wl.B, wl.H, wl.N, r_v)
+    lla.encode(xk, xv, wk, wv, ck, cv, T=wl.T, pos0=0)
+    torch.cuda.synchronize()
+    g = np.random.default_rng(0)
+    toks = np.sort(g.choice(wl.N, 64, replace=False))
+    for x, w, c, r, name in ((xk, wk, ck, r_k, "K"), (xv, wv, cv, r_v, "V")):
+        got = f64(lla.from_paged(c))
+        xs = f64(x[:, toks])                       # [B, 64, H, T*d]
+        ref = oracle.encode_batched(xs, None, f64(w))
+        assert_close(got[:, :, toks], ref, torch.bfloat16, f"sampled {name}")
+        assert np.all(np.isfinite(got))
+
+
+def test_encode_then_decode_chain_fp32():
+    """Workload 1: encode 512 tokens' loop-stacked K/V, then decode at every loop."""
+    wl = W.WORKLOADS["tiny_fp32"]
+    r_k, r_v = wl.ranks[0]
+    inputs, ck, cv = _run(wl, r_k, r_v, wl.B, wl.N, 0, wl.N, True, torch.float32)
+    xk, xv, wk, wv, muk, muv = inputs
+    c_k = oracle.encode_batched(f64(xk), f64(muk), f64(wk))
+    c_v = oracle.encode_batched(f64(xv), f64(muv), f64(wv))
+    for loop in range(wl.T):
+        q = W.queries(wl, 0, loop, device=DEV, dtype=torch.float32)
+        uk, uv, _, _ = W.codec_loop(wl, r_k, r_v, 0, loop, DEV, torch.float32)
+        sl = slice(loop * wl.d, (loop + 1) * wl.d)
+        mk, mv = muk[:, sl].contiguous(), muv[:, sl].contiguous()
+        out = lla.decode_attn(q, ck, cv, uk, uv, n_ctx=wl.N, mu_k=mk, mu_v=mv,
+                              workspace=lla.new_workspace(wl.B, wl.H, r_v, wl.N))
+        torch.cuda.synchronize()
+        ref = oracle.decode_attn_batched(f64(q), c_k, c_v, f64(uk), f64(uv), f64(mk), f64(mv))
+        assert_close(f64(out), ref, torch.float32, f"chain loop {loop}")
