@@ -3,22 +3,31 @@
 // softmax, z = sum_n a_n c_v[n], out = U_v z + mu_v.  K and V are never
 // materialised.
 //
-// The pass is HBM-bound (about 1 flop per latent byte).  Each wavefront
-// streams whole 64-token pages: one 16-byte load per lane covers EPL
-// consecutive tokens of one latent feature (the page is feature-major), so a
-// wave-wide load reads RPI full 128/256-byte feature rows.  Lane (rg, ts) owns
-// feature rows j = k*RPI + rg and token slice ts of every page:
-//   * scores: each lane accumulates q~_j * c_k[j][tokens of ts] over its rows,
-//     then a 3-step (bf16) xor butterfly over rg completes the dot products;
-//   * softmax: per-page max over the wave, running max m, running sum l, with
-//     the z accumulators rescaled only when m grows;
-//   * values: zacc[k] += sum over the lane's tokens of p_n c_v[j][n]; the
-//     reduction over token slices is deferred to the end of the scan.
-// The waves of a workgroup interleave pages and merge their (m, l, z) in LDS.
+// The pass is HBM-bound (about one flop per latent byte), so the kernel is
+// built around the load stream.  A cache page holds 64 tokens feature-major:
+// one feature row of the page is 128 contiguous bytes (bf16), and one 16-byte
+// load covers EPL = 8 consecutive tokens of one feature.  A wavefront works on
+// groups of PPG = 8 pages (512 tokens):
+//   * K phase -- lane (pg, ts) owns tokens ts*8..ts*8+7 of page pg of the
+//     group and walks every feature row j, accumulating q~_j * c_k[j][tokens]
+//     (q~_j is an LDS broadcast).  Each wave-wide load reads one 128-byte row
+//     segment of each of the 8 pages; the lane ends with 8 complete scores,
+//     so no cross-lane reduction and no redundant exp is needed.
+//   * softmax -- one wave-wide max per group, running max m and sum l; the z
+//     accumulators are rescaled only when m grows.
+//   * V phase -- the probabilities go through a per-wave LDS buffer, and lane
+//     (rg, ts) owns feature rows j = k*8 + rg and token slice ts of each page:
+//     zacc[k] += sum over its 8 tokens of p_n c_v[j][n]; the reduction over
+//     token slices is deferred to the end of the scan.
+// The waves of a workgroup interleave groups and merge their (m, l, z) in LDS.
 // When the context is split over several workgroups (split-K), each writes its
 // merged partial to the workspace and the last to arrive (an agent-scope
 // atomic counter) merges all partials and runs the value epilogue
 // out = U_v (z / l) + mu_v; the counter is left at zero.
+//
+// The prologue (q~ = U_k^T q) and the epilogue (U_v z) read the loop-l
+// up-projections with vector loads and reduce in a fixed order, so results
+// are bitwise reproducible.
 //
 // The same kernel serves the fp32 causal prefill: M queries per (b, h), query m
 // attending positions [0, p0 + m], one workgroup per query.
@@ -30,18 +39,122 @@
 namespace lla {
 namespace {
 
-constexpr int kWaves = 4;
-constexpr int kThreads = kWaves * kWave;
+constexpr int VB = 8;           // V row-group loads issued together per wave
 
-template <typename TIn, int GK, int GV>
-__global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a) {
+template <int BYTES> struct VecT;
+template <> struct VecT<16> { typedef uint4 type; };
+template <> struct VecT<8> { typedef uint2 type; };
+template <> struct VecT<4> { typedef uint32_t type; };
+template <> struct VecT<2> { typedef uint16_t type; };
+
+// Load VW consecutive elements (VW * sizeof(T) bytes, naturally aligned) as floats.
+template <typename T, int VW>
+__device__ __forceinline__ void load_vec(const T* p, float (&o)[VW]) {
+  typedef typename VecT<VW * sizeof(T)>::type V;
+  const V v = *reinterpret_cast<const V*>(p);
+  const T* e = reinterpret_cast<const T*>(&v);
+#pragma unroll
+  for (int i = 0; i < VW; ++i) o[i] = Elem<T>::get(e, i);
+}
+
+// q~[j] = qscale * sum_i U_k[i][j] q[i].  Thread f -> (column chunk jc of VW
+// columns, row block ib); row-block partials are summed in a fixed order.
+template <typename T, int VW, int kThreads>
+__device__ void absorb_query(const T* uk, int d, int rk, float qscale, const float* s_q,
+                             float* s_part, float* s_qt) {
+  const int nch = rk / VW;
+  const int rb = nch >= kThreads ? 1 : kThreads / nch;
+  for (int f = threadIdx.x; f < nch * rb; f += kThreads) {
+    const int jc = f % nch, ib = f / nch;
+    float acc[VW];
+#pragma unroll
+    for (int e = 0; e < VW; ++e) acc[e] = 0.f;
+#pragma unroll 8
+    for (int i = ib; i < d; i += rb) {
+      float u[VW];
+      load_vec<T, VW>(uk + (size_t)i * rk + jc * VW, u);
+      const float qi = s_q[i];
+#pragma unroll
+      for (int e = 0; e < VW; ++e) acc[e] = fmaf(u[e], qi, acc[e]);
+    }
+#pragma unroll
+    for (int e = 0; e < VW; ++e) s_part[ib * rk + jc * VW + e] = acc[e];
+  }
+  __syncthreads();
+  for (int j = threadIdx.x; j < rk; j += kThreads) {
+    float s = 0.f;
+    for (int ib = 0; ib < rb; ++ib) s += s_part[ib * rk + j];
+    s_qt[j] = s * qscale;
+  }
+  __syncthreads();
+}
+
+// out[i] = sum_j U_v[i][j] zn[j] (+ mu_v[i]).  P consecutive threads share a
+// row and split its column chunks; their partials combine by xor shuffles.
+template <typename T, int VW, int kThreads>
+__device__ void value_epilogue(const T* uv, const T* muv, int d, int rv, const float* s_zn,
+                               bool bad, int out_dtype, void* out, size_t obase) {
+  const int P = (kThreads / d) >= 8 ? 8 : (kThreads / d) >= 4 ? 4 : (kThreads / d) >= 2 ? 2 : 1;
+  const int t = threadIdx.x, i = t / P, part = t % P;
+  const int nch = rv / VW;
+  float acc = 0.f;
+  if (i < d) {
+#pragma unroll 8
+    for (int c = part; c < nch; c += P) {
+      float u[VW];
+      load_vec<T, VW>(uv + (size_t)i * rv + c * VW, u);
+#pragma unroll
+      for (int e = 0; e < VW; ++e) acc = fmaf(u[e], s_zn[c * VW + e], acc);
+    }
+  }
+  for (int off = 1; off < P; off <<= 1) acc += xor_shfl(acc, off);
+  if (i < d && part == 0) {
+    if (muv) acc += Elem<T>::get(muv, i);
+    if (bad) acc = __builtin_nanf("");
+    if (out_dtype == LLA_F32)
+      static_cast<float*>(out)[obase + i] = acc;
+    else
+      static_cast<bf16_t*>(out)[obase + i] = f32_to_bf16(acc);
+  }
+}
+
+// Raw buffer resource (gfx9 family word 3) over one contiguous region.
+typedef __amdgpu_buffer_rsrc_t BufRsrc;
+__device__ __forceinline__ BufRsrc make_rsrc(const void* base, size_t bytes) {
+  const int n = bytes >= 0xffffffffull ? -1 : (int)bytes;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, n, 0x00020000);
+}
+// 16-byte load at voffset (per lane) + soffset (uniform); offsets past the
+// region's size read as zero.
+__device__ __forceinline__ uint4 buf_ld16(BufRsrc r, int voff, int soff) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+template <typename T>
+__device__ __forceinline__ int vec_width(int r) {
+  constexpr int E = 16 / sizeof(T);
+  return (r % E == 0) ? E : (r % 4 == 0) ? 4 : (r % 2 == 0) ? 2 : 1;
+}
+
+template <typename TIn, int GV, int kWaves>
+__global__ __launch_bounds__(kWaves * kWave) __attribute__((amdgpu_waves_per_eu(4)))
+void decode_kernel(DecodeArgs a) {
+  constexpr int kThreads = kWaves * kWave;
   constexpr int EPL = Elem<TIn>::kPer16B;  // tokens covered by one 16-byte load
   constexpr int LPR = kPage / EPL;         // lanes per 64-token feature row
-  constexpr int RPI = kWave / LPR;         // feature rows per wave-wide load
+  constexpr int PPG = kWave / LPR;         // pages per group (K phase) = rows per load (V phase)
 
+  // s_work holds the prologue's row-block partials, then (after the prologue's
+  // last barrier) the per-wave probability buffers and latent partials.
+  constexpr int kPWave = PPG * kPage;
   __shared__ float s_q[kMaxHead];
-  __shared__ float s_qt[kMaxRank];
-  __shared__ float s_z[kWaves][kMaxRank];
+  __shared__ __attribute__((aligned(16))) float s_qt[kMaxRank];
+  __shared__ __attribute__((aligned(16))) float s_work[kWaves * (kPWave + kMaxRank)];
+  static_assert(kWaves * (kPWave + kMaxRank) >= kThreads * 8, "prologue partials do not fit");
+  float* const s_part = s_work;
+  float (*const s_p)[kPWave] = reinterpret_cast<float (*)[kPWave]>(s_work);
+  float (*const s_z)[kMaxRank] = reinterpret_cast<float (*)[kMaxRank]>(s_work + kWaves * kPWave);
   __shared__ float s_zn[kMaxRank];
   __shared__ float s_m[kWaves], s_l[kWaves];
   __shared__ int s_last;
@@ -66,119 +179,177 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a) {
 
   const size_t bh = (size_t)b * a.H + h;
   const size_t unit = bh * a.M + m;  // (b, h, m)
-
-  // ---- prologue: absorbed query q~ = U_k^T q, scale * log2(e) folded in ----
-  const TIn* qp = static_cast<const TIn*>(a.q) + unit * a.d;
-  for (int i = tid; i < a.d; i += kThreads) s_q[i] = Elem<TIn>::get(qp, i);
-  __syncthreads();
-  const TIn* uk = static_cast<const TIn*>(a.uk) + (size_t)h * a.d * a.rk;
-  for (int j = tid; j < a.rk; j += kThreads) {
-    float acc = 0.f;
-    for (int i = 0; i < a.d; ++i) acc = fmaf(Elem<TIn>::get(uk, (size_t)i * a.rk + j), s_q[i], acc);
-    s_qt[j] = acc * a.qscale;
-  }
-  __syncthreads();
-
-  const int rg = lane / LPR, ts = lane - rg * LPR;
   const int rk = a.rk, rv = a.rv;
-  float qreg[GK];
-#pragma unroll
-  for (int k = 0; k < GK; ++k) {
-    const int j = k * RPI + rg;
-    qreg[k] = (j < rk) ? s_qt[j] : 0.f;
+
+  // ---- prologue: absorbed query q~ = U_k^T q, with scale * log2(e) folded in ----
+  {
+    const TIn* qp = static_cast<const TIn*>(a.q) + unit * a.d;
+    for (int i = tid; i < a.d; i += kThreads) s_q[i] = Elem<TIn>::get(qp, i);
+    __syncthreads();
+    const TIn* uk = static_cast<const TIn*>(a.uk) + (size_t)h * a.d * rk;
+    switch (vec_width<TIn>(rk)) {
+      case 8: absorb_query<TIn, (EPL >= 8 ? 8 : 4), kThreads>(uk, a.d, rk, a.qscale, s_q, s_part, s_qt); break;
+      case 4: absorb_query<TIn, 4, kThreads>(uk, a.d, rk, a.qscale, s_q, s_part, s_qt); break;
+      case 2: absorb_query<TIn, 2, kThreads>(uk, a.d, rk, a.qscale, s_q, s_part, s_qt); break;
+      default: absorb_query<TIn, 1, kThreads>(uk, a.d, rk, a.qscale, s_q, s_part, s_qt); break;
+    }
   }
+
+  const int hi = lane / LPR, lo = lane - hi * LPR;
   float zacc[GV];
 #pragma unroll
   for (int k = 0; k < GV; ++k) zacc[k] = 0.f;
-  float m_run = neg_inf(), l_run = 0.f;
+  float m_run = neg_inf(), l_lane = 0.f;
 
-  const TIn* ckb = static_cast<const TIn*>(a.ck) + bh * (size_t)a.n_max * rk + ts * EPL;
-  const TIn* cvb = static_cast<const TIn*>(a.cv) + bh * (size_t)a.n_max * rv + ts * EPL;
+  // Buffer resources over this (b, h)'s latents: the row and page offsets are
+  // wave-uniform (SGPR), the lane part is one VGPR.
+  constexpr int ES = sizeof(TIn);
+  const BufRsrc rk_src = make_rsrc(static_cast<const TIn*>(a.ck) + bh * (size_t)a.n_max * rk,
+                                   (size_t)a.n_max * rk * ES);
+  const BufRsrc rv_src = make_rsrc(static_cast<const TIn*>(a.cv) + bh * (size_t)a.n_max * rv,
+                                   (size_t)a.n_max * rv * ES);
+  const int kpage_bytes = kPage * rk * ES, vpage_bytes = kPage * rv * ES;
+  const int vk_lane = hi * kpage_bytes + lo * 16;   // K phase: page hi of the group, slice lo
+  const int vv_lane = hi * kPage * ES + lo * 16;    // V phase: row hi of the row group, slice lo
+  const int vg_full = rv / PPG, vg_part = rv % PPG;  // full row groups, rows of the partial one
+  float* sp = s_p[wave];
 
-  // ---- latent scan ----
-  for (int p = pb + wave; p < pe; p += kWaves) {
-    const TIn* kp = ckb + (size_t)p * kPage * rk;
+  // ---- latent scan, PPG pages per wave per group ----
+  for (int g0 = pb + wave * PPG; g0 < pe; g0 += kWaves * PPG) {
+    const int np = min(PPG, pe - g0);
     float acc[EPL];
 #pragma unroll
     for (int e = 0; e < EPL; ++e) acc[e] = 0.f;
+    if (hi < np) {
+      const int gbase = g0 * kpage_bytes;
+      int j = 0;
+      for (; j + 8 <= rk; j += 8) {
+        const float4 qa = *reinterpret_cast<const float4*>(&s_qt[j]);
+        const float4 qb = *reinterpret_cast<const float4*>(&s_qt[j + 4]);
+        const float qj[8] = {qa.x, qa.y, qa.z, qa.w, qb.x, qb.y, qb.z, qb.w};
+        uint4 raw[8];
 #pragma unroll
-    for (int k = 0; k < GK; ++k) {
-      const int j = k * RPI + rg;
-      if (j < rk) {
+        for (int u = 0; u < 8; ++u) raw[u] = buf_ld16(rk_src, vk_lane, gbase + (j + u) * kPage * ES);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          float v[EPL];
+          Elem<TIn>::unpack(raw[u], v);
+#pragma unroll
+          for (int e = 0; e < EPL; ++e) acc[e] = fmaf(qj[u], v[e], acc[e]);
+        }
+      }
+      for (; j < rk; ++j) {
+        const float q1 = s_qt[j];
         float v[EPL];
-        Elem<TIn>::unpack(ld16(kp + (size_t)j * kPage), v);
+        Elem<TIn>::unpack(buf_ld16(rk_src, vk_lane, gbase + j * kPage * ES), v);
 #pragma unroll
-        for (int e = 0; e < EPL; ++e) acc[e] = fmaf(qreg[k], v[e], acc[e]);
+        for (int e = 0; e < EPL; ++e) acc[e] = fmaf(q1, v[e], acc[e]);
       }
     }
-#pragma unroll
-    for (int off = LPR; off < kWave; off <<= 1)
-#pragma unroll
-      for (int e = 0; e < EPL; ++e) acc[e] += xor_shfl(acc[e], off);
-
-    const int n0 = p * kPage + ts * EPL;
-    const bool tail = (p + 1) * kPage > N;
+    // scores of invalid pages / tokens beyond N are -inf
+    const int n0 = (g0 + hi) * kPage + lo * EPL;
     float mb = neg_inf();
 #pragma unroll
     for (int e = 0; e < EPL; ++e) {
-      if (tail && n0 + e >= N) acc[e] = neg_inf();
+      if (hi >= np || n0 + e >= N) acc[e] = neg_inf();
       mb = fmaxf(mb, acc[e]);
     }
 #pragma unroll
-    for (int off = 1; off < LPR; off <<= 1) mb = fmaxf(mb, xor_shfl(mb, off));
+    for (int off = 1; off < kWave; off <<= 1) mb = fmaxf(mb, xor_shfl(mb, off));
     if (mb > m_run) {
-      const float alpha = exp2f(m_run - mb);
-      l_run *= alpha;
+      const float alpha = fast_exp2(m_run - mb);
+      l_lane *= alpha;
 #pragma unroll
       for (int k = 0; k < GV; ++k) zacc[k] *= alpha;
       m_run = mb;
     }
     float pr[EPL];
-    float ls = 0.f;
 #pragma unroll
     for (int e = 0; e < EPL; ++e) {
-      pr[e] = exp2f(acc[e] - m_run);
-      ls += pr[e];
+      pr[e] = fast_exp2(acc[e] - m_run);
+      l_lane += pr[e];
     }
-    l_run += ls;
+#pragma unroll
+    for (int e = 0; e < EPL; e += 4)
+      *reinterpret_cast<float4*>(&sp[hi * kPage + lo * EPL + e]) =
+          make_float4(pr[e], pr[e + 1], pr[e + 2], pr[e + 3]);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
-    const TIn* vp = cvb + (size_t)p * kPage * rv;
+    // V phase: lane (hi = row in the row group, lo = token slice), page by page
+    for (int pg = 0; pg < np; ++pg) {
+      const int pv = g0 + pg;
+      float p8[EPL];
 #pragma unroll
-    for (int k = 0; k < GV; ++k) {
-      const int j = k * RPI + rg;
-      if (j < rv) {
-        float v[EPL];
-        Elem<TIn>::unpack(ld16(vp + (size_t)j * kPage), v);
-        if (tail) {
+      for (int e = 0; e < EPL; e += 4) {
+        const float4 t = *reinterpret_cast<const float4*>(&sp[pg * kPage + lo * EPL + e]);
+        p8[e] = t.x;
+        p8[e + 1] = t.y;
+        p8[e + 2] = t.z;
+        p8[e + 3] = t.w;
+      }
+      const bool tail = (pv + 1) * kPage > N;
+      if (tail) {  // tokens beyond N: weight 0 and value 0 (the slot may hold anything)
+        const int nv0 = pv * kPage + lo * EPL;
 #pragma unroll
-          for (int e = 0; e < EPL; ++e)
-            if (n0 + e >= N) v[e] = 0.f;
+        for (int e = 0; e < EPL; ++e)
+          if (nv0 + e >= N) p8[e] = 0.f;
+      }
+      const int pbase = pv * vpage_bytes;
+      // VB row groups per batch: their loads in flight together, then their FMAs;
+      // the scheduling barrier keeps later batches from being hoisted
+#pragma unroll
+      for (int kc = 0; kc < GV; kc += VB) {
+        uint4 raw[VB];
+#pragma unroll
+        for (int u = 0; u < VB; ++u) {
+          const int k = kc + u;
+          if (k < vg_full || (k == vg_full && hi < vg_part))
+            raw[u] = buf_ld16(rv_src, vv_lane, pbase + k * PPG * kPage * ES);
         }
-        float t = 0.f;
 #pragma unroll
-        for (int e = 0; e < EPL; ++e) t = fmaf(pr[e], v[e], t);
-        zacc[k] += t;
+        for (int u = 0; u < VB; ++u) {
+          const int k = kc + u;
+          if (k < vg_full || (k == vg_full && hi < vg_part)) {
+            float v[EPL];
+            Elem<TIn>::unpack(raw[u], v);
+            if (tail) {
+#pragma unroll
+              for (int e = 0; e < EPL; ++e)
+                if (p8[e] == 0.f) v[e] = 0.f;
+            }
+            float t = 0.f;
+#pragma unroll
+            for (int e = 0; e < EPL; ++e) t = fmaf(p8[e], v[e], t);
+            zacc[k] += t;
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
 
-  // ---- wave reduction over token slices ----
+  // ---- wave reductions: l over all lanes, z over token slices ----
 #pragma unroll
-  for (int off = 1; off < LPR; off <<= 1) {
-    l_run += xor_shfl(l_run, off);
+  for (int off = 1; off < kWave; off <<= 1) l_lane += xor_shfl(l_lane, off);
+#pragma unroll
+  for (int off = 1; off < LPR; off <<= 1)
 #pragma unroll
     for (int k = 0; k < GV; ++k) zacc[k] += xor_shfl(zacc[k], off);
-  }
-  if (ts == 0) {
+  if (lo == 0) {
 #pragma unroll
     for (int k = 0; k < GV; ++k) {
-      const int j = k * RPI + rg;
+      const int j = k * PPG + hi;
       if (j < rv) s_z[wave][j] = zacc[k];
     }
   }
   if (lane == 0) {
     s_m[wave] = m_run;
-    s_l[wave] = l_run;
+    s_l[wave] = l_lane;
   }
   __syncthreads();
 
@@ -190,7 +361,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a) {
   float lg = 0.f;
 #pragma unroll
   for (int w = 0; w < kWaves; ++w) {
-    wt[w] = (s_m[w] == neg_inf()) ? 0.f : exp2f(s_m[w] - mg);
+    wt[w] = (s_m[w] == neg_inf()) ? 0.f : fast_exp2(s_m[w] - mg);
     lg = fmaf(wt[w], s_l[w], lg);
   }
 
@@ -215,7 +386,10 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a) {
       part[0] = mg;
       part[1] = lg;
     }
-    __threadfence();
+    // The barrier orders every thread's partial stores before thread 0's
+    // agent-scope release; the fence is cumulative, so one per workgroup
+    // publishes them all.  The last arrival's acquire (by thread 0, then the
+    // barrier) makes every split's partial visible to the whole workgroup.
     __syncthreads();
     if (tid == 0) {
       const uint32_t prev =
@@ -224,21 +398,20 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a) {
     }
     __syncthreads();
     if (!s_last) return;
-    __threadfence();
     const float* P = a.part + unit * a.splits * stride;
     float ma = neg_inf();
     for (int s = 0; s < a.splits; ++s) ma = fmaxf(ma, P[(size_t)s * stride]);
     float la = 0.f;
     for (int s = 0; s < a.splits; ++s) {
       const float ms = P[(size_t)s * stride];
-      const float ws = (ms == neg_inf()) ? 0.f : exp2f(ms - ma);
+      const float ws = (ms == neg_inf()) ? 0.f : fast_exp2(ms - ma);
       la = fmaf(ws, P[(size_t)s * stride + 1], la);
     }
     for (int j = tid; j < rv; j += kThreads) {
       float z = 0.f;
       for (int s = 0; s < a.splits; ++s) {
         const float ms = P[(size_t)s * stride];
-        const float ws = (ms == neg_inf()) ? 0.f : exp2f(ms - ma);
+        const float ws = (ms == neg_inf()) ? 0.f : fast_exp2(ms - ma);
         z = fmaf(ws, P[(size_t)s * stride + 2 + j], z);
       }
       s_zn[j] = z / la;
@@ -247,53 +420,44 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a) {
   }
   __syncthreads();
 
-  // ---- value epilogue: out = U_v z + mu_v (16 lanes per output row) ----
+  // ---- value epilogue: out = U_v z + mu_v ----
   const TIn* uv = static_cast<const TIn*>(a.uv) + (size_t)h * a.d * rv;
   const TIn* muv = a.muv ? static_cast<const TIn*>(a.muv) + (size_t)h * a.d : nullptr;
-  const int sub = lane >> 4, sl = lane & 15;
-  for (int i0 = wave * 4; i0 < a.d; i0 += kWaves * 4) {
-    const int i = i0 + sub;
-    float t = 0.f;
-    if (i < a.d)
-      for (int j = sl; j < rv; j += 16) t = fmaf(Elem<TIn>::get(uv, (size_t)i * rv + j), s_zn[j], t);
-#pragma unroll
-    for (int off = 1; off < 16; off <<= 1) t += xor_shfl(t, off);
-    if (sl == 0 && i < a.d) {
-      if (muv) t += Elem<TIn>::get(muv, i);
-      if (bad) t = __builtin_nanf("");
-      if (a.out_dtype == LLA_F32)
-        static_cast<float*>(a.out)[unit * a.d + i] = t;
-      else
-        static_cast<bf16_t*>(a.out)[unit * a.d + i] = f32_to_bf16(t);
-    }
+  const size_t obase = unit * a.d;
+  switch (vec_width<TIn>(rv)) {
+    case 8: value_epilogue<TIn, (EPL >= 8 ? 8 : 4), kThreads>(uv, muv, a.d, rv, s_zn, bad, a.out_dtype, a.out, obase); break;
+    case 4: value_epilogue<TIn, 4, kThreads>(uv, muv, a.d, rv, s_zn, bad, a.out_dtype, a.out, obase); break;
+    case 2: value_epilogue<TIn, 2, kThreads>(uv, muv, a.d, rv, s_zn, bad, a.out_dtype, a.out, obase); break;
+    default: value_epilogue<TIn, 1, kThreads>(uv, muv, a.d, rv, s_zn, bad, a.out_dtype, a.out, obase); break;
   }
 }
 
-template <typename TIn, int GK, int GV>
+template <typename TIn, int GV>
 hipError_t launch_t(const DecodeArgs& a, hipStream_t stream) {
   dim3 grid(a.B * a.M * a.splits, a.H);
-  hipLaunchKernelGGL((decode_kernel<TIn, GK, GV>), grid, dim3(kThreads), 0, stream, a);
+  if (a.waves == 8)
+    hipLaunchKernelGGL((decode_kernel<TIn, GV, 8>), grid, dim3(8 * kWave), 0, stream, a);
+  else
+    hipLaunchKernelGGL((decode_kernel<TIn, GV, 4>), grid, dim3(4 * kWave), 0, stream, a);
   return hipGetLastError();
 }
 
-int bucket(int g) { return g <= 8 ? 8 : g <= 16 ? 16 : g <= 32 ? 32 : g <= 64 ? 64 : 128; }
-
 template <typename TIn>
 hipError_t dispatch(const DecodeArgs& a, hipStream_t stream) {
-  constexpr int RPI = kWave / (kPage / Elem<TIn>::kPer16B);
-  const int gk = bucket((a.rk + RPI - 1) / RPI);
-  const int gv = bucket((a.rv + RPI - 1) / RPI);
-#define LLA_CASE(K, V) \
-  if (gk == K && gv == V) return launch_t<TIn, K, V>(a, stream);
-  LLA_CASE(8, 8) LLA_CASE(8, 16) LLA_CASE(8, 32) LLA_CASE(8, 64)
-  LLA_CASE(16, 8) LLA_CASE(16, 16) LLA_CASE(16, 32) LLA_CASE(16, 64)
-  LLA_CASE(32, 8) LLA_CASE(32, 16) LLA_CASE(32, 32) LLA_CASE(32, 64)
-  LLA_CASE(64, 8) LLA_CASE(64, 16) LLA_CASE(64, 32) LLA_CASE(64, 64)
-  if constexpr (RPI == 4) {
-    LLA_CASE(8, 128) LLA_CASE(16, 128) LLA_CASE(32, 128) LLA_CASE(64, 128)
-    LLA_CASE(128, 8) LLA_CASE(128, 16) LLA_CASE(128, 32) LLA_CASE(128, 64) LLA_CASE(128, 128)
+  constexpr int RPL = kWave / (kPage / Elem<TIn>::kPer16B);  // V rows per wave-wide load
+  const int gv = (a.rv + RPL - 1) / RPL;
+  if (gv <= 4) return launch_t<TIn, 4>(a, stream);
+  if (gv <= 8) return launch_t<TIn, 8>(a, stream);
+  if (gv <= 16) return launch_t<TIn, 16>(a, stream);
+  if (gv <= 24) return launch_t<TIn, 24>(a, stream);
+  if (gv <= 32) return launch_t<TIn, 32>(a, stream);
+  if (gv <= 40) return launch_t<TIn, 40>(a, stream);
+  if (gv <= 48) return launch_t<TIn, 48>(a, stream);
+  if (gv <= 64) return launch_t<TIn, 64>(a, stream);
+  if constexpr (RPL == 4) {
+    if (gv <= 96) return launch_t<TIn, 96>(a, stream);
+    if (gv <= 128) return launch_t<TIn, 128>(a, stream);
   }
-#undef LLA_CASE
   return hipErrorInvalidValue;
 }
 

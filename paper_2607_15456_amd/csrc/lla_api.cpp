@@ -50,28 +50,42 @@ size_t workspace_bytes(int B, int H, int r_v, int n_ctx) {
   return counters + units * (size_t)max_splits(n_ctx) * (size_t)(r_v + 2) * sizeof(float);
 }
 
-// Number of workgroups each (b, h) context is split over: enough workgroups
-// to give every compute unit several, while each wave still scans at least
-// two pages.  LLA_DECODE_SPLITS overrides it (for tuning sweeps).
-int choose_splits(int units, int n_ctx) {
-  static const int forced = [] {
-    const char* e = std::getenv("LLA_DECODE_SPLITS");
-    return e ? std::atoi(e) : 0;
-  }();
+// Launch shape of the decode scan: wavefronts per workgroup and the number of
+// workgroups each (b, h) context is split over.  One workgroup per (b, h)
+// streams best as long as that already gives every compute unit 8 resident
+// wavefronts (4-wave workgroups when (b, h) units alone reach that, 8-wave
+// ones otherwise); only smaller batches split the context (split-K), up to 8
+// wavefronts per compute unit, with every wavefront keeping at least one
+// 8-page group.  LLA_DECODE_WAVES / LLA_DECODE_SPLITS override the choice
+// (for tuning sweeps).
+struct DecodeShape {
+  int waves, splits;
+};
+
+int env_int(const char* name) {
+  const char* e = std::getenv(name);
+  return e ? std::atoi(e) : 0;
+}
+
+DecodeShape choose_shape(int units, int n_ctx, bool allow_split) {
+  static const int forced_waves = env_int("LLA_DECODE_WAVES");
+  static const int forced_splits = env_int("LLA_DECODE_SPLITS");
   const int pages = (n_ctx + LLA_PAGE_TOKENS - 1) / LLA_PAGE_TOKENS;
-  int s;
-  if (forced > 0) {
-    s = forced;
-  } else {
-    const int target = 4 * lla::device_cu_count();
-    s = (target + units - 1) / units;
-    const int min_pages = 8;  // 4 waves x 2 pages
-    const int cap = pages / min_pages > 0 ? pages / min_pages : 1;
+  const int groups = (pages + 7) / 8;
+  const long target = 8L * lla::device_cu_count();  // resident wavefronts wanted
+  DecodeShape sh{4, 1};
+  if ((long)units * 4 < target && groups >= 8) sh.waves = 8;
+  if (allow_split && (long)units * sh.waves < target) {
+    long s = (target + (long)units * sh.waves - 1) / ((long)units * sh.waves);
+    const long cap = groups / sh.waves > 0 ? groups / sh.waves : 1;
     if (s > cap) s = cap;
+    sh.splits = (int)s;
   }
-  if (s > max_splits(n_ctx)) s = max_splits(n_ctx);
-  if (s < 1) s = 1;
-  return s;
+  if (forced_waves == 4 || forced_waves == 8) sh.waves = forced_waves;
+  if (forced_splits > 0 && allow_split) sh.splits = forced_splits;
+  if (sh.splits > max_splits(n_ctx)) sh.splits = max_splits(n_ctx);
+  if (sh.splits < 1) sh.splits = 1;
+  return sh;
 }
 
 lla_status hip_status(hipError_t e) { return e == hipSuccess ? LLA_OK : LLA_ERR_HIP; }
@@ -218,7 +232,9 @@ lla_status lla_decode_attn(int dtype, int out_dtype, int B, int H, int d_head, i
   a.muv = mu_v;
   a.qscale = (float)((double)scale * kLog2e);
   a.out = out;
-  a.splits = workspace ? choose_splits(B * H, n_ctx) : 1;
+  const DecodeShape sh = choose_shape(B * H, n_ctx, workspace != nullptr);
+  a.waves = sh.waves;
+  a.splits = sh.splits;
   if (a.splits > 1) {
     const size_t units = (size_t)B * H;
     const size_t counters = (units * sizeof(uint32_t) + 255) / 256 * 256;
@@ -279,6 +295,7 @@ lla_status lla_prefill_attn(int dtype, int out_dtype, int B, int H, int M, int d
   a.p0 = p0;
   a.causal = 1;
   a.splits = 1;
+  a.waves = 4;
   a.q = q;
   a.ck = c_k;
   a.cv = c_v;

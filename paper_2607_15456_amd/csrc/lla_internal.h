@@ -16,6 +16,7 @@ struct DecodeArgs {
   int p0;      // causal mode: position of query 0
   int causal;  // 0: decode (N_b from ctx_len / n_ctx); 1: query m attends [0, p0+m]
   int splits;  // workgroups per (b, h, m) along the context
+  int waves;   // wavefronts per workgroup (4 or 8)
   const int32_t* ctx_len;
   const void* q;
   const void* ck;
