@@ -1,7 +1,348 @@
-// Causal prefill attention over the paged latent cache (bf16, MFMA).
+// Causal prefill attention at loop l over the paged latent cache, bf16 inputs
+// on MFMA, absorbed form (App. J "Absorbed attention"):
+//   Q~ = Q U_k (scale * log2 e folded in),  S = Q~ C_k^T (key n <= query pos),
+//   P = softmax(S) row-wise (online over 64-token pages),  Z = P C_v,
+//   O = (Z / l) U_v^T + mu_v.
+// The paper's two-pass decoder re-forwards the prompt with attention over the
+// reconstructed cache (App. A); this kernel is that attention read straight
+// from the latents.
+//
+// One workgroup = 4 wavefronts x 32 queries of one (b, h).  Every product is
+// a v_mfma_f32_32x32x16_bf16 and is computed transposed so that each
+// accumulator's registers feed the next product's B operand with no
+// cross-lane movement:
+//   D1 = Q~^T   (M = feature j, N = query, K = d)     A: U_k^T (LDS)      B: Q rows (global)
+//   D2 = S^T    (M = key n,     N = query, K = j)     A: K tile (LDS, token-major)  B: D1 (hi + lo)
+//   D3 = Z^T   += (M = j,       N = query, K = key)   A: V tile (LDS, feature-major) B: P from D2
+//   D4 = O^T    (M = out i,     N = query, K = j)     A: U_v (LDS)        B: D3 / l
+// A 32x32 accumulator gives lane (q + 32g), register r the element
+// [8(r/4) + 4g + r%4][q]: every register of a lane belongs to the lane's
+// query q, so the softmax state (running max, rescaling) is lane-local.  The
+// K index of the next product is enumerated in that same order: K-step t,
+// lane half g, element e stands for index 16t + 8(e/4) + 4g + e%4, which is
+// exactly registers 8(t%2) + e of accumulator tile t/2.
+// The denominator l comes out of the value product: the padded V tile carries
+// a row of ones at feature r_v, so Z^T[r_v][q] = sum_n p[q][n].
+// Q~ enters the score product as two bf16 terms (hi + lo), so the scores carry
+// about 16 significant bits rather than bf16's 8: with peaked rows the score
+// magnitudes would otherwise turn Q~'s rounding into visible weight errors.
+// The running max enters the score product as its C operand (S - m), and is
+// only raised when a page exceeds it by more than 2^8 (lazy rescale), so most
+// pages cost one max, one exp2 and one conversion per score.
+// K/V pages are staged cooperatively into double-buffered LDS tiles (the K
+// page transposed to token-major on the way); the next page's global loads
+// are in flight while the current page is computed.
+
 #include "lla_device.h"
 #include "lla_internal.h"
+#include "../../include/lla.h"
 
 namespace lla {
-hipError_t launch_prefill_bf16(const PrefillArgs&, hipStream_t) { return hipErrorNotSupported; }
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int kPWaves = 4;
+constexpr int kPThreads = kPWaves * kWave;
+constexpr int kQBlock = kPWaves * 32;  // queries per workgroup
+constexpr int kMaxDPrefill = 128;
+constexpr float kLazy = 8.0f;          // rescale only when the max grows by more than this (log2)
+constexpr bf16_t kOne = 0x3F80;        // 1.0 in bf16
+
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+__device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// A/B operand for K-step ordering 16t + 8(e/4) + 4g + e%4 read from an LDS row:
+// elements [base + 4g .. +3] and [base + 8 + 4g .. +3].
+__device__ __forceinline__ bf16x8 lds_pair(const bf16_t* row, int base, int g) {
+  const uint2 lo = *reinterpret_cast<const uint2*>(row + base + 4 * g);
+  const uint2 hi = *reinterpret_cast<const uint2*>(row + base + 8 + 4 * g);
+  return as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
+}
+
+// Registers 8h..8h+7 of an accumulator, scaled, as a bf16 operand.
+__device__ __forceinline__ bf16x8 to_operand(const f32x16& acc, int h, float scale) {
+  bf16x8 o;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) o[e] = (__bf16)(acc[8 * h + e] * scale);
+  return o;
+}
+
+// The same as a two-term bf16 split x = hi + lo (about 16 significant bits).
+__device__ __forceinline__ void to_operand_split(const f32x16& acc, int h, float scale, bf16x8& hi,
+                                                 bf16x8& lo) {
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float x = acc[8 * h + e] * scale;
+    hi[e] = (__bf16)x;
+    lo[e] = (__bf16)(x - (float)hi[e]);
+  }
+}
+
+template <int RKP, int RVP>
+__global__ __launch_bounds__(kPThreads) void prefill_bf16_kernel(PrefillArgs a) {
+  constexpr int KS = RKP / 16;        // K-steps of the score product (over features)
+  constexpr int QT = RKP / 32;        // accumulator tiles of Q~^T
+  constexpr int ZT = RVP / 32;        // accumulator tiles of Z^T
+  constexpr int ZK = RVP / 16;        // K-steps of the output product
+  constexpr int CKS = RKP + 4;        // token-major K tile row stride (elements)
+  constexpr int CVS = kPage + 4;      // feature-major V tile row stride (elements)
+  constexpr int UKS = kMaxDPrefill + 8;
+  constexpr int UVS = RVP + 4;
+  constexpr int CH = ((64 + 96) * 8 + kPThreads - 1) / kPThreads;  // max 16-byte chunks per thread per page
+
+  __shared__ __attribute__((aligned(16))) bf16_t s_ukt[RKP * UKS];
+  __shared__ __attribute__((aligned(16))) bf16_t s_uv[kMaxDPrefill * UVS];
+  __shared__ __attribute__((aligned(16))) bf16_t s_ck[2][kPage * CKS];
+  __shared__ __attribute__((aligned(16))) bf16_t s_cv[2][RVP * CVS];
+
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  const int col = lane & 31, g = lane >> 5;
+  const int bh = blockIdx.x;
+  const int h = bh % a.H;
+  const int nqb = (a.M + kQBlock - 1) / kQBlock;
+  const int qb = nqb - 1 - (int)blockIdx.y;  // heaviest (latest) query blocks first
+  const int d = a.d, rk = a.rk, rv = a.rv, M = a.M, p0 = a.p0;
+  const int q0 = qb * kQBlock;
+  const int qw0 = q0 + wave * 32;
+  const int myq = qw0 + col;
+  const bool q_ok = myq < M;
+  const bool wave_live = qw0 < M;
+  const int qlast_w = min(qw0 + 31, M - 1);                    // last query of this wave
+  const int kmax = p0 + min(q0 + kQBlock, M);                  // keys [0, kmax) matter to the block
+  const int npages = (kmax + kPage - 1) / kPage;
+
+  // ---- constant LDS: U_k^T and U_v (zero padded), padding of the page tiles ----
+  const bf16_t* uk = static_cast<const bf16_t*>(a.uk) + (size_t)h * d * rk;  // [d][rk]
+  for (int e = tid; e < d * RKP; e += kPThreads) {
+    const int i = e / RKP, j = e - i * RKP;
+    s_ukt[j * UKS + i] = (j < rk) ? uk[(size_t)i * rk + j] : bf16_t(0);
+  }
+  const bf16_t* uv = static_cast<const bf16_t*>(a.uv) + (size_t)h * d * rv;  // [d][rv]
+  for (int e = tid; e < d * RVP; e += kPThreads) {
+    const int i = e / RVP, j = e - i * RVP;
+    s_uv[i * UVS + j] = (j < rv) ? uv[(size_t)i * rv + j] : bf16_t(0);
+  }
+  for (int e = tid; e < 2 * kPage * (RKP - rk); e += kPThreads) {  // K features >= r_k
+    const int buf = e / (kPage * (RKP - rk)), r = e - buf * kPage * (RKP - rk);
+    const int n = r / (RKP - rk), j = rk + (r - n * (RKP - rk));
+    s_ck[buf][n * CKS + j] = 0;
+  }
+  for (int e = tid; e < 2 * kPage * (RVP - rv); e += kPThreads) {  // V rows >= r_v: ones, then zeros
+    const int buf = e / (kPage * (RVP - rv)), r = e - buf * kPage * (RVP - rv);
+    const int j = rv + r / kPage, n = r % kPage;
+    s_cv[buf][j * CVS + n] = (j == rv) ? kOne : bf16_t(0);
+  }
+
+  // ---- page staging: (rk + rv) feature rows x 8 chunks of 8 tokens ----
+  const size_t unit = (size_t)(bh / a.H) * a.H + h;
+  const bf16_t* ckb = static_cast<const bf16_t*>(a.ck) + unit * (size_t)a.n_max * rk;
+  const bf16_t* cvb = static_cast<const bf16_t*>(a.cv) + unit * (size_t)a.n_max * rv;
+  const int nchunks = (rk + rv) * 8;
+  uint4 stage[CH];
+  auto load_page = [&](int pg) {
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+      const int ch = tid + c * kPThreads;
+      if (ch < nchunks) {
+        const int row = ch >> 3, n8 = (ch & 7) * 8;
+        stage[c] = row < rk ? ld16(ckb + ((size_t)pg * kPage * rk + row * kPage + n8))
+                            : ld16(cvb + ((size_t)pg * kPage * rv + (row - rk) * kPage + n8));
+      }
+    }
+  };
+  auto store_page = [&](int pg, int buf) {
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+      const int ch = tid + c * kPThreads;
+      if (ch < nchunks) {
+        const int row = ch >> 3, n8 = (ch & 7) * 8;
+        const bf16_t* v = reinterpret_cast<const bf16_t*>(&stage[c]);
+        if (row < rk) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) s_ck[buf][(n8 + e) * CKS + row] = v[e];
+        } else {
+          uint4 w = stage[c];
+          const int n0 = pg * kPage + n8;
+          if (n0 + 8 > kmax) {  // tokens past the last key: zero (the slot may hold anything)
+            bf16_t* wv = reinterpret_cast<bf16_t*>(&w);
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+              if (n0 + e >= kmax) wv[e] = 0;
+          }
+          bf16_t* dst = &s_cv[buf][(row - rk) * CVS + n8];
+          *reinterpret_cast<uint2*>(dst) = make_uint2(w.x, w.y);
+          *reinterpret_cast<uint2*>(dst + 4) = make_uint2(w.z, w.w);
+        }
+      }
+    }
+  };
+
+  load_page(0);
+  __syncthreads();  // constant LDS written
+  store_page(0, 0);
+
+  // ---- D1 = Q~^T for this wave's 32 queries ----
+  bf16x8 qop[KS], qlo[KS];  // Q~ as hi + lo bf16 terms: scores keep ~fp32 accuracy
+  {
+    f32x16 d1[QT];
+#pragma unroll
+    for (int t = 0; t < QT; ++t) d1[t] = f32x16{0.f};
+    const bf16_t* qrow = static_cast<const bf16_t*>(a.q) + (unit * M + (q_ok ? myq : 0)) * d;
+    const uint4 zero = make_uint4(0, 0, 0, 0);
+    for (int s = 0; s < d / 16; ++s) {
+      const uint4 bq = q_ok ? ld16(qrow + 16 * s + 8 * g) : zero;
+#pragma unroll
+      for (int t = 0; t < QT; ++t) {
+        const bf16x8 au = as_bf16x8(*reinterpret_cast<const uint4*>(&s_ukt[(32 * t + col) * UKS + 16 * s + 8 * g]));
+        d1[t] = mfma(au, as_bf16x8(bq), d1[t]);
+      }
+    }
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) to_operand_split(d1[ks / 2], ks % 2, a.qscale, qop[ks], qlo[ks]);
+  }
+  __syncthreads();  // page 0 staged
+
+  // ---- online softmax over the key pages ----
+  f32x16 zacc[ZT];
+#pragma unroll
+  for (int t = 0; t < ZT; ++t) zacc[t] = f32x16{0.f};
+  float m_run = 0.f;
+  const int qpos = p0 + myq;  // absolute position of this lane's query
+
+  for (int p = 0; p < npages; ++p) {
+    const int buf = p & 1;
+    if (p + 1 < npages) load_page(p + 1);
+    const int key0 = p * kPage;
+    if (wave_live && key0 <= p0 + qlast_w) {
+      const bool first = (p == 0);
+      const bool diag = key0 + kPage - 1 > p0 + qw0;
+      const f32x16 cinit = first ? f32x16{0.f} : f32x16{0.f} - m_run;
+      f32x16 sc[2];
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt) {
+        sc[kt] = cinit;
+        const bf16_t* krow = &s_ck[buf][(32 * kt + col) * CKS];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const bf16x8 ak = lds_pair(krow, 16 * ks, g);
+          sc[kt] = mfma(ak, qop[ks], sc[kt]);
+          sc[kt] = mfma(ak, qlo[ks], sc[kt]);
+        }
+      }
+      if (diag) {
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int n = key0 + 32 * kt + 8 * (r / 4) + 4 * g + (r % 4);
+            if (n > qpos) sc[kt][r] = neg_inf();
+          }
+      }
+      float mx = neg_inf();
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[kt][r]);
+      mx = fmaxf(mx, xor_shfl(mx, 32));
+      if (first) {
+        m_run = mx;
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) sc[kt] -= mx;
+      } else if (__builtin_amdgcn_ballot_w64(mx > kLazy) != 0) {
+        const float dl = mx > kLazy ? mx : 0.f;
+        const float alpha = __builtin_amdgcn_exp2f(-dl);
+        m_run += dl;
+#pragma unroll
+        for (int t = 0; t < ZT; ++t) zacc[t] *= alpha;
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) sc[kt] -= dl;
+      }
+      // P as the value product's B operands: K-step u = registers 8(u%2).. of tile u/2
+      bf16x8 pop[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pop[u][e] = (__bf16)__builtin_amdgcn_exp2f(sc[u / 2][8 * (u % 2) + e]);
+      }
+#pragma unroll
+      for (int t = 0; t < ZT; ++t) {
+        const bf16_t* vrow = &s_cv[buf][(32 * t + col) * CVS];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) zacc[t] = mfma(lds_pair(vrow, 16 * u, g), pop[u], zacc[t]);
+      }
+    }
+    if (p + 1 < npages) store_page(p + 1, buf ^ 1);
+    __syncthreads();
+  }
+
+  // ---- epilogue: l from the ones row, O^T = U_v (Z / l)^T + mu_v ----
+  if (!wave_live) return;
+  float lsum = 0.f;
+  {
+    const int t = rv / 32, rr = rv % 32;
+    const int gl = (rr / 4) % 2, reg = 4 * (rr / 8) + rr % 4;
+#pragma unroll
+    for (int tt = 0; tt < ZT; ++tt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        if (tt == t && r == reg && g == gl) lsum = zacc[tt][r];
+    lsum += xor_shfl(lsum, 32);
+  }
+  const float inv_l = 1.0f / lsum;
+  bf16x8 zop[ZK];
+#pragma unroll
+  for (int ks = 0; ks < ZK; ++ks) zop[ks] = to_operand(zacc[ks / 2], ks % 2, inv_l);
+  const bf16_t* muv = a.muv ? static_cast<const bf16_t*>(a.muv) + (size_t)h * d : nullptr;
+  const size_t orow = (unit * M + myq) * (size_t)d;
+  for (int it = 0; it < d / 32; ++it) {
+    f32x16 o = f32x16{0.f};
+    const bf16_t* urow = &s_uv[(32 * it + col) * UVS];
+#pragma unroll
+    for (int ks = 0; ks < ZK; ++ks) o = mfma(lds_pair(urow, 16 * ks, g), zop[ks], o);
+    if (q_ok) {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const int i0 = 32 * it + 8 * c + 4 * g;
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = o[4 * c + e] + (muv ? bf16_to_f32(muv[i0 + e]) : 0.f);
+        if (a.out_dtype == LLA_F32) {
+          *reinterpret_cast<float4*>(static_cast<float*>(a.out) + orow + i0) = make_float4(v[0], v[1], v[2], v[3]);
+        } else {
+          bf16_t* op = static_cast<bf16_t*>(a.out) + orow + i0;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) op[e] = f32_to_bf16(v[e]);
+        }
+      }
+    }
+  }
+}
+
+template <int RKP, int RVP>
+hipError_t launch_t(const PrefillArgs& a, hipStream_t stream) {
+  const int nqb = (a.M + kQBlock - 1) / kQBlock;
+  dim3 grid(a.B * a.H, nqb);
+  hipLaunchKernelGGL((prefill_bf16_kernel<RKP, RVP>), grid, dim3(kPThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_prefill_bf16(const PrefillArgs& a, hipStream_t stream) {
+  // K features padded to 32 / 64; V features padded past r_v (room for the ones row)
+  const int rkp = a.rk <= 32 ? 32 : 64;
+  const int rvp = a.rv < 32 ? 32 : a.rv < 64 ? 64 : 96;
+  if (rkp == 32 && rvp == 32) return launch_t<32, 32>(a, stream);
+  if (rkp == 32 && rvp == 64) return launch_t<32, 64>(a, stream);
+  if (rkp == 32 && rvp == 96) return launch_t<32, 96>(a, stream);
+  if (rkp == 64 && rvp == 32) return launch_t<64, 32>(a, stream);
+  if (rkp == 64 && rvp == 64) return launch_t<64, 64>(a, stream);
+  return launch_t<64, 96>(a, stream);
+}
+
 }  // namespace lla

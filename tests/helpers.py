@@ -27,9 +27,19 @@ def errors(got: np.ndarray, ref: np.ndarray):
     return float(np.max(np.abs(err))), float(np.linalg.norm(err) / np.linalg.norm(ref))
 
 
-def assert_close(got, ref, in_dtype, what=""):
+def round_bf16(x: np.ndarray) -> np.ndarray:
+    """Round-to-nearest-even to bfloat16 (via torch), back to float64."""
+    return torch.from_numpy(np.asarray(x, dtype=np.float32)).to(torch.bfloat16).to(torch.float64).numpy()
+
+
+def assert_close(got, ref, in_dtype, what="", out_bf16=False):
+    """Parity check at the stated tolerance.  A bf16 output is compared with
+    the reference rounded to bf16 the same way (the output type's own rounding
+    is not an error of the computation)."""
     got = np.asarray(got, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
+    if out_bf16:
+        ref = round_bf16(ref)
     assert got.shape == ref.shape, (got.shape, ref.shape)
     assert np.all(np.isfinite(got)), f"{what}: non-finite output"
     max_abs, rel = errors(got, ref)

@@ -103,7 +103,8 @@ def test_bf16_per_sequence_lengths_and_bf16_out():
         out = lla.decode_attn(q, pk, pv, uk, uv, n_ctx=N, ctx_len=ctx, workspace=ws, out_dtype=out_dtype)
         torch.cuda.synchronize()
         assert out.dtype == out_dtype
-        assert_close(f64(out), ref, torch.bfloat16, f"ctx_len out={out_dtype}")
+        assert_close(f64(out), ref, torch.bfloat16, f"ctx_len out={out_dtype}",
+                     out_bf16=out_dtype == torch.bfloat16)
 
 
 def test_out_of_range_lengths_give_nan():

@@ -1,0 +1,131 @@
+"""GPU parity of lla_prefill_attn (causal prefill over the latent cache) against
+the float64 oracle, through the C ABI."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_15456_amd import lla, workloads as W
+from tests.helpers import assert_close, f64, log
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+SMALL = W.Workload("pf_small", 1, 3, 128, 4, 2, 0, ((18, 30),), torch.bfloat16)
+
+
+def _paged(c, n_max, poison):
+    """Paged cache of the latents c [B, H, N, r]; slots past N hold NaN when poisoned
+    (they must not leak into any output), zeros otherwise."""
+    B, H, N, r = c.shape
+    full = c.new_full((B, H, n_max, r), float("nan") if poison else 0.0)
+    full[:, :, :N] = c
+    return full.view(B, H, n_max // 64, 64, r).transpose(-1, -2).contiguous()
+
+
+def _case(wl, r_k, r_v, B, M, p0, dtype, means=True, poison=True, n_max=None, qmul=1.0, kramp=0.0):
+    N = p0 + M
+    n_max = n_max or ((N + 63) // 64) * 64 + 64
+    ck = W.latents(wl, r_k, "k", 0, B=B, N=N, device=DEV, dtype=torch.float32)
+    cv = W.latents(wl, r_v, "v", 0, B=B, N=N, device=DEV, dtype=torch.float32)
+    if kramp:  # latents growing along the context: later keys score higher (forces rescales)
+        ck = ck * (1.0 + kramp * torch.arange(N, device=DEV, dtype=torch.float32)[None, None, :, None] / N)
+    ck, cv = ck.to(dtype), cv.to(dtype)
+    q = W.queries(wl, 0, 2, B=B, M=M, device=DEV, dtype=torch.float32)
+    q = (q * qmul).to(dtype)
+    uk, uv, muk, muv = W.codec_loop(wl, r_k, r_v, 0, 2, DEV, dtype, means=means)
+    pk, pv = _paged(ck, n_max, poison), _paged(cv, n_max, poison)
+    return q, ck, cv, uk, uv, muk, muv, pk, pv
+
+
+def _oracle(q, ck, cv, uk, uv, muk, muv, p0, rows=None, units=None, scale=None):
+    return oracle.prefill_attn_batched(f64(q), f64(ck), f64(cv), f64(uk), f64(uv),
+                                       None if muk is None else f64(muk),
+                                       None if muv is None else f64(muv), scale, p0=p0,
+                                       rows=rows, units=units)
+
+
+@pytest.mark.parametrize("r_k,r_v", [(18, 30), (36, 60), (7, 9), (64, 95), (32, 31), (33, 64), (1, 1)])
+@pytest.mark.parametrize("M,p0", [(1, 0), (33, 0), (128, 0), (200, 5), (77, 100), (130, 64)])
+def test_bf16_prefill(r_k, r_v, M, p0):
+    log(f"prefill bf16 r=({r_k},{r_v}) M={M} p0={p0}")
+    q, ck, cv, uk, uv, muk, muv, pk, pv = _case(SMALL, r_k, r_v, 2, M, p0, torch.bfloat16)
+    out = lla.prefill_attn(q, pk, pv, uk, uv, p0=p0, mu_k=muk, mu_v=muv)
+    torch.cuda.synchronize()
+    assert_close(f64(out), _oracle(q, ck, cv, uk, uv, muk, muv, p0), torch.bfloat16, "prefill")
+
+
+@pytest.mark.parametrize("M,p0", [(1, 0), (65, 3), (130, 64)])
+def test_fp32_prefill(M, p0):
+    log(f"prefill fp32 M={M} p0={p0}")
+    q, ck, cv, uk, uv, muk, muv, pk, pv = _case(SMALL, 36, 60, 2, M, p0, torch.float32)
+    out = lla.prefill_attn(q, pk, pv, uk, uv, p0=p0, mu_k=muk, mu_v=muv)
+    torch.cuda.synchronize()
+    assert_close(f64(out), _oracle(q, ck, cv, uk, uv, muk, muv, p0), torch.float32, "prefill fp32")
+
+
+def test_bf16_out_and_custom_scale():
+    q, ck, cv, uk, uv, muk, muv, pk, pv = _case(SMALL, 18, 30, 2, 150, 20, torch.bfloat16, means=False)
+    out = lla.prefill_attn(q, pk, pv, uk, uv, p0=20, scale=0.2, out_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    assert out.dtype == torch.bfloat16
+    assert_close(f64(out), _oracle(q, ck, cv, uk, uv, None, None, 20, scale=0.2), torch.bfloat16, "bf16 out",
+                 out_bf16=True)
+
+
+@pytest.mark.parametrize("qmul,kramp", [(4.0, 0.0), (1.0, 6.0), (3.0, 4.0)])
+def test_peaked_and_rising_scores(qmul, kramp):
+    """Peaked softmax rows and keys whose scores rise along the context: the
+    running max is raised page after page (lazy rescale path)."""
+    q, ck, cv, uk, uv, muk, muv, pk, pv = _case(SMALL, 18, 30, 2, 600, 0, torch.bfloat16, qmul=qmul,
+                                                kramp=kramp)
+    out = lla.prefill_attn(q, pk, pv, uk, uv, p0=0, mu_k=muk, mu_v=muv)
+    torch.cuda.synchronize()
+    assert_close(f64(out), _oracle(q, ck, cv, uk, uv, muk, muv, 0), torch.bfloat16, f"q x{qmul} ramp {kramp}")
+
+
+def test_prefill_rows_match_decode():
+    """Row m of a prefill equals a decode over the first p0 + m + 1 tokens."""
+    M, p0 = 96, 40
+    q, ck, cv, uk, uv, muk, muv, pk, pv = _case(SMALL, 36, 60, 2, M, p0, torch.bfloat16, poison=False)
+    out = lla.prefill_attn(q, pk, pv, uk, uv, p0=p0, mu_k=muk, mu_v=muv)
+    for m in (0, 31, 32, 95):
+        n = p0 + m + 1
+        dec = lla.decode_attn(q[:, :, m].contiguous(), pk, pv, uk, uv, n_ctx=n, mu_k=muk, mu_v=muv)
+        torch.cuda.synchronize()
+        assert_close(f64(out[:, :, m]), f64(dec), torch.bfloat16, f"row {m}")
+
+
+@pytest.mark.slow
+def test_full_prefill_write():
+    """Workload 5 at full size: encode 4 x 8192 tokens into the (18, 30) cache,
+    then causal prefill at every loop; sampled rows of sampled (b, h)."""
+    wl = W.WORKLOADS["prefill_write"]
+    r_k, r_v = wl.ranks[0]
+    B, M = wl.B, wl.N
+    log("prefill_write full size: encode")
+    xk = W.stacked_kv(wl, "k", 0, device=DEV)
+    xv = W.stacked_kv(wl, "v", 0, device=DEV)
+    wk = W.down_projection(wl, r_k, "k", 0, DEV)
+    wv = W.down_projection(wl, r_v, "v", 0, DEV)
+    ck = lla.alloc_cache(B, wl.H, M, r_k)
+    cv = lla.alloc_cache(B, wl.H, M, r_v)
+    lla.encode(xk, xv, wk, wv, ck, cv, T=wl.T, pos0=0)
+    del xk, xv
+    units = [(0, 0), (1, 7), (3, 15)]
+    rows = [0, 1, 63, 64, 127, 128, 4095, 5000, 8190, 8191]
+    lat_k = {u: f64(lla.from_paged(ck[u[0]:u[0] + 1, u[1]:u[1] + 1]))[0, 0] for u in units}
+    lat_v = {u: f64(lla.from_paged(cv[u[0]:u[0] + 1, u[1]:u[1] + 1]))[0, 0] for u in units}
+    for loop in range(wl.T):
+        log(f"prefill_write full size: loop {loop}")
+        q = W.queries(wl, 0, loop, M=M, device=DEV)
+        uk, uv, _, _ = W.codec_loop(wl, r_k, r_v, 0, loop, DEV)
+        out = lla.prefill_attn(q, ck, cv, uk, uv, p0=0)
+        torch.cuda.synchronize()
+        o = out[:, :, rows].cpu().double().numpy()
+        assert np.all(np.isfinite(out.cpu().numpy()))
+        for (b, h) in units:
+            ref = np.stack([oracle.decode_attn(f64(q[b, h, m]), lat_k[(b, h)][:m + 1], lat_v[(b, h)][:m + 1],
+                                               f64(uk[h]), f64(uv[h])) for m in rows])
+            assert_close(o[b, h], ref, torch.bfloat16, f"loop {loop} unit ({b},{h})")
