@@ -206,6 +206,86 @@ def cpu_baseline_decode(wl, r_k, r_v, cache, call, torch, budget_s=15.0):
 
 
 # ---------------------------------------------------------------------------
+# prefill + cache write (prefill_write)
+# ---------------------------------------------------------------------------
+
+def prefill_flops(B, H, M, p0, d, r_k, r_v):
+    """Algorithmic flops of one causal prefill call: 2 (r_k + r_v) per causal
+    (query, key) pair plus the absorption products Q U_k and Z U_v^T."""
+    pairs = M * p0 + M * (M + 1) // 2
+    return B * H * (2 * (r_k + r_v) * pairs + 2 * M * d * (r_k + r_v))
+
+
+def encode_bytes(B, M, H, K, r_k, r_v, elem=2):
+    """Algorithmic bytes of one encode: x_k, x_v read, W_down^T read, latents written."""
+    return 2 * B * M * H * K * elem + H * (r_k + r_v) * K * elem + B * H * M * (r_k + r_v) * elem
+
+
+def run_prefill(args, torch, lla, W):
+    wl = W.WORKLOADS["prefill_write"]
+    r_k, r_v = wl.ranks[0]
+    B, M, H, d, T = wl.B, wl.N, wl.H, wl.d, wl.T
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    xk = W.stacked_kv(wl, "k", 0, device=dev)
+    xv = W.stacked_kv(wl, "v", 0, device=dev)
+    wk = W.down_projection(wl, r_k, "k", 0, dev)
+    wv = W.down_projection(wl, r_v, "v", 0, dev)
+    ck = lla.alloc_cache(B, H, M, r_k, device=dev)
+    cv = lla.alloc_cache(B, H, M, r_v, device=dev)
+    loops = []
+    for l in range(T):
+        q = W.queries(wl, 0, l, M=M, device=dev)
+        uk, uv, _, _ = W.codec_loop(wl, r_k, r_v, 0, l, dev)
+        loops.append((q, uk, uv, torch.empty((B, H, M, d), dtype=torch.float32, device=dev)))
+    torch.cuda.synchronize()
+    enc_t, pre_t = KernelTimer(torch, stream), KernelTimer(torch, stream)
+
+    def step(timed):
+        s = enc_t.start() if timed else None
+        lla.encode(xk, xv, wk, wv, ck, cv, T=T, pos0=0)
+        if timed:
+            enc_t.stop(s)
+        for q, uk, uv, out in loops:
+            s = pre_t.start() if timed else None
+            lla.prefill_attn(q, ck, cv, uk, uv, p0=0, out=out)
+            if timed:
+                pre_t.stop(s)
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for _ in range(args.steps):
+        step(True)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    step_ms = t0.elapsed_time(t1) / args.steps
+    enc_ms, pre_ms = enc_t.mean_ms(), pre_t.mean_ms()
+    fl = prefill_flops(B, H, M, 0, d, r_k, r_v)
+    eb = encode_bytes(B, M, H, T * d, r_k, r_v)
+    tflops = fl / (pre_ms * 1e-3) / 1e12
+    return {
+        "metric": "prefill + cache write tokens/sec (encode of the loop-stacked K/V, causal prefill at every loop)",
+        "value": round(B * M / (step_ms * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(step_ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": wl.description, "batch": B, "new_tokens": M, "heads": H, "d_head": d, "loops": T,
+                   "r_k": r_k, "r_v": r_v, "parallelism": "single GPU"},
+        "roofline": {"bound": "mfma", "achieved": round(tflops, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(tflops / BF16_PEAK_TFLOPS, 4), "traffic": None,
+                     "kernel": "prefill_bf16_kernel (lla_prefill_attn)", "flops_per_launch": fl,
+                     "avg_launch_ms": round(pre_ms, 5)},
+        "encode": {"bound": "hbm", "achieved": round(eb / (enc_ms * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS,
+                   "unit": "GB/s", "frac": round(eb / (enc_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                   "bytes_per_launch": eb, "avg_launch_ms": round(enc_ms, 5)},
+        "cpu_baseline": None,
+    }
+
+
+# ---------------------------------------------------------------------------
 # main
 # ---------------------------------------------------------------------------
 
@@ -233,8 +313,8 @@ def main():
         return
 
     if args.workload == "prefill_write":
-        print(json.dumps({"error": "the prefill_write workload is measured once the bf16 prefill kernel exists"}))
-        sys.exit(2)
+        print(json.dumps(run_prefill(args, torch, lla, W)), flush=True)
+        return
 
     wl, results = run_decode(args, torch, lla, W)
     head = results[0]
