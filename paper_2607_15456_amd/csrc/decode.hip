@@ -39,7 +39,6 @@
 namespace lla {
 namespace {
 
-constexpr int VB = 8;           // V row-group loads issued together per wave
 
 template <int BYTES> struct VecT;
 template <> struct VecT<16> { typedef uint4 type; };
@@ -137,10 +136,15 @@ __device__ __forceinline__ int vec_width(int r) {
   return (r % E == 0) ? E : (r % 4 == 0) ? 4 : (r % 2 == 0) ? 2 : 1;
 }
 
-template <typename TIn, int GV, int kWaves>
-__global__ __launch_bounds__(kWaves * kWave) __attribute__((amdgpu_waves_per_eu(4)))
+// DEEP: at most two wavefronts per SIMD; the doubled register budget holds a
+// second batch of loads in flight (software pipelining).  Otherwise four per
+// SIMD, one batch at a time.
+template <typename TIn, int GV, int kWaves, bool DEEP>
+__global__ __launch_bounds__(kWaves * kWave) __attribute__((amdgpu_waves_per_eu(DEEP ? 2 : 4)))
 void decode_kernel(DecodeArgs a) {
   constexpr int kThreads = kWaves * kWave;
+  constexpr int KB = 8;  // K rows per load batch (DEEP keeps two batches in flight)
+  constexpr int VB = 8;  // V row groups per load batch
   constexpr int EPL = Elem<TIn>::kPer16B;  // tokens covered by one 16-byte load
   constexpr int LPR = kPage / EPL;         // lanes per 64-token feature row
   constexpr int PPG = kWave / LPR;         // pages per group (K phase) = rows per load (V phase)
@@ -159,7 +163,10 @@ void decode_kernel(DecodeArgs a) {
   __shared__ float s_m[kWaves], s_l[kWaves];
   __shared__ int s_last;
 
-  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  // the wave index is uniform across a wavefront; saying so keeps the page and
+  // row offsets of the buffer loads in scalar registers
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int bm = blockIdx.x / a.splits, split = blockIdx.x - bm * a.splits, h = blockIdx.y;
   int b, m, N;
   if (a.causal) {
@@ -215,6 +222,47 @@ void decode_kernel(DecodeArgs a) {
   float* sp = s_p[wave];
 
   // ---- latent scan, PPG pages per wave per group ----
+  // With PIPE (the DEEP variant's register budget) the next batch of rows is
+  // always in flight while the current one is multiplied: K batches ping-pong
+  // between two register sets, and V batches prefetch across row groups and
+  // pages, so the FMAs of one batch overlap the memory latency of the next.
+  constexpr bool PIPE = DEEP;
+  const int nkb = rk / KB;                                  // full K batches
+  const int nvb = (vg_full + (vg_part ? 1 : 0) + VB - 1) / VB;  // V batches per page
+  constexpr int NKC = (GV + VB - 1) / VB;
+
+  auto kload = [&](uint4 (&r)[KB], int gbase, int jb) {
+#pragma unroll
+    for (int u = 0; u < KB; ++u) r[u] = buf_ld16(rk_src, vk_lane, gbase + (jb * KB + u) * kPage * ES);
+  };
+  auto kfma = [&](const uint4 (&r)[KB], int jb, float (&acc)[EPL]) {
+    float qj[KB];
+#pragma unroll
+    for (int u = 0; u < KB; u += 4) {
+      const float4 qa = *reinterpret_cast<const float4*>(&s_qt[jb * KB + u]);
+      qj[u] = qa.x;
+      qj[u + 1] = qa.y;
+      qj[u + 2] = qa.z;
+      qj[u + 3] = qa.w;
+    }
+#pragma unroll
+    for (int u = 0; u < KB; ++u) {
+      float v[EPL];
+      Elem<TIn>::unpack(r[u], v);
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) acc[e] = fmaf(qj[u], v[e], acc[e]);
+    }
+  };
+  auto vload = [&](uint4 (&r)[VB], int pv, int kc) {
+    const int pbase = pv * vpage_bytes;
+#pragma unroll
+    for (int u = 0; u < VB; ++u) {
+      const int k = kc * VB + u;
+      if (k < vg_full || (k == vg_full && hi < vg_part))
+        r[u] = buf_ld16(rv_src, vv_lane, pbase + k * PPG * kPage * ES);
+    }
+  };
+
   for (int g0 = pb + wave * PPG; g0 < pe; g0 += kWaves * PPG) {
     const int np = min(PPG, pe - g0);
     float acc[EPL];
@@ -222,23 +270,23 @@ void decode_kernel(DecodeArgs a) {
     for (int e = 0; e < EPL; ++e) acc[e] = 0.f;
     if (hi < np) {
       const int gbase = g0 * kpage_bytes;
-      int j = 0;
-      for (; j + 8 <= rk; j += 8) {
-        const float4 qa = *reinterpret_cast<const float4*>(&s_qt[j]);
-        const float4 qb = *reinterpret_cast<const float4*>(&s_qt[j + 4]);
-        const float qj[8] = {qa.x, qa.y, qa.z, qa.w, qb.x, qb.y, qb.z, qb.w};
-        uint4 raw[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) raw[u] = buf_ld16(rk_src, vk_lane, gbase + (j + u) * kPage * ES);
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          float v[EPL];
-          Elem<TIn>::unpack(raw[u], v);
-#pragma unroll
-          for (int e = 0; e < EPL; ++e) acc[e] = fmaf(qj[u], v[e], acc[e]);
+      if constexpr (PIPE) {
+        uint4 ka[KB], kb2[KB];
+        if (nkb > 0) kload(ka, gbase, 0);
+        for (int jb = 0; jb < nkb; jb += 2) {
+          if (jb + 1 < nkb) kload(kb2, gbase, jb + 1);
+          kfma(ka, jb, acc);
+          if (jb + 2 < nkb) kload(ka, gbase, jb + 2);
+          if (jb + 1 < nkb) kfma(kb2, jb + 1, acc);
+        }
+      } else {
+        for (int jb = 0; jb < nkb; ++jb) {
+          uint4 ka[KB];
+          kload(ka, gbase, jb);
+          kfma(ka, jb, acc);
         }
       }
-      for (; j < rk; ++j) {
+      for (int j = nkb * KB; j < rk; ++j) {
         const float q1 = s_qt[j];
         float v[EPL];
         Elem<TIn>::unpack(buf_ld16(rk_src, vk_lane, gbase + j * kPage * ES), v);
@@ -246,6 +294,9 @@ void decode_kernel(DecodeArgs a) {
         for (int e = 0; e < EPL; ++e) acc[e] = fmaf(q1, v[e], acc[e]);
       }
     }
+    uint4 vcur[VB];
+    if constexpr (PIPE) vload(vcur, g0, 0);  // first V batch in flight during the softmax
+
     // scores of invalid pages / tokens beyond N are -inf
     const int n0 = (g0 + hi) * kPage + lo * EPL;
     float mb = neg_inf();
@@ -296,36 +347,41 @@ void decode_kernel(DecodeArgs a) {
         for (int e = 0; e < EPL; ++e)
           if (nv0 + e >= N) p8[e] = 0.f;
       }
-      const int pbase = pv * vpage_bytes;
-      // VB row groups per batch: their loads in flight together, then their FMAs;
-      // the scheduling barrier keeps later batches from being hoisted
 #pragma unroll
-      for (int kc = 0; kc < GV; kc += VB) {
-        uint4 raw[VB];
-#pragma unroll
-        for (int u = 0; u < VB; ++u) {
-          const int k = kc + u;
-          if (k < vg_full || (k == vg_full && hi < vg_part))
-            raw[u] = buf_ld16(rv_src, vv_lane, pbase + k * PPG * kPage * ES);
-        }
-#pragma unroll
-        for (int u = 0; u < VB; ++u) {
-          const int k = kc + u;
-          if (k < vg_full || (k == vg_full && hi < vg_part)) {
-            float v[EPL];
-            Elem<TIn>::unpack(raw[u], v);
-            if (tail) {
-#pragma unroll
-              for (int e = 0; e < EPL; ++e)
-                if (p8[e] == 0.f) v[e] = 0.f;
-            }
-            float t = 0.f;
-#pragma unroll
-            for (int e = 0; e < EPL; ++e) t = fmaf(p8[e], v[e], t);
-            zacc[k] += t;
+      for (int kc = 0; kc < NKC; ++kc) {
+        if (kc < nvb) {
+          uint4 vnext[VB];
+          if constexpr (PIPE) {
+            if (kc + 1 < nvb)
+              vload(vnext, pv, kc + 1);
+            else if (pg + 1 < np)
+              vload(vnext, pv + 1, 0);
+          } else {
+            vload(vcur, pv, kc);
           }
+#pragma unroll
+          for (int u = 0; u < VB; ++u) {
+            const int k = kc * VB + u;
+            if (k < GV && (k < vg_full || (k == vg_full && hi < vg_part))) {
+              float v[EPL];
+              Elem<TIn>::unpack(vcur[u], v);
+              if (tail) {
+#pragma unroll
+                for (int e = 0; e < EPL; ++e)
+                  if (p8[e] == 0.f) v[e] = 0.f;
+              }
+              float t = 0.f;
+#pragma unroll
+              for (int e = 0; e < EPL; ++e) t = fmaf(p8[e], v[e], t);
+              zacc[k] += t;
+            }
+          }
+          if constexpr (PIPE) {
+#pragma unroll
+            for (int u = 0; u < VB; ++u) vcur[u] = vnext[u];
+          }
+          __builtin_amdgcn_sched_barrier(0);
         }
-        __builtin_amdgcn_sched_barrier(0);
       }
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -435,10 +491,17 @@ void decode_kernel(DecodeArgs a) {
 template <typename TIn, int GV>
 hipError_t launch_t(const DecodeArgs& a, hipStream_t stream) {
   dim3 grid(a.B * a.M * a.splits, a.H);
-  if (a.waves == 8)
-    hipLaunchKernelGGL((decode_kernel<TIn, GV, 8>), grid, dim3(8 * kWave), 0, stream, a);
-  else
-    hipLaunchKernelGGL((decode_kernel<TIn, GV, 4>), grid, dim3(4 * kWave), 0, stream, a);
+  if (a.waves == 8) {
+    if (a.deep)
+      hipLaunchKernelGGL((decode_kernel<TIn, GV, 8, true>), grid, dim3(8 * kWave), 0, stream, a);
+    else
+      hipLaunchKernelGGL((decode_kernel<TIn, GV, 8, false>), grid, dim3(8 * kWave), 0, stream, a);
+  } else {
+    if (a.deep)
+      hipLaunchKernelGGL((decode_kernel<TIn, GV, 4, true>), grid, dim3(4 * kWave), 0, stream, a);
+    else
+      hipLaunchKernelGGL((decode_kernel<TIn, GV, 4, false>), grid, dim3(4 * kWave), 0, stream, a);
+  }
   return hipGetLastError();
 }
 

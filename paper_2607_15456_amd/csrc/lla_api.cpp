@@ -56,10 +56,10 @@ size_t workspace_bytes(int B, int H, int r_v, int n_ctx) {
 // wavefronts (4-wave workgroups when (b, h) units alone reach that, 8-wave
 // ones otherwise); only smaller batches split the context (split-K), up to 8
 // wavefronts per compute unit, with every wavefront keeping at least one
-// 8-page group.  LLA_DECODE_WAVES / LLA_DECODE_SPLITS override the choice
-// (for tuning sweeps).
+// 8-page group.  LLA_DECODE_WAVES / LLA_DECODE_SPLITS / LLA_DECODE_DEEP
+// override the choice (for tuning sweeps).
 struct DecodeShape {
-  int waves, splits;
+  int waves, splits, deep;
 };
 
 int env_int(const char* name) {
@@ -67,13 +67,17 @@ int env_int(const char* name) {
   return e ? std::atoi(e) : 0;
 }
 
-DecodeShape choose_shape(int units, int n_ctx, bool allow_split) {
+DecodeShape choose_shape(int units, int n_ctx, bool allow_split, bool bf16) {
   static const int forced_waves = env_int("LLA_DECODE_WAVES");
   static const int forced_splits = env_int("LLA_DECODE_SPLITS");
+  static const int forced_deep = env_int("LLA_DECODE_DEEP");
   const int pages = (n_ctx + LLA_PAGE_TOKENS - 1) / LLA_PAGE_TOKENS;
   const int groups = (pages + 7) / 8;
   const long target = 8L * lla::device_cu_count();  // resident wavefronts wanted
-  DecodeShape sh{4, 1};
+  // bf16: the software-pipelined variant (two batches of loads in flight per
+  // wavefront, at most 2 wavefronts per SIMD) measured as fast or faster on
+  // every decode workload; fp32 keeps the 4-per-SIMD variant.
+  DecodeShape sh{4, 1, bf16 ? 1 : 0};
   if ((long)units * 4 < target && groups >= 8) sh.waves = 8;
   if (allow_split && (long)units * sh.waves < target) {
     long s = (target + (long)units * sh.waves - 1) / ((long)units * sh.waves);
@@ -85,6 +89,7 @@ DecodeShape choose_shape(int units, int n_ctx, bool allow_split) {
   if (forced_splits > 0 && allow_split) sh.splits = forced_splits;
   if (sh.splits > max_splits(n_ctx)) sh.splits = max_splits(n_ctx);
   if (sh.splits < 1) sh.splits = 1;
+  if (forced_deep) sh.deep = forced_deep > 0 ? 1 : 0;
   return sh;
 }
 
@@ -232,9 +237,10 @@ lla_status lla_decode_attn(int dtype, int out_dtype, int B, int H, int d_head, i
   a.muv = mu_v;
   a.qscale = (float)((double)scale * kLog2e);
   a.out = out;
-  const DecodeShape sh = choose_shape(B * H, n_ctx, workspace != nullptr);
+  const DecodeShape sh = choose_shape(B * H, n_ctx, workspace != nullptr, dtype == LLA_BF16);
   a.waves = sh.waves;
   a.splits = sh.splits;
+  a.deep = sh.deep;
   if (a.splits > 1) {
     const size_t units = (size_t)B * H;
     const size_t counters = (units * sizeof(uint32_t) + 255) / 256 * 256;
@@ -296,6 +302,7 @@ lla_status lla_prefill_attn(int dtype, int out_dtype, int B, int H, int M, int d
   a.causal = 1;
   a.splits = 1;
   a.waves = 4;
+  a.deep = 0;
   a.q = q;
   a.ck = c_k;
   a.cv = c_v;

@@ -17,6 +17,7 @@ struct DecodeArgs {
   int causal;  // 0: decode (N_b from ctx_len / n_ctx); 1: query m attends [0, p0+m]
   int splits;  // workgroups per (b, h, m) along the context
   int waves;   // wavefronts per workgroup (4 or 8)
+  int deep;    // 1: at most 2 wavefronts per SIMD, 16-row load batches
   const int32_t* ctx_len;
   const void* q;
   const void* ck;
