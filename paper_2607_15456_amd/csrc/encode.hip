@@ -23,11 +23,13 @@ namespace lla {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 
-constexpr int kEncWaves = 4;
+// Per-axis fields selected without dynamic indexing (which would spill the
+// argument struct to scratch).
+template <typename T>
+__device__ __forceinline__ T pick(const T (&v)[2], int axis) { return axis ? v[1] : v[0]; }
 
 // Cache index of (b, h, position pos, feature row) in the paged layout.
 __device__ __forceinline__ size_t cache_index(int b, int h, int H, int n_max, int r, int pos,
@@ -36,46 +38,215 @@ __device__ __forceinline__ size_t cache_index(int b, int h, int H, int n_max, in
          (pos % kPage);
 }
 
-// grid: x = token-group blocks, y = row-tile blocks, z = axis * H + h
-// wr = waves of a workgroup laid along rows (1, 2 or 4); the rest along tokens.
-__global__ __launch_bounds__(kEncWaves * kWave) void encode_bf16_kernel(EncodeArgs a, int wr) {
-  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
-  const int axis = blockIdx.z / a.H, h = blockIdx.z - axis * a.H;
-  const int r = a.r[axis], K = a.K;
-  const int tg = blockIdx.x * (kEncWaves / wr) + wave / wr;
-  const int rt = blockIdx.y * wr + wave % wr;
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kEncTok = 32;           // tokens per workgroup block
+constexpr int kEncKC = 512;           // K elements staged per step
+constexpr int kEncXS = kEncKC + 8;    // LDS row stride (elements): 1040 B, staggers banks
+constexpr int kEncMaxTasks = 4;       // 16x16 output tiles per wavefront
+
+__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// One workgroup: 32 consecutive tokens (b, m flattened) x heads [h0, h1) x
+// 16-row output tiles [rt0, rt1) of one axis.  x is streamed through
+// double-buffered LDS one (head, 512-element K chunk) stage at a time: each
+// wave-wide load reads one token's contiguous 1 KB, and the next stage's loads
+// are in flight while the current stage is multiplied.  Each wavefront owns up
+// to 4 (row tile, token tile) 16x16 accumulators (v_mfma_f32_16x16x32_bf16:
+// A = 16 rows of W_down^T from L2, B = 16 tokens from LDS); a head's tiles
+// are written to the feature-major cache pages after its last K chunk.
+// grid: x = token blocks, y = head chunks, z = axis * nrc + row chunk
+__global__ __launch_bounds__(256) void encode_bf16_kernel(EncodeArgs a, int heads_per_wg, int rt_per_wg,
+                                                          int nrc) {
+  __shared__ __attribute__((aligned(16))) bf16_t s_x[2][kEncTok * kEncXS];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int axis = blockIdx.z / nrc, rc = blockIdx.z - axis * nrc;
+  const int r = pick(a.r, axis), K = a.K, H = a.H;
+  const int RT = (r + 15) / 16;
+  const int rt0 = rc * rt_per_wg;
+  if (rt0 >= RT) return;  // uniform over the workgroup
+  const int rt1 = min(RT, rt0 + rt_per_wg);
+  const int ntask = (rt1 - rt0) * 2;  // x 2 token tiles of 16
+  const int h0 = blockIdx.y * heads_per_wg, h1 = min(H, h0 + heads_per_wg);
   const int TT = a.B * a.M;
-  if (tg * 32 >= TT || rt * 32 >= r) return;
-
-  const int col = lane & 31, half = lane >> 5;
-  const int row_a = rt * 32 + col;  // A operand row (feature)
-  const int tok_b = tg * 32 + col;  // B operand column (token)
-  const bool row_ok = row_a < r, tok_ok = tok_b < TT;
-
-  const bf16_t* w = static_cast<const bf16_t*>(a.wdt[axis]) + ((size_t)h * r + (row_ok ? row_a : 0)) * K;
-  const bf16_t* x = static_cast<const bf16_t*>(a.x[axis]) + ((size_t)(tok_ok ? tok_b : 0) * a.H + h) * K;
-  const bf16_t* mu = a.mu[axis] ? static_cast<const bf16_t*>(a.mu[axis]) + (size_t)h * K : nullptr;
-
-  f32x16 acc = {0.f}, accm = {0.f};
+  const int t0 = blockIdx.x * kEncTok;
+  const int nkc = (K + kEncKC - 1) / kEncKC;
+  const int nstage = (h1 - h0) * nkc;
+  const bf16_t* xg = static_cast<const bf16_t*>(pick(a.x, axis));
+  const bf16_t* wg = static_cast<const bf16_t*>(pick(a.wdt, axis));
+  const bf16_t* mug = static_cast<const bf16_t*>(pick(a.mu, axis));
   const uint4 zero = make_uint4(0, 0, 0, 0);
-#pragma unroll 8
-  for (int k0 = 0; k0 < K; k0 += 16) {
-    const int k = k0 + half * 8;
-    const uint4 av = row_ok ? ld16(w + k) : zero;
-    const uint4 bv = tok_ok ? ld16(x + k) : zero;
-    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(av), as_bf16x8(bv), acc, 0, 0, 0);
-    if (mu) {
-      const uint4 mv = ld16(mu + k);
-      accm = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(av), as_bf16x8(mv), accm, 0, 0, 0);
-    }
-  }
-  if (!tok_ok) return;
-  const int b = tok_b / a.M, pos = a.pos0 + (tok_b - b * a.M);
-  bf16_t* c = static_cast<bf16_t*>(a.c[axis]);
+
+  uint4 rgs[8];
+  auto stage_load = [&](int st) {
+    const int h = h0 + st / nkc, k0 = (st % nkc) * kEncKC;
+    const int cpt = min(kEncKC, K - k0) / 8;  // 16-byte chunks per token
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const int row = rt * 32 + 8 * (i / 4) + 4 * half + (i % 4);
-    if (row < r) c[cache_index(b, h, a.H, a.n_max, r, pos, row)] = f32_to_bf16(acc[i] - accm[i]);
+    for (int i = 0; i < 8; ++i) {
+      const int c = tid + i * 256;
+      if (c < kEncTok * cpt) {
+        const int tok = c / cpt, part = c - tok * cpt, t = t0 + tok;
+        rgs[i] = t < TT ? ld16(xg + ((size_t)t * H + h) * K + k0 + part * 8) : zero;
+      }
+    }
+  };
+  auto stage_store = [&](int st, int buf) {
+    const int k0 = (st % nkc) * kEncKC;
+    const int cpt = min(kEncKC, K - k0) / 8;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int c = tid + i * 256;
+      if (c < kEncTok * cpt) {
+        const int tok = c / cpt, part = c - tok * cpt;
+        *reinterpret_cast<uint4*>(&s_x[buf][tok * kEncXS + part * 8]) = rgs[i];
+      }
+    }
+  };
+
+  f32x4 acc[kEncMaxTasks], accm[kEncMaxTasks];
+#pragma unroll
+  for (int u = 0; u < kEncMaxTasks; ++u) acc[u] = accm[u] = f32x4{0.f};
+  const int li = lane & 15, lg = lane >> 4;
+
+  stage_load(0);
+  stage_store(0, 0);
+  __syncthreads();
+  for (int st = 0; st < nstage; ++st) {
+    const int buf = st & 1;
+    if (st + 1 < nstage) stage_load(st + 1);
+    const int h = h0 + st / nkc, kc = st % nkc, k0 = kc * kEncKC;
+    const int ks = min(kEncKC, K - k0) / 32;  // K-steps of 32 in this chunk
+#pragma unroll
+    for (int u = 0; u < kEncMaxTasks; ++u) {
+      const int task = wave + 4 * u;
+      if (task < ntask) {
+        const int rt = rt0 + task / 2, tt = task % 2;
+        const int row = rt * 16 + li;
+        const bool row_ok = row < r;
+        const bf16_t* wrow = wg + ((size_t)h * r + (row_ok ? row : 0)) * K + k0 + 8 * lg;
+        const bf16_t* xrow = &s_x[buf][(tt * 16 + li) * kEncXS + 8 * lg];
+        const bf16_t* mrow = mug ? mug + (size_t)h * K + k0 + 8 * lg : nullptr;
+        for (int s = 0; s < ks; ++s) {
+          const bf16x8 av = as_bf16x8(row_ok ? ld16(wrow + 32 * s) : zero);
+          const bf16x8 bv = as_bf16x8(*reinterpret_cast<const uint4*>(xrow + 32 * s));
+          acc[u] = mfma16(av, bv, acc[u]);
+          if (mrow) accm[u] = mfma16(av, as_bf16x8(ld16(mrow + 32 * s)), accm[u]);
+        }
+        if (kc == nkc - 1) {  // head done: write its tile, c = x W - mu W
+          const int t = t0 + tt * 16 + li;
+          if (t < TT) {
+            const int b = t / a.M, pos = a.pos0 + (t - b * a.M);
+            bf16_t* c = static_cast<bf16_t*>(pick(a.c, axis));
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const int rr = rt * 16 + 4 * lg + e;
+              if (rr < r) c[cache_index(b, h, H, a.n_max, r, pos, rr)] = f32_to_bf16(acc[u][e] - accm[u][e]);
+            }
+          }
+          acc[u] = accm[u] = f32x4{0.f};
+        }
+      }
+    }
+    if (st + 1 < nstage) stage_store(st + 1, buf ^ 1);
+    __syncthreads();
+  }
+}
+
+// Many new tokens at small ranks (a prefill's cache write, r <= 64, T*d = KS*32):
+// the weights stay in registers and the tokens stream past them.  Grid:
+// x = token ranges, y = head, z = axis.  Wavefront w owns 16-row tile rt of
+// the head's W_down^T (its A fragments for the whole T*d held in KS registers
+// of 16 bytes) and one or two 16-token tiles of every 32-token block; blocks
+// of x are staged through double-buffered LDS with coalesced 1 KB loads.  The
+// mean term W_down^T mu is one extra product per workgroup at the start.
+template <int KS>
+__global__ __launch_bounds__(256) void encode_stream_kernel(EncodeArgs a, int blocks_per_wg) {
+  constexpr int K = KS * 32;
+  constexpr int XS = K + 8;
+  __shared__ __attribute__((aligned(16))) bf16_t s_x[2][kEncTok * XS];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int axis = blockIdx.z, h = blockIdx.y, H = a.H;
+  const int r = pick(a.r, axis);
+  const int RT = r > 32 ? 4 : 2;           // 16-row tiles (rows >= r are zero)
+  const int rt = wave % RT;
+  const int ntt = RT == 4 ? 2 : 1;         // token tiles per wavefront
+  const int tt0 = RT == 4 ? 0 : wave / 2;
+  const int TT = a.B * a.M;
+  const int nblk = (TT + kEncTok - 1) / kEncTok;
+  const int b0 = blockIdx.x * blocks_per_wg, b1 = min(nblk, b0 + blocks_per_wg);
+  if (b0 >= b1) return;
+  const int li = lane & 15, lg = lane >> 4;
+  const int row = rt * 16 + li;
+  const bool row_ok = row < r;
+  const uint4 zero = make_uint4(0, 0, 0, 0);
+
+  // resident A fragments of W_down^T rows [16 rt, 16 rt + 16)
+  const bf16_t* wrow = static_cast<const bf16_t*>(pick(a.wdt, axis)) + ((size_t)h * r + (row_ok ? row : 0)) * K + 8 * lg;
+  bf16x8 wf[KS];
+#pragma unroll
+  for (int s = 0; s < KS; ++s) wf[s] = as_bf16x8(row_ok ? ld16(wrow + 32 * s) : zero);
+  f32x4 bmu = f32x4{0.f};
+  if (pick(a.mu, axis)) {
+    const bf16_t* mrow = static_cast<const bf16_t*>(pick(a.mu, axis)) + (size_t)h * K + 8 * lg;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) bmu = mfma16(wf[s], as_bf16x8(ld16(mrow + 32 * s)), bmu);
+  }
+
+  const bf16_t* xg = static_cast<const bf16_t*>(pick(a.x, axis));
+  constexpr int CPT = K / 8;                               // 16-byte chunks per token
+  constexpr int NCH = (kEncTok * CPT + 255) / 256;         // chunks per thread per block
+  uint4 rgs[NCH];
+  auto load_blk = [&](int blk) {
+#pragma unroll
+    for (int i = 0; i < NCH; ++i) {
+      const int c = tid + i * 256;
+      if (c < kEncTok * CPT) {
+        const int tok = c / CPT, part = c - tok * CPT, t = blk * kEncTok + tok;
+        rgs[i] = t < TT ? ld16(xg + ((size_t)t * H + h) * K + part * 8) : zero;
+      }
+    }
+  };
+  auto store_blk = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < NCH; ++i) {
+      const int c = tid + i * 256;
+      if (c < kEncTok * CPT) {
+        const int tok = c / CPT, part = c - tok * CPT;
+        *reinterpret_cast<uint4*>(&s_x[buf][tok * XS + part * 8]) = rgs[i];
+      }
+    }
+  };
+
+  bf16_t* cout = static_cast<bf16_t*>(pick(a.c, axis));
+  load_blk(b0);
+  store_blk(0);
+  __syncthreads();
+  for (int blk = b0; blk < b1; ++blk) {
+    const int buf = (blk - b0) & 1;
+    if (blk + 1 < b1) load_blk(blk + 1);
+    for (int u = 0; u < ntt; ++u) {
+      const int tt = tt0 + u;
+      const bf16_t* xrow = &s_x[buf][(tt * 16 + li) * XS + 8 * lg];
+      f32x4 acc = f32x4{0.f};
+#pragma unroll
+      for (int s = 0; s < KS; ++s)
+        acc = mfma16(wf[s], as_bf16x8(*reinterpret_cast<const uint4*>(xrow + 32 * s)), acc);
+      const int t = blk * kEncTok + tt * 16 + li;
+      if (t < TT) {
+        const int b = t / a.M, pos = a.pos0 + (t - b * a.M);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int rr = rt * 16 + 4 * lg + e;
+          if (rr < r) cout[cache_index(b, h, H, a.n_max, r, pos, rr)] = f32_to_bf16(acc[e] - bmu[e]);
+        }
+      }
+    }
+    if (blk + 1 < b1) store_blk(buf ^ 1);
+    __syncthreads();
   }
 }
 
@@ -85,13 +256,13 @@ __global__ __launch_bounds__(256) void encode_f32_kernel(EncodeArgs a) {
   __shared__ float s_x[kT][kKC + 1];
   __shared__ float s_w[kT][kKC + 1];
   const int axis = blockIdx.z / a.H, h = blockIdx.z - axis * a.H;
-  const int r = a.r[axis], K = a.K, TT = a.B * a.M;
+  const int r = pick(a.r, axis), K = a.K, TT = a.B * a.M;
   if (blockIdx.y * kT >= r) return;
   const int tt = threadIdx.x / kT, rr = threadIdx.x % kT;
   const int tok = blockIdx.x * kT + tt, row = blockIdx.y * kT + rr;
-  const float* x = static_cast<const float*>(a.x[axis]);
-  const float* w = static_cast<const float*>(a.wdt[axis]) + (size_t)h * r * K;
-  const float* mu = a.mu[axis] ? static_cast<const float*>(a.mu[axis]) + (size_t)h * K : nullptr;
+  const float* x = static_cast<const float*>(pick(a.x, axis));
+  const float* w = static_cast<const float*>(pick(a.wdt, axis)) + (size_t)h * r * K;
+  const float* mu = pick(a.mu, axis) ? static_cast<const float*>(pick(a.mu, axis)) + (size_t)h * K : nullptr;
   float acc = 0.f;
   for (int k0 = 0; k0 < K; k0 += kKC) {
     for (int e = threadIdx.x; e < kT * kKC; e += 256) {
@@ -109,7 +280,7 @@ __global__ __launch_bounds__(256) void encode_f32_kernel(EncodeArgs a) {
   }
   if (tok < TT && row < r) {
     const int b = tok / a.M, pos = a.pos0 + (tok - b * a.M);
-    static_cast<float*>(a.c[axis])[cache_index(b, h, a.H, a.n_max, r, pos, row)] = acc;
+    static_cast<float*>(pick(a.c, axis))[cache_index(b, h, a.H, a.n_max, r, pos, row)] = acc;
   }
 }
 
@@ -119,10 +290,29 @@ hipError_t launch_encode(const EncodeArgs& a, hipStream_t stream) {
   const int TT = a.B * a.M;
   const int rmax = a.r[0] > a.r[1] ? a.r[0] : a.r[1];
   if (a.dtype == LLA_BF16) {
-    const int tiles = (rmax + 31) / 32, groups = (TT + 31) / 32;
-    const int wr = tiles >= 4 ? 4 : tiles >= 2 ? 2 : 1;
-    dim3 grid((groups + kEncWaves / wr - 1) / (kEncWaves / wr), (tiles + wr - 1) / wr, 2 * a.H);
-    hipLaunchKernelGGL(encode_bf16_kernel, grid, dim3(kEncWaves * kWave), 0, stream, a, wr);
+    // Many tokens: a workgroup streams all heads of its 32 tokens (one
+    // contiguous region of x).  Few tokens (a decode step's writes): one head
+    // and two row tiles per workgroup, so the weights spread over the machine.
+    const int blocks = (TT + kEncTok - 1) / kEncTok;
+    if (blocks >= 256 && rmax <= 64 && (a.K == 512 || a.K == 256)) {
+      // prefill-sized write: resident weights, streamed tokens; ~2 workgroups per CU
+      const int per_head = 2 * a.H;
+      int wgx = (2 * device_cu_count() + per_head - 1) / per_head;
+      if (wgx > blocks) wgx = blocks;
+      const int bpw = (blocks + wgx - 1) / wgx;
+      dim3 grid((blocks + bpw - 1) / bpw, a.H, 2);
+      if (a.K == 512)
+        hipLaunchKernelGGL((encode_stream_kernel<16>), grid, dim3(256), 0, stream, a, bpw);
+      else
+        hipLaunchKernelGGL((encode_stream_kernel<8>), grid, dim3(256), 0, stream, a, bpw);
+      return hipGetLastError();
+    }
+    const int heads_per_wg = blocks >= 256 ? a.H : 1;
+    const int rtmax = (rmax + 15) / 16;
+    const int rt_per_wg = blocks >= 256 ? (rtmax < 8 ? rtmax : 8) : 2;
+    const int nrc = (rtmax + rt_per_wg - 1) / rt_per_wg;
+    dim3 grid(blocks, (a.H + heads_per_wg - 1) / heads_per_wg, 2 * nrc);
+    hipLaunchKernelGGL(encode_bf16_kernel, grid, dim3(256), 0, stream, a, heads_per_wg, rt_per_wg, nrc);
   } else {
     dim3 grid((TT + kT - 1) / kT, (rmax + kT - 1) / kT, 2 * a.H);
     hipLaunchKernelGGL(encode_f32_kernel, grid, dim3(256), 0, stream, a);

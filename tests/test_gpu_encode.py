@@ -121,3 +121,17 @@ def test_encode_then_decode_chain_fp32():
         torch.cuda.synchronize()
         ref = oracle.decode_attn_batched(f64(q), c_k, c_v, f64(uk), f64(uv), f64(mk), f64(mv))
         assert_close(f64(out), ref, torch.float32, f"chain loop {loop}")
+
+
+@pytest.mark.parametrize("r_k,r_v,T,d,B,M,pos0", [
+    (18, 30, 4, 128, 3, 2900, 7),     # K = 512, 16-row tiles x 2, ragged last block
+    (33, 64, 4, 128, 2, 4100, 0),     # four 16-row tiles per wave
+    (5, 17, 2, 128, 1, 8200, 60),     # K = 256
+])
+def test_encode_many_tokens(r_k, r_v, T, d, B, M, pos0):
+    """Prefill-sized writes (>= 8192 tokens): the resident-weight streaming path."""
+    wl = W.Workload(f"enc_many_{T}_{d}", 1, 4, d, T, B, 0, ((r_k, r_v),), torch.bfloat16)
+    n_max = ((pos0 + M + 63) // 64) * 64 + 64
+    log(f"encode many tokens r=({r_k},{r_v}) K={T * d} B={B} M={M} pos0={pos0}")
+    inputs, ck, cv = _run(wl, r_k, r_v, B, M, pos0, n_max, True, torch.bfloat16)
+    _check(wl, inputs, ck, cv, pos0, M, torch.bfloat16, f"M={M}")
