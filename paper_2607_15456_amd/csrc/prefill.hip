@@ -52,6 +52,17 @@ constexpr bf16_t kOne = 0x3F80;        // 1.0 in bf16
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 
+// Raw buffer resource (gfx9 family word 3) over one contiguous region; loads
+// take a per-lane offset and a wave-uniform (scalar) offset.
+typedef __amdgpu_buffer_rsrc_t BufRsrc;
+__device__ __forceinline__ BufRsrc make_rsrc(const void* base, size_t bytes) {
+  const int n = bytes >= 0xffffffffull ? -1 : (int)bytes;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, n, 0x00020000);
+}
+__device__ __forceinline__ uint4 buf_ld16(BufRsrc r, int voff, int soff) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+
 __device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
@@ -93,14 +104,14 @@ __global__ __launch_bounds__(kPThreads) void prefill_bf16_kernel(PrefillArgs a) 
   constexpr int CVS = kPage + 4;      // feature-major V tile row stride (elements)
   constexpr int UKS = kMaxDPrefill + 8;
   constexpr int UVS = RVP + 4;
-  constexpr int CH = ((64 + 96) * 8 + kPThreads - 1) / kPThreads;  // max 16-byte chunks per thread per page
 
   __shared__ __attribute__((aligned(16))) bf16_t s_ukt[RKP * UKS];
   __shared__ __attribute__((aligned(16))) bf16_t s_uv[kMaxDPrefill * UVS];
   __shared__ __attribute__((aligned(16))) bf16_t s_ck[2][kPage * CKS];
   __shared__ __attribute__((aligned(16))) bf16_t s_cv[2][RVP * CVS];
 
-  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int col = lane & 31, g = lane >> 5;
   const int bh = blockIdx.x;
   const int h = bh % a.H;
@@ -127,10 +138,10 @@ __global__ __launch_bounds__(kPThreads) void prefill_bf16_kernel(PrefillArgs a) 
     const int i = e / RVP, j = e - i * RVP;
     s_uv[i * UVS + j] = (j < rv) ? uv[(size_t)i * rv + j] : bf16_t(0);
   }
-  for (int e = tid; e < 2 * kPage * (RKP - rk); e += kPThreads) {  // K features >= r_k
+  for (int e = tid; e < 2 * kPage * (RKP - rk); e += kPThreads) {  // K features >= r_k: 1, then 0
     const int buf = e / (kPage * (RKP - rk)), r = e - buf * kPage * (RKP - rk);
     const int n = r / (RKP - rk), j = rk + (r - n * (RKP - rk));
-    s_ck[buf][n * CKS + j] = 0;
+    s_ck[buf][n * CKS + j] = (j == rk) ? kOne : bf16_t(0);
   }
   for (int e = tid; e < 2 * kPage * (RVP - rv); e += kPThreads) {  // V rows >= r_v: ones, then zeros
     const int buf = e / (kPage * (RVP - rv)), r = e - buf * kPage * (RVP - rv);
@@ -138,46 +149,61 @@ __global__ __launch_bounds__(kPThreads) void prefill_bf16_kernel(PrefillArgs a) 
     s_cv[buf][j * CVS + n] = (j == rv) ? kOne : bf16_t(0);
   }
 
-  // ---- page staging: (rk + rv) feature rows x 8 chunks of 8 tokens ----
-  const size_t unit = (size_t)(bh / a.H) * a.H + h;
-  const bf16_t* ckb = static_cast<const bf16_t*>(a.ck) + unit * (size_t)a.n_max * rk;
-  const bf16_t* cvb = static_cast<const bf16_t*>(a.cv) + unit * (size_t)a.n_max * rv;
-  const int nchunks = (rk + rv) * 8;
-  uint4 stage[CH];
+  // ---- page staging ----
+  // A page of one axis is r feature rows of 128 contiguous bytes, so chunk ch
+  // (16 bytes, feature row ch/8, tokens 8(ch%8)..+7) sits at byte 16 ch of the
+  // page: buffer loads with the page offset in a scalar register and a fixed
+  // lane offset.  K chunks are transposed into the token-major tile on the way
+  // (8 two-byte LDS stores); V chunks are copied into the feature-major tile.
+  constexpr int CHK = (64 * 8 + kPThreads - 1) / kPThreads;  // r_k <= 64
+  constexpr int CHV = (95 * 8 + kPThreads - 1) / kPThreads;  // r_v <= 95
+  const size_t unit = (size_t)bh;
+  const BufRsrc ksrc = make_rsrc(static_cast<const bf16_t*>(a.ck) + unit * (size_t)a.n_max * rk,
+                                 (size_t)a.n_max * rk * 2);
+  const BufRsrc vsrc = make_rsrc(static_cast<const bf16_t*>(a.cv) + unit * (size_t)a.n_max * rv,
+                                 (size_t)a.n_max * rv * 2);
+  const int kpage_b = kPage * rk * 2, vpage_b = kPage * rv * 2;
+  const int nkch = rk * 8, nvch = rv * 8;
+  uint4 stk[CHK], stv[CHV];
   auto load_page = [&](int pg) {
 #pragma unroll
-    for (int c = 0; c < CH; ++c) {
+    for (int c = 0; c < CHK; ++c) {
       const int ch = tid + c * kPThreads;
-      if (ch < nchunks) {
-        const int row = ch >> 3, n8 = (ch & 7) * 8;
-        stage[c] = row < rk ? ld16(ckb + ((size_t)pg * kPage * rk + row * kPage + n8))
-                            : ld16(cvb + ((size_t)pg * kPage * rv + (row - rk) * kPage + n8));
-      }
+      if (ch < nkch) stk[c] = buf_ld16(ksrc, ch * 16, pg * kpage_b);
+    }
+#pragma unroll
+    for (int c = 0; c < CHV; ++c) {
+      const int ch = tid + c * kPThreads;
+      if (ch < nvch) stv[c] = buf_ld16(vsrc, ch * 16, pg * vpage_b);
     }
   };
   auto store_page = [&](int pg, int buf) {
 #pragma unroll
-    for (int c = 0; c < CH; ++c) {
+    for (int c = 0; c < CHK; ++c) {
       const int ch = tid + c * kPThreads;
-      if (ch < nchunks) {
-        const int row = ch >> 3, n8 = (ch & 7) * 8;
-        const bf16_t* v = reinterpret_cast<const bf16_t*>(&stage[c]);
-        if (row < rk) {
+      if (ch < nkch) {
+        const bf16_t* v = reinterpret_cast<const bf16_t*>(&stk[c]);
+        bf16_t* dst = &s_ck[buf][(ch & 7) * 8 * CKS + (ch >> 3)];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) s_ck[buf][(n8 + e) * CKS + row] = v[e];
-        } else {
-          uint4 w = stage[c];
-          const int n0 = pg * kPage + n8;
-          if (n0 + 8 > kmax) {  // tokens past the last key: zero (the slot may hold anything)
-            bf16_t* wv = reinterpret_cast<bf16_t*>(&w);
+        for (int e = 0; e < 8; ++e) dst[e * CKS] = v[e];
+      }
+    }
+    const bool last = (pg + 1) * kPage > kmax;  // tokens past the last key are zeroed
 #pragma unroll
-            for (int e = 0; e < 8; ++e)
-              if (n0 + e >= kmax) wv[e] = 0;
-          }
-          bf16_t* dst = &s_cv[buf][(row - rk) * CVS + n8];
-          *reinterpret_cast<uint2*>(dst) = make_uint2(w.x, w.y);
-          *reinterpret_cast<uint2*>(dst + 4) = make_uint2(w.z, w.w);
+    for (int c = 0; c < CHV; ++c) {
+      const int ch = tid + c * kPThreads;
+      if (ch < nvch) {
+        uint4 w = stv[c];
+        if (last) {
+          const int n0 = pg * kPage + (ch & 7) * 8;
+          bf16_t* wv = reinterpret_cast<bf16_t*>(&w);
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (n0 + e >= kmax) wv[e] = 0;
         }
+        bf16_t* dst = &s_cv[buf][(ch >> 3) * CVS + (ch & 7) * 8];
+        *reinterpret_cast<uint2*>(dst) = make_uint2(w.x, w.y);
+        *reinterpret_cast<uint2*>(dst + 4) = make_uint2(w.z, w.w);
       }
     }
   };
@@ -212,6 +238,26 @@ __global__ __launch_bounds__(kPThreads) void prefill_bf16_kernel(PrefillArgs a) 
 #pragma unroll
   for (int t = 0; t < ZT; ++t) zacc[t] = f32x16{0.f};
   float m_run = 0.f;
+  f32x16 negm = f32x16{0.f};  // -m_run in every register: the score product's C operand
+  // When r_k leaves a padding feature, -m_run rides in the score product
+  // itself: K feature r_k is 1 for every key and the same feature of Q~ holds
+  // -m_run (as hi + lo bf16), so the product yields S - m_run with a zero C
+  // operand and no per-page register copies.
+  const bool fold = rk < RKP;
+  const int fks = rk / 16, frem = rk % 16;
+  const int fg = (frem % 8) / 4, fe = 4 * (frem / 8) + frem % 4;
+  auto set_fold = [&](float negmv) {
+    const __bf16 hi = (__bf16)negmv;
+    const __bf16 lo = (__bf16)(negmv - (float)hi);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (ks == fks && e == fe && g == fg) {
+          qop[ks][e] = hi;
+          qlo[ks][e] = lo;
+        }
+  };
   const int qpos = p0 + myq;  // absolute position of this lane's query
 
   for (int p = 0; p < npages; ++p) {
@@ -221,17 +267,30 @@ __global__ __launch_bounds__(kPThreads) void prefill_bf16_kernel(PrefillArgs a) 
     if (wave_live && key0 <= p0 + qlast_w) {
       const bool first = (p == 0);
       const bool diag = key0 + kPage - 1 > p0 + qw0;
-      const f32x16 cinit = first ? f32x16{0.f} : f32x16{0.f} - m_run;
       f32x16 sc[2];
+      if (fold) {
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-        sc[kt] = cinit;
-        const bf16_t* krow = &s_ck[buf][(32 * kt + col) * CKS];
+        for (int kt = 0; kt < 2; ++kt) {
+          sc[kt] = f32x16{0.f};
+          const bf16_t* krow = &s_ck[buf][(32 * kt + col) * CKS];
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          const bf16x8 ak = lds_pair(krow, 16 * ks, g);
-          sc[kt] = mfma(ak, qop[ks], sc[kt]);
-          sc[kt] = mfma(ak, qlo[ks], sc[kt]);
+          for (int ks = 0; ks < KS; ++ks) {
+            const bf16x8 ak = lds_pair(krow, 16 * ks, g);
+            sc[kt] = mfma(ak, qop[ks], sc[kt]);
+            sc[kt] = mfma(ak, qlo[ks], sc[kt]);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) {
+          sc[kt] = negm;
+          const bf16_t* krow = &s_ck[buf][(32 * kt + col) * CKS];
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) {
+            const bf16x8 ak = lds_pair(krow, 16 * ks, g);
+            sc[kt] = mfma(ak, qop[ks], sc[kt]);
+            sc[kt] = mfma(ak, qlo[ks], sc[kt]);
+          }
         }
       }
       if (diag) {
@@ -247,16 +306,20 @@ __global__ __launch_bounds__(kPThreads) void prefill_bf16_kernel(PrefillArgs a) 
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[kt][r]);
+        for (int r = 0; r < 16; r += 2) mx = fmaxf(mx, fmaxf(sc[kt][r], sc[kt][r + 1]));
       mx = fmaxf(mx, xor_shfl(mx, 32));
       if (first) {
         m_run = mx;
+        negm = f32x16{0.f} - m_run;
+        if (fold) set_fold(-m_run);
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt) sc[kt] -= mx;
       } else if (__builtin_amdgcn_ballot_w64(mx > kLazy) != 0) {
         const float dl = mx > kLazy ? mx : 0.f;
         const float alpha = __builtin_amdgcn_exp2f(-dl);
         m_run += dl;
+        negm = f32x16{0.f} - m_run;
+        if (fold) set_fold(-m_run);
 #pragma unroll
         for (int t = 0; t < ZT; ++t) zacc[t] *= alpha;
 #pragma unroll
