@@ -34,10 +34,22 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2516.6  # 256 CU x 2.4 GHz x 4096 flop/clk, dense
 
-# FETCH_SIZE / WRITE_SIZE of the dominant kernel, per launch, from the rocprofv3
-# --pmc runs recorded under profiles/ (scaled by the copy-kernel calibration).
-# None until taken for the current kernel.
-MEASURED_TRAFFIC = {}
+# HBM bytes per launch of the dominant kernel: rocprofv3 --pmc FETCH_SIZE and
+# WRITE_SIZE (KiB per dispatch) scaled by what the same counters read for a
+# plain elementwise kernel of known size (FETCH_SIZE x 2.000, WRITE_SIZE x 1.000;
+# the runs are recorded under profiles/).  Keyed by (workload, r_k, r_v); an
+# entry is dropped when the kernel changes.
+FETCH_SCALE, WRITE_SCALE = 2.000, 1.000
+MEASURED_TRAFFIC = {
+    ("ouro14b_decode", 192, 320): {"fetch_kib": 1057142.75, "write_kib": 256.0},
+}
+
+
+def traffic_bytes(key):
+    t = MEASURED_TRAFFIC.get(key)
+    if t is None:
+        return None
+    return round(t["fetch_kib"] * 1024 * FETCH_SCALE + t["write_kib"] * 1024 * WRITE_SCALE)
 
 
 def parse():
@@ -50,7 +62,7 @@ def parse():
     p.add_argument("--tier", type=int, default=None, help="rank_sweep: run only this tier index")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--copy-probe", action="store_true",
-                   help="run a plain 1 GiB device copy (counter calibration for rocprofv3 --pmc)")
+                   help="run a plain 1 GiB read + 1 GiB write elementwise kernel (counter calibration for rocprofv3 --pmc)")
     return p.parse_args()
 
 
@@ -304,12 +316,13 @@ def main():
         sys.exit(1)
     lla.lib()
     if args.copy_probe:
-        src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        # one elementwise kernel per launch: reads 1 GiB, writes 1 GiB
+        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
         for _ in range(5):
-            dst.copy_(src)
+            torch.neg(src, out=dst)
         torch.cuda.synchronize()
-        print(json.dumps({"copy_probe_bytes": 1 << 30, "launches": 5}))
+        print(json.dumps({"copy_probe_read_bytes": 1 << 30, "copy_probe_write_bytes": 1 << 30, "launches": 5}))
         return
 
     if args.workload == "prefill_write":
@@ -321,7 +334,7 @@ def main():
     B, N, d = wl.B, wl.N, wl.d
     value = B / (head["step_ms"] * 1e-3)
     achieved = head["decode_gbs"]
-    traffic = MEASURED_TRAFFIC.get((wl.name, head["r_k"], head["r_v"]))
+    traffic = traffic_bytes((wl.name, head["r_k"], head["r_v"]))
     line = {
         "metric": "latent-cache decode attention tokens/sec and achieved HBM GB/s (% of peak)",
         "value": round(value, 2),
@@ -348,6 +361,7 @@ def main():
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
+            "traffic_unit": "HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, calibrated)",
             "kernel": "decode_kernel (lla_decode_attn)",
             "bytes_per_launch": head["decode_bytes"],
             "avg_launch_ms": round(head["decode_ms"], 5),

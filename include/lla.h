@@ -191,7 +191,7 @@ lla_status lla_decode_attn(int dtype, int out_dtype, int B, int H, int d_head, i
  * With dtype LLA_BF16 the contractions run on bf16 MFMA: the absorbed query,
  * the softmax weights and the normalised latent are rounded to bf16 before
  * their products (fp32 accumulation throughout).
- * Errors: LLA_ERR_INVALID_ARG; LLA_ERR_UNSUPPORTED for bf16 with r_k > 64,
+ * Errors: LLA_ERR_INVALID_ARG; LLA_ERR_UNSUPPORTED for bf16 with r_k > 95,
  * r_v > 95, d_head > 128 or M > 8388480; LLA_ERR_HIP.
  */
 lla_status lla_prefill_attn(int dtype, int out_dtype, int B, int H, int M, int d_head, int r_k,

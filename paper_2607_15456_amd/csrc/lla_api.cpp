@@ -265,7 +265,7 @@ lla_status lla_prefill_attn(int dtype, int out_dtype, int B, int H, int M, int d
   (void)mu_k;  // q . mu_k is constant over the keys of a query: it cancels in the softmax
   const float qscale = (float)((double)scale * kLog2e);
   if (dtype == LLA_BF16) {
-    if (r_k > 64 || r_v > 95 || d_head > 128 || (M + 127) / 128 > 65535) return LLA_ERR_UNSUPPORTED;
+    if (r_k > 95 || r_v > 95 || d_head > 128 || (M + 127) / 128 > 65535) return LLA_ERR_UNSUPPORTED;
     lla::PrefillArgs a{};
     a.out_dtype = out_dtype;
     a.B = B;

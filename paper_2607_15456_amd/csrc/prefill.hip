@@ -26,9 +26,12 @@
 // Q~ enters the score product as two bf16 terms (hi + lo), so the scores carry
 // about 16 significant bits rather than bf16's 8: with peaked rows the score
 // magnitudes would otherwise turn Q~'s rounding into visible weight errors.
-// The running max enters the score product as its C operand (S - m), and is
-// only raised when a page exceeds it by more than 2^8 (lazy rescale), so most
-// pages cost one max, one exp2 and one conversion per score.
+// The running max enters the score product through a padding feature (S - m
+// comes out of the MFMAs), and is only raised when a page exceeds it by more
+// than 2^8 (lazy rescale), so most pages cost
+// half a max3, one exp2 and half a packed conversion per score.  This file is
+// compiled without NaN semantics: scores are either finite or -inf (masked),
+// so max needs no NaN canonicalisation.
 // K/V pages are staged cooperatively into double-buffered LDS tiles (the K
 // page transposed to token-major on the way); the next page's global loads
 // are in flight while the current page is computed.
@@ -94,8 +97,24 @@ __device__ __forceinline__ void to_operand_split(const f32x16& acc, int h, float
   }
 }
 
+// Waves per SIMD the register budget is sized for: the smallest tiles fit
+// four (<= 128 VGPRs), the others two.
+constexpr int prefill_occupancy(int rkp, int rvp) { return rkp + rvp <= 64 ? 4 : 2; }
+
+// max over both halves of the wavefront (lane i and lane i ^ 32)
+__device__ __forceinline__ float half_swap_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+template <int N>
+struct IntC {
+  static constexpr int value = N;
+};
+
 template <int RKP, int RVP>
-__global__ __launch_bounds__(kPThreads) void prefill_bf16_kernel(PrefillArgs a) {
+__global__ __launch_bounds__(kPThreads) __attribute__((amdgpu_waves_per_eu(prefill_occupancy(RKP, RVP))))
+void prefill_bf16_kernel(PrefillArgs a) {
   constexpr int KS = RKP / 16;        // K-steps of the score product (over features)
   constexpr int QT = RKP / 32;        // accumulator tiles of Q~^T
   constexpr int ZT = RVP / 32;        // accumulator tiles of Z^T
@@ -104,11 +123,12 @@ __global__ __launch_bounds__(kPThreads) void prefill_bf16_kernel(PrefillArgs a) 
   constexpr int CVS = kPage + 4;      // feature-major V tile row stride (elements)
   constexpr int UKS = kMaxDPrefill + 8;
   constexpr int UVS = RVP + 4;
+  constexpr int KTILE = kPage * CKS, VTILE = RVP * CVS;
 
   __shared__ __attribute__((aligned(16))) bf16_t s_ukt[RKP * UKS];
   __shared__ __attribute__((aligned(16))) bf16_t s_uv[kMaxDPrefill * UVS];
-  __shared__ __attribute__((aligned(16))) bf16_t s_ck[2][kPage * CKS];
-  __shared__ __attribute__((aligned(16))) bf16_t s_cv[2][RVP * CVS];
+  __shared__ __attribute__((aligned(16))) bf16_t s_ck[2 * KTILE];
+  __shared__ __attribute__((aligned(16))) bf16_t s_cv[2 * VTILE];
 
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
@@ -128,6 +148,9 @@ __global__ __launch_bounds__(kPThreads) void prefill_bf16_kernel(PrefillArgs a) 
   const int npages = (kmax + kPage - 1) / kPage;
 
   // ---- constant LDS: U_k^T and U_v (zero padded), padding of the page tiles ----
+  // K feature RKP - 1 is 1 for every key (it carries the running max, below);
+  // K features r_k .. RKP - 2 are 0.  V row r_v is all ones (the denominator),
+  // V rows past it are 0.
   const bf16_t* uk = static_cast<const bf16_t*>(a.uk) + (size_t)h * d * rk;  // [d][rk]
   for (int e = tid; e < d * RKP; e += kPThreads) {
     const int i = e / RKP, j = e - i * RKP;
@@ -138,15 +161,15 @@ __global__ __launch_bounds__(kPThreads) void prefill_bf16_kernel(PrefillArgs a) 
     const int i = e / RVP, j = e - i * RVP;
     s_uv[i * UVS + j] = (j < rv) ? uv[(size_t)i * rv + j] : bf16_t(0);
   }
-  for (int e = tid; e < 2 * kPage * (RKP - rk); e += kPThreads) {  // K features >= r_k: 1, then 0
+  for (int e = tid; e < 2 * kPage * (RKP - rk); e += kPThreads) {
     const int buf = e / (kPage * (RKP - rk)), r = e - buf * kPage * (RKP - rk);
     const int n = r / (RKP - rk), j = rk + (r - n * (RKP - rk));
-    s_ck[buf][n * CKS + j] = (j == rk) ? kOne : bf16_t(0);
+    s_ck[buf * KTILE + n * CKS + j] = (j == RKP - 1) ? kOne : bf16_t(0);
   }
-  for (int e = tid; e < 2 * kPage * (RVP - rv); e += kPThreads) {  // V rows >= r_v: ones, then zeros
+  for (int e = tid; e < 2 * kPage * (RVP - rv); e += kPThreads) {
     const int buf = e / (kPage * (RVP - rv)), r = e - buf * kPage * (RVP - rv);
     const int j = rv + r / kPage, n = r % kPage;
-    s_cv[buf][j * CVS + n] = (j == rv) ? kOne : bf16_t(0);
+    s_cv[buf * VTILE + j * CVS + n] = (j == rv) ? kOne : bf16_t(0);
   }
 
   // ---- page staging ----
@@ -155,8 +178,8 @@ __global__ __launch_bounds__(kPThreads) void prefill_bf16_kernel(PrefillArgs a) 
   // page: buffer loads with the page offset in a scalar register and a fixed
   // lane offset.  K chunks are transposed into the token-major tile on the way
   // (8 two-byte LDS stores); V chunks are copied into the feature-major tile.
-  constexpr int CHK = (64 * 8 + kPThreads - 1) / kPThreads;  // r_k <= 64
-  constexpr int CHV = (95 * 8 + kPThreads - 1) / kPThreads;  // r_v <= 95
+  constexpr int CHK = ((RKP - 1) * 8 + kPThreads - 1) / kPThreads;  // r_k <= RKP - 1
+  constexpr int CHV = ((RVP - 1) * 8 + kPThreads - 1) / kPThreads;  // r_v <= RVP - 1
   const size_t unit = (size_t)bh;
   const BufRsrc ksrc = make_rsrc(static_cast<const bf16_t*>(a.ck) + unit * (size_t)a.n_max * rk,
                                  (size_t)a.n_max * rk * 2);
@@ -164,6 +187,17 @@ __global__ __launch_bounds__(kPThreads) void prefill_bf16_kernel(PrefillArgs a) 
                                  (size_t)a.n_max * rv * 2);
   const int kpage_b = kPage * rk * 2, vpage_b = kPage * rv * 2;
   const int nkch = rk * 8, nvch = rv * 8;
+  int kdst[CHK], vdst[CHV];  // LDS element offsets of this thread's chunks inside a tile
+#pragma unroll
+  for (int c = 0; c < CHK; ++c) {
+    const int ch = tid + c * kPThreads;
+    kdst[c] = (ch & 7) * 8 * CKS + (ch >> 3);
+  }
+#pragma unroll
+  for (int c = 0; c < CHV; ++c) {
+    const int ch = tid + c * kPThreads;
+    vdst[c] = (ch >> 3) * CVS + (ch & 7) * 8;
+  }
   uint4 stk[CHK], stv[CHV];
   auto load_page = [&](int pg) {
 #pragma unroll
@@ -177,13 +211,13 @@ __global__ __launch_bounds__(kPThreads) void prefill_bf16_kernel(PrefillArgs a) 
       if (ch < nvch) stv[c] = buf_ld16(vsrc, ch * 16, pg * vpage_b);
     }
   };
-  auto store_page = [&](int pg, int buf) {
+  auto store_page = [&](int pg, bf16_t* tk, bf16_t* tv) {
 #pragma unroll
     for (int c = 0; c < CHK; ++c) {
       const int ch = tid + c * kPThreads;
       if (ch < nkch) {
         const bf16_t* v = reinterpret_cast<const bf16_t*>(&stk[c]);
-        bf16_t* dst = &s_ck[buf][(ch & 7) * 8 * CKS + (ch >> 3)];
+        bf16_t* dst = tk + kdst[c];
 #pragma unroll
         for (int e = 0; e < 8; ++e) dst[e * CKS] = v[e];
       }
@@ -195,13 +229,17 @@ __global__ __launch_bounds__(kPThreads) void prefill_bf16_kernel(PrefillArgs a) 
       if (ch < nvch) {
         uint4 w = stv[c];
         if (last) {
-          const int n0 = pg * kPage + (ch & 7) * 8;
-          bf16_t* wv = reinterpret_cast<bf16_t*>(&w);
-#pragma unroll
-          for (int e = 0; e < 8; ++e)
-            if (n0 + e >= kmax) wv[e] = 0;
+          // keep tokens n0 + e < kmax: dword i holds tokens 2i (low half) and 2i + 1
+          const int nv = kmax - (pg * kPage + (ch & 7) * 8);
+          auto keep = [nv](int i) {
+            return nv > 2 * i + 1 ? 0xffffffffu : nv > 2 * i ? 0x0000ffffu : 0u;
+          };
+          w.x &= keep(0);
+          w.y &= keep(1);
+          w.z &= keep(2);
+          w.w &= keep(3);
         }
-        bf16_t* dst = &s_cv[buf][(ch >> 3) * CVS + (ch & 7) * 8];
+        bf16_t* dst = tv + vdst[c];
         *reinterpret_cast<uint2*>(dst) = make_uint2(w.x, w.y);
         *reinterpret_cast<uint2*>(dst + 4) = make_uint2(w.z, w.w);
       }
@@ -210,7 +248,7 @@ __global__ __launch_bounds__(kPThreads) void prefill_bf16_kernel(PrefillArgs a) 
 
   load_page(0);
   __syncthreads();  // constant LDS written
-  store_page(0, 0);
+  store_page(0, s_ck, s_cv);
 
   // ---- D1 = Q~^T for this wave's 32 queries ----
   bf16x8 qop[KS], qlo[KS];  // Q~ as hi + lo bf16 terms: scores keep ~fp32 accuracy
@@ -234,96 +272,77 @@ __global__ __launch_bounds__(kPThreads) void prefill_bf16_kernel(PrefillArgs a) 
   __syncthreads();  // page 0 staged
 
   // ---- online softmax over the key pages ----
+  // The running max rides in the score product itself: K feature RKP - 1 is 1
+  // for every key and the same feature of Q~ (K-step KS - 1, element 7 of the
+  // upper lane half) holds negm = -m as hi + lo bf16, so the MFMAs yield
+  // S - m directly.  negm is the exact value the product uses (hi + lo).
   f32x16 zacc[ZT];
 #pragma unroll
   for (int t = 0; t < ZT; ++t) zacc[t] = f32x16{0.f};
-  float m_run = 0.f;
-  f32x16 negm = f32x16{0.f};  // -m_run in every register: the score product's C operand
-  // When r_k leaves a padding feature, -m_run rides in the score product
-  // itself: K feature r_k is 1 for every key and the same feature of Q~ holds
-  // -m_run (as hi + lo bf16), so the product yields S - m_run with a zero C
-  // operand and no per-page register copies.
-  const bool fold = rk < RKP;
-  const int fks = rk / 16, frem = rk % 16;
-  const int fg = (frem % 8) / 4, fe = 4 * (frem / 8) + frem % 4;
-  auto set_fold = [&](float negmv) {
-    const __bf16 hi = (__bf16)negmv;
-    const __bf16 lo = (__bf16)(negmv - (float)hi);
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-        if (ks == fks && e == fe && g == fg) {
-          qop[ks][e] = hi;
-          qlo[ks][e] = lo;
-        }
-  };
+  float negm = 0.f;
   const int qpos = p0 + myq;  // absolute position of this lane's query
 
-  for (int p = 0; p < npages; ++p) {
-    const int buf = p & 1;
+  auto page = [&](int p, auto bufc) {
+    constexpr int buf = decltype(bufc)::value;
     if (p + 1 < npages) load_page(p + 1);
     const int key0 = p * kPage;
     if (wave_live && key0 <= p0 + qlast_w) {
-      const bool first = (p == 0);
       const bool diag = key0 + kPage - 1 > p0 + qw0;
-      f32x16 sc[2];
-      if (fold) {
+      const bf16_t* ktile = s_ck + buf * KTILE + col * CKS;
+      // the two key tiles' MFMA chains are interleaved
+      f32x16 sc[2] = {f32x16{0.f}, f32x16{0.f}};
 #pragma unroll
-        for (int kt = 0; kt < 2; ++kt) {
-          sc[kt] = f32x16{0.f};
-          const bf16_t* krow = &s_ck[buf][(32 * kt + col) * CKS];
-#pragma unroll
-          for (int ks = 0; ks < KS; ++ks) {
-            const bf16x8 ak = lds_pair(krow, 16 * ks, g);
-            sc[kt] = mfma(ak, qop[ks], sc[kt]);
-            sc[kt] = mfma(ak, qlo[ks], sc[kt]);
-          }
-        }
-      } else {
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt) {
-          sc[kt] = negm;
-          const bf16_t* krow = &s_ck[buf][(32 * kt + col) * CKS];
-#pragma unroll
-          for (int ks = 0; ks < KS; ++ks) {
-            const bf16x8 ak = lds_pair(krow, 16 * ks, g);
-            sc[kt] = mfma(ak, qop[ks], sc[kt]);
-            sc[kt] = mfma(ak, qlo[ks], sc[kt]);
-          }
-        }
+      for (int ks = 0; ks < KS; ++ks) {
+        const bf16x8 ak0 = lds_pair(ktile, 16 * ks, g);
+        const bf16x8 ak1 = lds_pair(ktile + 32 * CKS, 16 * ks, g);
+        sc[0] = mfma(ak0, qop[ks], sc[0]);
+        sc[1] = mfma(ak1, qop[ks], sc[1]);
+        sc[0] = mfma(ak0, qlo[ks], sc[0]);
+        sc[1] = mfma(ak1, qlo[ks], sc[1]);
       }
-      if (diag) {
+      if (__builtin_expect(diag, 0)) {
+        // key 32kt + 8(r/4) + 4g + r%4 of the page is visible iff 32kt + 8(r/4) + r%4 <= lim
+        const int lim = qpos - key0 - 4 * g;
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int n = key0 + 32 * kt + 8 * (r / 4) + 4 * g + (r % 4);
-            if (n > qpos) sc[kt][r] = neg_inf();
-          }
+          for (int r = 0; r < 16; ++r)
+            if (32 * kt + 8 * (r / 4) + (r % 4) > lim) sc[kt][r] = neg_inf();
       }
-      float mx = neg_inf();
+      // row max: four independent max3 chains of eight scores, then combined
+      float part[4];
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
+      for (int c = 0; c < 4; ++c) {
+        const f32x16& v = sc[c / 2];
+        const int o = 8 * (c % 2);
+        float m = fmaxf(fmaxf(v[o], v[o + 1]), v[o + 2]);
+        m = fmaxf(fmaxf(m, v[o + 3]), v[o + 4]);
+        m = fmaxf(fmaxf(m, v[o + 5]), v[o + 6]);
+        part[c] = fmaxf(m, v[o + 7]);
+      }
+      float mx = fmaxf(fmaxf(fmaxf(part[0], part[1]), part[2]), part[3]);
+      mx = half_swap_max(mx);
+      // Raise the running max on the first page, and later only when a score
+      // exceeds it by more than 2^kLazy.
+      const bool first = (p == 0);
+      const bool raise = first || mx > kLazy;
+      if (__builtin_expect(__builtin_amdgcn_ballot_w64(raise) != 0, 0)) {
+        // new fold value -(m + mx) as hi + lo; lanes that do not raise keep theirs
+        const float target = negm - mx;
+        const __bf16 hi = (__bf16)target;
+        const __bf16 lo = (__bf16)(target - (float)hi);
+        const float delta = raise ? ((float)hi + (float)lo) - negm : 0.f;
+        if (!first) {
+          const float alpha = __builtin_amdgcn_exp2f(delta);
 #pragma unroll
-        for (int r = 0; r < 16; r += 2) mx = fmaxf(mx, fmaxf(sc[kt][r], sc[kt][r + 1]));
-      mx = fmaxf(mx, xor_shfl(mx, 32));
-      if (first) {
-        m_run = mx;
-        negm = f32x16{0.f} - m_run;
-        if (fold) set_fold(-m_run);
+          for (int t = 0; t < ZT; ++t) zacc[t] *= alpha;
+        }
 #pragma unroll
-        for (int kt = 0; kt < 2; ++kt) sc[kt] -= mx;
-      } else if (__builtin_amdgcn_ballot_w64(mx > kLazy) != 0) {
-        const float dl = mx > kLazy ? mx : 0.f;
-        const float alpha = __builtin_amdgcn_exp2f(-dl);
-        m_run += dl;
-        negm = f32x16{0.f} - m_run;
-        if (fold) set_fold(-m_run);
-#pragma unroll
-        for (int t = 0; t < ZT; ++t) zacc[t] *= alpha;
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt) sc[kt] -= dl;
+        for (int kt = 0; kt < 2; ++kt) sc[kt] += delta;
+        negm += delta;
+        const bool put = raise && g == 1;
+        qop[KS - 1][7] = put ? hi : qop[KS - 1][7];
+        qlo[KS - 1][7] = put ? lo : qlo[KS - 1][7];
       }
       // P as the value product's B operands: K-step u = registers 8(u%2).. of tile u/2
       bf16x8 pop[4];
@@ -332,15 +351,19 @@ __global__ __launch_bounds__(kPThreads) void prefill_bf16_kernel(PrefillArgs a) 
 #pragma unroll
         for (int e = 0; e < 8; ++e) pop[u][e] = (__bf16)__builtin_amdgcn_exp2f(sc[u / 2][8 * (u % 2) + e]);
       }
+      const bf16_t* vtile = s_cv + buf * VTILE + col * CVS;
 #pragma unroll
       for (int t = 0; t < ZT; ++t) {
-        const bf16_t* vrow = &s_cv[buf][(32 * t + col) * CVS];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) zacc[t] = mfma(lds_pair(vrow, 16 * u, g), pop[u], zacc[t]);
+        for (int u = 0; u < 4; ++u) zacc[t] = mfma(lds_pair(vtile + 32 * t * CVS, 16 * u, g), pop[u], zacc[t]);
       }
     }
-    if (p + 1 < npages) store_page(p + 1, buf ^ 1);
+    if (p + 1 < npages) store_page(p + 1, s_ck + (buf ^ 1) * KTILE, s_cv + (buf ^ 1) * VTILE);
     __syncthreads();
+  };
+  for (int p = 0; p < npages; p += 2) {
+    page(p, IntC<0>{});
+    if (p + 1 < npages) page(p + 1, IntC<1>{});
   }
 
   // ---- epilogue: l from the ones row, O^T = U_v (Z / l)^T + mu_v ----
@@ -397,15 +420,21 @@ hipError_t launch_t(const PrefillArgs& a, hipStream_t stream) {
 }  // namespace
 
 hipError_t launch_prefill_bf16(const PrefillArgs& a, hipStream_t stream) {
-  // K features padded to 32 / 64; V features padded past r_v (room for the ones row)
-  const int rkp = a.rk <= 32 ? 32 : 64;
+  // K features padded past r_k (room for the running-max feature RKP - 1);
+  // V features padded past r_v (room for the ones row)
+  const int rkp = a.rk < 32 ? 32 : a.rk < 64 ? 64 : 96;
   const int rvp = a.rv < 32 ? 32 : a.rv < 64 ? 64 : 96;
-  if (rkp == 32 && rvp == 32) return launch_t<32, 32>(a, stream);
-  if (rkp == 32 && rvp == 64) return launch_t<32, 64>(a, stream);
-  if (rkp == 32 && rvp == 96) return launch_t<32, 96>(a, stream);
-  if (rkp == 64 && rvp == 32) return launch_t<64, 32>(a, stream);
-  if (rkp == 64 && rvp == 64) return launch_t<64, 64>(a, stream);
-  return launch_t<64, 96>(a, stream);
+  switch (rkp * 1000 + rvp) {
+    case 32032: return launch_t<32, 32>(a, stream);
+    case 32064: return launch_t<32, 64>(a, stream);
+    case 32096: return launch_t<32, 96>(a, stream);
+    case 64032: return launch_t<64, 32>(a, stream);
+    case 64064: return launch_t<64, 64>(a, stream);
+    case 64096: return launch_t<64, 96>(a, stream);
+    case 96032: return launch_t<96, 32>(a, stream);
+    case 96064: return launch_t<96, 64>(a, stream);
+    default: return launch_t<96, 96>(a, stream);
+  }
 }
 
 }  // namespace lla

@@ -158,7 +158,7 @@ def _prefill(**kw):
 
 @pytest.mark.parametrize("kw,code", [
     (dict(M=0), 1), (dict(p0=-1), 1), (dict(p0=449), 1), (dict(d=40), 1), (dict(q=MIS), 1),
-    (dict(scale=-1.0), 1), (dict(rk=65), 2), (dict(rv=96), 2), (dict(d=256), 2),
+    (dict(scale=-1.0), 1), (dict(rk=96), 2), (dict(rv=96), 2), (dict(d=256), 2),
 ])
 def test_prefill_rejects(kw, code):
     assert _prefill(**kw) == code

@@ -46,7 +46,8 @@ def _oracle(q, ck, cv, uk, uv, muk, muv, p0, rows=None, units=None, scale=None):
                                        rows=rows, units=units)
 
 
-@pytest.mark.parametrize("r_k,r_v", [(18, 30), (36, 60), (7, 9), (64, 95), (32, 31), (33, 64), (1, 1)])
+@pytest.mark.parametrize("r_k,r_v", [(18, 30), (36, 60), (7, 9), (64, 95), (32, 31), (33, 64), (1, 1),
+                                     (95, 95), (80, 40), (31, 95), (63, 20)])
 @pytest.mark.parametrize("M,p0", [(1, 0), (33, 0), (128, 0), (200, 5), (77, 100), (130, 64)])
 def test_bf16_prefill(r_k, r_v, M, p0):
     log(f"prefill bf16 r=({r_k},{r_v}) M={M} p0={p0}")
