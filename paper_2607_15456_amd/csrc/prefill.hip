@@ -33,8 +33,8 @@
 // compiled without NaN semantics: scores are either finite or -inf (masked),
 // so max needs no NaN canonicalisation.
 // K/V pages are staged cooperatively into double-buffered LDS tiles (the K
-// page transposed to token-major on the way); the next page's global loads
-// are in flight while the current page is computed.
+// page transposed to token-major on the way); the global loads of the two
+// following pages are in flight while the current page is computed.
 
 #include "lla_device.h"
 #include "lla_internal.h"
@@ -64,6 +64,9 @@ __device__ __forceinline__ BufRsrc make_rsrc(const void* base, size_t bytes) {
 }
 __device__ __forceinline__ uint4 buf_ld16(BufRsrc r, int voff, int soff) {
   return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+__device__ __forceinline__ uint16_t buf_ld2(BufRsrc r, int voff, int soff) {
+  return __builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0);
 }
 
 __device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
@@ -151,25 +154,65 @@ void prefill_bf16_kernel(PrefillArgs a) {
   // K feature RKP - 1 is 1 for every key (it carries the running max, below);
   // K features r_k .. RKP - 2 are 0.  V row r_v is all ones (the denominator),
   // V rows past it are 0.
-  const bf16_t* uk = static_cast<const bf16_t*>(a.uk) + (size_t)h * d * rk;  // [d][rk]
-  for (int e = tid; e < d * RKP; e += kPThreads) {
-    const int i = e / RKP, j = e - i * RKP;
-    s_ukt[j * UKS + i] = (j < rk) ? uk[(size_t)i * rk + j] : bf16_t(0);
+  // Thread (tj, ti) = (tid % 32, tid / 32) fills feature columns j = tj + 32 jj
+  // and rows i = ti + 8k of U_k^T (transposed) and U_v; features past r are
+  // zero.  The LDS offsets are compile-time apart, the global reads are buffer
+  // loads with the row offset in a scalar register, and all of a column's
+  // loads are issued before its stores.
+  {
+    const int tj = tid & 31, ti = tid >> 5;
+    const BufRsrc uks = make_rsrc(static_cast<const bf16_t*>(a.uk) + (size_t)h * d * rk, (size_t)d * rk * 2);
+    const BufRsrc uvs = make_rsrc(static_cast<const bf16_t*>(a.uv) + (size_t)h * d * rv, (size_t)d * rv * 2);
+    constexpr int KR = kMaxDPrefill / 8;  // rows per thread
+#pragma unroll
+    for (int jj = 0; jj < RKP / 32; ++jj) {
+      const int j = tj + 32 * jj;
+      uint16_t w[KR];
+#pragma unroll
+      for (int k = 0; k < KR; ++k) w[k] = 0;
+      if (j < rk) {
+#pragma unroll
+        for (int k = 0; k < KR; ++k)
+          if (8 * k < d) w[k] = buf_ld2(uks, (ti * rk + j) * 2, __builtin_amdgcn_readfirstlane(8 * k * rk * 2));
+      }
+#pragma unroll
+      for (int k = 0; k < KR; ++k)
+        if (8 * k < d) s_ukt[j * UKS + ti + 8 * k] = w[k];
+    }
+#pragma unroll
+    for (int jj = 0; jj < RVP / 32; ++jj) {
+      const int j = tj + 32 * jj;
+      uint16_t w[KR];
+#pragma unroll
+      for (int k = 0; k < KR; ++k) w[k] = 0;
+      if (j < rv) {
+#pragma unroll
+        for (int k = 0; k < KR; ++k)
+          if (8 * k < d) w[k] = buf_ld2(uvs, (ti * rv + j) * 2, __builtin_amdgcn_readfirstlane(8 * k * rv * 2));
+      }
+#pragma unroll
+      for (int k = 0; k < KR; ++k)
+        if (8 * k < d) s_uv[(ti + 8 * k) * UVS + j] = w[k];
+    }
   }
-  const bf16_t* uv = static_cast<const bf16_t*>(a.uv) + (size_t)h * d * rv;  // [d][rv]
-  for (int e = tid; e < d * RVP; e += kPThreads) {
-    const int i = e / RVP, j = e - i * RVP;
-    s_uv[i * UVS + j] = (j < rv) ? uv[(size_t)i * rv + j] : bf16_t(0);
+  // page-tile padding of both buffers: K columns r_k..RKP-1 of every token row
+  // (at most 32 of them, RKP - 32 <= r_k), V rows r_v..RVP-1 (16-byte stores)
+  {
+    const int n = tid & (kPage - 1), j0 = rk + (tid >> 6);
+#pragma unroll
+    for (int m = 0; m < 8; ++m) {
+      const int j = j0 + 4 * m;
+      if (j < RKP) {
+        const bf16_t v = (j == RKP - 1) ? kOne : bf16_t(0);
+        s_ck[n * CKS + j] = v;
+        s_ck[KTILE + n * CKS + j] = v;
+      }
+    }
   }
-  for (int e = tid; e < 2 * kPage * (RKP - rk); e += kPThreads) {
-    const int buf = e / (kPage * (RKP - rk)), r = e - buf * kPage * (RKP - rk);
-    const int n = r / (RKP - rk), j = rk + (r - n * (RKP - rk));
-    s_ck[buf * KTILE + n * CKS + j] = (j == RKP - 1) ? kOne : bf16_t(0);
-  }
-  for (int e = tid; e < 2 * kPage * (RVP - rv); e += kPThreads) {
-    const int buf = e / (kPage * (RVP - rv)), r = e - buf * kPage * (RVP - rv);
-    const int j = rv + r / kPage, n = r % kPage;
-    s_cv[buf * VTILE + j * CVS + n] = (j == rv) ? kOne : bf16_t(0);
+  for (int e = tid; e < 2 * 32 * 8; e += kPThreads) {
+    const int buf = e >> 8, j = rv + ((e >> 3) & 31), n8 = e & 7;
+    const uint32_t f = (j == rv) ? 0x3F803F80u : 0u;  // two bf16 ones, or zeros
+    if (j < RVP) *reinterpret_cast<uint4*>(&s_cv[buf * VTILE + j * CVS + 8 * n8]) = make_uint4(f, f, f, f);
   }
 
   // ---- page staging ----
@@ -198,25 +241,29 @@ void prefill_bf16_kernel(PrefillArgs a) {
     const int ch = tid + c * kPThreads;
     vdst[c] = (ch >> 3) * CVS + (ch & 7) * 8;
   }
-  uint4 stk[CHK], stv[CHV];
-  auto load_page = [&](int pg) {
+  // Two register sets: page p + 2 is in flight while page p + 1 waits in
+  // registers and page p is computed from LDS.  Every lane issues every load
+  // (lanes past the last chunk re-read chunk 0 and drop it), so the wait for
+  // one page never covers the next page's loads.
+  uint4 stk[2][CHK], stv[2][CHV];
+  auto load_page = [&](int pg, int set) {
 #pragma unroll
     for (int c = 0; c < CHK; ++c) {
       const int ch = tid + c * kPThreads;
-      if (ch < nkch) stk[c] = buf_ld16(ksrc, ch * 16, pg * kpage_b);
+      stk[set][c] = buf_ld16(ksrc, ch < nkch ? ch * 16 : 0, __builtin_amdgcn_readfirstlane(pg * kpage_b));
     }
 #pragma unroll
     for (int c = 0; c < CHV; ++c) {
       const int ch = tid + c * kPThreads;
-      if (ch < nvch) stv[c] = buf_ld16(vsrc, ch * 16, pg * vpage_b);
+      stv[set][c] = buf_ld16(vsrc, ch < nvch ? ch * 16 : 0, __builtin_amdgcn_readfirstlane(pg * vpage_b));
     }
   };
-  auto store_page = [&](int pg, bf16_t* tk, bf16_t* tv) {
+  auto store_page = [&](int pg, int set, bf16_t* tk, bf16_t* tv) {
 #pragma unroll
     for (int c = 0; c < CHK; ++c) {
       const int ch = tid + c * kPThreads;
       if (ch < nkch) {
-        const bf16_t* v = reinterpret_cast<const bf16_t*>(&stk[c]);
+        const bf16_t* v = reinterpret_cast<const bf16_t*>(&stk[set][c]);
         bf16_t* dst = tk + kdst[c];
 #pragma unroll
         for (int e = 0; e < 8; ++e) dst[e * CKS] = v[e];
@@ -227,7 +274,7 @@ void prefill_bf16_kernel(PrefillArgs a) {
     for (int c = 0; c < CHV; ++c) {
       const int ch = tid + c * kPThreads;
       if (ch < nvch) {
-        uint4 w = stv[c];
+        uint4 w = stv[set][c];
         if (last) {
           // keep tokens n0 + e < kmax: dword i holds tokens 2i (low half) and 2i + 1
           const int nv = kmax - (pg * kPage + (ch & 7) * 8);
@@ -246,9 +293,10 @@ void prefill_bf16_kernel(PrefillArgs a) {
     }
   };
 
-  load_page(0);
+  load_page(0, 0);
+  load_page(min(1, npages - 1), 1);
   __syncthreads();  // constant LDS written
-  store_page(0, s_ck, s_cv);
+  store_page(0, 0, s_ck, s_cv);
 
   // ---- D1 = Q~^T for this wave's 32 queries ----
   bf16x8 qop[KS], qlo[KS];  // Q~ as hi + lo bf16 terms: scores keep ~fp32 accuracy
@@ -257,13 +305,18 @@ void prefill_bf16_kernel(PrefillArgs a) {
 #pragma unroll
     for (int t = 0; t < QT; ++t) d1[t] = f32x16{0.f};
     const bf16_t* qrow = static_cast<const bf16_t*>(a.q) + (unit * M + (q_ok ? myq : 0)) * d;
-    const uint4 zero = make_uint4(0, 0, 0, 0);
-    for (int s = 0; s < d / 16; ++s) {
-      const uint4 bq = q_ok ? ld16(qrow + 16 * s + 8 * g) : zero;
+    uint4 bq[kMaxDPrefill / 16];  // the whole query row in flight at once
 #pragma unroll
-      for (int t = 0; t < QT; ++t) {
-        const bf16x8 au = as_bf16x8(*reinterpret_cast<const uint4*>(&s_ukt[(32 * t + col) * UKS + 16 * s + 8 * g]));
-        d1[t] = mfma(au, as_bf16x8(bq), d1[t]);
+    for (int s = 0; s < kMaxDPrefill / 16; ++s)
+      bq[s] = (q_ok && s < d / 16) ? ld16(qrow + 16 * s + 8 * g) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int s = 0; s < kMaxDPrefill / 16; ++s) {
+      if (s < d / 16) {
+#pragma unroll
+        for (int t = 0; t < QT; ++t) {
+          const bf16x8 au = as_bf16x8(*reinterpret_cast<const uint4*>(&s_ukt[(32 * t + col) * UKS + 16 * s + 8 * g]));
+          d1[t] = mfma(au, as_bf16x8(bq[s]), d1[t]);
+        }
       }
     }
 #pragma unroll
@@ -284,81 +337,95 @@ void prefill_bf16_kernel(PrefillArgs a) {
 
   auto page = [&](int p, auto bufc) {
     constexpr int buf = decltype(bufc)::value;
-    if (p + 1 < npages) load_page(p + 1);
+    // set buf held page p, already in LDS; near the end the last page is
+    // re-read rather than branching, so the wait below is always for one page
+    load_page(min(p + 2, npages - 1), buf);
     const int key0 = p * kPage;
     if (wave_live && key0 <= p0 + qlast_w) {
       const bool diag = key0 + kPage - 1 > p0 + qw0;
       const bf16_t* ktile = s_ck + buf * KTILE + col * CKS;
-      // the two key tiles' MFMA chains are interleaved
+      const bf16_t* vtile = s_cv + buf * VTILE + col * CVS;
+      // Both 32-key halves are scored up front (the second half's MFMAs run
+      // while the first half's softmax is on the VALU); each half is then
+      // its own online-softmax step.
+      // All K operands of the page are read from LDS before the first score
+      // MFMA, the V operands right after the last one: their latency is
+      // covered by the MFMAs instead of stalling each product.
+      bf16x8 ak[2][KS];
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) ak[kt][ks] = lds_pair(ktile + 32 * kt * CKS, 16 * ks, g);
+      __builtin_amdgcn_sched_barrier(0);
       f32x16 sc[2] = {f32x16{0.f}, f32x16{0.f}};
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const bf16x8 ak0 = lds_pair(ktile, 16 * ks, g);
-        const bf16x8 ak1 = lds_pair(ktile + 32 * CKS, 16 * ks, g);
-        sc[0] = mfma(ak0, qop[ks], sc[0]);
-        sc[1] = mfma(ak1, qop[ks], sc[1]);
-        sc[0] = mfma(ak0, qlo[ks], sc[0]);
-        sc[1] = mfma(ak1, qlo[ks], sc[1]);
-      }
-      if (__builtin_expect(diag, 0)) {
-        // key 32kt + 8(r/4) + 4g + r%4 of the page is visible iff 32kt + 8(r/4) + r%4 <= lim
-        const int lim = qpos - key0 - 4 * g;
+      for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-        for (int kt = 0; kt < 2; ++kt)
+        for (int ks = 0; ks < KS; ++ks) {
+          sc[kt] = mfma(ak[kt][ks], qop[ks], sc[kt]);
+          sc[kt] = mfma(ak[kt][ks], qlo[ks], sc[kt]);
+        }
+      bf16x8 av[ZT][4];
+#pragma unroll
+      for (int t = 0; t < ZT; ++t)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) av[t][u] = lds_pair(vtile + 32 * t * CVS, 16 * u, g);
+      __builtin_amdgcn_sched_barrier(0);
+      const int lim = qpos - key0 - 4 * g;
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt) {
+        f32x16& v = sc[kt];
+        if (__builtin_expect(diag, 0)) {
+          // key 32kt + 8(r/4) + 4g + r%4 of the page is visible iff 32kt + 8(r/4) + r%4 <= lim
 #pragma unroll
           for (int r = 0; r < 16; ++r)
-            if (32 * kt + 8 * (r / 4) + (r % 4) > lim) sc[kt][r] = neg_inf();
-      }
-      // row max: four independent max3 chains of eight scores, then combined
-      float part[4];
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const f32x16& v = sc[c / 2];
-        const int o = 8 * (c % 2);
-        float m = fmaxf(fmaxf(v[o], v[o + 1]), v[o + 2]);
-        m = fmaxf(fmaxf(m, v[o + 3]), v[o + 4]);
-        m = fmaxf(fmaxf(m, v[o + 5]), v[o + 6]);
-        part[c] = fmaxf(m, v[o + 7]);
-      }
-      float mx = fmaxf(fmaxf(fmaxf(part[0], part[1]), part[2]), part[3]);
-      mx = half_swap_max(mx);
-      // Raise the running max on the first page, and later only when a score
-      // exceeds it by more than 2^kLazy.
-      const bool first = (p == 0);
-      const bool raise = first || mx > kLazy;
-      if (__builtin_expect(__builtin_amdgcn_ballot_w64(raise) != 0, 0)) {
-        // new fold value -(m + mx) as hi + lo; lanes that do not raise keep theirs
-        const float target = negm - mx;
-        const __bf16 hi = (__bf16)target;
-        const __bf16 lo = (__bf16)(target - (float)hi);
-        const float delta = raise ? ((float)hi + (float)lo) - negm : 0.f;
-        if (!first) {
-          const float alpha = __builtin_amdgcn_exp2f(delta);
-#pragma unroll
-          for (int t = 0; t < ZT; ++t) zacc[t] *= alpha;
+            if (32 * kt + 8 * (r / 4) + (r % 4) > lim) v[r] = neg_inf();
         }
+        // row max of the half: two max3 chains of eight scores
+        float m0 = fmaxf(fmaxf(v[0], v[1]), v[2]), m1 = fmaxf(fmaxf(v[8], v[9]), v[10]);
+        m0 = fmaxf(fmaxf(m0, v[3]), v[4]);
+        m1 = fmaxf(fmaxf(m1, v[11]), v[12]);
+        m0 = fmaxf(fmaxf(m0, v[5]), v[6]);
+        m1 = fmaxf(fmaxf(m1, v[13]), v[14]);
+        float mx = fmaxf(fmaxf(m0, v[7]), fmaxf(m1, v[15]));
+        mx = half_swap_max(mx);
+        // Raise the running max on the first half-page, and later only when a
+        // score exceeds it by more than 2^kLazy.
+        const bool first = (p == 0 && kt == 0);
+        const bool raise = first || mx > kLazy;
+        if (__builtin_expect(__builtin_amdgcn_ballot_w64(raise) != 0, 0)) {
+          // new fold value -(m + mx) as hi + lo; lanes that do not raise keep theirs
+          const float target = negm - mx;
+          const __bf16 hi = (__bf16)target;
+          const __bf16 lo = (__bf16)(target - (float)hi);
+          const float delta = raise ? ((float)hi + (float)lo) - negm : 0.f;
+          if (!first) {
+            const float alpha = __builtin_amdgcn_exp2f(delta);
 #pragma unroll
-        for (int kt = 0; kt < 2; ++kt) sc[kt] += delta;
-        negm += delta;
-        const bool put = raise && g == 1;
-        qop[KS - 1][7] = put ? hi : qop[KS - 1][7];
-        qlo[KS - 1][7] = put ? lo : qlo[KS - 1][7];
-      }
-      // P as the value product's B operands: K-step u = registers 8(u%2).. of tile u/2
-      bf16x8 pop[4];
+            for (int t = 0; t < ZT; ++t) zacc[t] *= alpha;
+          }
+          // the scores not yet exponentiated were computed with the old fold
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
+          for (int k2 = kt; k2 < 2; ++k2) sc[k2] += delta;
+          negm += delta;
+          const bool put = raise && g == 1;
+          qop[KS - 1][7] = put ? hi : qop[KS - 1][7];
+          qlo[KS - 1][7] = put ? lo : qlo[KS - 1][7];
+        }
+        // P as the value product's B operands: K-step u = registers 8(u%2).. of this half
+        bf16x8 pop[2];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) pop[u][e] = (__bf16)__builtin_amdgcn_exp2f(sc[u / 2][8 * (u % 2) + e]);
-      }
-      const bf16_t* vtile = s_cv + buf * VTILE + col * CVS;
+        for (int u = 0; u < 2; ++u)
 #pragma unroll
-      for (int t = 0; t < ZT; ++t) {
+          for (int e = 0; e < 8; ++e) pop[u][e] = (__bf16)__builtin_amdgcn_exp2f(v[8 * u + e]);
 #pragma unroll
-        for (int u = 0; u < 4; ++u) zacc[t] = mfma(lds_pair(vtile + 32 * t * CVS, 16 * u, g), pop[u], zacc[t]);
+        for (int t = 0; t < ZT; ++t)
+#pragma unroll
+          for (int u = 0; u < 2; ++u)
+            zacc[t] = mfma(av[t][2 * kt + u], pop[u], zacc[t]);
       }
     }
-    if (p + 1 < npages) store_page(p + 1, s_ck + (buf ^ 1) * KTILE, s_cv + (buf ^ 1) * VTILE);
+    if (p + 1 < npages) store_page(p + 1, buf ^ 1, s_ck + (buf ^ 1) * KTILE, s_cv + (buf ^ 1) * VTILE);
     __syncthreads();
   };
   for (int p = 0; p < npages; p += 2) {
@@ -394,9 +461,12 @@ void prefill_bf16_kernel(PrefillArgs a) {
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
         const int i0 = 32 * it + 8 * c + 4 * g;
+        const uint2 mw = muv ? *reinterpret_cast<const uint2*>(muv + i0) : make_uint2(0, 0);
         float v[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = o[4 * c + e] + (muv ? bf16_to_f32(muv[i0 + e]) : 0.f);
+        v[0] = o[4 * c + 0] + bf16_lo(mw.x);
+        v[1] = o[4 * c + 1] + bf16_hi(mw.x);
+        v[2] = o[4 * c + 2] + bf16_lo(mw.y);
+        v[3] = o[4 * c + 3] + bf16_hi(mw.y);
         if (a.out_dtype == LLA_F32) {
           *reinterpret_cast<float4*>(static_cast<float*>(a.out) + orow + i0) = make_float4(v[0], v[1], v[2], v[3]);
         } else {
