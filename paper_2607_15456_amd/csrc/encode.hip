@@ -129,11 +129,22 @@ __global__ __launch_bounds__(256) void encode_bf16_kernel(EncodeArgs a, int head
         const bf16_t* wrow = wg + ((size_t)h * r + (row_ok ? row : 0)) * K + k0 + 8 * lg;
         const bf16_t* xrow = &s_x[buf][(tt * 16 + li) * kEncXS + 8 * lg];
         const bf16_t* mrow = mug ? mug + (size_t)h * K + k0 + 8 * lg : nullptr;
-        for (int s = 0; s < ks; ++s) {
-          const bf16x8 av = as_bf16x8(row_ok ? ld16(wrow + 32 * s) : zero);
-          const bf16x8 bv = as_bf16x8(*reinterpret_cast<const uint4*>(xrow + 32 * s));
-          acc[u] = mfma16(av, bv, acc[u]);
-          if (mrow) accm[u] = mfma16(av, as_bf16x8(ld16(mrow + 32 * s)), accm[u]);
+        // eight K-steps of W_down^T fragments in flight at once (with few
+        // tokens the weights are the whole traffic, and a load per step
+        // would expose the load latency sixteen times per chunk)
+        for (int s0 = 0; s0 < ks; s0 += 8) {
+          bf16x8 av[8];
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            av[j] = as_bf16x8(row_ok && s0 + j < ks ? ld16(wrow + 32 * (s0 + j)) : zero);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            if (s0 + j < ks) {
+              const bf16x8 bv = as_bf16x8(*reinterpret_cast<const uint4*>(xrow + 32 * (s0 + j)));
+              acc[u] = mfma16(av[j], bv, acc[u]);
+              if (mrow) accm[u] = mfma16(av[j], as_bf16x8(ld16(mrow + 32 * (s0 + j))), accm[u]);
+            }
+          }
         }
         if (kc == nkc - 1) {  // head done: write its tile, c = x W - mu W
           const int t = t0 + tt * 16 + li;
@@ -250,6 +261,60 @@ __global__ __launch_bounds__(256) void encode_stream_kernel(EncodeArgs a, int bl
   }
 }
 
+// Few new tokens (a decode step writes one per sequence): the weights are the
+// whole traffic, so every W_down^T element is read once and nothing waits on
+// more than one round of loads.  Workgroup = 32 rows of one (axis, head) x 32
+// tokens; wavefront w computes the 16x16 tile (row tile w % 2, token tile
+// w / 2) with both operands loaded straight from global memory, sixteen
+// K-steps of A and B fragments in flight at once (no LDS, no barrier).
+// grid: x = 32-token blocks, y = 32-row chunks of axis k then axis v, z = head
+__global__ __launch_bounds__(256) void encode_few_kernel(EncodeArgs a, int nrc_k) {
+  constexpr int CH = 16;  // K-steps per round of loads
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int axis = blockIdx.y >= (unsigned)nrc_k ? 1 : 0;
+  const int rc = blockIdx.y - axis * nrc_k;
+  const int h = blockIdx.z, H = a.H, K = a.K;
+  const int r = pick(a.r, axis);
+  const int li = lane & 15, lg = lane >> 4;
+  const int row = rc * 32 + (wave & 1) * 16 + li;
+  const int TT = a.B * a.M;
+  const int tcol = blockIdx.x * 32 + (wave >> 1) * 16 + li;  // token of this lane's B column
+  const bool row_ok = row < r, tok_ok = tcol < TT;
+  const bf16_t* wrow = static_cast<const bf16_t*>(pick(a.wdt, axis)) + ((size_t)h * r + (row_ok ? row : 0)) * K + 8 * lg;
+  const bf16_t* xrow = static_cast<const bf16_t*>(pick(a.x, axis)) + ((size_t)(tok_ok ? tcol : 0) * H + h) * K + 8 * lg;
+  const bf16_t* mrow = pick(a.mu, axis) ? static_cast<const bf16_t*>(pick(a.mu, axis)) + (size_t)h * K + 8 * lg : nullptr;
+  const uint4 zero = make_uint4(0, 0, 0, 0);
+  const int ks = K / 32;
+  f32x4 acc = f32x4{0.f}, accm = f32x4{0.f};
+  for (int s0 = 0; s0 < ks; s0 += CH) {
+    bf16x8 wf[CH], xf[CH], mf[CH];
+#pragma unroll
+    for (int j = 0; j < CH; ++j) {
+      const bool in = s0 + j < ks;
+      wf[j] = as_bf16x8(row_ok && in ? ld16(wrow + 32 * (s0 + j)) : zero);
+      xf[j] = as_bf16x8(tok_ok && in ? ld16(xrow + 32 * (s0 + j)) : zero);
+      mf[j] = as_bf16x8(mrow && in ? ld16(mrow + 32 * (s0 + j)) : zero);
+    }
+#pragma unroll
+    for (int j = 0; j < CH; ++j) {
+      acc = mfma16(wf[j], xf[j], acc);
+      if (mrow) accm = mfma16(wf[j], mf[j], accm);
+    }
+  }
+  // output tile: lane (li, lg) holds rows 4 lg .. 4 lg + 3 of token column li
+  const int t = blockIdx.x * 32 + (wave >> 1) * 16 + li;
+  if (t < TT) {
+    const int b = t / a.M, pos = a.pos0 + (t - b * a.M);
+    bf16_t* c = static_cast<bf16_t*>(pick(a.c, axis));
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int rr = rc * 32 + (wave & 1) * 16 + 4 * lg + e;
+      if (rr < r) c[cache_index(b, h, H, a.n_max, r, pos, rr)] = f32_to_bf16(acc[e] - accm[e]);
+    }
+  }
+}
+
 // fp32: 16 tokens x 16 rows per workgroup, K staged through LDS in chunks of 64.
 constexpr int kT = 16, kKC = 64;
 __global__ __launch_bounds__(256) void encode_f32_kernel(EncodeArgs a) {
@@ -291,9 +356,15 @@ hipError_t launch_encode(const EncodeArgs& a, hipStream_t stream) {
   const int rmax = a.r[0] > a.r[1] ? a.r[0] : a.r[1];
   if (a.dtype == LLA_BF16) {
     // Many tokens: a workgroup streams all heads of its 32 tokens (one
-    // contiguous region of x).  Few tokens (a decode step's writes): one head
-    // and two row tiles per workgroup, so the weights spread over the machine.
+    // contiguous region of x).  Fewer tokens: one head and two row tiles per
+    // workgroup, so the weights spread over the machine.
     const int blocks = (TT + kEncTok - 1) / kEncTok;
+    if (TT <= 64) {  // a decode step's writes: weights read once, one round of loads
+      const int nrc_k = (a.r[0] + 31) / 32, nrc_v = (a.r[1] + 31) / 32;
+      dim3 grid(blocks, nrc_k + nrc_v, a.H);
+      hipLaunchKernelGGL(encode_few_kernel, grid, dim3(256), 0, stream, a, nrc_k);
+      return hipGetLastError();
+    }
     if (blocks >= 256 && rmax <= 64 && (a.K == 512 || a.K == 256)) {
       // prefill-sized write: resident weights, streamed tokens; ~2 workgroups per CU
       const int per_head = 2 * a.H;

@@ -57,7 +57,7 @@ SMALL = W.Workload("enc_small", 1, 3, 128, 4, 3, 0, ((18, 30),), torch.bfloat16)
 
 
 @pytest.mark.parametrize("r_k,r_v", [(18, 30), (36, 60), (96, 160), (192, 320), (7, 9), (1, 512)])
-@pytest.mark.parametrize("M,pos0", [(1, 0), (1, 63), (100, 37), (64, 64), (129, 0)])
+@pytest.mark.parametrize("M,pos0", [(1, 0), (1, 63), (11, 5), (21, 40), (100, 37), (64, 64), (129, 0)])
 @pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
 def test_encode_ragged(r_k, r_v, M, pos0, dtype):
     n_max = 256
