@@ -179,28 +179,32 @@ def run_decode(args, torch, lla, W):
                    decode_ms=kern_ms, decode_bytes=nbytes, decode_gbs=nbytes / (kern_ms * 1e-3) / 1e9,
                    calls_per_step=wl.T * layers, splits_ws_bytes=ws.numel())
         print(f"[bench] {json.dumps(res)}", file=sys.stderr, flush=True)
-        res["cpu"] = None if args.no_cpu else cpu_baseline_decode(wl, r_k, r_v, caches[0], loops[0][0], torch)
+        res["cpu"] = None if args.no_cpu else cpu_baseline_decode(wl, r_k, r_v, caches, loops, torch)
         results.append(res)
         del caches, loops, writes, ws
         torch.cuda.empty_cache()
     return wl, results
 
 
-def cpu_baseline_decode(wl, r_k, r_v, cache, call, torch, budget_s=15.0):
+def cpu_baseline_decode(wl, r_k, r_v, caches, loops, torch, budget_s=15.0):
     """Time the oracle's plain-definition decode (reconstruct K_l, V_l; softmax
-    attention) on (b, h) units of one call until ~budget_s, then scale to the step."""
+    attention) on (b, h) units of the step's calls, in step order (loop l, layer
+    d, then b, h), until about budget_s of CPU time; scale the per-unit time to
+    the whole step."""
     import oracle
-
-    ck, cv = cache
-    q, uk, uv, _ = call
     from paper_2607_15456_amd.lla import from_paged
 
-    uk64 = uk.cpu().double().numpy()
-    uv64 = uv.cpu().double().numpy()
     units, t = 0, 0.0
-    order = [(b, h) for b in range(wl.B) for h in range(wl.H)]
+    order = [(l, d, b, h) for l in range(wl.T) for d in range(wl.layers)
+             for b in range(wl.B) for h in range(wl.H)]
+    host = {}
     while t < budget_s and units < len(order):
-        b, h = order[units]
+        l, d, b, h = order[units]
+        q, uk, uv, _ = loops[l][d]
+        if (l, d) not in host:
+            host = {(l, d): (uk.cpu().double().numpy(), uv.cpu().double().numpy())}
+        uk64, uv64 = host[(l, d)]
+        ck, cv = caches[d]
         kk = from_paged(ck[b:b + 1, h:h + 1], wl.N)[0, 0].cpu().double().numpy()
         vv = from_paged(cv[b:b + 1, h:h + 1], wl.N)[0, 0].cpu().double().numpy()
         qq = q[b, h].cpu().double().numpy()
@@ -211,10 +215,61 @@ def cpu_baseline_decode(wl, r_k, r_v, cache, call, torch, budget_s=15.0):
     per_unit = t / units
     step_s = per_unit * wl.B * wl.H * wl.T * wl.layers
     return dict(value=wl.B / step_s, unit="tokens/s", cores=cpu_threads(), kind="oracle",
-                sample=(f"oracle.decode_attn (float64, reconstruct-then-attend) on {units} of the "
-                        f"{wl.B * wl.H} (b, h) units of one (layer, loop) call, {t:.1f} s; per-unit time "
+                sample=(f"oracle.decode_attn (float64, reconstruct-then-attend) on the first {units} "
+                        f"(loop, layer, b, h) units of the step, {t:.1f} s of CPU time; per-unit time "
                         f"x {wl.B * wl.H} units x {wl.T * wl.layers} calls per step; the step's M=1 "
                         f"cache writes are not timed (under 0.1% of the work)"))
+
+
+def cpu_baseline_prefill(wl, r_k, r_v, tensors, torch, budget_s=15.0):
+    """Time the oracle on a sample of the prefill step: causal prefill rows of
+    the (loop, b, h) units in order, each unit's query positions in random
+    order (a row at position m attends m + 1 keys, so the mean sampled row
+    time estimates the mean over all rows), until about budget_s; plus the
+    Eq. 2 encode of a sample of tokens; both scaled to the whole step
+    (B H M rows x T loops, B M tokens)."""
+    import numpy as np
+    import oracle
+    from paper_2607_15456_amd.lla import from_paged
+
+    xk, xv, wk, wv, ck, cv, loops = tensors
+    B, M, H, T = wl.B, wl.N, wl.H, wl.T
+    rng = np.random.default_rng(0)
+    rows_t, nrows, nunits = 0.0, 0, 0
+    for l in range(T):
+        q, uk, uv, _ = loops[l]
+        for b in range(B):
+            for h in range(H):
+                if rows_t >= budget_s:
+                    break
+                ck0 = from_paged(ck[b:b + 1, h:h + 1], M)[0, 0].cpu().double().numpy()
+                cv0 = from_paged(cv[b:b + 1, h:h + 1], M)[0, 0].cpu().double().numpy()
+                q0 = q[b, h].cpu().double().numpy()
+                uk0, uv0 = uk[h].cpu().double().numpy(), uv[h].cpu().double().numpy()
+                nunits += 1
+                for m in rng.permutation(M):
+                    if rows_t >= budget_s:
+                        break
+                    m = int(m)
+                    t0 = time.perf_counter()
+                    oracle.prefill_attn(q0[m:m + 1], ck0[:m + 1], cv0[:m + 1], uk0, uv0, p0=m)
+                    rows_t += time.perf_counter() - t0
+                    nrows += 1
+    toks = 64
+    xk64 = xk[:1, :toks].cpu().double().numpy()
+    xv64 = xv[:1, :toks].cpu().double().numpy()
+    wk64, wv64 = wk.cpu().double().numpy(), wv.cpu().double().numpy()
+    t0 = time.perf_counter()
+    oracle.encode_batched(xk64, None, wk64)
+    oracle.encode_batched(xv64, None, wv64)
+    enc_t = time.perf_counter() - t0
+    step_s = rows_t / nrows * B * H * M * T + enc_t / toks * B * M
+    return dict(value=B * M / step_s, unit="tokens/s", cores=cpu_threads(), kind="oracle",
+                sample=(f"oracle.prefill_attn (float64, plain definition per row) on {nrows} query rows "
+                        f"of the first {nunits} (loop, b, h) units, each unit's rows in random order, "
+                        f"{rows_t:.1f} s; mean row time "
+                        f"x {B * H * M} rows x {T} loops; plus oracle.encode_batched of {toks} tokens "
+                        f"({enc_t:.2f} s) x {B * M} tokens"))
 
 
 # ---------------------------------------------------------------------------
@@ -293,7 +348,8 @@ def run_prefill(args, torch, lla, W):
         "encode": {"bound": "hbm", "achieved": round(eb / (enc_ms * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS,
                    "unit": "GB/s", "frac": round(eb / (enc_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                    "bytes_per_launch": eb, "avg_launch_ms": round(enc_ms, 5)},
-        "cpu_baseline": None,
+        "cpu_baseline": None if args.no_cpu else cpu_baseline_prefill(
+            wl, r_k, r_v, (xk, xv, wk, wv, ck, cv, loops), torch),
     }
 
 
