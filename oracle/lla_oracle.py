@@ -24,8 +24,11 @@ unchanged): s_n = scale * <q, k_n>, a = softmax(s), o = sum_n a_n v_n.
 
 Readings where the paper is silent (all listed in the design doc):
 * the softmax scale is a parameter; the teacher's 1/sqrt(d_head) is the default;
-* no RoPE on this path (the NoPE content path of App. J, where absorption is
-  exact);
+* no RoPE on the content path (the NoPE content path of App. J, where
+  absorption is exact); the decoupled rotary branch of App. J is a separate
+  per-token key, shared across loops, rotated half-split (pairs i, i + d_rope/2)
+  with angle p * base^(-2i/d_rope), and its softmax scale defaults to
+  1/sqrt(d_head + d_rope);
 * a decode query attends exactly the N cached latent entries [0, N);
 * a prefill query at absolute position p attends keys n <= p.
 
@@ -60,6 +63,11 @@ __all__ = [
     "decode_attn_batched",
     "prefill_attn_batched",
     "encode_batched",
+    "rope",
+    "decode_attn_rope",
+    "prefill_attn_rope",
+    "decode_attn_rope_batched",
+    "prefill_attn_rope_batched",
 ]
 
 
@@ -305,4 +313,110 @@ def prefill_attn_batched(Q, c_k, c_v, u_k, u_v, mu_k=None, mu_v=None, scale=None
             out[b, h, m] = decode_attn(Q[b, h, m], c_k[b, h, :n], c_v[b, h, :n], u_k[h], u_v[h],
                                        None if mu_k is None else mu_k[h],
                                        None if mu_v is None else mu_v[h], scale)
+    return out
+
+
+# ---------------------------------------------------------------------------
+# App. J "Absorbed attention": the NoPE content path plus a small explicit
+# rotary branch, shared across loops for each token (MLA-style decoupled RoPE).
+# The score of key n becomes scale * (<q, K_l[n]> + <RoPE(q_r, p_q), RoPE(k_r[n], p_n)>).
+# ---------------------------------------------------------------------------
+
+def rope(x, pos, base=10000.0):
+    """Rotary position embedding of x [..., d_rope] at position ``pos`` (scalar
+    or broadcastable to x's leading shape).  Half-split convention: feature i
+    pairs with feature i + d_rope/2 and turns by the angle pos * base^(-2i/d_rope)
+    (reading: the paper names no convention)."""
+    x = np.asarray(x, dtype=np.float64)
+    dr = x.shape[-1]
+    if dr % 2:
+        raise ValueError("d_rope must be even")
+    half = dr // 2
+    inv_freq = base ** (-2.0 * np.arange(half) / dr)
+    ang = np.asarray(pos, dtype=np.float64)[..., None] * inv_freq
+    c, s_ = np.cos(ang), np.sin(ang)
+    x1, x2 = x[..., :half], x[..., half:]
+    return np.concatenate([x1 * c - x2 * s_, x2 * c + x1 * s_], axis=-1)
+
+
+def decode_attn_rope(q, q_rope, c_k, c_v, k_rope, u_k, u_v, mu_k=None, mu_v=None, scale=None,
+                     base=10000.0, q_pos=None, k_pos=None):
+    """Loop-l decode with the decoupled rotary branch, plain definition: the
+    full key of token n is [K_l[n]; RoPE(k_rope[n], k_pos[n])] with K_l from
+    Eq. 3, the query is [q; RoPE(q_rope, q_pos)], then the teacher's attention.
+
+    q: [d]; q_rope: [d_rope] (unrotated); c_k: [N, r_k]; c_v: [N, r_v];
+    k_rope: [N, d_rope] (unrotated); k_pos defaults to 0..N-1 (the cache slot
+    is the position), q_pos to N - 1 (the newest token).  Returns [d]."""
+    q = np.asarray(q, dtype=np.float64)
+    k_rope = np.asarray(k_rope, dtype=np.float64)
+    N = k_rope.shape[0]
+    d, dr = q.shape[-1], k_rope.shape[-1]
+    if scale is None:
+        scale = default_scale(d + dr)
+    if k_pos is None:
+        k_pos = np.arange(N)
+    if q_pos is None:
+        q_pos = N - 1
+    K = np.concatenate([reconstruct(c_k, u_k, mu_k), rope(k_rope, k_pos, base)], axis=-1)
+    V = reconstruct(c_v, u_v, mu_v)
+    qf = np.concatenate([q, rope(q_rope, q_pos, base)])
+    return attention(qf, K, V, scale)
+
+
+def prefill_attn_rope(Q, Q_rope, c_k, c_v, k_rope, u_k, u_v, mu_k=None, mu_v=None, scale=None,
+                      base=10000.0, p0=0):
+    """Causal prefill with the rotary branch: query m sits at position p0 + m
+    and attends keys n <= p0 + m (plain definition, row by row)."""
+    Q = np.asarray(Q, dtype=np.float64)
+    out = np.empty_like(Q)
+    for m in range(Q.shape[0]):
+        n = p0 + m + 1
+        out[m] = decode_attn_rope(Q[m], Q_rope[m], c_k[:n], c_v[:n], k_rope[:n], u_k, u_v, mu_k,
+                                  mu_v, scale, base, q_pos=p0 + m)
+    return out
+
+
+def decode_attn_rope_batched(q, q_rope, c_k, c_v, k_rope, u_k, u_v, mu_k=None, mu_v=None,
+                             scale=None, base=10000.0, ctx_len=None, units=None):
+    """decode_attn_rope for every (b, h).  q: [B, H, d]; q_rope: [B, H, d_rope];
+    k_rope: [B, Hr, >=N, d_rope] with Hr = 1 (one rotary key per token, shared
+    by the heads) or Hr = H; other arguments as decode_attn_batched."""
+    q = np.asarray(q, dtype=np.float64)
+    B, H, d = q.shape
+    Hr = k_rope.shape[1]
+    if ctx_len is None:
+        ctx_len = c_k.shape[2]
+    lens = [int(ctx_len)] * B if np.ndim(ctx_len) == 0 else [int(v) for v in ctx_len]
+    out = np.full((B, H, d), np.nan)
+    todo = units if units is not None else [(b, h) for b in range(B) for h in range(H)]
+    for b, h in todo:
+        n = lens[b]
+        hr = 0 if Hr == 1 else h
+        out[b, h] = decode_attn_rope(q[b, h], q_rope[b, h], c_k[b, h, :n], c_v[b, h, :n],
+                                     k_rope[b, hr, :n], u_k[h], u_v[h],
+                                     None if mu_k is None else mu_k[h],
+                                     None if mu_v is None else mu_v[h], scale, base)
+    return out
+
+
+def prefill_attn_rope_batched(Q, Q_rope, c_k, c_v, k_rope, u_k, u_v, mu_k=None, mu_v=None,
+                              scale=None, base=10000.0, p0=0, units=None, rows=None):
+    """prefill_attn_rope for every (b, h) (or the given units / rows).
+    Q: [B, H, M, d]; Q_rope: [B, H, M, d_rope]; k_rope: [B, Hr, >=p0+M, d_rope]."""
+    Q = np.asarray(Q, dtype=np.float64)
+    B, H, M, d = Q.shape
+    Hr = k_rope.shape[1]
+    out = np.full((B, H, M, d), np.nan)
+    todo = units if units is not None else [(b, h) for b in range(B) for h in range(H)]
+    row_list = range(M) if rows is None else rows
+    for b, h in todo:
+        hr = 0 if Hr == 1 else h
+        for m in row_list:
+            n = p0 + m + 1
+            out[b, h, m] = decode_attn_rope(Q[b, h, m], Q_rope[b, h, m], c_k[b, h, :n], c_v[b, h, :n],
+                                            k_rope[b, hr, :n], u_k[h], u_v[h],
+                                            None if mu_k is None else mu_k[h],
+                                            None if mu_v is None else mu_v[h], scale, base,
+                                            q_pos=p0 + m)
     return out
