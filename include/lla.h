@@ -59,9 +59,10 @@
 extern "C" {
 #endif
 
-#define LLA_ABI_VERSION 1
+#define LLA_ABI_VERSION 2
 #define LLA_PAGE_TOKENS 64
 #define LLA_MAX_RANK 512
+#define LLA_MAX_ROPE 256
 #define LLA_MAX_SPLITS 64
 
 typedef enum lla_status {
@@ -198,6 +199,82 @@ lla_status lla_prefill_attn(int dtype, int out_dtype, int B, int H, int M, int d
                             int r_v, int n_max, int p0, const void* q, const void* c_k,
                             const void* c_v, const void* u_k, const void* u_v, const void* mu_k,
                             const void* mu_v, float scale, void* out, void* stream);
+
+/*
+ * Decoupled rotary branch (App. J, "Absorbed attention"): RoPE prevents exact
+ * absorption of the positional component, so a small explicit rotary key per
+ * token joins the NoPE content path; it is shared across the loops (written
+ * once per token) and, MLA-style, either shared by the heads (H_rope = 1) or
+ * one per head (H_rope = H).  With it, the score of key n becomes
+ *   scale * ( <q, K_l[n]> + <RoPE(q_r, p_q), RoPE(k_r[n], p_n)> ).
+ * RoPE here is half-split: feature i pairs with feature i + d_rope/2 and turns
+ * by the angle p * base^(-2i/d_rope) (the paper names no convention; this is
+ * the one of Llama-family models).  d_rope is a multiple of 8 in
+ * [8, LLA_MAX_ROPE].
+ *
+ * Rotary cache layout: like a latent cache of rank d_rope with H_rope heads,
+ *   element (b, g, token n, feature i) at
+ *     ((b*H_rope + g) * n_max + (n/64)*64) * d_rope + i*64 + (n % 64),
+ * holding keys already rotated at their position (slot n = position n).
+ */
+
+/*
+ * Rotate the rotary keys of M new tokens per sequence at positions
+ * pos0 .. pos0+M-1 and write them into the rotary cache (App. J).
+ *
+ *   k_rope  [B][M][H_rope][d_rope]  raw (unrotated) rotary keys, dtype
+ *   r_cache paged rotary cache (layout above), dtype, capacity n_max
+ *   base    the RoPE base (e.g. 10000), > 1
+ *
+ * Requires 0 <= pos0, pos0 + M <= n_max.  Writes exactly the slots
+ * [pos0, pos0 + M) of every (b, g); angles are formed in double precision and
+ * the result rounded to dtype (RNE for bf16).
+ * Errors: LLA_ERR_INVALID_ARG, LLA_ERR_HIP.
+ */
+lla_status lla_rope_write(int dtype, int B, int M, int H_rope, int d_rope, const void* k_rope,
+                          double base, void* r_cache, int n_max, int pos0, void* stream);
+
+/*
+ * Rotate query rotary parts (App. J) into a dense output:
+ *   x, y  [B][G][M][d_rope] of dtype (y may not alias x)
+ * Row (b, g, m) is rotated at position (pos ? pos[b] : pos0) + m, where pos is
+ * an optional device int32 [B] (for decode: each sequence's newest position,
+ * N_b - 1; for prefill: pos0 = p0 with M the new tokens).
+ * Errors: LLA_ERR_INVALID_ARG, LLA_ERR_HIP.
+ */
+lla_status lla_rope_rotate(int dtype, int B, int G, int M, int d_rope, const void* x,
+                           const int32_t* pos, int pos0, double base, void* y, void* stream);
+
+/*
+ * lla_decode_attn with the decoupled rotary branch:
+ *   q_rope   [B][H][d_rope]  the query's rotary part, already rotated at its
+ *                            position (lla_rope_rotate)
+ *   r_cache  rotary cache written by lla_rope_write (rotated keys)
+ * Slot n of r_cache is key n of the context, as for the latents.  The softmax
+ * scale is the caller's (the usual choice is 1/sqrt(d_head + d_rope)).
+ * Extra limits: ceil8(r_k) + d_rope <= LLA_MAX_RANK; H_rope is 1 or H.
+ * Errors: as lla_decode_attn.
+ */
+lla_status lla_decode_attn_rope(int dtype, int out_dtype, int B, int H, int d_head, int r_k,
+                                int r_v, int d_rope, int H_rope, int n_max, int n_ctx,
+                                const int32_t* ctx_len, const void* q, const void* q_rope,
+                                const void* c_k, const void* c_v, const void* r_cache,
+                                const void* u_k, const void* u_v, const void* mu_k,
+                                const void* mu_v, float scale, void* out, void* workspace,
+                                size_t ws_bytes, void* stream);
+
+/*
+ * lla_prefill_attn with the decoupled rotary branch:
+ *   q_rope  [B][H][M][d_rope]  rotary query parts rotated at p0 + m
+ * bf16 additionally requires r_k + d_rope <= 95 (else LLA_ERR_UNSUPPORTED).
+ * Errors: as lla_prefill_attn.
+ */
+lla_status lla_prefill_attn_rope(int dtype, int out_dtype, int B, int H, int M, int d_head,
+                                 int r_k, int r_v, int d_rope, int H_rope, int n_max, int p0,
+                                 const void* q, const void* q_rope, const void* c_k,
+                                 const void* c_v, const void* r_cache, const void* u_k,
+                                 const void* u_v, const void* mu_k, const void* mu_v, float scale,
+                                 void* out, void* stream);
 
 #ifdef __cplusplus
 }

@@ -16,5 +16,7 @@ from .lla import (  # noqa: F401
     new_workspace,
     prefill_attn,
     rho,
+    rope_rotate,
+    rope_write,
     to_paged,
 )

@@ -25,6 +25,10 @@
 // atomic counter) merges all partials and runs the value epilogue
 // out = U_v (z / l) + mu_v; the counter is left at zero.
 //
+// With the decoupled rotary branch (App. J: a small explicit rotary key per
+// token, shared across loops), the rotated query part joins q~ and the rotary
+// key rows are scanned right after the r_k content rows, in the same batches.
+//
 // The prologue (q~ = U_k^T q) and the epilogue (U_v z) read the loop-l
 // up-projections with vector loads and reduce in a fixed order, so results
 // are bitwise reproducible.
@@ -187,6 +191,7 @@ void decode_kernel(DecodeArgs a) {
   const size_t bh = (size_t)b * a.H + h;
   const size_t unit = bh * a.M + m;  // (b, h, m)
   const int rk = a.rk, rv = a.rv;
+  const int rq0 = (rk + 7) & ~7;  // s_qt slot of the first rotary row
 
   // ---- prologue: absorbed query q~ = U_k^T q, with scale * log2(e) folded in ----
   {
@@ -199,6 +204,13 @@ void decode_kernel(DecodeArgs a) {
       case 4: absorb_query<TIn, 4, kThreads>(uk, a.d, rk, a.qscale, s_q, s_part, s_qt); break;
       case 2: absorb_query<TIn, 2, kThreads>(uk, a.d, rk, a.qscale, s_q, s_part, s_qt); break;
       default: absorb_query<TIn, 1, kThreads>(uk, a.d, rk, a.qscale, s_q, s_part, s_qt); break;
+    }
+    // rotary branch: the (already rotated) query part joins q~ as extra rows,
+    // from a 16-byte aligned slot past the r_k content rows
+    if (a.dr) {
+      const TIn* qr = static_cast<const TIn*>(a.qr) + unit * a.dr;
+      for (int i = tid; i < a.dr; i += kThreads) s_qt[rq0 + i] = a.qscale * Elem<TIn>::get(qr, i);
+      __syncthreads();
     }
   }
 
@@ -217,6 +229,13 @@ void decode_kernel(DecodeArgs a) {
                                    (size_t)a.n_max * rv * ES);
   const int kpage_bytes = kPage * rk * ES, vpage_bytes = kPage * rv * ES;
   const int vk_lane = hi * kpage_bytes + lo * 16;   // K phase: page hi of the group, slice lo
+  // rotary keys of this (b, h): the same paging with dr feature rows
+  const size_t bhr = (size_t)b * a.Hr + (a.Hr == 1 ? 0 : h);
+  const BufRsrc rr_src = make_rsrc(a.dr ? static_cast<const TIn*>(a.rc) + bhr * (size_t)a.n_max * a.dr
+                                        : static_cast<const TIn*>(a.ck),
+                                   (size_t)a.n_max * a.dr * ES);
+  const int rpage_bytes = kPage * a.dr * ES;
+  const int vr_lane = hi * rpage_bytes + lo * 16;
   const int vv_lane = hi * kPage * ES + lo * 16;    // V phase: row hi of the row group, slice lo
   const int vg_full = rv / PPG, vg_part = rv % PPG;  // full row groups, rows of the partial one
   float* sp = s_p[wave];
@@ -228,18 +247,27 @@ void decode_kernel(DecodeArgs a) {
   // pages, so the FMAs of one batch overlap the memory latency of the next.
   constexpr bool PIPE = DEEP;
   const int nkb = rk / KB;                                  // full K batches
+  const int ntb = nkb + a.dr / KB;                          // plus the rotary rows (dr % 8 == 0)
   const int nvb = (vg_full + (vg_part ? 1 : 0) + VB - 1) / VB;  // V batches per page
   constexpr int NKC = (GV + VB - 1) / VB;
 
-  auto kload = [&](uint4 (&r)[KB], int gbase, int jb) {
+  // batch jb < nkb: content rows jb*KB.. of c_k; later batches: rotary rows
+  auto kload = [&](uint4 (&r)[KB], int g0p, int jb) {
+    if (jb < nkb) {
 #pragma unroll
-    for (int u = 0; u < KB; ++u) r[u] = buf_ld16(rk_src, vk_lane, gbase + (jb * KB + u) * kPage * ES);
+      for (int u = 0; u < KB; ++u) r[u] = buf_ld16(rk_src, vk_lane, g0p * kpage_bytes + (jb * KB + u) * kPage * ES);
+    } else {
+#pragma unroll
+      for (int u = 0; u < KB; ++u)
+        r[u] = buf_ld16(rr_src, vr_lane, g0p * rpage_bytes + ((jb - nkb) * KB + u) * kPage * ES);
+    }
   };
   auto kfma = [&](const uint4 (&r)[KB], int jb, float (&acc)[EPL]) {
     float qj[KB];
+    const int q0 = jb < nkb ? jb * KB : rq0 + (jb - nkb) * KB;
 #pragma unroll
     for (int u = 0; u < KB; u += 4) {
-      const float4 qa = *reinterpret_cast<const float4*>(&s_qt[jb * KB + u]);
+      const float4 qa = *reinterpret_cast<const float4*>(&s_qt[q0 + u]);
       qj[u] = qa.x;
       qj[u + 1] = qa.y;
       qj[u + 2] = qa.z;
@@ -272,17 +300,17 @@ void decode_kernel(DecodeArgs a) {
       const int gbase = g0 * kpage_bytes;
       if constexpr (PIPE) {
         uint4 ka[KB], kb2[KB];
-        if (nkb > 0) kload(ka, gbase, 0);
-        for (int jb = 0; jb < nkb; jb += 2) {
-          if (jb + 1 < nkb) kload(kb2, gbase, jb + 1);
+        if (ntb > 0) kload(ka, g0, 0);
+        for (int jb = 0; jb < ntb; jb += 2) {
+          if (jb + 1 < ntb) kload(kb2, g0, jb + 1);
           kfma(ka, jb, acc);
-          if (jb + 2 < nkb) kload(ka, gbase, jb + 2);
-          if (jb + 1 < nkb) kfma(kb2, jb + 1, acc);
+          if (jb + 2 < ntb) kload(ka, g0, jb + 2);
+          if (jb + 1 < ntb) kfma(kb2, jb + 1, acc);
         }
       } else {
-        for (int jb = 0; jb < nkb; ++jb) {
+        for (int jb = 0; jb < ntb; ++jb) {
           uint4 ka[KB];
-          kload(ka, gbase, jb);
+          kload(ka, g0, jb);
           kfma(ka, jb, acc);
         }
       }

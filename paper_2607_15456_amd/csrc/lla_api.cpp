@@ -23,6 +23,7 @@ bool dtype_ok(int t) { return t == LLA_F32 || t == LLA_BF16; }
 bool head_ok(int d) { return d >= 32 && d <= 256 && d % 32 == 0; }
 bool rank_ok(int r) { return r >= 1 && r <= LLA_MAX_RANK; }
 bool cap_ok(int n_max) { return n_max >= LLA_PAGE_TOKENS && n_max % LLA_PAGE_TOKENS == 0; }
+bool rope_ok(int d_rope) { return d_rope >= 8 && d_rope <= LLA_MAX_ROPE && d_rope % 8 == 0; }
 
 int64_t gcd64(int64_t a, int64_t b) {
   while (b) {
@@ -196,11 +197,13 @@ lla_status lla_decode_workspace_bytes(int B, int H, int r_v, int n_ctx, size_t* 
   return LLA_OK;
 }
 
-lla_status lla_decode_attn(int dtype, int out_dtype, int B, int H, int d_head, int r_k, int r_v,
-                           int n_max, int n_ctx, const int32_t* ctx_len, const void* q,
-                           const void* c_k, const void* c_v, const void* u_k, const void* u_v,
-                           const void* mu_k, const void* mu_v, float scale, void* out,
-                           void* workspace, size_t ws_bytes, void* stream) {
+namespace {
+lla_status decode_impl(int dtype, int out_dtype, int B, int H, int d_head, int r_k, int r_v,
+                       int d_rope, int H_rope, int n_max, int n_ctx, const int32_t* ctx_len,
+                       const void* q, const void* q_rope, const void* c_k, const void* c_v,
+                       const void* r_cache, const void* u_k, const void* u_v, const void* mu_k,
+                       const void* mu_v, float scale, void* out, void* workspace,
+                       size_t ws_bytes, void* stream) {
   if (!dtype_ok(dtype) || !dtype_ok(out_dtype) || B < 1 || H < 1 || !head_ok(d_head) ||
       !rank_ok(r_k) || !rank_ok(r_v) || !cap_ok(n_max) || n_ctx < 1 || n_ctx > n_max ||
       !std::isfinite(scale) || !(scale > 0.f))
@@ -209,6 +212,9 @@ lla_status lla_decode_attn(int dtype, int out_dtype, int B, int H, int d_head, i
   if (!ptr_ok(q) || !ptr_ok(c_k) || !ptr_ok(c_v) || !ptr_ok(u_k) || !ptr_ok(u_v) || !ptr_ok(out) ||
       !opt_ptr_ok(mu_k) || !opt_ptr_ok(mu_v) ||
       (ctx_len && (reinterpret_cast<uintptr_t>(ctx_len) & 3u)))
+    return LLA_ERR_INVALID_ARG;
+  if (d_rope && (!rope_ok(d_rope) || !(H_rope == 1 || H_rope == H) || !ptr_ok(q_rope) ||
+                 !ptr_ok(r_cache) || ((r_k + 7) / 8) * 8 + d_rope > LLA_MAX_RANK))
     return LLA_ERR_INVALID_ARG;
   if ((workspace == nullptr) != (ws_bytes == 0)) return LLA_ERR_WORKSPACE;
   if (workspace && (!aligned16(workspace) || ws_bytes < workspace_bytes(B, H, r_v, n_ctx)))
@@ -237,6 +243,10 @@ lla_status lla_decode_attn(int dtype, int out_dtype, int B, int H, int d_head, i
   a.muv = mu_v;
   a.qscale = (float)((double)scale * kLog2e);
   a.out = out;
+  a.dr = d_rope;
+  a.Hr = H_rope;
+  a.qr = q_rope;
+  a.rc = r_cache;
   const DecodeShape sh = choose_shape(B * H, n_ctx, workspace != nullptr, dtype == LLA_BF16);
   a.waves = sh.waves;
   a.splits = sh.splits;
@@ -249,11 +259,37 @@ lla_status lla_decode_attn(int dtype, int out_dtype, int B, int H, int d_head, i
   }
   return hip_status(lla::launch_decode(a, static_cast<hipStream_t>(stream)));
 }
+}  // namespace
 
-lla_status lla_prefill_attn(int dtype, int out_dtype, int B, int H, int M, int d_head, int r_k,
-                            int r_v, int n_max, int p0, const void* q, const void* c_k,
-                            const void* c_v, const void* u_k, const void* u_v, const void* mu_k,
-                            const void* mu_v, float scale, void* out, void* stream) {
+lla_status lla_decode_attn(int dtype, int out_dtype, int B, int H, int d_head, int r_k, int r_v,
+                           int n_max, int n_ctx, const int32_t* ctx_len, const void* q,
+                           const void* c_k, const void* c_v, const void* u_k, const void* u_v,
+                           const void* mu_k, const void* mu_v, float scale, void* out,
+                           void* workspace, size_t ws_bytes, void* stream) {
+  return decode_impl(dtype, out_dtype, B, H, d_head, r_k, r_v, 0, 1, n_max, n_ctx, ctx_len, q,
+                     nullptr, c_k, c_v, nullptr, u_k, u_v, mu_k, mu_v, scale, out, workspace,
+                     ws_bytes, stream);
+}
+
+lla_status lla_decode_attn_rope(int dtype, int out_dtype, int B, int H, int d_head, int r_k,
+                                int r_v, int d_rope, int H_rope, int n_max, int n_ctx,
+                                const int32_t* ctx_len, const void* q, const void* q_rope,
+                                const void* c_k, const void* c_v, const void* r_cache,
+                                const void* u_k, const void* u_v, const void* mu_k,
+                                const void* mu_v, float scale, void* out, void* workspace,
+                                size_t ws_bytes, void* stream) {
+  if (d_rope < 1) return LLA_ERR_INVALID_ARG;
+  return decode_impl(dtype, out_dtype, B, H, d_head, r_k, r_v, d_rope, H_rope, n_max, n_ctx,
+                     ctx_len, q, q_rope, c_k, c_v, r_cache, u_k, u_v, mu_k, mu_v, scale, out,
+                     workspace, ws_bytes, stream);
+}
+
+namespace {
+lla_status prefill_impl(int dtype, int out_dtype, int B, int H, int M, int d_head, int r_k, int r_v,
+                        int d_rope, int H_rope, int n_max, int p0, const void* q,
+                        const void* q_rope, const void* c_k, const void* c_v, const void* r_cache,
+                        const void* u_k, const void* u_v, const void* mu_k, const void* mu_v,
+                        float scale, void* out, void* stream) {
   if (!dtype_ok(dtype) || !dtype_ok(out_dtype) || B < 1 || H < 1 || M < 1 || !head_ok(d_head) ||
       !rank_ok(r_k) || !rank_ok(r_v) || !cap_ok(n_max) || p0 < 0 || (int64_t)p0 + M > n_max ||
       !std::isfinite(scale) || !(scale > 0.f))
@@ -262,10 +298,14 @@ lla_status lla_prefill_attn(int dtype, int out_dtype, int B, int H, int M, int d
   if (!ptr_ok(q) || !ptr_ok(c_k) || !ptr_ok(c_v) || !ptr_ok(u_k) || !ptr_ok(u_v) || !ptr_ok(out) ||
       !opt_ptr_ok(mu_k) || !opt_ptr_ok(mu_v))
     return LLA_ERR_INVALID_ARG;
+  if (d_rope && (!rope_ok(d_rope) || !(H_rope == 1 || H_rope == H) || !ptr_ok(q_rope) ||
+                 !ptr_ok(r_cache) || ((r_k + 7) / 8) * 8 + d_rope > LLA_MAX_RANK))
+    return LLA_ERR_INVALID_ARG;
   (void)mu_k;  // q . mu_k is constant over the keys of a query: it cancels in the softmax
   const float qscale = (float)((double)scale * kLog2e);
   if (dtype == LLA_BF16) {
-    if (r_k > 95 || r_v > 95 || d_head > 128 || (M + 127) / 128 > 65535) return LLA_ERR_UNSUPPORTED;
+    if (r_k + d_rope > 95 || r_v > 95 || d_head > 128 || (M + 127) / 128 > 65535)
+      return LLA_ERR_UNSUPPORTED;
     lla::PrefillArgs a{};
     a.out_dtype = out_dtype;
     a.B = B;
@@ -284,6 +324,10 @@ lla_status lla_prefill_attn(int dtype, int out_dtype, int B, int H, int M, int d
     a.muv = mu_v;
     a.qscale = qscale;
     a.out = out;
+    a.dr = d_rope;
+    a.Hr = H_rope;
+    a.qr = q_rope;
+    a.rc = r_cache;
     return hip_status(lla::launch_prefill_bf16(a, static_cast<hipStream_t>(stream)));
   }
   // fp32: the decode scan, one workgroup per query, query m over [0, p0 + m].
@@ -311,7 +355,74 @@ lla_status lla_prefill_attn(int dtype, int out_dtype, int B, int H, int M, int d
   a.muv = mu_v;
   a.qscale = qscale;
   a.out = out;
+  a.dr = d_rope;
+  a.Hr = H_rope;
+  a.qr = q_rope;
+  a.rc = r_cache;
   return hip_status(lla::launch_decode(a, static_cast<hipStream_t>(stream)));
+}
+}  // namespace
+
+lla_status lla_prefill_attn(int dtype, int out_dtype, int B, int H, int M, int d_head, int r_k,
+                            int r_v, int n_max, int p0, const void* q, const void* c_k,
+                            const void* c_v, const void* u_k, const void* u_v, const void* mu_k,
+                            const void* mu_v, float scale, void* out, void* stream) {
+  return prefill_impl(dtype, out_dtype, B, H, M, d_head, r_k, r_v, 0, 1, n_max, p0, q, nullptr,
+                      c_k, c_v, nullptr, u_k, u_v, mu_k, mu_v, scale, out, stream);
+}
+
+lla_status lla_prefill_attn_rope(int dtype, int out_dtype, int B, int H, int M, int d_head,
+                                 int r_k, int r_v, int d_rope, int H_rope, int n_max, int p0,
+                                 const void* q, const void* q_rope, const void* c_k,
+                                 const void* c_v, const void* r_cache, const void* u_k,
+                                 const void* u_v, const void* mu_k, const void* mu_v, float scale,
+                                 void* out, void* stream) {
+  if (d_rope < 1) return LLA_ERR_INVALID_ARG;
+  return prefill_impl(dtype, out_dtype, B, H, M, d_head, r_k, r_v, d_rope, H_rope, n_max, p0, q,
+                      q_rope, c_k, c_v, r_cache, u_k, u_v, mu_k, mu_v, scale, out, stream);
+}
+
+lla_status lla_rope_write(int dtype, int B, int M, int H_rope, int d_rope, const void* k_rope,
+                          double base, void* r_cache, int n_max, int pos0, void* stream) {
+  if (!dtype_ok(dtype) || B < 1 || M < 1 || H_rope < 1 || !rope_ok(d_rope) || !cap_ok(n_max) ||
+      pos0 < 0 || (int64_t)pos0 + M > n_max || !std::isfinite(base) || !(base > 1.0))
+    return LLA_ERR_INVALID_ARG;
+  if ((int64_t)B * M * H_rope * d_rope > (1LL << 34) || !ptr_ok(k_rope) || !ptr_ok(r_cache))
+    return LLA_ERR_INVALID_ARG;
+  lla::RopeArgs a{};
+  a.dtype = dtype;
+  a.B = B;
+  a.G = H_rope;
+  a.M = M;
+  a.dr = d_rope;
+  a.x = k_rope;
+  a.pos0 = pos0;
+  a.base = base;
+  a.y = r_cache;
+  a.n_max = n_max;
+  return hip_status(lla::launch_rope_write(a, static_cast<hipStream_t>(stream)));
+}
+
+lla_status lla_rope_rotate(int dtype, int B, int G, int M, int d_rope, const void* x,
+                           const int32_t* pos, int pos0, double base, void* y, void* stream) {
+  if (!dtype_ok(dtype) || B < 1 || G < 1 || M < 1 || !rope_ok(d_rope) || pos0 < 0 ||
+      !std::isfinite(base) || !(base > 1.0))
+    return LLA_ERR_INVALID_ARG;
+  if ((int64_t)B * G * M * d_rope > (1LL << 34) || !ptr_ok(x) || !ptr_ok(y) ||
+      (pos && (reinterpret_cast<uintptr_t>(pos) & 3u)))
+    return LLA_ERR_INVALID_ARG;
+  lla::RopeArgs a{};
+  a.dtype = dtype;
+  a.B = B;
+  a.G = G;
+  a.M = M;
+  a.dr = d_rope;
+  a.x = x;
+  a.pos = pos;
+  a.pos0 = pos0;
+  a.base = base;
+  a.y = y;
+  return hip_status(lla::launch_rope_rotate(a, static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

@@ -29,6 +29,10 @@ struct DecodeArgs {
   void* out;
   float* part;    // [units][splits][rv + 2] split partials (m, l, z)
   uint32_t* cnt;  // [units] arrival counters
+  // decoupled rotary branch (dr = 0: none): score += q_r . k_r[n]
+  int dr, Hr;      // rotary width; rotary keys per token (1: shared by the heads, or H)
+  const void* qr;  // [B][H][M][dr] rotated query parts
+  const void* rc;  // [B][Hr][n_max/64][dr][64] rotated keys, paged like the latents
 };
 
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
@@ -57,10 +61,28 @@ struct PrefillArgs {
   const void* muv;
   float qscale;
   void* out;
+  int dr, Hr;  // decoupled rotary branch, as in DecodeArgs (dr = 0: none)
+  const void* qr;
+  const void* rc;
 };
 
 // bf16 MFMA causal prefill.
 hipError_t launch_prefill_bf16(const PrefillArgs& a, hipStream_t stream);
+
+// Rotary embedding (half-split) of rows of dr elements.
+struct RopeArgs {
+  int dtype;
+  int B, G, M, dr;     // rows (b, g, m); write: x is [B][M][G][dr], rotate: [B][G][M][dr]
+  const void* x;
+  const int32_t* pos;  // rotate: per-batch base position (or null: pos0)
+  int pos0;
+  double base;
+  void* y;             // rotate: dense output like x; write: paged cache [B][G][n_max/64][dr][64]
+  int n_max;
+};
+
+hipError_t launch_rope_write(const RopeArgs& a, hipStream_t stream);
+hipError_t launch_rope_rotate(const RopeArgs& a, hipStream_t stream);
 
 int device_cu_count();  // compute units of the current device (cached)
 

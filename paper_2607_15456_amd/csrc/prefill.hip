@@ -23,6 +23,9 @@
 // exactly registers 8(t%2) + e of accumulator tile t/2.
 // The denominator l comes out of the value product: the padded V tile carries
 // a row of ones at feature r_v, so Z^T[r_v][q] = sum_n p[q][n].
+// With the decoupled rotary branch (App. J), the rotary key rows follow the r_k
+// content rows in the score tile and the rotated query part follows Q~'s, so
+// the same products add q_r . k_r to every score.
 // Q~ enters the score product as two bf16 terms (hi + lo), so the scores carry
 // about 16 significant bits rather than bf16's 8: with peaked rows the score
 // magnitudes would otherwise turn Q~'s rounding into visible weight errors.
@@ -141,6 +144,7 @@ void prefill_bf16_kernel(PrefillArgs a) {
   const int nqb = (a.M + kQBlock - 1) / kQBlock;
   const int qb = nqb - 1 - (int)blockIdx.y;  // heaviest (latest) query blocks first
   const int d = a.d, rk = a.rk, rv = a.rv, M = a.M, p0 = a.p0;
+  const int rke = rk + a.dr;  // score features: r_k content, then the rotary branch
   const int q0 = qb * kQBlock;
   const int qw0 = q0 + wave * 32;
   const int myq = qw0 + col;
@@ -198,7 +202,7 @@ void prefill_bf16_kernel(PrefillArgs a) {
   // page-tile padding of both buffers: K columns r_k..RKP-1 of every token row
   // (at most 32 of them, RKP - 32 <= r_k), V rows r_v..RVP-1 (16-byte stores)
   {
-    const int n = tid & (kPage - 1), j0 = rk + (tid >> 6);
+    const int n = tid & (kPage - 1), j0 = rke + (tid >> 6);
 #pragma unroll
     for (int m = 0; m < 8; ++m) {
       const int j = j0 + 4 * m;
@@ -229,7 +233,15 @@ void prefill_bf16_kernel(PrefillArgs a) {
   const BufRsrc vsrc = make_rsrc(static_cast<const bf16_t*>(a.cv) + unit * (size_t)a.n_max * rv,
                                  (size_t)a.n_max * rv * 2);
   const int kpage_b = kPage * rk * 2, vpage_b = kPage * rv * 2;
-  const int nkch = rk * 8, nvch = rv * 8;
+  const int nkch = rke * 8, nvch = rv * 8, ncch = rk * 8;  // K chunks: content, then rotary
+  // rotary keys: chunk ch >= r_k * 8 is chunk ch - r_k * 8 of the rotary page
+  // (feature row r_k + (ch - r_k * 8) / 8 of the score tile)
+  const bool rope = a.dr > 0;
+  const BufRsrc rsrc = make_rsrc(rope ? static_cast<const bf16_t*>(a.rc) +
+                                            ((size_t)(bh / a.H) * a.Hr + (a.Hr == 1 ? 0 : h)) * (size_t)a.n_max * a.dr
+                                      : static_cast<const bf16_t*>(a.ck),
+                                 (size_t)a.n_max * a.dr * 2);
+  const int rpage_b = kPage * a.dr * 2;
   int kdst[CHK], vdst[CHV];  // LDS element offsets of this thread's chunks inside a tile
 #pragma unroll
   for (int c = 0; c < CHK; ++c) {
@@ -250,7 +262,12 @@ void prefill_bf16_kernel(PrefillArgs a) {
 #pragma unroll
     for (int c = 0; c < CHK; ++c) {
       const int ch = tid + c * kPThreads;
-      stk[set][c] = buf_ld16(ksrc, ch < nkch ? ch * 16 : 0, __builtin_amdgcn_readfirstlane(pg * kpage_b));
+      stk[set][c] = buf_ld16(ksrc, ch < ncch ? ch * 16 : 0, __builtin_amdgcn_readfirstlane(pg * kpage_b));
+      if (rope) {
+        const uint4 w = buf_ld16(rsrc, ch >= ncch && ch < nkch ? (ch - ncch) * 16 : 0,
+                                 __builtin_amdgcn_readfirstlane(pg * rpage_b));
+        if (ch >= ncch) stk[set][c] = w;
+      }
     }
 #pragma unroll
     for (int c = 0; c < CHV; ++c) {
@@ -318,6 +335,16 @@ void prefill_bf16_kernel(PrefillArgs a) {
           d1[t] = mfma(au, as_bf16x8(bq[s]), d1[t]);
         }
       }
+    }
+    if (rope && q_ok) {  // the (already rotated) rotary query part fills features r_k .. rke - 1
+      const bf16_t* qrr = static_cast<const bf16_t*>(a.qr) + (unit * M + myq) * a.dr;
+#pragma unroll
+      for (int t = 0; t < QT; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int f = 32 * t + 8 * (r / 4) + 4 * g + (r % 4);
+          if (f >= rk && f < rke) d1[t][r] += bf16_to_f32(qrr[f - rk]);
+        }
     }
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) to_operand_split(d1[ks / 2], ks % 2, a.qscale, qop[ks], qlo[ks]);
@@ -490,9 +517,10 @@ hipError_t launch_t(const PrefillArgs& a, hipStream_t stream) {
 }  // namespace
 
 hipError_t launch_prefill_bf16(const PrefillArgs& a, hipStream_t stream) {
-  // K features padded past r_k (room for the running-max feature RKP - 1);
-  // V features padded past r_v (room for the ones row)
-  const int rkp = a.rk < 32 ? 32 : a.rk < 64 ? 64 : 96;
+  // K features padded past r_k + d_rope (room for the running-max feature
+  // RKP - 1); V features padded past r_v (room for the ones row)
+  const int rke = a.rk + a.dr;
+  const int rkp = rke < 32 ? 32 : rke < 64 ? 64 : 96;
   const int rvp = a.rv < 32 ? 32 : a.rv < 64 ? 64 : 96;
   switch (rkp * 1000 + rvp) {
     case 32032: return launch_t<32, 32>(a, stream);

@@ -41,6 +41,10 @@ _SIGS = {
     "lla_decode_workspace_bytes": (_c_int, [_c_int] * 4 + [ctypes.POINTER(_c_sz)]),
     "lla_decode_attn": (_c_int, [_c_int] * 9 + [_c_vp] * 8 + [_c_f, _c_vp, _c_vp, _c_sz, _c_vp]),
     "lla_prefill_attn": (_c_int, [_c_int] * 10 + [_c_vp] * 7 + [_c_f, _c_vp, _c_vp]),
+    "lla_rope_write": (_c_int, [_c_int] * 5 + [_c_vp, ctypes.c_double, _c_vp, _c_int, _c_int, _c_vp]),
+    "lla_rope_rotate": (_c_int, [_c_int] * 5 + [_c_vp, _c_vp, _c_int, ctypes.c_double, _c_vp, _c_vp]),
+    "lla_decode_attn_rope": (_c_int, [_c_int] * 11 + [_c_vp] * 10 + [_c_f, _c_vp, _c_vp, _c_sz, _c_vp]),
+    "lla_prefill_attn_rope": (_c_int, [_c_int] * 12 + [_c_vp] * 9 + [_c_f, _c_vp, _c_vp]),
 }
 
 _lib = None
@@ -198,12 +202,16 @@ def encode(x_k, x_v, wdt_k, wdt_v, c_k, c_v, *, T: int, pos0: int, mu_k=None, mu
 
 
 def decode_attn(q, c_k, c_v, u_k, u_v, *, n_ctx: int, ctx_len=None, mu_k=None, mu_v=None,
-                scale: float | None = None, out=None, out_dtype=torch.float32, workspace=None):
+                scale: float | None = None, out=None, out_dtype=torch.float32, workspace=None,
+                q_rope=None, r_cache=None):
     """Loop-l decode attention of q [B, H, d] over the paged latent cache.
 
     u_k: [H, d, r_k], u_v: [H, d, r_v] (loop-l up-projections); mu_*: [H, d] or
     None; ctx_len: int32 device tensor [B] or None (all sequences use n_ctx);
-    workspace: from new_workspace() or None (no split-K).  Returns out [B, H, d].
+    workspace: from new_workspace() or None (no split-K).  With the decoupled
+    rotary branch: q_rope [B, H, d_rope] already rotated (rope_rotate) and
+    r_cache the paged rotary cache [B, H_rope, n_max/64, d_rope, 64] (rope_write);
+    the default scale is then 1/sqrt(d + d_rope).  Returns out [B, H, d].
     """
     dev = q.device
     B, H, d = q.shape
@@ -228,18 +236,46 @@ def decode_attn(q, c_k, c_v, u_k, u_v, *, n_ctx: int, ctx_len=None, mu_k=None, m
     if workspace is not None:
         _need(workspace, "workspace", None, dev)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    if (q_rope is None) != (r_cache is None):
+        raise ValueError("q_rope and r_cache go together")
+    if q_rope is None:
+        if scale is None:
+            scale = 1.0 / math.sqrt(d)
+        _check(lib().lla_decode_attn(_dt(q), _out_code(out.dtype), B, H, d, r_k, r_v, n_max, n_ctx,
+                                     _ptr(ctx_len), _ptr(q), _ptr(c_k), _ptr(c_v), _ptr(u_k), _ptr(u_v),
+                                     _ptr(mu_k), _ptr(mu_v), float(scale), _ptr(out), _ptr(workspace),
+                                     ws_bytes, _stream(q)))
+        return out
+    H_rope, d_rope = _rope_shapes(q_rope, r_cache, q.dtype, dev, B, H, n_max)
+    if q_rope.shape != (B, H, d_rope):
+        raise ValueError("q_rope must have shape [B, H, d_rope]")
     if scale is None:
-        scale = 1.0 / math.sqrt(d)
-    _check(lib().lla_decode_attn(_dt(q), _out_code(out.dtype), B, H, d, r_k, r_v, n_max, n_ctx,
-                                 _ptr(ctx_len), _ptr(q), _ptr(c_k), _ptr(c_v), _ptr(u_k), _ptr(u_v),
-                                 _ptr(mu_k), _ptr(mu_v), float(scale), _ptr(out), _ptr(workspace),
-                                 ws_bytes, _stream(q)))
+        scale = 1.0 / math.sqrt(d + d_rope)
+    _check(lib().lla_decode_attn_rope(_dt(q), _out_code(out.dtype), B, H, d, r_k, r_v, d_rope, H_rope,
+                                      n_max, n_ctx, _ptr(ctx_len), _ptr(q), _ptr(q_rope), _ptr(c_k),
+                                      _ptr(c_v), _ptr(r_cache), _ptr(u_k), _ptr(u_v), _ptr(mu_k),
+                                      _ptr(mu_v), float(scale), _ptr(out), _ptr(workspace), ws_bytes,
+                                      _stream(q)))
     return out
 
 
+def _rope_shapes(q_rope, r_cache, dtype, dev, B, H, n_max):
+    _need(q_rope, "q_rope", dtype, dev)
+    _need(r_cache, "r_cache", dtype, dev)
+    if r_cache.dim() != 5 or r_cache.shape[0] != B or r_cache.shape[2] * PAGE != n_max or r_cache.shape[4] != PAGE:
+        raise ValueError("r_cache must be [B, H_rope, n_max/64, d_rope, 64] with the latents' n_max")
+    H_rope, d_rope = r_cache.shape[1], r_cache.shape[3]
+    if H_rope not in (1, H):
+        raise ValueError("r_cache must hold 1 or H rotary keys per token")
+    return H_rope, d_rope
+
+
 def prefill_attn(q, c_k, c_v, u_k, u_v, *, p0: int, mu_k=None, mu_v=None, scale: float | None = None,
-                 out=None, out_dtype=torch.float32):
-    """Causal loop-l prefill of q [B, H, M, d] at positions p0..p0+M-1 over the paged cache."""
+                 out=None, out_dtype=torch.float32, q_rope=None, r_cache=None):
+    """Causal loop-l prefill of q [B, H, M, d] at positions p0..p0+M-1 over the paged cache.
+
+    With the rotary branch: q_rope [B, H, M, d_rope] rotated at p0 + m
+    (rope_rotate with pos0=p0) and the rotary cache r_cache (rope_write)."""
     dev = q.device
     B, H, M, d = q.shape
     for t, n in ((q, "q"), (c_k, "c_k"), (c_v, "c_v"), (u_k, "u_k"), (u_v, "u_v")):
@@ -256,9 +292,59 @@ def prefill_attn(q, c_k, c_v, u_k, u_v, *, p0: int, mu_k=None, mu_v=None, scale:
         out = torch.empty((B, H, M, d), dtype=out_dtype, device=dev)
     else:
         _need(out, "out", None, dev)
+    if (q_rope is None) != (r_cache is None):
+        raise ValueError("q_rope and r_cache go together")
+    if q_rope is None:
+        if scale is None:
+            scale = 1.0 / math.sqrt(d)
+        _check(lib().lla_prefill_attn(_dt(q), _out_code(out.dtype), B, H, M, d, r_k, r_v, n_max, p0,
+                                      _ptr(q), _ptr(c_k), _ptr(c_v), _ptr(u_k), _ptr(u_v), _ptr(mu_k),
+                                      _ptr(mu_v), float(scale), _ptr(out), _stream(q)))
+        return out
+    H_rope, d_rope = _rope_shapes(q_rope, r_cache, q.dtype, dev, B, H, n_max)
+    if q_rope.shape != (B, H, M, d_rope):
+        raise ValueError("q_rope must have shape [B, H, M, d_rope]")
     if scale is None:
-        scale = 1.0 / math.sqrt(d)
-    _check(lib().lla_prefill_attn(_dt(q), _out_code(out.dtype), B, H, M, d, r_k, r_v, n_max, p0,
-                                  _ptr(q), _ptr(c_k), _ptr(c_v), _ptr(u_k), _ptr(u_v), _ptr(mu_k),
-                                  _ptr(mu_v), float(scale), _ptr(out), _stream(q)))
+        scale = 1.0 / math.sqrt(d + d_rope)
+    _check(lib().lla_prefill_attn_rope(_dt(q), _out_code(out.dtype), B, H, M, d, r_k, r_v, d_rope, H_rope,
+                                       n_max, p0, _ptr(q), _ptr(q_rope), _ptr(c_k), _ptr(c_v),
+                                       _ptr(r_cache), _ptr(u_k), _ptr(u_v), _ptr(mu_k), _ptr(mu_v),
+                                       float(scale), _ptr(out), _stream(q)))
+    return out
+
+
+def rope_write(k_rope, r_cache, *, pos0: int, base: float = 10000.0):
+    """Rotate the rotary keys k_rope [B, M, H_rope, d_rope] at positions
+    pos0..pos0+M-1 and write them into r_cache [B, H_rope, n_max/64, d_rope, 64]."""
+    dev = k_rope.device
+    _need(k_rope, "k_rope", None, dev)
+    _need(r_cache, "r_cache", k_rope.dtype, dev)
+    B, M, G, dr = k_rope.shape
+    n_max = r_cache.shape[2] * PAGE
+    if r_cache.shape != (B, G, n_max // PAGE, dr, PAGE):
+        raise ValueError("inconsistent shapes")
+    _check(lib().lla_rope_write(_dt(k_rope), B, M, G, dr, _ptr(k_rope), float(base), _ptr(r_cache),
+                                n_max, pos0, _stream(k_rope)))
+
+
+def rope_rotate(x, *, pos=None, pos0: int = 0, base: float = 10000.0, out=None):
+    """Rotate rows of x [B, G, M, d_rope] (or [B, G, d_rope], M = 1): row (b, g, m)
+    at position (pos[b] if pos is given, else pos0) + m.  pos: int32 device [B]."""
+    dev = x.device
+    _need(x, "x", None, dev)
+    shape = x.shape
+    xx = x if x.dim() == 4 else x.unsqueeze(2)
+    B, G, M, dr = xx.shape
+    if pos is not None:
+        _need(pos, "pos", torch.int32, dev)
+        if pos.shape != (B,):
+            raise ValueError("pos must have shape [B]")
+    if out is None:
+        out = torch.empty(shape, dtype=x.dtype, device=dev)
+    else:
+        _need(out, "out", x.dtype, dev)
+        if out.shape != shape:
+            raise ValueError("out must have x's shape")
+    _check(lib().lla_rope_rotate(_dt(x), B, G, M, dr, _ptr(x), _ptr(pos), pos0, float(base), _ptr(out),
+                                 _stream(x)))
     return out

@@ -30,14 +30,15 @@ def test_header_declares_the_boundary():
     names = _declared()
     assert names == sorted(["lla_status_string", "lla_abi_version", "lla_rho", "lla_cache_bytes",
                             "lla_encode", "lla_decode_workspace_bytes", "lla_decode_attn",
-                            "lla_prefill_attn"])
+                            "lla_prefill_attn", "lla_rope_write", "lla_rope_rotate",
+                            "lla_decode_attn_rope", "lla_prefill_attn_rope"])
 
 
 def test_library_exports_every_declared_symbol():
     h = ctypes.CDLL(lla.LIB_PATH)
     for name in _declared():
         assert hasattr(h, name), name
-    assert lla.abi_version() == 1
+    assert lla.abi_version() == 2
 
 
 def test_status_strings():
@@ -162,3 +163,74 @@ def _prefill(**kw):
 ])
 def test_prefill_rejects(kw, code):
     assert _prefill(**kw) == code
+
+
+# ---- the decoupled rotary branch ----
+
+def _decode_rope(**kw):
+    a = dict(dtype=1, out_dtype=0, B=2, H=16, d=128, rk=96, rv=160, dr=64, Hr=1, n_max=512, n_ctx=512,
+             ctx_len=None, q=P, qr=P, ck=P, cv=P, rc=P, uk=P, uv=P, muk=None, muv=None, scale=0.088, out=P,
+             ws=None, ws_bytes=0, stream=None)
+    a.update(kw)
+    return lla.lib().lla_decode_attn_rope(a["dtype"], a["out_dtype"], a["B"], a["H"], a["d"], a["rk"],
+                                          a["rv"], a["dr"], a["Hr"], a["n_max"], a["n_ctx"], a["ctx_len"],
+                                          a["q"], a["qr"], a["ck"], a["cv"], a["rc"], a["uk"], a["uv"],
+                                          a["muk"], a["muv"], a["scale"], a["out"], a["ws"], a["ws_bytes"],
+                                          a["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dr=0), 1), (dict(dr=12), 1), (dict(dr=264), 1), (dict(Hr=2), 1), (dict(Hr=0), 1),
+    (dict(qr=None), 1), (dict(rc=None), 1), (dict(qr=MIS), 1), (dict(rk=500, dr=16), 1),
+    (dict(B=0), 1), (dict(ws=P, ws_bytes=0), 3),
+])
+def test_decode_rope_rejects(kw, code):
+    assert _decode_rope(**kw) == code
+
+
+def _prefill_rope(**kw):
+    a = dict(dtype=1, out_dtype=0, B=1, H=16, M=64, d=128, rk=18, rv=30, dr=64, Hr=16, n_max=512, p0=0,
+             q=P, qr=P, ck=P, cv=P, rc=P, uk=P, uv=P, muk=None, muv=None, scale=0.088, out=P, stream=None)
+    a.update(kw)
+    return lla.lib().lla_prefill_attn_rope(a["dtype"], a["out_dtype"], a["B"], a["H"], a["M"], a["d"],
+                                           a["rk"], a["rv"], a["dr"], a["Hr"], a["n_max"], a["p0"], a["q"],
+                                           a["qr"], a["ck"], a["cv"], a["rc"], a["uk"], a["uv"], a["muk"],
+                                           a["muv"], a["scale"], a["out"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dr=0), 1), (dict(dr=20), 1), (dict(Hr=3), 1), (dict(qr=None), 1), (dict(rc=MIS), 1),
+    (dict(M=0), 1), (dict(rk=32, dr=64), 2), (dict(rv=96), 2),
+])
+def test_prefill_rope_rejects(kw, code):
+    assert _prefill_rope(**kw) == code
+
+
+def _rope_write(**kw):
+    a = dict(dtype=1, B=2, M=8, Hr=1, dr=64, x=P, base=10000.0, rc=P, n_max=512, pos0=0, stream=None)
+    a.update(kw)
+    return lla.lib().lla_rope_write(a["dtype"], a["B"], a["M"], a["Hr"], a["dr"], a["x"], a["base"], a["rc"],
+                                    a["n_max"], a["pos0"], a["stream"])
+
+
+@pytest.mark.parametrize("kw", [
+    dict(dtype=2), dict(B=0), dict(M=0), dict(Hr=0), dict(dr=6), dict(dr=0), dict(x=None), dict(rc=MIS),
+    dict(n_max=100), dict(pos0=-1), dict(pos0=505), dict(base=1.0), dict(base=float("nan")),
+])
+def test_rope_write_rejects(kw):
+    assert _rope_write(**kw) == lla.LLA_ERR_INVALID_ARG
+
+
+def _rope_rotate(**kw):
+    a = dict(dtype=1, B=2, G=16, M=1, dr=64, x=P, pos=None, pos0=0, base=10000.0, y=P, stream=None)
+    a.update(kw)
+    return lla.lib().lla_rope_rotate(a["dtype"], a["B"], a["G"], a["M"], a["dr"], a["x"], a["pos"], a["pos0"],
+                                     a["base"], a["y"], a["stream"])
+
+
+@pytest.mark.parametrize("kw", [
+    dict(dtype=5), dict(B=0), dict(G=0), dict(M=0), dict(dr=10), dict(x=None), dict(y=MIS),
+    dict(pos=P + 2), dict(pos0=-3), dict(base=0.5),
+])
+def test_rope_rotate_rejects(kw):
+    assert _rope_rotate(**kw) == lla.LLA_ERR_INVALID_ARG
