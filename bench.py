@@ -60,6 +60,9 @@ def parse():
     p.add_argument("--workload", default="ouro14b_decode",
                    choices=["ouro14b_decode", "ouro26b_long", "rank_sweep", "prefill_write"])
     p.add_argument("--tier", type=int, default=None, help="rank_sweep: run only this tier index")
+    p.add_argument("--rope", type=int, default=0,
+                   help="add the decoupled rotary branch with this d_rope (one rotary key per token, "
+                        "shared by the heads and the loops); ouro14b_decode and prefill_write")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--copy-probe", action="store_true",
                    help="run a plain 1 GiB read + 1 GiB write elementwise kernel (counter calibration for rocprofv3 --pmc)")
@@ -105,9 +108,11 @@ def cpu_threads():
 # decode workloads (ouro14b_decode, ouro26b_long, rank_sweep)
 # ---------------------------------------------------------------------------
 
-def decode_bytes(B, H, d, N, r_k, r_v, elem=2, out_elem=4):
-    """Algorithmic bytes of one decode launch: latents + loop-l U_k, U_v + q + out."""
-    return B * H * N * (r_k + r_v) * elem + H * d * (r_k + r_v) * elem + B * H * d * elem + B * H * d * out_elem
+def decode_bytes(B, H, d, N, r_k, r_v, elem=2, out_elem=4, d_rope=0, H_rope=1):
+    """Algorithmic bytes of one decode launch: latents + loop-l U_k, U_v + q + out
+    (+ the rotary keys, once per (b, rotary head), and the rotary query parts)."""
+    return (B * H * N * (r_k + r_v) * elem + H * d * (r_k + r_v) * elem + B * H * d * elem + B * H * d * out_elem
+            + B * H_rope * N * d_rope * elem + B * H * d_rope * elem)
 
 
 def run_decode(args, torch, lla, W):
@@ -142,6 +147,20 @@ def run_decode(args, torch, lla, W):
             wv = W.down_projection(wl, r_v, "v", d, dev)
             writes.append((xk, xv, wk, wv))
         ws = lla.new_workspace(wl.B, wl.H, r_v, wl.N, dev)
+        dr = args.rope
+        rope = None
+        if dr:
+            # per layer: a rotary cache (keys written and rotated at setup), the new
+            # token's raw rotary key; per (loop, layer): the raw rotary query part
+            rope = {"cache": [], "key": [], "q": [[None] * layers for _ in range(wl.T)],
+                    "q_rot": torch.empty((wl.B, wl.H, dr), dtype=wl.dtype, device=dev)}
+            for d in range(layers):
+                rc = lla.alloc_cache(wl.B, 1, n_max, dr, device=dev)
+                lla.rope_write(W.rotary_keys(wl, dr, 1, d, device=dev), rc, pos0=0)
+                rope["cache"].append(rc)
+                rope["key"].append(W.rotary_keys(wl, dr, 1, d, N=1, device=dev))
+                for l in range(wl.T):
+                    rope["q"][l][d] = W.rotary_queries(wl, dr, d, l, device=dev)
         torch.cuda.synchronize()
 
         timer = KernelTimer(torch, stream)
@@ -151,14 +170,23 @@ def run_decode(args, torch, lla, W):
                 for d in range(layers):
                     q, uk, uv, out = loops[l][d]
                     ck, cv = caches[d]
-                    s = timer.start() if timed else None
-                    lla.decode_attn(q, ck, cv, uk, uv, n_ctx=wl.N, out=out, workspace=ws)
+                    if rope:
+                        # the new token sits at position N; its query is rotated there
+                        lla.rope_rotate(rope["q"][l][d], pos0=wl.N, out=rope["q_rot"])
+                        s = timer.start() if timed else None
+                        lla.decode_attn(q, ck, cv, uk, uv, n_ctx=wl.N, out=out, workspace=ws,
+                                        q_rope=rope["q_rot"], r_cache=rope["cache"][d])
+                    else:
+                        s = timer.start() if timed else None
+                        lla.decode_attn(q, ck, cv, uk, uv, n_ctx=wl.N, out=out, workspace=ws)
                     if timed:
                         timer.stop(s)
             for d in range(layers):
                 xk, xv, wk, wv = writes[d]
                 ck, cv = caches[d]
                 lla.encode(xk, xv, wk, wv, ck, cv, T=wl.T, pos0=wl.N)
+                if rope:
+                    lla.rope_write(rope["key"][d], rope["cache"][d], pos0=wl.N)
 
         for _ in range(args.warmup):
             step(False)
@@ -174,14 +202,14 @@ def run_decode(args, torch, lla, W):
         wall = time.perf_counter() - wall0
         step_ms = t0.elapsed_time(t1) / args.steps
         kern_ms = timer.mean_ms()
-        nbytes = decode_bytes(wl.B, wl.H, wl.d, wl.N, r_k, r_v)
+        nbytes = decode_bytes(wl.B, wl.H, wl.d, wl.N, r_k, r_v, d_rope=dr)
         res = dict(tier=ti, r_k=r_k, r_v=r_v, step_ms=step_ms, wall_step_ms=1e3 * wall / args.steps,
                    decode_ms=kern_ms, decode_bytes=nbytes, decode_gbs=nbytes / (kern_ms * 1e-3) / 1e9,
                    calls_per_step=wl.T * layers, splits_ws_bytes=ws.numel())
         print(f"[bench] {json.dumps(res)}", file=sys.stderr, flush=True)
-        res["cpu"] = None if args.no_cpu else cpu_baseline_decode(wl, r_k, r_v, caches, loops, torch)
+        res["cpu"] = None if (args.no_cpu or dr) else cpu_baseline_decode(wl, r_k, r_v, caches, loops, torch)
         results.append(res)
-        del caches, loops, writes, ws
+        del caches, loops, writes, ws, rope
         torch.cuda.empty_cache()
     return wl, results
 
@@ -276,11 +304,11 @@ def cpu_baseline_prefill(wl, r_k, r_v, tensors, torch, budget_s=15.0):
 # prefill + cache write (prefill_write)
 # ---------------------------------------------------------------------------
 
-def prefill_flops(B, H, M, p0, d, r_k, r_v):
-    """Algorithmic flops of one causal prefill call: 2 (r_k + r_v) per causal
-    (query, key) pair plus the absorption products Q U_k and Z U_v^T."""
+def prefill_flops(B, H, M, p0, d, r_k, r_v, d_rope=0):
+    """Algorithmic flops of one causal prefill call: 2 (r_k + d_rope + r_v) per
+    causal (query, key) pair plus the absorption products Q U_k and Z U_v^T."""
     pairs = M * p0 + M * (M + 1) // 2
-    return B * H * (2 * (r_k + r_v) * pairs + 2 * M * d * (r_k + r_v))
+    return B * H * (2 * (r_k + d_rope + r_v) * pairs + 2 * M * d * (r_k + r_v))
 
 
 def encode_bytes(B, M, H, K, r_k, r_v, elem=2):
@@ -305,6 +333,14 @@ def run_prefill(args, torch, lla, W):
         q = W.queries(wl, 0, l, M=M, device=dev)
         uk, uv, _, _ = W.codec_loop(wl, r_k, r_v, 0, l, dev)
         loops.append((q, uk, uv, torch.empty((B, H, M, d), dtype=torch.float32, device=dev)))
+    dr = args.rope
+    if dr:
+        if r_k + dr > 95:
+            raise SystemExit("prefill_write: r_k + d_rope must stay <= 95 for the bf16 prefill")
+        k_rope = W.rotary_keys(wl, dr, 1, 0, device=dev)
+        r_cache = lla.alloc_cache(B, 1, M, dr, device=dev)
+        q_rope = [W.rotary_queries(wl, dr, 0, l, M=M, device=dev) for l in range(T)]
+        q_rot = torch.empty_like(q_rope[0])
     torch.cuda.synchronize()
     enc_t, pre_t = KernelTimer(torch, stream), KernelTimer(torch, stream)
 
@@ -313,9 +349,16 @@ def run_prefill(args, torch, lla, W):
         lla.encode(xk, xv, wk, wv, ck, cv, T=T, pos0=0)
         if timed:
             enc_t.stop(s)
-        for q, uk, uv, out in loops:
-            s = pre_t.start() if timed else None
-            lla.prefill_attn(q, ck, cv, uk, uv, p0=0, out=out)
+        if dr:
+            lla.rope_write(k_rope, r_cache, pos0=0)
+        for l, (q, uk, uv, out) in enumerate(loops):
+            if dr:
+                lla.rope_rotate(q_rope[l], pos0=0, out=q_rot)
+                s = pre_t.start() if timed else None
+                lla.prefill_attn(q, ck, cv, uk, uv, p0=0, out=out, q_rope=q_rot, r_cache=r_cache)
+            else:
+                s = pre_t.start() if timed else None
+                lla.prefill_attn(q, ck, cv, uk, uv, p0=0, out=out)
             if timed:
                 pre_t.stop(s)
 
@@ -330,7 +373,7 @@ def run_prefill(args, torch, lla, W):
     torch.cuda.synchronize()
     step_ms = t0.elapsed_time(t1) / args.steps
     enc_ms, pre_ms = enc_t.mean_ms(), pre_t.mean_ms()
-    fl = prefill_flops(B, H, M, 0, d, r_k, r_v)
+    fl = prefill_flops(B, H, M, 0, d, r_k, r_v, dr)
     eb = encode_bytes(B, M, H, T * d, r_k, r_v)
     tflops = fl / (pre_ms * 1e-3) / 1e12
     return {
@@ -339,8 +382,9 @@ def run_prefill(args, torch, lla, W):
         "unit": "tokens/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(step_ms, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": wl.description, "batch": B, "new_tokens": M, "heads": H, "d_head": d, "loops": T,
-                   "r_k": r_k, "r_v": r_v, "parallelism": "single GPU"},
+        "config": {"workload": wl.description + (f"; decoupled rotary branch d_rope {dr}" if dr else ""),
+                   "batch": B, "new_tokens": M, "heads": H, "d_head": d, "loops": T,
+                   "r_k": r_k, "r_v": r_v, "d_rope": dr, "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "achieved": round(tflops, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(tflops / BF16_PEAK_TFLOPS, 4), "traffic": None,
                      "kernel": "prefill_bf16_kernel (lla_prefill_attn)", "flops_per_launch": fl,
@@ -348,7 +392,7 @@ def run_prefill(args, torch, lla, W):
         "encode": {"bound": "hbm", "achieved": round(eb / (enc_ms * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS,
                    "unit": "GB/s", "frac": round(eb / (enc_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                    "bytes_per_launch": eb, "avg_launch_ms": round(enc_ms, 5)},
-        "cpu_baseline": None if args.no_cpu else cpu_baseline_prefill(
+        "cpu_baseline": None if (args.no_cpu or dr) else cpu_baseline_prefill(
             wl, r_k, r_v, (xk, xv, wk, wv, ck, cv, loops), torch),
     }
 
@@ -390,7 +434,7 @@ def main():
     B, N, d = wl.B, wl.N, wl.d
     value = B / (head["step_ms"] * 1e-3)
     achieved = head["decode_gbs"]
-    traffic = traffic_bytes((wl.name, head["r_k"], head["r_v"]))
+    traffic = None if args.rope else traffic_bytes((wl.name, head["r_k"], head["r_v"]))
     line = {
         "metric": "latent-cache decode attention tokens/sec and achieved HBM GB/s (% of peak)",
         "value": round(value, 2),
@@ -405,7 +449,9 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {
-            "workload": wl.description,
+            "workload": wl.description + (f"; decoupled rotary branch d_rope {args.rope} (one rotary key "
+                                          f"per token shared by the heads)" if args.rope else ""),
+            "d_rope": args.rope,
             "layers": wl.layers, "loops": wl.T, "heads": wl.H, "d_head": d, "batch": B, "context": N,
             "r_k": head["r_k"], "r_v": head["r_v"], "calls_per_step": head["calls_per_step"],
             "parallelism": "single GPU",

@@ -6,8 +6,8 @@
 // Keys are rotated once, when their token is written (the branch is shared by
 // the loops, so there is one write per token); queries are rotated by the
 // caller through lla_rope_rotate before the attention call.  The angle is
-// formed and reduced in double precision (positions reach 2^24 and beyond), so
-// the only rounding that matters is the final one to the storage type.
+// formed and reduced to [-pi, pi] in double precision (positions reach 2^24
+// and beyond) and its sine and cosine taken in fp32, about 1e-7 absolute.
 
 #include "lla_device.h"
 #include "lla_internal.h"
@@ -21,60 +21,73 @@ __device__ __forceinline__ float load_elem(const void* p, size_t i) {
   return Elem<T>::get(static_cast<const T*>(p), i);
 }
 
-// (cos, sin) of p * base^(-2i/dr)
-__device__ __forceinline__ void rope_cs(int p, int i, int dr, double base, float& c, float& s) {
-  const double ang = (double)p * pow(base, -2.0 * i / dr);
-  double sd, cd;
-  sincos(ang, &sd, &cd);
-  c = (float)cd;
-  s = (float)sd;
+// The dr/2 inverse frequencies base^(-2i/dr), once per workgroup (double).
+__device__ __forceinline__ void inv_freq_table(double* t, int dr, double base) {
+  for (int i = threadIdx.x; i < dr / 2; i += blockDim.x) t[i] = pow(base, -2.0 * i / dr);
+  __syncthreads();
 }
 
-// One thread per (row, pair).  Write: row (b, m, g) of x [B][M][G][dr] lands at
-// position pos0 + m of the paged cache of (b, g).
+// (cos, sin) of p * inv_freq: the angle is formed and reduced to [-pi, pi] in
+// double (positions reach 2^24 and beyond), then evaluated in fp32.
+__device__ __forceinline__ void rope_cs(int p, double inv_freq, float& c, float& s) {
+  constexpr double kTwoPi = 6.283185307179586476925286766559;
+  const double ang = (double)p * inv_freq;
+  const double r = ang - rint(ang * (1.0 / kTwoPi)) * kTwoPi;
+  sincosf((float)r, &s, &c);
+}
+
+// One thread per (b, m, pair i): the angle is shared by the G heads of the
+// row, so cos and sin are formed once and applied G times.
+// Write: row (b, m, g) of x [B][M][G][dr] lands at position pos0 + m of the
+// paged cache of (b, g).
 template <typename T>
 __global__ __launch_bounds__(256) void rope_write_kernel(RopeArgs a) {
+  __shared__ double s_inv[LLA_MAX_ROPE / 2];
+  inv_freq_table(s_inv, a.dr, a.base);
   const int half = a.dr / 2;
   const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const size_t rows = (size_t)a.B * a.M * a.G;
-  if (idx >= rows * half) return;
-  const size_t row = idx / half;
-  const int i = (int)(idx - row * half);
-  const int g = (int)(row % a.G);
-  const size_t bm = row / a.G;
+  if (idx >= (size_t)a.B * a.M * half) return;
+  const size_t bm = idx / half;
+  const int i = (int)(idx - bm * half);
   const int m = (int)(bm % a.M), b = (int)(bm / a.M);
   const int pos = a.pos0 + m;
   float c, s;
-  rope_cs(pos, i, a.dr, a.base, c, s);
-  const float x1 = load_elem<T>(a.x, row * a.dr + i), x2 = load_elem<T>(a.x, row * a.dr + i + half);
-  const size_t page = ((size_t)(b * a.G + g) * a.n_max + (size_t)(pos / kPage) * kPage) * a.dr;
+  rope_cs(pos, s_inv[i], c, s);
   T* y = static_cast<T*>(a.y);
-  store_out(y, page + (size_t)i * kPage + pos % kPage, x1 * c - x2 * s);
-  store_out(y, page + (size_t)(i + half) * kPage + pos % kPage, x2 * c + x1 * s);
+  for (int g = 0; g < a.G; ++g) {
+    const size_t row = bm * a.G + g;
+    const float x1 = load_elem<T>(a.x, row * a.dr + i), x2 = load_elem<T>(a.x, row * a.dr + i + half);
+    const size_t page = ((size_t)(b * a.G + g) * a.n_max + (size_t)(pos / kPage) * kPage) * a.dr;
+    store_out(y, page + (size_t)i * kPage + pos % kPage, x1 * c - x2 * s);
+    store_out(y, page + (size_t)(i + half) * kPage + pos % kPage, x2 * c + x1 * s);
+  }
 }
 
 // Rotate: row (b, g, m) of x [B][G][M][dr] at position (pos ? pos[b] : pos0) + m.
 template <typename T>
 __global__ __launch_bounds__(256) void rope_rotate_kernel(RopeArgs a) {
+  __shared__ double s_inv[LLA_MAX_ROPE / 2];
+  inv_freq_table(s_inv, a.dr, a.base);
   const int half = a.dr / 2;
   const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const size_t rows = (size_t)a.B * a.G * a.M;
-  if (idx >= rows * half) return;
-  const size_t row = idx / half;
-  const int i = (int)(idx - row * half);
-  const int m = (int)(row % a.M);
-  const int b = (int)(row / ((size_t)a.G * a.M));
+  if (idx >= (size_t)a.B * a.M * half) return;
+  const size_t bm = idx / half;
+  const int i = (int)(idx - bm * half);
+  const int m = (int)(bm % a.M), b = (int)(bm / a.M);
   const int pos = (a.pos ? a.pos[b] : a.pos0) + m;
   float c, s;
-  rope_cs(pos, i, a.dr, a.base, c, s);
-  const float x1 = load_elem<T>(a.x, row * a.dr + i), x2 = load_elem<T>(a.x, row * a.dr + i + half);
+  rope_cs(pos, s_inv[i], c, s);
   T* y = static_cast<T*>(a.y);
-  store_out(y, row * a.dr + i, x1 * c - x2 * s);
-  store_out(y, row * a.dr + i + half, x2 * c + x1 * s);
+  for (int g = 0; g < a.G; ++g) {
+    const size_t row = ((size_t)b * a.G + g) * a.M + m;
+    const float x1 = load_elem<T>(a.x, row * a.dr + i), x2 = load_elem<T>(a.x, row * a.dr + i + half);
+    store_out(y, row * a.dr + i, x1 * c - x2 * s);
+    store_out(y, row * a.dr + i + half, x2 * c + x1 * s);
+  }
 }
 
 dim3 grid_for(const RopeArgs& a) {
-  const size_t n = (size_t)a.B * a.G * a.M * (a.dr / 2);
+  const size_t n = (size_t)a.B * a.M * (a.dr / 2);
   return dim3((unsigned)((n + 255) / 256));
 }
 
