@@ -68,6 +68,10 @@ __all__ = [
     "prefill_attn_rope",
     "decode_attn_rope_batched",
     "prefill_attn_rope_batched",
+    "kept_positions",
+    "ring_slot",
+    "decode_attn_evict",
+    "decode_attn_rope_evict",
 ]
 
 
@@ -420,3 +424,46 @@ def prefill_attn_rope_batched(Q, Q_rope, c_k, c_v, k_rope, u_k, u_v, mu_k=None, 
                                             None if mu_v is None else mu_v[h], scale, base,
                                             q_pos=p0 + m)
     return out
+
+
+# ---------------------------------------------------------------------------
+# Sequence-axis eviction composed with the latent cache (App. J "Eviction and
+# long-context prefill"; tab:evict): a StreamingLLM-style budget keeps the
+# first `sink` tokens and the most recent `window` tokens.
+# ---------------------------------------------------------------------------
+
+def kept_positions(N: int, sink: int, window: int):
+    """Positions of a context of N tokens that a (sink, window) budget keeps."""
+    if N <= sink + window:
+        return list(range(N))
+    return list(range(sink)) + list(range(N - window, N))
+
+
+def ring_slot(p: int, sink: int, window: int) -> int:
+    """Cache slot of position p when the window part is a ring of ``window`` slots
+    after the ``sink`` fixed ones (reading: the paper does not say how the
+    budget is laid out; any bijection of the kept positions onto the slots
+    gives the same attention on the content path)."""
+    return p if p < sink else sink + (p - sink) % window
+
+
+def decode_attn_evict(q, c_k, c_v, u_k, u_v, mu_k=None, mu_v=None, scale=None, sink=4, window=256):
+    """Loop-l decode of the newest token over the tokens an eviction budget keeps
+    (plain definition: select the kept positions of the full latent history, then
+    decode_attn).  c_k, c_v: [N, r] for every position 0..N-1."""
+    keep = kept_positions(np.asarray(c_k).shape[0], sink, window)
+    c_k = np.asarray(c_k, dtype=np.float64)[keep]
+    c_v = np.asarray(c_v, dtype=np.float64)[keep]
+    return decode_attn(q, c_k, c_v, u_k, u_v, mu_k, mu_v, scale)
+
+
+def decode_attn_rope_evict(q, q_rope, c_k, c_v, k_rope, u_k, u_v, mu_k=None, mu_v=None, scale=None,
+                           base=10000.0, sink=4, window=256):
+    """decode_attn_rope over the kept positions: the rotary keys keep their true
+    positions, and the query sits at N - 1."""
+    N = np.asarray(c_k).shape[0]
+    keep = kept_positions(N, sink, window)
+    return decode_attn_rope(q, q_rope, np.asarray(c_k, dtype=np.float64)[keep],
+                            np.asarray(c_v, dtype=np.float64)[keep],
+                            np.asarray(k_rope, dtype=np.float64)[keep], u_k, u_v, mu_k, mu_v, scale, base,
+                            q_pos=N - 1, k_pos=np.asarray(keep))
