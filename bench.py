@@ -60,6 +60,10 @@ def parse():
     p.add_argument("--workload", default="ouro14b_decode",
                    choices=["ouro14b_decode", "ouro26b_long", "rank_sweep", "prefill_write"])
     p.add_argument("--tier", type=int, default=None, help="rank_sweep: run only this tier index")
+    p.add_argument("--evict", default=None,
+                   help="SINK,WINDOW: decode workloads keep a sink + window eviction budget (ring cache of "
+                        "SINK + WINDOW slots, the step's new token written into its ring slot)")
+    p.add_argument("--ranks", default=None, help="R_K,R_V: override a decode workload's ranks")
     p.add_argument("--rope", type=int, default=0,
                    help="add the decoupled rotary branch with this d_rope (one rotary key per token, "
                         "shared by the heads and the loops); ouro14b_decode and prefill_write")
@@ -120,10 +124,19 @@ def run_decode(args, torch, lla, W):
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream(dev)
     tiers = list(enumerate(wl.ranks))
+    if args.ranks:
+        tiers = [(0, tuple(int(v) for v in args.ranks.split(",")))]
     if args.tier is not None:
         tiers = [tiers[args.tier]]
     layers = wl.layers
     n_max = wl.N + 64  # room for the token the step writes at position N
+    n_ctx = wl.N
+    evict = None
+    if args.evict:
+        # the context is wl.N tokens long, the cache keeps sink + window of them in a ring
+        evict = tuple(int(v) for v in args.evict.split(","))
+        n_ctx = min(wl.N, sum(evict))
+        n_max = (sum(evict) + 63) // 64 * 64
     results = []
     for ti, (r_k, r_v) in tiers:
         print(f"[bench] {wl.name} tier {ti} r=({r_k},{r_v}): allocating {layers} layer caches", file=sys.stderr,
@@ -146,7 +159,7 @@ def run_decode(args, torch, lla, W):
             wk = W.down_projection(wl, r_k, "k", d, dev)
             wv = W.down_projection(wl, r_v, "v", d, dev)
             writes.append((xk, xv, wk, wv))
-        ws = lla.new_workspace(wl.B, wl.H, r_v, wl.N, dev)
+        ws = lla.new_workspace(wl.B, wl.H, r_v, n_ctx, dev)
         dr = args.rope
         rope = None
         if dr:
@@ -156,7 +169,7 @@ def run_decode(args, torch, lla, W):
                     "q_rot": torch.empty((wl.B, wl.H, dr), dtype=wl.dtype, device=dev)}
             for d in range(layers):
                 rc = lla.alloc_cache(wl.B, 1, n_max, dr, device=dev)
-                lla.rope_write(W.rotary_keys(wl, dr, 1, d, device=dev), rc, pos0=0)
+                lla.rope_write(W.rotary_keys(wl, dr, 1, d, N=n_ctx, device=dev), rc, pos0=0)
                 rope["cache"].append(rc)
                 rope["key"].append(W.rotary_keys(wl, dr, 1, d, N=1, device=dev))
                 for l in range(wl.T):
@@ -174,19 +187,19 @@ def run_decode(args, torch, lla, W):
                         # the new token sits at position N; its query is rotated there
                         lla.rope_rotate(rope["q"][l][d], pos0=wl.N, out=rope["q_rot"])
                         s = timer.start() if timed else None
-                        lla.decode_attn(q, ck, cv, uk, uv, n_ctx=wl.N, out=out, workspace=ws,
+                        lla.decode_attn(q, ck, cv, uk, uv, n_ctx=n_ctx, out=out, workspace=ws,
                                         q_rope=rope["q_rot"], r_cache=rope["cache"][d])
                     else:
                         s = timer.start() if timed else None
-                        lla.decode_attn(q, ck, cv, uk, uv, n_ctx=wl.N, out=out, workspace=ws)
+                        lla.decode_attn(q, ck, cv, uk, uv, n_ctx=n_ctx, out=out, workspace=ws)
                     if timed:
                         timer.stop(s)
             for d in range(layers):
                 xk, xv, wk, wv = writes[d]
                 ck, cv = caches[d]
-                lla.encode(xk, xv, wk, wv, ck, cv, T=wl.T, pos0=wl.N)
+                lla.encode(xk, xv, wk, wv, ck, cv, T=wl.T, pos0=wl.N, evict=evict)
                 if rope:
-                    lla.rope_write(rope["key"][d], rope["cache"][d], pos0=wl.N)
+                    lla.rope_write(rope["key"][d], rope["cache"][d], pos0=wl.N, evict=evict)
 
         for _ in range(args.warmup):
             step(False)
@@ -202,12 +215,13 @@ def run_decode(args, torch, lla, W):
         wall = time.perf_counter() - wall0
         step_ms = t0.elapsed_time(t1) / args.steps
         kern_ms = timer.mean_ms()
-        nbytes = decode_bytes(wl.B, wl.H, wl.d, wl.N, r_k, r_v, d_rope=dr)
+        nbytes = decode_bytes(wl.B, wl.H, wl.d, n_ctx, r_k, r_v, d_rope=dr)
         res = dict(tier=ti, r_k=r_k, r_v=r_v, step_ms=step_ms, wall_step_ms=1e3 * wall / args.steps,
                    decode_ms=kern_ms, decode_bytes=nbytes, decode_gbs=nbytes / (kern_ms * 1e-3) / 1e9,
                    calls_per_step=wl.T * layers, splits_ws_bytes=ws.numel())
         print(f"[bench] {json.dumps(res)}", file=sys.stderr, flush=True)
-        res["cpu"] = None if (args.no_cpu or dr) else cpu_baseline_decode(wl, r_k, r_v, caches, loops, torch)
+        res["cpu"] = (None if (args.no_cpu or dr or evict or args.ranks)
+                      else cpu_baseline_decode(wl, r_k, r_v, caches, loops, torch))
         results.append(res)
         del caches, loops, writes, ws, rope
         torch.cuda.empty_cache()
@@ -434,7 +448,7 @@ def main():
     B, N, d = wl.B, wl.N, wl.d
     value = B / (head["step_ms"] * 1e-3)
     achieved = head["decode_gbs"]
-    traffic = None if args.rope else traffic_bytes((wl.name, head["r_k"], head["r_v"]))
+    traffic = None if (args.rope or args.evict) else traffic_bytes((wl.name, head["r_k"], head["r_v"]))
     line = {
         "metric": "latent-cache decode attention tokens/sec and achieved HBM GB/s (% of peak)",
         "value": round(value, 2),
@@ -450,9 +464,13 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": wl.description + (f"; decoupled rotary branch d_rope {args.rope} (one rotary key "
-                                          f"per token shared by the heads)" if args.rope else ""),
+                                          f"per token shared by the heads)" if args.rope else "")
+            + (f"; ranks overridden to ({head['r_k']}, {head['r_v']})" if args.ranks else "")
+            + (f"; eviction budget sink+window = {args.evict.replace(',', '+')} (ring cache)" if args.evict else ""),
             "d_rope": args.rope,
+            "evict": args.evict,
             "layers": wl.layers, "loops": wl.T, "heads": wl.H, "d_head": d, "batch": B, "context": N,
+            "attended_slots": min(N, sum(int(v) for v in args.evict.split(","))) if args.evict else N,
             "r_k": head["r_k"], "r_v": head["r_v"], "calls_per_step": head["calls_per_step"],
             "parallelism": "single GPU",
         },

@@ -59,7 +59,7 @@
 extern "C" {
 #endif
 
-#define LLA_ABI_VERSION 2
+#define LLA_ABI_VERSION 3
 #define LLA_PAGE_TOKENS 64
 #define LLA_MAX_RANK 512
 #define LLA_MAX_ROPE 256
@@ -275,6 +275,38 @@ lla_status lla_prefill_attn_rope(int dtype, int out_dtype, int B, int H, int M, 
                                  const void* c_v, const void* r_cache, const void* u_k,
                                  const void* u_v, const void* mu_k, const void* mu_v, float scale,
                                  void* out, void* stream);
+
+/*
+ * Sequence-axis eviction composed with the latent cache (App. J "Eviction and
+ * long-context prefill"; tab:evict): a StreamingLLM-style budget keeps the
+ * first `sink` tokens and the most recent `window` tokens.  The cache then
+ * holds sink + window slots: position p lives in slot p when p < sink, else in
+ * slot sink + (p - sink) % window (a ring).  Attention on the content path
+ * does not depend on the order of the keys, so the decode entry points attend
+ * slots [0, min(N, sink + window)) unchanged (pass that as n_ctx / ctx_len);
+ * rotary keys are rotated at their true position before they are stored, so
+ * the rotary branch composes too (rotate the query at its true position).
+ */
+
+/*
+ * lla_encode writing position pos0 + m into its ring slot.
+ * Requires sink >= 0, window >= 1, sink + window <= n_max, and the M tokens to
+ * land in distinct slots: at most `window` of them at positions >= sink.
+ * Errors: LLA_ERR_INVALID_ARG, LLA_ERR_HIP.
+ */
+lla_status lla_encode_ring(int dtype, int B, int M, int H, int T, int d_head, int r_k, int r_v,
+                           const void* x_k, const void* x_v, const void* mu_k, const void* mu_v,
+                           const void* wdt_k, const void* wdt_v, void* c_k, void* c_v, int n_max,
+                           int pos0, int sink, int window, void* stream);
+
+/*
+ * lla_rope_write rotating key m at its position pos0 + m and storing it in the
+ * position's ring slot; the same slot requirements as lla_encode_ring.
+ * Errors: LLA_ERR_INVALID_ARG, LLA_ERR_HIP.
+ */
+lla_status lla_rope_write_ring(int dtype, int B, int M, int H_rope, int d_rope, const void* k_rope,
+                               double base, void* r_cache, int n_max, int pos0, int sink,
+                               int window, void* stream);
 
 #ifdef __cplusplus
 }

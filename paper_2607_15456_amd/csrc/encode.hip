@@ -149,7 +149,7 @@ __global__ __launch_bounds__(256) void encode_bf16_kernel(EncodeArgs a, int head
         if (kc == nkc - 1) {  // head done: write its tile, c = x W - mu W
           const int t = t0 + tt * 16 + li;
           if (t < TT) {
-            const int b = t / a.M, pos = a.pos0 + (t - b * a.M);
+            const int b = t / a.M, pos = ring_slot(a.pos0 + (t - b * a.M), a.sink, a.window);
             bf16_t* c = static_cast<bf16_t*>(pick(a.c, axis));
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
@@ -248,7 +248,7 @@ __global__ __launch_bounds__(256) void encode_stream_kernel(EncodeArgs a, int bl
         acc = mfma16(wf[s], as_bf16x8(*reinterpret_cast<const uint4*>(xrow + 32 * s)), acc);
       const int t = blk * kEncTok + tt * 16 + li;
       if (t < TT) {
-        const int b = t / a.M, pos = a.pos0 + (t - b * a.M);
+        const int b = t / a.M, pos = ring_slot(a.pos0 + (t - b * a.M), a.sink, a.window);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int rr = rt * 16 + 4 * lg + e;
@@ -305,7 +305,7 @@ __global__ __launch_bounds__(256) void encode_few_kernel(EncodeArgs a, int nrc_k
   // output tile: lane (li, lg) holds rows 4 lg .. 4 lg + 3 of token column li
   const int t = blockIdx.x * 32 + (wave >> 1) * 16 + li;
   if (t < TT) {
-    const int b = t / a.M, pos = a.pos0 + (t - b * a.M);
+    const int b = t / a.M, pos = ring_slot(a.pos0 + (t - b * a.M), a.sink, a.window);
     bf16_t* c = static_cast<bf16_t*>(pick(a.c, axis));
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -344,7 +344,7 @@ __global__ __launch_bounds__(256) void encode_f32_kernel(EncodeArgs a) {
     __syncthreads();
   }
   if (tok < TT && row < r) {
-    const int b = tok / a.M, pos = a.pos0 + (tok - b * a.M);
+    const int b = tok / a.M, pos = ring_slot(a.pos0 + (tok - b * a.M), a.sink, a.window);
     static_cast<float*>(pick(a.c, axis))[cache_index(b, h, a.H, a.n_max, r, pos, row)] = acc;
   }
 }

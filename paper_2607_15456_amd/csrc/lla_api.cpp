@@ -159,12 +159,25 @@ lla_status lla_cache_bytes(int64_t layers, int64_t heads, int64_t T, int64_t d_h
   return LLA_OK;
 }
 
-lla_status lla_encode(int dtype, int B, int M, int H, int T, int d_head, int r_k, int r_v,
-                      const void* x_k, const void* x_v, const void* mu_k, const void* mu_v,
-                      const void* wdt_k, const void* wdt_v, void* c_k, void* c_v, int n_max,
-                      int pos0, void* stream) {
+namespace {
+// Slots of M new tokens at positions pos0 .. pos0+M-1: with an eviction budget
+// (window > 0) they must fit the cache and land in distinct slots.
+bool slots_ok(int M, int n_max, int pos0, int sink, int window) {
+  if (pos0 < 0) return false;
+  if (window == 0) return sink == 0 && (int64_t)pos0 + M <= n_max;
+  if (window < 0 || sink < 0 || (int64_t)sink + window > n_max) return false;
+  if ((int64_t)pos0 + M > std::numeric_limits<int>::max()) return false;
+  const int64_t first_ring = pos0 > sink ? pos0 : sink;
+  const int64_t in_ring = (int64_t)pos0 + M - first_ring;
+  return in_ring <= window;
+}
+
+lla_status encode_impl(int dtype, int B, int M, int H, int T, int d_head, int r_k, int r_v,
+                       const void* x_k, const void* x_v, const void* mu_k, const void* mu_v,
+                       const void* wdt_k, const void* wdt_v, void* c_k, void* c_v, int n_max,
+                       int pos0, int sink, int window, void* stream) {
   if (!dtype_ok(dtype) || B < 1 || M < 1 || H < 1 || T < 1 || !head_ok(d_head) || !rank_ok(r_k) ||
-      !rank_ok(r_v) || !cap_ok(n_max) || pos0 < 0 || (int64_t)pos0 + M > n_max)
+      !rank_ok(r_v) || !cap_ok(n_max) || !slots_ok(M, n_max, pos0, sink, window))
     return LLA_ERR_INVALID_ARG;
   if ((int64_t)T * d_head > (1 << 20) || (int64_t)B * M > (1 << 30)) return LLA_ERR_INVALID_ARG;
   if (!ptr_ok(x_k) || !ptr_ok(x_v) || !ptr_ok(wdt_k) || !ptr_ok(wdt_v) || !ptr_ok(c_k) ||
@@ -188,7 +201,51 @@ lla_status lla_encode(int dtype, int B, int M, int H, int T, int d_head, int r_k
   a.c[1] = c_v;
   a.n_max = n_max;
   a.pos0 = pos0;
+  a.sink = sink;
+  a.window = window;
   return hip_status(lla::launch_encode(a, static_cast<hipStream_t>(stream)));
+}
+
+lla_status rope_write_impl(int dtype, int B, int M, int H_rope, int d_rope, const void* k_rope,
+                           double base, void* r_cache, int n_max, int pos0, int sink, int window,
+                           void* stream) {
+  if (!dtype_ok(dtype) || B < 1 || M < 1 || H_rope < 1 || !rope_ok(d_rope) || !cap_ok(n_max) ||
+      !slots_ok(M, n_max, pos0, sink, window) || !std::isfinite(base) || !(base > 1.0))
+    return LLA_ERR_INVALID_ARG;
+  if ((int64_t)B * M * H_rope * d_rope > (1LL << 34) || !ptr_ok(k_rope) || !ptr_ok(r_cache))
+    return LLA_ERR_INVALID_ARG;
+  lla::RopeArgs a{};
+  a.dtype = dtype;
+  a.B = B;
+  a.G = H_rope;
+  a.M = M;
+  a.dr = d_rope;
+  a.x = k_rope;
+  a.pos0 = pos0;
+  a.base = base;
+  a.y = r_cache;
+  a.n_max = n_max;
+  a.sink = sink;
+  a.window = window;
+  return hip_status(lla::launch_rope_write(a, static_cast<hipStream_t>(stream)));
+}
+}  // namespace
+
+lla_status lla_encode(int dtype, int B, int M, int H, int T, int d_head, int r_k, int r_v,
+                      const void* x_k, const void* x_v, const void* mu_k, const void* mu_v,
+                      const void* wdt_k, const void* wdt_v, void* c_k, void* c_v, int n_max,
+                      int pos0, void* stream) {
+  return encode_impl(dtype, B, M, H, T, d_head, r_k, r_v, x_k, x_v, mu_k, mu_v, wdt_k, wdt_v, c_k,
+                     c_v, n_max, pos0, 0, 0, stream);
+}
+
+lla_status lla_encode_ring(int dtype, int B, int M, int H, int T, int d_head, int r_k, int r_v,
+                           const void* x_k, const void* x_v, const void* mu_k, const void* mu_v,
+                           const void* wdt_k, const void* wdt_v, void* c_k, void* c_v, int n_max,
+                           int pos0, int sink, int window, void* stream) {
+  if (window < 1) return LLA_ERR_INVALID_ARG;
+  return encode_impl(dtype, B, M, H, T, d_head, r_k, r_v, x_k, x_v, mu_k, mu_v, wdt_k, wdt_v, c_k,
+                     c_v, n_max, pos0, sink, window, stream);
 }
 
 lla_status lla_decode_workspace_bytes(int B, int H, int r_v, int n_ctx, size_t* bytes) {
@@ -384,23 +441,16 @@ lla_status lla_prefill_attn_rope(int dtype, int out_dtype, int B, int H, int M, 
 
 lla_status lla_rope_write(int dtype, int B, int M, int H_rope, int d_rope, const void* k_rope,
                           double base, void* r_cache, int n_max, int pos0, void* stream) {
-  if (!dtype_ok(dtype) || B < 1 || M < 1 || H_rope < 1 || !rope_ok(d_rope) || !cap_ok(n_max) ||
-      pos0 < 0 || (int64_t)pos0 + M > n_max || !std::isfinite(base) || !(base > 1.0))
-    return LLA_ERR_INVALID_ARG;
-  if ((int64_t)B * M * H_rope * d_rope > (1LL << 34) || !ptr_ok(k_rope) || !ptr_ok(r_cache))
-    return LLA_ERR_INVALID_ARG;
-  lla::RopeArgs a{};
-  a.dtype = dtype;
-  a.B = B;
-  a.G = H_rope;
-  a.M = M;
-  a.dr = d_rope;
-  a.x = k_rope;
-  a.pos0 = pos0;
-  a.base = base;
-  a.y = r_cache;
-  a.n_max = n_max;
-  return hip_status(lla::launch_rope_write(a, static_cast<hipStream_t>(stream)));
+  return rope_write_impl(dtype, B, M, H_rope, d_rope, k_rope, base, r_cache, n_max, pos0, 0, 0,
+                         stream);
+}
+
+lla_status lla_rope_write_ring(int dtype, int B, int M, int H_rope, int d_rope, const void* k_rope,
+                               double base, void* r_cache, int n_max, int pos0, int sink,
+                               int window, void* stream) {
+  if (window < 1) return LLA_ERR_INVALID_ARG;
+  return rope_write_impl(dtype, B, M, H_rope, d_rope, k_rope, base, r_cache, n_max, pos0, sink,
+                         window, stream);
 }
 
 lla_status lla_rope_rotate(int dtype, int B, int G, int M, int d_rope, const void* x,

@@ -62,4 +62,10 @@ __device__ __forceinline__ float xor_shfl(float v, int mask) { return __shfl_xor
 
 __device__ __forceinline__ float neg_inf() { return -__builtin_inff(); }
 
+// Cache slot of token position pos under a sink + window eviction budget (the
+// window part is a ring after the sink slots); window 0 means no eviction.
+__device__ __forceinline__ int ring_slot(int pos, int sink, int window) {
+  return (window == 0 || pos < sink) ? pos : sink + (pos - sink) % window;
+}
+
 }  // namespace lla

@@ -46,6 +46,7 @@ struct EncodeArgs {
   const void* wdt[2];
   void* c[2];
   int n_max, pos0;
+  int sink, window;  // eviction budget: position p goes to slot ring_slot(p) (window 0: slot p)
 };
 
 hipError_t launch_encode(const EncodeArgs& a, hipStream_t stream);
@@ -79,6 +80,7 @@ struct RopeArgs {
   double base;
   void* y;             // rotate: dense output like x; write: paged cache [B][G][n_max/64][dr][64]
   int n_max;
+  int sink, window;    // write: eviction budget as in EncodeArgs
 };
 
 hipError_t launch_rope_write(const RopeArgs& a, hipStream_t stream);

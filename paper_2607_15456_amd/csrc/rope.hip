@@ -38,8 +38,8 @@ __device__ __forceinline__ void rope_cs(int p, double inv_freq, float& c, float&
 
 // One thread per (b, m, pair i): the angle is shared by the G heads of the
 // row, so cos and sin are formed once and applied G times.
-// Write: row (b, m, g) of x [B][M][G][dr] lands at position pos0 + m of the
-// paged cache of (b, g).
+// Write: row (b, m, g) of x [B][M][G][dr] is rotated at position pos0 + m and
+// lands in that position's slot of the paged cache of (b, g).
 template <typename T>
 __global__ __launch_bounds__(256) void rope_write_kernel(RopeArgs a) {
   __shared__ double s_inv[LLA_MAX_ROPE / 2];
@@ -51,15 +51,16 @@ __global__ __launch_bounds__(256) void rope_write_kernel(RopeArgs a) {
   const int i = (int)(idx - bm * half);
   const int m = (int)(bm % a.M), b = (int)(bm / a.M);
   const int pos = a.pos0 + m;
+  const int slot = ring_slot(pos, a.sink, a.window);  // rotated at its true position, stored at its slot
   float c, s;
   rope_cs(pos, s_inv[i], c, s);
   T* y = static_cast<T*>(a.y);
   for (int g = 0; g < a.G; ++g) {
     const size_t row = bm * a.G + g;
     const float x1 = load_elem<T>(a.x, row * a.dr + i), x2 = load_elem<T>(a.x, row * a.dr + i + half);
-    const size_t page = ((size_t)(b * a.G + g) * a.n_max + (size_t)(pos / kPage) * kPage) * a.dr;
-    store_out(y, page + (size_t)i * kPage + pos % kPage, x1 * c - x2 * s);
-    store_out(y, page + (size_t)(i + half) * kPage + pos % kPage, x2 * c + x1 * s);
+    const size_t page = ((size_t)(b * a.G + g) * a.n_max + (size_t)(slot / kPage) * kPage) * a.dr;
+    store_out(y, page + (size_t)i * kPage + slot % kPage, x1 * c - x2 * s);
+    store_out(y, page + (size_t)(i + half) * kPage + slot % kPage, x2 * c + x1 * s);
   }
 }
 

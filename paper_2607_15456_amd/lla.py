@@ -45,6 +45,8 @@ _SIGS = {
     "lla_rope_rotate": (_c_int, [_c_int] * 5 + [_c_vp, _c_vp, _c_int, ctypes.c_double, _c_vp, _c_vp]),
     "lla_decode_attn_rope": (_c_int, [_c_int] * 11 + [_c_vp] * 10 + [_c_f, _c_vp, _c_vp, _c_sz, _c_vp]),
     "lla_prefill_attn_rope": (_c_int, [_c_int] * 12 + [_c_vp] * 9 + [_c_f, _c_vp, _c_vp]),
+    "lla_encode_ring": (_c_int, [_c_int] * 8 + [_c_vp] * 8 + [_c_int] * 4 + [_c_vp]),
+    "lla_rope_write_ring": (_c_int, [_c_int] * 5 + [_c_vp, ctypes.c_double, _c_vp] + [_c_int] * 4 + [_c_vp]),
 }
 
 _lib = None
@@ -176,11 +178,17 @@ def new_workspace(B: int, H: int, r_v: int, n_ctx: int, device="cuda") -> torch.
 # Device entry points
 # ---------------------------------------------------------------------------
 
-def encode(x_k, x_v, wdt_k, wdt_v, c_k, c_v, *, T: int, pos0: int, mu_k=None, mu_v=None):
+def ring_slot(p: int, sink: int, window: int) -> int:
+    """Slot of position p in a sink + window eviction cache (as lla_encode_ring)."""
+    return p if p < sink else sink + (p - sink) % window
+
+
+def encode(x_k, x_v, wdt_k, wdt_v, c_k, c_v, *, T: int, pos0: int, mu_k=None, mu_v=None, evict=None):
     """Write (x - mu) W_down for both axes into cache slots [pos0, pos0 + M) (Eq. 2).
 
     x_k, x_v: [B, M, H, T*d]; wdt_k: [H, r_k, T*d]; wdt_v: [H, r_v, T*d];
     mu_k, mu_v: [H, T*d] or None; c_k, c_v: paged caches [B, H, n_max/64, r, 64].
+    evict = (sink, window): positions go to their ring slots (lla_encode_ring).
     """
     dev = x_k.device
     for t, n in ((x_k, "x_k"), (x_v, "x_v"), (wdt_k, "wdt_k"), (wdt_v, "wdt_v"), (c_k, "c_k"), (c_v, "c_v")):
@@ -196,9 +204,15 @@ def encode(x_k, x_v, wdt_k, wdt_v, c_k, c_v, *, T: int, pos0: int, mu_k=None, mu
     if (x_v.shape != x_k.shape or wdt_k.shape != (H, r_k, K) or wdt_v.shape != (H, r_v, K)
             or c_k.shape != (B, H, n_max // PAGE, r_k, PAGE) or c_v.shape != (B, H, n_max // PAGE, r_v, PAGE)):
         raise ValueError("inconsistent shapes")
-    _check(lib().lla_encode(_dt(x_k), B, M, H, T, K // T, r_k, r_v, _ptr(x_k), _ptr(x_v), _ptr(mu_k),
-                            _ptr(mu_v), _ptr(wdt_k), _ptr(wdt_v), _ptr(c_k), _ptr(c_v), n_max, pos0,
-                            _stream(x_k)))
+    if evict is None:
+        _check(lib().lla_encode(_dt(x_k), B, M, H, T, K // T, r_k, r_v, _ptr(x_k), _ptr(x_v), _ptr(mu_k),
+                                _ptr(mu_v), _ptr(wdt_k), _ptr(wdt_v), _ptr(c_k), _ptr(c_v), n_max, pos0,
+                                _stream(x_k)))
+    else:
+        sink, window = evict
+        _check(lib().lla_encode_ring(_dt(x_k), B, M, H, T, K // T, r_k, r_v, _ptr(x_k), _ptr(x_v), _ptr(mu_k),
+                                     _ptr(mu_v), _ptr(wdt_k), _ptr(wdt_v), _ptr(c_k), _ptr(c_v), n_max, pos0,
+                                     sink, window, _stream(x_k)))
 
 
 def decode_attn(q, c_k, c_v, u_k, u_v, *, n_ctx: int, ctx_len=None, mu_k=None, mu_v=None,
@@ -313,9 +327,10 @@ def prefill_attn(q, c_k, c_v, u_k, u_v, *, p0: int, mu_k=None, mu_v=None, scale:
     return out
 
 
-def rope_write(k_rope, r_cache, *, pos0: int, base: float = 10000.0):
+def rope_write(k_rope, r_cache, *, pos0: int, base: float = 10000.0, evict=None):
     """Rotate the rotary keys k_rope [B, M, H_rope, d_rope] at positions
-    pos0..pos0+M-1 and write them into r_cache [B, H_rope, n_max/64, d_rope, 64]."""
+    pos0..pos0+M-1 and write them into r_cache [B, H_rope, n_max/64, d_rope, 64]
+    (into their ring slots when evict = (sink, window))."""
     dev = k_rope.device
     _need(k_rope, "k_rope", None, dev)
     _need(r_cache, "r_cache", k_rope.dtype, dev)
@@ -323,8 +338,13 @@ def rope_write(k_rope, r_cache, *, pos0: int, base: float = 10000.0):
     n_max = r_cache.shape[2] * PAGE
     if r_cache.shape != (B, G, n_max // PAGE, dr, PAGE):
         raise ValueError("inconsistent shapes")
-    _check(lib().lla_rope_write(_dt(k_rope), B, M, G, dr, _ptr(k_rope), float(base), _ptr(r_cache),
-                                n_max, pos0, _stream(k_rope)))
+    if evict is None:
+        _check(lib().lla_rope_write(_dt(k_rope), B, M, G, dr, _ptr(k_rope), float(base), _ptr(r_cache),
+                                    n_max, pos0, _stream(k_rope)))
+    else:
+        sink, window = evict
+        _check(lib().lla_rope_write_ring(_dt(k_rope), B, M, G, dr, _ptr(k_rope), float(base), _ptr(r_cache),
+                                         n_max, pos0, sink, window, _stream(k_rope)))
 
 
 def rope_rotate(x, *, pos=None, pos0: int = 0, base: float = 10000.0, out=None):

@@ -31,14 +31,15 @@ def test_header_declares_the_boundary():
     assert names == sorted(["lla_status_string", "lla_abi_version", "lla_rho", "lla_cache_bytes",
                             "lla_encode", "lla_decode_workspace_bytes", "lla_decode_attn",
                             "lla_prefill_attn", "lla_rope_write", "lla_rope_rotate",
-                            "lla_decode_attn_rope", "lla_prefill_attn_rope"])
+                            "lla_decode_attn_rope", "lla_prefill_attn_rope", "lla_encode_ring",
+                            "lla_rope_write_ring"])
 
 
 def test_library_exports_every_declared_symbol():
     h = ctypes.CDLL(lla.LIB_PATH)
     for name in _declared():
         assert hasattr(h, name), name
-    assert lla.abi_version() == 2
+    assert lla.abi_version() == 3
 
 
 def test_status_strings():
@@ -234,3 +235,38 @@ def _rope_rotate(**kw):
 ])
 def test_rope_rotate_rejects(kw):
     assert _rope_rotate(**kw) == lla.LLA_ERR_INVALID_ARG
+
+
+# ---- eviction (ring slots) ----
+
+def _encode_ring(**kw):
+    a = dict(dtype=1, B=2, M=8, H=16, T=4, d=128, rk=18, rv=30, xk=P, xv=P, muk=None, muv=None, wk=P, wv=P,
+             ck=P, cv=P, n_max=320, pos0=1000, sink=4, window=256, stream=None)
+    a.update(kw)
+    return lla.lib().lla_encode_ring(a["dtype"], a["B"], a["M"], a["H"], a["T"], a["d"], a["rk"], a["rv"],
+                                     a["xk"], a["xv"], a["muk"], a["muv"], a["wk"], a["wv"], a["ck"], a["cv"],
+                                     a["n_max"], a["pos0"], a["sink"], a["window"], a["stream"])
+
+
+@pytest.mark.parametrize("kw", [
+    dict(window=0), dict(window=-1), dict(sink=-1), dict(sink=100, window=256), dict(M=257),
+    dict(pos0=-1), dict(n_max=256), dict(xk=None), dict(dtype=7),
+    dict(pos0=0, M=261),  # 257 of the 261 positions would share 256 ring slots
+])
+def test_encode_ring_rejects(kw):
+    assert _encode_ring(**kw) == lla.LLA_ERR_INVALID_ARG
+
+
+def _rope_write_ring(**kw):
+    a = dict(dtype=1, B=2, M=8, Hr=1, dr=64, x=P, base=10000.0, rc=P, n_max=320, pos0=1 << 20, sink=4,
+             window=256, stream=None)
+    a.update(kw)
+    return lla.lib().lla_rope_write_ring(a["dtype"], a["B"], a["M"], a["Hr"], a["dr"], a["x"], a["base"],
+                                         a["rc"], a["n_max"], a["pos0"], a["sink"], a["window"], a["stream"])
+
+
+@pytest.mark.parametrize("kw", [
+    dict(window=0), dict(sink=65, window=256), dict(M=300), dict(dr=12), dict(rc=None), dict(base=-2.0),
+])
+def test_rope_write_ring_rejects(kw):
+    assert _rope_write_ring(**kw) == lla.LLA_ERR_INVALID_ARG
