@@ -72,6 +72,9 @@ __all__ = [
     "ring_slot",
     "decode_attn_evict",
     "decode_attn_rope_evict",
+    "stack_loops_heads",
+    "decode_attn_2d",
+    "decode_attn_2d_batched",
 ]
 
 
@@ -467,3 +470,49 @@ def decode_attn_rope_evict(q, q_rope, c_k, c_v, k_rope, u_k, u_v, mu_k=None, mu_
                             np.asarray(c_v, dtype=np.float64)[keep],
                             np.asarray(k_rope, dtype=np.float64)[keep], u_k, u_v, mu_k, mu_v, scale, base,
                             q_pos=N - 1, k_pos=np.asarray(keep))
+
+
+# ---------------------------------------------------------------------------
+# LLA-2D (Sec. 3 "The LLA-2D variant (loop x head)"): one latent per token and
+# layer for all H heads.  The down-projection input is the full T*H*d stack,
+# and loop l, head h is reconstructed from the shared latent with its own
+# up-projection slice.
+# ---------------------------------------------------------------------------
+
+def stack_loops_heads(per_loop_head):
+    """The LLA-2D stack: x = [x_{1,1}; ...; x_{1,H}; x_{2,1}; ...; x_{T,H}],
+    loop-major then head-major (reading: Eq. 1's loop stacking, with each
+    loop's vector being all heads' K (or V) concatenated).
+    per_loop_head[t][h]: [..., d]."""
+    return np.concatenate([np.asarray(v, dtype=np.float64) for loop in per_loop_head for v in loop], axis=-1)
+
+
+def decode_attn_2d(q, c_k, c_v, u_k, u_v, mu_k=None, mu_v=None, scale=None):
+    """Loop-l decode of all H heads over one shared latent per token (plain
+    definition): head h reconstructs K_{l,h} = c_k U_{k,l,h}^T + mu_{k,l,h} and
+    V_{l,h} likewise (Eq. 3 with the (l, h) slice of W_up), then runs the
+    teacher's attention.
+
+    q: [H, d]; c_k: [N, r_k]; c_v: [N, r_v]; u_k: [H, d, r_k]; u_v: [H, d, r_v];
+    mu_k, mu_v: [H, d] or None.  Returns [H, d]."""
+    q = np.asarray(q, dtype=np.float64)
+    H = q.shape[0]
+    return np.stack([decode_attn(q[h], c_k, c_v, u_k[h], u_v[h],
+                                 None if mu_k is None else mu_k[h],
+                                 None if mu_v is None else mu_v[h], scale) for h in range(H)])
+
+
+def decode_attn_2d_batched(q, c_k, c_v, u_k, u_v, mu_k=None, mu_v=None, scale=None, ctx_len=None,
+                           batches=None):
+    """decode_attn_2d for every sequence b (or those in ``batches``).
+    q: [B, H, d]; c_k: [B, >=N, r_k]; c_v: [B, >=N, r_v].  Returns [B, H, d]."""
+    q = np.asarray(q, dtype=np.float64)
+    B, H, d = q.shape
+    if ctx_len is None:
+        ctx_len = c_k.shape[1]
+    lens = [int(ctx_len)] * B if np.ndim(ctx_len) == 0 else [int(v) for v in ctx_len]
+    out = np.full((B, H, d), np.nan)
+    for b in (range(B) if batches is None else batches):
+        n = lens[b]
+        out[b] = decode_attn_2d(q[b], c_k[b, :n], c_v[b, :n], u_k, u_v, mu_k, mu_v, scale)
+    return out
