@@ -58,7 +58,7 @@ def parse():
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--workload", default="ouro14b_decode",
-                   choices=["ouro14b_decode", "ouro26b_long", "rank_sweep", "prefill_write"])
+                   choices=["ouro14b_decode", "ouro26b_long", "rank_sweep", "prefill_write", "ouro14b_2d"])
     p.add_argument("--tier", type=int, default=None, help="rank_sweep: run only this tier index")
     p.add_argument("--evict", default=None,
                    help="SINK,WINDOW: decode workloads keep a sink + window eviction budget (ring cache of "
@@ -412,6 +412,86 @@ def run_prefill(args, torch, lla, W):
 
 
 # ---------------------------------------------------------------------------
+# LLA-2D decode (ouro14b_2d)
+# ---------------------------------------------------------------------------
+
+def decode_2d_bytes(B, H, d, N, r_k, r_v, elem=2, out_elem=4):
+    """Algorithmic bytes of one LLA-2D decode call: the shared latents (once per
+    sequence), loop-l U_k, U_v of every head, queries and fp32 outputs."""
+    return B * N * (r_k + r_v) * elem + H * d * (r_k + r_v) * elem + B * H * d * elem + B * H * d * out_elem
+
+
+def run_decode_2d(args, torch, lla, W):
+    wl = W.WORKLOADS["ouro14b_2d"]
+    r_k, r_v = wl.ranks[0]
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    n_max = wl.N + 64
+    K = wl.T * wl.H * wl.d
+    caches, writes = [], []
+    for d in range(wl.layers):
+        ck, cv = lla.alloc_cache_2d(wl.B, n_max, r_k, r_v, device=dev)
+        ck.copy_(W.normal(ck.shape, (wl.name, "c_k", d), 1.0, wl.dtype, dev))
+        cv.copy_(W.normal(cv.shape, (wl.name, "c_v", d), 1.0, wl.dtype, dev))
+        caches.append((ck, cv))
+        writes.append((W.normal((wl.B, 1, K), (wl.name, "x_k", d), 1.0, wl.dtype, dev),
+                       W.normal((wl.B, 1, K), (wl.name, "x_v", d), 1.0, wl.dtype, dev),
+                       W.normal((r_k, K), (wl.name, "Wd_k", d), 1.0 / K, wl.dtype, dev),
+                       W.normal((r_v, K), (wl.name, "Wd_v", d), 1.0 / K, wl.dtype, dev)))
+    loops = [[None] * wl.layers for _ in range(wl.T)]
+    for l in range(wl.T):
+        for d in range(wl.layers):
+            uk, uv = W.codec_loop_2d(wl, r_k, r_v, d, l, dev)
+            loops[l][d] = (W.queries(wl, d, l, device=dev), uk, uv,
+                           torch.empty((wl.B, wl.H, wl.d), dtype=torch.float32, device=dev))
+    ws = torch.empty(lla.decode_2d_workspace_bytes(wl.B, wl.H, r_k, r_v, wl.N), dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+    timer = KernelTimer(torch, stream)
+
+    def step(timed):
+        for l in range(wl.T):
+            for d in range(wl.layers):
+                q, uk, uv, out = loops[l][d]
+                ck, cv = caches[d]
+                s = timer.start() if timed else None
+                lla.decode_attn_2d(q, ck, cv, uk, uv, n_ctx=wl.N, out=out, workspace=ws)
+                if timed:
+                    timer.stop(s)
+        for d in range(wl.layers):
+            xk, xv, wk, wv = writes[d]
+            ck, cv = caches[d]
+            lla.encode_2d(xk, xv, wk, wv, ck, cv, T=wl.T, H=wl.H, pos0=wl.N)
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for _ in range(args.steps):
+        step(True)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    step_ms = t0.elapsed_time(t1) / args.steps
+    call_ms = timer.mean_ms()
+    nbytes = decode_2d_bytes(wl.B, wl.H, wl.d, wl.N, r_k, r_v)
+    gbs = nbytes / (call_ms * 1e-3) / 1e9
+    return {
+        "metric": "LLA-2D latent-cache decode attention tokens/sec and achieved HBM GB/s (% of peak)",
+        "value": round(wl.B / (step_ms * 1e-3), 2), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(step_ms, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": wl.description, "layers": wl.layers, "loops": wl.T, "heads": wl.H, "d_head": wl.d,
+                   "batch": wl.B, "context": wl.N, "r_k": r_k, "r_v": r_v, "calls_per_step": wl.T * wl.layers,
+                   "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": "absorb2d + scan2d + merge2d (lla_decode_attn_2d)", "bytes_per_launch": nbytes,
+                     "avg_launch_ms": round(call_ms, 5)},
+        "cpu_baseline": None,
+    }
+
+
+# ---------------------------------------------------------------------------
 # main
 # ---------------------------------------------------------------------------
 
@@ -441,6 +521,9 @@ def main():
 
     if args.workload == "prefill_write":
         print(json.dumps(run_prefill(args, torch, lla, W)), flush=True)
+        return
+    if args.workload == "ouro14b_2d":
+        print(json.dumps(run_decode_2d(args, torch, lla, W)), flush=True)
         return
 
     wl, results = run_decode(args, torch, lla, W)

@@ -59,10 +59,11 @@
 extern "C" {
 #endif
 
-#define LLA_ABI_VERSION 3
+#define LLA_ABI_VERSION 4
 #define LLA_PAGE_TOKENS 64
 #define LLA_MAX_RANK 512
 #define LLA_MAX_ROPE 256
+#define LLA_MAX_RANK_2D 1024
 #define LLA_MAX_SPLITS 64
 
 typedef enum lla_status {
@@ -307,6 +308,59 @@ lla_status lla_encode_ring(int dtype, int B, int M, int H, int T, int d_head, in
 lla_status lla_rope_write_ring(int dtype, int B, int M, int H_rope, int d_rope, const void* k_rope,
                                double base, void* r_cache, int n_max, int pos0, int sink,
                                int window, void* stream);
+
+/*
+ * LLA-2D (Sec. 3 "The LLA-2D variant (loop x head)"): one latent per token and
+ * layer reconstructs all H heads, (r_k + r_v) scalars per token per layer, a
+ * factor H below per-head LLA.  The down-projection input is the whole
+ * loop-major, head-major stack x = [x_{1,1}; ...; x_{1,H}; ...; x_{T,H}] of
+ * T*H*d_head values, and loop l, head h has its own up-projection slice
+ * U_{k,l,h} [d_head][r_k] (likewise U_v).
+ *
+ * Cache layouts (one sequence b of capacity n_max):
+ *   key latents   token-major: element (b, n, j) at (b*n_max + n)*r_k + j
+ *   value latents paged feature-major, as a per-head cache with H = 1:
+ *                 element (b, n, j) at (b*n_max + (n/64)*64)*r_v + j*64 + n%64
+ * Supported: bf16 only, H = 16, r_k a multiple of 32 and r_v a multiple of 16,
+ * both <= LLA_MAX_RANK_2D (else LLA_ERR_UNSUPPORTED).
+ */
+
+/*
+ * Write c = (x - mu) W_down of M new tokens per sequence into the LLA-2D
+ * caches at positions pos0 .. pos0+M-1 (Eqs. 1-2 over the T*H*d_head stack).
+ *   x_k, x_v      [B][M][T*H*d_head]
+ *   mu_k, mu_v    [T*H*d_head] or NULL
+ *   wdt_k, wdt_v  [r][T*H*d_head]  (W_down transposed)
+ *   c_k, c_v      the 2D caches (layouts above), capacity n_max
+ * Errors: LLA_ERR_INVALID_ARG, LLA_ERR_UNSUPPORTED, LLA_ERR_HIP.
+ */
+lla_status lla_encode_2d(int dtype, int B, int M, int H, int T, int d_head, int r_k, int r_v,
+                         const void* x_k, const void* x_v, const void* mu_k, const void* mu_v,
+                         const void* wdt_k, const void* wdt_v, void* c_k, void* c_v, int n_max,
+                         int pos0, void* stream);
+
+/* Workspace bytes lla_decode_attn_2d needs (the absorbed queries and the split
+ * partials).  Host only.  Errors: LLA_ERR_INVALID_ARG. */
+lla_status lla_decode_2d_workspace_bytes(int B, int H, int r_k, int r_v, int n_ctx, size_t* bytes);
+
+/*
+ * Loop-l decode of all H heads of every sequence over its shared LLA-2D latents
+ * (absorbed form of App. J applied per head): q~_h = U_{k,l,h}^T q_h, scores
+ * q~_h . c_k[n] over n < N_b, softmax, z_h = sum_n p_n c_v[n],
+ * out_h = U_{v,l,h} z_h + mu_{v,l,h}.
+ *   q    [B][H][d_head];  u_k [H][d_head][r_k];  u_v [H][d_head][r_v]
+ *   mu_k, mu_v [H][d_head] or NULL (mu_k cancels in the softmax)
+ *   out  [B][H][d_head] of out_dtype
+ *   workspace  device memory of at least lla_decode_2d_workspace_bytes (no
+ *              initial contents needed; calls sharing it must be ordered)
+ * ctx_len and n_ctx as for lla_decode_attn (NaN output for a bad length).
+ * Errors: LLA_ERR_INVALID_ARG, LLA_ERR_UNSUPPORTED, LLA_ERR_WORKSPACE, LLA_ERR_HIP.
+ */
+lla_status lla_decode_attn_2d(int dtype, int out_dtype, int B, int H, int d_head, int r_k, int r_v,
+                              int n_max, int n_ctx, const int32_t* ctx_len, const void* q,
+                              const void* c_k, const void* c_v, const void* u_k, const void* u_v,
+                              const void* mu_k, const void* mu_v, float scale, void* out,
+                              void* workspace, size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -1,0 +1,430 @@
+// LLA-2D decode (Sec. 3 "The LLA-2D variant (loop x head)"): one latent per
+// token and layer reconstructs all H heads, so the H queries of a sequence
+// share every latent read.  Absorbed form (App. J "Absorbed attention"), per
+// head h of loop l:
+//   q~_h = U_{k,l,h}^T q_h,  s_h[n] = q~_h . c_k[n],  p_h = softmax(s_h),
+//   z_h = sum_n p_h[n] c_v[n],  o_h = U_{v,l,h} z_h + mu_{v,l,h}.
+// Scores and values are two small-N GEMMs per page of 64 tokens (N = H = 16
+// heads), on v_mfma_f32_16x16x32_bf16:
+//   S^T [tokens x heads] = C_k [tokens x r_k] . Q~^T    A: 8 consecutive features of
+//                                                        one token (token-major key cache)
+//   Z^T [features x heads] += C_v^T [features x tokens] . P^T
+//                                                        A: 8 consecutive tokens of one
+//                                                        feature (paged feature-major values)
+// so both operands load straight from the caches with 16-byte loads.  In a
+// 16x16 accumulator lane (col + 16g) holds rows 4g..4g+3 of column col: the
+// column is a head, so the running max and the rescale of Z are lane-local.
+// Q~ enters as hi + lo bf16 terms (about 16 significant bits in the scores).
+//
+// Three launches: absorb (Q~ for every (b, h) into the workspace), scan (each
+// workgroup one sequence and a range of pages; 4 wavefronts each score one
+// 16-token tile of a page and each accumulate a quarter of Z's feature tiles;
+// softmax partials to the workspace), merge (per (b, h): combine the partials,
+// o = U_v z / l + mu_v).
+
+#include "lla_device.h"
+#include "lla_internal.h"
+#include "../../include/lla.h"
+
+namespace lla {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kHeads2d = 16;  // the N of every product: one column per head
+constexpr int kScanWaves = 4;
+constexpr float kLazy2d = 8.0f;  // raise the running max only when it grows by more than this (log2)
+
+__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+typedef __amdgpu_buffer_rsrc_t BufRsrc;
+__device__ __forceinline__ BufRsrc make_rsrc(const void* base, size_t bytes) {
+  const int n = bytes >= 0xffffffffull ? -1 : (int)bytes;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, n, 0x00020000);
+}
+__device__ __forceinline__ uint4 buf_ld16(BufRsrc r, int voff, int soff) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+
+// ---- absorb: Q~[b][h][j] = qscale * sum_i U_k[h][i][j] q[b][h][i] ----
+// grid (H, ceil(r_k / 64), ceil(B / 32)): a workgroup stages U_k[h][:, 64 columns]
+// and 32 queries of head h in LDS; thread (b, 8-column group) accumulates 8
+// columns and stores them as hi and lo bf16 terms ([B][2][H][r_k]), the form the
+// scan's score products take.
+constexpr int kAbsB = 32, kAbsJ = 64;
+__global__ __launch_bounds__(256) void absorb2d_kernel(Decode2dArgs a) {
+  __shared__ float s_q[kAbsB][kMaxHead + 1];
+  __shared__ __attribute__((aligned(16))) bf16_t s_u[kMaxHead][kAbsJ];
+  const int h = blockIdx.x, j0 = blockIdx.y * kAbsJ, b0 = blockIdx.z * kAbsB;
+  const int nb = min(kAbsB, a.B - b0), nj = min(kAbsJ, a.rk - j0);  // nj: a multiple of 32
+  const int d8 = a.d / 8, nj8 = nj / 8;
+  const bf16_t* q = static_cast<const bf16_t*>(a.q);
+  const bf16_t* uk = static_cast<const bf16_t*>(a.uk) + (size_t)h * a.d * a.rk + j0;
+  {
+    // 16-byte loads, all of a thread's issued before its LDS stores
+    constexpr int kQ = kAbsB * kMaxHead / 8 / 256, kU = kMaxHead * kAbsJ / 8 / 256;
+    uint4 xq[kQ], xu[kU];
+#pragma unroll
+    for (int k = 0; k < kQ; ++k) {
+      const int e = threadIdx.x + 256 * k, bb = e / d8, c = e - bb * d8;
+      xq[k] = bb < nb ? *reinterpret_cast<const uint4*>(q + ((size_t)(b0 + bb) * a.H + h) * a.d + 8 * c)
+                      : uint4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int k = 0; k < kU; ++k) {
+      const int e = threadIdx.x + 256 * k, i = e / nj8, c = e - i * nj8;
+      xu[k] = i < a.d ? *reinterpret_cast<const uint4*>(uk + (size_t)i * a.rk + 8 * c) : uint4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int k = 0; k < kQ; ++k) {
+      const int e = threadIdx.x + 256 * k, bb = e / d8, c = e - bb * d8;
+      if (bb < nb) {
+        float* dst = &s_q[bb][8 * c];
+        dst[0] = bf16_lo(xq[k].x);
+        dst[1] = bf16_hi(xq[k].x);
+        dst[2] = bf16_lo(xq[k].y);
+        dst[3] = bf16_hi(xq[k].y);
+        dst[4] = bf16_lo(xq[k].z);
+        dst[5] = bf16_hi(xq[k].z);
+        dst[6] = bf16_lo(xq[k].w);
+        dst[7] = bf16_hi(xq[k].w);
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < kU; ++k) {
+      const int e = threadIdx.x + 256 * k, i = e / nj8, c = e - i * nj8;
+      if (i < a.d) *reinterpret_cast<uint4*>(&s_u[i][8 * c]) = xu[k];
+    }
+  }
+  __syncthreads();
+  const int bb = threadIdx.x / 8, jg = (threadIdx.x % 8) * 8;
+  if (bb >= nb || jg >= nj) return;
+  float acc[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+  for (int i = 0; i < a.d; ++i) {
+    const uint4 w = *reinterpret_cast<const uint4*>(&s_u[i][jg]);
+    const float qi = s_q[bb][i];
+    acc[0] = fmaf(bf16_lo(w.x), qi, acc[0]);
+    acc[1] = fmaf(bf16_hi(w.x), qi, acc[1]);
+    acc[2] = fmaf(bf16_lo(w.y), qi, acc[2]);
+    acc[3] = fmaf(bf16_hi(w.y), qi, acc[3]);
+    acc[4] = fmaf(bf16_lo(w.z), qi, acc[4]);
+    acc[5] = fmaf(bf16_hi(w.z), qi, acc[5]);
+    acc[6] = fmaf(bf16_lo(w.w), qi, acc[6]);
+    acc[7] = fmaf(bf16_hi(w.w), qi, acc[7]);
+  }
+  uint32_t hi[4], lo[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float x0 = acc[2 * e] * a.qscale, x1 = acc[2 * e + 1] * a.qscale;
+    const __bf16 h0 = (__bf16)x0, h1 = (__bf16)x1;
+    hi[e] = (uint32_t)__builtin_bit_cast(bf16_t, h0) | ((uint32_t)__builtin_bit_cast(bf16_t, h1) << 16);
+    lo[e] = (uint32_t)__builtin_bit_cast(bf16_t, (__bf16)(x0 - (float)h0)) |
+            ((uint32_t)__builtin_bit_cast(bf16_t, (__bf16)(x1 - (float)h1)) << 16);
+  }
+  const size_t plane = (size_t)kHeads2d * a.rk;
+  bf16_t* out = a.qt + (size_t)(b0 + bb) * 2 * plane + (size_t)h * a.rk + j0 + jg;
+  *reinterpret_cast<uint4*>(out) = uint4{hi[0], hi[1], hi[2], hi[3]};
+  *reinterpret_cast<uint4*>(out + plane) = uint4{lo[0], lo[1], lo[2], lo[3]};
+}
+
+// ---- scan: one sequence b, pages [pb, pe); partials (m, l, z) per head ----
+// VT: value feature tiles (16 features each) per wavefront; KS: score K-steps of 32 features.
+template <int KS, int VT>
+__global__ __launch_bounds__(kScanWaves * kWave) __attribute__((amdgpu_waves_per_eu(4 * KS + 12 * VT <= 132 ? 3 : 2)))
+void scan2d_kernel(Decode2dArgs a) {
+  constexpr int PS = kPage + 8;  // P row stride (bf16): [head][token]
+  constexpr int QS = KS * 32 + 8;  // Q~ row stride (bf16): rows hi 0..15, lo 16..31
+  __shared__ __attribute__((aligned(16))) bf16_t s_q[2 * kHeads2d * QS];
+  __shared__ __attribute__((aligned(16))) bf16_t s_p[2][kHeads2d * PS];
+  __shared__ float s_max[kScanWaves][kHeads2d];
+  __shared__ float s_l[kScanWaves][kHeads2d];
+
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int col = lane & 15, g = lane >> 4;  // col: token row (A) / head column (B, D)
+  const int split = blockIdx.x, b = blockIdx.y;
+  const int rk = a.rk, rv = a.rv;
+  const int N = a.ctx_len ? a.ctx_len[b] : a.n_ctx;
+  const bool bad = (N < 1) || (N > a.n_ctx);
+  const int pages = bad ? 0 : (N + kPage - 1) / kPage;
+  const int per = (pages + a.splits - 1) / a.splits;
+  const int pb = min(pages, split * per), pe = min(pages, pb + per);
+
+  // Q~ of the 16 heads (hi and lo planes from the absorb launch) -> LDS
+  {
+    constexpr int kPer = (4 * KS * 32 + kScanWaves * kWave - 1) / (kScanWaves * kWave);
+    const int row8 = rk / 8, n16 = 4 * rk;  // 16-byte chunks: per row, in all 32 rows
+    const uint4* src = reinterpret_cast<const uint4*>(a.qt + (size_t)b * 2 * kHeads2d * rk);
+    uint4 x[kPer];
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      const int e = tid + k * kScanWaves * kWave;
+      x[k] = e < n16 ? src[e] : uint4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      const int e = tid + k * kScanWaves * kWave;
+      if (e < n16) {
+        const int row = e / row8;
+        *reinterpret_cast<uint4*>(&s_q[row * QS + 8 * (e - row * row8)]) = x[k];
+      }
+    }
+    // zero columns r_k .. 32 KS - 1 (the unused K-steps multiply them)
+    const int pad8 = (KS * 32 - rk) / 8;
+    for (int e = tid; e < 2 * kHeads2d * pad8; e += kScanWaves * kWave) {
+      const int row = e / pad8;
+      *reinterpret_cast<uint4*>(&s_q[row * QS + rk + 8 * (e - row * pad8)]) = uint4{0, 0, 0, 0};
+    }
+  }
+  __syncthreads();
+
+  // key rows: token-major [n_max][r_k]; value pages: [n_max/64][r_v][64]
+  const BufRsrc ksrc = make_rsrc(static_cast<const bf16_t*>(a.ck) + (size_t)b * a.n_max * rk,
+                                 (size_t)a.n_max * rk * 2);
+  const BufRsrc vsrc = make_rsrc(static_cast<const bf16_t*>(a.cv) + (size_t)b * a.n_max * rv,
+                                 (size_t)a.n_max * rv * 2);
+  const int vtiles = rv / 16;
+  // A fragments: keys of token 16*wave + col, features 32 s + 8 g; values of
+  // feature 16 t + col, tokens 32 u + 8 g.  The per-lane part of each address is
+  // one register; the step, tile and page parts are uniform (scalar offset).
+  const int k_lane = ((wave * 16 + col) * rk + 8 * g) * 2;
+  const int v_lane = (col * kPage + 8 * g) * 2;
+  const int ks = rk / 32;  // K-steps in use (r_k is a multiple of 32)
+  // every lane issues every load (steps past r_k re-read the last one and are
+  // not multiplied), so the waits count loads exactly
+  auto kload = [&](uint4 (&kf)[KS], int page) {
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+      kf[s] = buf_ld16(ksrc, k_lane, __builtin_amdgcn_readfirstlane(page * kPage * rk * 2 + min(s, ks - 1) * 64));
+  };
+  auto vload = [&](uint4 (&vf)[VT][2], int page) {
+#pragma unroll
+    for (int t = 0; t < VT; ++t) {
+      const int tile = min(wave + kScanWaves * t, vtiles - 1);  // tiles past r_v re-read the last one
+      const int soff = __builtin_amdgcn_readfirstlane((page * rv + tile * 16) * kPage * 2);
+#pragma unroll
+      for (int u = 0; u < 2; ++u) vf[t][u] = buf_ld16(vsrc, v_lane + 64 * u, soff);
+    }
+  };
+
+  f32x4 zacc[VT];
+#pragma unroll
+  for (int t = 0; t < VT; ++t) zacc[t] = f32x4{0.f};
+  float m_run = neg_inf(), l_run = 0.f;  // of head `col` (same in all 4 lane groups)
+
+  // One page in flight per wavefront (its keys and values are loaded before
+  // its scores are computed); latency is covered by the other resident
+  // workgroups rather than by a second register set.
+  int pbuf = 0;
+  for (int p = pb; p < pe; ++p) {
+    uint4 kf[KS], vf[VT][2];
+    kload(kf, p);
+    vload(vf, p);
+    // ---- S^T tile: tokens 16 wave .. +15 of the page x 16 heads ----
+    f32x4 sc = f32x4{0.f};
+    int qo = col * QS + 8 * g;
+    asm volatile("" : "+v"(qo));  // re-read Q~ from LDS every page rather than pin it in registers
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {  // steps past r_k meet zero Q~ columns: no branch
+      const bf16x8 bq = as_bf16x8(*reinterpret_cast<const uint4*>(&s_q[qo + 32 * s]));
+      const bf16x8 bl = as_bf16x8(*reinterpret_cast<const uint4*>(&s_q[qo + kHeads2d * QS + 32 * s]));
+      sc = mfma16(as_bf16x8(kf[s]), bq, sc);
+      sc = mfma16(as_bf16x8(kf[s]), bl, sc);
+    }
+    // tokens beyond the context (the last page) score -inf
+    const int tok0 = p * kPage + wave * 16 + 4 * g;
+    float mx = neg_inf();
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      if (tok0 + r >= N) sc[r] = neg_inf();
+      mx = fmaxf(mx, sc[r]);
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+    if (lane < 16) s_max[wave][col] = mx;
+    __syncthreads();
+    float pm = fmaxf(fmaxf(s_max[0][col], s_max[1][col]), fmaxf(s_max[2][col], s_max[3][col]));
+    // lazy running max: raised on the first page and when the page exceeds it by > 2^kLazy2d
+    if (m_run == neg_inf() || pm > m_run + kLazy2d) {
+      const float alpha = m_run == neg_inf() ? 0.f : __builtin_amdgcn_exp2f(m_run - pm);
+      l_run *= alpha;
+#pragma unroll
+      for (int t = 0; t < VT; ++t) zacc[t] *= alpha;
+      m_run = pm;
+    }
+    float pr[4], ls = 0.f;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      pr[r] = __builtin_amdgcn_exp2f(sc[r] - m_run);
+      ls += pr[r];
+    }
+    ls += __shfl_xor(ls, 16, kWave);
+    ls += __shfl_xor(ls, 32, kWave);
+    l_run += ls;  // this wave's 16 tokens; the 4 waves' sums are added at the end
+    {
+      uint2 w;
+      w.x = (uint32_t)__builtin_bit_cast(bf16_t, (__bf16)pr[0]) | ((uint32_t)__builtin_bit_cast(bf16_t, (__bf16)pr[1]) << 16);
+      w.y = (uint32_t)__builtin_bit_cast(bf16_t, (__bf16)pr[2]) | ((uint32_t)__builtin_bit_cast(bf16_t, (__bf16)pr[3]) << 16);
+      *reinterpret_cast<uint2*>(&s_p[pbuf][col * PS + wave * 16 + 4 * g]) = w;
+    }
+    __syncthreads();
+    // ---- Z^T += C_v^T P^T for this wave's feature tiles ----
+    // Branch-free: value slots past the context may hold anything, so the
+    // tokens at or beyond N are masked to zero (all-ones masks before the last
+    // page); tiles past r_v are multiplied too and never stored.
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const bf16x8 bp = as_bf16x8(*reinterpret_cast<const uint4*>(&s_p[pbuf][col * PS + 32 * u + 8 * g]));
+      const int nv = N - (p * kPage + 32 * u + 8 * g);
+      uint32_t keep[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) keep[i] = nv > 2 * i + 1 ? 0xffffffffu : nv > 2 * i ? 0x0000ffffu : 0u;
+#pragma unroll
+      for (int t = 0; t < VT; ++t) {
+        const uint4 v = uint4{vf[t][u].x & keep[0], vf[t][u].y & keep[1], vf[t][u].z & keep[2], vf[t][u].w & keep[3]};
+        zacc[t] = mfma16(as_bf16x8(v), bp, zacc[t]);
+      }
+    }
+    pbuf ^= 1;
+  }
+
+  // ---- partials: m, l (summed over the 4 waves), z of this wave's tiles ----
+  if (lane < 16) s_l[wave][col] = l_run;
+  __syncthreads();
+  const size_t pbase = (((size_t)b * a.splits + split) * kHeads2d + col) * (size_t)(rv + 2);
+  if (wave == 0 && lane < 16) {
+    a.part[pbase] = m_run;
+    a.part[pbase + 1] = s_l[0][col] + s_l[1][col] + s_l[2][col] + s_l[3][col];
+  }
+#pragma unroll
+  for (int t = 0; t < VT; ++t) {
+    const int tile = wave + kScanWaves * t;
+    if (tile < vtiles) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) a.part[pbase + 2 + tile * 16 + 4 * g + r] = zacc[t][r];
+    }
+  }
+}
+
+// ---- merge: per (b, h), combine the splits and apply U_v ----
+__global__ __launch_bounds__(256) void merge2d_kernel(Decode2dArgs a) {
+  __shared__ float s_z[LLA_MAX_RANK_2D];
+  __shared__ float s_w[LLA_MAX_SPLITS];
+  __shared__ float s_inv;
+  const int h = blockIdx.x, b = blockIdx.y, rv = a.rv;
+  const int N = a.ctx_len ? a.ctx_len[b] : a.n_ctx;
+  const bool bad = (N < 1) || (N > a.n_ctx);
+  const float* part = a.part + ((size_t)b * a.splits * kHeads2d + h) * (size_t)(rv + 2);
+  const size_t sstride = (size_t)kHeads2d * (rv + 2);
+  if (threadIdx.x < kWave) {  // one wavefront: lane s reads split s (splits <= 64)
+    const int s = threadIdx.x;
+    const float ms = s < a.splits ? part[s * sstride] : neg_inf();
+    const float ls = s < a.splits ? part[s * sstride + 1] : 0.f;
+    float m = ms;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) m = fmaxf(m, __shfl_xor(m, off, kWave));
+    const float w = ms == neg_inf() ? 0.f : __builtin_amdgcn_exp2f(ms - m);
+    float l = w * ls;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) l += __shfl_xor(l, off, kWave);
+    if (s < a.splits) s_w[s] = w;
+    if (s == 0) s_inv = 1.0f / l;
+  }
+  __syncthreads();
+  for (int j = threadIdx.x; j < rv; j += 256) {
+    float z = 0.f;
+    for (int s0 = 0; s0 < a.splits; s0 += 16) {  // 16 partials in flight at a time
+      float v[16];
+#pragma unroll
+      for (int k = 0; k < 16; ++k) v[k] = s0 + k < a.splits ? part[(s0 + k) * sstride + 2 + j] : 0.f;
+#pragma unroll
+      for (int k = 0; k < 16; ++k)
+        if (s0 + k < a.splits) z = fmaf(s_w[s0 + k], v[k], z);
+    }
+    s_z[j] = z * s_inv;
+  }
+  __syncthreads();
+  const bf16_t* uv = static_cast<const bf16_t*>(a.uv) + (size_t)h * a.d * rv;
+  const bf16_t* muv = a.muv ? static_cast<const bf16_t*>(a.muv) + (size_t)h * a.d : nullptr;
+  // 4 threads per output row, each a quarter of the row, combined by shuffles
+  const int i = threadIdx.x / 4, part4 = threadIdx.x % 4;
+  for (int i0 = 0; i0 < a.d; i0 += 64) {
+    const int row = i0 + i;
+    float acc = 0.f;
+    if (row < a.d) {
+      const uint4* ur = reinterpret_cast<const uint4*>(uv + (size_t)row * rv);
+      const int n8 = rv / 8;
+      for (int c0 = part4; c0 < n8; c0 += 32) {  // 8 row chunks in flight at a time
+        uint4 w[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) w[k] = c0 + 4 * k < n8 ? ur[c0 + 4 * k] : uint4{0, 0, 0, 0};
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const int j = 8 * min(c0 + 4 * k, n8 - 1);  // chunks past the row are zero
+          acc = fmaf(bf16_lo(w[k].x), s_z[j], acc);
+          acc = fmaf(bf16_hi(w[k].x), s_z[j + 1], acc);
+          acc = fmaf(bf16_lo(w[k].y), s_z[j + 2], acc);
+          acc = fmaf(bf16_hi(w[k].y), s_z[j + 3], acc);
+          acc = fmaf(bf16_lo(w[k].z), s_z[j + 4], acc);
+          acc = fmaf(bf16_hi(w[k].z), s_z[j + 5], acc);
+          acc = fmaf(bf16_lo(w[k].w), s_z[j + 6], acc);
+          acc = fmaf(bf16_hi(w[k].w), s_z[j + 7], acc);
+        }
+      }
+    }
+    acc += __shfl_xor(acc, 1, kWave);
+    acc += __shfl_xor(acc, 2, kWave);
+    if (row < a.d && part4 == 0) {
+      float v = acc + (muv ? bf16_to_f32(muv[row]) : 0.f);
+      if (bad) v = __builtin_nanf("");
+      const size_t o = ((size_t)b * a.H + h) * a.d + row;
+      if (a.out_dtype == LLA_F32)
+        static_cast<float*>(a.out)[o] = v;
+      else
+        static_cast<bf16_t*>(a.out)[o] = f32_to_bf16(v);
+    }
+  }
+}
+
+template <int KS, int VT>
+void launch_scan(const Decode2dArgs& a, hipStream_t stream) {
+  hipLaunchKernelGGL((scan2d_kernel<KS, VT>), dim3(a.splits, a.B), dim3(kScanWaves * kWave), 0, stream, a);
+}
+
+}  // namespace
+
+int decode_2d_splits(int B, int n_ctx) {
+  const int pages = (n_ctx + kPage - 1) / kPage;
+  int s = (2 * device_cu_count() + B - 1) / B;  // about two workgroups per compute unit
+  if (s > pages) s = pages;
+  if (s > LLA_MAX_SPLITS) s = LLA_MAX_SPLITS;
+  return s < 1 ? 1 : s;
+}
+
+hipError_t launch_decode_2d(const Decode2dArgs& a, hipStream_t stream) {
+  hipLaunchKernelGGL(absorb2d_kernel, dim3(a.H, (a.rk + kAbsJ - 1) / kAbsJ, (a.B + kAbsB - 1) / kAbsB),
+                     dim3(256), 0, stream, a);
+  // K-steps of 32 key features; value tiles of 16 features spread over the 4 wavefronts
+  const int ks = a.rk / 32, vt = (a.rv / 16 + kScanWaves - 1) / kScanWaves;
+  const int vtb = vt <= 2 ? 2 : vt <= 4 ? 4 : vt <= 8 ? 8 : 16;
+  const int ksb = ks <= 4 ? 4 : ks <= 8 ? 8 : ks == 9 ? 9 : ks <= 12 ? 12 : ks <= 16 ? 16 : 32;
+#define LLA_SCAN(K, V) \
+  if (ksb == K && vtb == V) launch_scan<K, V>(a, stream);
+  LLA_SCAN(4, 2) LLA_SCAN(4, 4) LLA_SCAN(4, 8) LLA_SCAN(4, 16)
+  LLA_SCAN(8, 2) LLA_SCAN(8, 4) LLA_SCAN(8, 8) LLA_SCAN(8, 16)
+  LLA_SCAN(9, 2) LLA_SCAN(9, 4) LLA_SCAN(9, 8) LLA_SCAN(9, 16)
+  LLA_SCAN(12, 2) LLA_SCAN(12, 4) LLA_SCAN(12, 8) LLA_SCAN(12, 16)
+  LLA_SCAN(16, 2) LLA_SCAN(16, 4) LLA_SCAN(16, 8) LLA_SCAN(16, 16)
+  LLA_SCAN(32, 2) LLA_SCAN(32, 4) LLA_SCAN(32, 8) LLA_SCAN(32, 16)
+#undef LLA_SCAN
+  hipLaunchKernelGGL(merge2d_kernel, dim3(a.H, a.B), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace lla

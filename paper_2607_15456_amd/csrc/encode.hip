@@ -31,9 +31,11 @@ __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast
 template <typename T>
 __device__ __forceinline__ T pick(const T (&v)[2], int axis) { return axis ? v[1] : v[0]; }
 
-// Cache index of (b, h, position pos, feature row) in the paged layout.
+// Cache index of (b, h, slot pos, feature row): the paged feature-major layout,
+// or (tm, the LLA-2D key cache) token-major rows of r features.
 __device__ __forceinline__ size_t cache_index(int b, int h, int H, int n_max, int r, int pos,
-                                              int row) {
+                                              int row, bool tm = false) {
+  if (tm) return ((size_t)(b * H + h) * n_max + pos) * r + row;
   return ((size_t)(b * H + h) * n_max + (size_t)(pos / kPage) * kPage) * r + (size_t)row * kPage +
          (pos % kPage);
 }
@@ -154,7 +156,7 @@ __global__ __launch_bounds__(256) void encode_bf16_kernel(EncodeArgs a, int head
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
               const int rr = rt * 16 + 4 * lg + e;
-              if (rr < r) c[cache_index(b, h, H, a.n_max, r, pos, rr)] = f32_to_bf16(acc[u][e] - accm[u][e]);
+              if (rr < r) c[cache_index(b, h, H, a.n_max, r, pos, rr, axis == 0 && a.k_token_major)] = f32_to_bf16(acc[u][e] - accm[u][e]);
             }
           }
           acc[u] = accm[u] = f32x4{0.f};
@@ -252,7 +254,7 @@ __global__ __launch_bounds__(256) void encode_stream_kernel(EncodeArgs a, int bl
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int rr = rt * 16 + 4 * lg + e;
-          if (rr < r) cout[cache_index(b, h, H, a.n_max, r, pos, rr)] = f32_to_bf16(acc[e] - bmu[e]);
+          if (rr < r) cout[cache_index(b, h, H, a.n_max, r, pos, rr, axis == 0 && a.k_token_major)] = f32_to_bf16(acc[e] - bmu[e]);
         }
       }
     }
@@ -310,7 +312,7 @@ __global__ __launch_bounds__(256) void encode_few_kernel(EncodeArgs a, int nrc_k
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int rr = rc * 32 + (wave & 1) * 16 + 4 * lg + e;
-      if (rr < r) c[cache_index(b, h, H, a.n_max, r, pos, rr)] = f32_to_bf16(acc[e] - accm[e]);
+      if (rr < r) c[cache_index(b, h, H, a.n_max, r, pos, rr, axis == 0 && a.k_token_major)] = f32_to_bf16(acc[e] - accm[e]);
     }
   }
 }
@@ -345,7 +347,7 @@ __global__ __launch_bounds__(256) void encode_f32_kernel(EncodeArgs a) {
   }
   if (tok < TT && row < r) {
     const int b = tok / a.M, pos = ring_slot(a.pos0 + (tok - b * a.M), a.sink, a.window);
-    static_cast<float*>(pick(a.c, axis))[cache_index(b, h, a.H, a.n_max, r, pos, row)] = acc;
+    static_cast<float*>(pick(a.c, axis))[cache_index(b, h, a.H, a.n_max, r, pos, row, axis == 0 && a.k_token_major)] = acc;
   }
 }
 

@@ -475,4 +475,97 @@ lla_status lla_rope_rotate(int dtype, int B, int G, int M, int d_rope, const voi
   return hip_status(lla::launch_rope_rotate(a, static_cast<hipStream_t>(stream)));
 }
 
+namespace {
+bool rank2d_ok(int r_k, int r_v) {
+  return r_k % 32 == 0 && r_v % 16 == 0 && r_k <= LLA_MAX_RANK_2D && r_v <= LLA_MAX_RANK_2D;
+}
+size_t ws2d_bytes(int B, int H, int r_k, int r_v, int n_ctx) {
+  const size_t qt = ((size_t)B * 2 * H * r_k * sizeof(uint16_t) + 255) / 256 * 256;
+  return qt + (size_t)B * lla::decode_2d_splits(B, n_ctx) * H * (size_t)(r_v + 2) * sizeof(float);
+}
+}  // namespace
+
+lla_status lla_encode_2d(int dtype, int B, int M, int H, int T, int d_head, int r_k, int r_v,
+                         const void* x_k, const void* x_v, const void* mu_k, const void* mu_v,
+                         const void* wdt_k, const void* wdt_v, void* c_k, void* c_v, int n_max,
+                         int pos0, void* stream) {
+  if (!dtype_ok(dtype) || B < 1 || M < 1 || H < 1 || T < 1 || !head_ok(d_head) || r_k < 1 ||
+      r_v < 1 || !cap_ok(n_max) || pos0 < 0 || (int64_t)pos0 + M > n_max)
+    return LLA_ERR_INVALID_ARG;
+  if ((int64_t)T * H * d_head > (1 << 20) || (int64_t)B * M > (1 << 30)) return LLA_ERR_INVALID_ARG;
+  if (!ptr_ok(x_k) || !ptr_ok(x_v) || !ptr_ok(wdt_k) || !ptr_ok(wdt_v) || !ptr_ok(c_k) ||
+      !ptr_ok(c_v) || !opt_ptr_ok(mu_k) || !opt_ptr_ok(mu_v))
+    return LLA_ERR_INVALID_ARG;
+  if (dtype != LLA_BF16 || !rank2d_ok(r_k, r_v)) return LLA_ERR_UNSUPPORTED;
+  lla::EncodeArgs a{};
+  a.dtype = dtype;
+  a.B = B;
+  a.M = M;
+  a.H = 1;  // one latent per token: the whole T*H*d stack is a single "head"
+  a.K = T * H * d_head;
+  a.r[0] = r_k;
+  a.r[1] = r_v;
+  a.x[0] = x_k;
+  a.x[1] = x_v;
+  a.mu[0] = mu_k;
+  a.mu[1] = mu_v;
+  a.wdt[0] = wdt_k;
+  a.wdt[1] = wdt_v;
+  a.c[0] = c_k;
+  a.c[1] = c_v;
+  a.n_max = n_max;
+  a.pos0 = pos0;
+  a.k_token_major = 1;
+  return hip_status(lla::launch_encode(a, static_cast<hipStream_t>(stream)));
+}
+
+lla_status lla_decode_2d_workspace_bytes(int B, int H, int r_k, int r_v, int n_ctx, size_t* bytes) {
+  if (B < 1 || H < 1 || r_k < 1 || r_v < 1 || n_ctx < 1 || !bytes) return LLA_ERR_INVALID_ARG;
+  *bytes = ws2d_bytes(B, H, r_k, r_v, n_ctx);
+  return LLA_OK;
+}
+
+lla_status lla_decode_attn_2d(int dtype, int out_dtype, int B, int H, int d_head, int r_k, int r_v,
+                              int n_max, int n_ctx, const int32_t* ctx_len, const void* q,
+                              const void* c_k, const void* c_v, const void* u_k, const void* u_v,
+                              const void* mu_k, const void* mu_v, float scale, void* out,
+                              void* workspace, size_t ws_bytes, void* stream) {
+  if (!dtype_ok(dtype) || !dtype_ok(out_dtype) || B < 1 || H < 1 || !head_ok(d_head) || r_k < 1 ||
+      r_v < 1 || !cap_ok(n_max) || n_ctx < 1 || n_ctx > n_max || !std::isfinite(scale) ||
+      !(scale > 0.f))
+    return LLA_ERR_INVALID_ARG;
+  if ((int64_t)B > (1 << 20)) return LLA_ERR_INVALID_ARG;
+  if (!ptr_ok(q) || !ptr_ok(c_k) || !ptr_ok(c_v) || !ptr_ok(u_k) || !ptr_ok(u_v) || !ptr_ok(out) ||
+      !opt_ptr_ok(mu_k) || !opt_ptr_ok(mu_v) ||
+      (ctx_len && (reinterpret_cast<uintptr_t>(ctx_len) & 3u)))
+    return LLA_ERR_INVALID_ARG;
+  if (dtype != LLA_BF16 || H != 16 || !rank2d_ok(r_k, r_v)) return LLA_ERR_UNSUPPORTED;
+  if (!workspace || !aligned16(workspace) || ws_bytes < ws2d_bytes(B, H, r_k, r_v, n_ctx))
+    return LLA_ERR_WORKSPACE;
+  (void)mu_k;  // q . mu_k is constant over the context: it cancels in the softmax
+  lla::Decode2dArgs a{};
+  a.out_dtype = out_dtype;
+  a.B = B;
+  a.H = H;
+  a.d = d_head;
+  a.rk = r_k;
+  a.rv = r_v;
+  a.n_max = n_max;
+  a.n_ctx = n_ctx;
+  a.splits = lla::decode_2d_splits(B, n_ctx);
+  a.ctx_len = ctx_len;
+  a.q = q;
+  a.ck = c_k;
+  a.cv = c_v;
+  a.uk = u_k;
+  a.uv = u_v;
+  a.muv = mu_v;
+  a.qscale = (float)((double)scale * kLog2e);
+  a.out = out;
+  a.qt = static_cast<uint16_t*>(workspace);
+  a.part = reinterpret_cast<float*>(static_cast<char*>(workspace) +
+                                    ((size_t)B * 2 * H * r_k * sizeof(uint16_t) + 255) / 256 * 256);
+  return hip_status(lla::launch_decode_2d(a, static_cast<hipStream_t>(stream)));
+}
+
 }  // extern "C"

@@ -47,9 +47,30 @@ struct EncodeArgs {
   void* c[2];
   int n_max, pos0;
   int sink, window;  // eviction budget: position p goes to slot ring_slot(p) (window 0: slot p)
+  int k_token_major;  // 1: the K latents are written token-major (the LLA-2D key cache)
 };
 
 hipError_t launch_encode(const EncodeArgs& a, hipStream_t stream);
+
+// LLA-2D decode: one latent per token for all heads.
+struct Decode2dArgs {
+  int out_dtype;
+  int B, H, d, rk, rv, n_max, n_ctx, splits;
+  const int32_t* ctx_len;
+  const void* q;   // [B][H][d]
+  const void* ck;  // [B][n_max][rk] token-major
+  const void* cv;  // [B][n_max/64][rv][64] paged feature-major
+  const void* uk;  // [H][d][rk]
+  const void* uv;  // [H][d][rv]
+  const void* muv; // [H][d] or null
+  float qscale;    // scale * log2(e)
+  void* out;       // [B][H][d]
+  uint16_t* qt;    // workspace: [B][2][H][rk] absorbed queries (scaled), hi and lo bf16 planes
+  float* part;     // workspace: [B][splits][H][rv + 2] partials (m, l, z)
+};
+
+hipError_t launch_decode_2d(const Decode2dArgs& a, hipStream_t stream);
+int decode_2d_splits(int B, int n_ctx);  // split count the launch uses (also sizes the workspace)
 
 struct PrefillArgs {
   int out_dtype;

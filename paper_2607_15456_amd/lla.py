@@ -47,6 +47,9 @@ _SIGS = {
     "lla_prefill_attn_rope": (_c_int, [_c_int] * 12 + [_c_vp] * 9 + [_c_f, _c_vp, _c_vp]),
     "lla_encode_ring": (_c_int, [_c_int] * 8 + [_c_vp] * 8 + [_c_int] * 4 + [_c_vp]),
     "lla_rope_write_ring": (_c_int, [_c_int] * 5 + [_c_vp, ctypes.c_double, _c_vp] + [_c_int] * 4 + [_c_vp]),
+    "lla_encode_2d": (_c_int, [_c_int] * 8 + [_c_vp] * 8 + [_c_int, _c_int, _c_vp]),
+    "lla_decode_2d_workspace_bytes": (_c_int, [_c_int] * 5 + [ctypes.POINTER(_c_sz)]),
+    "lla_decode_attn_2d": (_c_int, [_c_int] * 9 + [_c_vp] * 8 + [_c_f, _c_vp, _c_vp, _c_sz, _c_vp]),
 }
 
 _lib = None
@@ -367,4 +370,70 @@ def rope_rotate(x, *, pos=None, pos0: int = 0, base: float = 10000.0, out=None):
             raise ValueError("out must have x's shape")
     _check(lib().lla_rope_rotate(_dt(x), B, G, M, dr, _ptr(x), _ptr(pos), pos0, float(base), _ptr(out),
                                  _stream(x)))
+    return out
+
+
+# ---------------------------------------------------------------------------
+# LLA-2D: one latent per token for all heads
+# ---------------------------------------------------------------------------
+
+def alloc_cache_2d(B, n_max, r_k, r_v, dtype=torch.bfloat16, device="cuda"):
+    """The LLA-2D caches: keys token-major [B, n_max, r_k], values paged
+    feature-major [B, n_max/64, r_v, 64]."""
+    if n_max % PAGE:
+        raise ValueError("n_max must be a multiple of 64")
+    return (torch.empty((B, n_max, r_k), dtype=dtype, device=device),
+            torch.empty((B, n_max // PAGE, r_v, PAGE), dtype=dtype, device=device))
+
+
+def encode_2d(x_k, x_v, wdt_k, wdt_v, c_k, c_v, *, T: int, H: int, pos0: int, mu_k=None, mu_v=None):
+    """LLA-2D write of M new tokens: x_k, x_v [B, M, T*H*d] (loop-major, head-major),
+    wdt_* [r, T*H*d], mu_* [T*H*d] or None; caches from alloc_cache_2d."""
+    dev = x_k.device
+    for t, n in ((x_k, "x_k"), (x_v, "x_v"), (wdt_k, "wdt_k"), (wdt_v, "wdt_v"), (c_k, "c_k"), (c_v, "c_v")):
+        _need(t, n, x_k.dtype, dev)
+    B, M, K = x_k.shape
+    if K % (T * H):
+        raise ValueError("last dim of x must be T * H * d_head")
+    r_k, r_v = wdt_k.shape[0], wdt_v.shape[0]
+    n_max = c_k.shape[1]
+    if (x_v.shape != x_k.shape or wdt_k.shape != (r_k, K) or wdt_v.shape != (r_v, K)
+            or c_k.shape != (B, n_max, r_k) or c_v.shape != (B, n_max // PAGE, r_v, PAGE)):
+        raise ValueError("inconsistent shapes")
+    _check(lib().lla_encode_2d(_dt(x_k), B, M, H, T, K // (T * H), r_k, r_v, _ptr(x_k), _ptr(x_v), _ptr(mu_k),
+                               _ptr(mu_v), _ptr(wdt_k), _ptr(wdt_v), _ptr(c_k), _ptr(c_v), n_max, pos0,
+                               _stream(x_k)))
+
+
+def decode_2d_workspace_bytes(B: int, H: int, r_k: int, r_v: int, n_ctx: int) -> int:
+    out = _c_sz()
+    _check(lib().lla_decode_2d_workspace_bytes(B, H, r_k, r_v, n_ctx, ctypes.byref(out)))
+    return out.value
+
+
+def decode_attn_2d(q, c_k, c_v, u_k, u_v, *, n_ctx: int, ctx_len=None, mu_k=None, mu_v=None,
+                   scale: float | None = None, out=None, out_dtype=torch.float32, workspace=None):
+    """LLA-2D loop-l decode of q [B, H, d] over the shared latents (caches from
+    alloc_cache_2d); u_k [H, d, r_k], u_v [H, d, r_v].  Returns out [B, H, d]."""
+    dev = q.device
+    B, H, d = q.shape
+    for t, n in ((q, "q"), (c_k, "c_k"), (c_v, "c_v"), (u_k, "u_k"), (u_v, "u_v")):
+        _need(t, n, q.dtype, dev)
+    r_k, r_v = u_k.shape[2], u_v.shape[2]
+    n_max = c_k.shape[1]
+    if (c_k.shape != (B, n_max, r_k) or c_v.shape != (B, n_max // PAGE, r_v, PAGE)
+            or u_k.shape != (H, d, r_k) or u_v.shape != (H, d, r_v)):
+        raise ValueError("inconsistent shapes")
+    if ctx_len is not None:
+        _need(ctx_len, "ctx_len", torch.int32, dev)
+    if out is None:
+        out = torch.empty((B, H, d), dtype=out_dtype, device=dev)
+    if workspace is None:
+        workspace = torch.empty(decode_2d_workspace_bytes(B, H, r_k, r_v, n_ctx), dtype=torch.uint8, device=dev)
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    _check(lib().lla_decode_attn_2d(_dt(q), _out_code(out.dtype), B, H, d, r_k, r_v, n_max, n_ctx,
+                                    _ptr(ctx_len), _ptr(q), _ptr(c_k), _ptr(c_v), _ptr(u_k), _ptr(u_v),
+                                    _ptr(mu_k), _ptr(mu_v), float(scale), _ptr(out), _ptr(workspace),
+                                    workspace.numel() * workspace.element_size(), _stream(q)))
     return out

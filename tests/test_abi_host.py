@@ -32,14 +32,15 @@ def test_header_declares_the_boundary():
                             "lla_encode", "lla_decode_workspace_bytes", "lla_decode_attn",
                             "lla_prefill_attn", "lla_rope_write", "lla_rope_rotate",
                             "lla_decode_attn_rope", "lla_prefill_attn_rope", "lla_encode_ring",
-                            "lla_rope_write_ring"])
+                            "lla_rope_write_ring", "lla_encode_2d", "lla_decode_2d_workspace_bytes",
+                            "lla_decode_attn_2d"])
 
 
 def test_library_exports_every_declared_symbol():
     h = ctypes.CDLL(lla.LIB_PATH)
     for name in _declared():
         assert hasattr(h, name), name
-    assert lla.abi_version() == 3
+    assert lla.abi_version() == 4
 
 
 def test_status_strings():
@@ -270,3 +271,49 @@ def _rope_write_ring(**kw):
 ])
 def test_rope_write_ring_rejects(kw):
     assert _rope_write_ring(**kw) == lla.LLA_ERR_INVALID_ARG
+
+
+# ---- LLA-2D ----
+
+def _decode_2d(**kw):
+    a = dict(dtype=1, out_dtype=0, B=2, H=16, d=128, rk=288, rv=480, n_max=512, n_ctx=512, ctx_len=None,
+             q=P, ck=P, cv=P, uk=P, uv=P, muk=None, muv=None, scale=0.088, out=P, ws=P, ws_bytes=1 << 30,
+             stream=None)
+    a.update(kw)
+    return lla.lib().lla_decode_attn_2d(a["dtype"], a["out_dtype"], a["B"], a["H"], a["d"], a["rk"], a["rv"],
+                                        a["n_max"], a["n_ctx"], a["ctx_len"], a["q"], a["ck"], a["cv"],
+                                        a["uk"], a["uv"], a["muk"], a["muv"], a["scale"], a["out"], a["ws"],
+                                        a["ws_bytes"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(B=0), 1), (dict(d=40), 1), (dict(n_ctx=0), 1), (dict(n_ctx=600), 1), (dict(q=None), 1),
+    (dict(ck=MIS), 1), (dict(scale=0.0), 1), (dict(dtype=0), 2), (dict(H=8), 2), (dict(rk=300), 2),
+    (dict(rv=490), 2), (dict(rk=1056), 2), (dict(ws=None, ws_bytes=0), 3), (dict(ws_bytes=64), 3),
+    (dict(ws=MIS), 3),
+])
+def test_decode_2d_rejects(kw, code):
+    assert _decode_2d(**kw) == code
+
+
+def test_decode_2d_workspace_grows_with_ranks():
+    a = lla.decode_2d_workspace_bytes(32, 16, 288, 480, 4096)
+    b = lla.decode_2d_workspace_bytes(32, 16, 576, 960, 4096)
+    assert 0 < a < b
+
+
+def _encode_2d(**kw):
+    a = dict(dtype=1, B=2, M=8, H=16, T=4, d=128, rk=288, rv=480, xk=P, xv=P, muk=None, muv=None, wk=P,
+             wv=P, ck=P, cv=P, n_max=512, pos0=0, stream=None)
+    a.update(kw)
+    return lla.lib().lla_encode_2d(a["dtype"], a["B"], a["M"], a["H"], a["T"], a["d"], a["rk"], a["rv"],
+                                   a["xk"], a["xv"], a["muk"], a["muv"], a["wk"], a["wv"], a["ck"], a["cv"],
+                                   a["n_max"], a["pos0"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(B=0), 1), (dict(pos0=510), 1), (dict(xk=MIS), 1), (dict(n_max=500), 1), (dict(dtype=0), 2),
+    (dict(rk=100), 2),
+])
+def test_encode_2d_rejects(kw, code):
+    assert _encode_2d(**kw) == code
