@@ -445,6 +445,7 @@ def run_decode_2d(args, torch, lla, W):
             loops[l][d] = (W.queries(wl, d, l, device=dev), uk, uv,
                            torch.empty((wl.B, wl.H, wl.d), dtype=torch.float32, device=dev))
     ws = torch.empty(lla.decode_2d_workspace_bytes(wl.B, wl.H, r_k, r_v, wl.N), dtype=torch.uint8, device=dev)
+    ews = lla.new_encode_2d_workspace(wl.B, 1, wl.H, wl.T, wl.d, r_k, r_v, device=dev)
     torch.cuda.synchronize()
     timer = KernelTimer(torch, stream)
 
@@ -460,7 +461,7 @@ def run_decode_2d(args, torch, lla, W):
         for d in range(wl.layers):
             xk, xv, wk, wv = writes[d]
             ck, cv = caches[d]
-            lla.encode_2d(xk, xv, wk, wv, ck, cv, T=wl.T, H=wl.H, pos0=wl.N)
+            lla.encode_2d(xk, xv, wk, wv, ck, cv, T=wl.T, H=wl.H, pos0=wl.N, workspace=ews)
 
     for _ in range(args.warmup):
         step(False)

@@ -59,7 +59,7 @@
 extern "C" {
 #endif
 
-#define LLA_ABI_VERSION 4
+#define LLA_ABI_VERSION 5
 #define LLA_PAGE_TOKENS 64
 #define LLA_MAX_RANK 512
 #define LLA_MAX_ROPE 256
@@ -332,12 +332,24 @@ lla_status lla_rope_write_ring(int dtype, int B, int M, int H_rope, int d_rope, 
  *   mu_k, mu_v    [T*H*d_head] or NULL
  *   wdt_k, wdt_v  [r][T*H*d_head]  (W_down transposed)
  *   c_k, c_v      the 2D caches (layouts above), capacity n_max
- * Errors: LLA_ERR_INVALID_ARG, LLA_ERR_UNSUPPORTED, LLA_ERR_HIP.
+ *   workspace     NULL (ws_bytes ignored), or a device buffer of ws_bytes >=
+ *                 lla_encode_2d_workspace_bytes(): with at most 64 new tokens
+ *                 and a stack of >= 2048 values, the contraction is then split
+ *                 over the stack so the weights spread over every compute
+ *                 unit (a decode step's write), in two launches that pass fp32
+ *                 partial sums through the workspace (no initial contents
+ *                 needed).  Calls that share a workspace must not overlap.
+ * Errors: LLA_ERR_INVALID_ARG, LLA_ERR_UNSUPPORTED, LLA_ERR_WORKSPACE, LLA_ERR_HIP.
  */
 lla_status lla_encode_2d(int dtype, int B, int M, int H, int T, int d_head, int r_k, int r_v,
                          const void* x_k, const void* x_v, const void* mu_k, const void* mu_v,
                          const void* wdt_k, const void* wdt_v, void* c_k, void* c_v, int n_max,
-                         int pos0, void* stream);
+                         int pos0, void* workspace, size_t ws_bytes, void* stream);
+
+/* Workspace bytes lla_encode_2d uses for M new tokens per sequence (0: the
+ * write is not split and takes no workspace).  Errors: LLA_ERR_INVALID_ARG. */
+lla_status lla_encode_2d_workspace_bytes(int B, int M, int H, int T, int d_head, int r_k, int r_v,
+                                         size_t* bytes);
 
 /* Workspace bytes lla_decode_attn_2d needs (the absorbed queries and the split
  * partials).  Host only.  Errors: LLA_ERR_INVALID_ARG. */

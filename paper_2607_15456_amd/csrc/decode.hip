@@ -470,10 +470,12 @@ void decode_kernel(DecodeArgs a) {
       part[0] = mg;
       part[1] = lg;
     }
-    // The barrier orders every thread's partial stores before thread 0's
-    // agent-scope release; the fence is cumulative, so one per workgroup
-    // publishes them all.  The last arrival's acquire (by thread 0, then the
-    // barrier) makes every split's partial visible to the whole workgroup.
+    // Every wavefront releases its own partial stores at agent scope (a
+    // workgroup barrier alone does not carry them to other compute units);
+    // thread 0's counter update then publishes the arrival, and the last
+    // arrival's acquire (by thread 0, then the barrier) makes every split's
+    // partial visible to the whole workgroup.
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
     __syncthreads();
     if (tid == 0) {
       const uint32_t prev =

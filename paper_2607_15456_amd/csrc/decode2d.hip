@@ -51,86 +51,85 @@ __device__ __forceinline__ uint4 buf_ld16(BufRsrc r, int voff, int soff) {
 }
 
 // ---- absorb: Q~[b][h][j] = qscale * sum_i U_k[h][i][j] q[b][h][i] ----
-// grid (H, ceil(r_k / 64), ceil(B / 32)): a workgroup stages U_k[h][:, 64 columns]
-// and 32 queries of head h in LDS; thread (b, 8-column group) accumulates 8
-// columns and stores them as hi and lo bf16 terms ([B][2][H][r_k]), the form the
-// scan's score products take.
-constexpr int kAbsB = 32, kAbsJ = 64;
+// One v_mfma_f32_32x32x16_bf16 chain per wavefront computes a 32 (features j)
+// x 32 (sequences b) tile of Q~^T over K = d:  A = U_k^T (LDS, transposed on
+// the way in), B = q rows (16-byte global loads).  A 32x32 accumulator gives
+// lane (c + 32 g), register r the element [8 (r/4) + 4 g + r%4][c], so each
+// lane stores runs of 4 consecutive features of one sequence.  Outputs are
+// stored as hi and lo bf16 terms ([B][2][H][r_k]), the form the scan takes.
+// grid (H, ceil(r_k / 128), ceil(B / 32)); wavefront w covers features
+// 128 blockIdx.y + 32 w.
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+constexpr int kAbsJ = 128, kAbsB = 32;
 __global__ __launch_bounds__(256) void absorb2d_kernel(Decode2dArgs a) {
-  __shared__ float s_q[kAbsB][kMaxHead + 1];
-  __shared__ __attribute__((aligned(16))) bf16_t s_u[kMaxHead][kAbsJ];
+  constexpr int US = kMaxHead + 8;  // transposed U_k row stride (bf16)
+  __shared__ __attribute__((aligned(16))) bf16_t s_ut[kAbsJ * US];
   const int h = blockIdx.x, j0 = blockIdx.y * kAbsJ, b0 = blockIdx.z * kAbsB;
-  const int nb = min(kAbsB, a.B - b0), nj = min(kAbsJ, a.rk - j0);  // nj: a multiple of 32
-  const int d8 = a.d / 8, nj8 = nj / 8;
-  const bf16_t* q = static_cast<const bf16_t*>(a.q);
-  const bf16_t* uk = static_cast<const bf16_t*>(a.uk) + (size_t)h * a.d * a.rk + j0;
-  {
-    // 16-byte loads, all of a thread's issued before its LDS stores
-    constexpr int kQ = kAbsB * kMaxHead / 8 / 256, kU = kMaxHead * kAbsJ / 8 / 256;
-    uint4 xq[kQ], xu[kU];
+  const int d = a.d, rk = a.rk, nj = min(kAbsJ, rk - j0);  // nj: a multiple of 32
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  const int c = lane & 31, g = lane >> 5;
+  const bf16_t* uk = static_cast<const bf16_t*>(a.uk) + (size_t)h * d * rk + j0;
+  const bf16_t* qrow = static_cast<const bf16_t*>(a.q) + ((size_t)(b0 + c) * a.H + h) * d;
+  const bool q_ok = b0 + c < a.B;
+  // U_k[h][2p .. 2p+1][j0 + 8c .. +7] -> s_ut[8c + x][2p .. 2p+1] as one dword per
+  // x; item e = (c, p) with p fastest, so a wavefront's LDS writes fall on
+  // consecutive dwords.  All loads first.
+  constexpr int kU = kMaxHead / 2 * kAbsJ / 8 / 256;
+  const int np = d / 2, nitems = np * (nj / 8);
+  uint4 xu[kU][2];
 #pragma unroll
-    for (int k = 0; k < kQ; ++k) {
-      const int e = threadIdx.x + 256 * k, bb = e / d8, c = e - bb * d8;
-      xq[k] = bb < nb ? *reinterpret_cast<const uint4*>(q + ((size_t)(b0 + bb) * a.H + h) * a.d + 8 * c)
-                      : uint4{0, 0, 0, 0};
-    }
+  for (int k = 0; k < kU; ++k) {
+    const int e = tid + 256 * k, c = e / np, p = e - c * np;
+    const bf16_t* src = uk + (size_t)(2 * p) * rk + 8 * c;
+    xu[k][0] = e < nitems ? *reinterpret_cast<const uint4*>(src) : uint4{0, 0, 0, 0};
+    xu[k][1] = e < nitems ? *reinterpret_cast<const uint4*>(src + rk) : uint4{0, 0, 0, 0};
+  }
+  uint4 xq[kMaxHead / 16];  // B fragments: q[b][16 t + 8 g .. +7]
 #pragma unroll
-    for (int k = 0; k < kU; ++k) {
-      const int e = threadIdx.x + 256 * k, i = e / nj8, c = e - i * nj8;
-      xu[k] = i < a.d ? *reinterpret_cast<const uint4*>(uk + (size_t)i * a.rk + 8 * c) : uint4{0, 0, 0, 0};
-    }
+  for (int t = 0; t < kMaxHead / 16; ++t)
+    xq[t] = (q_ok && 16 * t < d) ? *reinterpret_cast<const uint4*>(qrow + 16 * t + 8 * g) : uint4{0, 0, 0, 0};
 #pragma unroll
-    for (int k = 0; k < kQ; ++k) {
-      const int e = threadIdx.x + 256 * k, bb = e / d8, c = e - bb * d8;
-      if (bb < nb) {
-        float* dst = &s_q[bb][8 * c];
-        dst[0] = bf16_lo(xq[k].x);
-        dst[1] = bf16_hi(xq[k].x);
-        dst[2] = bf16_lo(xq[k].y);
-        dst[3] = bf16_hi(xq[k].y);
-        dst[4] = bf16_lo(xq[k].z);
-        dst[5] = bf16_hi(xq[k].z);
-        dst[6] = bf16_lo(xq[k].w);
-        dst[7] = bf16_hi(xq[k].w);
+  for (int k = 0; k < kU; ++k) {
+    const int e = tid + 256 * k, c = e / np, p = e - c * np;
+    if (e < nitems) {
+      const uint32_t r0[4] = {xu[k][0].x, xu[k][0].y, xu[k][0].z, xu[k][0].w};
+      const uint32_t r1[4] = {xu[k][1].x, xu[k][1].y, xu[k][1].z, xu[k][1].w};
+      uint32_t* dst = reinterpret_cast<uint32_t*>(s_ut) + (8 * c) * (US / 2) + p;
+#pragma unroll
+      for (int x = 0; x < 4; ++x) {
+        dst[(2 * x) * (US / 2)] = (r0[x] & 0xffffu) | (r1[x] << 16);
+        dst[(2 * x + 1) * (US / 2)] = (r0[x] >> 16) | (r1[x] & 0xffff0000u);
       }
-    }
-#pragma unroll
-    for (int k = 0; k < kU; ++k) {
-      const int e = threadIdx.x + 256 * k, i = e / nj8, c = e - i * nj8;
-      if (i < a.d) *reinterpret_cast<uint4*>(&s_u[i][8 * c]) = xu[k];
     }
   }
   __syncthreads();
-  const int bb = threadIdx.x / 8, jg = (threadIdx.x % 8) * 8;
-  if (bb >= nb || jg >= nj) return;
-  float acc[8];
+  if (32 * wave >= nj) return;
+  f32x16 acc = f32x16{0.f};
+  const bf16_t* ua = &s_ut[(32 * wave + c) * US + 8 * g];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) acc[e] = 0.f;
-  for (int i = 0; i < a.d; ++i) {
-    const uint4 w = *reinterpret_cast<const uint4*>(&s_u[i][jg]);
-    const float qi = s_q[bb][i];
-    acc[0] = fmaf(bf16_lo(w.x), qi, acc[0]);
-    acc[1] = fmaf(bf16_hi(w.x), qi, acc[1]);
-    acc[2] = fmaf(bf16_lo(w.y), qi, acc[2]);
-    acc[3] = fmaf(bf16_hi(w.y), qi, acc[3]);
-    acc[4] = fmaf(bf16_lo(w.z), qi, acc[4]);
-    acc[5] = fmaf(bf16_hi(w.z), qi, acc[5]);
-    acc[6] = fmaf(bf16_lo(w.w), qi, acc[6]);
-    acc[7] = fmaf(bf16_hi(w.w), qi, acc[7]);
+  for (int t = 0; t < kMaxHead / 16; ++t) {
+    if (16 * t < d) {
+      const bf16x8 av = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(ua + 16 * t));
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, __builtin_bit_cast(bf16x8, xq[t]), acc, 0, 0, 0);
+    }
   }
-  uint32_t hi[4], lo[4];
+  if (!q_ok) return;
+  const size_t plane = (size_t)kHeads2d * rk;
+  bf16_t* out = a.qt + (size_t)(b0 + c) * 2 * plane + (size_t)h * rk + j0 + 32 * wave + 4 * g;
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const float x0 = acc[2 * e] * a.qscale, x1 = acc[2 * e + 1] * a.qscale;
-    const __bf16 h0 = (__bf16)x0, h1 = (__bf16)x1;
-    hi[e] = (uint32_t)__builtin_bit_cast(bf16_t, h0) | ((uint32_t)__builtin_bit_cast(bf16_t, h1) << 16);
-    lo[e] = (uint32_t)__builtin_bit_cast(bf16_t, (__bf16)(x0 - (float)h0)) |
-            ((uint32_t)__builtin_bit_cast(bf16_t, (__bf16)(x1 - (float)h1)) << 16);
+  for (int m = 0; m < 4; ++m) {  // registers 4m .. 4m+3: features 8m + 4g .. +3
+    uint32_t hi[2], lo[2];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const float x0 = acc[4 * m + 2 * e] * a.qscale, x1 = acc[4 * m + 2 * e + 1] * a.qscale;
+      const __bf16 h0 = (__bf16)x0, h1 = (__bf16)x1;
+      hi[e] = (uint32_t)__builtin_bit_cast(bf16_t, h0) | ((uint32_t)__builtin_bit_cast(bf16_t, h1) << 16);
+      lo[e] = (uint32_t)__builtin_bit_cast(bf16_t, (__bf16)(x0 - (float)h0)) |
+              ((uint32_t)__builtin_bit_cast(bf16_t, (__bf16)(x1 - (float)h1)) << 16);
+    }
+    *reinterpret_cast<uint2*>(out + 8 * m) = uint2{hi[0], hi[1]};
+    *reinterpret_cast<uint2*>(out + plane + 8 * m) = uint2{lo[0], lo[1]};
   }
-  const size_t plane = (size_t)kHeads2d * a.rk;
-  bf16_t* out = a.qt + (size_t)(b0 + bb) * 2 * plane + (size_t)h * a.rk + j0 + jg;
-  *reinterpret_cast<uint4*>(out) = uint4{hi[0], hi[1], hi[2], hi[3]};
-  *reinterpret_cast<uint4*>(out + plane) = uint4{lo[0], lo[1], lo[2], lo[3]};
 }
 
 // ---- scan: one sequence b, pages [pb, pe); partials (m, l, z) per head ----
@@ -312,83 +311,149 @@ void scan2d_kernel(Decode2dArgs a) {
   }
 }
 
-// ---- merge: per (b, h), combine the splits and apply U_v ----
+// ---- merge: per (head h, two sequences), combine the splits and apply U_v ----
+// The loads that depend on nothing (the U_v rows this thread multiplies, the
+// split statistics, the z partials) are all issued first, so a workgroup pays
+// about one memory latency; U_v is read once for both sequences.
+// U_v layout over a wavefront: lane (r8 = lane / 8, c8 = lane % 8) takes rows
+// 8 (wave + 4 k) + r8 and 16-byte chunks c8 + 8 m, so one load instruction
+// reads 8 whole 128-byte row segments; the 8 lanes of a row add their parts
+// with three shuffles.  z feature tid + 256 m.
+constexpr int kMergeB = 1;   // sequences per workgroup
+constexpr int kMergeR = 4;   // U_v rows per thread held (d <= 128)
+constexpr int kMergeC = 8;   // U_v chunks per row and thread held (r_v <= 512)
+constexpr int kMergeM = 2;   // z features per thread held (r_v <= 512)
+constexpr int kMergeS = 16;  // splits held
 __global__ __launch_bounds__(256) void merge2d_kernel(Decode2dArgs a) {
-  __shared__ float s_z[LLA_MAX_RANK_2D];
-  __shared__ float s_w[LLA_MAX_SPLITS];
-  __shared__ float s_inv;
-  const int h = blockIdx.x, b = blockIdx.y, rv = a.rv;
-  const int N = a.ctx_len ? a.ctx_len[b] : a.n_ctx;
-  const bool bad = (N < 1) || (N > a.n_ctx);
-  const float* part = a.part + ((size_t)b * a.splits * kHeads2d + h) * (size_t)(rv + 2);
+  __shared__ float s_z[kMergeB][LLA_MAX_RANK_2D];
+  __shared__ float s_w[kMergeB][LLA_MAX_SPLITS];
+  __shared__ float s_inv[kMergeB];
+  const int h = blockIdx.x, b0 = blockIdx.y * kMergeB, rv = a.rv, d = a.d, S = a.splits;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  const int nb = min(kMergeB, a.B - b0);
   const size_t sstride = (size_t)kHeads2d * (rv + 2);
-  if (threadIdx.x < kWave) {  // one wavefront: lane s reads split s (splits <= 64)
-    const int s = threadIdx.x;
-    const float ms = s < a.splits ? part[s * sstride] : neg_inf();
-    const float ls = s < a.splits ? part[s * sstride + 1] : 0.f;
+  auto part_of = [&](int bb) { return a.part + ((size_t)(b0 + bb) * S * kHeads2d + h) * (size_t)(rv + 2); };
+  const bf16_t* uv = static_cast<const bf16_t*>(a.uv) + (size_t)h * d * rv;
+  const int n8 = rv / 8, r8 = lane >> 3, c8 = lane & 7;
+  auto row_of = [&](int k) { return 8 * (wave + 4 * k) + r8; };
+  // 1) U_v chunks
+  uint4 w[kMergeR][kMergeC];
+#pragma unroll
+  for (int k = 0; k < kMergeR; ++k)
+#pragma unroll
+    for (int m = 0; m < kMergeC; ++m) {
+      const int row = row_of(k), cj = c8 + 8 * m;
+      w[k][m] = (row < d && cj < n8) ? *reinterpret_cast<const uint4*>(uv + (size_t)row * rv + 8 * cj)
+                                     : uint4{0, 0, 0, 0};
+    }
+  // 2) split statistics: wave bb, lane s
+  float ms = neg_inf(), ls = 0.f;
+  if (wave < nb && lane < S) {
+    ms = part_of(wave)[lane * sstride];
+    ls = part_of(wave)[lane * sstride + 1];
+  }
+  // 3) z partials
+  float zp[kMergeB][kMergeM][kMergeS];
+#pragma unroll
+  for (int bb = 0; bb < kMergeB; ++bb)
+#pragma unroll
+    for (int m = 0; m < kMergeM; ++m)
+#pragma unroll
+      for (int s = 0; s < kMergeS; ++s) {
+        const int j = tid + 256 * m;
+        zp[bb][m][s] = (bb < nb && j < rv && s < S) ? part_of(bb)[s * sstride + 2 + j] : 0.f;
+      }
+  const bf16_t* muv = a.muv ? static_cast<const bf16_t*>(a.muv) + (size_t)h * d : nullptr;
+
+  // split weights of sequence `wave` (one wavefront each)
+  if (wave < nb) {
     float m = ms;
 #pragma unroll
     for (int off = 1; off < kWave; off <<= 1) m = fmaxf(m, __shfl_xor(m, off, kWave));
-    const float w = ms == neg_inf() ? 0.f : __builtin_amdgcn_exp2f(ms - m);
-    float l = w * ls;
+    const float wt = ms == neg_inf() ? 0.f : __builtin_amdgcn_exp2f(ms - m);
+    float l = wt * ls;
 #pragma unroll
     for (int off = 1; off < kWave; off <<= 1) l += __shfl_xor(l, off, kWave);
-    if (s < a.splits) s_w[s] = w;
-    if (s == 0) s_inv = 1.0f / l;
+    if (lane < S) s_w[wave][lane] = wt;
+    if (lane == 0) s_inv[wave] = 1.0f / l;
   }
   __syncthreads();
-  for (int j = threadIdx.x; j < rv; j += 256) {
-    float z = 0.f;
-    for (int s0 = 0; s0 < a.splits; s0 += 16) {  // 16 partials in flight at a time
-      float v[16];
 #pragma unroll
-      for (int k = 0; k < 16; ++k) v[k] = s0 + k < a.splits ? part[(s0 + k) * sstride + 2 + j] : 0.f;
+  for (int bb = 0; bb < kMergeB; ++bb) {
+    if (bb >= nb) break;
 #pragma unroll
-      for (int k = 0; k < 16; ++k)
-        if (s0 + k < a.splits) z = fmaf(s_w[s0 + k], v[k], z);
+    for (int m = 0; m < kMergeM; ++m) {
+      const int j = tid + 256 * m;
+      float z = 0.f;
+#pragma unroll
+      for (int s = 0; s < kMergeS; ++s)
+        if (s < S) z = fmaf(s_w[bb][s], zp[bb][m][s], z);
+      for (int s = kMergeS; s < S; ++s)
+        if (j < rv) z = fmaf(s_w[bb][s], part_of(bb)[s * sstride + 2 + j], z);
+      if (j < rv) s_z[bb][j] = z * s_inv[bb];
     }
-    s_z[j] = z * s_inv;
+    for (int j = tid + 256 * kMergeM; j < rv; j += 256) {  // r_v > 512
+      float z = 0.f;
+      for (int s = 0; s < S; ++s) z = fmaf(s_w[bb][s], part_of(bb)[s * sstride + 2 + j], z);
+      s_z[bb][j] = z * s_inv[bb];
+    }
   }
   __syncthreads();
-  const bf16_t* uv = static_cast<const bf16_t*>(a.uv) + (size_t)h * a.d * rv;
-  const bf16_t* muv = a.muv ? static_cast<const bf16_t*>(a.muv) + (size_t)h * a.d : nullptr;
-  // 4 threads per output row, each a quarter of the row, combined by shuffles
-  const int i = threadIdx.x / 4, part4 = threadIdx.x % 4;
-  for (int i0 = 0; i0 < a.d; i0 += 64) {
-    const int row = i0 + i;
-    float acc = 0.f;
-    if (row < a.d) {
-      const uint4* ur = reinterpret_cast<const uint4*>(uv + (size_t)row * rv);
-      const int n8 = rv / 8;
-      for (int c0 = part4; c0 < n8; c0 += 32) {  // 8 row chunks in flight at a time
-        uint4 w[8];
+  // o[b][row] = sum_j U_v[row][j] z[b][j] (+ mu_v)
+  auto fma8 = [&](float (&acc)[kMergeB], uint4 v, int cj) {
 #pragma unroll
-        for (int k = 0; k < 8; ++k) w[k] = c0 + 4 * k < n8 ? ur[c0 + 4 * k] : uint4{0, 0, 0, 0};
+    for (int bb = 0; bb < kMergeB; ++bb) {
+      const float* z = &s_z[bb][8 * cj];
+      float x = acc[bb];
+      x = fmaf(bf16_lo(v.x), z[0], x);
+      x = fmaf(bf16_hi(v.x), z[1], x);
+      x = fmaf(bf16_lo(v.y), z[2], x);
+      x = fmaf(bf16_hi(v.y), z[3], x);
+      x = fmaf(bf16_lo(v.z), z[4], x);
+      x = fmaf(bf16_hi(v.z), z[5], x);
+      x = fmaf(bf16_lo(v.w), z[6], x);
+      x = fmaf(bf16_hi(v.w), z[7], x);
+      acc[bb] = x;
+    }
+  };
+  auto finish = [&](float (&acc)[kMergeB], int row) {
 #pragma unroll
-        for (int k = 0; k < 8; ++k) {
-          const int j = 8 * min(c0 + 4 * k, n8 - 1);  // chunks past the row are zero
-          acc = fmaf(bf16_lo(w[k].x), s_z[j], acc);
-          acc = fmaf(bf16_hi(w[k].x), s_z[j + 1], acc);
-          acc = fmaf(bf16_lo(w[k].y), s_z[j + 2], acc);
-          acc = fmaf(bf16_hi(w[k].y), s_z[j + 3], acc);
-          acc = fmaf(bf16_lo(w[k].z), s_z[j + 4], acc);
-          acc = fmaf(bf16_hi(w[k].z), s_z[j + 5], acc);
-          acc = fmaf(bf16_lo(w[k].w), s_z[j + 6], acc);
-          acc = fmaf(bf16_hi(w[k].w), s_z[j + 7], acc);
-        }
+    for (int bb = 0; bb < kMergeB; ++bb) {
+      float x = acc[bb];
+      x += __shfl_xor(x, 1, kWave);
+      x += __shfl_xor(x, 2, kWave);
+      x += __shfl_xor(x, 4, kWave);
+      if (row < d && c8 == 0 && bb < nb) {
+        const int b = b0 + bb;
+        const int N = a.ctx_len ? a.ctx_len[b] : a.n_ctx;
+        float v = x + (muv ? bf16_to_f32(muv[row]) : 0.f);
+        if (N < 1 || N > a.n_ctx) v = __builtin_nanf("");
+        const size_t o = ((size_t)b * a.H + h) * d + row;
+        if (a.out_dtype == LLA_F32)
+          static_cast<float*>(a.out)[o] = v;
+        else
+          static_cast<bf16_t*>(a.out)[o] = f32_to_bf16(v);
       }
     }
-    acc += __shfl_xor(acc, 1, kWave);
-    acc += __shfl_xor(acc, 2, kWave);
-    if (row < a.d && part4 == 0) {
-      float v = acc + (muv ? bf16_to_f32(muv[row]) : 0.f);
-      if (bad) v = __builtin_nanf("");
-      const size_t o = ((size_t)b * a.H + h) * a.d + row;
-      if (a.out_dtype == LLA_F32)
-        static_cast<float*>(a.out)[o] = v;
-      else
-        static_cast<bf16_t*>(a.out)[o] = f32_to_bf16(v);
-    }
+  };
+#pragma unroll
+  for (int k = 0; k < kMergeR; ++k) {
+    const int row = row_of(k);
+    if (8 * (wave + 4 * k) >= d) break;  // uniform
+    float acc[kMergeB] = {};
+#pragma unroll
+    for (int m = 0; m < kMergeC; ++m)
+      if (c8 + 8 * m < n8) fma8(acc, w[k][m], c8 + 8 * m);
+    for (int cj = c8 + 8 * kMergeC; cj < n8; cj += 8)  // r_v > 512
+      if (row < d) fma8(acc, *reinterpret_cast<const uint4*>(uv + (size_t)row * rv + 8 * cj), cj);
+    finish(acc, row);
+  }
+  for (int k = kMergeR; 8 * (wave + 4 * k) < d; ++k) {  // d > 128
+    const int row = row_of(k);
+    float acc[kMergeB] = {};
+    for (int cj = c8; cj < n8; cj += 8)
+      if (row < d) fma8(acc, *reinterpret_cast<const uint4*>(uv + (size_t)row * rv + 8 * cj), cj);
+    finish(acc, row);
   }
 }
 
@@ -423,7 +488,7 @@ hipError_t launch_decode_2d(const Decode2dArgs& a, hipStream_t stream) {
   LLA_SCAN(16, 2) LLA_SCAN(16, 4) LLA_SCAN(16, 8) LLA_SCAN(16, 16)
   LLA_SCAN(32, 2) LLA_SCAN(32, 4) LLA_SCAN(32, 8) LLA_SCAN(32, 16)
 #undef LLA_SCAN
-  hipLaunchKernelGGL(merge2d_kernel, dim3(a.H, a.B), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(merge2d_kernel, dim3(a.H, (a.B + kMergeB - 1) / kMergeB), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 

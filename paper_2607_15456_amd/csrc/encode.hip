@@ -269,14 +269,19 @@ __global__ __launch_bounds__(256) void encode_stream_kernel(EncodeArgs a, int bl
 // tokens; wavefront w computes the 16x16 tile (row tile w % 2, token tile
 // w / 2) with both operands loaded straight from global memory, sixteen
 // K-steps of A and B fragments in flight at once (no LDS, no barrier).
-// grid: x = 32-token blocks, y = 32-row chunks of axis k then axis v, z = head
+// With a long K (the LLA-2D stack) the K-steps are split over ksplit
+// workgroups per tile so the weights spread over the whole machine; each
+// writes its fp32 partial tile and encode_reduce_kernel (the next launch)
+// adds them and writes the cache.
+// grid: x = 32-token blocks, y = 32-row chunks of axis k then axis v,
+// z = head * ksplit + K-split
 __global__ __launch_bounds__(256) void encode_few_kernel(EncodeArgs a, int nrc_k) {
   constexpr int CH = 16;  // K-steps per round of loads
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int axis = blockIdx.y >= (unsigned)nrc_k ? 1 : 0;
   const int rc = blockIdx.y - axis * nrc_k;
-  const int h = blockIdx.z, H = a.H, K = a.K;
+  const int split = blockIdx.z % a.ksplit, h = blockIdx.z / a.ksplit, H = a.H, K = a.K;
   const int r = pick(a.r, axis);
   const int li = lane & 15, lg = lane >> 4;
   const int row = rc * 32 + (wave & 1) * 16 + li;
@@ -287,13 +292,14 @@ __global__ __launch_bounds__(256) void encode_few_kernel(EncodeArgs a, int nrc_k
   const bf16_t* xrow = static_cast<const bf16_t*>(pick(a.x, axis)) + ((size_t)(tok_ok ? tcol : 0) * H + h) * K + 8 * lg;
   const bf16_t* mrow = pick(a.mu, axis) ? static_cast<const bf16_t*>(pick(a.mu, axis)) + (size_t)h * K + 8 * lg : nullptr;
   const uint4 zero = make_uint4(0, 0, 0, 0);
-  const int ks = K / 32;
+  const int per = (K / 32 + a.ksplit - 1) / a.ksplit;  // K-steps of this split: [sb, se)
+  const int sb = split * per, se = min(K / 32, sb + per);
   f32x4 acc = f32x4{0.f}, accm = f32x4{0.f};
-  for (int s0 = 0; s0 < ks; s0 += CH) {
+  for (int s0 = sb; s0 < se; s0 += CH) {
     bf16x8 wf[CH], xf[CH], mf[CH];
 #pragma unroll
     for (int j = 0; j < CH; ++j) {
-      const bool in = s0 + j < ks;
+      const bool in = s0 + j < se;
       wf[j] = as_bf16x8(row_ok && in ? ld16(wrow + 32 * (s0 + j)) : zero);
       xf[j] = as_bf16x8(tok_ok && in ? ld16(xrow + 32 * (s0 + j)) : zero);
       mf[j] = as_bf16x8(mrow && in ? ld16(mrow + 32 * (s0 + j)) : zero);
@@ -304,6 +310,12 @@ __global__ __launch_bounds__(256) void encode_few_kernel(EncodeArgs a, int nrc_k
       if (mrow) accm = mfma16(wf[j], mf[j], accm);
     }
   }
+  acc -= accm;
+  if (a.ksplit > 1) {  // partial tile; encode_reduce_kernel adds the splits
+    const size_t unit = ((size_t)h * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x;
+    *reinterpret_cast<f32x4*>(a.part + (unit * a.ksplit + split) * 1024 + tid * 4) = acc;
+    return;
+  }
   // output tile: lane (li, lg) holds rows 4 lg .. 4 lg + 3 of token column li
   const int t = blockIdx.x * 32 + (wave >> 1) * 16 + li;
   if (t < TT) {
@@ -312,7 +324,38 @@ __global__ __launch_bounds__(256) void encode_few_kernel(EncodeArgs a, int nrc_k
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int rr = rc * 32 + (wave & 1) * 16 + 4 * lg + e;
-      if (rr < r) c[cache_index(b, h, H, a.n_max, r, pos, rr, axis == 0 && a.k_token_major)] = f32_to_bf16(acc[e] - accm[e]);
+      if (rr < r) c[cache_index(b, h, H, a.n_max, r, pos, rr, axis == 0 && a.k_token_major)] = f32_to_bf16(acc[e]);
+    }
+  }
+}
+
+// Second launch of a split write: tile unit (grid x, y, z as the split launch
+// with z = head) adds its ksplit fp32 partials in split order and writes the
+// cache exactly as the unsplit path does.
+__global__ __launch_bounds__(256) void encode_reduce_kernel(EncodeArgs a, int nrc_k) {
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  const int axis = blockIdx.y >= (unsigned)nrc_k ? 1 : 0;
+  const int rc = blockIdx.y - axis * nrc_k;
+  const int h = blockIdx.z, H = a.H, r = pick(a.r, axis), TT = a.B * a.M;
+  const int li = lane & 15, lg = lane >> 4;
+  const size_t unit = ((size_t)h * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x;
+  const float* part = a.part + unit * a.ksplit * 1024 + tid * 4;
+  constexpr int kPre = 32;  // partials in flight at once
+  f32x4 v[kPre];
+#pragma unroll
+  for (int s = 0; s < kPre; ++s)
+    v[s] = s < a.ksplit ? *reinterpret_cast<const f32x4*>(part + (size_t)s * 1024) : f32x4{0.f};
+  f32x4 acc = f32x4{0.f};
+#pragma unroll
+  for (int s = 0; s < kPre; ++s) acc += v[s];
+  const int t = blockIdx.x * 32 + (wave >> 1) * 16 + li;
+  if (t < TT) {
+    const int b = t / a.M, pos = ring_slot(a.pos0 + (t - b * a.M), a.sink, a.window);
+    bf16_t* c = static_cast<bf16_t*>(pick(a.c, axis));
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int rr = rc * 32 + (wave & 1) * 16 + 4 * lg + e;
+      if (rr < r) c[cache_index(b, h, H, a.n_max, r, pos, rr, axis == 0 && a.k_token_major)] = f32_to_bf16(acc[e]);
     }
   }
 }
@@ -353,6 +396,19 @@ __global__ __launch_bounds__(256) void encode_f32_kernel(EncodeArgs a) {
 
 }  // namespace
 
+int encode_ksplit(int TT, int K) {
+  if (TT > 64 || K < 2048) return 1;
+  const int s = K / 512;  // 16 K-steps (one round of loads) per split
+  return s > 32 ? 32 : s;
+}
+
+size_t encode_ws_bytes(int B, int M, int H, int K, int r_k, int r_v) {
+  const int TT = B * M, ks = encode_ksplit(TT, K);
+  if (ks == 1) return 0;
+  const size_t units = (size_t)((TT + kEncTok - 1) / kEncTok) * ((r_k + 31) / 32 + (r_v + 31) / 32) * H;
+  return units * ks * 1024 * sizeof(float);
+}
+
 hipError_t launch_encode(const EncodeArgs& a, hipStream_t stream) {
   const int TT = a.B * a.M;
   const int rmax = a.r[0] > a.r[1] ? a.r[0] : a.r[1];
@@ -363,8 +419,10 @@ hipError_t launch_encode(const EncodeArgs& a, hipStream_t stream) {
     const int blocks = (TT + kEncTok - 1) / kEncTok;
     if (TT <= 64) {  // a decode step's writes: weights read once, one round of loads
       const int nrc_k = (a.r[0] + 31) / 32, nrc_v = (a.r[1] + 31) / 32;
-      dim3 grid(blocks, nrc_k + nrc_v, a.H);
+      dim3 grid(blocks, nrc_k + nrc_v, a.H * a.ksplit);
       hipLaunchKernelGGL(encode_few_kernel, grid, dim3(256), 0, stream, a, nrc_k);
+      if (a.ksplit > 1)
+        hipLaunchKernelGGL(encode_reduce_kernel, dim3(blocks, nrc_k + nrc_v, a.H), dim3(256), 0, stream, a, nrc_k);
       return hipGetLastError();
     }
     if (blocks >= 256 && rmax <= 64 && (a.K == 512 || a.K == 256)) {

@@ -203,6 +203,7 @@ lla_status encode_impl(int dtype, int B, int M, int H, int T, int d_head, int r_
   a.pos0 = pos0;
   a.sink = sink;
   a.window = window;
+  a.ksplit = 1;
   return hip_status(lla::launch_encode(a, static_cast<hipStream_t>(stream)));
 }
 
@@ -485,10 +486,19 @@ size_t ws2d_bytes(int B, int H, int r_k, int r_v, int n_ctx) {
 }
 }  // namespace
 
+lla_status lla_encode_2d_workspace_bytes(int B, int M, int H, int T, int d_head, int r_k, int r_v,
+                                         size_t* bytes) {
+  if (B < 1 || M < 1 || H < 1 || T < 1 || !head_ok(d_head) || r_k < 1 || r_v < 1 || !bytes ||
+      (int64_t)T * H * d_head > (1 << 20) || (int64_t)B * M > (1 << 30))
+    return LLA_ERR_INVALID_ARG;
+  *bytes = lla::encode_ws_bytes(B, M, 1, T * H * d_head, r_k, r_v);
+  return LLA_OK;
+}
+
 lla_status lla_encode_2d(int dtype, int B, int M, int H, int T, int d_head, int r_k, int r_v,
                          const void* x_k, const void* x_v, const void* mu_k, const void* mu_v,
                          const void* wdt_k, const void* wdt_v, void* c_k, void* c_v, int n_max,
-                         int pos0, void* stream) {
+                         int pos0, void* workspace, size_t ws_bytes, void* stream) {
   if (!dtype_ok(dtype) || B < 1 || M < 1 || H < 1 || T < 1 || !head_ok(d_head) || r_k < 1 ||
       r_v < 1 || !cap_ok(n_max) || pos0 < 0 || (int64_t)pos0 + M > n_max)
     return LLA_ERR_INVALID_ARG;
@@ -516,6 +526,13 @@ lla_status lla_encode_2d(int dtype, int B, int M, int H, int T, int d_head, int 
   a.n_max = n_max;
   a.pos0 = pos0;
   a.k_token_major = 1;
+  a.ksplit = 1;
+  const size_t need = lla::encode_ws_bytes(B, M, 1, a.K, r_k, r_v);
+  if (workspace && need > 0) {  // split the long K over the machine
+    if (!aligned16(workspace) || ws_bytes < need) return LLA_ERR_WORKSPACE;
+    a.ksplit = lla::encode_ksplit(B * M, a.K);
+    a.part = static_cast<float*>(workspace);
+  }
   return hip_status(lla::launch_encode(a, static_cast<hipStream_t>(stream)));
 }
 

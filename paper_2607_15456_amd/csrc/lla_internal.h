@@ -48,7 +48,16 @@ struct EncodeArgs {
   int n_max, pos0;
   int sink, window;  // eviction budget: position p goes to slot ring_slot(p) (window 0: slot p)
   int k_token_major;  // 1: the K latents are written token-major (the LLA-2D key cache)
+  // Few-token writes with a long K: the K range is split over ksplit
+  // workgroups per output tile (ksplit 1: no split, no workspace); part holds
+  // the fp32 partial tiles a second launch adds.
+  int ksplit;
+  float* part;
 };
+
+// Split count and workspace size of a few-token write (0 bytes: not split).
+int encode_ksplit(int TT, int K);
+size_t encode_ws_bytes(int B, int M, int H, int K, int r_k, int r_v);
 
 hipError_t launch_encode(const EncodeArgs& a, hipStream_t stream);
 

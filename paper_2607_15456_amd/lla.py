@@ -47,7 +47,8 @@ _SIGS = {
     "lla_prefill_attn_rope": (_c_int, [_c_int] * 12 + [_c_vp] * 9 + [_c_f, _c_vp, _c_vp]),
     "lla_encode_ring": (_c_int, [_c_int] * 8 + [_c_vp] * 8 + [_c_int] * 4 + [_c_vp]),
     "lla_rope_write_ring": (_c_int, [_c_int] * 5 + [_c_vp, ctypes.c_double, _c_vp] + [_c_int] * 4 + [_c_vp]),
-    "lla_encode_2d": (_c_int, [_c_int] * 8 + [_c_vp] * 8 + [_c_int, _c_int, _c_vp]),
+    "lla_encode_2d": (_c_int, [_c_int] * 8 + [_c_vp] * 8 + [_c_int, _c_int, _c_vp, _c_sz, _c_vp]),
+    "lla_encode_2d_workspace_bytes": (_c_int, [_c_int] * 7 + [ctypes.POINTER(_c_sz)]),
     "lla_decode_2d_workspace_bytes": (_c_int, [_c_int] * 5 + [ctypes.POINTER(_c_sz)]),
     "lla_decode_attn_2d": (_c_int, [_c_int] * 9 + [_c_vp] * 8 + [_c_f, _c_vp, _c_vp, _c_sz, _c_vp]),
 }
@@ -386,9 +387,25 @@ def alloc_cache_2d(B, n_max, r_k, r_v, dtype=torch.bfloat16, device="cuda"):
             torch.empty((B, n_max // PAGE, r_v, PAGE), dtype=dtype, device=device))
 
 
-def encode_2d(x_k, x_v, wdt_k, wdt_v, c_k, c_v, *, T: int, H: int, pos0: int, mu_k=None, mu_v=None):
+def encode_2d_workspace_bytes(B: int, M: int, H: int, T: int, d_head: int, r_k: int, r_v: int) -> int:
+    out = _c_sz()
+    _check(lib().lla_encode_2d_workspace_bytes(B, M, H, T, d_head, r_k, r_v, ctypes.byref(out)))
+    return out.value
+
+
+def new_encode_2d_workspace(B: int, M: int, H: int, T: int, d_head: int, r_k: int, r_v: int, device="cuda"):
+    """A workspace for encode_2d (fp32 partial sums of a split write); None when
+    the write takes none."""
+    n = encode_2d_workspace_bytes(B, M, H, T, d_head, r_k, r_v)
+    return torch.empty(n, dtype=torch.uint8, device=device) if n else None
+
+
+def encode_2d(x_k, x_v, wdt_k, wdt_v, c_k, c_v, *, T: int, H: int, pos0: int, mu_k=None, mu_v=None,
+              workspace=None):
     """LLA-2D write of M new tokens: x_k, x_v [B, M, T*H*d] (loop-major, head-major),
-    wdt_* [r, T*H*d], mu_* [T*H*d] or None; caches from alloc_cache_2d."""
+    wdt_* [r, T*H*d], mu_* [T*H*d] or None; caches from alloc_cache_2d.  workspace:
+    from new_encode_2d_workspace (splits a decode step's write over the machine)
+    or None."""
     dev = x_k.device
     for t, n in ((x_k, "x_k"), (x_v, "x_v"), (wdt_k, "wdt_k"), (wdt_v, "wdt_v"), (c_k, "c_k"), (c_v, "c_v")):
         _need(t, n, x_k.dtype, dev)
@@ -402,6 +419,7 @@ def encode_2d(x_k, x_v, wdt_k, wdt_v, c_k, c_v, *, T: int, H: int, pos0: int, mu
         raise ValueError("inconsistent shapes")
     _check(lib().lla_encode_2d(_dt(x_k), B, M, H, T, K // (T * H), r_k, r_v, _ptr(x_k), _ptr(x_v), _ptr(mu_k),
                                _ptr(mu_v), _ptr(wdt_k), _ptr(wdt_v), _ptr(c_k), _ptr(c_v), n_max, pos0,
+                               _ptr(workspace), 0 if workspace is None else workspace.numel() * workspace.element_size(),
                                _stream(x_k)))
 
 

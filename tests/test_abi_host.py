@@ -32,15 +32,15 @@ def test_header_declares_the_boundary():
                             "lla_encode", "lla_decode_workspace_bytes", "lla_decode_attn",
                             "lla_prefill_attn", "lla_rope_write", "lla_rope_rotate",
                             "lla_decode_attn_rope", "lla_prefill_attn_rope", "lla_encode_ring",
-                            "lla_rope_write_ring", "lla_encode_2d", "lla_decode_2d_workspace_bytes",
-                            "lla_decode_attn_2d"])
+                            "lla_rope_write_ring", "lla_encode_2d", "lla_encode_2d_workspace_bytes",
+                            "lla_decode_2d_workspace_bytes", "lla_decode_attn_2d"])
 
 
 def test_library_exports_every_declared_symbol():
     h = ctypes.CDLL(lla.LIB_PATH)
     for name in _declared():
         assert hasattr(h, name), name
-    assert lla.abi_version() == 4
+    assert lla.abi_version() == 5
 
 
 def test_status_strings():
@@ -304,16 +304,24 @@ def test_decode_2d_workspace_grows_with_ranks():
 
 def _encode_2d(**kw):
     a = dict(dtype=1, B=2, M=8, H=16, T=4, d=128, rk=288, rv=480, xk=P, xv=P, muk=None, muv=None, wk=P,
-             wv=P, ck=P, cv=P, n_max=512, pos0=0, stream=None)
+             wv=P, ck=P, cv=P, n_max=512, pos0=0, ws=None, ws_bytes=0, stream=None)
     a.update(kw)
     return lla.lib().lla_encode_2d(a["dtype"], a["B"], a["M"], a["H"], a["T"], a["d"], a["rk"], a["rv"],
                                    a["xk"], a["xv"], a["muk"], a["muv"], a["wk"], a["wv"], a["ck"], a["cv"],
-                                   a["n_max"], a["pos0"], a["stream"])
+                                   a["n_max"], a["pos0"], a["ws"], a["ws_bytes"], a["stream"])
 
 
 @pytest.mark.parametrize("kw,code", [
     (dict(B=0), 1), (dict(pos0=510), 1), (dict(xk=MIS), 1), (dict(n_max=500), 1), (dict(dtype=0), 2),
     (dict(rk=100), 2),
+    (dict(B=32, M=1, ws=P, ws_bytes=16), 3), (dict(B=32, M=1, ws=MIS, ws_bytes=1 << 30), 3),
 ])
 def test_encode_2d_rejects(kw, code):
     assert _encode_2d(**kw) == code
+
+
+def test_encode_2d_workspace_only_for_split_writes():
+    # a decode step's write (32 tokens, a 8192-value stack) is split; a prefill-sized one is not
+    assert lla.encode_2d_workspace_bytes(32, 1, 16, 4, 128, 288, 480) > 0
+    assert lla.encode_2d_workspace_bytes(4, 1024, 16, 4, 128, 288, 480) == 0
+    assert lla.encode_2d_workspace_bytes(32, 1, 4, 1, 64, 288, 480) == 0  # stack of 256

@@ -97,3 +97,38 @@ def test_encode_2d_then_decode(M, pos0):
         torch.cuda.synchronize()
         ref = oracle.decode_attn_2d_batched(f64(q), gk[:, :M], gv[:, :M], f64(uk), f64(uv))
         assert_close(f64(out), ref, torch.bfloat16, "encode -> decode")
+
+
+@pytest.mark.parametrize("B,M,T,d", [(32, 1, 4, 128), (5, 3, 4, 128), (33, 1, 4, 128), (64, 1, 2, 64),
+                                     (2, 1, 4, 256)])
+def test_encode_2d_split_write(B, M, T, d):
+    """A decode step's write (few tokens, a long loop x head stack): the contraction
+    is split over the stack and the fp32 partials are added by a second launch.
+    Two calls in a row on one workspace."""
+    H, r_k, r_v = 16, 288, 480
+    K = T * H * d
+    ws = lla.new_encode_2d_workspace(B, M, H, T, d, r_k, r_v, device=DEV)
+    assert ws is not None
+    n_max = 128
+    # variance 1/(16 K): latents ~ N(0, 1/8), so a one-ulp bf16 rounding flip stays below 2e-2
+    wk = W.normal((r_k, K), ("two_d", "Wd_k", K), 1.0 / (16 * K), torch.bfloat16, DEV)
+    wv = W.normal((r_v, K), ("two_d", "Wd_v", K), 1.0 / (16 * K), torch.bfloat16, DEV)
+    mu = W.normal((K,), ("two_d", "mu", K), 1.0, torch.bfloat16, DEV)
+    ck, cv = lla.alloc_cache_2d(B, n_max, r_k, r_v, device=DEV)
+    ck.fill_(7.0)
+    cv.fill_(7.0)
+    for call, pos0 in enumerate((5, 70)):
+        log(f"encode 2d split B={B} M={M} K={K} call {call}")
+        xk = W.normal((B, M, K), ("two_d", "sx_k", call), 1.0, torch.bfloat16, DEV)
+        xv = W.normal((B, M, K), ("two_d", "sx_v", call), 1.0, torch.bfloat16, DEV)
+        lla.encode_2d(xk, xv, wk, wv, ck, cv, T=T, H=H, pos0=pos0, mu_k=mu, mu_v=mu, workspace=ws)
+        torch.cuda.synchronize()
+        refk = np.stack([oracle.encode(f64(xk)[b], f64(mu), f64(wk).T) for b in range(B)])
+        refv = np.stack([oracle.encode(f64(xv)[b], f64(mu), f64(wv).T) for b in range(B)])
+        gk = f64(ck)
+        gv = f64(cv).transpose(0, 1, 3, 2).reshape(B, n_max, r_v)
+        assert_close(gk[:, pos0:pos0 + M], refk, torch.bfloat16, f"split keys call {call}", out_bf16=True)
+        assert_close(gv[:, pos0:pos0 + M], refv, torch.bfloat16, f"split values call {call}", out_bf16=True)
+    written = np.zeros(n_max, bool)
+    written[5:5 + M] = written[70:70 + M] = True
+    assert np.all(f64(ck)[:, ~written] == 7.0), "slots outside the writes changed"
