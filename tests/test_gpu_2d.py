@@ -132,3 +132,46 @@ def test_encode_2d_split_write(B, M, T, d):
     written = np.zeros(n_max, bool)
     written[5:5 + M] = written[70:70 + M] = True
     assert np.all(f64(ck)[:, ~written] == 7.0), "slots outside the writes changed"
+
+
+def test_graph_replay_matches_eager():
+    """The decode and the split write captured in a HIP graph and replayed three
+    times, with eager work in between, give the eager results bit for bit."""
+    B, T, H, d, r_k, r_v, N = 4, 4, 16, 128, 288, 480, 700
+    n_max = 768
+    K = T * H * d
+    ck = W.latents_2d(WL, r_k, "k", 2, B=B, N=N, device=DEV)
+    cv = W.latents_2d(WL, r_v, "v", 2, B=B, N=N, device=DEV)
+    kc, vc = _keys(ck, n_max), _paged_v(cv, n_max)
+    q = W.queries(WL, 2, 3, B=B, device=DEV)
+    uk, uv = W.codec_loop_2d(WL, r_k, r_v, 2, 3, DEV)
+    ws = torch.empty(lla.decode_2d_workspace_bytes(B, H, r_k, r_v, N), dtype=torch.uint8, device=DEV)
+    xk = W.normal((B, 1, K), ("two_d", "gx_k"), 1.0, torch.bfloat16, DEV)
+    xv = W.normal((B, 1, K), ("two_d", "gx_v"), 1.0, torch.bfloat16, DEV)
+    wk = W.normal((r_k, K), ("two_d", "gWd_k"), 1.0 / (16 * K), torch.bfloat16, DEV)
+    wv = W.normal((r_v, K), ("two_d", "gWd_v"), 1.0 / (16 * K), torch.bfloat16, DEV)
+    ews = lla.new_encode_2d_workspace(B, 1, H, T, d, r_k, r_v, device=DEV)
+    eager = lla.decode_attn_2d(q, kc, vc, uk, uv, n_ctx=N, workspace=ws)
+    ek, ev = lla.alloc_cache_2d(B, 128, r_k, r_v, device=DEV)
+    ek.zero_()
+    ev.zero_()
+    lla.encode_2d(xk, xv, wk, wv, ek, ev, T=T, H=H, pos0=70, workspace=ews)
+    torch.cuda.synchronize()
+    out = torch.empty_like(eager)
+    gk, gv = torch.zeros_like(ek), torch.zeros_like(ev)
+    g = torch.cuda.CUDAGraph()
+    cap = torch.cuda.Stream()
+    with torch.cuda.graph(g, stream=cap):
+        lla.decode_attn_2d(q, kc, vc, uk, uv, n_ctx=N, out=out, workspace=ws)
+        lla.encode_2d(xk, xv, wk, wv, gk, gv, T=T, H=H, pos0=70, workspace=ews)
+    for rep in range(3):
+        log(f"graph replay {rep}")
+        out.fill_(float("nan"))
+        gk.zero_()
+        gv.zero_()
+        ws.fill_(0xff)  # the workspace's contents must not matter
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, eager), f"decode replay {rep}"
+        assert torch.equal(gk, ek) and torch.equal(gv, ev), f"write replay {rep}"
