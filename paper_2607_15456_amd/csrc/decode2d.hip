@@ -133,19 +133,29 @@ __global__ __launch_bounds__(256) void absorb2d_kernel(Decode2dArgs a) {
 }
 
 // ---- scan: one sequence b, pages [pb, pe); partials (m, l, z) per head ----
+// Two page streams per workgroup: wavefronts 4 s .. 4 s + 3 (stream s) take the
+// pages pb + s, pb + s + 2, ...; each stream keeps its own softmax state and
+// the two are combined on chip at the end, so a split costs one partial.
 // VT: value feature tiles (16 features each) per wavefront; KS: score K-steps of 32 features.
+constexpr int kStreams = 2;
+constexpr int kScanThreads = kStreams * kScanWaves * kWave;
 template <int KS, int VT>
-__global__ __launch_bounds__(kScanWaves * kWave) __attribute__((amdgpu_waves_per_eu(4 * KS + 12 * VT <= 132 ? 3 : 2)))
+__global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void scan2d_kernel(Decode2dArgs a) {
   constexpr int PS = kPage + 8;  // P row stride (bf16): [head][token]
   constexpr int QS = KS * 32 + 8;  // Q~ row stride (bf16): rows hi 0..15, lo 16..31
-  __shared__ __attribute__((aligned(16))) bf16_t s_q[2 * kHeads2d * QS];
-  __shared__ __attribute__((aligned(16))) bf16_t s_p[2][kHeads2d * PS];
-  __shared__ float s_max[kScanWaves][kHeads2d];
-  __shared__ float s_l[kScanWaves][kHeads2d];
+  // Q~ during the loop; stream 1's z tiles for the final combine afterwards
+  constexpr int kQBytes = 2 * kHeads2d * QS * 2, kXBytes = kScanWaves * VT * 4 * kWave * 4;
+  __shared__ __attribute__((aligned(16))) char s_raw[kQBytes > kXBytes ? kQBytes : kXBytes];
+  __shared__ __attribute__((aligned(16))) bf16_t s_p[kStreams][2][kHeads2d * PS];
+  __shared__ float s_max[kStreams][kScanWaves][kHeads2d];
+  __shared__ float s_l[kStreams][kScanWaves][kHeads2d];
+  __shared__ float s_m1[kHeads2d];
+  bf16_t* s_q = reinterpret_cast<bf16_t*>(s_raw);
 
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int stream = wave / kScanWaves, sw = wave % kScanWaves;  // stream, wavefront in it
   const int col = lane & 15, g = lane >> 4;  // col: token row (A) / head column (B, D)
   const int split = blockIdx.x, b = blockIdx.y;
   const int rk = a.rk, rv = a.rv;
@@ -157,18 +167,18 @@ void scan2d_kernel(Decode2dArgs a) {
 
   // Q~ of the 16 heads (hi and lo planes from the absorb launch) -> LDS
   {
-    constexpr int kPer = (4 * KS * 32 + kScanWaves * kWave - 1) / (kScanWaves * kWave);
+    constexpr int kPer = (4 * KS * 32 + kScanThreads - 1) / kScanThreads;
     const int row8 = rk / 8, n16 = 4 * rk;  // 16-byte chunks: per row, in all 32 rows
     const uint4* src = reinterpret_cast<const uint4*>(a.qt + (size_t)b * 2 * kHeads2d * rk);
     uint4 x[kPer];
 #pragma unroll
     for (int k = 0; k < kPer; ++k) {
-      const int e = tid + k * kScanWaves * kWave;
+      const int e = tid + k * kScanThreads;
       x[k] = e < n16 ? src[e] : uint4{0, 0, 0, 0};
     }
 #pragma unroll
     for (int k = 0; k < kPer; ++k) {
-      const int e = tid + k * kScanWaves * kWave;
+      const int e = tid + k * kScanThreads;
       if (e < n16) {
         const int row = e / row8;
         *reinterpret_cast<uint4*>(&s_q[row * QS + 8 * (e - row * row8)]) = x[k];
@@ -176,7 +186,7 @@ void scan2d_kernel(Decode2dArgs a) {
     }
     // zero columns r_k .. 32 KS - 1 (the unused K-steps multiply them)
     const int pad8 = (KS * 32 - rk) / 8;
-    for (int e = tid; e < 2 * kHeads2d * pad8; e += kScanWaves * kWave) {
+    for (int e = tid; e < 2 * kHeads2d * pad8; e += kScanThreads) {
       const int row = e / pad8;
       *reinterpret_cast<uint4*>(&s_q[row * QS + rk + 8 * (e - row * pad8)]) = uint4{0, 0, 0, 0};
     }
@@ -189,10 +199,10 @@ void scan2d_kernel(Decode2dArgs a) {
   const BufRsrc vsrc = make_rsrc(static_cast<const bf16_t*>(a.cv) + (size_t)b * a.n_max * rv,
                                  (size_t)a.n_max * rv * 2);
   const int vtiles = rv / 16;
-  // A fragments: keys of token 16*wave + col, features 32 s + 8 g; values of
+  // A fragments: keys of token 16*sw + col, features 32 s + 8 g; values of
   // feature 16 t + col, tokens 32 u + 8 g.  The per-lane part of each address is
   // one register; the step, tile and page parts are uniform (scalar offset).
-  const int k_lane = ((wave * 16 + col) * rk + 8 * g) * 2;
+  const int k_lane = ((sw * 16 + col) * rk + 8 * g) * 2;
   const int v_lane = (col * kPage + 8 * g) * 2;
   const int ks = rk / 32;  // K-steps in use (r_k is a multiple of 32)
   // every lane issues every load (steps past r_k re-read the last one and are
@@ -205,7 +215,7 @@ void scan2d_kernel(Decode2dArgs a) {
   auto vload = [&](uint4 (&vf)[VT][2], int page) {
 #pragma unroll
     for (int t = 0; t < VT; ++t) {
-      const int tile = min(wave + kScanWaves * t, vtiles - 1);  // tiles past r_v re-read the last one
+      const int tile = min(sw + kScanWaves * t, vtiles - 1);  // tiles past r_v re-read the last one
       const int soff = __builtin_amdgcn_readfirstlane((page * rv + tile * 16) * kPage * 2);
 #pragma unroll
       for (int u = 0; u < 2; ++u) vf[t][u] = buf_ld16(vsrc, v_lane + 64 * u, soff);
@@ -218,95 +228,119 @@ void scan2d_kernel(Decode2dArgs a) {
   float m_run = neg_inf(), l_run = 0.f;  // of head `col` (same in all 4 lane groups)
 
   // One page in flight per wavefront (its keys and values are loaded before
-  // its scores are computed); latency is covered by the other resident
-  // workgroups rather than by a second register set.
+  // its scores are computed); the other stream and the other resident
+  // workgroups cover the latency.  A stream without a page this round still
+  // meets the barriers.
   int pbuf = 0;
-  for (int p = pb; p < pe; ++p) {
+  const int rounds = (pe - pb + kStreams - 1) / kStreams;
+  for (int it = 0; it < rounds; ++it) {
+    const int p = pb + kStreams * it + stream;
+    const bool act = p < pe;  // uniform over the stream
     uint4 kf[KS], vf[VT][2];
-    kload(kf, p);
-    vload(vf, p);
-    // ---- S^T tile: tokens 16 wave .. +15 of the page x 16 heads ----
     f32x4 sc = f32x4{0.f};
-    int qo = col * QS + 8 * g;
-    asm volatile("" : "+v"(qo));  // re-read Q~ from LDS every page rather than pin it in registers
+    if (act) {
+      kload(kf, p);
+      vload(vf, p);
+      // ---- S^T tile: tokens 16 sw .. +15 of the page x 16 heads ----
+      int qo = col * QS + 8 * g;
+      asm volatile("" : "+v"(qo));  // re-read Q~ from LDS every page rather than pin it in registers
 #pragma unroll
-    for (int s = 0; s < KS; ++s) {  // steps past r_k meet zero Q~ columns: no branch
-      const bf16x8 bq = as_bf16x8(*reinterpret_cast<const uint4*>(&s_q[qo + 32 * s]));
-      const bf16x8 bl = as_bf16x8(*reinterpret_cast<const uint4*>(&s_q[qo + kHeads2d * QS + 32 * s]));
-      sc = mfma16(as_bf16x8(kf[s]), bq, sc);
-      sc = mfma16(as_bf16x8(kf[s]), bl, sc);
-    }
-    // tokens beyond the context (the last page) score -inf
-    const int tok0 = p * kPage + wave * 16 + 4 * g;
-    float mx = neg_inf();
+      for (int s = 0; s < KS; ++s) {  // steps past r_k meet zero Q~ columns: no branch
+        const bf16x8 bq = as_bf16x8(*reinterpret_cast<const uint4*>(&s_q[qo + 32 * s]));
+        const bf16x8 bl = as_bf16x8(*reinterpret_cast<const uint4*>(&s_q[qo + kHeads2d * QS + 32 * s]));
+        sc = mfma16(as_bf16x8(kf[s]), bq, sc);
+        sc = mfma16(as_bf16x8(kf[s]), bl, sc);
+      }
+      // tokens beyond the context (the last page) score -inf
+      const int tok0 = p * kPage + sw * 16 + 4 * g;
+      float mx = neg_inf();
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      if (tok0 + r >= N) sc[r] = neg_inf();
-      mx = fmaxf(mx, sc[r]);
+      for (int r = 0; r < 4; ++r) {
+        if (tok0 + r >= N) sc[r] = neg_inf();
+        mx = fmaxf(mx, sc[r]);
+      }
+      mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+      if (lane < 16) s_max[stream][sw][col] = mx;
     }
-    mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-    if (lane < 16) s_max[wave][col] = mx;
     __syncthreads();
-    float pm = fmaxf(fmaxf(s_max[0][col], s_max[1][col]), fmaxf(s_max[2][col], s_max[3][col]));
-    // lazy running max: raised on the first page and when the page exceeds it by > 2^kLazy2d
-    if (m_run == neg_inf() || pm > m_run + kLazy2d) {
-      const float alpha = m_run == neg_inf() ? 0.f : __builtin_amdgcn_exp2f(m_run - pm);
-      l_run *= alpha;
+    if (act) {
+      const float pm = fmaxf(fmaxf(s_max[stream][0][col], s_max[stream][1][col]),
+                             fmaxf(s_max[stream][2][col], s_max[stream][3][col]));
+      // lazy running max: raised on the first page and when the page exceeds it by > 2^kLazy2d
+      if (m_run == neg_inf() || pm > m_run + kLazy2d) {
+        const float alpha = m_run == neg_inf() ? 0.f : __builtin_amdgcn_exp2f(m_run - pm);
+        l_run *= alpha;
 #pragma unroll
-      for (int t = 0; t < VT; ++t) zacc[t] *= alpha;
-      m_run = pm;
-    }
-    float pr[4], ls = 0.f;
+        for (int t = 0; t < VT; ++t) zacc[t] *= alpha;
+        m_run = pm;
+      }
+      float pr[4], ls = 0.f;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      pr[r] = __builtin_amdgcn_exp2f(sc[r] - m_run);
-      ls += pr[r];
-    }
-    ls += __shfl_xor(ls, 16, kWave);
-    ls += __shfl_xor(ls, 32, kWave);
-    l_run += ls;  // this wave's 16 tokens; the 4 waves' sums are added at the end
-    {
+      for (int r = 0; r < 4; ++r) {
+        pr[r] = __builtin_amdgcn_exp2f(sc[r] - m_run);
+        ls += pr[r];
+      }
+      ls += __shfl_xor(ls, 16, kWave);
+      ls += __shfl_xor(ls, 32, kWave);
+      l_run += ls;  // this wave's 16 tokens; the waves' sums are added at the end
       uint2 w;
       w.x = (uint32_t)__builtin_bit_cast(bf16_t, (__bf16)pr[0]) | ((uint32_t)__builtin_bit_cast(bf16_t, (__bf16)pr[1]) << 16);
       w.y = (uint32_t)__builtin_bit_cast(bf16_t, (__bf16)pr[2]) | ((uint32_t)__builtin_bit_cast(bf16_t, (__bf16)pr[3]) << 16);
-      *reinterpret_cast<uint2*>(&s_p[pbuf][col * PS + wave * 16 + 4 * g]) = w;
+      *reinterpret_cast<uint2*>(&s_p[stream][pbuf][col * PS + sw * 16 + 4 * g]) = w;
     }
     __syncthreads();
-    // ---- Z^T += C_v^T P^T for this wave's feature tiles ----
-    // Branch-free: value slots past the context may hold anything, so the
-    // tokens at or beyond N are masked to zero (all-ones masks before the last
-    // page); tiles past r_v are multiplied too and never stored.
+    if (act) {
+      // ---- Z^T += C_v^T P^T for this wave's feature tiles ----
+      // Branch-free: value slots past the context may hold anything, so the
+      // tokens at or beyond N are masked to zero (all-ones masks before the
+      // last page); tiles past r_v are multiplied too and never stored.
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const bf16x8 bp = as_bf16x8(*reinterpret_cast<const uint4*>(&s_p[pbuf][col * PS + 32 * u + 8 * g]));
-      const int nv = N - (p * kPage + 32 * u + 8 * g);
-      uint32_t keep[4];
+      for (int u = 0; u < 2; ++u) {
+        const bf16x8 bp = as_bf16x8(*reinterpret_cast<const uint4*>(&s_p[stream][pbuf][col * PS + 32 * u + 8 * g]));
+        const int nv = N - (p * kPage + 32 * u + 8 * g);
+        uint32_t keep[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) keep[i] = nv > 2 * i + 1 ? 0xffffffffu : nv > 2 * i ? 0x0000ffffu : 0u;
+        for (int i = 0; i < 4; ++i) keep[i] = nv > 2 * i + 1 ? 0xffffffffu : nv > 2 * i ? 0x0000ffffu : 0u;
 #pragma unroll
-      for (int t = 0; t < VT; ++t) {
-        const uint4 v = uint4{vf[t][u].x & keep[0], vf[t][u].y & keep[1], vf[t][u].z & keep[2], vf[t][u].w & keep[3]};
-        zacc[t] = mfma16(as_bf16x8(v), bp, zacc[t]);
+        for (int t = 0; t < VT; ++t) {
+          const uint4 v = uint4{vf[t][u].x & keep[0], vf[t][u].y & keep[1], vf[t][u].z & keep[2], vf[t][u].w & keep[3]};
+          zacc[t] = mfma16(as_bf16x8(v), bp, zacc[t]);
+        }
       }
     }
     pbuf ^= 1;
   }
 
-  // ---- partials: m, l (summed over the 4 waves), z of this wave's tiles ----
-  if (lane < 16) s_l[wave][col] = l_run;
+  // ---- combine the two streams, then the partial (m, l, z) of this split ----
+  if (lane < 16) s_l[stream][sw][col] = l_run;
+  __syncthreads();  // every wave is past its last read of Q~: s_raw now holds stream 1's tiles
+  float* s_x = reinterpret_cast<float*>(s_raw);
+  if (stream == 1) {
+#pragma unroll
+    for (int t = 0; t < VT; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) s_x[((sw * VT + t) * 4 + r) * kWave + lane] = zacc[t][r];
+    if (sw == 0 && lane < 16) s_m1[col] = m_run;
+  }
   __syncthreads();
+  if (stream == 1) return;
+  const float m1 = s_m1[col], mm = fmaxf(m_run, m1);
+  const float w0 = m_run == neg_inf() ? 0.f : __builtin_amdgcn_exp2f(m_run - mm);
+  const float w1 = m1 == neg_inf() ? 0.f : __builtin_amdgcn_exp2f(m1 - mm);
   const size_t pbase = (((size_t)b * a.splits + split) * kHeads2d + col) * (size_t)(rv + 2);
-  if (wave == 0 && lane < 16) {
-    a.part[pbase] = m_run;
-    a.part[pbase + 1] = s_l[0][col] + s_l[1][col] + s_l[2][col] + s_l[3][col];
+  if (sw == 0 && lane < 16) {
+    a.part[pbase] = mm;
+    a.part[pbase + 1] = w0 * (s_l[0][0][col] + s_l[0][1][col] + s_l[0][2][col] + s_l[0][3][col]) +
+                        w1 * (s_l[1][0][col] + s_l[1][1][col] + s_l[1][2][col] + s_l[1][3][col]);
   }
 #pragma unroll
   for (int t = 0; t < VT; ++t) {
-    const int tile = wave + kScanWaves * t;
+    const int tile = sw + kScanWaves * t;
     if (tile < vtiles) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) a.part[pbase + 2 + tile * 16 + 4 * g + r] = zacc[t][r];
+      for (int r = 0; r < 4; ++r)
+        a.part[pbase + 2 + tile * 16 + 4 * g + r] = w0 * zacc[t][r] + w1 * s_x[((sw * VT + t) * 4 + r) * kWave + lane];
     }
   }
 }
@@ -459,14 +493,14 @@ __global__ __launch_bounds__(256) void merge2d_kernel(Decode2dArgs a) {
 
 template <int KS, int VT>
 void launch_scan(const Decode2dArgs& a, hipStream_t stream) {
-  hipLaunchKernelGGL((scan2d_kernel<KS, VT>), dim3(a.splits, a.B), dim3(kScanWaves * kWave), 0, stream, a);
+  hipLaunchKernelGGL((scan2d_kernel<KS, VT>), dim3(a.splits, a.B), dim3(kScanThreads), 0, stream, a);
 }
 
 }  // namespace
 
 int decode_2d_splits(int B, int n_ctx) {
   const int pages = (n_ctx + kPage - 1) / kPage;
-  int s = (2 * device_cu_count() + B - 1) / B;  // about two workgroups per compute unit
+  int s = (device_cu_count() + B - 1) / B;  // about one (two-stream) workgroup per compute unit
   if (s > pages) s = pages;
   if (s > LLA_MAX_SPLITS) s = LLA_MAX_SPLITS;
   return s < 1 ? 1 : s;
