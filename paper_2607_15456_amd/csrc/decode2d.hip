@@ -165,34 +165,6 @@ void scan2d_kernel(Decode2dArgs a) {
   const int per = (pages + a.splits - 1) / a.splits;
   const int pb = min(pages, split * per), pe = min(pages, pb + per);
 
-  // Q~ of the 16 heads (hi and lo planes from the absorb launch) -> LDS
-  {
-    constexpr int kPer = (4 * KS * 32 + kScanThreads - 1) / kScanThreads;
-    const int row8 = rk / 8, n16 = 4 * rk;  // 16-byte chunks: per row, in all 32 rows
-    const uint4* src = reinterpret_cast<const uint4*>(a.qt + (size_t)b * 2 * kHeads2d * rk);
-    uint4 x[kPer];
-#pragma unroll
-    for (int k = 0; k < kPer; ++k) {
-      const int e = tid + k * kScanThreads;
-      x[k] = e < n16 ? src[e] : uint4{0, 0, 0, 0};
-    }
-#pragma unroll
-    for (int k = 0; k < kPer; ++k) {
-      const int e = tid + k * kScanThreads;
-      if (e < n16) {
-        const int row = e / row8;
-        *reinterpret_cast<uint4*>(&s_q[row * QS + 8 * (e - row * row8)]) = x[k];
-      }
-    }
-    // zero columns r_k .. 32 KS - 1 (the unused K-steps multiply them)
-    const int pad8 = (KS * 32 - rk) / 8;
-    for (int e = tid; e < 2 * kHeads2d * pad8; e += kScanThreads) {
-      const int row = e / pad8;
-      *reinterpret_cast<uint4*>(&s_q[row * QS + rk + 8 * (e - row * pad8)]) = uint4{0, 0, 0, 0};
-    }
-  }
-  __syncthreads();
-
   // key rows: token-major [n_max][r_k]; value pages: [n_max/64][r_v][64]
   const BufRsrc ksrc = make_rsrc(static_cast<const bf16_t*>(a.ck) + (size_t)b * a.n_max * rk,
                                  (size_t)a.n_max * rk * 2);
@@ -221,26 +193,59 @@ void scan2d_kernel(Decode2dArgs a) {
       for (int u = 0; u < 2; ++u) vf[t][u] = buf_ld16(vsrc, v_lane + 64 * u, soff);
     }
   };
+  // The first page's loads go out before Q~ is staged (they do not depend on
+  // it); afterwards a page's keys are requested as soon as the previous
+  // page's scores have consumed the key registers, its values once the
+  // previous page's value products are issued.
+  uint4 kf[KS], vf[VT][2];
+  if (pb + stream < pe) {
+    kload(kf, pb + stream);
+    vload(vf, pb + stream);
+  }
+
+  // Q~ of the 16 heads (hi and lo planes from the absorb launch) -> LDS
+  {
+    constexpr int kPer = (4 * KS * 32 + kScanThreads - 1) / kScanThreads;
+    const int row8 = rk / 8, n16 = 4 * rk;  // 16-byte chunks: per row, in all 32 rows
+    const uint4* src = reinterpret_cast<const uint4*>(a.qt + (size_t)b * 2 * kHeads2d * rk);
+    uint4 x[kPer];
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      const int e = tid + k * kScanThreads;
+      x[k] = e < n16 ? src[e] : uint4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      const int e = tid + k * kScanThreads;
+      if (e < n16) {
+        const int row = e / row8;
+        *reinterpret_cast<uint4*>(&s_q[row * QS + 8 * (e - row * row8)]) = x[k];
+      }
+    }
+    // zero columns r_k .. 32 KS - 1 (the unused K-steps multiply them)
+    const int pad8 = (KS * 32 - rk) / 8;
+    for (int e = tid; e < 2 * kHeads2d * pad8; e += kScanThreads) {
+      const int row = e / pad8;
+      *reinterpret_cast<uint4*>(&s_q[row * QS + rk + 8 * (e - row * pad8)]) = uint4{0, 0, 0, 0};
+    }
+  }
+  __syncthreads();
 
   f32x4 zacc[VT];
 #pragma unroll
   for (int t = 0; t < VT; ++t) zacc[t] = f32x4{0.f};
   float m_run = neg_inf(), l_run = 0.f;  // of head `col` (same in all 4 lane groups)
 
-  // One page in flight per wavefront (its keys and values are loaded before
-  // its scores are computed); the other stream and the other resident
-  // workgroups cover the latency.  A stream without a page this round still
-  // meets the barriers.
+  // One page in flight per wavefront; the other stream covers part of the
+  // latency.  A stream without a page this round still meets the barriers.
   int pbuf = 0;
   const int rounds = (pe - pb + kStreams - 1) / kStreams;
   for (int it = 0; it < rounds; ++it) {
     const int p = pb + kStreams * it + stream;
     const bool act = p < pe;  // uniform over the stream
-    uint4 kf[KS], vf[VT][2];
+    const bool more = p + kStreams < pe;
     f32x4 sc = f32x4{0.f};
     if (act) {
-      kload(kf, p);
-      vload(vf, p);
       // ---- S^T tile: tokens 16 sw .. +15 of the page x 16 heads ----
       int qo = col * QS + 8 * g;
       asm volatile("" : "+v"(qo));  // re-read Q~ from LDS every page rather than pin it in registers
@@ -251,6 +256,7 @@ void scan2d_kernel(Decode2dArgs a) {
         sc = mfma16(as_bf16x8(kf[s]), bq, sc);
         sc = mfma16(as_bf16x8(kf[s]), bl, sc);
       }
+      if (more) kload(kf, p + kStreams);
       // tokens beyond the context (the last page) score -inf
       const int tok0 = p * kPage + sw * 16 + 4 * g;
       float mx = neg_inf();
@@ -308,6 +314,7 @@ void scan2d_kernel(Decode2dArgs a) {
           zacc[t] = mfma16(as_bf16x8(v), bp, zacc[t]);
         }
       }
+      if (more) vload(vf, p + kStreams);
     }
     pbuf ^= 1;
   }
