@@ -29,6 +29,9 @@ Readings where the paper is silent (all listed in the design doc):
   per-token key, shared across loops, rotated half-split (pairs i, i + d_rope/2)
   with angle p * base^(-2i/d_rope), and its softmax scale defaults to
   1/sqrt(d_head + d_rope);
+* full RoPE (the paper's accuracy path): the rotary phase of a token's position
+  is applied to the loop-l reconstruction of its key (values carry none), with
+  the same half-split convention over all d_head features;
 * a decode query attends exactly the N cached latent entries [0, N);
 * a prefill query at absolute position p attends keys n <= p.
 
@@ -75,6 +78,8 @@ __all__ = [
     "stack_loops_heads",
     "decode_attn_2d",
     "decode_attn_2d_batched",
+    "decode_attn_fullrope",
+    "decode_attn_fullrope_batched",
 ]
 
 
@@ -515,4 +520,62 @@ def decode_attn_2d_batched(q, c_k, c_v, u_k, u_v, mu_k=None, mu_v=None, scale=No
     for b in (range(B) if batches is None else batches):
         n = lens[b]
         out[b] = decode_attn_2d(q[b], c_k[b, :n], c_v[b, :n], u_k, u_v, mu_k, mu_v, scale)
+    return out
+
+
+# ---------------------------------------------------------------------------
+# Sec. 3 "RoPE and reconstruction": the latent is fit to the pre-RoPE content
+# projection, and since a token keeps its position at every recurrence step its
+# rotary phase is applied after the loop-l reconstruction.  This is the full-RoPE
+# path all main accuracy results use (App. J, tab:decoupled_char), read here as
+# reconstruct-then-attend over the latent cache: the rotation differs per key
+# position, so the key up-projection cannot move to the query side (App. J);
+# values carry no rotary phase.
+# ---------------------------------------------------------------------------
+
+def decode_attn_fullrope(q, c_k, c_v, u_k, u_v, mu_k=None, mu_v=None, scale=None, base=10000.0,
+                         q_pos=None, k_pos=None):
+    """Loop-l decode with full RoPE, plain definition: every cached key is
+    reconstructed with Eq. 3 and then rotated at its position,
+    K_l[n] = RoPE(c_k[n] U_k^T + mu_k, k_pos[n]); values V_l[n] = c_v[n] U_v^T + mu_v
+    are not rotated; the query is RoPE(q, q_pos); then the teacher's attention
+    with its scale 1/sqrt(d_head).
+
+    q: [d] (unrotated); c_k: [N, r_k]; c_v: [N, r_v]; u_k: [d, r_k]; u_v: [d, r_v];
+    mu_k, mu_v: [d] or None.  k_pos defaults to 0..N-1 (cache slot n holds
+    position n), q_pos to N - 1 (the newest cached token).  Returns [d]."""
+    q = np.asarray(q, dtype=np.float64)
+    N = np.asarray(c_k).shape[0]
+    d = q.shape[-1]
+    if scale is None:
+        scale = default_scale(d)
+    if k_pos is None:
+        k_pos = np.arange(N)
+    if q_pos is None:
+        q_pos = N - 1
+    K = rope(reconstruct(c_k, u_k, mu_k), k_pos, base)
+    V = reconstruct(c_v, u_v, mu_v)
+    return attention(rope(q, q_pos, base), K, V, scale)
+
+
+def decode_attn_fullrope_batched(q, c_k, c_v, u_k, u_v, mu_k=None, mu_v=None, scale=None,
+                                 base=10000.0, ctx_len=None, q_pos=None, units=None):
+    """decode_attn_fullrope for every (b, h) (or the pairs in ``units``).
+    q: [B, H, d]; c_k: [B, H, >=N, r_k]; c_v: [B, H, >=N, r_v]; u_k: [H, d, r_k];
+    u_v: [H, d, r_v]; ctx_len: int or per-batch ints; q_pos: None (N_b - 1 for
+    every sequence) or per-batch ints.  Returns [B, H, d] (NaN where not computed)."""
+    q = np.asarray(q, dtype=np.float64)
+    B, H, d = q.shape
+    if ctx_len is None:
+        ctx_len = c_k.shape[2]
+    lens = [int(ctx_len)] * B if np.ndim(ctx_len) == 0 else [int(v) for v in ctx_len]
+    qp = [n - 1 for n in lens] if q_pos is None else [int(v) for v in q_pos]
+    out = np.full((B, H, d), np.nan)
+    todo = units if units is not None else [(b, h) for b in range(B) for h in range(H)]
+    for b, h in todo:
+        n = lens[b]
+        out[b, h] = decode_attn_fullrope(q[b, h], c_k[b, h, :n], c_v[b, h, :n], u_k[h], u_v[h],
+                                         None if mu_k is None else mu_k[h],
+                                         None if mu_v is None else mu_v[h], scale, base,
+                                         q_pos=qp[b])
     return out
