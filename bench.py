@@ -67,6 +67,9 @@ def parse():
     p.add_argument("--rope", type=int, default=0,
                    help="add the decoupled rotary branch with this d_rope (one rotary key per token, "
                         "shared by the heads and the loops); ouro14b_decode and prefill_write")
+    p.add_argument("--fullrope", action="store_true",
+                   help="decode workloads: full-RoPE reconstruct-then-attend decode (keys rebuilt from the "
+                        "latents and rotated at their positions; lla_decode_attn_fullrope)")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--no-graph", action="store_true",
                    help="ouro14b_2d: launch every call from Python instead of replaying HIP graphs")
@@ -185,7 +188,10 @@ def run_decode(args, torch, lla, W):
                 for d in range(layers):
                     q, uk, uv, out = loops[l][d]
                     ck, cv = caches[d]
-                    if rope:
+                    if args.fullrope:
+                        s = timer.start() if timed else None
+                        lla.decode_attn_fullrope(q, ck, cv, uk, uv, n_ctx=n_ctx, out=out, workspace=ws)
+                    elif rope:
                         # the new token sits at position N; its query is rotated there
                         lla.rope_rotate(rope["q"][l][d], pos0=wl.N, out=rope["q_rot"])
                         s = timer.start() if timed else None
@@ -223,18 +229,18 @@ def run_decode(args, torch, lla, W):
                    calls_per_step=wl.T * layers, splits_ws_bytes=ws.numel())
         print(f"[bench] {json.dumps(res)}", file=sys.stderr, flush=True)
         res["cpu"] = (None if (args.no_cpu or dr or evict or args.ranks)
-                      else cpu_baseline_decode(wl, r_k, r_v, caches, loops, torch))
+                      else cpu_baseline_decode(wl, r_k, r_v, caches, loops, torch, fullrope=args.fullrope))
         results.append(res)
         del caches, loops, writes, ws, rope
         torch.cuda.empty_cache()
     return wl, results
 
 
-def cpu_baseline_decode(wl, r_k, r_v, caches, loops, torch, budget_s=15.0):
-    """Time the oracle's plain-definition decode (reconstruct K_l, V_l; softmax
-    attention) on (b, h) units of the step's calls, in step order (loop l, layer
-    d, then b, h), until about budget_s of CPU time; scale the per-unit time to
-    the whole step."""
+def cpu_baseline_decode(wl, r_k, r_v, caches, loops, torch, budget_s=15.0, fullrope=False):
+    """Time the oracle's plain-definition decode (reconstruct K_l, V_l -- and
+    rotate the keys with full RoPE -- then softmax attention) on (b, h) units of
+    the step's calls, in step order (loop l, layer d, then b, h), until about
+    budget_s of CPU time; scale the per-unit time to the whole step."""
     import oracle
     from paper_2607_15456_amd.lla import from_paged
 
@@ -253,13 +259,17 @@ def cpu_baseline_decode(wl, r_k, r_v, caches, loops, torch, budget_s=15.0):
         vv = from_paged(cv[b:b + 1, h:h + 1], wl.N)[0, 0].cpu().double().numpy()
         qq = q[b, h].cpu().double().numpy()
         t0 = time.perf_counter()
-        oracle.decode_attn(qq, kk, vv, uk64[h], uv64[h])
+        if fullrope:
+            oracle.decode_attn_fullrope(qq, kk, vv, uk64[h], uv64[h])
+        else:
+            oracle.decode_attn(qq, kk, vv, uk64[h], uv64[h])
         t += time.perf_counter() - t0
         units += 1
     per_unit = t / units
     step_s = per_unit * wl.B * wl.H * wl.T * wl.layers
     return dict(value=wl.B / step_s, unit="tokens/s", cores=cpu_threads(), kind="oracle",
-                sample=(f"oracle.decode_attn (float64, reconstruct-then-attend) on the first {units} "
+                sample=(f"oracle.{'decode_attn_fullrope' if fullrope else 'decode_attn'} (float64, "
+                        f"reconstruct-then-attend) on the first {units} "
                         f"(loop, layer, b, h) units of the step, {t:.1f} s of CPU time; per-unit time "
                         f"x {wl.B * wl.H} units x {wl.T * wl.layers} calls per step; the step's M=1 "
                         f"cache writes are not timed (under 0.1% of the work)"))
@@ -555,7 +565,8 @@ def main():
     B, N, d = wl.B, wl.N, wl.d
     value = B / (head["step_ms"] * 1e-3)
     achieved = head["decode_gbs"]
-    traffic = None if (args.rope or args.evict) else traffic_bytes((wl.name, head["r_k"], head["r_v"]))
+    traffic = (None if (args.rope or args.evict or args.fullrope)
+               else traffic_bytes((wl.name, head["r_k"], head["r_v"])))
     line = {
         "metric": "latent-cache decode attention tokens/sec and achieved HBM GB/s (% of peak)",
         "value": round(value, 2),
@@ -573,7 +584,10 @@ def main():
             "workload": wl.description + (f"; decoupled rotary branch d_rope {args.rope} (one rotary key "
                                           f"per token shared by the heads)" if args.rope else "")
             + (f"; ranks overridden to ({head['r_k']}, {head['r_v']})" if args.ranks else "")
-            + (f"; eviction budget sink+window = {args.evict.replace(',', '+')} (ring cache)" if args.evict else ""),
+            + (f"; eviction budget sink+window = {args.evict.replace(',', '+')} (ring cache)" if args.evict else "")
+            + ("; full-RoPE reconstruct-then-attend (keys rebuilt from the latents and rotated at their "
+               "positions, RoPE base 10000)" if args.fullrope else ""),
+            "fullrope": bool(args.fullrope),
             "d_rope": args.rope,
             "evict": args.evict,
             "layers": wl.layers, "loops": wl.T, "heads": wl.H, "d_head": d, "batch": B, "context": N,
@@ -589,7 +603,8 @@ def main():
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
             "traffic_unit": "HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, calibrated)",
-            "kernel": "decode_kernel (lla_decode_attn)",
+            "kernel": ("fullrope_mfma_kernel (lla_decode_attn_fullrope)" if args.fullrope
+                       else "decode_kernel (lla_decode_attn)"),
             "bytes_per_launch": head["decode_bytes"],
             "avg_launch_ms": round(head["decode_ms"], 5),
         },

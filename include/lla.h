@@ -59,7 +59,7 @@
 extern "C" {
 #endif
 
-#define LLA_ABI_VERSION 5
+#define LLA_ABI_VERSION 6
 #define LLA_PAGE_TOKENS 64
 #define LLA_MAX_RANK 512
 #define LLA_MAX_ROPE 256
@@ -200,6 +200,40 @@ lla_status lla_prefill_attn(int dtype, int out_dtype, int B, int H, int M, int d
                             int r_v, int n_max, int p0, const void* q, const void* c_k,
                             const void* c_v, const void* u_k, const void* u_v, const void* mu_k,
                             const void* mu_v, float scale, void* out, void* stream);
+
+/*
+ * Loop-l decode with full RoPE, reconstruct-then-attend (Sec. 3 "RoPE and
+ * reconstruction"): the latent is fit to the pre-RoPE content projection and a
+ * token's rotary phase, the same at every loop, is applied after the loop-l
+ * reconstruction.  Every cached key is rebuilt and rotated at its position,
+ *   K_l[n] = RoPE(U_k c_k[n] + mu_k, n)          (slot n holds position n)
+ *   s_n    = scale * < RoPE(q, p_q), K_l[n] >     n < N_b
+ *   out    = U_v (sum_n softmax(s)_n c_v[n]) + mu_v
+ * Values carry no rotary phase, so the value side keeps the absorbed form of
+ * App. J; the key side cannot (the rotation differs per key), so K is
+ * reconstructed on chip (never written to memory).  RoPE is half-split over
+ * the whole head (feature i pairs with i + d_head/2, angle p * base^(-2i/d_head)).
+ *
+ *   q        [B][H][d_head]  loop-l queries, NOT rotated (the kernel rotates)
+ *   q_pos    device int32 [B] or NULL: the query position p_q of sequence b;
+ *            NULL means N_b - 1 (the newest cached token)
+ *   mu_k     [H][d_head] or NULL: added before the rotation (it does not
+ *            cancel here)
+ *   base     RoPE base (finite, > 1), e.g. 10000
+ *   scale    softmax scale, the teacher's 1/sqrt(d_head)
+ *   other arguments as for lla_decode_attn; the workspace is the one sized by
+ *   lla_decode_workspace_bytes (the context may be split over workgroups).
+ * bf16 with d_head = 128 and r_k <= 288 runs on bf16 MFMA (fp32 accumulation,
+ * keys reconstructed exactly from bf16 operands); fp32 and other shapes run a
+ * plain fp32 kernel.
+ * Errors: LLA_ERR_INVALID_ARG, LLA_ERR_WORKSPACE, LLA_ERR_HIP.
+ */
+lla_status lla_decode_attn_fullrope(int dtype, int out_dtype, int B, int H, int d_head, int r_k,
+                                    int r_v, int n_max, int n_ctx, const int32_t* ctx_len,
+                                    const int32_t* q_pos, const void* q, const void* c_k,
+                                    const void* c_v, const void* u_k, const void* u_v,
+                                    const void* mu_k, const void* mu_v, double base, float scale,
+                                    void* out, void* workspace, size_t ws_bytes, void* stream);
 
 /*
  * Decoupled rotary branch (App. J, "Absorbed attention"): RoPE prevents exact

@@ -1,0 +1,577 @@
+// Loop-l decode with full RoPE over the paged latent cache: the
+// reconstruct-then-attend path (Sec. 3 "RoPE and reconstruction").  The latent
+// is fit to the pre-RoPE content projection, so every cached key is rebuilt
+// with Eq. 3, K_l[n] = U_k c_k[n] + mu_k, and turned by its position's rotary
+// phase; values carry no phase.  The rotation differs from key to key, so the
+// key up-projection cannot move to the query side (App. J); the value side
+// still can: z = sum_n p_n c_v[n], out = U_v z + mu_v.
+//
+// Score of key n with the query rotated at p_q (half-split pairs (i, i + 64)
+// as complex numbers):  <RoPE(q, p_q), RoPE(k, n)> = <RoPE(q, p_q - n), k>.
+// With n = n0 + t (n0 a 32-token tile base) the query weight of token t is
+// RoPE(QP, -t), QP = RoPE(q, p_q - n0): QP is formed once per tile (angle in
+// double precision), and cos / sin of t * theta_f, the same for every tile,
+// stay in registers.
+//
+// bf16 kernel (d_head = 128): a workgroup of 4 wavefronts takes one (b, h)
+// and a range of 64-token pages.  Wavefront m rebuilds rows 32m .. 32m + 31
+// of K^T for both 32-token tiles of every page on v_mfma_f32_32x32x16_bf16:
+//   A = U_k rows 32m + i (held in registers for the whole scan),
+//   B = the key page, staged in LDS with XOR-swizzled 16-byte chunks and read
+//       with ds_read_b64_tr_b16 (lane l gets one token's 4 features),
+// so lane (col + 32 g), register r holds K[32m + 8(r/4) + 4g + r%4][token col].
+// The lane multiplies its 16 reconstructed features by the rotated query
+// weights, the two lane halves and the four wavefronts add their parts (LDS,
+// one barrier per page), and every wavefront runs the same online softmax.
+// Values: wavefront m owns latent rows [8 VR m, 8 VR (m + 1)) and streams them
+// with 16-byte loads of 8 tokens, as in the absorbed decode.  Key pages are
+// loaded into registers one page ahead and written to a two-slot LDS ring.
+//
+// A plain kernel (one thread per token and feature, reconstruction in fp32)
+// serves fp32 inputs and every shape the MFMA kernel does not take.
+
+#include "lla_device.h"
+#include "lla_internal.h"
+#include "../../include/lla.h"
+
+namespace lla {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+#define LLA_LDS __attribute__((address_space(3)))
+
+constexpr int kFrWaves = 4;
+constexpr int kFrThreads = kFrWaves * kWave;
+constexpr int kFrD = 128;  // d_head of the MFMA kernel
+constexpr double kTwoPi = 6.283185307179586476925286766559;
+
+typedef __amdgpu_buffer_rsrc_t BufRsrc;
+__device__ __forceinline__ BufRsrc make_rsrc(const void* base, size_t bytes) {
+  const int n = bytes >= 0xffffffffull ? -1 : (int)bytes;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, n, 0x00020000);
+}
+__device__ __forceinline__ uint4 buf_ld16(BufRsrc r, int voff, int soff) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+__device__ __forceinline__ uint2 lds_tr16(const bf16_t* p) {
+  return __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((LLA_LDS i16x4*)(p)));
+}
+__device__ __forceinline__ f32x16 mfma32(uint4 a, uint4 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b),
+                                                 c, 0, 0, 0);
+}
+
+// (cos, sin) of p * theta with the angle formed and reduced in double.
+__device__ __forceinline__ void rot_cs(double p, double theta, float& c, float& s) {
+  const double ang = p * theta;
+  const double r = ang - rint(ang * (1.0 / kTwoPi)) * kTwoPi;
+  sincosf((float)r, &s, &c);
+}
+
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// out[i] = sum_j U_v[i][j] zn[j] + mu_v[i] (zn already normalised), 256
+// threads: P consecutive threads share row i and take every P-th column; their
+// partial sums combine by xor shuffles in a fixed order.
+template <typename T>
+__device__ void fr_epilogue(const FullRopeArgs& a, int h, size_t unit, const float* s_zn, bool bad) {
+  const int d = a.d, rv = a.rv;
+  const int P = 256 / d >= 8 ? 8 : 256 / d >= 4 ? 4 : 256 / d >= 2 ? 2 : 1;
+  const int i = threadIdx.x / P, part = threadIdx.x % P;
+  const T* uv = static_cast<const T*>(a.uv) + (size_t)h * d * rv;
+  float acc = 0.f;
+  if (i < d) {
+    const T* row = uv + (size_t)i * rv;
+    for (int j = part; j < rv; j += P) acc = fmaf(Elem<T>::get(row, j), s_zn[j], acc);
+  }
+  for (int off = 1; off < P; off <<= 1) acc += __shfl_xor(acc, off, kWave);
+  if (i < d && part == 0) {
+    if (a.muv) acc += Elem<T>::get(static_cast<const T*>(a.muv), (size_t)h * d + i);
+    if (bad) acc = __builtin_nanf("");
+    if (a.out_dtype == LLA_F32)
+      static_cast<float*>(a.out)[unit * d + i] = acc;
+    else
+      static_cast<bf16_t*>(a.out)[unit * d + i] = f32_to_bf16(acc);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// MFMA kernel: bf16, d_head = 128, r_k <= 16 KS, r_v <= 32 VR.
+// ---------------------------------------------------------------------------
+template <int KS, int VR, bool MU, int OCC>
+__global__ __launch_bounds__(kFrThreads) __attribute__((amdgpu_waves_per_eu(OCC)))
+void fullrope_mfma_kernel(FullRopeArgs a) {
+  constexpr int RKP = KS * 16;            // padded key rank (K of the product)
+  constexpr int KI = RKP / 8;             // 8-row load instructions per key page
+  constexpr int KD = (KI + kFrWaves - 1) / kFrWaves;  // ... per wavefront
+  constexpr int kSlot = RKP * kPage;      // bf16 elements of one staged page
+  __shared__ __attribute__((aligned(16))) bf16_t s_k[2 * kSlot];
+  __shared__ __attribute__((aligned(16))) float s_qp[kFrWaves][2][2][32];  // [wave][tile][re/im][freq]
+  __shared__ __attribute__((aligned(16))) float s_sc[2][kFrWaves][kPage];  // partial scores
+  __shared__ float s_z[kMaxRank];
+  __shared__ float s_ml[2];
+  __shared__ int s_last;
+
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int col = lane & 31, g = lane >> 5;
+  const int hi = lane >> 3, lo = lane & 7;  // value phase: row in the 8-row group, token slice
+  const int b = blockIdx.x / a.splits, split = blockIdx.x - b * a.splits, h = blockIdx.y;
+  const int N = a.ctx_len ? a.ctx_len[b] : a.n_ctx;
+  const bool bad = (N < 1) || (N > a.n_ctx);
+  const int pages = bad ? 0 : (N + kPage - 1) / kPage;
+  const int per = (pages + a.splits - 1) / a.splits;
+  const int pb = min(pages, split * per), pe = min(pages, pb + per);
+  const int pq = a.q_pos ? a.q_pos[b] : N - 1;
+  const size_t bh = (size_t)b * a.H + h;
+  const int rk = a.rk, rv = a.rv;
+
+  // ---- U_k rows 32 wave + col, features 16 s + 8 g .. +7: the A operands ----
+  uint4 ua[KS];
+  {
+    const bf16_t* urow = static_cast<const bf16_t*>(a.uk) + ((size_t)h * kFrD + 32 * wave + col) * rk;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const int j0 = 16 * s + 8 * g;
+      if ((rk & 7) == 0) {
+        ua[s] = j0 < rk ? *reinterpret_cast<const uint4*>(urow + j0) : uint4{0, 0, 0, 0};
+      } else {
+        uint32_t w[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const uint32_t x0 = j0 + 2 * e < rk ? urow[j0 + 2 * e] : 0u;
+          const uint32_t x1 = j0 + 2 * e + 1 < rk ? urow[j0 + 2 * e + 1] : 0u;
+          w[e] = x0 | (x1 << 16);
+        }
+        ua[s] = uint4{w[0], w[1], w[2], w[3]};
+      }
+    }
+  }
+  // ---- rotation constants ----
+  // Lane (col, g), register r of tile `wave`: feature i = 32 wave + fr(r) with
+  // fr(r) = 8 (r/4) + 4 g + r%4, frequency f = i mod 64 = 32 (wave & 1) + fr(r).
+  // cos / sin of col * theta_f (token offset inside a 32-token tile).
+  const bool first_half = wave < 2;
+  float cs_c[16], cs_s[16];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int f = 32 * (wave & 1) + 8 * (r / 4) + 4 * g + r % 4;
+    rot_cs((double)col, pow(a.base, -2.0 * f / kFrD), cs_c[r], cs_s[r]);
+  }
+  // query rotation: lane (fq = col, tile tq = g) forms QP for frequency
+  // 32 (wave & 1) + fq of tile tq of every page
+  const int fq = 32 * (wave & 1) + col;
+  const double theta_q = pow(a.base, -2.0 * fq / kFrD);
+  float q1, q2;
+  {
+    const bf16_t* qp = static_cast<const bf16_t*>(a.q) + bh * kFrD;
+    q1 = bf16_to_f32(qp[fq]) * a.qscale;
+    q2 = bf16_to_f32(qp[fq + 64]) * a.qscale;
+  }
+  float mu[16];
+  if constexpr (MU) {
+    const bf16_t* mk = static_cast<const bf16_t*>(a.muk) + (size_t)h * kFrD + 32 * wave;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mu[r] = bf16_to_f32(mk[8 * (r / 4) + 4 * g + r % 4]);
+  }
+
+  // ---- buffers over this (b, h)'s latents ----
+  const BufRsrc ksrc = make_rsrc(static_cast<const bf16_t*>(a.ck) + bh * (size_t)a.n_max * rk,
+                                 (size_t)a.n_max * rk * 2);
+  const BufRsrc vsrc = make_rsrc(static_cast<const bf16_t*>(a.cv) + bh * (size_t)a.n_max * rv,
+                                 (size_t)a.n_max * rv * 2);
+  const int kpage = kPage * rk * 2, vpage = kPage * rv * 2;  // bytes per page
+  // key loads: instruction k = wave + 4 u covers page rows 8k .. 8k+7; lane ->
+  // row 8k + lane/8, 16-byte chunk lane%8 (one contiguous KB per instruction)
+  const int krow = lane >> 3;
+  const int kswz = ((lane >> 4) & 1) << 2;                            // chunk XOR of row 8k + krow
+  const int kdst = krow * kPage + (((lane & 7) ^ kswz) << 3);          // LDS element offset in the row block
+  // transposed reads: lane (x16 = lane % 16, G = lane / 16) of tile nt reads
+  // rows 16 s + 8 g + 4 e2 + x16/4, tokens 32 nt + 16 (G % 2) + 4 (x16 % 4) .. +3
+  const int x16 = lane & 15, th = (lane >> 4) & 1, sw1 = (x16 >> 3) & 1;
+  const int cl = 2 * th + ((x16 & 3) >> 1);
+  int troff[2];
+#pragma unroll
+  for (int nt = 0; nt < 2; ++nt)
+    troff[nt] = (8 * g + (x16 >> 2)) * kPage + ((4 * (nt ^ sw1) + cl) << 3) + 4 * (x16 & 1);
+  // value rows of this wavefront: 8 VR wave + 8 k + hi, tokens 8 lo .. 8 lo + 7
+  const int vrow0 = 8 * VR * wave;
+
+  uint4 kreg[KD];
+  // Rows past r_k are zero.  A lane whose row is past r_k reads row r_k - 1
+  // instead (every address stays inside the page's r_k rows) and drops it.
+  auto kload = [&](int p) {
+#pragma unroll
+    for (int u = 0; u < KD; ++u) {
+      const int k = wave + kFrWaves * u;
+      const int row = 8 * k + krow;
+      if (k < KI && 8 * k < rk) {  // uniform
+        const int voff = (min(row, rk - 1) - 8 * k) * (kPage * 2) + (lane & 7) * 16;
+        const uint4 v = buf_ld16(ksrc, voff, p * kpage + 8 * k * kPage * 2);
+        kreg[u] = row < rk ? v : uint4{0, 0, 0, 0};
+      } else {
+        kreg[u] = uint4{0, 0, 0, 0};
+      }
+    }
+  };
+  auto kstore = [&](int slot) {
+#pragma unroll
+    for (int u = 0; u < KD; ++u) {
+      const int k = wave + kFrWaves * u;
+      if (k < KI) *reinterpret_cast<uint4*>(&s_k[slot * kSlot + 8 * k * kPage + kdst]) = kreg[u];
+    }
+  };
+  uint4 vreg[VR];
+  // A lane whose row is past r_v reads row r_v - 1 (never used).
+  auto vload = [&](int p) {
+#pragma unroll
+    for (int k = 0; k < VR; ++k) {
+      const int j0 = vrow0 + 8 * k;
+      if (j0 < rv) {  // uniform: the 8-row group starts inside r_v
+        const int voff = (min(j0 + hi, rv - 1) - j0) * (kPage * 2) + lo * 16;
+        vreg[k] = buf_ld16(vsrc, voff, p * vpage + j0 * kPage * 2);
+      }
+    }
+  };
+
+  float zacc[VR];
+#pragma unroll
+  for (int k = 0; k < VR; ++k) zacc[k] = 0.f;
+  float m_run = neg_inf(), l_lane = 0.f;
+
+  if (pb < pe) {
+    kload(pb);
+    kstore(0);
+    if (pb + 1 < pe) kload(pb + 1);
+    vload(pb);
+  }
+  __syncthreads();
+
+  for (int p = pb; p < pe; ++p) {
+    const int slot = (p - pb) & 1;
+    // ---- rotated query of this page's two tiles ----
+    {
+      float c, s;
+      rot_cs((double)pq - (double)(p * kPage + 32 * g), theta_q, c, s);
+      s_qp[wave][g][0][col] = q1 * c - q2 * s;
+      s_qp[wave][g][1][col] = q2 * c + q1 * s;
+    }
+    // ---- K^T rows 32 wave .. +31 of both tiles ----
+    f32x16 acc[2];
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[nt][r] = MU ? mu[r] : 0.f;
+    }
+    const bf16_t* kb = &s_k[slot * kSlot];
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt) {
+        const uint2 r0 = lds_tr16(kb + troff[nt] + 16 * s * kPage);
+        const uint2 r1 = lds_tr16(kb + troff[nt] + (16 * s + 4) * kPage);
+        acc[nt] = mfma32(ua[s], uint4{r0.x, r0.y, r1.x, r1.y}, acc[nt]);
+      }
+    }
+    wave_sync();
+    // ---- rotated dot products: this lane's 16 features of token col ----
+    float part[2];
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) {
+      float sum = 0.f;
+#pragma unroll
+      for (int a4 = 0; a4 < 4; ++a4) {
+        const float4 p1 = *reinterpret_cast<const float4*>(&s_qp[wave][nt][0][8 * a4 + 4 * g]);
+        const float4 p2 = *reinterpret_cast<const float4*>(&s_qp[wave][nt][1][8 * a4 + 4 * g]);
+        const float x1[4] = {p1.x, p1.y, p1.z, p1.w}, x2[4] = {p2.x, p2.y, p2.z, p2.w};
+#pragma unroll
+        for (int b4 = 0; b4 < 4; ++b4) {
+          const int r = 4 * a4 + b4;
+          const float w = first_half ? fmaf(x1[b4], cs_c[r], x2[b4] * cs_s[r])
+                                     : fmaf(x2[b4], cs_c[r], -(x1[b4] * cs_s[r]));
+          sum = fmaf(w, acc[nt][r], sum);
+        }
+      }
+      part[nt] = sum + __shfl_xor(sum, 32, kWave);
+    }
+    s_sc[slot][wave][lane] = g ? part[1] : part[0];  // lane = token 32 g + col
+    // ---- next key page into the other ring slot, the one after into registers ----
+    if (p + 1 < pe) {
+      kstore(slot ^ 1);
+      if (p + 2 < pe) kload(p + 2);
+    }
+    __syncthreads();
+
+    // ---- softmax over the page: lane (hi, lo) holds tokens 8 lo .. 8 lo + 7 ----
+    float sc[8];
+#pragma unroll
+    for (int e = 0; e < 8; e += 4) {
+      float4 t = *reinterpret_cast<const float4*>(&s_sc[slot][0][8 * lo + e]);
+#pragma unroll
+      for (int w = 1; w < kFrWaves; ++w) {
+        const float4 u = *reinterpret_cast<const float4*>(&s_sc[slot][w][8 * lo + e]);
+        t.x += u.x;
+        t.y += u.y;
+        t.z += u.z;
+        t.w += u.w;
+      }
+      sc[e] = t.x;
+      sc[e + 1] = t.y;
+      sc[e + 2] = t.z;
+      sc[e + 3] = t.w;
+    }
+    const int n0 = p * kPage + 8 * lo;
+    float mx = neg_inf();
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      if (n0 + e >= N) sc[e] = neg_inf();
+      mx = fmaxf(mx, sc[e]);
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 1, kWave));
+    mx = fmaxf(mx, __shfl_xor(mx, 2, kWave));
+    mx = fmaxf(mx, __shfl_xor(mx, 4, kWave));
+    if (mx > m_run) {
+      const float alpha = __builtin_amdgcn_exp2f(m_run - mx);
+      l_lane *= alpha;
+#pragma unroll
+      for (int k = 0; k < VR; ++k) zacc[k] *= alpha;
+      m_run = mx;
+    }
+    float pr[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      pr[e] = __builtin_amdgcn_exp2f(sc[e] - m_run);  // exp2(-inf) = 0 past N
+      l_lane += pr[e];
+    }
+    // ---- values: z[row] += sum over the lane's 8 tokens ----
+    const bool tail = (p + 1) * kPage > N;
+#pragma unroll
+    for (int k = 0; k < VR; ++k) {
+      if (vrow0 + 8 * k < rv && vrow0 + 8 * k + hi < rv) {
+        float v[8];
+        Elem<bf16_t>::unpack(vreg[k], v);
+        if (tail) {  // slots past the context may hold anything
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (n0 + e >= N) v[e] = 0.f;
+        }
+        float t = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) t = fmaf(pr[e], v[e], t);
+        zacc[k] += t;
+      }
+    }
+    if (p + 1 < pe) vload(p + 1);
+  }
+
+  // ---- reductions: z over token slices, l over token slices ----
+#pragma unroll
+  for (int off = 1; off < 8; off <<= 1) {
+    l_lane += __shfl_xor(l_lane, off, kWave);
+#pragma unroll
+    for (int k = 0; k < VR; ++k) zacc[k] += __shfl_xor(zacc[k], off, kWave);
+  }
+  if (lo == 0) {
+#pragma unroll
+    for (int k = 0; k < VR; ++k) {
+      const int j = vrow0 + 8 * k + hi;
+      if (j < rv) s_z[j] = zacc[k];
+    }
+  }
+  if (tid == 0) {
+    s_ml[0] = m_run;
+    s_ml[1] = l_lane;
+  }
+  __syncthreads();
+
+  const size_t unit = bh;
+  if (a.splits == 1) {
+    const float inv = 1.0f / s_ml[1];
+    for (int j = tid; j < rv; j += kFrThreads) s_z[j] *= inv;
+  } else {
+    const int stride = rv + 2;
+    float* part = a.part + (unit * a.splits + split) * stride;
+    for (int j = tid; j < rv; j += kFrThreads) part[2 + j] = s_z[j];
+    if (tid == 0) {
+      part[0] = s_ml[0];
+      part[1] = s_ml[1];
+    }
+    // each wavefront releases its partial stores at agent scope; the last
+    // arrival's acquire makes every split's partial visible
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    __syncthreads();
+    if (tid == 0) {
+      const uint32_t prev =
+          __hip_atomic_fetch_add(a.cnt + unit, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+      s_last = (prev == (uint32_t)(a.splits - 1));
+    }
+    __syncthreads();
+    if (!s_last) return;
+    const float* P = a.part + unit * a.splits * stride;
+    float ma = neg_inf();
+    for (int s = 0; s < a.splits; ++s) ma = fmaxf(ma, P[(size_t)s * stride]);
+    float la = 0.f;
+    for (int s = 0; s < a.splits; ++s) {
+      const float ms = P[(size_t)s * stride];
+      la = fmaf(ms == neg_inf() ? 0.f : __builtin_amdgcn_exp2f(ms - ma), P[(size_t)s * stride + 1], la);
+    }
+    __syncthreads();
+    for (int j = tid; j < rv; j += kFrThreads) {
+      float z = 0.f;
+      for (int s = 0; s < a.splits; ++s) {
+        const float ms = P[(size_t)s * stride];
+        z = fmaf(ms == neg_inf() ? 0.f : __builtin_amdgcn_exp2f(ms - ma), P[(size_t)s * stride + 2 + j], z);
+      }
+      s_z[j] = z / la;
+    }
+    if (tid == 0) __hip_atomic_store(a.cnt + unit, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();
+  fr_epilogue<bf16_t>(a, h, unit, s_z, bad);
+}
+
+// ---------------------------------------------------------------------------
+// Plain kernel: one workgroup per (b, h), 32-token chunks.  K is rebuilt into
+// LDS in fp32 (one thread per (token, feature)), each of 32 threads rotates
+// the query to its key's position and takes the dot product, then the chunk
+// joins the online softmax and the latent-space value sum.
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void fullrope_plain_kernel(FullRopeArgs a) {
+  constexpr int kChunk = 32;
+  __shared__ float s_q[kMaxHead];
+  __shared__ double s_theta[kMaxHead / 2];
+  __shared__ float s_key[kChunk * kMaxHead];
+  __shared__ float s_sc[kChunk];
+  __shared__ float s_z[kMaxRank];
+  const int tid = threadIdx.x, b = blockIdx.x, h = blockIdx.y;
+  const int d = a.d, half = d / 2, rk = a.rk, rv = a.rv;
+  const int N = a.ctx_len ? a.ctx_len[b] : a.n_ctx;
+  const bool bad = (N < 1) || (N > a.n_ctx);
+  const int n_end = bad ? 0 : N;
+  const int pq = a.q_pos ? a.q_pos[b] : N - 1;
+  const size_t bh = (size_t)b * a.H + h;
+  const T* q = static_cast<const T*>(a.q) + bh * d;
+  for (int i = tid; i < d; i += 256) s_q[i] = Elem<T>::get(q, i) * a.qscale;
+  for (int f = tid; f < half; f += 256) s_theta[f] = pow(a.base, -2.0 * f / d);
+  const T* ck = static_cast<const T*>(a.ck) + bh * (size_t)a.n_max * rk;
+  const T* cv = static_cast<const T*>(a.cv) + bh * (size_t)a.n_max * rv;
+  const T* uk = static_cast<const T*>(a.uk) + (size_t)h * d * rk;
+  const T* mk = a.muk ? static_cast<const T*>(a.muk) + (size_t)h * d : nullptr;
+  // paged feature-major element (n, j) of a rank-r cache
+  auto at = [](int n, int j, int r) { return (size_t)(n / kPage) * kPage * r + (size_t)j * kPage + n % kPage; };
+  float z[2] = {0.f, 0.f};
+  float m_run = neg_inf(), l_run = 0.f;
+  __syncthreads();
+  for (int n0 = 0; n0 < n_end; n0 += kChunk) {
+    for (int e = tid; e < kChunk * d; e += 256) {
+      const int t = e % kChunk, i = e / kChunk, n = n0 + t;
+      float k = 0.f;
+      if (n < N) {
+        for (int j = 0; j < rk; ++j) k = fmaf(Elem<T>::get(uk, (size_t)i * rk + j), Elem<T>::get(ck, at(n, j, rk)), k);
+        if (mk) k += Elem<T>::get(mk, i);
+      }
+      s_key[t * d + i] = k;
+    }
+    __syncthreads();
+    if (tid < kChunk) {
+      const int n = n0 + tid;
+      float s = neg_inf();
+      if (n < N) {
+        s = 0.f;
+        for (int f = 0; f < half; ++f) {
+          float c, sn;
+          rot_cs((double)pq - (double)n, s_theta[f], c, sn);
+          const float w1 = s_q[f] * c - s_q[f + half] * sn, w2 = s_q[f + half] * c + s_q[f] * sn;
+          s = fmaf(w1, s_key[tid * d + f], fmaf(w2, s_key[tid * d + f + half], s));
+        }
+      }
+      s_sc[tid] = s;
+    }
+    __syncthreads();
+    float cm = neg_inf();
+    for (int t = 0; t < kChunk; ++t) cm = fmaxf(cm, s_sc[t]);
+    const float mn = fmaxf(m_run, cm);
+    const float alpha = m_run == neg_inf() ? 0.f : exp2f(m_run - mn);
+    float ls = 0.f;
+    for (int t = 0; t < kChunk; ++t) ls += s_sc[t] == neg_inf() ? 0.f : exp2f(s_sc[t] - mn);
+    l_run = l_run * alpha + ls;
+    for (int u = 0; u < 2; ++u) {
+      const int j = tid + 256 * u;
+      if (j < rv) {
+        float acc = z[u] * alpha;
+        for (int t = 0; t < kChunk && n0 + t < N; ++t)
+          acc = fmaf(exp2f(s_sc[t] - mn), Elem<T>::get(cv, at(n0 + t, j, rv)), acc);
+        z[u] = acc;
+      }
+    }
+    m_run = mn;
+    __syncthreads();
+  }
+  for (int u = 0; u < 2; ++u) {
+    const int j = tid + 256 * u;
+    if (j < rv) s_z[j] = z[u] / l_run;
+  }
+  __syncthreads();
+  fr_epilogue<T>(a, h, bh, s_z, bad);
+}
+
+template <int KS, int VR, int OCC>
+hipError_t launch_mfma(const FullRopeArgs& a, hipStream_t stream) {
+  const dim3 grid(a.B * a.splits, a.H);
+  if (a.muk)
+    hipLaunchKernelGGL((fullrope_mfma_kernel<KS, VR, true, OCC>), grid, dim3(kFrThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL((fullrope_mfma_kernel<KS, VR, false, OCC>), grid, dim3(kFrThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+template <int KS>
+hipError_t launch_vr(const FullRopeArgs& a, hipStream_t stream) {
+  constexpr int OCC = KS <= 12 ? 2 : 1;
+  const int vr = (a.rv + 31) / 32;
+  if (vr <= 2) return launch_mfma<KS, 2, OCC>(a, stream);
+  if (vr <= 4) return launch_mfma<KS, 4, OCC>(a, stream);
+  if (vr <= 6) return launch_mfma<KS, 6, OCC>(a, stream);
+  if (vr <= 8) return launch_mfma<KS, 8, OCC>(a, stream);
+  if (vr <= 10) return launch_mfma<KS, 10, OCC>(a, stream);
+  if (vr <= 12) return launch_mfma<KS, 12, OCC>(a, stream);
+  return launch_mfma<KS, 16, 1>(a, stream);
+}
+
+}  // namespace
+
+bool fullrope_mfma_ok(int dtype, int d_head, int r_k, int r_v) {
+  return dtype == LLA_BF16 && d_head == kFrD && r_k <= kFullRopeMaxRankK && r_v <= kMaxRank;
+}
+
+int fullrope_occupancy(int r_k) { return (r_k + 15) / 16 <= 12 ? 2 : 1; }
+
+hipError_t launch_decode_fullrope(const FullRopeArgs& a, hipStream_t stream) {
+  if (!fullrope_mfma_ok(a.dtype, a.d, a.rk, a.rv)) {
+    const dim3 grid(a.B, a.H);
+    if (a.dtype == LLA_BF16)
+      hipLaunchKernelGGL(fullrope_plain_kernel<bf16_t>, grid, dim3(256), 0, stream, a);
+    else
+      hipLaunchKernelGGL(fullrope_plain_kernel<float>, grid, dim3(256), 0, stream, a);
+    return hipGetLastError();
+  }
+  switch ((a.rk + 15) / 16) {
+    case 1: case 2: return launch_vr<2>(a, stream);
+    case 3: case 4: return launch_vr<4>(a, stream);
+    case 5: case 6: return launch_vr<6>(a, stream);
+    case 7: case 8: return launch_vr<8>(a, stream);
+    case 9: case 10: return launch_vr<10>(a, stream);
+    case 11: case 12: return launch_vr<12>(a, stream);
+    case 13: case 14: case 15: case 16: return launch_vr<16>(a, stream);
+    default: return launch_vr<18>(a, stream);
+  }
+}
+
+}  // namespace lla

@@ -342,6 +342,71 @@ lla_status lla_decode_attn_rope(int dtype, int out_dtype, int B, int H, int d_he
                      workspace, ws_bytes, stream);
 }
 
+lla_status lla_decode_attn_fullrope(int dtype, int out_dtype, int B, int H, int d_head, int r_k,
+                                    int r_v, int n_max, int n_ctx, const int32_t* ctx_len,
+                                    const int32_t* q_pos, const void* q, const void* c_k,
+                                    const void* c_v, const void* u_k, const void* u_v,
+                                    const void* mu_k, const void* mu_v, double base, float scale,
+                                    void* out, void* workspace, size_t ws_bytes, void* stream) {
+  if (!dtype_ok(dtype) || !dtype_ok(out_dtype) || B < 1 || H < 1 || !head_ok(d_head) ||
+      !rank_ok(r_k) || !rank_ok(r_v) || !cap_ok(n_max) || n_ctx < 1 || n_ctx > n_max ||
+      !std::isfinite(scale) || !(scale > 0.f) || !std::isfinite(base) || !(base > 1.0))
+    return LLA_ERR_INVALID_ARG;
+  if ((int64_t)B * H > (1 << 24)) return LLA_ERR_INVALID_ARG;
+  if (!ptr_ok(q) || !ptr_ok(c_k) || !ptr_ok(c_v) || !ptr_ok(u_k) || !ptr_ok(u_v) || !ptr_ok(out) ||
+      !opt_ptr_ok(mu_k) || !opt_ptr_ok(mu_v) ||
+      (ctx_len && (reinterpret_cast<uintptr_t>(ctx_len) & 3u)) ||
+      (q_pos && (reinterpret_cast<uintptr_t>(q_pos) & 3u)))
+    return LLA_ERR_INVALID_ARG;
+  if ((workspace == nullptr) != (ws_bytes == 0)) return LLA_ERR_WORKSPACE;
+  if (workspace && (!aligned16(workspace) || ws_bytes < workspace_bytes(B, H, r_v, n_ctx)))
+    return LLA_ERR_WORKSPACE;
+  lla::FullRopeArgs a{};
+  a.dtype = dtype;
+  a.out_dtype = out_dtype;
+  a.B = B;
+  a.H = H;
+  a.d = d_head;
+  a.rk = r_k;
+  a.rv = r_v;
+  a.n_max = n_max;
+  a.n_ctx = n_ctx;
+  a.ctx_len = ctx_len;
+  a.q_pos = q_pos;
+  a.q = q;
+  a.ck = c_k;
+  a.cv = c_v;
+  a.uk = u_k;
+  a.uv = u_v;
+  a.muk = mu_k;
+  a.muv = mu_v;
+  a.base = base;
+  a.qscale = (float)((double)scale * kLog2e);
+  a.out = out;
+  a.splits = 1;
+  // Split the context only for the MFMA kernel and only when the (b, h) units
+  // alone leave compute units without a resident workgroup; every split keeps
+  // at least 4 pages (the prologue forms the rotation constants and loads U_k).
+  if (workspace && lla::fullrope_mfma_ok(dtype, d_head, r_k, r_v)) {
+    static const int forced = env_int("LLA_FULLROPE_SPLITS");
+    const long target = (long)lla::fullrope_occupancy(r_k) * lla::device_cu_count();
+    const long units = (long)B * H;
+    long s = units < target ? (target + units - 1) / units : 1;
+    const long cap = ((n_ctx + LLA_PAGE_TOKENS - 1) / LLA_PAGE_TOKENS) / 4;
+    if (s > cap) s = cap;
+    if (forced > 0) s = forced;
+    if (s > max_splits(n_ctx)) s = max_splits(n_ctx);
+    a.splits = s < 1 ? 1 : (int)s;
+  }
+  if (a.splits > 1) {
+    const size_t units = (size_t)B * H;
+    const size_t counters = (units * sizeof(uint32_t) + 255) / 256 * 256;
+    a.cnt = static_cast<uint32_t*>(workspace);
+    a.part = reinterpret_cast<float*>(static_cast<char*>(workspace) + counters);
+  }
+  return hip_status(lla::launch_decode_fullrope(a, static_cast<hipStream_t>(stream)));
+}
+
 namespace {
 lla_status prefill_impl(int dtype, int out_dtype, int B, int H, int M, int d_head, int r_k, int r_v,
                         int d_rope, int H_rope, int n_max, int p0, const void* q,

@@ -116,6 +116,32 @@ struct RopeArgs {
 hipError_t launch_rope_write(const RopeArgs& a, hipStream_t stream);
 hipError_t launch_rope_rotate(const RopeArgs& a, hipStream_t stream);
 
+// Full-RoPE reconstruct-then-attend decode (keys rebuilt and rotated per position).
+constexpr int kFullRopeMaxRankK = 288;  // largest r_k of the MFMA kernel
+struct FullRopeArgs {
+  int dtype, out_dtype;
+  int B, H, d, rk, rv, n_max, n_ctx;
+  int splits;               // workgroups per (b, h) along the context
+  const int32_t* ctx_len;   // [B] or null (n_ctx)
+  const int32_t* q_pos;     // [B] query positions or null (N_b - 1)
+  const void* q;            // [B][H][d] unrotated queries
+  const void* ck;           // paged latents, like the absorbed decode
+  const void* cv;
+  const void* uk;           // [H][d][rk]
+  const void* uv;           // [H][d][rv]
+  const void* muk;          // [H][d] or null
+  const void* muv;          // [H][d] or null
+  double base;              // RoPE base
+  float qscale;             // softmax scale * log2(e)
+  void* out;                // [B][H][d]
+  float* part;              // [B*H][splits][rv + 2] split partials (m, l, z)
+  uint32_t* cnt;            // [B*H] arrival counters
+};
+
+hipError_t launch_decode_fullrope(const FullRopeArgs& a, hipStream_t stream);
+bool fullrope_mfma_ok(int dtype, int d_head, int r_k, int r_v);  // the MFMA kernel takes this shape
+int fullrope_occupancy(int r_k);  // resident workgroups per compute unit of the MFMA kernel
+
 int device_cu_count();  // compute units of the current device (cached)
 
 }  // namespace lla

@@ -51,6 +51,8 @@ _SIGS = {
     "lla_encode_2d_workspace_bytes": (_c_int, [_c_int] * 7 + [ctypes.POINTER(_c_sz)]),
     "lla_decode_2d_workspace_bytes": (_c_int, [_c_int] * 5 + [ctypes.POINTER(_c_sz)]),
     "lla_decode_attn_2d": (_c_int, [_c_int] * 9 + [_c_vp] * 8 + [_c_f, _c_vp, _c_vp, _c_sz, _c_vp]),
+    "lla_decode_attn_fullrope": (_c_int, [_c_int] * 9 + [_c_vp] * 9 + [ctypes.c_double, _c_f, _c_vp, _c_vp,
+                                                                          _c_sz, _c_vp]),
 }
 
 _lib = None
@@ -454,4 +456,45 @@ def decode_attn_2d(q, c_k, c_v, u_k, u_v, *, n_ctx: int, ctx_len=None, mu_k=None
                                     _ptr(ctx_len), _ptr(q), _ptr(c_k), _ptr(c_v), _ptr(u_k), _ptr(u_v),
                                     _ptr(mu_k), _ptr(mu_v), float(scale), _ptr(out), _ptr(workspace),
                                     workspace.numel() * workspace.element_size(), _stream(q)))
+    return out
+
+
+def decode_attn_fullrope(q, c_k, c_v, u_k, u_v, *, n_ctx: int, ctx_len=None, q_pos=None, mu_k=None,
+                         mu_v=None, base: float = 10000.0, scale: float | None = None, out=None,
+                         out_dtype=torch.float32, workspace=None):
+    """Loop-l decode with full RoPE (reconstruct-then-attend) of q [B, H, d]
+    (unrotated) over the paged latent cache: keys are rebuilt with U_k and
+    rotated at their slot positions, the query at q_pos (int32 device tensor
+    [B]; None means each sequence's newest cached token, N_b - 1).  Other
+    arguments as decode_attn; the default scale is 1/sqrt(d).  Returns out [B, H, d]."""
+    dev = q.device
+    B, H, d = q.shape
+    for t, n in ((q, "q"), (c_k, "c_k"), (c_v, "c_v"), (u_k, "u_k"), (u_v, "u_v")):
+        _need(t, n, q.dtype, dev)
+    for t, n in ((mu_k, "mu_k"), (mu_v, "mu_v")):
+        if t is not None:
+            _need(t, n, q.dtype, dev)
+    r_k, r_v = u_k.shape[2], u_v.shape[2]
+    n_max = c_k.shape[2] * PAGE
+    if (c_k.shape != (B, H, n_max // PAGE, r_k, PAGE) or c_v.shape != (B, H, n_max // PAGE, r_v, PAGE)
+            or u_k.shape != (H, d, r_k) or u_v.shape != (H, d, r_v)):
+        raise ValueError("inconsistent shapes")
+    for t, n in ((ctx_len, "ctx_len"), (q_pos, "q_pos")):
+        if t is not None:
+            _need(t, n, torch.int32, dev)
+            if t.shape != (B,):
+                raise ValueError(f"{n} must have shape [B]")
+    if out is None:
+        out = torch.empty((B, H, d), dtype=out_dtype, device=dev)
+    else:
+        _need(out, "out", None, dev)
+    if workspace is not None:
+        _need(workspace, "workspace", None, dev)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    _check(lib().lla_decode_attn_fullrope(_dt(q), _out_code(out.dtype), B, H, d, r_k, r_v, n_max, n_ctx,
+                                          _ptr(ctx_len), _ptr(q_pos), _ptr(q), _ptr(c_k), _ptr(c_v), _ptr(u_k),
+                                          _ptr(u_v), _ptr(mu_k), _ptr(mu_v), float(base), float(scale),
+                                          _ptr(out), _ptr(workspace), ws_bytes, _stream(q)))
     return out

@@ -33,14 +33,15 @@ def test_header_declares_the_boundary():
                             "lla_prefill_attn", "lla_rope_write", "lla_rope_rotate",
                             "lla_decode_attn_rope", "lla_prefill_attn_rope", "lla_encode_ring",
                             "lla_rope_write_ring", "lla_encode_2d", "lla_encode_2d_workspace_bytes",
-                            "lla_decode_2d_workspace_bytes", "lla_decode_attn_2d"])
+                            "lla_decode_2d_workspace_bytes", "lla_decode_attn_2d",
+                            "lla_decode_attn_fullrope"])
 
 
 def test_library_exports_every_declared_symbol():
     h = ctypes.CDLL(lla.LIB_PATH)
     for name in _declared():
         assert hasattr(h, name), name
-    assert lla.abi_version() == 5
+    assert lla.abi_version() == 6
 
 
 def test_status_strings():
@@ -325,3 +326,27 @@ def test_encode_2d_workspace_only_for_split_writes():
     assert lla.encode_2d_workspace_bytes(32, 1, 16, 4, 128, 288, 480) > 0
     assert lla.encode_2d_workspace_bytes(4, 1024, 16, 4, 128, 288, 480) == 0
     assert lla.encode_2d_workspace_bytes(32, 1, 4, 1, 64, 288, 480) == 0  # stack of 256
+
+
+# ---- full-RoPE reconstruct-then-attend decode ----
+
+def _decode_fullrope(**kw):
+    a = dict(dtype=1, out_dtype=0, B=2, H=16, d=128, rk=192, rv=320, n_max=512, n_ctx=512, ctx_len=None,
+             q_pos=None, q=P, ck=P, cv=P, uk=P, uv=P, muk=None, muv=None, base=10000.0, scale=0.088, out=P,
+             ws=None, ws_bytes=0, stream=None)
+    a.update(kw)
+    return lla.lib().lla_decode_attn_fullrope(a["dtype"], a["out_dtype"], a["B"], a["H"], a["d"], a["rk"],
+                                              a["rv"], a["n_max"], a["n_ctx"], a["ctx_len"], a["q_pos"], a["q"],
+                                              a["ck"], a["cv"], a["uk"], a["uv"], a["muk"], a["muv"], a["base"],
+                                              a["scale"], a["out"], a["ws"], a["ws_bytes"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dtype=2), 1), (dict(B=0), 1), (dict(d=48), 1), (dict(rk=0), 1), (dict(rv=513), 1),
+    (dict(n_max=100), 1), (dict(n_ctx=0), 1), (dict(n_ctx=513), 1), (dict(scale=0.0), 1),
+    (dict(base=1.0), 1), (dict(base=float("inf")), 1), (dict(q=None), 1), (dict(ck=MIS), 1),
+    (dict(muk=MIS), 1), (dict(q_pos=P + 2), 1), (dict(ctx_len=P + 1), 1),
+    (dict(ws=P, ws_bytes=0), 3), (dict(ws=P, ws_bytes=64), 3), (dict(ws=MIS, ws_bytes=1 << 30), 3),
+])
+def test_decode_fullrope_rejects(kw, code):
+    assert _decode_fullrope(**kw) == code
