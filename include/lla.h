@@ -223,7 +223,7 @@ lla_status lla_prefill_attn(int dtype, int out_dtype, int B, int H, int M, int d
  *   scale    softmax scale, the teacher's 1/sqrt(d_head)
  *   other arguments as for lla_decode_attn; the workspace is the one sized by
  *   lla_decode_workspace_bytes (the context may be split over workgroups).
- * bf16 with d_head = 128 and r_k <= 288 runs on bf16 MFMA (fp32 accumulation,
+ * bf16 with d_head = 128 and r_k <= 256 runs on bf16 MFMA (fp32 accumulation,
  * keys reconstructed exactly from bf16 operands); fp32 and other shapes run a
  * plain fp32 kernel.
  * Errors: LLA_ERR_INVALID_ARG, LLA_ERR_WORKSPACE, LLA_ERR_HIP.

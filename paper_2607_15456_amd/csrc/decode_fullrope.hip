@@ -11,12 +11,12 @@
 // With n = n0 + t (n0 a 32-token tile base) the query weight of token t is
 // RoPE(QP, -t), QP = RoPE(q, p_q - n0): QP is formed once per tile (angle in
 // double precision), and cos / sin of t * theta_f, the same for every tile,
-// stay in registers.
+// are tabulated in LDS once per workgroup.
 //
 // bf16 kernel (d_head = 128): a workgroup of 4 wavefronts takes one (b, h)
 // and a range of 64-token pages.  Wavefront m rebuilds rows 32m .. 32m + 31
 // of K^T for both 32-token tiles of every page on v_mfma_f32_32x32x16_bf16:
-//   A = U_k rows 32m + i (held in registers for the whole scan),
+//   A = U_k rows 32m + i (staged in LDS once per workgroup),
 //   B = the key page, staged in LDS with XOR-swizzled 16-byte chunks and read
 //       with ds_read_b64_tr_b16 (lane l gets one token's 4 features),
 // so lane (col + 32 g), register r holds K[32m + 8(r/4) + 4g + r%4][token col].
@@ -25,7 +25,8 @@
 // one barrier per page), and every wavefront runs the same online softmax.
 // Values: wavefront m owns latent rows [8 VR m, 8 VR (m + 1)) and streams them
 // with 16-byte loads of 8 tokens, as in the absorbed decode.  Key pages are
-// loaded into registers one page ahead and written to a two-slot LDS ring.
+// loaded into registers two pages ahead and written to a two-slot LDS ring;
+// value pages are loaded two pages ahead (two register sets alternate).
 //
 // A plain kernel (one thread per token and feature, reconstruction in fp32)
 // serves fp32 inputs and every shape the MFMA kernel does not take.
@@ -70,6 +71,29 @@ __device__ __forceinline__ void rot_cs(double p, double theta, float& c, float& 
   sincosf((float)r, &s, &c);
 }
 
+// Lane exchanges without LDS: DPP within 8-lane groups, permlane32 swap
+// across the two wave halves.
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+// over lanes 8k .. 8k + 7: quad xor 1, quad xor 2, then mirror within 8 lanes
+__device__ __forceinline__ float max8(float x) {
+  x = fmaxf(x, dpp<0xB1>(x));
+  x = fmaxf(x, dpp<0x4E>(x));
+  return fmaxf(x, dpp<0x141>(x));
+}
+__device__ __forceinline__ float sum8(float x) {
+  x += dpp<0xB1>(x);
+  x += dpp<0x4E>(x);
+  return x + dpp<0x141>(x);
+}
+// x[lane] + x[lane ^ 32]
+__device__ __forceinline__ float sum_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
@@ -111,7 +135,14 @@ void fullrope_mfma_kernel(FullRopeArgs a) {
   constexpr int KI = RKP / 8;             // 8-row load instructions per key page
   constexpr int KD = (KI + kFrWaves - 1) / kFrWaves;  // ... per wavefront
   constexpr int kSlot = RKP * kPage;      // bf16 elements of one staged page
+  constexpr int US = RKP + 8;             // U_k row stride (bf16): 16-byte reads of 16 rows hit distinct banks
   __shared__ __attribute__((aligned(16))) bf16_t s_k[2 * kSlot];
+  __shared__ __attribute__((aligned(16))) bf16_t s_u[kFrD * US];
+  // cos / sin of t * theta_f for token offsets t < 32 and the 64 frequencies,
+  // [half][t][f - 32 half], each row rotated by 4 (t / 2) floats so that lanes
+  // reading different t hit different banks
+  __shared__ __attribute__((aligned(16))) float s_cos[2][32][32];
+  __shared__ __attribute__((aligned(16))) float s_sin[2][32][32];
   __shared__ __attribute__((aligned(16))) float s_qp[kFrWaves][2][2][32];  // [wave][tile][re/im][freq]
   __shared__ __attribute__((aligned(16))) float s_sc[2][kFrWaves][kPage];  // partial scores
   __shared__ float s_z[kMaxRank];
@@ -132,38 +163,39 @@ void fullrope_mfma_kernel(FullRopeArgs a) {
   const size_t bh = (size_t)b * a.H + h;
   const int rk = a.rk, rv = a.rv;
 
-  // ---- U_k rows 32 wave + col, features 16 s + 8 g .. +7: the A operands ----
-  uint4 ua[KS];
+  // ---- U_k of head h into LDS (rows = features of K, columns past r_k zero) ----
   {
-    const bf16_t* urow = static_cast<const bf16_t*>(a.uk) + ((size_t)h * kFrD + 32 * wave + col) * rk;
-#pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      const int j0 = 16 * s + 8 * g;
+    const bf16_t* uk = static_cast<const bf16_t*>(a.uk) + (size_t)h * kFrD * rk;
+    constexpr int C8 = US / 8;  // 16-byte chunks per LDS row
+    for (int e = tid; e < kFrD * C8; e += kFrThreads) {
+      const int i = e / C8, j0 = 8 * (e - i * C8);
+      uint4 v;
       if ((rk & 7) == 0) {
-        ua[s] = j0 < rk ? *reinterpret_cast<const uint4*>(urow + j0) : uint4{0, 0, 0, 0};
+        v = j0 < rk ? *reinterpret_cast<const uint4*>(uk + (size_t)i * rk + j0) : uint4{0, 0, 0, 0};
       } else {
         uint32_t w[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const uint32_t x0 = j0 + 2 * e < rk ? urow[j0 + 2 * e] : 0u;
-          const uint32_t x1 = j0 + 2 * e + 1 < rk ? urow[j0 + 2 * e + 1] : 0u;
-          w[e] = x0 | (x1 << 16);
+        for (int x = 0; x < 4; ++x) {
+          const uint32_t x0 = j0 + 2 * x < rk ? uk[(size_t)i * rk + j0 + 2 * x] : 0u;
+          const uint32_t x1 = j0 + 2 * x + 1 < rk ? uk[(size_t)i * rk + j0 + 2 * x + 1] : 0u;
+          w[x] = x0 | (x1 << 16);
         }
-        ua[s] = uint4{w[0], w[1], w[2], w[3]};
+        v = uint4{w[0], w[1], w[2], w[3]};
       }
+      *reinterpret_cast<uint4*>(&s_u[i * US + j0]) = v;
+    }
+    for (int e = tid; e < 2 * 32 * 32; e += kFrThreads) {
+      const int hf = e >> 10, t = (e >> 5) & 31, fr = e & 31;
+      float c, sn;
+      rot_cs((double)t, pow(a.base, -2.0 * (32 * hf + fr) / kFrD), c, sn);
+      s_cos[hf][t][(fr + 4 * (t >> 1)) & 31] = c;
+      s_sin[hf][t][(fr + 4 * (t >> 1)) & 31] = sn;
     }
   }
-  // ---- rotation constants ----
   // Lane (col, g), register r of tile `wave`: feature i = 32 wave + fr(r) with
   // fr(r) = 8 (r/4) + 4 g + r%4, frequency f = i mod 64 = 32 (wave & 1) + fr(r).
-  // cos / sin of col * theta_f (token offset inside a 32-token tile).
   const bool first_half = wave < 2;
-  float cs_c[16], cs_s[16];
-#pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const int f = 32 * (wave & 1) + 8 * (r / 4) + 4 * g + r % 4;
-    rot_cs((double)col, pow(a.base, -2.0 * f / kFrD), cs_c[r], cs_s[r]);
-  }
+  const int hf = wave & 1;
   // query rotation: lane (fq = col, tile tq = g) forms QP for frequency
   // 32 (wave & 1) + fq of tile tq of every page
   const int fq = 32 * (wave & 1) + col;
@@ -203,40 +235,39 @@ void fullrope_mfma_kernel(FullRopeArgs a) {
   // value rows of this wavefront: 8 VR wave + 8 k + hi, tokens 8 lo .. 8 lo + 7
   const int vrow0 = 8 * VR * wave;
 
-  uint4 kreg[KD];
-  // Rows past r_k are zero.  A lane whose row is past r_k reads row r_k - 1
-  // instead (every address stays inside the page's r_k rows) and drops it.
-  auto kload = [&](int p) {
+  // Two register sets of key and value loads alternate between even and odd
+  // pages, so every load is issued two pages before it is used.
+  uint4 kA[KD], kB[KD], vA[VR], vB[VR];
+  // A lane whose row is past r_k reads row r_k - 1 instead (every address
+  // stays inside the page's r_k rows); rows past r_k are stored as zeros.  The
+  // loaded registers are not touched until they are stored, so no wait is
+  // needed before the next page's loads are issued.
+  // Every lane issues every load (instructions wholly past r_k re-read the
+  // last rows), so the compiler's waits count loads exactly.
+  auto kload = [&](uint4 (&kr)[KD], int p) {
+#pragma unroll
+    for (int u = 0; u < KD; ++u) {
+      const int k8 = min(8 * (wave + kFrWaves * u), (rk - 1) & ~7);  // first row of the instruction
+      const int voff = (min(k8 + krow, rk - 1) - k8) * (kPage * 2) + (lane & 7) * 16;
+      kr[u] = buf_ld16(ksrc, voff, p * kpage + k8 * kPage * 2);
+    }
+  };
+  auto kstore = [&](const uint4 (&kr)[KD], int slot) {
 #pragma unroll
     for (int u = 0; u < KD; ++u) {
       const int k = wave + kFrWaves * u;
-      const int row = 8 * k + krow;
-      if (k < KI && 8 * k < rk) {  // uniform
-        const int voff = (min(row, rk - 1) - 8 * k) * (kPage * 2) + (lane & 7) * 16;
-        const uint4 v = buf_ld16(ksrc, voff, p * kpage + 8 * k * kPage * 2);
-        kreg[u] = row < rk ? v : uint4{0, 0, 0, 0};
-      } else {
-        kreg[u] = uint4{0, 0, 0, 0};
-      }
+      const bool live = 8 * k + krow < rk;
+      *reinterpret_cast<uint4*>(&s_k[slot * kSlot + 8 * k * kPage + kdst]) = live ? kr[u] : uint4{0, 0, 0, 0};
     }
   };
-  auto kstore = [&](int slot) {
-#pragma unroll
-    for (int u = 0; u < KD; ++u) {
-      const int k = wave + kFrWaves * u;
-      if (k < KI) *reinterpret_cast<uint4*>(&s_k[slot * kSlot + 8 * k * kPage + kdst]) = kreg[u];
-    }
-  };
-  uint4 vreg[VR];
-  // A lane whose row is past r_v reads row r_v - 1 (never used).
-  auto vload = [&](int p) {
+  // A lane whose row is past r_v reads row r_v - 1 (never used); every lane
+  // issues every load, as for the keys.
+  auto vload = [&](uint4 (&vr)[VR], int p) {
 #pragma unroll
     for (int k = 0; k < VR; ++k) {
-      const int j0 = vrow0 + 8 * k;
-      if (j0 < rv) {  // uniform: the 8-row group starts inside r_v
-        const int voff = (min(j0 + hi, rv - 1) - j0) * (kPage * 2) + lo * 16;
-        vreg[k] = buf_ld16(vsrc, voff, p * vpage + j0 * kPage * 2);
-      }
+      const int j0 = min(vrow0 + 8 * k, rv - 1);
+      const int voff = (min(vrow0 + 8 * k + hi, rv - 1) - j0) * (kPage * 2) + lo * 16;
+      vr[k] = buf_ld16(vsrc, voff, p * vpage + j0 * kPage * 2);
     }
   };
 
@@ -244,23 +275,65 @@ void fullrope_mfma_kernel(FullRopeArgs a) {
 #pragma unroll
   for (int k = 0; k < VR; ++k) zacc[k] = 0.f;
   float m_run = neg_inf(), l_lane = 0.f;
+  // softmax weights of the last scored page and its rescale factor; its value
+  // products run at the start of the next page
+  float pr[8], alpha = 1.f;
 
-  if (pb < pe) {
-    kload(pb);
-    kstore(0);
-    if (pb + 1 < pe) kload(pb + 1);
-    vload(pb);
-  }
-  __syncthreads();
+  // z[row] = alpha z[row] + sum over the lane's 8 tokens of pr * value; on the
+  // context's last page, value slots past N (which may hold anything) are zeroed
+  auto vconsume = [&](const uint4 (&vr)[VR], int p) {
+#pragma unroll
+    for (int k = 0; k < VR; ++k) zacc[k] *= alpha;
+    const int nv = N - (p * kPage + 8 * lo);  // valid tokens of this lane's slice
+    if ((p + 1) * kPage > N) {  // uniform
+      uint32_t keep[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) keep[i] = nv > 2 * i + 1 ? 0xffffffffu : nv > 2 * i ? 0x0000ffffu : 0u;
+#pragma unroll
+      for (int k = 0; k < VR; ++k) {
+        if (vrow0 + 8 * k < rv) {  // uniform
+          const uint4 w = uint4{vr[k].x & keep[0], vr[k].y & keep[1], vr[k].z & keep[2], vr[k].w & keep[3]};
+          float v[8];
+          Elem<bf16_t>::unpack(w, v);
+          float t = 0.f;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) t = fmaf(pr[e], v[e], t);
+          zacc[k] += t;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < VR; ++k) {
+        if (vrow0 + 8 * k < rv) {  // uniform
+          float v[8];
+          Elem<bf16_t>::unpack(vr[k], v);
+          float t = 0.f;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) t = fmaf(pr[e], v[e], t);
+          zacc[k] += t;
+        }
+      }
+    }
+  };
 
-  for (int p = pb; p < pe; ++p) {
-    const int slot = (p - pb) & 1;
+  // Page p = pb + i.  Set (i + 1) % 2 of the key and value registers holds
+  // page p + 1's keys and page p - 1's values on entry: the keys go to LDS and
+  // page p + 3's are requested, the values are multiplied and page p + 1's
+  // requested -- all before this page's products, so two pages of keys and of
+  // values stay in flight while the wavefront computes.  Past the last page
+  // the loads re-read it: every load is issued, so the waits count exactly.
+  auto body = [&](int i, uint4 (&kr)[KD], uint4 (&vr)[VR]) {
+    const int p = pb + i, slot = i & 1;
+    kstore(kr, slot ^ 1);
+    kload(kr, min(p + 3, pe - 1));
+    if (i > 0) vconsume(vr, p - 1);
+    vload(vr, min(p + 1, pe - 1));
     // ---- rotated query of this page's two tiles ----
     {
-      float c, s;
-      rot_cs((double)pq - (double)(p * kPage + 32 * g), theta_q, c, s);
-      s_qp[wave][g][0][col] = q1 * c - q2 * s;
-      s_qp[wave][g][1][col] = q2 * c + q1 * s;
+      float c, sn;
+      rot_cs((double)pq - (double)(p * kPage + 32 * g), theta_q, c, sn);
+      s_qp[wave][g][0][col] = q1 * c - q2 * sn;
+      s_qp[wave][g][1][col] = q2 * c + q1 * sn;
     }
     // ---- K^T rows 32 wave .. +31 of both tiles ----
     f32x16 acc[2];
@@ -272,15 +345,25 @@ void fullrope_mfma_kernel(FullRopeArgs a) {
     const bf16_t* kb = &s_k[slot * kSlot];
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
+      const uint4 ua = *reinterpret_cast<const uint4*>(&s_u[(32 * wave + col) * US + 16 * s + 8 * g]);
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) {
         const uint2 r0 = lds_tr16(kb + troff[nt] + 16 * s * kPage);
         const uint2 r1 = lds_tr16(kb + troff[nt] + (16 * s + 4) * kPage);
-        acc[nt] = mfma32(ua[s], uint4{r0.x, r0.y, r1.x, r1.y}, acc[nt]);
+        acc[nt] = mfma32(ua, uint4{r0.x, r0.y, r1.x, r1.y}, acc[nt]);
       }
     }
     wave_sync();
     // ---- rotated dot products: this lane's 16 features of token col ----
+    float cs_c[16], cs_s[16];
+#pragma unroll
+    for (int a4 = 0; a4 < 4; ++a4) {
+      const int f0 = (8 * a4 + 4 * g + 4 * (col >> 1)) & 31;
+      const float4 c4 = *reinterpret_cast<const float4*>(&s_cos[hf][col][f0]);
+      const float4 s4 = *reinterpret_cast<const float4*>(&s_sin[hf][col][f0]);
+      cs_c[4 * a4] = c4.x; cs_c[4 * a4 + 1] = c4.y; cs_c[4 * a4 + 2] = c4.z; cs_c[4 * a4 + 3] = c4.w;
+      cs_s[4 * a4] = s4.x; cs_s[4 * a4 + 1] = s4.y; cs_s[4 * a4 + 2] = s4.z; cs_s[4 * a4 + 3] = s4.w;
+    }
     float part[2];
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt) {
@@ -298,14 +381,9 @@ void fullrope_mfma_kernel(FullRopeArgs a) {
           sum = fmaf(w, acc[nt][r], sum);
         }
       }
-      part[nt] = sum + __shfl_xor(sum, 32, kWave);
+      part[nt] = sum_halves(sum);
     }
     s_sc[slot][wave][lane] = g ? part[1] : part[0];  // lane = token 32 g + col
-    // ---- next key page into the other ring slot, the one after into registers ----
-    if (p + 1 < pe) {
-      kstore(slot ^ 1);
-      if (p + 2 < pe) kload(p + 2);
-    }
     __syncthreads();
 
     // ---- softmax over the page: lane (hi, lo) holds tokens 8 lo .. 8 lo + 7 ----
@@ -333,50 +411,47 @@ void fullrope_mfma_kernel(FullRopeArgs a) {
       if (n0 + e >= N) sc[e] = neg_inf();
       mx = fmaxf(mx, sc[e]);
     }
-    mx = fmaxf(mx, __shfl_xor(mx, 1, kWave));
-    mx = fmaxf(mx, __shfl_xor(mx, 2, kWave));
-    mx = fmaxf(mx, __shfl_xor(mx, 4, kWave));
+    mx = max8(mx);
+    alpha = 1.f;
     if (mx > m_run) {
-      const float alpha = __builtin_amdgcn_exp2f(m_run - mx);
+      alpha = __builtin_amdgcn_exp2f(m_run - mx);
       l_lane *= alpha;
-#pragma unroll
-      for (int k = 0; k < VR; ++k) zacc[k] *= alpha;
       m_run = mx;
     }
-    float pr[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       pr[e] = __builtin_amdgcn_exp2f(sc[e] - m_run);  // exp2(-inf) = 0 past N
       l_lane += pr[e];
     }
-    // ---- values: z[row] += sum over the lane's 8 tokens ----
-    const bool tail = (p + 1) * kPage > N;
-#pragma unroll
-    for (int k = 0; k < VR; ++k) {
-      if (vrow0 + 8 * k < rv && vrow0 + 8 * k + hi < rv) {
-        float v[8];
-        Elem<bf16_t>::unpack(vreg[k], v);
-        if (tail) {  // slots past the context may hold anything
-#pragma unroll
-          for (int e = 0; e < 8; ++e)
-            if (n0 + e >= N) v[e] = 0.f;
-        }
-        float t = 0.f;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) t = fmaf(pr[e], v[e], t);
-        zacc[k] += t;
-      }
-    }
-    if (p + 1 < pe) vload(p + 1);
+  };
+
+  // Prologue: page pb's keys into slot 0; keys of pb + 1 in set B, pb + 2 in
+  // set A; values of pb in set A (set B is loaded by the first page).
+  if (pb < pe) {
+    kload(kA, pb);
+    kstore(kA, 0);
+    kload(kB, min(pb + 1, pe - 1));
+    kload(kA, min(pb + 2, pe - 1));
+    vload(vA, pb);
+  }
+  __syncthreads();
+  const int npg = pe - pb;
+  int i = 0;
+  for (; i + 1 < npg; i += 2) {
+    body(i, kB, vB);
+    body(i + 1, kA, vA);
+  }
+  if (i < npg) {
+    body(i, kB, vB);
+    vconsume(vA, pe - 1);  // npg odd: the last page's values are in set A
+  } else if (npg > 0) {
+    vconsume(vB, pe - 1);  // npg even: in set B
   }
 
   // ---- reductions: z over token slices, l over token slices ----
+  l_lane = sum8(l_lane);
 #pragma unroll
-  for (int off = 1; off < 8; off <<= 1) {
-    l_lane += __shfl_xor(l_lane, off, kWave);
-#pragma unroll
-    for (int k = 0; k < VR; ++k) zacc[k] += __shfl_xor(zacc[k], off, kWave);
-  }
+  for (int k = 0; k < VR; ++k) zacc[k] = sum8(zacc[k]);
   if (lo == 0) {
 #pragma unroll
     for (int k = 0; k < VR; ++k) {
@@ -532,17 +607,37 @@ hipError_t launch_mfma(const FullRopeArgs& a, hipStream_t stream) {
   return hipGetLastError();
 }
 
+// Resident wavefronts per SIMD: 2 while the registers fit in 256 (two key and
+// two value load sets, accumulators, z, the rotation constants of a page and
+// about 80 more), else 1.  The LDS of two workgroups must fit as well.
+constexpr int fr_occ(int KS, int VR) {
+  return 2 * 4 * ((KS * 2 + kFrWaves - 1) / kFrWaves) + 2 * 4 * VR + VR + 32 + 32 + 80 <= 256 &&
+                 2 * (2 * KS * 16 * kPage * 2 + kFrD * (KS * 16 + 8) * 2 + 16384 + 4096 + 3072) <= 160 * 1024
+             ? 2
+             : 1;
+}
+
+// Template buckets: K-steps of 16 key features, 8-row value groups per wavefront.
+int ks_bucket(int r_k) {
+  const int ks = (r_k + 15) / 16;
+  return ks <= 2 ? 2 : ks <= 4 ? 4 : ks <= 6 ? 6 : ks <= 8 ? 8 : ks <= 10 ? 10 : ks <= 12 ? 12 : 16;
+}
+int vr_bucket(int r_v) {
+  const int vr = (r_v + 31) / 32;
+  return vr <= 2 ? 2 : vr <= 4 ? 4 : vr <= 6 ? 6 : vr <= 8 ? 8 : vr <= 10 ? 10 : vr <= 12 ? 12 : 16;
+}
+
 template <int KS>
 hipError_t launch_vr(const FullRopeArgs& a, hipStream_t stream) {
-  constexpr int OCC = KS <= 12 ? 2 : 1;
-  const int vr = (a.rv + 31) / 32;
-  if (vr <= 2) return launch_mfma<KS, 2, OCC>(a, stream);
-  if (vr <= 4) return launch_mfma<KS, 4, OCC>(a, stream);
-  if (vr <= 6) return launch_mfma<KS, 6, OCC>(a, stream);
-  if (vr <= 8) return launch_mfma<KS, 8, OCC>(a, stream);
-  if (vr <= 10) return launch_mfma<KS, 10, OCC>(a, stream);
-  if (vr <= 12) return launch_mfma<KS, 12, OCC>(a, stream);
-  return launch_mfma<KS, 16, 1>(a, stream);
+  switch (vr_bucket(a.rv)) {
+    case 2: return launch_mfma<KS, 2, fr_occ(KS, 2)>(a, stream);
+    case 4: return launch_mfma<KS, 4, fr_occ(KS, 4)>(a, stream);
+    case 6: return launch_mfma<KS, 6, fr_occ(KS, 6)>(a, stream);
+    case 8: return launch_mfma<KS, 8, fr_occ(KS, 8)>(a, stream);
+    case 10: return launch_mfma<KS, 10, fr_occ(KS, 10)>(a, stream);
+    case 12: return launch_mfma<KS, 12, fr_occ(KS, 12)>(a, stream);
+    default: return launch_mfma<KS, 16, fr_occ(KS, 16)>(a, stream);
+  }
 }
 
 }  // namespace
@@ -551,7 +646,7 @@ bool fullrope_mfma_ok(int dtype, int d_head, int r_k, int r_v) {
   return dtype == LLA_BF16 && d_head == kFrD && r_k <= kFullRopeMaxRankK && r_v <= kMaxRank;
 }
 
-int fullrope_occupancy(int r_k) { return (r_k + 15) / 16 <= 12 ? 2 : 1; }
+int fullrope_occupancy(int r_k, int r_v) { return fr_occ(ks_bucket(r_k), vr_bucket(r_v)); }
 
 hipError_t launch_decode_fullrope(const FullRopeArgs& a, hipStream_t stream) {
   if (!fullrope_mfma_ok(a.dtype, a.d, a.rk, a.rv)) {
@@ -562,15 +657,14 @@ hipError_t launch_decode_fullrope(const FullRopeArgs& a, hipStream_t stream) {
       hipLaunchKernelGGL(fullrope_plain_kernel<float>, grid, dim3(256), 0, stream, a);
     return hipGetLastError();
   }
-  switch ((a.rk + 15) / 16) {
-    case 1: case 2: return launch_vr<2>(a, stream);
-    case 3: case 4: return launch_vr<4>(a, stream);
-    case 5: case 6: return launch_vr<6>(a, stream);
-    case 7: case 8: return launch_vr<8>(a, stream);
-    case 9: case 10: return launch_vr<10>(a, stream);
-    case 11: case 12: return launch_vr<12>(a, stream);
-    case 13: case 14: case 15: case 16: return launch_vr<16>(a, stream);
-    default: return launch_vr<18>(a, stream);
+  switch (ks_bucket(a.rk)) {
+    case 2: return launch_vr<2>(a, stream);
+    case 4: return launch_vr<4>(a, stream);
+    case 6: return launch_vr<6>(a, stream);
+    case 8: return launch_vr<8>(a, stream);
+    case 10: return launch_vr<10>(a, stream);
+    case 12: return launch_vr<12>(a, stream);
+    default: return launch_vr<16>(a, stream);
   }
 }
 

@@ -389,7 +389,7 @@ lla_status lla_decode_attn_fullrope(int dtype, int out_dtype, int B, int H, int 
   // at least 4 pages (the prologue forms the rotation constants and loads U_k).
   if (workspace && lla::fullrope_mfma_ok(dtype, d_head, r_k, r_v)) {
     static const int forced = env_int("LLA_FULLROPE_SPLITS");
-    const long target = (long)lla::fullrope_occupancy(r_k) * lla::device_cu_count();
+    const long target = (long)lla::fullrope_occupancy(r_k, r_v) * lla::device_cu_count();
     const long units = (long)B * H;
     long s = units < target ? (target + units - 1) / units : 1;
     const long cap = ((n_ctx + LLA_PAGE_TOKENS - 1) / LLA_PAGE_TOKENS) / 4;

@@ -117,7 +117,7 @@ hipError_t launch_rope_write(const RopeArgs& a, hipStream_t stream);
 hipError_t launch_rope_rotate(const RopeArgs& a, hipStream_t stream);
 
 // Full-RoPE reconstruct-then-attend decode (keys rebuilt and rotated per position).
-constexpr int kFullRopeMaxRankK = 288;  // largest r_k of the MFMA kernel
+constexpr int kFullRopeMaxRankK = 256;  // largest r_k of the MFMA kernel
 struct FullRopeArgs {
   int dtype, out_dtype;
   int B, H, d, rk, rv, n_max, n_ctx;
@@ -140,7 +140,7 @@ struct FullRopeArgs {
 
 hipError_t launch_decode_fullrope(const FullRopeArgs& a, hipStream_t stream);
 bool fullrope_mfma_ok(int dtype, int d_head, int r_k, int r_v);  // the MFMA kernel takes this shape
-int fullrope_occupancy(int r_k);  // resident workgroups per compute unit of the MFMA kernel
+int fullrope_occupancy(int r_k, int r_v);  // resident workgroups per compute unit of the MFMA kernel
 
 int device_cu_count();  // compute units of the current device (cached)
 
