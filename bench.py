@@ -37,11 +37,12 @@ BF16_PEAK_TFLOPS = 2516.6  # 256 CU x 2.4 GHz x 4096 flop/clk, dense
 # HBM bytes per launch of the dominant kernel: rocprofv3 --pmc FETCH_SIZE and
 # WRITE_SIZE (KiB per dispatch) scaled by what the same counters read for a
 # plain elementwise kernel of known size (FETCH_SIZE x 2.000, WRITE_SIZE x 1.000;
-# the runs are recorded under profiles/).  Keyed by (workload, r_k, r_v); an
-# entry is dropped when the kernel changes.
+# the runs are recorded under profiles/).  Keyed by (workload, r_k, r_v, path);
+# an entry is dropped when the kernel changes.
 FETCH_SCALE, WRITE_SCALE = 2.000, 1.000
 MEASURED_TRAFFIC = {
-    ("ouro14b_decode", 192, 320): {"fetch_kib": 1057142.75, "write_kib": 256.0},
+    ("ouro14b_decode", 192, 320, "absorbed"): {"fetch_kib": 1057142.75, "write_kib": 256.0},
+    ("ouro14b_decode", 192, 320, "fullrope"): {"fetch_kib": 1057715.28, "write_kib": 256.0},
 }
 
 
@@ -565,8 +566,8 @@ def main():
     B, N, d = wl.B, wl.N, wl.d
     value = B / (head["step_ms"] * 1e-3)
     achieved = head["decode_gbs"]
-    traffic = (None if (args.rope or args.evict or args.fullrope)
-               else traffic_bytes((wl.name, head["r_k"], head["r_v"])))
+    traffic = (None if (args.rope or args.evict)
+               else traffic_bytes((wl.name, head["r_k"], head["r_v"], "fullrope" if args.fullrope else "absorbed")))
     line = {
         "metric": "latent-cache decode attention tokens/sec and achieved HBM GB/s (% of peak)",
         "value": round(value, 2),
