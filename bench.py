@@ -73,7 +73,10 @@ def parse():
                         "latents and rotated at their positions; lla_decode_attn_fullrope)")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--no-graph", action="store_true",
-                   help="ouro14b_2d: launch every call from Python instead of replaying HIP graphs")
+                   help="ouro14b_2d and --evict: launch every call from Python instead of replaying HIP graphs")
+    p.add_argument("--graph", action="store_true",
+                   help="decode workloads: replay the step from HIP graphs (the default with --evict, whose "
+                        "calls are short enough for Python launch overhead to dominate)")
     p.add_argument("--copy-probe", action="store_true",
                    help="run a plain 1 GiB read + 1 GiB write elementwise kernel (counter calibration for rocprofv3 --pmc)")
     return p.parse_args()
@@ -185,6 +188,10 @@ def run_decode(args, torch, lla, W):
         timer = KernelTimer(torch, stream)
 
         def step(timed):
+            step_decode(timed)
+            step_writes()
+
+        def step_decode(timed):
             for l in range(wl.T):
                 for d in range(layers):
                     q, uk, uv, out = loops[l][d]
@@ -203,6 +210,8 @@ def run_decode(args, torch, lla, W):
                         lla.decode_attn(q, ck, cv, uk, uv, n_ctx=n_ctx, out=out, workspace=ws)
                     if timed:
                         timer.stop(s)
+
+        def step_writes():
             for d in range(layers):
                 xk, xv, wk, wv = writes[d]
                 ck, cv = caches[d]
@@ -213,21 +222,44 @@ def run_decode(args, torch, lla, W):
         for _ in range(args.warmup):
             step(False)
         torch.cuda.synchronize()
+        use_graph = (args.graph or bool(evict)) and not args.no_graph
+        if use_graph:
+            # the step's decode launches and its cache writes replayed from two HIP
+            # graphs; HIP events around the decode graph give the mean launch time
+            # as the span over its calls (with --rope the span includes the query
+            # rotations)
+            g_dec, g_wr = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+            cap = torch.cuda.Stream(dev)
+            with torch.cuda.graph(g_dec, stream=cap):
+                step_decode(False)
+            with torch.cuda.graph(g_wr, stream=cap):
+                step_writes()
+            torch.cuda.synchronize()
+            g_dec.replay()
+            g_wr.replay()
+            torch.cuda.synchronize()
         t0 = torch.cuda.Event(enable_timing=True)
         t1 = torch.cuda.Event(enable_timing=True)
         t0.record(stream)
         wall0 = time.perf_counter()
         for _ in range(args.steps):
-            step(True)
+            if use_graph:
+                e = timer.start()
+                g_dec.replay()
+                timer.stop(e)
+                g_wr.replay()
+            else:
+                step(True)
         t1.record(stream)
         torch.cuda.synchronize()
         wall = time.perf_counter() - wall0
         step_ms = t0.elapsed_time(t1) / args.steps
-        kern_ms = timer.mean_ms()
+        kern_ms = timer.mean_ms() / (wl.T * layers if use_graph else 1)
         nbytes = decode_bytes(wl.B, wl.H, wl.d, n_ctx, r_k, r_v, d_rope=dr)
         res = dict(tier=ti, r_k=r_k, r_v=r_v, step_ms=step_ms, wall_step_ms=1e3 * wall / args.steps,
                    decode_ms=kern_ms, decode_bytes=nbytes, decode_gbs=nbytes / (kern_ms * 1e-3) / 1e9,
-                   calls_per_step=wl.T * layers, splits_ws_bytes=ws.numel())
+                   calls_per_step=wl.T * layers, splits_ws_bytes=ws.numel(),
+                   launch="hip_graph" if use_graph else "eager")
         print(f"[bench] {json.dumps(res)}", file=sys.stderr, flush=True)
         res["cpu"] = (None if (args.no_cpu or dr or evict or args.ranks)
                       else cpu_baseline_decode(wl, r_k, r_v, caches, loops, torch, fullrope=args.fullrope))
@@ -594,7 +626,7 @@ def main():
             "layers": wl.layers, "loops": wl.T, "heads": wl.H, "d_head": d, "batch": B, "context": N,
             "attended_slots": min(N, sum(int(v) for v in args.evict.split(","))) if args.evict else N,
             "r_k": head["r_k"], "r_v": head["r_v"], "calls_per_step": head["calls_per_step"],
-            "parallelism": "single GPU",
+            "launch": head["launch"], "parallelism": "single GPU",
         },
         "roofline": {
             "bound": "hbm",

@@ -205,13 +205,15 @@ void decode_kernel(DecodeArgs a) {
       case 2: absorb_query<TIn, 2, kThreads>(uk, a.d, rk, a.qscale, s_q, s_part, s_qt); break;
       default: absorb_query<TIn, 1, kThreads>(uk, a.d, rk, a.qscale, s_q, s_part, s_qt); break;
     }
-    // rotary branch: the (already rotated) query part joins q~ as extra rows,
-    // from a 16-byte aligned slot past the r_k content rows
+    // the last content batch is padded to 8 rows with zero weights; the rotary
+    // branch: the (already rotated) query part joins q~ as extra rows, from the
+    // 16-byte aligned slot past the padded content rows
+    for (int j = rk + tid; j < rq0; j += kThreads) s_qt[j] = 0.f;
     if (a.dr) {
       const TIn* qr = static_cast<const TIn*>(a.qr) + unit * a.dr;
       for (int i = tid; i < a.dr; i += kThreads) s_qt[rq0 + i] = a.qscale * Elem<TIn>::get(qr, i);
-      __syncthreads();
     }
+    __syncthreads();
   }
 
   const int hi = lane / LPR, lo = lane - hi * LPR;
@@ -246,16 +248,19 @@ void decode_kernel(DecodeArgs a) {
   // between two register sets, and V batches prefetch across row groups and
   // pages, so the FMAs of one batch overlap the memory latency of the next.
   constexpr bool PIPE = DEEP;
-  const int nkb = rk / KB;                                  // full K batches
+  const int nkb = (rk + KB - 1) / KB;                       // K batches (the last padded, zero weights)
   const int ntb = nkb + a.dr / KB;                          // plus the rotary rows (dr % 8 == 0)
   const int nvb = (vg_full + (vg_part ? 1 : 0) + VB - 1) / VB;  // V batches per page
   constexpr int NKC = (GV + VB - 1) / VB;
 
-  // batch jb < nkb: content rows jb*KB.. of c_k; later batches: rotary rows
+  // batch jb < nkb: content rows jb*KB.. of c_k (rows past r_k re-read row
+  // r_k - 1, weighted by zero); later batches: rotary rows.  Every batch issues
+  // all its loads, so the compiler's waits count loads exactly.
   auto kload = [&](uint4 (&r)[KB], int g0p, int jb) {
     if (jb < nkb) {
 #pragma unroll
-      for (int u = 0; u < KB; ++u) r[u] = buf_ld16(rk_src, vk_lane, g0p * kpage_bytes + (jb * KB + u) * kPage * ES);
+      for (int u = 0; u < KB; ++u)
+        r[u] = buf_ld16(rk_src, vk_lane, g0p * kpage_bytes + min(jb * KB + u, rk - 1) * kPage * ES);
     } else {
 #pragma unroll
       for (int u = 0; u < KB; ++u)
@@ -297,7 +302,6 @@ void decode_kernel(DecodeArgs a) {
 #pragma unroll
     for (int e = 0; e < EPL; ++e) acc[e] = 0.f;
     if (hi < np) {
-      const int gbase = g0 * kpage_bytes;
       if constexpr (PIPE) {
         uint4 ka[KB], kb2[KB];
         if (ntb > 0) kload(ka, g0, 0);
@@ -313,13 +317,6 @@ void decode_kernel(DecodeArgs a) {
           kload(ka, g0, jb);
           kfma(ka, jb, acc);
         }
-      }
-      for (int j = nkb * KB; j < rk; ++j) {
-        const float q1 = s_qt[j];
-        float v[EPL];
-        Elem<TIn>::unpack(buf_ld16(rk_src, vk_lane, gbase + j * kPage * ES), v);
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) acc[e] = fmaf(q1, v[e], acc[e]);
       }
     }
     uint4 vcur[VB];
