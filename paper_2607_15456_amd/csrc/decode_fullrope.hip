@@ -13,17 +13,18 @@
 // double precision), and cos / sin of t * theta_f, the same for every tile,
 // are tabulated in LDS once per workgroup.
 //
-// bf16 kernel (d_head = 128): a workgroup of 4 wavefronts takes one (b, h)
-// and a range of 64-token pages.  Wavefront m rebuilds rows 32m .. 32m + 31
-// of K^T for both 32-token tiles of every page on v_mfma_f32_32x32x16_bf16:
+// bf16 kernel (d_head = 128): a workgroup of 8 wavefronts (two per SIMD) takes
+// one (b, h) and a range of 64-token pages.  Wavefront w rebuilds rows
+// 32m .. 32m + 31 (m = w % 4) of K^T for 32-token tile w / 4 of every page on
+// v_mfma_f32_32x32x16_bf16:
 //   A = U_k rows 32m + i (staged in LDS once per workgroup),
 //   B = the key page, staged in LDS with XOR-swizzled 16-byte chunks and read
 //       with ds_read_b64_tr_b16 (lane l gets one token's 4 features),
 // so lane (col + 32 g), register r holds K[32m + 8(r/4) + 4g + r%4][token col].
 // The lane multiplies its 16 reconstructed features by the rotated query
-// weights, the two lane halves and the four wavefronts add their parts (LDS,
-// one barrier per page), and every wavefront runs the same online softmax.
-// Values: wavefront m owns latent rows [8 VR m, 8 VR (m + 1)) and streams them
+// weights, the two lane halves and the four M-tiles add their parts (LDS, one
+// barrier per page), and every wavefront runs the same online softmax.
+// Values: wavefront w owns latent rows [8 VR w, 8 VR (w + 1)) and streams them
 // with 16-byte loads of 8 tokens, as in the absorbed decode.  Key pages are
 // loaded into registers two pages ahead and written to a two-slot LDS ring;
 // value pages are loaded two pages ahead (two register sets alternate).
@@ -43,7 +44,7 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 #define LLA_LDS __attribute__((address_space(3)))
 
-constexpr int kFrWaves = 4;
+constexpr int kFrWaves = 8;  // two per SIMD: wavefront w takes M-tile w % 4 of token tile w / 4
 constexpr int kFrThreads = kFrWaves * kWave;
 constexpr int kFrD = 128;  // d_head of the MFMA kernel
 constexpr double kTwoPi = 6.283185307179586476925286766559;
@@ -100,13 +101,13 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// out[i] = sum_j U_v[i][j] zn[j] + mu_v[i] (zn already normalised), 256
+// out[i] = sum_j U_v[i][j] zn[j] + mu_v[i] (zn already normalised), NT
 // threads: P consecutive threads share row i and take every P-th column; their
 // partial sums combine by xor shuffles in a fixed order.
-template <typename T>
+template <typename T, int NT>
 __device__ void fr_epilogue(const FullRopeArgs& a, int h, size_t unit, const float* s_zn, bool bad) {
   const int d = a.d, rv = a.rv;
-  const int P = 256 / d >= 8 ? 8 : 256 / d >= 4 ? 4 : 256 / d >= 2 ? 2 : 1;
+  const int P = NT / d >= 8 ? 8 : NT / d >= 4 ? 4 : NT / d >= 2 ? 2 : 1;
   const int i = threadIdx.x / P, part = threadIdx.x % P;
   const T* uv = static_cast<const T*>(a.uv) + (size_t)h * d * rv;
   float acc = 0.f;
@@ -126,10 +127,10 @@ __device__ void fr_epilogue(const FullRopeArgs& a, int h, size_t unit, const flo
 }
 
 // ---------------------------------------------------------------------------
-// MFMA kernel: bf16, d_head = 128, r_k <= 16 KS, r_v <= 32 VR.
+// MFMA kernel: bf16, d_head = 128, r_k <= 16 KS, r_v <= 64 VR.
 // ---------------------------------------------------------------------------
-template <int KS, int VR, bool MU, int OCC>
-__global__ __launch_bounds__(kFrThreads) __attribute__((amdgpu_waves_per_eu(OCC)))
+template <int KS, int VR, bool MU>
+__global__ __launch_bounds__(kFrThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void fullrope_mfma_kernel(FullRopeArgs a) {
   constexpr int RKP = KS * 16;            // padded key rank (K of the product)
   constexpr int KI = RKP / 8;             // 8-row load instructions per key page
@@ -143,8 +144,8 @@ void fullrope_mfma_kernel(FullRopeArgs a) {
   // reading different t hit different banks
   __shared__ __attribute__((aligned(16))) float s_cos[2][32][32];
   __shared__ __attribute__((aligned(16))) float s_sin[2][32][32];
-  __shared__ __attribute__((aligned(16))) float s_qp[kFrWaves][2][2][32];  // [wave][tile][re/im][freq]
-  __shared__ __attribute__((aligned(16))) float s_sc[2][kFrWaves][kPage];  // partial scores
+  __shared__ __attribute__((aligned(16))) float s_qp[kFrWaves][2][32];  // [wave][re/im][freq] of its tile
+  __shared__ __attribute__((aligned(16))) float s_sc[2][4][kPage];      // partial scores per M-tile
   __shared__ float s_z[kMaxRank];
   __shared__ float s_ml[2];
   __shared__ int s_last;
@@ -152,6 +153,7 @@ void fullrope_mfma_kernel(FullRopeArgs a) {
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int col = lane & 31, g = lane >> 5;
+  const int mt = wave & 3, nt = wave >> 2;  // M-tile (32 features of K) and 32-token tile of the page
   const int hi = lane >> 3, lo = lane & 7;  // value phase: row in the 8-row group, token slice
   const int b = blockIdx.x / a.splits, split = blockIdx.x - b * a.splits, h = blockIdx.y;
   const int N = a.ctx_len ? a.ctx_len[b] : a.n_ctx;
@@ -163,42 +165,13 @@ void fullrope_mfma_kernel(FullRopeArgs a) {
   const size_t bh = (size_t)b * a.H + h;
   const int rk = a.rk, rv = a.rv;
 
-  // ---- U_k of head h into LDS (rows = features of K, columns past r_k zero) ----
-  {
-    const bf16_t* uk = static_cast<const bf16_t*>(a.uk) + (size_t)h * kFrD * rk;
-    constexpr int C8 = US / 8;  // 16-byte chunks per LDS row
-    for (int e = tid; e < kFrD * C8; e += kFrThreads) {
-      const int i = e / C8, j0 = 8 * (e - i * C8);
-      uint4 v;
-      if ((rk & 7) == 0) {
-        v = j0 < rk ? *reinterpret_cast<const uint4*>(uk + (size_t)i * rk + j0) : uint4{0, 0, 0, 0};
-      } else {
-        uint32_t w[4];
-#pragma unroll
-        for (int x = 0; x < 4; ++x) {
-          const uint32_t x0 = j0 + 2 * x < rk ? uk[(size_t)i * rk + j0 + 2 * x] : 0u;
-          const uint32_t x1 = j0 + 2 * x + 1 < rk ? uk[(size_t)i * rk + j0 + 2 * x + 1] : 0u;
-          w[x] = x0 | (x1 << 16);
-        }
-        v = uint4{w[0], w[1], w[2], w[3]};
-      }
-      *reinterpret_cast<uint4*>(&s_u[i * US + j0]) = v;
-    }
-    for (int e = tid; e < 2 * 32 * 32; e += kFrThreads) {
-      const int hf = e >> 10, t = (e >> 5) & 31, fr = e & 31;
-      float c, sn;
-      rot_cs((double)t, pow(a.base, -2.0 * (32 * hf + fr) / kFrD), c, sn);
-      s_cos[hf][t][(fr + 4 * (t >> 1)) & 31] = c;
-      s_sin[hf][t][(fr + 4 * (t >> 1)) & 31] = sn;
-    }
-  }
-  // Lane (col, g), register r of tile `wave`: feature i = 32 wave + fr(r) with
-  // fr(r) = 8 (r/4) + 4 g + r%4, frequency f = i mod 64 = 32 (wave & 1) + fr(r).
-  const bool first_half = wave < 2;
-  const int hf = wave & 1;
-  // query rotation: lane (fq = col, tile tq = g) forms QP for frequency
-  // 32 (wave & 1) + fq of tile tq of every page
-  const int fq = 32 * (wave & 1) + col;
+  // Lane (col, g), register r of M-tile mt: feature i = 32 mt + fr(r) with
+  // fr(r) = 8 (r/4) + 4 g + r%4, frequency f = i mod 64 = 32 (mt & 1) + fr(r).
+  const bool first_half = mt < 2;
+  const int hf = mt & 1;
+  // query rotation: lane col forms QP for frequency 32 (mt & 1) + col of this
+  // wavefront's token tile of every page
+  const int fq = 32 * (mt & 1) + col;
   const double theta_q = pow(a.base, -2.0 * fq / kFrD);
   float q1, q2;
   {
@@ -208,7 +181,7 @@ void fullrope_mfma_kernel(FullRopeArgs a) {
   }
   float mu[16];
   if constexpr (MU) {
-    const bf16_t* mk = static_cast<const bf16_t*>(a.muk) + (size_t)h * kFrD + 32 * wave;
+    const bf16_t* mk = static_cast<const bf16_t*>(a.muk) + (size_t)h * kFrD + 32 * mt;
 #pragma unroll
     for (int r = 0; r < 16; ++r) mu[r] = bf16_to_f32(mk[8 * (r / 4) + 4 * g + r % 4]);
   }
@@ -219,7 +192,7 @@ void fullrope_mfma_kernel(FullRopeArgs a) {
   const BufRsrc vsrc = make_rsrc(static_cast<const bf16_t*>(a.cv) + bh * (size_t)a.n_max * rv,
                                  (size_t)a.n_max * rv * 2);
   const int kpage = kPage * rk * 2, vpage = kPage * rv * 2;  // bytes per page
-  // key loads: instruction k = wave + 4 u covers page rows 8k .. 8k+7; lane ->
+  // key loads: instruction k = wave + 8 u covers page rows 8k .. 8k+7; lane ->
   // row 8k + lane/8, 16-byte chunk lane%8 (one contiguous KB per instruction)
   const int krow = lane >> 3;
   const int kswz = ((lane >> 4) & 1) << 2;                            // chunk XOR of row 8k + krow
@@ -228,10 +201,7 @@ void fullrope_mfma_kernel(FullRopeArgs a) {
   // rows 16 s + 8 g + 4 e2 + x16/4, tokens 32 nt + 16 (G % 2) + 4 (x16 % 4) .. +3
   const int x16 = lane & 15, th = (lane >> 4) & 1, sw1 = (x16 >> 3) & 1;
   const int cl = 2 * th + ((x16 & 3) >> 1);
-  int troff[2];
-#pragma unroll
-  for (int nt = 0; nt < 2; ++nt)
-    troff[nt] = (8 * g + (x16 >> 2)) * kPage + ((4 * (nt ^ sw1) + cl) << 3) + 4 * (x16 & 1);
+  const int troff = (8 * g + (x16 >> 2)) * kPage + ((4 * (nt ^ sw1) + cl) << 3) + 4 * (x16 & 1);
   // value rows of this wavefront: 8 VR wave + 8 k + hi, tokens 8 lo .. 8 lo + 7
   const int vrow0 = 8 * VR * wave;
 
@@ -256,8 +226,10 @@ void fullrope_mfma_kernel(FullRopeArgs a) {
 #pragma unroll
     for (int u = 0; u < KD; ++u) {
       const int k = wave + kFrWaves * u;
-      const bool live = 8 * k + krow < rk;
-      *reinterpret_cast<uint4*>(&s_k[slot * kSlot + 8 * k * kPage + kdst]) = live ? kr[u] : uint4{0, 0, 0, 0};
+      if (k < KI) {  // uniform
+        const bool live = 8 * k + krow < rk;
+        *reinterpret_cast<uint4*>(&s_k[slot * kSlot + 8 * k * kPage + kdst]) = live ? kr[u] : uint4{0, 0, 0, 0};
+      }
     }
   };
   // A lane whose row is past r_v reads row r_v - 1 (never used); every lane
@@ -328,30 +300,24 @@ void fullrope_mfma_kernel(FullRopeArgs a) {
     kload(kr, min(p + 3, pe - 1));
     if (i > 0) vconsume(vr, p - 1);
     vload(vr, min(p + 1, pe - 1));
-    // ---- rotated query of this page's two tiles ----
+    // ---- rotated query of this wavefront's token tile ----
     {
       float c, sn;
-      rot_cs((double)pq - (double)(p * kPage + 32 * g), theta_q, c, sn);
-      s_qp[wave][g][0][col] = q1 * c - q2 * sn;
-      s_qp[wave][g][1][col] = q2 * c + q1 * sn;
+      rot_cs((double)pq - (double)(p * kPage + 32 * nt), theta_q, c, sn);
+      s_qp[wave][0][col] = q1 * c - q2 * sn;  // both lane halves write the same value
+      s_qp[wave][1][col] = q2 * c + q1 * sn;
     }
-    // ---- K^T rows 32 wave .. +31 of both tiles ----
-    f32x16 acc[2];
+    // ---- K^T rows 32 mt .. +31 of token tile nt ----
+    f32x16 acc;
 #pragma unroll
-    for (int nt = 0; nt < 2; ++nt) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[nt][r] = MU ? mu[r] : 0.f;
-    }
+    for (int r = 0; r < 16; ++r) acc[r] = MU ? mu[r] : 0.f;
     const bf16_t* kb = &s_k[slot * kSlot];
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
-      const uint4 ua = *reinterpret_cast<const uint4*>(&s_u[(32 * wave + col) * US + 16 * s + 8 * g]);
-#pragma unroll
-      for (int nt = 0; nt < 2; ++nt) {
-        const uint2 r0 = lds_tr16(kb + troff[nt] + 16 * s * kPage);
-        const uint2 r1 = lds_tr16(kb + troff[nt] + (16 * s + 4) * kPage);
-        acc[nt] = mfma32(ua, uint4{r0.x, r0.y, r1.x, r1.y}, acc[nt]);
-      }
+      const uint4 ua = *reinterpret_cast<const uint4*>(&s_u[(32 * mt + col) * US + 16 * s + 8 * g]);
+      const uint2 r0 = lds_tr16(kb + troff + 16 * s * kPage);
+      const uint2 r1 = lds_tr16(kb + troff + (16 * s + 4) * kPage);
+      acc = mfma32(ua, uint4{r0.x, r0.y, r1.x, r1.y}, acc);
     }
     wave_sync();
     // ---- rotated dot products: this lane's 16 features of token col ----
@@ -364,26 +330,22 @@ void fullrope_mfma_kernel(FullRopeArgs a) {
       cs_c[4 * a4] = c4.x; cs_c[4 * a4 + 1] = c4.y; cs_c[4 * a4 + 2] = c4.z; cs_c[4 * a4 + 3] = c4.w;
       cs_s[4 * a4] = s4.x; cs_s[4 * a4 + 1] = s4.y; cs_s[4 * a4 + 2] = s4.z; cs_s[4 * a4 + 3] = s4.w;
     }
-    float part[2];
+    float sum = 0.f;
 #pragma unroll
-    for (int nt = 0; nt < 2; ++nt) {
-      float sum = 0.f;
+    for (int a4 = 0; a4 < 4; ++a4) {
+      const float4 p1 = *reinterpret_cast<const float4*>(&s_qp[wave][0][8 * a4 + 4 * g]);
+      const float4 p2 = *reinterpret_cast<const float4*>(&s_qp[wave][1][8 * a4 + 4 * g]);
+      const float x1[4] = {p1.x, p1.y, p1.z, p1.w}, x2[4] = {p2.x, p2.y, p2.z, p2.w};
 #pragma unroll
-      for (int a4 = 0; a4 < 4; ++a4) {
-        const float4 p1 = *reinterpret_cast<const float4*>(&s_qp[wave][nt][0][8 * a4 + 4 * g]);
-        const float4 p2 = *reinterpret_cast<const float4*>(&s_qp[wave][nt][1][8 * a4 + 4 * g]);
-        const float x1[4] = {p1.x, p1.y, p1.z, p1.w}, x2[4] = {p2.x, p2.y, p2.z, p2.w};
-#pragma unroll
-        for (int b4 = 0; b4 < 4; ++b4) {
-          const int r = 4 * a4 + b4;
-          const float w = first_half ? fmaf(x1[b4], cs_c[r], x2[b4] * cs_s[r])
-                                     : fmaf(x2[b4], cs_c[r], -(x1[b4] * cs_s[r]));
-          sum = fmaf(w, acc[nt][r], sum);
-        }
+      for (int b4 = 0; b4 < 4; ++b4) {
+        const int r = 4 * a4 + b4;
+        const float w = first_half ? fmaf(x1[b4], cs_c[r], x2[b4] * cs_s[r])
+                                   : fmaf(x2[b4], cs_c[r], -(x1[b4] * cs_s[r]));
+        sum = fmaf(w, acc[r], sum);
       }
-      part[nt] = sum_halves(sum);
     }
-    s_sc[slot][wave][lane] = g ? part[1] : part[0];  // lane = token 32 g + col
+    sum = sum_halves(sum);  // M-tile mt's part of the score of token 32 nt + col
+    if (g == 0) s_sc[slot][mt][32 * nt + col] = sum;
     __syncthreads();
 
     // ---- softmax over the page: lane (hi, lo) holds tokens 8 lo .. 8 lo + 7 ----
@@ -392,7 +354,7 @@ void fullrope_mfma_kernel(FullRopeArgs a) {
     for (int e = 0; e < 8; e += 4) {
       float4 t = *reinterpret_cast<const float4*>(&s_sc[slot][0][8 * lo + e]);
 #pragma unroll
-      for (int w = 1; w < kFrWaves; ++w) {
+      for (int w = 1; w < 4; ++w) {
         const float4 u = *reinterpret_cast<const float4*>(&s_sc[slot][w][8 * lo + e]);
         t.x += u.x;
         t.y += u.y;
@@ -427,12 +389,48 @@ void fullrope_mfma_kernel(FullRopeArgs a) {
 
   // Prologue: page pb's keys into slot 0; keys of pb + 1 in set B, pb + 2 in
   // set A; values of pb in set A (set B is loaded by the first page).
+  // The first pages are requested before U_k and the rotation table are
+  // staged, so their latency overlaps the staging.
   if (pb < pe) {
     kload(kA, pb);
-    kstore(kA, 0);
     kload(kB, min(pb + 1, pe - 1));
-    kload(kA, min(pb + 2, pe - 1));
     vload(vA, pb);
+  }
+  // ---- U_k of head h into LDS (rows = features of K, columns past r_k zero) ----
+  {
+    const bf16_t* uk = static_cast<const bf16_t*>(a.uk) + (size_t)h * kFrD * rk;
+    constexpr int C8 = US / 8;  // 16-byte chunks per LDS row
+    for (int e = tid; e < kFrD * C8; e += kFrThreads) {
+      const int i = e / C8, j0 = 8 * (e - i * C8);
+      uint4 v;
+      if ((rk & 7) == 0) {
+        v = j0 < rk ? *reinterpret_cast<const uint4*>(uk + (size_t)i * rk + j0) : uint4{0, 0, 0, 0};
+      } else {
+        uint32_t w[4];
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+          const uint32_t x0 = j0 + 2 * x < rk ? uk[(size_t)i * rk + j0 + 2 * x] : 0u;
+          const uint32_t x1 = j0 + 2 * x + 1 < rk ? uk[(size_t)i * rk + j0 + 2 * x + 1] : 0u;
+          w[x] = x0 | (x1 << 16);
+        }
+        v = uint4{w[0], w[1], w[2], w[3]};
+      }
+      *reinterpret_cast<uint4*>(&s_u[i * US + j0]) = v;
+    }
+    // the thread's frequencies are fr = tid % 32 and 32 + fr for every e
+    static_assert(kFrThreads % 32 == 0, "");
+    const double th0 = pow(a.base, -2.0 * (tid & 31) / kFrD), th1 = pow(a.base, -2.0 * (32 + (tid & 31)) / kFrD);
+    for (int e = tid; e < 2 * 32 * 32; e += kFrThreads) {
+      const int hf = e >> 10, t = (e >> 5) & 31, fr = e & 31;
+      float c, sn;
+      rot_cs((double)t, hf ? th1 : th0, c, sn);
+      s_cos[hf][t][(fr + 4 * (t >> 1)) & 31] = c;
+      s_sin[hf][t][(fr + 4 * (t >> 1)) & 31] = sn;
+    }
+  }
+  if (pb < pe) {
+    kstore(kA, 0);
+    kload(kA, min(pb + 2, pe - 1));
   }
   __syncthreads();
   const int npg = pe - pb;
@@ -508,7 +506,7 @@ void fullrope_mfma_kernel(FullRopeArgs a) {
     if (tid == 0) __hip_atomic_store(a.cnt + unit, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   __syncthreads();
-  fr_epilogue<bf16_t>(a, h, unit, s_z, bad);
+  fr_epilogue<bf16_t, kFrThreads>(a, h, unit, s_z, bad);
 }
 
 // ---------------------------------------------------------------------------
@@ -594,27 +592,17 @@ __global__ __launch_bounds__(256) void fullrope_plain_kernel(FullRopeArgs a) {
     if (j < rv) s_z[j] = z[u] / l_run;
   }
   __syncthreads();
-  fr_epilogue<T>(a, h, bh, s_z, bad);
+  fr_epilogue<T, 256>(a, h, bh, s_z, bad);
 }
 
-template <int KS, int VR, int OCC>
+template <int KS, int VR>
 hipError_t launch_mfma(const FullRopeArgs& a, hipStream_t stream) {
   const dim3 grid(a.B * a.splits, a.H);
   if (a.muk)
-    hipLaunchKernelGGL((fullrope_mfma_kernel<KS, VR, true, OCC>), grid, dim3(kFrThreads), 0, stream, a);
+    hipLaunchKernelGGL((fullrope_mfma_kernel<KS, VR, true>), grid, dim3(kFrThreads), 0, stream, a);
   else
-    hipLaunchKernelGGL((fullrope_mfma_kernel<KS, VR, false, OCC>), grid, dim3(kFrThreads), 0, stream, a);
+    hipLaunchKernelGGL((fullrope_mfma_kernel<KS, VR, false>), grid, dim3(kFrThreads), 0, stream, a);
   return hipGetLastError();
-}
-
-// Resident wavefronts per SIMD: 2 while the registers fit in 256 (two key and
-// two value load sets, accumulators, z, the rotation constants of a page and
-// about 80 more), else 1.  The LDS of two workgroups must fit as well.
-constexpr int fr_occ(int KS, int VR) {
-  return 2 * 4 * ((KS * 2 + kFrWaves - 1) / kFrWaves) + 2 * 4 * VR + VR + 32 + 32 + 80 <= 256 &&
-                 2 * (2 * KS * 16 * kPage * 2 + kFrD * (KS * 16 + 8) * 2 + 16384 + 4096 + 3072) <= 160 * 1024
-             ? 2
-             : 1;
 }
 
 // Template buckets: K-steps of 16 key features, 8-row value groups per wavefront.
@@ -623,20 +611,20 @@ int ks_bucket(int r_k) {
   return ks <= 2 ? 2 : ks <= 4 ? 4 : ks <= 6 ? 6 : ks <= 8 ? 8 : ks <= 10 ? 10 : ks <= 12 ? 12 : 16;
 }
 int vr_bucket(int r_v) {
-  const int vr = (r_v + 31) / 32;
-  return vr <= 2 ? 2 : vr <= 4 ? 4 : vr <= 6 ? 6 : vr <= 8 ? 8 : vr <= 10 ? 10 : vr <= 12 ? 12 : 16;
+  const int vr = (r_v + 8 * kFrWaves - 1) / (8 * kFrWaves);  // 8-row value groups per wavefront
+  return vr <= 1 ? 1 : vr <= 2 ? 2 : vr <= 3 ? 3 : vr <= 4 ? 4 : vr <= 5 ? 5 : vr <= 6 ? 6 : 8;
 }
 
 template <int KS>
 hipError_t launch_vr(const FullRopeArgs& a, hipStream_t stream) {
   switch (vr_bucket(a.rv)) {
-    case 2: return launch_mfma<KS, 2, fr_occ(KS, 2)>(a, stream);
-    case 4: return launch_mfma<KS, 4, fr_occ(KS, 4)>(a, stream);
-    case 6: return launch_mfma<KS, 6, fr_occ(KS, 6)>(a, stream);
-    case 8: return launch_mfma<KS, 8, fr_occ(KS, 8)>(a, stream);
-    case 10: return launch_mfma<KS, 10, fr_occ(KS, 10)>(a, stream);
-    case 12: return launch_mfma<KS, 12, fr_occ(KS, 12)>(a, stream);
-    default: return launch_mfma<KS, 16, fr_occ(KS, 16)>(a, stream);
+    case 1: return launch_mfma<KS, 1>(a, stream);
+    case 2: return launch_mfma<KS, 2>(a, stream);
+    case 3: return launch_mfma<KS, 3>(a, stream);
+    case 4: return launch_mfma<KS, 4>(a, stream);
+    case 5: return launch_mfma<KS, 5>(a, stream);
+    case 6: return launch_mfma<KS, 6>(a, stream);
+    default: return launch_mfma<KS, 8>(a, stream);
   }
 }
 
@@ -646,7 +634,11 @@ bool fullrope_mfma_ok(int dtype, int d_head, int r_k, int r_v) {
   return dtype == LLA_BF16 && d_head == kFrD && r_k <= kFullRopeMaxRankK && r_v <= kMaxRank;
 }
 
-int fullrope_occupancy(int r_k, int r_v) { return fr_occ(ks_bucket(r_k), vr_bucket(r_v)); }
+int fullrope_occupancy(int r_k, int r_v) {
+  (void)r_k;
+  (void)r_v;
+  return 1;  // one 8-wavefront workgroup per compute unit
+}
 
 hipError_t launch_decode_fullrope(const FullRopeArgs& a, hipStream_t stream) {
   if (!fullrope_mfma_ok(a.dtype, a.d, a.rk, a.rv)) {
