@@ -65,6 +65,8 @@ __all__ = [
     "split_merge",
     "decode_attn_batched",
     "prefill_attn_batched",
+    "prefill_attn_2d",
+    "prefill_attn_2d_batched",
     "encode_batched",
     "rope",
     "decode_attn_rope",
@@ -520,6 +522,41 @@ def decode_attn_2d_batched(q, c_k, c_v, u_k, u_v, mu_k=None, mu_v=None, scale=No
     for b in (range(B) if batches is None else batches):
         n = lens[b]
         out[b] = decode_attn_2d(q[b], c_k[b, :n], c_v[b, :n], u_k, u_v, mu_k, mu_v, scale)
+    return out
+
+
+def prefill_attn_2d(Q, c_k, c_v, u_k, u_v, mu_k=None, mu_v=None, scale=None, p0=0):
+    """LLA-2D causal prefill at loop l (plain definition): head h rebuilds
+    K_{l,h} = c_k U_{k,l,h}^T + mu_{k,l,h} and V_{l,h} likewise from the shared
+    latents (Eq. 3 with the (l, h) slice of W_up), and its query m, at absolute
+    position p0 + m, attends keys n <= p0 + m with the teacher's attention.
+
+    Q: [H, M, d]; c_k: [>= p0+M, r_k]; c_v: [>= p0+M, r_v]; u_k: [H, d, r_k];
+    u_v: [H, d, r_v]; mu_k, mu_v: [H, d] or None.  Returns [H, M, d]."""
+    Q = np.asarray(Q, dtype=np.float64)
+    H, M, d = Q.shape
+    if scale is None:
+        scale = default_scale(d)
+    n_all = p0 + M
+    out = np.empty_like(Q)
+    for h in range(H):
+        K = reconstruct(c_k[:n_all], u_k[h], None if mu_k is None else mu_k[h])
+        V = reconstruct(c_v[:n_all], u_v[h], None if mu_v is None else mu_v[h])
+        for m in range(M):
+            n = p0 + m + 1
+            out[h, m] = attention(Q[h, m], K[:n], V[:n], scale)
+    return out
+
+
+def prefill_attn_2d_batched(Q, c_k, c_v, u_k, u_v, mu_k=None, mu_v=None, scale=None, p0=0,
+                            batches=None):
+    """prefill_attn_2d for every sequence b (or those in ``batches``).
+    Q: [B, H, M, d]; c_k: [B, >= p0+M, r_k]; c_v: [B, >= p0+M, r_v] (token-major).
+    Returns [B, H, M, d] (sequences not computed are NaN)."""
+    Q = np.asarray(Q, dtype=np.float64)
+    out = np.full(Q.shape, np.nan)
+    for b in (range(Q.shape[0]) if batches is None else batches):
+        out[b] = prefill_attn_2d(Q[b], c_k[b], c_v[b], u_k, u_v, mu_k, mu_v, scale, p0)
     return out
 
 
