@@ -59,7 +59,7 @@
 extern "C" {
 #endif
 
-#define LLA_ABI_VERSION 6
+#define LLA_ABI_VERSION 7
 #define LLA_PAGE_TOKENS 64
 #define LLA_MAX_RANK 512
 #define LLA_MAX_ROPE 256
@@ -355,8 +355,9 @@ lla_status lla_rope_write_ring(int dtype, int B, int M, int H_rope, int d_rope, 
  *   key latents   token-major: element (b, n, j) at (b*n_max + n)*r_k + j
  *   value latents paged feature-major, as a per-head cache with H = 1:
  *                 element (b, n, j) at (b*n_max + (n/64)*64)*r_v + j*64 + n%64
- * Supported: bf16 only, H = 16, r_k a multiple of 32 and r_v a multiple of 16,
- * both <= LLA_MAX_RANK_2D (else LLA_ERR_UNSUPPORTED).
+ * The write and the decode support bf16 only, H = 16, r_k a multiple of 32 and
+ * r_v a multiple of 16, both <= LLA_MAX_RANK_2D (else LLA_ERR_UNSUPPORTED); the
+ * prefill's limits are stated with it.
  */
 
 /*
@@ -407,6 +408,40 @@ lla_status lla_decode_attn_2d(int dtype, int out_dtype, int B, int H, int d_head
                               const void* c_k, const void* c_v, const void* u_k, const void* u_v,
                               const void* mu_k, const void* mu_v, float scale, void* out,
                               void* workspace, size_t ws_bytes, void* stream);
+
+/* Workspace bytes lla_prefill_attn_2d needs when the keys span positions
+ * 0 .. n_keys-1 (n_keys = p0 + M): every head's rebuilt keys and values in
+ * fp16, 4 * B * H * d_head * (n_keys rounded up to 64) bytes.  Host only.
+ * Errors: LLA_ERR_INVALID_ARG. */
+lla_status lla_prefill_2d_workspace_bytes(int B, int H, int d_head, int n_keys, size_t* bytes);
+
+/*
+ * Loop-l causal prefill of all H heads over the shared LLA-2D latents, on the
+ * full-memory path of App. J ("Per-head LLA versus LLA-2D at inference"):
+ * every head's K_h = c_k U_{k,l,h}^T and V_h = c_v U_{v,l,h}^T (Eq. 3 with the
+ * (l, h) slice of W_up) are rebuilt for positions 0 .. p0+M-1 into the
+ * workspace, then query m of head h, at position p0 + m, attends the keys
+ * n <= p0 + m:  out = softmax(scale * K_h q) V_h + mu_{v,l,h}.  The rebuilt
+ * K and V, the query and the softmax weights enter the products in fp16
+ * (accumulation in fp32): |q|, |K| and |V| entries must stay below 65504, else
+ * the output is not finite.
+ *   q    [B][H][M][d_head]; out [B][H][M][d_head] of out_dtype
+ *   c_k, c_v  the 2D caches (layouts above) of capacity n_max, holding latents
+ *        at positions 0 .. p0+M-1 (p0 + M <= n_max); later slots are not read
+ *   u_k [H][d_head][r_k]; u_v [H][d_head][r_v]; mu_k, mu_v [H][d_head] or NULL
+ *        (mu_k cancels in the softmax)
+ *   workspace  device memory of at least lla_prefill_2d_workspace_bytes(B, H,
+ *        d_head, p0 + M), 16-byte aligned; overwritten, no initial contents
+ *        needed; calls sharing it must be ordered on the stream
+ * Supported: bf16, d_head = 128, r_k and r_v multiples of 16 up to 512, any H
+ * (else LLA_ERR_UNSUPPORTED).
+ * Errors: LLA_ERR_INVALID_ARG, LLA_ERR_UNSUPPORTED, LLA_ERR_WORKSPACE, LLA_ERR_HIP.
+ */
+lla_status lla_prefill_attn_2d(int dtype, int out_dtype, int B, int H, int M, int d_head, int r_k,
+                               int r_v, int n_max, int p0, const void* q, const void* c_k,
+                               const void* c_v, const void* u_k, const void* u_v, const void* mu_k,
+                               const void* mu_v, float scale, void* out, void* workspace,
+                               size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

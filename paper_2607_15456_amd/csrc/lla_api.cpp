@@ -650,4 +650,53 @@ lla_status lla_decode_attn_2d(int dtype, int out_dtype, int B, int H, int d_head
   return hip_status(lla::launch_decode_2d(a, static_cast<hipStream_t>(stream)));
 }
 
+lla_status lla_prefill_2d_workspace_bytes(int B, int H, int d_head, int n_keys, size_t* bytes) {
+  if (B < 1 || H < 1 || !head_ok(d_head) || n_keys < 1 || !bytes) return LLA_ERR_INVALID_ARG;
+  const size_t nk = ((size_t)n_keys + 63) / 64 * 64;
+  *bytes = 4 * (size_t)B * H * d_head * nk;
+  return LLA_OK;
+}
+
+lla_status lla_prefill_attn_2d(int dtype, int out_dtype, int B, int H, int M, int d_head, int r_k,
+                               int r_v, int n_max, int p0, const void* q, const void* c_k,
+                               const void* c_v, const void* u_k, const void* u_v, const void* mu_k,
+                               const void* mu_v, float scale, void* out, void* workspace,
+                               size_t ws_bytes, void* stream) {
+  if (!dtype_ok(dtype) || !dtype_ok(out_dtype) || B < 1 || H < 1 || M < 1 || !head_ok(d_head) ||
+      r_k < 1 || r_v < 1 || !cap_ok(n_max) || p0 < 0 || (int64_t)p0 + M > n_max ||
+      !std::isfinite(scale) || !(scale > 0.f))
+    return LLA_ERR_INVALID_ARG;
+  if ((int64_t)B * H * M > (1 << 30) || (int64_t)B * H > 65535) return LLA_ERR_INVALID_ARG;
+  if (!ptr_ok(q) || !ptr_ok(c_k) || !ptr_ok(c_v) || !ptr_ok(u_k) || !ptr_ok(u_v) || !ptr_ok(out) ||
+      !opt_ptr_ok(mu_k) || !opt_ptr_ok(mu_v))
+    return LLA_ERR_INVALID_ARG;
+  if (dtype != LLA_BF16 || d_head != 128 || r_k % 16 || r_v % 16 || r_k > 512 || r_v > 512)
+    return LLA_ERR_UNSUPPORTED;
+  size_t need = 0;
+  lla_prefill_2d_workspace_bytes(B, H, d_head, p0 + M, &need);
+  if (!workspace || !aligned16(workspace) || ws_bytes < need) return LLA_ERR_WORKSPACE;
+  (void)mu_k;  // q . mu_k is the same for every key of a query: it cancels in the softmax
+  lla::Prefill2dArgs a{};
+  a.out_dtype = out_dtype;
+  a.B = B;
+  a.H = H;
+  a.M = M;
+  a.rk = r_k;
+  a.rv = r_v;
+  a.n_max = n_max;
+  a.p0 = p0;
+  a.nk = (p0 + M + 63) / 64 * 64;
+  a.q = q;
+  a.ck = c_k;
+  a.cv = c_v;
+  a.uk = u_k;
+  a.uv = u_v;
+  a.muv = mu_v;
+  a.qscale = (float)((double)scale * kLog2e);
+  a.out = out;
+  a.kh = workspace;
+  a.vt = static_cast<char*>(workspace) + need / 2;
+  return hip_status(lla::launch_prefill_2d(a, static_cast<hipStream_t>(stream)));
+}
+
 }  // extern "C"

@@ -100,6 +100,26 @@ struct PrefillArgs {
 // bf16 MFMA causal prefill.
 hipError_t launch_prefill_bf16(const PrefillArgs& a, hipStream_t stream);
 
+// LLA-2D causal prefill: each head's K and V rebuilt into the workspace, then
+// attention over them (d_head = 128, bf16).
+struct Prefill2dArgs {
+  int out_dtype;
+  int B, H, M, rk, rv, n_max, p0;
+  int nk;           // rebuilt keys per sequence: p0 + M rounded up to a page
+  const void* q;    // [B][H][M][128]
+  const void* ck;   // [B][n_max][rk] token-major
+  const void* cv;   // [B][n_max/64][rv][64] paged feature-major
+  const void* uk;   // [H][128][rk]
+  const void* uv;   // [H][128][rv]
+  const void* muv;  // [H][128] or null
+  float qscale;     // softmax scale * log2(e)
+  void* out;        // [B][H][M][128]
+  void* kh;         // workspace: [B][H][nk][128] rebuilt keys
+  void* vt;         // workspace: [B][H][nk/64][128][64] rebuilt values, feature-major pages
+};
+size_t prefill_2d_ws_bytes(int B, int H, int n_keys);  // both rebuilt tensors
+hipError_t launch_prefill_2d(const Prefill2dArgs& a, hipStream_t stream);
+
 // Rotary embedding (half-split) of rows of dr elements.
 struct RopeArgs {
   int dtype;

@@ -1,0 +1,420 @@
+// LLA-2D causal prefill at loop l (Sec. 3 "The LLA-2D variant (loop x head)";
+// App. J "Per-head LLA versus LLA-2D at inference": either variant may take
+// the full-memory path that materialises K/V or attend over the latents).
+//
+// With one latent per token for all heads the ranks exceed d_head (288 / 480
+// against 128 at the 21.33x operating point), so the absorbed form would cost
+// 2 (r_k + r_v) flops per causal score, against 2 d_head (r_k + r_v) per key
+// and head to rebuild K and V once plus 4 d_head per score to attend over them.
+// For a prompt of M new tokens that is about 3x fewer flops from M ~ 128 on,
+// so this path rebuilds:
+//
+//   recon2d_kernel:  K_h = C_k U_{k,h}^T and V_h = C_v U_{v,h}^T (Eq. 3 with the
+//                    (l, h) slice of W_up) for every cached token n < p0 + M,
+//                    rounded to fp16, into a caller-owned workspace;
+//   flash2d_kernel:  causal attention of the M queries of every head over its
+//                    rebuilt K_h, V_h (d_head = 128), online softmax over
+//                    64-key pages, then out = O / l + mu_v.
+//
+// mu_k is not added: q . mu_k is the same for every key and cancels in the
+// softmax.  mu_v is added to the normalised output (the weights sum to 1).
+//
+// The attention's products run on fp16 MFMAs (the same rate as bf16 on this
+// chip): the bf16 query converts to fp16 exactly, and the rebuilt K and V and
+// the softmax weights keep 11 significant bits instead of bf16's 8, so the
+// rounding of these intermediates stays well inside the bf16 error budget even
+// for peaked rows.  Values beyond fp16's range (65504) become infinite and the
+// output is then not finite.
+//
+// Workspace layouts, chosen so that every MFMA operand of the attention is one
+// 16-byte LDS read:
+//   kh [B][H][nk][128]            keys token-major (a key's 128 features contiguous)
+//   vt [B][H][nk/64][128][64]     values feature-major per 64-key page; inside each
+//                                 16-key block the keys are stored in the order
+//                                 0-3, 8-11, 4-7, 12-15 (the order in which a
+//                                 32x32 accumulator hands its rows to a lane half)
+// with nk = p0 + M rounded up to a page; tokens n >= p0 + M are written as 0.
+
+#include "lla_device.h"
+#include "lla_internal.h"
+#include "../../include/lla.h"
+
+namespace lla {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int kD = 128;            // d_head of both kernels
+constexpr int kThreads = 256;      // 4 wavefronts
+constexpr int kRTok = 128;         // tokens per rebuild workgroup (two pages)
+constexpr int kQBlock = 128;       // queries per attention workgroup (32 per wavefront)
+constexpr float kLazy = 8.0f;      // raise the running max only when it grows by more than this (log2)
+
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
+__device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f16x8 as_f16x8(uint4 v) { return __builtin_bit_cast(f16x8, v); }
+__device__ __forceinline__ f32x16 mfma_h(f16x8 a, f16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+// two fp32 values as bf16 (output) or fp16 (rebuilt K / V), round to nearest even
+__device__ __forceinline__ uint32_t pack2(float lo, float hi) {
+  return uint32_t(f32_to_bf16(lo)) | (uint32_t(f32_to_bf16(hi)) << 16);
+}
+__device__ __forceinline__ uint32_t pack2h(float lo, float hi) {
+  const _Float16 a = (_Float16)lo, b = (_Float16)hi;
+  return uint32_t(__builtin_bit_cast(uint16_t, a)) | (uint32_t(__builtin_bit_cast(uint16_t, b)) << 16);
+}
+// max over both halves of the wavefront (lane i and lane i ^ 32)
+__device__ __forceinline__ float half_swap_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float half_swap_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// ---------------------------------------------------------------------------
+// Rebuild.  One workgroup = 128 tokens of one sequence, every head: the latent
+// tile is staged once in LDS token-major (a token's r features contiguous) and
+// wavefront w computes features 32w .. 32w + 31 of every head, with that
+// head's up-projection rows as the other operand (16-byte loads).
+//   keys:   D = K^T (M = feature, N = token, K = latent feature j), so a lane
+//           holds 4-feature runs of one token (8-byte stores);
+//   values: D = V (M = token, N = feature), so a lane holds the tokens
+//           16 b + 8 g .. + 7 of the permuted order of one feature (16-byte stores).
+// ---------------------------------------------------------------------------
+template <int AXIS, int KS>  // AXIS 0: keys, 1: values; KS = r / 16
+__global__ __launch_bounds__(kThreads) void recon2d_kernel(Prefill2dArgs a) {
+  constexpr int R = KS * 16;
+  constexpr int CS = R + 8;  // LDS row stride (bf16): 16-byte reads of 16 rows hit distinct banks
+  __shared__ __attribute__((aligned(16))) bf16_t s_c[kRTok * CS];
+
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int col = lane & 31, g = lane >> 5;
+  const int b = blockIdx.y, n0 = blockIdx.x * kRTok;
+  const int nvalid = a.p0 + a.M;  // tokens that hold latents; the rest are rebuilt as 0
+  const int H = a.H;
+
+  // ---- latent tile, token-major, zero past nvalid ----
+  if (AXIS == 0) {
+    const bf16_t* src = static_cast<const bf16_t*>(a.ck) + (size_t)b * a.n_max * R;
+    constexpr int C8 = R / 8;
+    for (int e = tid; e < kRTok * C8; e += kThreads) {
+      const int n = e / C8, c8 = e - n * C8;
+      const uint4 v = n0 + n < nvalid ? ld16(src + (size_t)(n0 + n) * R + 8 * c8) : make_uint4(0, 0, 0, 0);
+      *reinterpret_cast<uint4*>(&s_c[n * CS + 8 * c8]) = v;
+    }
+  } else {
+    // values: pages [R][64] feature-major; chunk = 8 tokens of one feature,
+    // transposed into the token-major tile with 2-byte stores
+    const bf16_t* src = static_cast<const bf16_t*>(a.cv) + (size_t)b * a.n_max * R;
+    for (int e = tid; e < kRTok / kPage * R * 8; e += kThreads) {
+      const int pg = e / (R * 8), rem = e - pg * (R * 8), j = rem >> 3, t8 = rem & 7;
+      const int nb = n0 + pg * kPage + 8 * t8;  // first token of the chunk
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (nb < nvalid) {
+        v = ld16(src + (size_t)(n0 / kPage + pg) * kPage * R + (size_t)j * kPage + 8 * t8);
+        const int nv = nvalid - nb;  // tokens of the chunk that hold latents
+        if (nv < 8) {
+          auto keep = [nv](int i) { return nv > 2 * i + 1 ? 0xffffffffu : nv > 2 * i ? 0x0000ffffu : 0u; };
+          v.x &= keep(0);
+          v.y &= keep(1);
+          v.z &= keep(2);
+          v.w &= keep(3);
+        }
+      }
+      const bf16_t* h8 = reinterpret_cast<const bf16_t*>(&v);
+      bf16_t* dst = &s_c[(pg * kPage + 8 * t8) * CS + j];
+#pragma unroll
+      for (int e2 = 0; e2 < 8; ++e2) dst[e2 * CS] = h8[e2];
+    }
+  }
+  __syncthreads();
+
+  const bf16_t* U = static_cast<const bf16_t*>(AXIS == 0 ? a.uk : a.uv);
+  const int ntile = min(kRTok, a.nk - n0) / 32;  // 32-token tiles of this workgroup inside nk
+  // up-projection rows 32 wave + col of head h as K-step operands
+  auto load_u = [&](int h, uint4 (&u)[KS]) {
+    const bf16_t* row = U + ((size_t)h * kD + 32 * wave + col) * R + 8 * g;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) u[s] = ld16(row + 16 * s);
+  };
+  uint4 ua[KS];
+  auto head = [&](int h, const uint4 (&u)[KS]) {
+    f32x16 acc[kRTok / 32];
+#pragma unroll
+    for (int nt = 0; nt < kRTok / 32; ++nt) acc[nt] = f32x16{0.f};
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+#pragma unroll
+      for (int nt = 0; nt < kRTok / 32; ++nt) {
+        if (nt < ntile) {
+          const bf16x8 c = as_bf16x8(*reinterpret_cast<const uint4*>(&s_c[(32 * nt + col) * CS + 16 * s + 8 * g]));
+          acc[nt] = AXIS == 0 ? mfma(as_bf16x8(u[s]), c, acc[nt]) : mfma(c, as_bf16x8(u[s]), acc[nt]);
+        }
+      }
+    }
+    const size_t bh = (size_t)b * H + h;
+#pragma unroll
+    for (int nt = 0; nt < kRTok / 32; ++nt) {
+      if (nt >= ntile) continue;
+      if (AXIS == 0) {
+        // lane (token col, half g), register r: feature 32 wave + 8 (r/4) + 4 g + r%4
+        uint16_t* dst = static_cast<uint16_t*>(a.kh) + (bh * a.nk + n0 + 32 * nt + col) * kD + 32 * wave + 4 * g;
+#pragma unroll
+        for (int c4 = 0; c4 < 4; ++c4)
+          *reinterpret_cast<uint2*>(dst + 8 * c4) =
+              make_uint2(pack2h(acc[nt][4 * c4], acc[nt][4 * c4 + 1]), pack2h(acc[nt][4 * c4 + 2], acc[nt][4 * c4 + 3]));
+      } else {
+        // lane (feature col, half g), registers 8 blk .. 8 blk + 7: tokens at
+        // permuted positions 16 blk + 8 g .. + 7 of the tile's 32
+        const int tok0 = n0 + 32 * nt;
+        uint16_t* dst = static_cast<uint16_t*>(a.vt) +
+                      ((bh * (a.nk / kPage) + tok0 / kPage) * kD + 32 * wave + col) * kPage + tok0 % kPage + 8 * g;
+#pragma unroll
+        for (int blk = 0; blk < 2; ++blk) {
+          const f32x16& x = acc[nt];
+          const int r0 = 8 * blk;
+          *reinterpret_cast<uint4*>(dst + 16 * blk) =
+              make_uint4(pack2h(x[r0], x[r0 + 1]), pack2h(x[r0 + 2], x[r0 + 3]), pack2h(x[r0 + 4], x[r0 + 5]),
+                         pack2h(x[r0 + 6], x[r0 + 7]));
+        }
+      }
+    }
+  };
+  // every operand load of a head is issued before its first product, so the
+  // products of the early K-steps overlap the later loads
+  for (int h = 0; h < H; ++h) {
+    load_u(h, ua);
+    head(h, ua);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Attention.  One workgroup = 4 wavefronts x 32 queries of one (b, h); keys in
+// 64-token pages staged in LDS (K token-major, V feature-major), two pages in
+// flight in registers.  Products (v_mfma_f32_32x32x16_f16), transposed so each
+// accumulator feeds the next product with no lane exchange:
+//   S^T  (M = key, N = query, K = feature): A = K tile rows,  B = the query (registers)
+//   O^T += (M = feature, N = query, K = key): A = V^T tile rows, B = P from S^T
+// A 32x32 accumulator gives lane (q + 32 g), register r the row 8(r/4) + 4g + r%4
+// of column q: registers 8u .. 8u + 7 of a key tile are the keys
+// 16u + 8(e/4) + 4g + e%4, e < 8, which the permuted V^T rows hold contiguously.
+// ---------------------------------------------------------------------------
+template <int N>
+struct IntC {
+  static constexpr int value = N;
+};
+
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
+void flash2d_kernel(Prefill2dArgs a) {
+  constexpr int KS = kD / 16;       // K-steps of the score product
+  constexpr int KST = kD + 8;       // K tile row stride (fp16 elements)
+  constexpr int VST = kPage + 8;    // V^T tile row stride (fp16 elements)
+  constexpr int KTILE = kPage * KST, VTILE = kD * VST;
+  constexpr int CH = kPage * kD / 8 / kThreads;  // 16-byte chunks per thread per page and axis (4)
+  __shared__ __attribute__((aligned(16))) uint16_t s_k[2 * KTILE];  // fp16
+  __shared__ __attribute__((aligned(16))) uint16_t s_v[2 * VTILE];
+
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int col = lane & 31, g = lane >> 5;
+  const int bh = blockIdx.x, h = bh % a.H;
+  const int M = a.M, p0 = a.p0;
+  const int nqb = (M + kQBlock - 1) / kQBlock;
+  const int qb = nqb - 1 - (int)blockIdx.y;  // heaviest (latest) query blocks first
+  const int q0 = qb * kQBlock, qw0 = q0 + 32 * wave;
+  const int myq = qw0 + col;
+  const bool q_ok = myq < M, wave_live = qw0 < M;
+  const int qlast_w = min(qw0 + 31, M - 1);
+  const int kmax = p0 + min(q0 + kQBlock, M);  // keys [0, kmax) matter to the workgroup
+  const int npages = (kmax + kPage - 1) / kPage;
+
+  // ---- page staging: both pages are 16 KB contiguous in the workspace ----
+  const uint16_t* kbase = static_cast<const uint16_t*>(a.kh) + (size_t)bh * a.nk * kD;
+  const uint16_t* vbase = static_cast<const uint16_t*>(a.vt) + (size_t)bh * a.nk * kD;
+  uint4 stk[2][CH], stv[2][CH];
+  auto load_page = [&](int pg, int set) {
+    const uint16_t* kp = kbase + (size_t)pg * kPage * kD;
+    const uint16_t* vp = vbase + (size_t)pg * kPage * kD;
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+      stk[set][c] = ld16(kp + 8 * (tid + c * kThreads));
+      stv[set][c] = ld16(vp + 8 * (tid + c * kThreads));
+    }
+  };
+  auto store_page = [&](int set, int buf) {
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+      const int ch = tid + c * kThreads;
+      *reinterpret_cast<uint4*>(&s_k[buf * KTILE + (ch >> 4) * KST + 8 * (ch & 15)]) = stk[set][c];
+      *reinterpret_cast<uint4*>(&s_v[buf * VTILE + (ch >> 3) * VST + 8 * (ch & 7)]) = stv[set][c];
+    }
+  };
+
+  load_page(0, 0);
+  load_page(min(1, npages - 1), 1);
+  // the query as the score product's B operand: lane (q, g), K-step s = features
+  // 16s + 8g .. + 7, converted from bf16 to fp16
+  f16x8 qop[KS];
+  {
+    const bf16_t* qrow = static_cast<const bf16_t*>(a.q) + ((size_t)bh * M + (q_ok ? myq : 0)) * kD + 8 * g;
+    uint4 raw[KS];
+#pragma unroll
+    for (int s = 0; s < KS; ++s) raw[s] = ld16(qrow + 16 * s);
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      float x[8];
+      Elem<bf16_t>::unpack(raw[s], x);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qop[s][e] = (_Float16)x[e];
+    }
+  }
+  store_page(0, 0);
+  __syncthreads();
+
+  f32x16 oacc[kD / 32];
+#pragma unroll
+  for (int t = 0; t < kD / 32; ++t) oacc[t] = f32x16{0.f};
+  float m_run = neg_inf(), l_lane = 0.f;
+  const float qs = a.qscale;
+  const int qpos = p0 + myq;
+
+  auto page = [&](int p, auto bufc) {
+    constexpr int buf = decltype(bufc)::value;
+    // set buf held page p (already in LDS); page p + 2 goes into it (near the
+    // end the last page is re-read, so every wait is for exactly one page)
+    load_page(min(p + 2, npages - 1), buf);
+    const int key0 = p * kPage;
+    if (wave_live && key0 <= p0 + qlast_w) {
+      const bool diag = key0 + kPage - 1 > p0 + qw0;
+      const uint16_t* kt_row = s_k + buf * KTILE + col * KST + 8 * g;
+      const uint16_t* vt_row = s_v + buf * VTILE + col * VST + 8 * g;
+      f32x16 sc[2] = {f32x16{0.f}, f32x16{0.f}};
+#pragma unroll
+      for (int s = 0; s < KS; ++s)
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+          sc[kt] = mfma_h(as_f16x8(*reinterpret_cast<const uint4*>(kt_row + 32 * kt * KST + 16 * s)), qop[s], sc[kt]);
+      const int lim = qpos - key0 - 4 * g;
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt) {
+        f32x16& v = sc[kt];
+        if (__builtin_expect(diag, 0)) {
+          // key 32kt + 8(r/4) + 4g + r%4 of the page is visible iff 32kt + 8(r/4) + r%4 <= lim
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            if (32 * kt + 8 * (r / 4) + (r % 4) > lim) v[r] = neg_inf();
+        }
+        float m0 = fmaxf(fmaxf(v[0], v[1]), v[2]), m1 = fmaxf(fmaxf(v[8], v[9]), v[10]);
+        m0 = fmaxf(fmaxf(m0, v[3]), v[4]);
+        m1 = fmaxf(fmaxf(m1, v[11]), v[12]);
+        m0 = fmaxf(fmaxf(m0, v[5]), v[6]);
+        m1 = fmaxf(fmaxf(m1, v[13]), v[14]);
+        const float mx = half_swap_max(fmaxf(fmaxf(m0, v[7]), fmaxf(m1, v[15]))) * qs;
+        // raise the running max on the first half-page, then only when a
+        // score exceeds it by more than 2^kLazy (the weights stay below 2^kLazy)
+        const bool raise = mx > m_run + kLazy || (p == 0 && kt == 0);
+        if (__builtin_expect(__builtin_amdgcn_ballot_w64(raise) != 0, 0)) {
+          if (raise) {
+            const float alpha = m_run == neg_inf() ? 0.f : __builtin_amdgcn_exp2f(m_run - mx);
+#pragma unroll
+            for (int t = 0; t < kD / 32; ++t) oacc[t] *= alpha;
+            l_lane *= alpha;
+            m_run = mx;
+          }
+        }
+        f16x8 pop[2];
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float pv = __builtin_amdgcn_exp2f(fmaf(v[8 * u + e], qs, -m_run));  // exp2(-inf) = 0
+            l_lane += pv;
+            pop[u][e] = (_Float16)pv;
+          }
+#pragma unroll
+        for (int t = 0; t < kD / 32; ++t)
+#pragma unroll
+          for (int u = 0; u < 2; ++u)
+            oacc[t] = mfma_h(as_f16x8(*reinterpret_cast<const uint4*>(vt_row + 32 * t * VST + 32 * kt + 16 * u)),
+                             pop[u], oacc[t]);
+      }
+    }
+    if (p + 1 < npages) store_page(buf ^ 1, buf ^ 1);
+    __syncthreads();
+  };
+  for (int p = 0; p < npages; p += 2) {
+    page(p, IntC<0>{});
+    if (p + 1 < npages) page(p + 1, IntC<1>{});
+  }
+
+  // ---- epilogue: out = O / l + mu_v ----
+  if (!wave_live) return;
+  const float inv_l = 1.0f / half_swap_sum(l_lane);
+  const bf16_t* muv = a.muv ? static_cast<const bf16_t*>(a.muv) + (size_t)h * kD : nullptr;
+  const size_t orow = ((size_t)bh * M + myq) * kD;
+  if (!q_ok) return;
+#pragma unroll
+  for (int t = 0; t < kD / 32; ++t) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int i0 = 32 * t + 8 * c + 4 * g;
+      const uint2 mw = muv ? *reinterpret_cast<const uint2*>(muv + i0) : make_uint2(0, 0);
+      const float v0 = fmaf(oacc[t][4 * c + 0], inv_l, bf16_lo(mw.x));
+      const float v1 = fmaf(oacc[t][4 * c + 1], inv_l, bf16_hi(mw.x));
+      const float v2 = fmaf(oacc[t][4 * c + 2], inv_l, bf16_lo(mw.y));
+      const float v3 = fmaf(oacc[t][4 * c + 3], inv_l, bf16_hi(mw.y));
+      if (a.out_dtype == LLA_F32)
+        *reinterpret_cast<float4*>(static_cast<float*>(a.out) + orow + i0) = make_float4(v0, v1, v2, v3);
+      else
+        *reinterpret_cast<uint2*>(static_cast<bf16_t*>(a.out) + orow + i0) = make_uint2(pack2(v0, v1), pack2(v2, v3));
+    }
+  }
+}
+
+template <int AXIS, int KS>
+hipError_t launch_recon(const Prefill2dArgs& a, hipStream_t stream) {
+  const dim3 grid((a.nk + kRTok - 1) / kRTok, a.B);
+  hipLaunchKernelGGL((recon2d_kernel<AXIS, KS>), grid, dim3(kThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+template <int AXIS>
+hipError_t launch_recon_r(const Prefill2dArgs& a, int r, hipStream_t stream) {
+  switch (r / 16) {
+#define LLA_R(ks) \
+  case ks: return launch_recon<AXIS, ks>(a, stream);
+    LLA_R(1) LLA_R(2) LLA_R(3) LLA_R(4) LLA_R(5) LLA_R(6) LLA_R(7) LLA_R(8)
+    LLA_R(9) LLA_R(10) LLA_R(11) LLA_R(12) LLA_R(13) LLA_R(14) LLA_R(15) LLA_R(16)
+    LLA_R(17) LLA_R(18) LLA_R(19) LLA_R(20) LLA_R(21) LLA_R(22) LLA_R(23) LLA_R(24)
+    LLA_R(25) LLA_R(26) LLA_R(27) LLA_R(28) LLA_R(29) LLA_R(30) LLA_R(31) LLA_R(32)
+#undef LLA_R
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace
+
+size_t prefill_2d_ws_bytes(int B, int H, int n_keys) {
+  const size_t nk = ((size_t)n_keys + kPage - 1) / kPage * kPage;
+  return 2 * (size_t)B * H * nk * kD * sizeof(bf16_t);
+}
+
+hipError_t launch_prefill_2d(const Prefill2dArgs& a, hipStream_t stream) {
+  hipError_t e = launch_recon_r<0>(a, a.rk, stream);
+  if (e != hipSuccess) return e;
+  e = launch_recon_r<1>(a, a.rv, stream);
+  if (e != hipSuccess) return e;
+  const dim3 grid(a.B * a.H, (a.M + kQBlock - 1) / kQBlock);
+  hipLaunchKernelGGL(flash2d_kernel, grid, dim3(kThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace lla

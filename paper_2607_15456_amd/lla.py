@@ -51,6 +51,8 @@ _SIGS = {
     "lla_encode_2d_workspace_bytes": (_c_int, [_c_int] * 7 + [ctypes.POINTER(_c_sz)]),
     "lla_decode_2d_workspace_bytes": (_c_int, [_c_int] * 5 + [ctypes.POINTER(_c_sz)]),
     "lla_decode_attn_2d": (_c_int, [_c_int] * 9 + [_c_vp] * 8 + [_c_f, _c_vp, _c_vp, _c_sz, _c_vp]),
+    "lla_prefill_2d_workspace_bytes": (_c_int, [_c_int] * 4 + [ctypes.POINTER(_c_sz)]),
+    "lla_prefill_attn_2d": (_c_int, [_c_int] * 10 + [_c_vp] * 7 + [_c_f, _c_vp, _c_vp, _c_sz, _c_vp]),
     "lla_decode_attn_fullrope": (_c_int, [_c_int] * 9 + [_c_vp] * 9 + [ctypes.c_double, _c_f, _c_vp, _c_vp,
                                                                           _c_sz, _c_vp]),
 }
@@ -456,6 +458,41 @@ def decode_attn_2d(q, c_k, c_v, u_k, u_v, *, n_ctx: int, ctx_len=None, mu_k=None
                                     _ptr(ctx_len), _ptr(q), _ptr(c_k), _ptr(c_v), _ptr(u_k), _ptr(u_v),
                                     _ptr(mu_k), _ptr(mu_v), float(scale), _ptr(out), _ptr(workspace),
                                     workspace.numel() * workspace.element_size(), _stream(q)))
+    return out
+
+
+def prefill_2d_workspace_bytes(B: int, H: int, d_head: int, n_keys: int) -> int:
+    out = _c_sz()
+    _check(lib().lla_prefill_2d_workspace_bytes(B, H, d_head, n_keys, ctypes.byref(out)))
+    return out.value
+
+
+def prefill_attn_2d(q, c_k, c_v, u_k, u_v, *, p0: int = 0, mu_k=None, mu_v=None,
+                    scale: float | None = None, out=None, out_dtype=torch.float32, workspace=None):
+    """LLA-2D causal prefill of q [B, H, M, d] at positions p0 .. p0+M-1 over the
+    shared latents (caches from alloc_cache_2d, filled up to p0+M-1); u_k
+    [H, d, r_k], u_v [H, d, r_v].  workspace: uint8 device tensor of at least
+    prefill_2d_workspace_bytes(B, H, d, p0 + M) (allocated if None).
+    Returns out [B, H, M, d]."""
+    dev = q.device
+    B, H, M, d = q.shape
+    for t, n in ((q, "q"), (c_k, "c_k"), (c_v, "c_v"), (u_k, "u_k"), (u_v, "u_v")):
+        _need(t, n, q.dtype, dev)
+    r_k, r_v = u_k.shape[2], u_v.shape[2]
+    n_max = c_k.shape[1]
+    if (c_k.shape != (B, n_max, r_k) or c_v.shape != (B, n_max // PAGE, r_v, PAGE)
+            or u_k.shape != (H, d, r_k) or u_v.shape != (H, d, r_v)):
+        raise ValueError("inconsistent shapes")
+    if out is None:
+        out = torch.empty((B, H, M, d), dtype=out_dtype, device=dev)
+    if workspace is None:
+        workspace = torch.empty(prefill_2d_workspace_bytes(B, H, d, p0 + M), dtype=torch.uint8, device=dev)
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    _check(lib().lla_prefill_attn_2d(_dt(q), _out_code(out.dtype), B, H, M, d, r_k, r_v, n_max, p0,
+                                     _ptr(q), _ptr(c_k), _ptr(c_v), _ptr(u_k), _ptr(u_v), _ptr(mu_k),
+                                     _ptr(mu_v), float(scale), _ptr(out), _ptr(workspace),
+                                     workspace.numel() * workspace.element_size(), _stream(q)))
     return out
 
 

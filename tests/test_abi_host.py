@@ -34,14 +34,15 @@ def test_header_declares_the_boundary():
                             "lla_decode_attn_rope", "lla_prefill_attn_rope", "lla_encode_ring",
                             "lla_rope_write_ring", "lla_encode_2d", "lla_encode_2d_workspace_bytes",
                             "lla_decode_2d_workspace_bytes", "lla_decode_attn_2d",
-                            "lla_decode_attn_fullrope"])
+                            "lla_decode_attn_fullrope", "lla_prefill_2d_workspace_bytes",
+                            "lla_prefill_attn_2d"])
 
 
 def test_library_exports_every_declared_symbol():
     h = ctypes.CDLL(lla.LIB_PATH)
     for name in _declared():
         assert hasattr(h, name), name
-    assert lla.abi_version() == 6
+    assert lla.abi_version() == 7
 
 
 def test_status_strings():
@@ -350,3 +351,33 @@ def _decode_fullrope(**kw):
 ])
 def test_decode_fullrope_rejects(kw, code):
     assert _decode_fullrope(**kw) == code
+
+
+# ---- LLA-2D causal prefill ----
+
+def test_prefill_2d_workspace_bytes():
+    # rebuilt keys and values of every head, bf16: 4 * B * H * d * (n_keys rounded up to 64)
+    assert lla.prefill_2d_workspace_bytes(4, 16, 128, 8192) == 4 * 4 * 16 * 128 * 8192
+    assert lla.prefill_2d_workspace_bytes(1, 1, 128, 1) == 4 * 128 * 64
+    assert lla.prefill_2d_workspace_bytes(2, 3, 128, 65) == 4 * 2 * 3 * 128 * 128
+
+
+def _prefill_2d(**kw):
+    a = dict(dtype=1, out_dtype=0, B=2, H=16, M=100, d=128, rk=288, rv=480, n_max=512, p0=0, q=P, ck=P, cv=P,
+             uk=P, uv=P, muk=None, muv=None, scale=0.088, out=P, ws=P, ws_bytes=1 << 30, stream=None)
+    a.update(kw)
+    return lla.lib().lla_prefill_attn_2d(a["dtype"], a["out_dtype"], a["B"], a["H"], a["M"], a["d"], a["rk"],
+                                         a["rv"], a["n_max"], a["p0"], a["q"], a["ck"], a["cv"], a["uk"], a["uv"],
+                                         a["muk"], a["muv"], a["scale"], a["out"], a["ws"], a["ws_bytes"],
+                                         a["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dtype=2), 1), (dict(B=0), 1), (dict(M=0), 1), (dict(d=48), 1), (dict(rk=0), 1),
+    (dict(n_max=100), 1), (dict(p0=-1), 1), (dict(p0=413), 1), (dict(scale=float("nan")), 1),
+    (dict(q=None), 1), (dict(cv=MIS), 1), (dict(muv=MIS), 1),
+    (dict(dtype=0), 2), (dict(d=64), 2), (dict(rk=40), 2), (dict(rv=520), 2),
+    (dict(ws=None), 3), (dict(ws_bytes=4 * 2 * 16 * 128 * 128 - 1), 3), (dict(ws=MIS), 3),
+])
+def test_prefill_2d_rejects(kw, code):
+    assert _prefill_2d(**kw) == code
