@@ -59,7 +59,8 @@ def parse():
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--workload", default="ouro14b_decode",
-                   choices=["ouro14b_decode", "ouro26b_long", "rank_sweep", "prefill_write", "ouro14b_2d"])
+                   choices=["ouro14b_decode", "ouro26b_long", "rank_sweep", "prefill_write", "ouro14b_2d",
+                            "prefill_2d"])
     p.add_argument("--tier", type=int, default=None, help="rank_sweep: run only this tier index")
     p.add_argument("--evict", default=None,
                    help="SINK,WINDOW: decode workloads keep a sink + window eviction budget (ring cache of "
@@ -559,6 +560,117 @@ def run_decode_2d(args, torch, lla, W):
 
 
 # ---------------------------------------------------------------------------
+# LLA-2D prefill + cache write (prefill_2d)
+# ---------------------------------------------------------------------------
+
+def prefill_2d_flops(B, H, M, p0, d, r_k, r_v):
+    """Algorithmic flops of one LLA-2D prefill call on the rebuild path: every
+    head's K and V rebuilt for the p0 + M cached tokens (2 d (r_k + r_v) per
+    token and head), then 4 d per causal (query, key) pair (scores and values)."""
+    pairs = M * p0 + M * (M + 1) // 2
+    return B * H * (2 * d * (r_k + r_v) * (p0 + M) + 4 * d * pairs)
+
+
+def run_prefill_2d(args, torch, lla, W):
+    wl = W.WORKLOADS["prefill_2d"]
+    r_k, r_v = wl.ranks[0]
+    B, M, H, d, T = wl.B, wl.N, wl.H, wl.d, wl.T
+    K = T * H * d
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    xk = W.normal((B, M, K), (wl.name, "x_k"), 1.0, wl.dtype, dev)
+    xv = W.normal((B, M, K), (wl.name, "x_v"), 1.0, wl.dtype, dev)
+    wk = W.normal((r_k, K), (wl.name, "Wd_k"), 1.0 / K, wl.dtype, dev)
+    wv = W.normal((r_v, K), (wl.name, "Wd_v"), 1.0 / K, wl.dtype, dev)
+    ck, cv = lla.alloc_cache_2d(B, M, r_k, r_v, device=dev)
+    loops = []
+    for l in range(T):
+        uk, uv = W.codec_loop_2d(wl, r_k, r_v, 0, l, dev)
+        loops.append((W.queries(wl, 0, l, M=M, device=dev), uk, uv,
+                      torch.empty((B, H, M, d), dtype=torch.float32, device=dev)))
+    ws = torch.empty(lla.prefill_2d_workspace_bytes(B, H, d, M), dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+    enc_t, pre_t = KernelTimer(torch, stream), KernelTimer(torch, stream)
+
+    def step(timed):
+        s = enc_t.start() if timed else None
+        lla.encode_2d(xk, xv, wk, wv, ck, cv, T=T, H=H, pos0=0)
+        if timed:
+            enc_t.stop(s)
+        for q, uk, uv, out in loops:
+            s = pre_t.start() if timed else None
+            lla.prefill_attn_2d(q, ck, cv, uk, uv, p0=0, out=out, workspace=ws)
+            if timed:
+                pre_t.stop(s)
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for _ in range(args.steps):
+        step(True)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    step_ms = t0.elapsed_time(t1) / args.steps
+    enc_ms, pre_ms = enc_t.mean_ms(), pre_t.mean_ms()
+    fl = prefill_2d_flops(B, H, M, 0, d, r_k, r_v)
+    eb = 2 * B * M * K * 2 + (r_k + r_v) * K * 2 + B * M * (r_k + r_v) * 2
+    tflops = fl / (pre_ms * 1e-3) / 1e12
+    return {
+        "metric": "LLA-2D prefill + cache write tokens/sec (2D encode of the loop x head stack, causal prefill "
+                  "of all heads at every loop)",
+        "value": round(B * M / (step_ms * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(step_ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": wl.description, "batch": B, "new_tokens": M, "heads": H, "d_head": d, "loops": T,
+                   "r_k": r_k, "r_v": r_v, "parallelism": "single GPU"},
+        "roofline": {"bound": "mfma", "achieved": round(tflops, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(tflops / BF16_PEAK_TFLOPS, 4), "traffic": None,
+                     "kernel": "recon2d_kernel (K, V) + flash2d_kernel (lla_prefill_attn_2d)",
+                     "flops_per_launch": fl, "avg_launch_ms": round(pre_ms, 5)},
+        "encode": {"bound": "hbm", "achieved": round(eb / (enc_ms * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS,
+                   "unit": "GB/s", "frac": round(eb / (enc_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                   "bytes_per_launch": eb, "avg_launch_ms": round(enc_ms, 5)},
+        "cpu_baseline": None if args.no_cpu else cpu_baseline_prefill_2d(wl, r_k, r_v, ck, cv, loops, torch),
+    }
+
+
+def cpu_baseline_prefill_2d(wl, r_k, r_v, ck, cv, loops, torch, budget_s=15.0):
+    """Time the oracle on a sample of the step's prefill: query rows of sequence
+    0 at random positions, all heads at once (oracle.prefill_attn_2d on a
+    one-row prompt at offset m, which rebuilds every head's K and V over the
+    row's m + 1 keys), until about budget_s; the mean row time is scaled to
+    the B M rows x T loops of the step (the 2D encode is not timed)."""
+    import numpy as np
+    import oracle
+    from paper_2607_15456_amd.lla import from_paged
+
+    B, M, T = wl.B, wl.N, wl.T
+    ck0 = ck[0].cpu().double().numpy()
+    cv0 = from_paged(cv[0:1, None], M)[0, 0].cpu().double().numpy()
+    q, uk, uv, _ = loops[0]
+    q0, uk0, uv0 = q[0].cpu().double().numpy(), uk.cpu().double().numpy(), uv.cpu().double().numpy()
+    rng = np.random.default_rng(0)
+    spent, nrows = 0.0, 0
+    for m in rng.permutation(M):
+        if spent >= budget_s:
+            break
+        m = int(m)
+        t0 = time.perf_counter()
+        oracle.prefill_attn_2d(q0[:, m:m + 1], ck0, cv0, uk0, uv0, p0=m)
+        spent += time.perf_counter() - t0
+        nrows += 1
+    step_s = spent / nrows * B * M * T
+    return dict(value=B * M / step_s, unit="tokens/s", cores=cpu_threads(), kind="oracle",
+                sample=(f"oracle.prefill_attn_2d (float64, plain definition) on {nrows} query rows of "
+                        f"sequence 0 at loop 0 (all {wl.H} heads, rows at random positions), "
+                        f"{spent:.1f} s of CPU time; per-row time x {B * M} rows x {T} loops; the 2D encode "
+                        "is not timed"))
+
+
+# ---------------------------------------------------------------------------
 # main
 # ---------------------------------------------------------------------------
 
@@ -591,6 +703,9 @@ def main():
         return
     if args.workload == "ouro14b_2d":
         print(json.dumps(run_decode_2d(args, torch, lla, W)), flush=True)
+        return
+    if args.workload == "prefill_2d":
+        print(json.dumps(run_prefill_2d(args, torch, lla, W)), flush=True)
         return
 
     wl, results = run_decode(args, torch, lla, W)

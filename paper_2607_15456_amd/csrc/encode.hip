@@ -41,6 +41,7 @@ __device__ __forceinline__ size_t cache_index(int b, int h, int H, int n_max, in
 }
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int kEncTok = 32;           // tokens per workgroup block
 constexpr int kEncKC = 512;           // K elements staged per step
@@ -329,6 +330,164 @@ __global__ __launch_bounds__(256) void encode_few_kernel(EncodeArgs a, int nrc_k
   }
 }
 
+// Prefill-sized writes over a long stack (the LLA-2D down-projection, K =
+// T*H*d = 8192 values into r = 288 / 480): 2 r flops per byte of x, a
+// compute-bound GEMM.  A workgroup of 8 wavefronts takes 256 tokens x 96 rows
+// of one axis; both operands are staged through double-buffered LDS in K-chunks
+// of 64 (two further chunks in flight in registers), and wavefront w computes
+// tokens 32w .. 32w + 31 x all 96 rows on v_mfma_f32_32x32x16_bf16 (one
+// launch per axis):
+//   keys   (token-major cache): D = C^T (M = row, N = token), a lane holds
+//          4-row runs of one token;
+//   values (feature-major pages): D = C (M = token, N = row).
+// The row blocks of one token block are dispatched back to back on one XCD
+// (workgroup i runs on XCD i % 8), so its x chunks come from that XCD's L2
+// after the first read.  With a mean, wavefronts 0 .. 2 also form W_down^T mu
+// for one 32-row tile each (mu as a broadcast operand), shared through LDS.
+// grid: x = (row blocks) * (token blocks rounded up to 8), y = head
+constexpr int kGTok = 256, kGRow = 96, kGKC = 64, kGS = kGKC + 8;
+constexpr int kGThreads = 512;
+
+__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+template <int AXIS>
+__global__ __launch_bounds__(kGThreads) __attribute__((amdgpu_waves_per_eu(2)))
+void encode_gemm_kernel(EncodeArgs a, int nrb, int ntb) {
+  __shared__ __attribute__((aligned(16))) bf16_t s_x[2][kGTok * kGS];
+  __shared__ __attribute__((aligned(16))) bf16_t s_w[2][kGRow * kGS];
+  __shared__ float s_mu[kGRow];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int col = lane & 31, g = lane >> 5;
+  // XCD-aware order: the j-th workgroup of XCD x takes token block x + 8 (j / nrb), row block j % nrb
+  const int xcd = blockIdx.x % 8, j = blockIdx.x / 8;
+  const int tb = xcd + 8 * (j / nrb), rb = j % nrb;
+  if (tb >= ntb) return;  // padding of the grid to whole rounds of 8 token blocks
+  constexpr int axis = AXIS;
+  const int row0 = rb * kGRow;
+  const int r = pick(a.r, axis), K = a.K, H = a.H, h = blockIdx.y;
+  const int TT = a.B * a.M, t0 = tb * kGTok;
+  const bf16_t* xg = static_cast<const bf16_t*>(pick(a.x, axis));
+  const bf16_t* wg = static_cast<const bf16_t*>(pick(a.wdt, axis)) + (size_t)h * r * K;
+  const int nkc = K / kGKC;
+
+  // staging: x chunk = 256 tokens x 64 (4 chunks of 16 bytes per thread),
+  // W chunk = 96 rows x 64 (768 chunks: threads 0 .. 255 take two)
+  uint4 sxa[4], swa[2], sxb[4], swb[2];  // two register sets, named at compile time
+  auto load = [&](int kc, uint4 (&sx)[4], uint4 (&sw)[2]) {
+    const int k0 = kc * kGKC;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = tid + i * kGThreads, tok = c >> 3, part = c & 7, t = t0 + tok;
+      sx[i] = ld16(xg + ((size_t)(t < TT ? t : TT - 1) * H + h) * K + k0 + 8 * part);
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int c = tid + i * kGThreads, row = row0 + (c >> 3), part = c & 7;
+      sw[i] = ld16(wg + (size_t)(row < r ? row : r - 1) * K + k0 + 8 * part);
+    }
+  };
+  auto store = [&](const uint4 (&sx)[4], const uint4 (&sw)[2], int buf) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = tid + i * kGThreads, tok = c >> 3, part = c & 7;
+      *reinterpret_cast<uint4*>(&s_x[buf][tok * kGS + 8 * part]) = t0 + tok < TT ? sx[i] : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int c = tid + i * kGThreads, rr = c >> 3, part = c & 7;
+      if (c < kGRow * 8)
+        *reinterpret_cast<uint4*>(&s_w[buf][rr * kGS + 8 * part]) = row0 + rr < r ? sw[i] : make_uint4(0, 0, 0, 0);
+    }
+  };
+
+  f32x16 acc[3], accm = f32x16{0.f};
+#pragma unroll
+  for (int rt = 0; rt < 3; ++rt) acc[rt] = f32x16{0.f};
+  const bool mu = pick(a.mu, axis) != nullptr;  // uniform
+  const bf16_t* mug = mu ? static_cast<const bf16_t*>(pick(a.mu, axis)) + (size_t)h * K + 8 * g : nullptr;
+
+  auto chunk = [&](int kc, int buf) {
+    const bf16_t* xs = &s_x[buf][(32 * wave + col) * kGS + 8 * g];
+    const bf16_t* ws = &s_w[buf][col * kGS + 8 * g];
+#pragma unroll
+    for (int s = 0; s < kGKC / 16; ++s) {
+      const bf16x8 xo = as_bf16x8(*reinterpret_cast<const uint4*>(xs + 16 * s));
+#pragma unroll
+      for (int rt = 0; rt < 3; ++rt) {
+        const bf16x8 wo = as_bf16x8(*reinterpret_cast<const uint4*>(ws + 32 * rt * kGS + 16 * s));
+        acc[rt] = axis == 0 ? mfma32(wo, xo, acc[rt]) : mfma32(xo, wo, acc[rt]);
+      }
+      if (mu && wave < 3) {
+        const bf16x8 wo = as_bf16x8(*reinterpret_cast<const uint4*>(ws + 32 * wave * kGS + 16 * s));
+        accm = mfma32(wo, as_bf16x8(ld16(mug + kc * kGKC + 16 * s)), accm);
+      }
+    }
+  };
+
+  // set a holds even chunks, set b odd ones; chunk kc is in LDS buffer kc % 2
+  load(0, sxa, swa);
+  load(nkc > 1 ? 1 : 0, sxb, swb);
+  store(sxa, swa, 0);
+  __syncthreads();
+  for (int kc = 0; kc < nkc; kc += 2) {
+    load(min(kc + 2, nkc - 1), sxa, swa);
+    chunk(kc, 0);
+    if (kc + 1 < nkc) store(sxb, swb, 1);
+    __syncthreads();
+    if (kc + 1 < nkc) {
+      load(min(kc + 3, nkc - 1), sxb, swb);
+      chunk(kc + 1, 1);
+      if (kc + 2 < nkc) store(sxa, swa, 0);
+      __syncthreads();
+    }
+  }
+  if (mu) {
+    // accm (M = row of tile `wave`, N = any column): rows 8(q/4) + 4g + q%4
+    if (wave < 3 && col == 0) {
+#pragma unroll
+      for (int q = 0; q < 16; ++q) s_mu[32 * wave + 8 * (q / 4) + 4 * g + q % 4] = accm[q];
+    }
+    __syncthreads();
+  }
+
+  bf16_t* cout = static_cast<bf16_t*>(pick(a.c, axis));
+  if (axis == 0) {
+    // lane (token col, half g), register q of row tile rt: row 32 rt + 8(q/4) + 4g + q%4
+    const int t = t0 + 32 * wave + col;
+    if (t < TT) {
+      const int b = t / a.M, pos = ring_slot(a.pos0 + (t - b * a.M), a.sink, a.window);
+#pragma unroll
+      for (int rt = 0; rt < 3; ++rt)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          const int rl = 32 * rt + 8 * (q / 4) + 4 * g + q % 4, row = row0 + rl;
+          if (row < r)
+            cout[cache_index(b, h, H, a.n_max, r, pos, row, a.k_token_major != 0)] =
+                f32_to_bf16(acc[rt][q] - (mu ? s_mu[rl] : 0.f));
+        }
+    }
+  } else {
+    // lane (row col of tile rt, half g), register q: token 32 wave + 8(q/4) + 4g + q%4
+#pragma unroll
+    for (int rt = 0; rt < 3; ++rt) {
+      const int rl = 32 * rt + col, row = row0 + rl;
+      if (row >= r) continue;
+      const float m = mu ? s_mu[rl] : 0.f;
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const int t = t0 + 32 * wave + 8 * (q / 4) + 4 * g + q % 4;
+        if (t < TT) {
+          const int b = t / a.M, pos = ring_slot(a.pos0 + (t - b * a.M), a.sink, a.window);
+          cout[cache_index(b, h, H, a.n_max, r, pos, row)] = f32_to_bf16(acc[rt][q] - m);
+        }
+      }
+    }
+  }
+}
+
 // Second launch of a split write: tile unit (grid x, y, z as the split launch
 // with z = head) adds its ksplit fp32 partials in split order and writes the
 // cache exactly as the unsplit path does.
@@ -436,6 +595,14 @@ hipError_t launch_encode(const EncodeArgs& a, hipStream_t stream) {
         hipLaunchKernelGGL((encode_stream_kernel<16>), grid, dim3(256), 0, stream, a, bpw);
       else
         hipLaunchKernelGGL((encode_stream_kernel<8>), grid, dim3(256), 0, stream, a, bpw);
+      return hipGetLastError();
+    }
+    if (TT >= kGTok && a.K >= 2048 && a.K % kGKC == 0) {
+      // prefill-sized write over a long stack (the LLA-2D down-projection): a compute-bound GEMM
+      const int ntb = (TT + kGTok - 1) / kGTok, ntb8 = (ntb + 7) / 8 * 8;
+      const int nrb_k = (a.r[0] + kGRow - 1) / kGRow, nrb_v = (a.r[1] + kGRow - 1) / kGRow;
+      hipLaunchKernelGGL(encode_gemm_kernel<0>, dim3(nrb_k * ntb8, a.H), dim3(kGThreads), 0, stream, a, nrb_k, ntb);
+      hipLaunchKernelGGL(encode_gemm_kernel<1>, dim3(nrb_v * ntb8, a.H), dim3(kGThreads), 0, stream, a, nrb_v, ntb);
       return hipGetLastError();
     }
     const int heads_per_wg = blocks >= 256 ? a.H : 1;

@@ -99,6 +99,36 @@ def test_encode_2d_then_decode(M, pos0):
         assert_close(f64(out), ref, torch.bfloat16, "encode -> decode")
 
 
+@pytest.mark.parametrize("B,M,pos0,r_k,r_v", [(2, 520, 64, 288, 480), (3, 256, 0, 96, 160), (1, 1000, 24, 576, 400)])
+def test_encode_2d_prompt_write_with_means(B, M, pos0, r_k, r_v):
+    """A prompt-sized 2D write (the tiled GEMM over the loop x head stack): token
+    blocks straddle sequences, row blocks are partial at r = 400, 576, both means."""
+    T, H, d = 4, 16, 128
+    n_max = ((pos0 + M + 63) // 64) * 64 + 64
+    K = T * H * d
+    log(f"encode 2d prompt write B={B} M={M} pos0={pos0} r=({r_k},{r_v})")
+    xk = W.normal((B, M, K), ("two_d", "px_k", M), 1.0, torch.bfloat16, DEV)
+    xv = W.normal((B, M, K), ("two_d", "px_v", M), 1.0, torch.bfloat16, DEV)
+    # variance 1/(16 K): latents ~ N(0, 1/8), so a one-ulp bf16 rounding flip stays below 2e-2
+    wk = W.normal((r_k, K), ("two_d", "pWd_k", r_k), 1.0 / (16 * K), torch.bfloat16, DEV)
+    wv = W.normal((r_v, K), ("two_d", "pWd_v", r_v), 1.0 / (16 * K), torch.bfloat16, DEV)
+    muk = W.normal((K,), ("two_d", "pmu_k"), 1.0, torch.bfloat16, DEV)
+    muv = W.normal((K,), ("two_d", "pmu_v"), 1.0, torch.bfloat16, DEV)
+    ck, cv = lla.alloc_cache_2d(B, n_max, r_k, r_v, device=DEV)
+    ck.fill_(7.0)
+    cv.fill_(7.0)
+    lla.encode_2d(xk, xv, wk, wv, ck, cv, T=T, H=H, pos0=pos0, mu_k=muk, mu_v=muv)
+    torch.cuda.synchronize()
+    refk = np.stack([oracle.encode(f64(xk)[b], f64(muk), f64(wk).T) for b in range(B)])
+    refv = np.stack([oracle.encode(f64(xv)[b], f64(muv), f64(wv).T) for b in range(B)])
+    gk = f64(ck)
+    gv = f64(cv).transpose(0, 1, 3, 2).reshape(B, n_max, r_v)
+    assert_close(gk[:, pos0:pos0 + M], refk, torch.bfloat16, "2d keys", out_bf16=True)
+    assert_close(gv[:, pos0:pos0 + M], refv, torch.bfloat16, "2d values", out_bf16=True)
+    assert np.all(gk[:, :pos0] == 7.0) and np.all(gk[:, pos0 + M:] == 7.0)
+    assert np.all(gv[:, :pos0] == 7.0) and np.all(gv[:, pos0 + M:] == 7.0)
+
+
 @pytest.mark.parametrize("B,M,T,d", [(32, 1, 4, 128), (5, 3, 4, 128), (33, 1, 4, 128), (64, 1, 2, 64),
                                      (2, 1, 4, 256)])
 def test_encode_2d_split_write(B, M, T, d):
