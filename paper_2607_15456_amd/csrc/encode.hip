@@ -335,8 +335,7 @@ __global__ __launch_bounds__(256) void encode_few_kernel(EncodeArgs a, int nrc_k
 // compute-bound GEMM.  A workgroup of 8 wavefronts takes 256 tokens x 96 rows
 // of one axis; both operands are staged through double-buffered LDS in K-chunks
 // of 64 (two further chunks in flight in registers), and wavefront w computes
-// tokens 32w .. 32w + 31 x all 96 rows on v_mfma_f32_32x32x16_bf16 (one
-// launch per axis):
+// tokens 32w .. 32w + 31 x all 96 rows on v_mfma_f32_32x32x16_bf16:
 //   keys   (token-major cache): D = C^T (M = row, N = token), a lane holds
 //          4-row runs of one token;
 //   values (feature-major pages): D = C (M = token, N = row).
@@ -344,7 +343,6 @@ __global__ __launch_bounds__(256) void encode_few_kernel(EncodeArgs a, int nrc_k
 // (workgroup i runs on XCD i % 8), so its x chunks come from that XCD's L2
 // after the first read.  With a mean, wavefronts 0 .. 2 also form W_down^T mu
 // for one 32-row tile each (mu as a broadcast operand), shared through LDS.
-// grid: x = (row blocks) * (token blocks rounded up to 8), y = head
 constexpr int kGTok = 256, kGRow = 96, kGKC = 64, kGS = kGKC + 8;
 constexpr int kGThreads = 512;
 
@@ -353,18 +351,11 @@ __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
 }
 
 template <int AXIS>
-__global__ __launch_bounds__(kGThreads) __attribute__((amdgpu_waves_per_eu(2)))
-void encode_gemm_kernel(EncodeArgs a, int nrb, int ntb) {
-  __shared__ __attribute__((aligned(16))) bf16_t s_x[2][kGTok * kGS];
-  __shared__ __attribute__((aligned(16))) bf16_t s_w[2][kGRow * kGS];
-  __shared__ float s_mu[kGRow];
+__device__ __forceinline__ void encode_gemm_body(const EncodeArgs& a, int tb, int rb, bf16_t (*s_x)[kGTok * kGS],
+                                                 bf16_t (*s_w)[kGRow * kGS], float* s_mu) {
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int col = lane & 31, g = lane >> 5;
-  // XCD-aware order: the j-th workgroup of XCD x takes token block x + 8 (j / nrb), row block j % nrb
-  const int xcd = blockIdx.x % 8, j = blockIdx.x / 8;
-  const int tb = xcd + 8 * (j / nrb), rb = j % nrb;
-  if (tb >= ntb) return;  // padding of the grid to whole rounds of 8 token blocks
   constexpr int axis = AXIS;
   const int row0 = rb * kGRow;
   const int r = pick(a.r, axis), K = a.K, H = a.H, h = blockIdx.y;
@@ -488,6 +479,24 @@ void encode_gemm_kernel(EncodeArgs a, int nrb, int ntb) {
   }
 }
 
+// Both axes in one launch (1024 equal workgroups for the 2D prompt write of
+// 4 x 8192 tokens: four full rounds of the machine).  XCD-aware order: the
+// j-th workgroup of XCD x takes token block x + 8 (j / nrb) and row block
+// j % nrb (the row blocks of axis k, then those of axis v).
+__global__ __launch_bounds__(kGThreads) __attribute__((amdgpu_waves_per_eu(2)))
+void encode_gemm_kernel(EncodeArgs a, int nrb_k, int nrb, int ntb) {
+  __shared__ __attribute__((aligned(16))) bf16_t s_x[2][kGTok * kGS];
+  __shared__ __attribute__((aligned(16))) bf16_t s_w[2][kGRow * kGS];
+  __shared__ float s_mu[kGRow];
+  const int xcd = blockIdx.x % 8, j = blockIdx.x / 8;
+  const int tb = xcd + 8 * (j / nrb), rb = j % nrb;
+  if (tb >= ntb) return;  // padding of the grid to whole rounds of 8 token blocks
+  if (rb < nrb_k)
+    encode_gemm_body<0>(a, tb, rb, s_x, s_w, s_mu);
+  else
+    encode_gemm_body<1>(a, tb, rb - nrb_k, s_x, s_w, s_mu);
+}
+
 // Second launch of a split write: tile unit (grid x, y, z as the split launch
 // with z = head) adds its ksplit fp32 partials in split order and writes the
 // cache exactly as the unsplit path does.
@@ -600,9 +609,8 @@ hipError_t launch_encode(const EncodeArgs& a, hipStream_t stream) {
     if (TT >= kGTok && a.K >= 2048 && a.K % kGKC == 0) {
       // prefill-sized write over a long stack (the LLA-2D down-projection): a compute-bound GEMM
       const int ntb = (TT + kGTok - 1) / kGTok, ntb8 = (ntb + 7) / 8 * 8;
-      const int nrb_k = (a.r[0] + kGRow - 1) / kGRow, nrb_v = (a.r[1] + kGRow - 1) / kGRow;
-      hipLaunchKernelGGL(encode_gemm_kernel<0>, dim3(nrb_k * ntb8, a.H), dim3(kGThreads), 0, stream, a, nrb_k, ntb);
-      hipLaunchKernelGGL(encode_gemm_kernel<1>, dim3(nrb_v * ntb8, a.H), dim3(kGThreads), 0, stream, a, nrb_v, ntb);
+      const int nrb_k = (a.r[0] + kGRow - 1) / kGRow, nrb = nrb_k + (a.r[1] + kGRow - 1) / kGRow;
+      hipLaunchKernelGGL(encode_gemm_kernel, dim3(nrb * ntb8, a.H), dim3(kGThreads), 0, stream, a, nrb_k, nrb, ntb);
       return hipGetLastError();
     }
     const int heads_per_wg = blocks >= 256 ? a.H : 1;

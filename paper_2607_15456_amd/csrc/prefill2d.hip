@@ -303,39 +303,49 @@ void flash2d_kernel(Prefill2dArgs a) {
         for (int kt = 0; kt < 2; ++kt)
           sc[kt] = mfma_h(as_f16x8(*reinterpret_cast<const uint4*>(kt_row + 32 * kt * KST + 16 * s)), qop[s], sc[kt]);
       const int lim = qpos - key0 - 4 * g;
+      if (__builtin_expect(diag, 0)) {
+        // key 32kt + 8(r/4) + 4g + r%4 of the page is visible iff 32kt + 8(r/4) + r%4 <= lim
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-        f32x16& v = sc[kt];
-        if (__builtin_expect(diag, 0)) {
-          // key 32kt + 8(r/4) + 4g + r%4 of the page is visible iff 32kt + 8(r/4) + r%4 <= lim
+        for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
           for (int r = 0; r < 16; ++r)
-            if (32 * kt + 8 * (r / 4) + (r % 4) > lim) v[r] = neg_inf();
-        }
-        float m0 = fmaxf(fmaxf(v[0], v[1]), v[2]), m1 = fmaxf(fmaxf(v[8], v[9]), v[10]);
-        m0 = fmaxf(fmaxf(m0, v[3]), v[4]);
-        m1 = fmaxf(fmaxf(m1, v[11]), v[12]);
-        m0 = fmaxf(fmaxf(m0, v[5]), v[6]);
-        m1 = fmaxf(fmaxf(m1, v[13]), v[14]);
-        const float mx = half_swap_max(fmaxf(fmaxf(m0, v[7]), fmaxf(m1, v[15]))) * qs;
-        // raise the running max on the first half-page, then only when a
-        // score exceeds it by more than 2^kLazy (the weights stay below 2^kLazy)
-        const bool raise = mx > m_run + kLazy || (p == 0 && kt == 0);
-        if (__builtin_expect(__builtin_amdgcn_ballot_w64(raise) != 0, 0)) {
-          if (raise) {
-            const float alpha = m_run == neg_inf() ? 0.f : __builtin_amdgcn_exp2f(m_run - mx);
+            if (32 * kt + 8 * (r / 4) + (r % 4) > lim) sc[kt][r] = neg_inf();
+      }
+      // page maximum of the lane's query: four max3 chains, then the other lane half
+      float m0 = fmaxf(fmaxf(sc[0][0], sc[0][1]), sc[0][2]), m1 = fmaxf(fmaxf(sc[0][8], sc[0][9]), sc[0][10]);
+      float m2 = fmaxf(fmaxf(sc[1][0], sc[1][1]), sc[1][2]), m3 = fmaxf(fmaxf(sc[1][8], sc[1][9]), sc[1][10]);
 #pragma unroll
-            for (int t = 0; t < kD / 32; ++t) oacc[t] *= alpha;
-            l_lane *= alpha;
-            m_run = mx;
-          }
+      for (int r = 3; r < 7; r += 2) {
+        m0 = fmaxf(fmaxf(m0, sc[0][r]), sc[0][r + 1]);
+        m1 = fmaxf(fmaxf(m1, sc[0][8 + r]), sc[0][9 + r]);
+        m2 = fmaxf(fmaxf(m2, sc[1][r]), sc[1][r + 1]);
+        m3 = fmaxf(fmaxf(m3, sc[1][8 + r]), sc[1][9 + r]);
+      }
+      m0 = fmaxf(fmaxf(m0, sc[0][7]), fmaxf(m1, sc[0][15]));
+      m2 = fmaxf(fmaxf(m2, sc[1][7]), fmaxf(m3, sc[1][15]));
+      const float mx = half_swap_max(fmaxf(m0, m2)) * qs;
+      // raise the running max on the first page, then only when a score
+      // exceeds it by more than 2^kLazy (the weights stay below 2^kLazy)
+      const bool raise = mx > m_run + kLazy || p == 0;
+      if (__builtin_expect(__builtin_amdgcn_ballot_w64(raise) != 0, 0)) {
+        if (raise) {
+          const float alpha = m_run == neg_inf() ? 0.f : __builtin_amdgcn_exp2f(m_run - mx);
+#pragma unroll
+          for (int t = 0; t < kD / 32; ++t) oacc[t] *= alpha;
+          l_lane *= alpha;
+          m_run = mx;
         }
+      }
+      // one branch-free block: the second half's exponentials can issue
+      // between the first half's value products
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt) {
         f16x8 pop[2];
 #pragma unroll
         for (int u = 0; u < 2; ++u)
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
-            const float pv = __builtin_amdgcn_exp2f(fmaf(v[8 * u + e], qs, -m_run));  // exp2(-inf) = 0
+            const float pv = __builtin_amdgcn_exp2f(fmaf(sc[kt][8 * u + e], qs, -m_run));  // exp2(-inf) = 0
             l_lane += pv;
             pop[u][e] = (_Float16)pv;
           }
