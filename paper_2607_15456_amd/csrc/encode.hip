@@ -29,7 +29,10 @@ __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast
 // Per-axis fields selected without dynamic indexing (which would spill the
 // argument struct to scratch).
 template <typename T>
-__device__ __forceinline__ T pick(const T (&v)[2], int axis) { return axis ? v[1] : v[0]; }
+__device__ __forceinline__ T pick(const T (&v)[2], int axis) {
+  const T v0 = v[0], v1 = v[1];  // values, so the select is not between two addresses
+  return axis ? v1 : v0;
+}
 
 // Cache index of (b, h, slot pos, feature row): the paged feature-major layout,
 // or (tm, the LLA-2D key cache) token-major rows of r features.
@@ -81,7 +84,6 @@ __global__ __launch_bounds__(256) void encode_bf16_kernel(EncodeArgs a, int head
   const bf16_t* xg = static_cast<const bf16_t*>(pick(a.x, axis));
   const bf16_t* wg = static_cast<const bf16_t*>(pick(a.wdt, axis));
   const bf16_t* mug = static_cast<const bf16_t*>(pick(a.mu, axis));
-  const uint4 zero = make_uint4(0, 0, 0, 0);
 
   uint4 rgs[8];
   auto stage_load = [&](int st) {
@@ -92,7 +94,8 @@ __global__ __launch_bounds__(256) void encode_bf16_kernel(EncodeArgs a, int head
       const int c = tid + i * 256;
       if (c < kEncTok * cpt) {
         const int tok = c / cpt, part = c - tok * cpt, t = t0 + tok;
-        rgs[i] = t < TT ? ld16(xg + ((size_t)t * H + h) * K + k0 + part * 8) : zero;
+        // tokens past the last one re-read it: their output columns are never stored
+        rgs[i] = ld16(xg + ((size_t)min(t, TT - 1) * H + h) * K + k0 + part * 8);
       }
     }
   };
@@ -139,7 +142,7 @@ __global__ __launch_bounds__(256) void encode_bf16_kernel(EncodeArgs a, int head
           bf16x8 av[8];
 #pragma unroll
           for (int j = 0; j < 8; ++j)
-            av[j] = as_bf16x8(row_ok && s0 + j < ks ? ld16(wrow + 32 * (s0 + j)) : zero);
+            av[j] = as_bf16x8(row_ok && s0 + j < ks ? ld16(wrow + 32 * (s0 + j)) : make_uint4(0, 0, 0, 0));
 #pragma unroll
           for (int j = 0; j < 8; ++j) {
             if (s0 + j < ks) {
@@ -196,13 +199,12 @@ __global__ __launch_bounds__(256) void encode_stream_kernel(EncodeArgs a, int bl
   const int li = lane & 15, lg = lane >> 4;
   const int row = rt * 16 + li;
   const bool row_ok = row < r;
-  const uint4 zero = make_uint4(0, 0, 0, 0);
 
   // resident A fragments of W_down^T rows [16 rt, 16 rt + 16)
   const bf16_t* wrow = static_cast<const bf16_t*>(pick(a.wdt, axis)) + ((size_t)h * r + (row_ok ? row : 0)) * K + 8 * lg;
   bf16x8 wf[KS];
 #pragma unroll
-  for (int s = 0; s < KS; ++s) wf[s] = as_bf16x8(row_ok ? ld16(wrow + 32 * s) : zero);
+  for (int s = 0; s < KS; ++s) wf[s] = as_bf16x8(row_ok ? ld16(wrow + 32 * s) : make_uint4(0, 0, 0, 0));
   f32x4 bmu = f32x4{0.f};
   if (pick(a.mu, axis)) {
     const bf16_t* mrow = static_cast<const bf16_t*>(pick(a.mu, axis)) + (size_t)h * K + 8 * lg;
@@ -220,7 +222,8 @@ __global__ __launch_bounds__(256) void encode_stream_kernel(EncodeArgs a, int bl
       const int c = tid + i * 256;
       if (c < kEncTok * CPT) {
         const int tok = c / CPT, part = c - tok * CPT, t = blk * kEncTok + tok;
-        rgs[i] = t < TT ? ld16(xg + ((size_t)t * H + h) * K + part * 8) : zero;
+        // tokens past the last one re-read it: their output columns are never stored
+        rgs[i] = ld16(xg + ((size_t)min(t, TT - 1) * H + h) * K + part * 8);
       }
     }
   };

@@ -12,7 +12,7 @@
 // accumulator's registers feed the next product's B operand with no
 // cross-lane movement:
 //   D1 = Q~^T   (M = feature j, N = query, K = d)     A: U_k^T (LDS)      B: Q rows (global)
-//   D2 = S^T    (M = key n,     N = query, K = j)     A: K tile (LDS, token-major)  B: D1 (hi + lo)
+//   D2 = S^T    (M = key n,     N = query, K = j)     A: K tile (LDS, token-major)  B: D1 (fp16)
 //   D3 = Z^T   += (M = j,       N = query, K = key)   A: V tile (LDS, feature-major) B: P from D2
 //   D4 = O^T    (M = out i,     N = query, K = j)     A: U_v (LDS)        B: D3 / l
 // A 32x32 accumulator gives lane (q + 32g), register r the element
@@ -26,9 +26,13 @@
 // With the decoupled rotary branch (App. J), the rotary key rows follow the r_k
 // content rows in the score tile and the rotated query part follows Q~'s, so
 // the same products add q_r . k_r to every score.
-// Q~ enters the score product as two bf16 terms (hi + lo), so the scores carry
-// about 16 significant bits rather than bf16's 8: with peaked rows the score
-// magnitudes would otherwise turn Q~'s rounding into visible weight errors.
+// The score, value and output products run on v_mfma_f32_32x32x16_f16 (the
+// bf16 rate): Q~, the softmax weights and Z / l enter them in fp16, and the
+// key and value pages and U_v are converted from bf16 to fp16 (exact) as they
+// are staged, so these intermediates keep 11 significant bits rather than
+// bf16's 8, in one product per K-step (a two-term bf16 split of Q~ needs two).
+// Latents or U_v entries beyond fp16's range (65504) would make the output
+// non-finite.
 // The running max enters the score product through a padding feature (S - m
 // comes out of the MFMAs), and is only raised when a page exceeds it by more
 // than 2^8 (lazy rescale), so most pages cost
@@ -47,6 +51,7 @@ namespace lla {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int kPWaves = 4;
@@ -54,7 +59,7 @@ constexpr int kPThreads = kPWaves * kWave;
 constexpr int kQBlock = kPWaves * 32;  // queries per workgroup
 constexpr int kMaxDPrefill = 128;
 constexpr float kLazy = 8.0f;          // rescale only when the max grows by more than this (log2)
-constexpr bf16_t kOne = 0x3F80;        // 1.0 in bf16
+constexpr uint16_t kOneH = 0x3C00;     // 1.0 in fp16
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 
@@ -75,6 +80,10 @@ __device__ __forceinline__ uint16_t buf_ld2(BufRsrc r, int voff, int soff) {
 __device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
+__device__ __forceinline__ f32x16 mfma_h(f16x8 a, f16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ uint16_t f16_bits(float x) { return __builtin_bit_cast(uint16_t, (_Float16)x); }
 
 // A/B operand for K-step ordering 16t + 8(e/4) + 4g + e%4 read from an LDS row:
 // elements [base + 4g .. +3] and [base + 8 + 4g .. +3].
@@ -92,15 +101,12 @@ __device__ __forceinline__ bf16x8 to_operand(const f32x16& acc, int h, float sca
   return o;
 }
 
-// The same as a two-term bf16 split x = hi + lo (about 16 significant bits).
-__device__ __forceinline__ void to_operand_split(const f32x16& acc, int h, float scale, bf16x8& hi,
-                                                 bf16x8& lo) {
+// The same in fp16 (11 significant bits).
+__device__ __forceinline__ f16x8 to_operand_h(const f32x16& acc, int h, float scale) {
+  f16x8 o;
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const float x = acc[8 * h + e] * scale;
-    hi[e] = (__bf16)x;
-    lo[e] = (__bf16)(x - (float)hi[e]);
-  }
+  for (int e = 0; e < 8; ++e) o[e] = (_Float16)(acc[8 * h + e] * scale);
+  return o;
 }
 
 // Waves per SIMD the register budget is sized for: the smallest tiles fit
@@ -132,9 +138,9 @@ void prefill_bf16_kernel(PrefillArgs a) {
   constexpr int KTILE = kPage * CKS, VTILE = RVP * CVS;
 
   __shared__ __attribute__((aligned(16))) bf16_t s_ukt[RKP * UKS];
-  __shared__ __attribute__((aligned(16))) bf16_t s_uv[kMaxDPrefill * UVS];
-  __shared__ __attribute__((aligned(16))) bf16_t s_ck[2 * KTILE];
-  __shared__ __attribute__((aligned(16))) bf16_t s_cv[2 * VTILE];
+  __shared__ __attribute__((aligned(16))) uint16_t s_uv[kMaxDPrefill * UVS];  // fp16
+  __shared__ __attribute__((aligned(16))) uint16_t s_ck[2 * KTILE];  // fp16 key tiles
+  __shared__ __attribute__((aligned(16))) uint16_t s_cv[2 * VTILE];  // fp16 value tiles
 
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
@@ -196,7 +202,7 @@ void prefill_bf16_kernel(PrefillArgs a) {
       }
 #pragma unroll
       for (int k = 0; k < KR; ++k)
-        if (8 * k < d) s_uv[(ti + 8 * k) * UVS + j] = w[k];
+        if (8 * k < d) s_uv[(ti + 8 * k) * UVS + j] = f16_bits(bf16_to_f32(w[k]));  // exact
     }
   }
   // page-tile padding of both buffers: K columns r_k..RKP-1 of every token row
@@ -207,7 +213,7 @@ void prefill_bf16_kernel(PrefillArgs a) {
     for (int m = 0; m < 8; ++m) {
       const int j = j0 + 4 * m;
       if (j < RKP) {
-        const bf16_t v = (j == RKP - 1) ? kOne : bf16_t(0);
+        const uint16_t v = (j == RKP - 1) ? kOneH : uint16_t(0);
         s_ck[n * CKS + j] = v;
         s_ck[KTILE + n * CKS + j] = v;
       }
@@ -215,7 +221,7 @@ void prefill_bf16_kernel(PrefillArgs a) {
   }
   for (int e = tid; e < 2 * 32 * 8; e += kPThreads) {
     const int buf = e >> 8, j = rv + ((e >> 3) & 31), n8 = e & 7;
-    const uint32_t f = (j == rv) ? 0x3F803F80u : 0u;  // two bf16 ones, or zeros
+    const uint32_t f = (j == rv) ? 0x3C003C00u : 0u;  // two fp16 ones, or zeros
     if (j < RVP) *reinterpret_cast<uint4*>(&s_cv[buf * VTILE + j * CVS + 8 * n8]) = make_uint4(f, f, f, f);
   }
 
@@ -275,15 +281,17 @@ void prefill_bf16_kernel(PrefillArgs a) {
       stv[set][c] = buf_ld16(vsrc, ch < nvch ? ch * 16 : 0, __builtin_amdgcn_readfirstlane(pg * vpage_b));
     }
   };
-  auto store_page = [&](int pg, int set, bf16_t* tk, bf16_t* tv) {
+  auto store_page = [&](int pg, int set, uint16_t* tk, uint16_t* tv) {
 #pragma unroll
     for (int c = 0; c < CHK; ++c) {
       const int ch = tid + c * kPThreads;
       if (ch < nkch) {
-        const bf16_t* v = reinterpret_cast<const bf16_t*>(&stk[set][c]);
-        bf16_t* dst = tk + kdst[c];
+        // keys: bf16 -> fp16 (exact within fp16's range), transposed to token-major
+        float v[8];
+        Elem<bf16_t>::unpack(stk[set][c], v);
+        uint16_t* dst = tk + kdst[c];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) dst[e * CKS] = v[e];
+        for (int e = 0; e < 8; ++e) dst[e * CKS] = f16_bits(v[e]);
       }
     }
     const bool last = (pg + 1) * kPage > kmax;  // tokens past the last key are zeroed
@@ -303,9 +311,15 @@ void prefill_bf16_kernel(PrefillArgs a) {
           w.z &= keep(2);
           w.w &= keep(3);
         }
-        bf16_t* dst = tv + vdst[c];
-        *reinterpret_cast<uint2*>(dst) = make_uint2(w.x, w.y);
-        *reinterpret_cast<uint2*>(dst + 4) = make_uint2(w.z, w.w);
+        // bf16 -> fp16 (exact within fp16's range); masked tokens stay 0
+        float x[8];
+        Elem<bf16_t>::unpack(w, x);
+        uint32_t hw[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) hw[i] = uint32_t(f16_bits(x[2 * i])) | (uint32_t(f16_bits(x[2 * i + 1])) << 16);
+        uint16_t* dst = tv + vdst[c];
+        *reinterpret_cast<uint2*>(dst) = make_uint2(hw[0], hw[1]);
+        *reinterpret_cast<uint2*>(dst + 4) = make_uint2(hw[2], hw[3]);
       }
     }
   };
@@ -316,7 +330,7 @@ void prefill_bf16_kernel(PrefillArgs a) {
   store_page(0, 0, s_ck, s_cv);
 
   // ---- D1 = Q~^T for this wave's 32 queries ----
-  bf16x8 qop[KS], qlo[KS];  // Q~ as hi + lo bf16 terms: scores keep ~fp32 accuracy
+  f16x8 qop[KS];  // Q~ in fp16
   {
     f32x16 d1[QT];
 #pragma unroll
@@ -347,15 +361,15 @@ void prefill_bf16_kernel(PrefillArgs a) {
         }
     }
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) to_operand_split(d1[ks / 2], ks % 2, a.qscale, qop[ks], qlo[ks]);
+    for (int ks = 0; ks < KS; ++ks) qop[ks] = to_operand_h(d1[ks / 2], ks % 2, a.qscale);
   }
   __syncthreads();  // page 0 staged
 
   // ---- online softmax over the key pages ----
   // The running max rides in the score product itself: K feature RKP - 1 is 1
   // for every key and the same feature of Q~ (K-step KS - 1, element 7 of the
-  // upper lane half) holds negm = -m as hi + lo bf16, so the MFMAs yield
-  // S - m directly.  negm is the exact value the product uses (hi + lo).
+  // upper lane half) holds negm = -m in fp16, so the MFMAs yield S - m
+  // directly.  negm is the exact value the product uses.
   f32x16 zacc[ZT];
 #pragma unroll
   for (int t = 0; t < ZT; ++t) zacc[t] = f32x16{0.f};
@@ -370,33 +384,34 @@ void prefill_bf16_kernel(PrefillArgs a) {
     const int key0 = p * kPage;
     if (wave_live && key0 <= p0 + qlast_w) {
       const bool diag = key0 + kPage - 1 > p0 + qw0;
-      const bf16_t* ktile = s_ck + buf * KTILE + col * CKS;
-      const bf16_t* vtile = s_cv + buf * VTILE + col * CVS;
+      const uint16_t* ktile = s_ck + buf * KTILE + col * CKS;
+      const bf16_t* vtile = reinterpret_cast<const bf16_t*>(s_cv) + buf * VTILE + col * CVS;  // fp16 bits
       // Both 32-key halves are scored up front (the second half's MFMAs run
       // while the first half's softmax is on the VALU); each half is then
       // its own online-softmax step.
       // All K operands of the page are read from LDS before the first score
       // MFMA, the V operands right after the last one: their latency is
       // covered by the MFMAs instead of stalling each product.
-      bf16x8 ak[2][KS];
+      f16x8 ak[2][KS];
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) ak[kt][ks] = lds_pair(ktile + 32 * kt * CKS, 16 * ks, g);
+        for (int ks = 0; ks < KS; ++ks)
+          ak[kt][ks] = __builtin_bit_cast(f16x8, lds_pair(reinterpret_cast<const bf16_t*>(ktile) + 32 * kt * CKS,
+                                                          16 * ks, g));
       __builtin_amdgcn_sched_barrier(0);
       f32x16 sc[2] = {f32x16{0.f}, f32x16{0.f}};
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-          sc[kt] = mfma(ak[kt][ks], qop[ks], sc[kt]);
-          sc[kt] = mfma(ak[kt][ks], qlo[ks], sc[kt]);
+          sc[kt] = mfma_h(ak[kt][ks], qop[ks], sc[kt]);
         }
-      bf16x8 av[ZT][4];
+      f16x8 av[ZT][4];
 #pragma unroll
       for (int t = 0; t < ZT; ++t)
 #pragma unroll
-        for (int u = 0; u < 4; ++u) av[t][u] = lds_pair(vtile + 32 * t * CVS, 16 * u, g);
+        for (int u = 0; u < 4; ++u) av[t][u] = __builtin_bit_cast(f16x8, lds_pair(vtile + 32 * t * CVS, 16 * u, g));
       __builtin_amdgcn_sched_barrier(0);
       const int lim = qpos - key0 - 4 * g;
 #pragma unroll
@@ -421,11 +436,9 @@ void prefill_bf16_kernel(PrefillArgs a) {
         const bool first = (p == 0 && kt == 0);
         const bool raise = first || mx > kLazy;
         if (__builtin_expect(__builtin_amdgcn_ballot_w64(raise) != 0, 0)) {
-          // new fold value -(m + mx) as hi + lo; lanes that do not raise keep theirs
-          const float target = negm - mx;
-          const __bf16 hi = (__bf16)target;
-          const __bf16 lo = (__bf16)(target - (float)hi);
-          const float delta = raise ? ((float)hi + (float)lo) - negm : 0.f;
+          // new fold value -(m + mx) in fp16; lanes that do not raise keep theirs
+          const _Float16 t16 = (_Float16)(negm - mx);
+          const float delta = raise ? (float)t16 - negm : 0.f;
           if (!first) {
             const float alpha = __builtin_amdgcn_exp2f(delta);
 #pragma unroll
@@ -436,20 +449,19 @@ void prefill_bf16_kernel(PrefillArgs a) {
           for (int k2 = kt; k2 < 2; ++k2) sc[k2] += delta;
           negm += delta;
           const bool put = raise && g == 1;
-          qop[KS - 1][7] = put ? hi : qop[KS - 1][7];
-          qlo[KS - 1][7] = put ? lo : qlo[KS - 1][7];
+          qop[KS - 1][7] = put ? t16 : qop[KS - 1][7];
         }
         // P as the value product's B operands: K-step u = registers 8(u%2).. of this half
-        bf16x8 pop[2];
+        f16x8 pop[2];
 #pragma unroll
         for (int u = 0; u < 2; ++u)
 #pragma unroll
-          for (int e = 0; e < 8; ++e) pop[u][e] = (__bf16)__builtin_amdgcn_exp2f(v[8 * u + e]);
+          for (int e = 0; e < 8; ++e) pop[u][e] = (_Float16)__builtin_amdgcn_exp2f(v[8 * u + e]);
 #pragma unroll
         for (int t = 0; t < ZT; ++t)
 #pragma unroll
           for (int u = 0; u < 2; ++u)
-            zacc[t] = mfma(av[t][2 * kt + u], pop[u], zacc[t]);
+            zacc[t] = mfma_h(av[t][2 * kt + u], pop[u], zacc[t]);
       }
     }
     if (p + 1 < npages) store_page(p + 1, buf ^ 1, s_ck + (buf ^ 1) * KTILE, s_cv + (buf ^ 1) * VTILE);
@@ -474,16 +486,16 @@ void prefill_bf16_kernel(PrefillArgs a) {
     lsum += xor_shfl(lsum, 32);
   }
   const float inv_l = 1.0f / lsum;
-  bf16x8 zop[ZK];
+  f16x8 zop[ZK];
 #pragma unroll
-  for (int ks = 0; ks < ZK; ++ks) zop[ks] = to_operand(zacc[ks / 2], ks % 2, inv_l);
+  for (int ks = 0; ks < ZK; ++ks) zop[ks] = to_operand_h(zacc[ks / 2], ks % 2, inv_l);
   const bf16_t* muv = a.muv ? static_cast<const bf16_t*>(a.muv) + (size_t)h * d : nullptr;
   const size_t orow = (unit * M + myq) * (size_t)d;
   for (int it = 0; it < d / 32; ++it) {
     f32x16 o = f32x16{0.f};
-    const bf16_t* urow = &s_uv[(32 * it + col) * UVS];
+    const bf16_t* urow = reinterpret_cast<const bf16_t*>(&s_uv[(32 * it + col) * UVS]);  // fp16 bits
 #pragma unroll
-    for (int ks = 0; ks < ZK; ++ks) o = mfma(lds_pair(urow, 16 * ks, g), zop[ks], o);
+    for (int ks = 0; ks < ZK; ++ks) o = mfma_h(__builtin_bit_cast(f16x8, lds_pair(urow, 16 * ks, g)), zop[ks], o);
     if (q_ok) {
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
