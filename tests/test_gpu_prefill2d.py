@@ -98,6 +98,32 @@ def test_prefill_2d_full_cache_and_shared_workspace():
     assert_close(got, ref, torch.bfloat16, "second call")
 
 
+@pytest.mark.parametrize("B,H,M,p0,n_max", [(1, 1, 100, 27, 128), (1, 2, 1, 255, 256), (3, 1, 64, 0, 64),
+                                              (1, 5, 129, 0, 192)])
+def test_prefill_2d_edges(B, H, M, p0, n_max):
+    """One head or one sequence, a prompt that ends mid-page or at the cache's
+    last slot, a one-token prompt at the end of a long cached prefix, exactly
+    one page, one query past a 128-query block."""
+    log(f"prefill 2d edges B={B} H={H} M={M} p0={p0} n_max={n_max}")
+    got, h = _run(B, H, M, p0, 288, 480, seed=5, n_max=n_max)
+    ref = oracle.prefill_attn_2d_batched(h["q"], h["ck"], h["cv"], h["uk"], h["uv"], p0=p0)
+    assert_close(got, ref, torch.bfloat16, f"edges B={B} H={H} M={M} p0={p0}")
+
+
+def test_prefill_2d_rejects_small_workspace():
+    B, H, M = 1, 2, 70
+    wl = _wl(H)
+    ck = W.latents_2d(wl, 96, "k", 6, B=B, N=M, device=DEV)
+    cv = W.latents_2d(wl, 160, "v", 6, B=B, N=M, device=DEV)
+    kc, vc = _caches(ck, cv, 128)
+    q = W.queries(wl, 6, 1, B=B, M=M, device=DEV)
+    uk, uv = W.codec_loop_2d(wl, 96, 160, 6, 1, DEV)
+    need = lla.prefill_2d_workspace_bytes(B, H, 128, M)
+    ws = torch.empty(need - 16, dtype=torch.uint8, device=DEV)
+    with pytest.raises(lla.LLAError):
+        lla.prefill_attn_2d(q, kc, vc, uk, uv, p0=0, workspace=ws)
+
+
 @pytest.mark.slow
 def test_prefill_2d_full_size_sampled_rows():
     """The benchmark's shape (4 sequences x 8192 new tokens, 16 heads, (288, 480)):
