@@ -434,7 +434,8 @@ lla_status lla_prefill_2d_workspace_bytes(int B, int H, int d_head, int n_keys, 
  *        d_head, p0 + M), 16-byte aligned; overwritten, no initial contents
  *        needed; calls sharing it must be ordered on the stream
  * Supported: bf16, d_head = 128, r_k and r_v multiples of 16 up to 512, any H
- * (else LLA_ERR_UNSUPPORTED).
+ * (else LLA_ERR_UNSUPPORTED).  B*H*M <= 2^30 and B <= 65535 (else
+ * LLA_ERR_INVALID_ARG).
  * Errors: LLA_ERR_INVALID_ARG, LLA_ERR_UNSUPPORTED, LLA_ERR_WORKSPACE, LLA_ERR_HIP.
  */
 lla_status lla_prefill_attn_2d(int dtype, int out_dtype, int B, int H, int M, int d_head, int r_k,

@@ -375,7 +375,7 @@ def _prefill_2d(**kw):
 @pytest.mark.parametrize("kw,code", [
     (dict(dtype=2), 1), (dict(B=0), 1), (dict(M=0), 1), (dict(d=48), 1), (dict(rk=0), 1),
     (dict(n_max=100), 1), (dict(p0=-1), 1), (dict(p0=413), 1), (dict(scale=float("nan")), 1),
-    (dict(q=None), 1), (dict(cv=MIS), 1), (dict(muv=MIS), 1),
+    (dict(q=None), 1), (dict(cv=MIS), 1), (dict(muv=MIS), 1), (dict(B=65536, H=1, M=1), 1),
     (dict(dtype=0), 2), (dict(d=64), 2), (dict(rk=40), 2), (dict(rv=520), 2),
     (dict(ws=None), 3), (dict(ws_bytes=4 * 2 * 16 * 128 * 128 - 1), 3), (dict(ws=MIS), 3),
 ])
