@@ -49,7 +49,8 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 constexpr int kD = 128;            // d_head of both kernels
 constexpr int kThreads = 256;      // 4 wavefronts
 constexpr int kRTok = 128;         // tokens per rebuild workgroup (two pages)
-constexpr int kQBlock = 128;       // queries per attention workgroup (32 per wavefront)
+constexpr int kQBlock = 256;       // queries per attention workgroup (32 per wavefront)
+constexpr int kFThreads = 512;     // attention workgroup: 8 wavefronts
 constexpr float kLazy = 8.0f;      // raise the running max only when it grows by more than this (log2)
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
@@ -197,9 +198,9 @@ __global__ __launch_bounds__(kThreads) void recon2d_kernel(Prefill2dArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Attention.  One workgroup = 4 wavefronts x 32 queries of one (b, h); keys in
-// 64-token pages staged in LDS (K token-major, V feature-major), two pages in
-// flight in registers.  Products (v_mfma_f32_32x32x16_f16), transposed so each
+// Attention.  One workgroup = 8 wavefronts x 32 queries of one (b, h); keys in
+// 64-token pages staged in LDS (K token-major, V feature-major) once for the 8
+// wavefronts, two pages in flight in registers.  Products (v_mfma_f32_32x32x16_f16), transposed so each
 // accumulator feeds the next product with no lane exchange:
 //   S^T  (M = key, N = query, K = feature): A = K tile rows,  B = the query (registers)
 //   O^T += (M = feature, N = query, K = key): A = V^T tile rows, B = P from S^T
@@ -212,13 +213,13 @@ struct IntC {
   static constexpr int value = N;
 };
 
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ __launch_bounds__(kFThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void flash2d_kernel(Prefill2dArgs a) {
   constexpr int KS = kD / 16;       // K-steps of the score product
   constexpr int KST = kD + 8;       // K tile row stride (fp16 elements)
   constexpr int VST = kPage + 8;    // V^T tile row stride (fp16 elements)
   constexpr int KTILE = kPage * KST, VTILE = kD * VST;
-  constexpr int CH = kPage * kD / 8 / kThreads;  // 16-byte chunks per thread per page and axis (4)
+  constexpr int CH = kPage * kD / 8 / kFThreads;  // 16-byte chunks per thread per page and axis (2)
   __shared__ __attribute__((aligned(16))) uint16_t s_k[2 * KTILE];  // fp16
   __shared__ __attribute__((aligned(16))) uint16_t s_v[2 * VTILE];
 
@@ -245,14 +246,14 @@ void flash2d_kernel(Prefill2dArgs a) {
     const uint16_t* vp = vbase + (size_t)pg * kPage * kD;
 #pragma unroll
     for (int c = 0; c < CH; ++c) {
-      stk[set][c] = ld16(kp + 8 * (tid + c * kThreads));
-      stv[set][c] = ld16(vp + 8 * (tid + c * kThreads));
+      stk[set][c] = ld16(kp + 8 * (tid + c * kFThreads));
+      stv[set][c] = ld16(vp + 8 * (tid + c * kFThreads));
     }
   };
   auto store_page = [&](int set, int buf) {
 #pragma unroll
     for (int c = 0; c < CH; ++c) {
-      const int ch = tid + c * kThreads;
+      const int ch = tid + c * kFThreads;
       *reinterpret_cast<uint4*>(&s_k[buf * KTILE + (ch >> 4) * KST + 8 * (ch & 15)]) = stk[set][c];
       *reinterpret_cast<uint4*>(&s_v[buf * VTILE + (ch >> 3) * VST + 8 * (ch & 7)]) = stv[set][c];
     }
@@ -423,7 +424,7 @@ hipError_t launch_prefill_2d(const Prefill2dArgs& a, hipStream_t stream) {
   e = launch_recon_r<1>(a, a.rv, stream);
   if (e != hipSuccess) return e;
   const dim3 grid(a.B * a.H, (a.M + kQBlock - 1) / kQBlock);
-  hipLaunchKernelGGL(flash2d_kernel, grid, dim3(kThreads), 0, stream, a);
+  hipLaunchKernelGGL(flash2d_kernel, grid, dim3(kFThreads), 0, stream, a);
   return hipGetLastError();
 }
 
