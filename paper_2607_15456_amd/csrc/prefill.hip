@@ -7,7 +7,7 @@
 // reconstructed cache (App. A); this kernel is that attention read straight
 // from the latents.
 //
-// One workgroup = 4 wavefronts x 32 queries of one (b, h).  Every product is
+// One workgroup = 8 wavefronts x 32 queries of one (b, h).  Every product is
 // a v_mfma_f32_32x32x16_bf16 and is computed transposed so that each
 // accumulator's registers feed the next product's B operand with no
 // cross-lane movement:
@@ -54,7 +54,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int kPWaves = 4;
+constexpr int kPWaves = 8;
 constexpr int kPThreads = kPWaves * kWave;
 constexpr int kQBlock = kPWaves * 32;  // queries per workgroup
 constexpr int kMaxDPrefill = 128;
@@ -165,15 +165,16 @@ void prefill_bf16_kernel(PrefillArgs a) {
   // K features r_k .. RKP - 2 are 0.  V row r_v is all ones (the denominator),
   // V rows past it are 0.
   // Thread (tj, ti) = (tid % 32, tid / 32) fills feature columns j = tj + 32 jj
-  // and rows i = ti + 8k of U_k^T (transposed) and U_v; features past r are
+  // and rows i = ti + TI k (TI = threads / 32) of U_k^T (transposed) and U_v; features past r are
   // zero.  The LDS offsets are compile-time apart, the global reads are buffer
   // loads with the row offset in a scalar register, and all of a column's
   // loads are issued before its stores.
   {
     const int tj = tid & 31, ti = tid >> 5;
+    constexpr int TI = kPThreads / 32;  // row stride (d_head is a multiple of 32, so of TI)
     const BufRsrc uks = make_rsrc(static_cast<const bf16_t*>(a.uk) + (size_t)h * d * rk, (size_t)d * rk * 2);
     const BufRsrc uvs = make_rsrc(static_cast<const bf16_t*>(a.uv) + (size_t)h * d * rv, (size_t)d * rv * 2);
-    constexpr int KR = kMaxDPrefill / 8;  // rows per thread
+    constexpr int KR = kMaxDPrefill / TI;  // rows per thread
 #pragma unroll
     for (int jj = 0; jj < RKP / 32; ++jj) {
       const int j = tj + 32 * jj;
@@ -183,11 +184,11 @@ void prefill_bf16_kernel(PrefillArgs a) {
       if (j < rk) {
 #pragma unroll
         for (int k = 0; k < KR; ++k)
-          if (8 * k < d) w[k] = buf_ld2(uks, (ti * rk + j) * 2, __builtin_amdgcn_readfirstlane(8 * k * rk * 2));
+          if (TI * k < d) w[k] = buf_ld2(uks, (ti * rk + j) * 2, __builtin_amdgcn_readfirstlane(TI * k * rk * 2));
       }
 #pragma unroll
       for (int k = 0; k < KR; ++k)
-        if (8 * k < d) s_ukt[j * UKS + ti + 8 * k] = w[k];
+        if (TI * k < d) s_ukt[j * UKS + ti + TI * k] = w[k];
     }
 #pragma unroll
     for (int jj = 0; jj < RVP / 32; ++jj) {
@@ -198,25 +199,21 @@ void prefill_bf16_kernel(PrefillArgs a) {
       if (j < rv) {
 #pragma unroll
         for (int k = 0; k < KR; ++k)
-          if (8 * k < d) w[k] = buf_ld2(uvs, (ti * rv + j) * 2, __builtin_amdgcn_readfirstlane(8 * k * rv * 2));
+          if (TI * k < d) w[k] = buf_ld2(uvs, (ti * rv + j) * 2, __builtin_amdgcn_readfirstlane(TI * k * rv * 2));
       }
 #pragma unroll
       for (int k = 0; k < KR; ++k)
-        if (8 * k < d) s_uv[(ti + 8 * k) * UVS + j] = f16_bits(bf16_to_f32(w[k]));  // exact
+        if (TI * k < d) s_uv[(ti + TI * k) * UVS + j] = f16_bits(bf16_to_f32(w[k]));  // exact
     }
   }
   // page-tile padding of both buffers: K columns r_k..RKP-1 of every token row
   // (at most 32 of them, RKP - 32 <= r_k), V rows r_v..RVP-1 (16-byte stores)
   {
-    const int n = tid & (kPage - 1), j0 = rke + (tid >> 6);
-#pragma unroll
-    for (int m = 0; m < 8; ++m) {
-      const int j = j0 + 4 * m;
-      if (j < RKP) {
-        const uint16_t v = (j == RKP - 1) ? kOneH : uint16_t(0);
-        s_ck[n * CKS + j] = v;
-        s_ck[KTILE + n * CKS + j] = v;
-      }
+    const int n = tid & (kPage - 1);
+    for (int j = rke + (tid >> 6); j < RKP; j += kPThreads / kPage) {
+      const uint16_t v = (j == RKP - 1) ? kOneH : uint16_t(0);
+      s_ck[n * CKS + j] = v;
+      s_ck[KTILE + n * CKS + j] = v;
     }
   }
   for (int e = tid; e < 2 * 32 * 8; e += kPThreads) {
