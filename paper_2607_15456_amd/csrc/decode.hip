@@ -543,6 +543,7 @@ hipError_t dispatch(const DecodeArgs& a, hipStream_t stream) {
   if (gv <= 32) return launch_t<TIn, 32>(a, stream);
   if (gv <= 40) return launch_t<TIn, 40>(a, stream);
   if (gv <= 48) return launch_t<TIn, 48>(a, stream);
+  if (gv <= 56) return launch_t<TIn, 56>(a, stream);
   if (gv <= 64) return launch_t<TIn, 64>(a, stream);
   if constexpr (RPL == 4) {
     if (gv <= 96) return launch_t<TIn, 96>(a, stream);
