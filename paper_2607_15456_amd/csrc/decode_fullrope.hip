@@ -54,8 +54,11 @@ __device__ __forceinline__ BufRsrc make_rsrc(const void* base, size_t bytes) {
   const int n = bytes >= 0xffffffffull ? -1 : (int)bytes;
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, n, 0x00020000);
 }
+// Latent pages are read exactly once per call: non-temporal cache policy
+// (aux bit 1, "nt"), so they do not displace reusable lines in L2 and the MALL.
+constexpr int kCpolNT = 2;
 __device__ __forceinline__ uint4 buf_ld16(BufRsrc r, int voff, int soff) {
-  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, kCpolNT));
 }
 __device__ __forceinline__ uint2 lds_tr16(const bf16_t* p) {
   return __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((LLA_LDS i16x4*)(p)));
