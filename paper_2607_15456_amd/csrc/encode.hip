@@ -44,6 +44,12 @@ __device__ __forceinline__ size_t cache_index(int b, int h, int H, int n_max, in
 }
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+// 16-byte load with the non-temporal cache policy: for data read exactly once
+__device__ __forceinline__ uint4 ld16_nt(const void* p) {
+  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int kEncTok = 32;           // tokens per workgroup block
@@ -222,8 +228,9 @@ __global__ __launch_bounds__(256) void encode_stream_kernel(EncodeArgs a, int bl
       const int c = tid + i * 256;
       if (c < kEncTok * CPT) {
         const int tok = c / CPT, part = c - tok * CPT, t = blk * kEncTok + tok;
-        // tokens past the last one re-read it: their output columns are never stored
-        rgs[i] = ld16(xg + ((size_t)min(t, TT - 1) * H + h) * K + part * 8);
+        // tokens past the last one re-read it: their output columns are never stored;
+        // x is read once (non-temporal: 210 -> 192 us on the 4 x 8192-token write)
+        rgs[i] = ld16_nt(xg + ((size_t)min(t, TT - 1) * H + h) * K + part * 8);
       }
     }
   };
