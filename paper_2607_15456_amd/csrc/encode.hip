@@ -44,12 +44,7 @@ __device__ __forceinline__ size_t cache_index(int b, int h, int H, int n_max, in
 }
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-// 16-byte load with the non-temporal cache policy: for data read exactly once
-__device__ __forceinline__ uint4 ld16_nt(const void* p) {
-  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
-  return make_uint4(v.x, v.y, v.z, v.w);
-}
+
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int kEncTok = 32;           // tokens per workgroup block
