@@ -41,9 +41,10 @@ COMMON = [
 ]
 
 
-# Per-source additions.  The prefill's scores are finite or -inf by
-# construction, so it is built without NaN semantics (max without quieting).
-EXTRA = {"prefill.hip": ["-fno-honor-nans"]}
+# Per-source additions.  The prefills' scores are finite or -inf by
+# construction (finite queries, finite latents up to the prompt's end, zeros
+# after it), so they are built without NaN semantics (max without quieting).
+EXTRA = {"prefill.hip": ["-fno-honor-nans"], "prefill2d.hip": ["-fno-honor-nans"]}
 
 
 def sources():

@@ -45,6 +45,7 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kD = 128;            // d_head of both kernels
 constexpr int kThreads = 256;      // 4 wavefronts
@@ -345,11 +346,16 @@ void flash2d_kernel(Prefill2dArgs a) {
 #pragma unroll
         for (int u = 0; u < 2; ++u)
 #pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const float pv = __builtin_amdgcn_exp2f(fmaf(sc[kt][8 * u + e], qs, -m_run));  // exp2(-inf) = 0
-            l_lane += pv;
-            pop[u][e] = (_Float16)pv;
-          }
+          for (int e = 0; e < 8; ++e)
+            pop[u][e] = (_Float16)__builtin_amdgcn_exp2f(fmaf(sc[kt][8 * u + e], qs, -m_run));  // exp2(-inf) = 0
+        // the normaliser sums the fp16 weights the value product uses, two per
+        // v_dot2_f32_f16 against (1, 1) with fp32 accumulation
+        const f16x2 ones = {(_Float16)1.0f, (_Float16)1.0f};
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+          for (int e = 0; e < 8; e += 2)
+            l_lane = __builtin_amdgcn_fdot2(f16x2{pop[u][e], pop[u][e + 1]}, ones, l_lane, false);
 #pragma unroll
         for (int t = 0; t < kD / 32; ++t)
 #pragma unroll
