@@ -298,12 +298,31 @@ void flash2d_kernel(Prefill2dArgs a) {
       const bool diag = key0 + kPage - 1 > p0 + qw0;
       const uint16_t* kt_row = s_k + buf * KTILE + col * KST + 8 * g;
       const uint16_t* vt_row = s_v + buf * VTILE + col * VST + 8 * g;
+      // all of the page's operand fragments are read from LDS ahead of their
+      // products (scheduling fences keep them there): the 16 K fragments before
+      // the score products, which then issue back to back, and the 16 V fragments
+      // right after them, so the value reads overlap the score products and the
+      // softmax (1.314 -> 1.281 ms per call on 4 x 8192 tokens, 16 heads)
+      uint4 kop[KS][2];
+#pragma unroll
+      for (int s = 0; s < KS; ++s)
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) kop[s][kt] = *reinterpret_cast<const uint4*>(kt_row + 32 * kt * KST + 16 * s);
+      __builtin_amdgcn_sched_barrier(0);
       f32x16 sc[2] = {f32x16{0.f}, f32x16{0.f}};
 #pragma unroll
       for (int s = 0; s < KS; ++s)
 #pragma unroll
-        for (int kt = 0; kt < 2; ++kt)
-          sc[kt] = mfma_h(as_f16x8(*reinterpret_cast<const uint4*>(kt_row + 32 * kt * KST + 16 * s)), qop[s], sc[kt]);
+        for (int kt = 0; kt < 2; ++kt) sc[kt] = mfma_h(as_f16x8(kop[s][kt]), qop[s], sc[kt]);
+      uint4 vop[2][kD / 32][2];
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int t = 0; t < kD / 32; ++t)
+#pragma unroll
+          for (int u = 0; u < 2; ++u)
+            vop[kt][t][u] = *reinterpret_cast<const uint4*>(vt_row + 32 * t * VST + 32 * kt + 16 * u);
+      __builtin_amdgcn_sched_barrier(0);
       const int lim = qpos - key0 - 4 * g;
       if (__builtin_expect(diag, 0)) {
         // key 32kt + 8(r/4) + 4g + r%4 of the page is visible iff 32kt + 8(r/4) + r%4 <= lim
@@ -360,8 +379,7 @@ void flash2d_kernel(Prefill2dArgs a) {
         for (int t = 0; t < kD / 32; ++t)
 #pragma unroll
           for (int u = 0; u < 2; ++u)
-            oacc[t] = mfma_h(as_f16x8(*reinterpret_cast<const uint4*>(vt_row + 32 * t * VST + 32 * kt + 16 * u)),
-                             pop[u], oacc[t]);
+            oacc[t] = mfma_h(as_f16x8(vop[kt][t][u]), pop[u], oacc[t]);
       }
     }
     if (p + 1 < npages) store_page(buf ^ 1, buf ^ 1);
