@@ -84,6 +84,14 @@ __device__ __forceinline__ f32x16 mfma_h(f16x8 a, f16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
 }
 __device__ __forceinline__ uint16_t f16_bits(float x) { return __builtin_bit_cast(uint16_t, (_Float16)x); }
+// Two floats to two fp16 (round to nearest even) in one v_cvt_pk_f16_f32; written
+// out because the compiler splits a packed conversion whose halves are stored
+// separately back into two single conversions.
+__device__ __forceinline__ uint32_t cvt_pk_f16(float lo, float hi) {
+  uint32_t r;
+  asm("v_cvt_pk_f16_f32 %0, %1, %2" : "=v"(r) : "v"(lo), "v"(hi));
+  return r;
+}
 
 // A/B operand for K-step ordering 16t + 8(e/4) + 4g + e%4 read from an LDS row:
 // elements [base + 4g .. +3] and [base + 8 + 4g .. +3].
@@ -286,9 +294,15 @@ void prefill_bf16_kernel(PrefillArgs a) {
         // keys: bf16 -> fp16 (exact within fp16's range), transposed to token-major
         float v[8];
         Elem<bf16_t>::unpack(stk[set][c], v);
+        // packed conversions (round to nearest even); the high halves are stored
+        // straight from the packed register
         uint16_t* dst = tk + kdst[c];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) dst[e * CKS] = f16_bits(v[e]);
+        for (int e = 0; e < 8; e += 2) {
+          const uint32_t w = cvt_pk_f16(v[e], v[e + 1]);
+          dst[e * CKS] = (uint16_t)w;
+          dst[(e + 1) * CKS] = (uint16_t)(w >> 16);
+        }
       }
     }
     const bool last = (pg + 1) * kPage > kmax;  // tokens past the last key are zeroed
@@ -311,12 +325,13 @@ void prefill_bf16_kernel(PrefillArgs a) {
         // bf16 -> fp16 (exact within fp16's range); masked tokens stay 0
         float x[8];
         Elem<bf16_t>::unpack(w, x);
-        uint32_t hw[4];
+        f16x8 hx;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) hw[i] = uint32_t(f16_bits(x[2 * i])) | (uint32_t(f16_bits(x[2 * i + 1])) << 16);
+        for (int e = 0; e < 8; ++e) hx[e] = (_Float16)x[e];
+        const uint4 hw = __builtin_bit_cast(uint4, hx);
         uint16_t* dst = tv + vdst[c];
-        *reinterpret_cast<uint2*>(dst) = make_uint2(hw[0], hw[1]);
-        *reinterpret_cast<uint2*>(dst + 4) = make_uint2(hw[2], hw[3]);
+        *reinterpret_cast<uint2*>(dst) = make_uint2(hw.x, hw.y);
+        *reinterpret_cast<uint2*>(dst + 4) = make_uint2(hw.z, hw.w);
       }
     }
   };
