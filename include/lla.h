@@ -422,9 +422,11 @@ lla_status lla_prefill_2d_workspace_bytes(int B, int H, int d_head, int n_keys, 
  * (l, h) slice of W_up) are rebuilt for positions 0 .. p0+M-1 into the
  * workspace, then query m of head h, at position p0 + m, attends the keys
  * n <= p0 + m:  out = softmax(scale * K_h q) V_h + mu_{v,l,h}.  The rebuilt
- * K and V, the query and the softmax weights enter the products in fp16
- * (accumulation in fp32): |q|, |K| and |V| entries must stay below 65504, else
- * the output is not finite.
+ * K and V, the query scaled by scale * log2(e) and the softmax weights enter
+ * the products in fp16 (accumulation in fp32), and the running row maximum of
+ * the base-2 logits scale * log2(e) * q.k is held in fp16: |q|, |K| and |V|
+ * entries and those logits must stay below 65504 in magnitude, else the output
+ * is not finite.
  *   q    [B][H][M][d_head]; out [B][H][M][d_head] of out_dtype
  *   c_k, c_v  the 2D caches (layouts above) of capacity n_max, holding latents
  *        at positions 0 .. p0+M-1 (p0 + M <= n_max); later slots are not read

@@ -263,7 +263,9 @@ void flash2d_kernel(Prefill2dArgs a) {
   load_page(0, 0);
   load_page(min(1, npages - 1), 1);
   // the query as the score product's B operand: lane (q, g), K-step s = features
-  // 16s + 8g .. + 7, converted from bf16 to fp16
+  // 16s + 8g .. + 7, scaled by scale * log2(e) and rounded to fp16, so the score
+  // product yields base-2 logits
+  const float qs = a.qscale;
   f16x8 qop[KS];
   {
     const bf16_t* qrow = static_cast<const bf16_t*>(a.q) + ((size_t)bh * M + (q_ok ? myq : 0)) * kD + 8 * g;
@@ -275,17 +277,21 @@ void flash2d_kernel(Prefill2dArgs a) {
       float x[8];
       Elem<bf16_t>::unpack(raw[s], x);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) qop[s][e] = (_Float16)x[e];
+      for (int e = 0; e < 8; ++e) qop[s][e] = (_Float16)(x[e] * qs);
     }
   }
+  // One more K-step carries the running max: A holds 1 in feature 0 for every
+  // key, B holds -m in feature 0 for the lane's query, so the score products
+  // yield s - m directly.  m is kept representable in fp16 (every raise rounds
+  // it), which makes the shift exact and the rescale exp2(m_old - m_new) exact.
+  const f16x8 a_one = {(_Float16)(g == 0 ? 1.f : 0.f), 0, 0, 0, 0, 0, 0, 0};
   store_page(0, 0);
   __syncthreads();
 
   f32x16 oacc[kD / 32];
 #pragma unroll
   for (int t = 0; t < kD / 32; ++t) oacc[t] = f32x16{0.f};
-  float m_run = neg_inf(), l_lane = 0.f;
-  const float qs = a.qscale;
+  float m_run = 0.f, l_lane = 0.f;  // the first page always raises m
   const int qpos = p0 + myq;
 
   auto page = [&](int p, auto bufc) {
@@ -309,7 +315,10 @@ void flash2d_kernel(Prefill2dArgs a) {
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt) kop[s][kt] = *reinterpret_cast<const uint4*>(kt_row + 32 * kt * KST + 16 * s);
       __builtin_amdgcn_sched_barrier(0);
-      f32x16 sc[2] = {f32x16{0.f}, f32x16{0.f}};
+      const f16x8 b_m = {(_Float16)(g == 0 ? -m_run : 0.f), 0, 0, 0, 0, 0, 0, 0};
+      f32x16 sc[2];
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt) sc[kt] = mfma_h(a_one, b_m, f32x16{0.f});
 #pragma unroll
       for (int s = 0; s < KS; ++s)
 #pragma unroll
@@ -344,17 +353,21 @@ void flash2d_kernel(Prefill2dArgs a) {
       }
       m0 = fmaxf(fmaxf(m0, sc[0][7]), fmaxf(m1, sc[0][15]));
       m2 = fmaxf(fmaxf(m2, sc[1][7]), fmaxf(m3, sc[1][15]));
-      const float mx = half_swap_max(fmaxf(m0, m2)) * qs;
+      const float mx = half_swap_max(fmaxf(m0, m2));  // page max of s - m
       // raise the running max on the first page, then only when a score
       // exceeds it by more than 2^kLazy (the weights stay below 2^kLazy)
-      const bool raise = mx > m_run + kLazy || p == 0;
+      const bool raise = mx > kLazy || p == 0;
       if (__builtin_expect(__builtin_amdgcn_ballot_w64(raise) != 0, 0)) {
         if (raise) {
-          const float alpha = m_run == neg_inf() ? 0.f : __builtin_amdgcn_exp2f(m_run - mx);
+          const float m_new = (float)(_Float16)(m_run + mx);
+          const float delta = m_new - m_run;  // exact: both are fp16 values
+          const float alpha = p == 0 ? 0.f : __builtin_amdgcn_exp2f(-delta);
 #pragma unroll
           for (int t = 0; t < kD / 32; ++t) oacc[t] *= alpha;
           l_lane *= alpha;
-          m_run = mx;
+#pragma unroll
+          for (int kt = 0; kt < 2; ++kt) sc[kt] -= delta;
+          m_run = m_new;
         }
       }
       // one branch-free block: the second half's exponentials can issue
@@ -366,7 +379,7 @@ void flash2d_kernel(Prefill2dArgs a) {
         for (int u = 0; u < 2; ++u)
 #pragma unroll
           for (int e = 0; e < 8; ++e)
-            pop[u][e] = (_Float16)__builtin_amdgcn_exp2f(fmaf(sc[kt][8 * u + e], qs, -m_run));  // exp2(-inf) = 0
+            pop[u][e] = (_Float16)__builtin_amdgcn_exp2f(sc[kt][8 * u + e]);  // exp2(-inf) = 0
         // the normaliser sums the fp16 weights the value product uses, two per
         // v_dot2_f32_f16 against (1, 1) with fp32 accumulation
         const f16x2 ones = {(_Float16)1.0f, (_Float16)1.0f};
