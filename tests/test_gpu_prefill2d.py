@@ -145,3 +145,13 @@ def test_prefill_2d_full_size_sampled_rows():
         for i, m in enumerate((0, 1, 63, 64, 127, 128, 1000, 4095, 8191)):
             ref = oracle.decode_attn_2d(hq[b, :, m], hk[b, :m + 1], hv[b, :m + 1], huk, huv)
             assert_close(got[b, :, i], ref, torch.bfloat16, f"b={b} row {m}")
+
+
+def test_prefill_2d_large_logits():
+    """scale 1.0: base-2 logits of tens, the running maximum (held in fp16)
+    raised on many pages and shifted inside the score product."""
+    B, H, M, p0 = 1, 2, 260, 30
+    log("prefill 2d large logits")
+    got, h = _run(B, H, M, p0, 96, 160, seed=7, scale=1.0)
+    ref = oracle.prefill_attn_2d_batched(h["q"], h["ck"], h["cv"], h["uk"], h["uv"], scale=1.0, p0=p0)
+    assert_close(got, ref, torch.bfloat16, "large logits")
