@@ -90,6 +90,11 @@ __device__ __forceinline__ float half_swap_sum(float x) {
 //   values: D = V (M = token, N = feature), so a lane holds the tokens
 //           16 b + 8 g .. + 7 of the permuted order of one feature (16-byte stores).
 // ---------------------------------------------------------------------------
+template <int N>
+struct IntC {
+  static constexpr int value = N;
+};
+
 template <int AXIS, int KS>  // AXIS 0: keys, 1: values; KS = r / 16
 __global__ __launch_bounds__(kThreads) void recon2d_kernel(Prefill2dArgs a) {
   constexpr int R = KS * 16;
@@ -148,24 +153,25 @@ __global__ __launch_bounds__(kThreads) void recon2d_kernel(Prefill2dArgs a) {
     for (int s = 0; s < KS; ++s) u[s] = ld16(row + 16 * s);
   };
   uint4 ua[KS];
-  auto head = [&](int h, const uint4 (&u)[KS]) {
-    f32x16 acc[kRTok / 32];
+  // NT = the workgroup's token tiles, a compile-time count so the product loop
+  // has no branches (a guard per product had split every MFMA into a block of
+  // its own, each waiting on its own LDS read)
+  auto head = [&](int h, const uint4 (&u)[KS], auto ntc) {
+    constexpr int NT = decltype(ntc)::value;
+    f32x16 acc[NT];
 #pragma unroll
-    for (int nt = 0; nt < kRTok / 32; ++nt) acc[nt] = f32x16{0.f};
+    for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x16{0.f};
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
 #pragma unroll
-      for (int nt = 0; nt < kRTok / 32; ++nt) {
-        if (nt < ntile) {
-          const bf16x8 c = as_bf16x8(*reinterpret_cast<const uint4*>(&s_c[(32 * nt + col) * CS + 16 * s + 8 * g]));
-          acc[nt] = AXIS == 0 ? mfma(as_bf16x8(u[s]), c, acc[nt]) : mfma(c, as_bf16x8(u[s]), acc[nt]);
-        }
+      for (int nt = 0; nt < NT; ++nt) {
+        const bf16x8 c = as_bf16x8(*reinterpret_cast<const uint4*>(&s_c[(32 * nt + col) * CS + 16 * s + 8 * g]));
+        acc[nt] = AXIS == 0 ? mfma(as_bf16x8(u[s]), c, acc[nt]) : mfma(c, as_bf16x8(u[s]), acc[nt]);
       }
     }
     const size_t bh = (size_t)b * H + h;
 #pragma unroll
-    for (int nt = 0; nt < kRTok / 32; ++nt) {
-      if (nt >= ntile) continue;
+    for (int nt = 0; nt < NT; ++nt) {
       if (AXIS == 0) {
         // lane (token col, half g), register r: feature 32 wave + 8 (r/4) + 4 g + r%4
         uint16_t* dst = static_cast<uint16_t*>(a.kh) + (bh * a.nk + n0 + 32 * nt + col) * kD + 32 * wave + 4 * g;
@@ -194,7 +200,13 @@ __global__ __launch_bounds__(kThreads) void recon2d_kernel(Prefill2dArgs a) {
   // products of the early K-steps overlap the later loads
   for (int h = 0; h < H; ++h) {
     load_u(h, ua);
-    head(h, ua);
+    switch (ntile) {  // uniform; 2 or 4 (the key count is a multiple of 64)
+      case 4: head(h, ua, IntC<4>{}); break;
+      case 3: head(h, ua, IntC<3>{}); break;
+      case 2: head(h, ua, IntC<2>{}); break;
+      case 1: head(h, ua, IntC<1>{}); break;
+      default: break;
+    }
   }
 }
 
@@ -209,11 +221,6 @@ __global__ __launch_bounds__(kThreads) void recon2d_kernel(Prefill2dArgs a) {
 // of column q: registers 8u .. 8u + 7 of a key tile are the keys
 // 16u + 8(e/4) + 4g + e%4, e < 8, which the permuted V^T rows hold contiguously.
 // ---------------------------------------------------------------------------
-template <int N>
-struct IntC {
-  static constexpr int value = N;
-};
-
 __global__ __launch_bounds__(kFThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void flash2d_kernel(Prefill2dArgs a) {
   constexpr int KS = kD / 16;       // K-steps of the score product
