@@ -60,6 +60,10 @@ __device__ __forceinline__ uint4 buf_ld16(BufRsrc r, int voff, int soff) {
 // grid (H, ceil(r_k / 128), ceil(B / 32)); wavefront w covers features
 // 128 blockIdx.y + 32 w.
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+template <int N>
+struct KSteps {
+  static constexpr int value = N;
+};
 constexpr int kAbsJ = 128, kAbsB = 32;
 __global__ __launch_bounds__(256) void absorb2d_kernel(Decode2dArgs a) {
   constexpr int US = kMaxHead + 8;  // transposed U_k row stride (bf16)
@@ -106,12 +110,25 @@ __global__ __launch_bounds__(256) void absorb2d_kernel(Decode2dArgs a) {
   if (32 * wave >= nj) return;
   f32x16 acc = f32x16{0.f};
   const bf16_t* ua = &s_ut[(32 * wave + c) * US + 8 * g];
+  // the K-step count as a compile-time parameter (d / 16, dispatched once), so
+  // the chain has no branch per product
+  auto chain = [&](auto ktc) {
+    constexpr int KT = decltype(ktc)::value;
 #pragma unroll
-  for (int t = 0; t < kMaxHead / 16; ++t) {
-    if (16 * t < d) {
+    for (int t = 0; t < KT; ++t) {
       const bf16x8 av = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(ua + 16 * t));
       acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, __builtin_bit_cast(bf16x8, xq[t]), acc, 0, 0, 0);
     }
+  };
+  switch (d / 32) {  // d_head: a multiple of 32 up to 256
+    case 1: chain(KSteps<2>{}); break;
+    case 2: chain(KSteps<4>{}); break;
+    case 3: chain(KSteps<6>{}); break;
+    case 4: chain(KSteps<8>{}); break;
+    case 5: chain(KSteps<10>{}); break;
+    case 6: chain(KSteps<12>{}); break;
+    case 7: chain(KSteps<14>{}); break;
+    default: chain(KSteps<16>{}); break;
   }
   if (!q_ok) return;
   const size_t plane = (size_t)kHeads2d * rk;

@@ -144,12 +144,34 @@ __global__ __launch_bounds__(256) void encode_bf16_kernel(EncodeArgs a, int head
 #pragma unroll
           for (int j = 0; j < 8; ++j)
             av[j] = as_bf16x8(row_ok && s0 + j < ks ? ld16(wrow + 32 * (s0 + j)) : make_uint4(0, 0, 0, 0));
+          if (s0 + 8 <= ks) {
+            // a whole group: no guard per product (a guard there makes each
+            // MFMA a block of its own, waiting on its own operand reads)
+            if (mrow) {
+              uint4 mv[8];
 #pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            if (s0 + j < ks) {
-              const bf16x8 bv = as_bf16x8(*reinterpret_cast<const uint4*>(xrow + 32 * (s0 + j)));
-              acc[u] = mfma16(av[j], bv, acc[u]);
-              if (mrow) accm[u] = mfma16(av[j], as_bf16x8(ld16(mrow + 32 * (s0 + j))), accm[u]);
+              for (int j = 0; j < 8; ++j) mv[j] = ld16(mrow + 32 * (s0 + j));
+#pragma unroll
+              for (int j = 0; j < 8; ++j) {
+                const bf16x8 bv = as_bf16x8(*reinterpret_cast<const uint4*>(xrow + 32 * (s0 + j)));
+                acc[u] = mfma16(av[j], bv, acc[u]);
+                accm[u] = mfma16(av[j], as_bf16x8(mv[j]), accm[u]);
+              }
+            } else {
+#pragma unroll
+              for (int j = 0; j < 8; ++j) {
+                const bf16x8 bv = as_bf16x8(*reinterpret_cast<const uint4*>(xrow + 32 * (s0 + j)));
+                acc[u] = mfma16(av[j], bv, acc[u]);
+              }
+            }
+          } else {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+              if (s0 + j < ks) {
+                const bf16x8 bv = as_bf16x8(*reinterpret_cast<const uint4*>(xrow + 32 * (s0 + j)));
+                acc[u] = mfma16(av[j], bv, acc[u]);
+                if (mrow) accm[u] = mfma16(av[j], as_bf16x8(ld16(mrow + 32 * (s0 + j))), accm[u]);
+              }
             }
           }
         }
@@ -416,10 +438,18 @@ __device__ __forceinline__ void encode_gemm_body(const EncodeArgs& a, int tb, in
         const bf16x8 wo = as_bf16x8(*reinterpret_cast<const uint4*>(ws + 32 * rt * kGS + 16 * s));
         acc[rt] = axis == 0 ? mfma32(wo, xo, acc[rt]) : mfma32(xo, wo, acc[rt]);
       }
-      if (mu && wave < 3) {
-        const bf16x8 wo = as_bf16x8(*reinterpret_cast<const uint4*>(ws + 32 * wave * kGS + 16 * s));
-        accm = mfma32(wo, as_bf16x8(ld16(mug + kc * kGKC + 16 * s)), accm);
+    }
+    // the mean's products in one block after the chunk's (a guard inside the
+    // K-step loop made each of them a block of its own)
+    if (mu && wave < 3) {
+      uint4 wm[kGKC / 16], mo[kGKC / 16];
+#pragma unroll
+      for (int s = 0; s < kGKC / 16; ++s) {
+        wm[s] = *reinterpret_cast<const uint4*>(ws + 32 * wave * kGS + 16 * s);
+        mo[s] = ld16(mug + kc * kGKC + 16 * s);
       }
+#pragma unroll
+      for (int s = 0; s < kGKC / 16; ++s) accm = mfma32(as_bf16x8(wm[s]), as_bf16x8(mo[s]), accm);
     }
   };
 
