@@ -59,7 +59,7 @@
 extern "C" {
 #endif
 
-#define LLA_ABI_VERSION 7
+#define LLA_ABI_VERSION 8
 #define LLA_PAGE_TOKENS 64
 #define LLA_MAX_RANK 512
 #define LLA_MAX_ROPE 256
@@ -138,6 +138,18 @@ lla_status lla_encode(int dtype, int B, int M, int H, int T, int d_head, int r_k
  * arguments.  Host only.  Errors: LLA_ERR_INVALID_ARG.
  */
 lla_status lla_decode_workspace_bytes(int B, int H, int r_v, int n_ctx, size_t* bytes);
+
+/*
+ * Number of workgroups lla_decode_attn and lla_decode_attn_rope split the
+ * context of every (b, h) over for these sizes on the current device, with a
+ * workspace (with_workspace != 0) or without one (then always 1).  Splitting
+ * is chosen only when the (b, h) units alone leave compute units without 8
+ * resident wavefronts (small batches, long contexts); the partial softmax
+ * states (m, l, z) of the splits are merged as in the split-K step of the
+ * decode (the softmax over a union of disjoint key ranges).  Host only.
+ * Errors: LLA_ERR_INVALID_ARG.
+ */
+lla_status lla_decode_splits(int dtype, int B, int H, int n_ctx, int with_workspace, int* splits);
 
 /*
  * Loop-l decode attention over the latent cache, absorbed form (App. J):

@@ -394,10 +394,11 @@ void decode_kernel(DecodeArgs a) {
             if (k < GV && (k < vg_full || (k == vg_full && hi < vg_part))) {
               float v[EPL];
               Elem<TIn>::unpack(vcur[u], v);
-              if (tail) {
+              if (tail) {  // slots past N: value 0 (an attended NaN still propagates)
+                const int nv0 = pv * kPage + lo * EPL;
 #pragma unroll
                 for (int e = 0; e < EPL; ++e)
-                  if (p8[e] == 0.f) v[e] = 0.f;
+                  if (nv0 + e >= N) v[e] = 0.f;
               }
               float t = 0.f;
 #pragma unroll

@@ -255,6 +255,13 @@ lla_status lla_decode_workspace_bytes(int B, int H, int r_v, int n_ctx, size_t* 
   return LLA_OK;
 }
 
+lla_status lla_decode_splits(int dtype, int B, int H, int n_ctx, int with_workspace, int* splits) {
+  if (!dtype_ok(dtype) || B < 1 || H < 1 || n_ctx < 1 || !splits || (int64_t)B * H > (1 << 24))
+    return LLA_ERR_INVALID_ARG;
+  *splits = choose_shape(B * H, n_ctx, with_workspace != 0, dtype == LLA_BF16).splits;
+  return LLA_OK;
+}
+
 namespace {
 lla_status decode_impl(int dtype, int out_dtype, int B, int H, int d_head, int r_k, int r_v,
                        int d_rope, int H_rope, int n_max, int n_ctx, const int32_t* ctx_len,

@@ -48,3 +48,25 @@ def assert_close(got, ref, in_dtype, what="", out_bf16=False):
         assert rel <= FP32_REL_L2, (what, rel)
     else:
         assert max_abs <= BF16_MAX_ABS and rel <= BF16_REL_L2, (what, max_abs, rel)
+
+
+def f64_dev(t: torch.Tensor) -> np.ndarray:
+    """Like f64, with the (exact) widening done on the device before the copy:
+    faster for the multi-GB tensors of the full-size workloads."""
+    return t.detach().to(torch.float64).to("cpu").numpy()
+
+
+def assert_units_close(got, ref, what=""):
+    """bf16 parity for every unit separately: got, ref are [units..., d] arrays;
+    each unit's last-axis vector must meet max-abs and relative L2 on its own."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert got.shape == ref.shape, (got.shape, ref.shape)
+    assert np.all(np.isfinite(got)), f"{what}: non-finite output"
+    g2, r2 = got.reshape(-1, got.shape[-1]), ref.reshape(-1, ref.shape[-1])
+    max_abs = np.max(np.abs(g2 - r2), axis=1)
+    rel = np.linalg.norm(g2 - r2, axis=1) / np.linalg.norm(r2, axis=1)
+    worst = int(np.argmax(rel))
+    log(f"  {what}: {g2.shape[0]} units, worst max_abs={max_abs.max():.3e} "
+        f"worst rel_l2={rel.max():.3e} (unit {np.unravel_index(worst, got.shape[:-1])})")
+    assert max_abs.max() <= BF16_MAX_ABS and rel.max() <= BF16_REL_L2, (what, max_abs.max(), rel.max())

@@ -29,7 +29,7 @@ def _declared():
 def test_header_declares_the_boundary():
     names = _declared()
     assert names == sorted(["lla_status_string", "lla_abi_version", "lla_rho", "lla_cache_bytes",
-                            "lla_encode", "lla_decode_workspace_bytes", "lla_decode_attn",
+                            "lla_encode", "lla_decode_workspace_bytes", "lla_decode_splits", "lla_decode_attn",
                             "lla_prefill_attn", "lla_rope_write", "lla_rope_rotate",
                             "lla_decode_attn_rope", "lla_prefill_attn_rope", "lla_encode_ring",
                             "lla_rope_write_ring", "lla_encode_2d", "lla_encode_2d_workspace_bytes",
@@ -42,7 +42,26 @@ def test_library_exports_every_declared_symbol():
     h = ctypes.CDLL(lla.LIB_PATH)
     for name in _declared():
         assert hasattr(h, name), name
-    assert lla.abi_version() == 7
+    assert lla.abi_version() == 8
+
+
+def test_decode_split_choice():
+    """The split-K choice (the library's launch heuristic on a 256-CU MI355X): a
+    batch that fills the machine with one workgroup per (b, h) is not split; one
+    sequence of 16 heads over a long context is, in proportion to its pages."""
+    import torch
+    bf, f32 = torch.bfloat16, torch.float32
+    assert lla.decode_splits(bf, 32, 16, 4096) == 1          # the Ouro-1.4B decode step
+    assert lla.decode_splits(bf, 16, 16, 32768) == 1         # the Ouro-2.6B long-context step
+    assert lla.decode_splits(bf, 64, 16, 8192) == 1          # the rank sweep
+    for dt in (bf, f32):
+        assert lla.decode_splits(dt, 1, 16, 8192) == 2
+        assert lla.decode_splits(dt, 1, 16, 32768) == 8
+        assert lla.decode_splits(dt, 2, 16, 32768) == 8
+        assert lla.decode_splits(dt, 1, 16, 32768, with_workspace=False) == 1
+        assert lla.decode_splits(dt, 1, 16, 512) == 1
+    with pytest.raises(lla.LLAError):
+        lla.decode_splits(bf, 0, 16, 4096)
 
 
 def test_status_strings():

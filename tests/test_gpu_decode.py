@@ -11,7 +11,7 @@ import torch
 
 import oracle
 from paper_2607_15456_amd import lla, workloads as W
-from tests.helpers import assert_close, f64, log
+from tests.helpers import assert_close, assert_units_close, f64, f64_dev, log
 
 pytestmark = pytest.mark.gpu
 
@@ -149,11 +149,63 @@ def test_mu_k_cancels():
 
 
 # ---------------------------------------------------------------------------
-# Full-size workloads, in the launch configuration the benchmark times
-# (default split heuristic with a workspace); sampled (b, h) units.
+# Split-K: shapes the library's launch heuristic really splits (one or two
+# sequences of 16 heads over a long context), in fp32 and bf16, with ragged
+# and out-of-range per-sequence lengths.  The chosen split count is asserted.
 # ---------------------------------------------------------------------------
 
-def _full_size(wl, r_k, r_v, layer, loop, units):
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("N,splits", [(8192, 2), (32768, 8)])
+def test_split_k_long_context(dtype, N, splits):
+    B, H = 2, 16
+    r_k, r_v = (96, 160) if dtype == torch.float32 else (36, 60)
+    wl = W.Workload("split_k", 1, H, 128, 4, B, N, ((r_k, r_v),), dtype)
+    assert lla.decode_splits(dtype, B, H, N) == splits
+    log(f"split-K {dtype} N={N} splits={splits}")
+    ck, cv, q, uk, uv, muk, muv, pk, pv = _case(wl, r_k, r_v, B, N, N, 0, 1, True, dtype)
+    ws = lla.new_workspace(B, H, r_v, N)
+    ck64, cv64 = f64_dev(ck), f64_dev(cv)
+    q64, uk64, uv64, muv64 = f64(q), f64(uk), f64(uv), f64(muv)
+
+    def ref(lens):
+        return np.stack([np.stack([oracle.decode_attn_absorbed(q64[b, h], ck64[b, h, :lens[b]], cv64[b, h, :lens[b]],
+                                                               uk64[h], uv64[h], None, muv64[h])
+                                   for h in range(H)]) for b in range(B)])
+
+    for lens in ([N, N], [N, N - 1000], [N - 63, 64 * 37 + 5], [1, N]):
+        ctx = torch.tensor(lens, dtype=torch.int32, device=DEV)
+        out = lla.decode_attn(q, pk, pv, uk, uv, n_ctx=N, ctx_len=ctx, mu_k=muk, mu_v=muv, workspace=ws)
+        torch.cuda.synchronize()
+        assert_close(f64(out), ref(lens), dtype, f"lens={lens}")
+    # out-of-range lengths: NaN for that sequence, the other still right, and
+    # the arrival counters left at zero for the next call
+    ctx = torch.tensor([0, N - 5], dtype=torch.int32, device=DEV)
+    out = lla.decode_attn(q, pk, pv, uk, uv, n_ctx=N, ctx_len=ctx, mu_k=muk, mu_v=muv, workspace=ws)
+    torch.cuda.synchronize()
+    o = f64(out)
+    assert np.all(np.isnan(o[0]))
+    assert_close(o[1:], ref([N, N - 5])[1:], dtype, "valid sequence")
+    ctx = torch.tensor([N, N + 1], dtype=torch.int32, device=DEV)
+    out = lla.decode_attn(q, pk, pv, uk, uv, n_ctx=N, ctx_len=ctx, mu_k=muk, mu_v=muv, workspace=ws)
+    torch.cuda.synchronize()
+    o = f64(out)
+    assert np.all(np.isnan(o[1]))
+    assert_close(o[:1], ref([N, N])[:1], dtype, "valid sequence")
+    counters = ws[:4 * B * H].view(torch.int32)
+    assert int(counters.abs().sum()) == 0
+    out = lla.decode_attn(q, pk, pv, uk, uv, n_ctx=N, mu_k=muk, mu_v=muv, workspace=ws)
+    torch.cuda.synchronize()
+    assert_close(f64(out), ref([N, N]), dtype, "after the NaN calls")
+
+
+# ---------------------------------------------------------------------------
+# Full-size workloads, in the launch configuration the benchmark times
+# (default split heuristic with a workspace).  Every (b, h) unit is checked
+# against the absorbed oracle (App. J; pinned against the plain definition
+# and brute force), and a sample against the plain definition itself.
+# ---------------------------------------------------------------------------
+
+def _full_size(wl, r_k, r_v, layer, loop, plain_units):
     n_max = wl.N + 64 if wl.name == "ouro14b_decode" else wl.N
     log(f"{wl.name} r=({r_k},{r_v}) layer={layer} loop={loop} B={wl.B} N={wl.N}")
     pk = lla.to_paged(W.latents(wl, r_k, "k", layer, device=DEV), n_max)
@@ -163,12 +215,18 @@ def _full_size(wl, r_k, r_v, layer, loop, units):
     ws = lla.new_workspace(wl.B, wl.H, r_v, wl.N)
     out = lla.decode_attn(q, pk, pv, uk, uv, n_ctx=wl.N, workspace=ws)
     torch.cuda.synchronize()
-    o = f64(out)
-    for b, h in units:
-        ck = f64(lla.from_paged(pk[b:b + 1, h:h + 1], wl.N))[0, 0]
-        cv = f64(lla.from_paged(pv[b:b + 1, h:h + 1], wl.N))[0, 0]
-        ref = oracle.decode_attn(f64(q[b, h]), ck, cv, f64(uk[h]), f64(uv[h]))
-        assert_close(o[b, h], ref, torch.bfloat16, f"unit ({b},{h})")
+    o, q64, uk64, uv64 = f64(out), f64(q), f64(uk), f64(uv)
+    ref = np.empty_like(o)
+    for b in range(wl.B):
+        ck = f64_dev(lla.from_paged(pk[b:b + 1], wl.N))[0]
+        cv = f64_dev(lla.from_paged(pv[b:b + 1], wl.N))[0]
+        for h in range(wl.H):
+            ref[b, h] = oracle.decode_attn_absorbed(q64[b, h], ck[h], cv[h], uk64[h], uv64[h])
+        for bb, h in plain_units:
+            if bb == b:
+                plain = oracle.decode_attn(q64[b, h], ck[h], cv[h], uk64[h], uv64[h])
+                assert_close(o[b, h], plain, torch.bfloat16, f"unit ({b},{h}) plain definition")
+    assert_units_close(o, ref, "every (b, h) unit, absorbed oracle")
     del pk, pv
     torch.cuda.empty_cache()
 

@@ -7,7 +7,7 @@ import torch
 
 import oracle
 from paper_2607_15456_amd import lla, workloads as W
-from tests.helpers import assert_close, f64, log
+from tests.helpers import assert_close, assert_units_close, f64, f64_dev, log
 
 pytestmark = pytest.mark.gpu
 
@@ -101,32 +101,47 @@ def test_prefill_rows_match_decode():
 @pytest.mark.slow
 def test_full_prefill_write():
     """Workload 5 at full size: encode 4 x 8192 tokens into the (18, 30) cache,
-    then causal prefill at every loop; sampled rows of sampled (b, h)."""
+    then causal prefill at every loop.  Every (b, h) unit is checked at the
+    first and last row of every 256-query block (and a few more rows) against
+    the absorbed oracle over the row's prefix (App. J; a prefill row is the
+    decode of the context that ends at its position), and three units at ten
+    rows against the plain definition."""
     wl = W.WORKLOADS["prefill_write"]
     r_k, r_v = wl.ranks[0]
-    B, M = wl.B, wl.N
+    B, M, H = wl.B, wl.N, wl.H
     log("prefill_write full size: encode")
     xk = W.stacked_kv(wl, "k", 0, device=DEV)
     xv = W.stacked_kv(wl, "v", 0, device=DEV)
     wk = W.down_projection(wl, r_k, "k", 0, DEV)
     wv = W.down_projection(wl, r_v, "v", 0, DEV)
-    ck = lla.alloc_cache(B, wl.H, M, r_k)
-    cv = lla.alloc_cache(B, wl.H, M, r_v)
+    ck = lla.alloc_cache(B, H, M, r_k)
+    cv = lla.alloc_cache(B, H, M, r_v)
     lla.encode(xk, xv, wk, wv, ck, cv, T=wl.T, pos0=0)
     del xk, xv
-    units = [(0, 0), (1, 7), (3, 15)]
-    rows = [0, 1, 63, 64, 127, 128, 4095, 5000, 8190, 8191]
-    lat_k = {u: f64(lla.from_paged(ck[u[0]:u[0] + 1, u[1]:u[1] + 1]))[0, 0] for u in units}
-    lat_v = {u: f64(lla.from_paged(cv[u[0]:u[0] + 1, u[1]:u[1] + 1]))[0, 0] for u in units}
+    plain_units = [(0, 0), (1, 7), (3, 15)]
+    plain_rows = [0, 1, 63, 64, 127, 128, 4095, 5000, 8190, 8191]
+    rows = sorted(set(plain_rows) | {256 * qb + e for qb in range(M // 256) for e in (0, 255)})
+    lat_k = f64_dev(lla.from_paged(ck))
+    lat_v = f64_dev(lla.from_paged(cv))
     for loop in range(wl.T):
         log(f"prefill_write full size: loop {loop}")
         q = W.queries(wl, 0, loop, M=M, device=DEV)
         uk, uv, _, _ = W.codec_loop(wl, r_k, r_v, 0, loop, DEV)
         out = lla.prefill_attn(q, ck, cv, uk, uv, p0=0)
         torch.cuda.synchronize()
-        o = out[:, :, rows].cpu().double().numpy()
-        assert np.all(np.isfinite(out.cpu().numpy()))
-        for (b, h) in units:
-            ref = np.stack([oracle.decode_attn(f64(q[b, h, m]), lat_k[(b, h)][:m + 1], lat_v[(b, h)][:m + 1],
-                                               f64(uk[h]), f64(uv[h])) for m in rows])
-            assert_close(o[b, h], ref, torch.bfloat16, f"loop {loop} unit ({b},{h})")
+        assert bool(torch.isfinite(out).all())
+        o = f64_dev(out[:, :, rows])
+        q64 = f64_dev(q[:, :, rows])
+        uk64, uv64 = f64(uk), f64(uv)
+        ref = np.empty_like(o)
+        for b in range(B):
+            for h in range(H):
+                for i, m in enumerate(rows):
+                    ref[b, h, i] = oracle.decode_attn_absorbed(q64[b, h, i], lat_k[b, h, :m + 1], lat_v[b, h, :m + 1],
+                                                               uk64[h], uv64[h])
+        assert_units_close(o, ref, f"loop {loop}: every (b, h) at {len(rows)} rows")
+        for (b, h) in plain_units:
+            idx = [rows.index(m) for m in plain_rows]
+            plain = np.stack([oracle.decode_attn(q64[b, h, i], lat_k[b, h, :rows[i] + 1], lat_v[b, h, :rows[i] + 1],
+                                                 uk64[h], uv64[h]) for i in idx])
+            assert_close(o[b, h, idx], plain, torch.bfloat16, f"loop {loop} unit ({b},{h}) plain definition")

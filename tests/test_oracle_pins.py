@@ -448,3 +448,60 @@ def test_pins_accept_the_oracle():
                                     _mutant_wrong_loop_mu, _mutant_absorbed_drops_mu_v])
 def test_pins_reject_planted_mistakes(mutant):
     assert not _decode_pins_pass(mutant)
+
+
+# ---------------------------------------------------------------------------
+# The batched prefill wrapper, every row against pure-Python brute force at an
+# offset p0 > 0; slips in the causal length must fail.
+# ---------------------------------------------------------------------------
+
+def _py_prefill_row(q, ck, cv, Uk, Uv, muk, muv, n, scale):
+    d, rk, rv = len(q), ck.shape[1], cv.shape[1]
+    K = [[sum(ck[t, j] * Uk[i, j] for j in range(rk)) + muk[i] for i in range(d)] for t in range(n)]
+    V = [[sum(cv[t, j] * Uv[i, j] for j in range(rv)) + muv[i] for i in range(d)] for t in range(n)]
+    return np.array(_py_attention(list(q), K, V, scale))
+
+
+def _prefill_batched_pin_passes(fn):
+    g = _rng(41)
+    B, H, d, rk, rv, p0, M = 2, 2, 4, 3, 5, 3, 5
+    Q = g.standard_normal((B, H, M, d))
+    ck, cv = g.standard_normal((B, H, p0 + M, rk)), g.standard_normal((B, H, p0 + M, rv))
+    Uk, Uv = g.standard_normal((H, d, rk)), g.standard_normal((H, d, rv))
+    muk, muv = g.standard_normal((H, d)), g.standard_normal((H, d))
+    out = fn(Q, ck, cv, Uk, Uv, muk, muv, 0.6, p0)
+    for b in range(B):
+        for h in range(H):
+            for m in range(M):
+                ref = _py_prefill_row(Q[b, h, m], ck[b, h], cv[b, h], Uk[h], Uv[h], muk[h], muv[h],
+                                      p0 + m + 1, 0.6)
+                if not np.max(np.abs(out[b, h, m] - ref)) < 1e-12:
+                    return False
+    return True
+
+
+def _prefill_batched_mutant(n_of):
+    def fn(Q, ck, cv, Uk, Uv, muk, muv, scale, p0):
+        B, H, M, d = Q.shape
+        out = np.empty(Q.shape)
+        for b in range(B):
+            for h in range(H):
+                for m in range(M):
+                    n = n_of(p0, m)
+                    out[b, h, m] = oracle.decode_attn(Q[b, h, m], ck[b, h, :n], cv[b, h, :n], Uk[h], Uv[h],
+                                                      muk[h], muv[h], scale)
+        return out
+    return fn
+
+
+def test_prefill_batched_rows_match_bruteforce():
+    assert _prefill_batched_pin_passes(
+        lambda Q, ck, cv, Uk, Uv, muk, muv, s, p0: oracle.prefill_attn_batched(Q, ck, cv, Uk, Uv, muk, muv, s,
+                                                                               p0=p0))
+
+
+@pytest.mark.parametrize("n_of", [lambda p0, m: p0 + 1, lambda p0, m: m + 1, lambda p0, m: p0 + m,
+                                  lambda p0, m: p0 + m + 2])
+def test_prefill_batched_pin_rejects_slips(n_of):
+    assert _prefill_batched_pin_passes(_prefill_batched_mutant(lambda p0, m: p0 + m + 1))
+    assert not _prefill_batched_pin_passes(_prefill_batched_mutant(n_of))

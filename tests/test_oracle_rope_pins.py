@@ -243,3 +243,77 @@ def test_decode_pin_rejects_unrotated_query():
     # a slip that rotates the keys but feeds the query unrotated (position 0)
     wrong = oracle.decode_attn_rope(q, qr, ck, cv, kr, Uk, Uv, muk, muv, scale=0.41, q_pos=0)
     assert np.max(np.abs(wrong - ref)) > 1e-3
+
+
+# ---------------------------------------------------------------------------
+# the batched prefill wrapper: every row of several queries past an offset,
+# against the brute force above, with one rotary key per token (shared by the
+# heads) and one per head
+# ---------------------------------------------------------------------------
+
+def _batched_prefill_case(g, Hr):
+    B, H, d, dr, rk, rv, p0, M = 2, 3, 4, 4, 3, 2, 5, 6
+    Q, QR = g.standard_normal((B, H, M, d)), g.standard_normal((B, H, M, dr))
+    ck, cv = g.standard_normal((B, H, p0 + M, rk)), g.standard_normal((B, H, p0 + M, rv))
+    kr = g.standard_normal((B, Hr, p0 + M, dr))
+    Uk, Uv = g.standard_normal((H, d, rk)), g.standard_normal((H, d, rv))
+    muk, muv = g.standard_normal((H, d)), g.standard_normal((H, d))
+    return Q, QR, ck, cv, kr, Uk, Uv, muk, muv, p0
+
+
+def _batched_prefill_pin_passes(fn, Hr):
+    g = _rng(40 + Hr)
+    Q, QR, ck, cv, kr, Uk, Uv, muk, muv, p0 = _batched_prefill_case(g, Hr)
+    B, H, M, _ = Q.shape
+    out = fn(Q, QR, ck, cv, kr, Uk, Uv, muk, muv, 0.45, 500.0, p0)
+    for b in range(B):
+        for h in range(H):
+            hr = 0 if Hr == 1 else h
+            for m in range(M):
+                n = p0 + m + 1
+                ref = _bruteforce(Q[b, h, m], QR[b, h, m], ck[b, h, :n], cv[b, h, :n], kr[b, hr, :n],
+                                  Uk[h], Uv[h], muk[h], muv[h], 0.45, 500.0, p0 + m)
+                if not np.max(np.abs(out[b, h, m] - ref)) < 1e-12:
+                    return False
+    return True
+
+
+def _oracle_batched(Q, QR, ck, cv, kr, Uk, Uv, muk, muv, scale, base, p0):
+    return oracle.prefill_attn_rope_batched(Q, QR, ck, cv, kr, Uk, Uv, muk, muv, scale, base, p0)
+
+
+def _batched_mutant(q_pos_of, n_of):
+    """The batched wrapper with one slip in the query position or the causal length."""
+    def fn(Q, QR, ck, cv, kr, Uk, Uv, muk, muv, scale, base, p0):
+        B, H, M, d = Q.shape
+        Hr = kr.shape[1]
+        out = np.empty((B, H, M, d))
+        for b in range(B):
+            for h in range(H):
+                hr = 0 if Hr == 1 else h
+                for m in range(M):
+                    n = n_of(p0, m)
+                    out[b, h, m] = oracle.decode_attn_rope(Q[b, h, m], QR[b, h, m], ck[b, h, :n], cv[b, h, :n],
+                                                           kr[b, hr, :n], Uk[h], Uv[h], muk[h], muv[h], scale,
+                                                           base, q_pos=q_pos_of(p0, m))
+        return out
+    return fn
+
+
+@pytest.mark.parametrize("Hr", [1, 3])
+def test_prefill_rope_batched_rows_match_bruteforce(Hr):
+    assert _batched_prefill_pin_passes(_oracle_batched, Hr)
+
+
+@pytest.mark.parametrize("Hr", [1, 3])
+@pytest.mark.parametrize("slip", ["q_pos=p0", "n=p0+1", "q_pos=m", "n=m+1"])
+def test_prefill_rope_batched_pin_rejects_slips(Hr, slip):
+    good_q, good_n = (lambda p0, m: p0 + m), (lambda p0, m: p0 + m + 1)
+    mutants = {
+        "q_pos=p0": _batched_mutant(lambda p0, m: p0, good_n),
+        "n=p0+1": _batched_mutant(good_q, lambda p0, m: p0 + 1),
+        "q_pos=m": _batched_mutant(lambda p0, m: m, good_n),
+        "n=m+1": _batched_mutant(good_q, lambda p0, m: m + 1),
+    }
+    assert _batched_prefill_pin_passes(_batched_mutant(good_q, good_n), Hr)  # the harness itself
+    assert not _batched_prefill_pin_passes(mutants[slip], Hr)
