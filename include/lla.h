@@ -65,13 +65,15 @@ extern "C" {
 #define LLA_MAX_ROPE 256
 #define LLA_MAX_RANK_2D 1024
 #define LLA_MAX_SPLITS 64
+#define LLA_NOALLOC_SCRATCH_BYTES (4u << 20) /* static scratch per device of lla_decode_attn_noalloc */
 
 typedef enum lla_status {
   LLA_OK = 0,
   LLA_ERR_INVALID_ARG = 1, /* a size, pointer, alignment or value is invalid */
   LLA_ERR_UNSUPPORTED = 2, /* valid in the paper's terms, not supported here */
   LLA_ERR_WORKSPACE = 3,   /* the decode workspace is missing or too small  */
-  LLA_ERR_HIP = 4          /* the HIP runtime reported an error on launch    */
+  LLA_ERR_HIP = 4,         /* the HIP runtime reported an error on launch    */
+  LLA_ERR_SCRATCH = 5      /* lla_decode_attn_noalloc: more than its static scratch */
 } lla_status;
 
 typedef enum lla_dtype {
@@ -188,6 +190,30 @@ lla_status lla_decode_attn(int dtype, int out_dtype, int B, int H, int d_head, i
                            const void* c_k, const void* c_v, const void* u_k, const void* u_v,
                            const void* mu_k, const void* mu_v, float scale, void* out,
                            void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * lla_decode_attn for callers that cannot allocate (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * arguments without the workspace, the same kernels, launch shape and
+ * results.  When the context is split across workgroups, the arrival counters
+ * and partial softmax states live in a static device array of
+ * LLA_NOALLOC_SCRATCH_BYTES that the library holds on every GPU it runs on
+ * until the process ends; the call clears the counters with a fill kernel
+ * (no memset node) and never calls an allocating routine.  Every call on one
+ * GPU shares that GPU's array and it keeps the last call's contents: calls
+ * that may overlap on one GPU (different streams, or threads) race and must
+ * be ordered by the caller.  The first call on a device resolves the array's
+ * address (hipGetSymbolAddress).
+ * Errors: as lla_decode_attn, and LLA_ERR_SCRATCH when the split the launch
+ * heuristic chooses needs more than LLA_NOALLOC_SCRATCH_BYTES (4 bytes per
+ * (b, h) unit rounded up to 256, plus 4 * (r_v + 2) bytes per unit and split;
+ * on a 256-CU MI355X the default heuristic stays below 1.1 MiB).
+ */
+lla_status lla_decode_attn_noalloc(int dtype, int out_dtype, int B, int H, int d_head, int r_k,
+                                   int r_v, int n_max, int n_ctx, const int32_t* ctx_len,
+                                   const void* q, const void* c_k, const void* c_v, const void* u_k,
+                                   const void* u_v, const void* mu_k, const void* mu_v, float scale,
+                                   void* out, void* stream);
 
 /*
  * Causal prefill attention at loop l over the latent cache (absorbed form,

@@ -8,6 +8,7 @@
 #include <cstdint>
 #include <cstdlib>
 #include <limits>
+#include <mutex>
 
 #include "../../include/lla.h"
 #include "lla_internal.h"
@@ -122,6 +123,9 @@ const char* lla_status_string(int status) {
     case LLA_ERR_UNSUPPORTED: return "LLA_ERR_UNSUPPORTED: valid arguments not supported by this build";
     case LLA_ERR_WORKSPACE: return "LLA_ERR_WORKSPACE: decode workspace missing or too small";
     case LLA_ERR_HIP: return "LLA_ERR_HIP: the HIP runtime reported an error";
+    case LLA_ERR_SCRATCH:
+      return "LLA_ERR_SCRATCH: the call needs more than the library's static scratch "
+             "(LLA_NOALLOC_SCRATCH_BYTES per device)";
     default: return "unknown lla_status";
   }
 }
@@ -263,12 +267,47 @@ lla_status lla_decode_splits(int dtype, int B, int H, int n_ctx, int with_worksp
 }
 
 namespace {
+// ---- static scratch of the allocation-free decode entry point ----
+// One array per device (each GPU the library runs on holds its own copy until
+// the process ends).  Host code never uses the array's name as an address:
+// hipGetSymbolAddress resolves the device address once per device, and that
+// pointer is what kernels and fills receive.
+constexpr size_t kStaticScratchBytes = LLA_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+constexpr int kMaxDevices = 64;
+struct ScratchSlot {
+  std::once_flag once;
+  void* ptr = nullptr;
+  hipError_t err = hipSuccess;
+};
+ScratchSlot g_scratch[kMaxDevices];
+
+// Device address of the current device's scratch, resolved on the first call
+// on that device (with it current).
+lla_status static_scratch_base(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return LLA_ERR_HIP;
+  ScratchSlot& slot = g_scratch[dev];
+  std::call_once(slot.once, [&slot] {
+    slot.err = hipGetSymbolAddress(&slot.ptr, HIP_SYMBOL(scratch));
+  });
+  if (slot.err != hipSuccess || slot.ptr == nullptr) return LLA_ERR_HIP;
+  *out = slot.ptr;
+  return LLA_OK;
+}
+
+__global__ void zero_u32_kernel(uint32_t* p, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0u;
+}
+
 lla_status decode_impl(int dtype, int out_dtype, int B, int H, int d_head, int r_k, int r_v,
                        int d_rope, int H_rope, int n_max, int n_ctx, const int32_t* ctx_len,
                        const void* q, const void* q_rope, const void* c_k, const void* c_v,
                        const void* r_cache, const void* u_k, const void* u_v, const void* mu_k,
                        const void* mu_v, float scale, void* out, void* workspace,
-                       size_t ws_bytes, void* stream) {
+                       size_t ws_bytes, void* stream, bool static_scratch = false) {
   if (!dtype_ok(dtype) || !dtype_ok(out_dtype) || B < 1 || H < 1 || !head_ok(d_head) ||
       !rank_ok(r_k) || !rank_ok(r_v) || !cap_ok(n_max) || n_ctx < 1 || n_ctx > n_max ||
       !std::isfinite(scale) || !(scale > 0.f))
@@ -281,9 +320,11 @@ lla_status decode_impl(int dtype, int out_dtype, int B, int H, int d_head, int r
   if (d_rope && (!rope_ok(d_rope) || !(H_rope == 1 || H_rope == H) || !ptr_ok(q_rope) ||
                  !ptr_ok(r_cache) || ((r_k + 7) / 8) * 8 + d_rope > LLA_MAX_RANK))
     return LLA_ERR_INVALID_ARG;
-  if ((workspace == nullptr) != (ws_bytes == 0)) return LLA_ERR_WORKSPACE;
-  if (workspace && (!aligned16(workspace) || ws_bytes < workspace_bytes(B, H, r_v, n_ctx)))
-    return LLA_ERR_WORKSPACE;
+  if (!static_scratch) {
+    if ((workspace == nullptr) != (ws_bytes == 0)) return LLA_ERR_WORKSPACE;
+    if (workspace && (!aligned16(workspace) || ws_bytes < workspace_bytes(B, H, r_v, n_ctx)))
+      return LLA_ERR_WORKSPACE;
+  }
   (void)mu_k;  // q . mu_k is constant over the context: it cancels in the softmax
 
   lla::DecodeArgs a{};
@@ -312,17 +353,38 @@ lla_status decode_impl(int dtype, int out_dtype, int B, int H, int d_head, int r
   a.Hr = H_rope;
   a.qr = q_rope;
   a.rc = r_cache;
-  const DecodeShape sh = choose_shape(B * H, n_ctx, workspace != nullptr, dtype == LLA_BF16);
+  const DecodeShape sh = choose_shape(B * H, n_ctx, static_scratch || workspace != nullptr,
+                                      dtype == LLA_BF16);
   a.waves = sh.waves;
   a.splits = sh.splits;
   a.deep = sh.deep;
-  if (a.splits > 1) {
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  if (static_scratch) {
+    // partials of exactly the chosen split count, in the device's static array
+    void* base = nullptr;
+    const lla_status e = static_scratch_base(&base);
+    if (e != LLA_OK) return e;
+    if (a.splits > 1) {
+      const size_t units = (size_t)B * H;
+      const size_t counters = (units * sizeof(uint32_t) + 255) / 256 * 256;
+      if (counters + units * a.splits * (size_t)(r_v + 2) * sizeof(float) > kStaticScratchBytes)
+        return LLA_ERR_SCRATCH;
+      // the arrival counters must start at zero; a fill kernel, not a memset
+      // node, so the call can be captured into a graph
+      const int n = (int)units;
+      hipLaunchKernelGGL(zero_u32_kernel, dim3((n + 255) / 256), dim3(256), 0, st,
+                         static_cast<uint32_t*>(base), n);
+      if (hipGetLastError() != hipSuccess) return LLA_ERR_HIP;
+      a.cnt = static_cast<uint32_t*>(base);
+      a.part = reinterpret_cast<float*>(static_cast<char*>(base) + counters);
+    }
+  } else if (a.splits > 1) {
     const size_t units = (size_t)B * H;
     const size_t counters = (units * sizeof(uint32_t) + 255) / 256 * 256;
     a.cnt = static_cast<uint32_t*>(workspace);
     a.part = reinterpret_cast<float*>(static_cast<char*>(workspace) + counters);
   }
-  return hip_status(lla::launch_decode(a, static_cast<hipStream_t>(stream)));
+  return hip_status(lla::launch_decode(a, st));
 }
 }  // namespace
 
@@ -334,6 +396,16 @@ lla_status lla_decode_attn(int dtype, int out_dtype, int B, int H, int d_head, i
   return decode_impl(dtype, out_dtype, B, H, d_head, r_k, r_v, 0, 1, n_max, n_ctx, ctx_len, q,
                      nullptr, c_k, c_v, nullptr, u_k, u_v, mu_k, mu_v, scale, out, workspace,
                      ws_bytes, stream);
+}
+
+lla_status lla_decode_attn_noalloc(int dtype, int out_dtype, int B, int H, int d_head, int r_k,
+                                   int r_v, int n_max, int n_ctx, const int32_t* ctx_len,
+                                   const void* q, const void* c_k, const void* c_v, const void* u_k,
+                                   const void* u_v, const void* mu_k, const void* mu_v, float scale,
+                                   void* out, void* stream) {
+  return decode_impl(dtype, out_dtype, B, H, d_head, r_k, r_v, 0, 1, n_max, n_ctx, ctx_len, q,
+                     nullptr, c_k, c_v, nullptr, u_k, u_v, mu_k, mu_v, scale, out, nullptr, 0,
+                     stream, /*static_scratch=*/true);
 }
 
 lla_status lla_decode_attn_rope(int dtype, int out_dtype, int B, int H, int d_head, int r_k,

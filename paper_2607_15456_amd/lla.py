@@ -24,7 +24,7 @@ PAGE = 64
 MAX_RANK = 512
 MAX_SPLITS = 64
 
-LLA_OK, LLA_ERR_INVALID_ARG, LLA_ERR_UNSUPPORTED, LLA_ERR_WORKSPACE, LLA_ERR_HIP = range(5)
+LLA_OK, LLA_ERR_INVALID_ARG, LLA_ERR_UNSUPPORTED, LLA_ERR_WORKSPACE, LLA_ERR_HIP, LLA_ERR_SCRATCH = range(6)
 LLA_F32, LLA_BF16 = 0, 1
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblla.so")
@@ -41,6 +41,7 @@ _SIGS = {
     "lla_decode_workspace_bytes": (_c_int, [_c_int] * 4 + [ctypes.POINTER(_c_sz)]),
     "lla_decode_splits": (_c_int, [_c_int] * 5 + [ctypes.POINTER(_c_int)]),
     "lla_decode_attn": (_c_int, [_c_int] * 9 + [_c_vp] * 8 + [_c_f, _c_vp, _c_vp, _c_sz, _c_vp]),
+    "lla_decode_attn_noalloc": (_c_int, [_c_int] * 9 + [_c_vp] * 8 + [_c_f, _c_vp, _c_vp]),
     "lla_prefill_attn": (_c_int, [_c_int] * 10 + [_c_vp] * 7 + [_c_f, _c_vp, _c_vp]),
     "lla_rope_write": (_c_int, [_c_int] * 5 + [_c_vp, ctypes.c_double, _c_vp, _c_int, _c_int, _c_vp]),
     "lla_rope_rotate": (_c_int, [_c_int] * 5 + [_c_vp, _c_vp, _c_int, ctypes.c_double, _c_vp, _c_vp]),
@@ -287,6 +288,36 @@ def decode_attn(q, c_k, c_v, u_k, u_v, *, n_ctx: int, ctx_len=None, mu_k=None, m
                                       _ptr(c_v), _ptr(r_cache), _ptr(u_k), _ptr(u_v), _ptr(mu_k),
                                       _ptr(mu_v), float(scale), _ptr(out), _ptr(workspace), ws_bytes,
                                       _stream(q)))
+    return out
+
+
+def decode_attn_noalloc(q, c_k, c_v, u_k, u_v, *, n_ctx: int, out, ctx_len=None, mu_k=None, mu_v=None,
+                        scale: float | None = None):
+    """lla_decode_attn_noalloc: decode_attn with no workspace (the library's
+    static scratch holds the split-K partials).  ``out`` [B, H, d] is
+    caller-allocated (f32 or bf16); nothing is allocated here either."""
+    dev = q.device
+    B, H, d = q.shape
+    for t, n in ((q, "q"), (c_k, "c_k"), (c_v, "c_v"), (u_k, "u_k"), (u_v, "u_v")):
+        _need(t, n, q.dtype, dev)
+    for t, n in ((mu_k, "mu_k"), (mu_v, "mu_v")):
+        if t is not None:
+            _need(t, n, q.dtype, dev)
+    r_k, r_v = u_k.shape[2], u_v.shape[2]
+    n_max = c_k.shape[2] * PAGE
+    if (c_k.shape != (B, H, n_max // PAGE, r_k, PAGE) or c_v.shape != (B, H, n_max // PAGE, r_v, PAGE)
+            or u_k.shape != (H, d, r_k) or u_v.shape != (H, d, r_v) or out.shape != (B, H, d)):
+        raise ValueError("inconsistent shapes")
+    _need(out, "out", None, dev)
+    if ctx_len is not None:
+        _need(ctx_len, "ctx_len", torch.int32, dev)
+        if ctx_len.shape != (B,):
+            raise ValueError("ctx_len must have shape [B]")
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    _check(lib().lla_decode_attn_noalloc(_dt(q), _out_code(out.dtype), B, H, d, r_k, r_v, n_max, n_ctx,
+                                         _ptr(ctx_len), _ptr(q), _ptr(c_k), _ptr(c_v), _ptr(u_k), _ptr(u_v),
+                                         _ptr(mu_k), _ptr(mu_v), float(scale), _ptr(out), _stream(q)))
     return out
 
 

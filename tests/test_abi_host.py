@@ -30,6 +30,7 @@ def test_header_declares_the_boundary():
     names = _declared()
     assert names == sorted(["lla_status_string", "lla_abi_version", "lla_rho", "lla_cache_bytes",
                             "lla_encode", "lla_decode_workspace_bytes", "lla_decode_splits", "lla_decode_attn",
+                            "lla_decode_attn_noalloc",
                             "lla_prefill_attn", "lla_rope_write", "lla_rope_rotate",
                             "lla_decode_attn_rope", "lla_prefill_attn_rope", "lla_encode_ring",
                             "lla_rope_write_ring", "lla_encode_2d", "lla_encode_2d_workspace_bytes",
@@ -65,7 +66,8 @@ def test_decode_split_choice():
 
 
 def test_status_strings():
-    for code, tag in [(0, "LLA_OK"), (1, "INVALID_ARG"), (2, "UNSUPPORTED"), (3, "WORKSPACE"), (4, "HIP")]:
+    for code, tag in [(0, "LLA_OK"), (1, "INVALID_ARG"), (2, "UNSUPPORTED"), (3, "WORKSPACE"), (4, "HIP"),
+                      (5, "SCRATCH")]:
         assert tag in lla.status_string(code)
     assert "unknown" in lla.status_string(99)
 
@@ -151,6 +153,24 @@ def _decode(**kw):
 ])
 def test_decode_rejects(kw, code):
     assert _decode(**kw) == code
+
+
+def _decode_noalloc(**kw):
+    a = dict(dtype=1, out_dtype=0, B=2, H=16, d=128, rk=96, rv=160, n_max=512, n_ctx=512, ctx_len=None,
+             q=P, ck=P, cv=P, uk=P, uv=P, muk=None, muv=None, scale=0.088, out=P, stream=None)
+    a.update(kw)
+    return lla.lib().lla_decode_attn_noalloc(a["dtype"], a["out_dtype"], a["B"], a["H"], a["d"], a["rk"],
+                                             a["rv"], a["n_max"], a["n_ctx"], a["ctx_len"], a["q"], a["ck"],
+                                             a["cv"], a["uk"], a["uv"], a["muk"], a["muv"], a["scale"], a["out"],
+                                             a["stream"])
+
+
+@pytest.mark.parametrize("kw", [
+    dict(dtype=2), dict(B=0), dict(d=48), dict(rk=0), dict(rv=513), dict(n_max=500), dict(n_ctx=0),
+    dict(n_ctx=513), dict(scale=float("nan")), dict(q=None), dict(ck=MIS), dict(out=None), dict(ctx_len=P + 2),
+])
+def test_decode_noalloc_rejects(kw):
+    assert _decode_noalloc(**kw) == lla.LLA_ERR_INVALID_ARG
 
 
 def _encode(**kw):

@@ -1,0 +1,76 @@
+"""lla_decode_attn_noalloc (the allocation-free decode: split-K partials in the
+library's static per-device scratch) against lla_decode_attn with a caller
+workspace, through the C ABI: bitwise-equal outputs, both within the bf16 /
+fp32 bars of the float64 oracle, on consecutive calls whose second input is
+smaller (the scratch keeps the previous call's contents)."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_15456_amd import lla, workloads as W
+from tests.helpers import assert_close, f64, f64_dev, log
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def _case(dtype, B, H, N, r_k, r_v, seed):
+    wl = W.Workload(f"noalloc_{seed}", 1, H, 128, 4, B, N, ((r_k, r_v),), dtype)
+    ck = W.latents(wl, r_k, "k", 0, device=DEV, dtype=dtype)
+    cv = W.latents(wl, r_v, "v", 0, device=DEV, dtype=dtype)
+    q = W.queries(wl, 0, 1, device=DEV, dtype=dtype)
+    uk, uv, muk, muv = W.codec_loop(wl, r_k, r_v, 0, 1, DEV, dtype, means=True)
+    return q, ck, cv, uk, uv, muk, muv, lla.to_paged(ck, N), lla.to_paged(cv, N)
+
+
+def _check(dtype, B, H, N, r_k, r_v, seed, lens=None):
+    q, ck, cv, uk, uv, muk, muv, pk, pv = _case(dtype, B, H, N, r_k, r_v, seed)
+    splits = lla.decode_splits(dtype, B, H, N)
+    log(f"noalloc {dtype} B={B} H={H} N={N} r=({r_k},{r_v}) splits={splits} lens={lens}")
+    ctx = None if lens is None else torch.tensor(lens, dtype=torch.int32, device=DEV)
+    out = torch.full((B, H, 128), 123.0, dtype=torch.float32, device=DEV)
+    lla.decode_attn_noalloc(q, pk, pv, uk, uv, n_ctx=N, ctx_len=ctx, mu_k=muk, mu_v=muv, out=out)
+    ref_gpu = lla.decode_attn(q, pk, pv, uk, uv, n_ctx=N, ctx_len=ctx, mu_k=muk, mu_v=muv,
+                              workspace=lla.new_workspace(B, H, r_v, N))
+    torch.cuda.synchronize()
+    o = f64(out)
+    assert torch.equal(out, ref_gpu) or (np.isnan(o) == np.isnan(f64(ref_gpu))).all() and \
+        np.array_equal(o[~np.isnan(o)], f64(ref_gpu)[~np.isnan(o)]), "differs from lla_decode_attn"
+    lens_ = [N] * B if lens is None else lens
+    ck64, cv64, q64 = f64_dev(ck), f64_dev(cv), f64(q)
+    uk64, uv64, muv64 = f64(uk), f64(uv), f64(muv)
+    for b in range(B):
+        if not 1 <= lens_[b] <= N:
+            assert np.all(np.isnan(o[b]))
+            continue
+        n = lens_[b]
+        ref = np.stack([oracle.decode_attn_absorbed(q64[b, h], ck64[b, h, :n], cv64[b, h, :n], uk64[h], uv64[h],
+                                                    None, muv64[h]) for h in range(H)])
+        assert_close(o[b], ref, dtype, f"sequence {b}")
+    return splits
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_noalloc_matches_workspace_decode_twice_smaller_second(dtype):
+    r_k, r_v = (36, 60) if dtype == torch.bfloat16 else (96, 160)
+    # first call: 8 splits over 32768 tokens; second, smaller: 2 splits over 8192
+    assert _check(dtype, 1, 16, 32768, r_k, r_v, 1) == 8
+    assert _check(dtype, 1, 16, 8192, r_k, r_v, 2) == 2
+    # a batch that does not split (no scratch used), then split again with
+    # ragged and out-of-range lengths (the counters must start at zero)
+    assert _check(dtype, 8, 16, 1024, r_k, r_v, 3) == 1
+    assert _check(dtype, 2, 16, 16384, r_k, r_v, 4, lens=[16384, 0]) > 1
+    assert _check(dtype, 2, 16, 16384, r_k, r_v, 5, lens=[5000, 16383]) > 1
+
+
+def test_noalloc_rejects_bad_arguments_before_launch():
+    q, ck, cv, uk, uv, muk, muv, pk, pv = _case(torch.bfloat16, 1, 16, 1024, 36, 60, 6)
+    out = torch.zeros((1, 16, 128), device=DEV)
+    with pytest.raises(lla.LLAError) as e:
+        lla.decode_attn_noalloc(q, pk, pv, uk, uv, n_ctx=0, out=out)
+    assert e.value.status == lla.LLA_ERR_INVALID_ARG
+    torch.cuda.synchronize()
+    assert int(torch.count_nonzero(out)) == 0
