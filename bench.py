@@ -65,7 +65,7 @@ def parse():
     p.add_argument("--evict", default=None,
                    help="SINK,WINDOW: decode workloads keep a sink + window eviction budget (ring cache of "
                         "SINK + WINDOW slots, the step's new token written into its ring slot)")
-    p.add_argument("--ranks", default=None, help="R_K,R_V: override a decode workload's ranks")
+    p.add_argument("--ranks", default=None, help="R_K,R_V: override a decode or prefill_write workload's ranks")
     p.add_argument("--rope", type=int, default=0,
                    help="add the decoupled rotary branch with this d_rope (one rotary key per token, "
                         "shared by the heads and the loops); ouro14b_decode and prefill_write")
@@ -371,6 +371,16 @@ def prefill_flops(B, H, M, p0, d, r_k, r_v, d_rope=0):
     return B * H * (2 * (r_k + d_rope + r_v) * pairs + 2 * M * d * (r_k + r_v))
 
 
+def prefill_rebuild_flops(B, H, M, p0, d, r_k, r_v):
+    """Flops of one prefill call on the rebuild path (bf16 ranks above 95): every
+    head's K and V rebuilt for the p0 + M positions (2 d (r_k + r_v) per token),
+    then 4 d per causal (query, key) pair (scores and values at d_head).  At
+    these ranks it is the smaller count: the absorbed form costs 2 (r_k + r_v)
+    per pair, 512 at (96, 160) and 1536 at (288, 480), against 4 d = 512."""
+    pairs = M * p0 + M * (M + 1) // 2
+    return B * H * (2 * d * (r_k + r_v) * (p0 + M) + 4 * d * pairs)
+
+
 def encode_bytes(B, M, H, K, r_k, r_v, elem=2):
     """Algorithmic bytes of one encode: x_k, x_v read, W_down^T read, latents written."""
     return 2 * B * M * H * K * elem + H * (r_k + r_v) * K * elem + B * H * M * (r_k + r_v) * elem
@@ -379,8 +389,13 @@ def encode_bytes(B, M, H, K, r_k, r_v, elem=2):
 def run_prefill(args, torch, lla, W):
     wl = W.WORKLOADS["prefill_write"]
     r_k, r_v = wl.ranks[0]
+    if args.ranks:
+        r_k, r_v = (int(v) for v in args.ranks.split(","))
     B, M, H, d, T = wl.B, wl.N, wl.H, wl.d, wl.T
     dev = torch.device("cuda:0")
+    ws_bytes = lla.prefill_workspace_bytes(wl.dtype, B, H, M, d, r_k, r_v, 0)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev) if ws_bytes else None
+    rebuild = ws_bytes > 0
     stream = torch.cuda.current_stream(dev)
     xk = W.stacked_kv(wl, "k", 0, device=dev)
     xv = W.stacked_kv(wl, "v", 0, device=dev)
@@ -418,7 +433,7 @@ def run_prefill(args, torch, lla, W):
                 lla.prefill_attn(q, ck, cv, uk, uv, p0=0, out=out, q_rope=q_rot, r_cache=r_cache)
             else:
                 s = pre_t.start() if timed else None
-                lla.prefill_attn(q, ck, cv, uk, uv, p0=0, out=out)
+                lla.prefill_attn(q, ck, cv, uk, uv, p0=0, out=out, workspace=ws)
             if timed:
                 pre_t.stop(s)
 
@@ -433,7 +448,7 @@ def run_prefill(args, torch, lla, W):
     torch.cuda.synchronize()
     step_ms = t0.elapsed_time(t1) / args.steps
     enc_ms, pre_ms = enc_t.mean_ms(), pre_t.mean_ms()
-    fl = prefill_flops(B, H, M, 0, d, r_k, r_v, dr)
+    fl = prefill_rebuild_flops(B, H, M, 0, d, r_k, r_v) if rebuild else prefill_flops(B, H, M, 0, d, r_k, r_v, dr)
     eb = encode_bytes(B, M, H, T * d, r_k, r_v)
     tflops = fl / (pre_ms * 1e-3) / 1e12
     return {
@@ -442,12 +457,15 @@ def run_prefill(args, torch, lla, W):
         "unit": "tokens/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(step_ms, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": wl.description + (f"; decoupled rotary branch d_rope {dr}" if dr else ""),
+        "config": {"workload": wl.description + (f"; decoupled rotary branch d_rope {dr}" if dr else "")
+                   + (f"; ranks overridden to ({r_k}, {r_v})" if args.ranks else ""),
                    "batch": B, "new_tokens": M, "heads": H, "d_head": d, "loops": T,
                    "r_k": r_k, "r_v": r_v, "d_rope": dr, "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "achieved": round(tflops, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(tflops / BF16_PEAK_TFLOPS, 4), "traffic": None,
-                     "kernel": "prefill_bf16_kernel (lla_prefill_attn)", "flops_per_launch": fl,
+                     "kernel": ("recon2d_kernel (K, V rebuilt per head) + flash2d_kernel (lla_prefill_attn, "
+                                "rebuild path; flops counted as rebuild + 4 d per causal pair)" if rebuild
+                                else "prefill_bf16_kernel (lla_prefill_attn)"), "flops_per_launch": fl,
                      "avg_launch_ms": round(pre_ms, 5)},
         "encode": {"bound": "hbm", "achieved": round(eb / (enc_ms * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS,
                    "unit": "GB/s", "frac": round(eb / (enc_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),

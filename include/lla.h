@@ -27,7 +27,10 @@
  *   Outputs are valid once the stream has reached that point.
  * - Every entry point validates all scalar arguments and pointers on the host
  *   before launching anything.  On any error nothing is launched and no
- *   output is touched.  NaN/Inf in the data are propagated, not checked.
+ *   output is touched.  NaN/Inf in the data are not checked: a non-finite
+ *   value in data an output depends on makes that output non-finite, and
+ *   cache slots a call does not attend are never read into a result.  The
+ *   prefills add one exception, stated with lla_prefill_attn.
  * - dtype arguments take lla_dtype values.  "dtype" is the element type of
  *   every input tensor of the call (queries, latents, projections, means);
  *   accumulation is always fp32.
@@ -59,7 +62,7 @@
 extern "C" {
 #endif
 
-#define LLA_ABI_VERSION 8
+#define LLA_ABI_VERSION 9
 #define LLA_PAGE_TOKENS 64
 #define LLA_MAX_RANK 512
 #define LLA_MAX_ROPE 256
@@ -216,28 +219,61 @@ lla_status lla_decode_attn_noalloc(int dtype, int out_dtype, int B, int H, int d
                                    void* out, void* stream);
 
 /*
- * Causal prefill attention at loop l over the latent cache (absorbed form,
- * App. J; pass 2 of the two-pass decoder of App. A reads the cache this way):
- * query m of sequence b sits at absolute position p0 + m and attends the
- * cached tokens n <= p0 + m, i.e. row m equals lla_decode_attn with
- * N = p0 + m + 1.  The cache must already hold positions [0, p0 + M) (write
- * them with lla_encode first).
+ * Causal prefill attention at loop l over the latent cache: query m of
+ * sequence b sits at absolute position p0 + m and attends the cached tokens
+ * n <= p0 + m, i.e. row m equals lla_decode_attn with N = p0 + m + 1 (pass 2
+ * of the two-pass decoder of App. A reads the cache this way).  The cache
+ * must already hold positions [0, p0 + M) (write them with lla_encode first);
+ * later slots are not read.
  *
  *   q    [B][H][M][d_head]   loop-l queries
  *   out  [B][H][M][d_head]   of out_dtype
+ *   workspace  device memory of ws_bytes >= lla_prefill_workspace_bytes() for
+ *        these sizes (16-byte aligned, no initial contents needed, overwritten;
+ *        calls sharing it must be ordered on the stream), or NULL with
+ *        ws_bytes == 0 when that size is 0
  *   other arguments as for lla_decode_attn.
  *
  * Requires M >= 1, p0 >= 0, p0 + M <= n_max, and the decode size limits.
- * With dtype LLA_BF16 the contractions run on bf16 MFMA: the absorbed query,
- * the softmax weights and the normalised latent are rounded to bf16 before
- * their products (fp32 accumulation throughout).
- * Errors: LLA_ERR_INVALID_ARG; LLA_ERR_UNSUPPORTED for bf16 with r_k > 95,
- * r_v > 95, d_head > 128 or M > 8388480; LLA_ERR_HIP.
+ * fp32 runs an fp32 scan (one workgroup per query).  bf16 runs one of two
+ * kernels, each with fp32 accumulation:
+ *  - r_k <= 95 and r_v <= 95 (d_head <= 128): the absorbed form of App. J,
+ *    q~ = U_k^T q, s_n = q~ . c_k[n], z = sum_n p_n c_v[n], out = U_v z / l +
+ *    mu_v, with no workspace.  The latent pages and U_v are converted from
+ *    bf16 to fp16 (exact within fp16's range), and q~ * scale * log2(e), the
+ *    softmax weights and z / l are rounded to fp16 before their products.
+ *  - otherwise (d_head = 128, r_k and r_v multiples of 8 up to LLA_MAX_RANK):
+ *    every head's K_l = c_k U_k^T and V_l = c_v U_v^T (Eq. 3) are rebuilt for
+ *    positions [0, p0 + M) on MFMA into the workspace in fp16, then the
+ *    teacher's attention runs over them; q * scale * log2(e) and the softmax
+ *    weights enter its products in fp16.  The workspace holds
+ *    4 * B * H * d_head * (p0 + M rounded up to 64) bytes.
+ * fp16 range: the fp16 operands above (latent and U_v entries, rebuilt K and
+ * V entries, scaled queries q~ or q) and the base-2 logits
+ * scale * log2(e) * q . k (the running row maximum is held in fp16) must stay
+ * below 65504 in magnitude; beyond it the affected outputs are not finite.
+ * Non-finite data: a masked (future) key of a 64-key page enters the value
+ * product with weight 0, and 0 * NaN is NaN, so a non-finite value latent at
+ * position n may also make non-finite the outputs of the queries at positions
+ * 64 * floor(n / 64) - 31 .. n - 1 (at most 95 before it); queries before
+ * those are unaffected.  A non-finite key latent affects only the queries
+ * that attend it.
+ * Errors: LLA_ERR_INVALID_ARG; LLA_ERR_WORKSPACE (missing or too small);
+ * LLA_ERR_UNSUPPORTED for bf16 shapes neither kernel takes, or more than
+ * 65535 query blocks (256 queries) or (b, h) pairs on the rebuild path;
+ * LLA_ERR_HIP.
  */
 lla_status lla_prefill_attn(int dtype, int out_dtype, int B, int H, int M, int d_head, int r_k,
                             int r_v, int n_max, int p0, const void* q, const void* c_k,
                             const void* c_v, const void* u_k, const void* u_v, const void* mu_k,
-                            const void* mu_v, float scale, void* out, void* stream);
+                            const void* mu_v, float scale, void* out, void* workspace,
+                            size_t ws_bytes, void* stream);
+
+/* Workspace bytes lla_prefill_attn needs for these sizes: 0 when the call
+ * takes none (fp32, or bf16 with both ranks <= 95 and d_head <= 128).  Host
+ * only.  Errors: LLA_ERR_INVALID_ARG. */
+lla_status lla_prefill_workspace_bytes(int dtype, int B, int H, int M, int d_head, int r_k, int r_v,
+                                      int p0, size_t* bytes);
 
 /*
  * Loop-l decode with full RoPE, reconstruct-then-attend (Sec. 3 "RoPE and
@@ -337,9 +373,12 @@ lla_status lla_decode_attn_rope(int dtype, int out_dtype, int B, int H, int d_he
                                 size_t ws_bytes, void* stream);
 
 /*
- * lla_prefill_attn with the decoupled rotary branch:
+ * lla_prefill_attn with the decoupled rotary branch (no workspace):
  *   q_rope  [B][H][M][d_rope]  rotary query parts rotated at p0 + m
- * bf16 additionally requires r_k + d_rope <= 95 (else LLA_ERR_UNSUPPORTED).
+ * bf16 runs the absorbed kernel only and requires r_k + d_rope <= 95 and
+ * r_v <= 95 (else LLA_ERR_UNSUPPORTED); the rotary keys and query parts enter
+ * its score product in fp16, under lla_prefill_attn's range and non-finite
+ * rules.
  * Errors: as lla_prefill_attn.
  */
 lla_status lla_prefill_attn_rope(int dtype, int out_dtype, int B, int H, int M, int d_head,
@@ -464,7 +503,9 @@ lla_status lla_prefill_2d_workspace_bytes(int B, int H, int d_head, int n_keys, 
  * the products in fp16 (accumulation in fp32), and the running row maximum of
  * the base-2 logits scale * log2(e) * q.k is held in fp16: |q|, |K| and |V|
  * entries and those logits must stay below 65504 in magnitude, else the output
- * is not finite.
+ * is not finite.  Non-finite latents follow lla_prefill_attn's rule (a value
+ * latent at position n may also reach the queries at positions
+ * 64 * floor(n / 64) - 31 .. n - 1).
  *   q    [B][H][M][d_head]; out [B][H][M][d_head] of out_dtype
  *   c_k, c_v  the 2D caches (layouts above) of capacity n_max, holding latents
  *        at positions 0 .. p0+M-1 (p0 + M <= n_max); later slots are not read

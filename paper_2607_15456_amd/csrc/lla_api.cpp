@@ -487,11 +487,25 @@ lla_status lla_decode_attn_fullrope(int dtype, int out_dtype, int B, int H, int 
 }
 
 namespace {
+// bf16 prefill kernels: the absorbed kernel takes feature tiles up to 96 (one
+// of them carries the running max, one the denominator); larger ranks rebuild
+// each head's K and V (d_head 128, ranks multiples of 8) into the workspace.
+bool prefill_absorbed_ok(int d_head, int r_k, int r_v, int d_rope) {
+  return r_k + d_rope <= 95 && r_v <= 95 && d_head <= 128;
+}
+bool prefill_rebuild_ok(int d_head, int r_k, int r_v, int d_rope) {
+  return d_rope == 0 && d_head == 128 && r_k % 8 == 0 && r_v % 8 == 0;
+}
+size_t prefill_rebuild_bytes(int B, int H, int d_head, int n_keys) {
+  const size_t nk = ((size_t)n_keys + LLA_PAGE_TOKENS - 1) / LLA_PAGE_TOKENS * LLA_PAGE_TOKENS;
+  return 4 * (size_t)B * H * d_head * nk;  // fp16 K and V
+}
+
 lla_status prefill_impl(int dtype, int out_dtype, int B, int H, int M, int d_head, int r_k, int r_v,
                         int d_rope, int H_rope, int n_max, int p0, const void* q,
                         const void* q_rope, const void* c_k, const void* c_v, const void* r_cache,
                         const void* u_k, const void* u_v, const void* mu_k, const void* mu_v,
-                        float scale, void* out, void* stream) {
+                        float scale, void* out, void* workspace, size_t ws_bytes, void* stream) {
   if (!dtype_ok(dtype) || !dtype_ok(out_dtype) || B < 1 || H < 1 || M < 1 || !head_ok(d_head) ||
       !rank_ok(r_k) || !rank_ok(r_v) || !cap_ok(n_max) || p0 < 0 || (int64_t)p0 + M > n_max ||
       !std::isfinite(scale) || !(scale > 0.f))
@@ -505,9 +519,36 @@ lla_status prefill_impl(int dtype, int out_dtype, int B, int H, int M, int d_hea
     return LLA_ERR_INVALID_ARG;
   (void)mu_k;  // q . mu_k is constant over the keys of a query: it cancels in the softmax
   const float qscale = (float)((double)scale * kLog2e);
-  if (dtype == LLA_BF16) {
-    if (r_k + d_rope > 95 || r_v > 95 || d_head > 128 || (M + 127) / 128 > 65535)
+  if ((workspace == nullptr) != (ws_bytes == 0)) return LLA_ERR_WORKSPACE;
+  if (dtype == LLA_BF16 && !prefill_absorbed_ok(d_head, r_k, r_v, d_rope)) {
+    if (!prefill_rebuild_ok(d_head, r_k, r_v, d_rope) || (M + 255) / 256 > 65535 || (int64_t)B * H > 65535)
       return LLA_ERR_UNSUPPORTED;
+    if (!workspace || !aligned16(workspace) || ws_bytes < prefill_rebuild_bytes(B, H, d_head, p0 + M))
+      return LLA_ERR_WORKSPACE;
+    lla::Prefill2dArgs a{};
+    a.out_dtype = out_dtype;
+    a.B = B;
+    a.H = H;
+    a.M = M;
+    a.rk = r_k;
+    a.rv = r_v;
+    a.n_max = n_max;
+    a.p0 = p0;
+    a.nk = (p0 + M + LLA_PAGE_TOKENS - 1) / LLA_PAGE_TOKENS * LLA_PAGE_TOKENS;
+    a.q = q;
+    a.ck = c_k;
+    a.cv = c_v;
+    a.uk = u_k;
+    a.uv = u_v;
+    a.muv = mu_v;
+    a.qscale = qscale;
+    a.out = out;
+    a.kh = workspace;
+    a.vt = static_cast<char*>(workspace) + prefill_rebuild_bytes(B, H, d_head, p0 + M) / 2;
+    return hip_status(lla::launch_prefill_rebuild(a, static_cast<hipStream_t>(stream)));
+  }
+  if (dtype == LLA_BF16) {
+    if ((M + 127) / 128 > 65535) return LLA_ERR_UNSUPPORTED;
     lla::PrefillArgs a{};
     a.out_dtype = out_dtype;
     a.B = B;
@@ -565,12 +606,25 @@ lla_status prefill_impl(int dtype, int out_dtype, int B, int H, int M, int d_hea
 }
 }  // namespace
 
+lla_status lla_prefill_workspace_bytes(int dtype, int B, int H, int M, int d_head, int r_k, int r_v,
+                                      int p0, size_t* bytes) {
+  if (!dtype_ok(dtype) || B < 1 || H < 1 || M < 1 || !head_ok(d_head) || !rank_ok(r_k) ||
+      !rank_ok(r_v) || p0 < 0 || (int64_t)p0 + M > std::numeric_limits<int>::max() || !bytes)
+    return LLA_ERR_INVALID_ARG;
+  *bytes = (dtype == LLA_BF16 && !prefill_absorbed_ok(d_head, r_k, r_v, 0))
+               ? prefill_rebuild_bytes(B, H, d_head, p0 + M)
+               : 0;
+  return LLA_OK;
+}
+
 lla_status lla_prefill_attn(int dtype, int out_dtype, int B, int H, int M, int d_head, int r_k,
                             int r_v, int n_max, int p0, const void* q, const void* c_k,
                             const void* c_v, const void* u_k, const void* u_v, const void* mu_k,
-                            const void* mu_v, float scale, void* out, void* stream) {
+                            const void* mu_v, float scale, void* out, void* workspace,
+                            size_t ws_bytes, void* stream) {
   return prefill_impl(dtype, out_dtype, B, H, M, d_head, r_k, r_v, 0, 1, n_max, p0, q, nullptr,
-                      c_k, c_v, nullptr, u_k, u_v, mu_k, mu_v, scale, out, stream);
+                      c_k, c_v, nullptr, u_k, u_v, mu_k, mu_v, scale, out, workspace, ws_bytes,
+                      stream);
 }
 
 lla_status lla_prefill_attn_rope(int dtype, int out_dtype, int B, int H, int M, int d_head,
@@ -581,7 +635,8 @@ lla_status lla_prefill_attn_rope(int dtype, int out_dtype, int B, int H, int M, 
                                  void* out, void* stream) {
   if (d_rope < 1) return LLA_ERR_INVALID_ARG;
   return prefill_impl(dtype, out_dtype, B, H, M, d_head, r_k, r_v, d_rope, H_rope, n_max, p0, q,
-                      q_rope, c_k, c_v, r_cache, u_k, u_v, mu_k, mu_v, scale, out, stream);
+                      q_rope, c_k, c_v, r_cache, u_k, u_v, mu_k, mu_v, scale, out, nullptr, 0,
+                      stream);
 }
 
 lla_status lla_rope_write(int dtype, int B, int M, int H_rope, int d_rope, const void* k_rope,

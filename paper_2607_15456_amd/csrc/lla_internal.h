@@ -107,8 +107,8 @@ struct Prefill2dArgs {
   int B, H, M, rk, rv, n_max, p0;
   int nk;           // rebuilt keys per sequence: p0 + M rounded up to a page
   const void* q;    // [B][H][M][128]
-  const void* ck;   // [B][n_max][rk] token-major
-  const void* cv;   // [B][n_max/64][rv][64] paged feature-major
+  const void* ck;   // [B][n_max][rk] token-major (per head: [B][H][n_max/64][rk][64])
+  const void* cv;   // [B][n_max/64][rv][64] paged feature-major (per head: [B][H][...])
   const void* uk;   // [H][128][rk]
   const void* uv;   // [H][128][rv]
   const void* muv;  // [H][128] or null
@@ -119,6 +119,10 @@ struct Prefill2dArgs {
 };
 size_t prefill_2d_ws_bytes(int B, int H, int n_keys);  // both rebuilt tensors
 hipError_t launch_prefill_2d(const Prefill2dArgs& a, hipStream_t stream);
+// The same attention over per-head latents (ck, cv paged feature-major per
+// (b, h), ranks multiples of 8 up to 512): each head's K and V rebuilt from
+// its own latents, then flash2d_kernel.
+hipError_t launch_prefill_rebuild(const Prefill2dArgs& a, hipStream_t stream);
 
 // Rotary embedding (half-split) of rows of dr elements.
 struct RopeArgs {

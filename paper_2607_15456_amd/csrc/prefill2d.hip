@@ -70,6 +70,15 @@ __device__ __forceinline__ uint32_t pack2h(float lo, float hi) {
   const _Float16 a = (_Float16)lo, b = (_Float16)hi;
   return uint32_t(__builtin_bit_cast(uint16_t, a)) | (uint32_t(__builtin_bit_cast(uint16_t, b)) << 16);
 }
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+// ds_read_b64_tr_b16: each 16-lane group reads a 16 x 4 block of 16-bit values
+// (lane L: 4 consecutive elements at its address) and lane L receives element
+// L % 4 of the lanes 4 e + L / 4, e = 0..3
+__device__ __forceinline__ uint2 lds_tr16(const bf16_t* p) {
+  return __builtin_bit_cast(uint2,
+                            __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p)));
+}
+
 // max over both halves of the wavefront (lane i and lane i ^ 32)
 __device__ __forceinline__ float half_swap_max(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
@@ -95,38 +104,54 @@ struct IntC {
   static constexpr int value = N;
 };
 
-template <int AXIS, int KS>  // AXIS 0: keys, 1: values; KS = r / 16
+// PH selects the per-head cache (one latent per (b, h); both axes paged
+// feature-major, rank r any multiple of 8, padded to KS*16 with zeros): the
+// workgroup rebuilds the one head h of its (b, h) from one 64-token page of
+// that head's latents.
+//
+// Feature-major pages (per-head caches, and the 2D values) are staged as they
+// are, 16-byte chunks of 8 tokens of one feature, with the chunk index of rows
+// 4k+2, 4k+3 XORed with 4; ds_read_b64_tr_b16 then hands each lane one token's
+// 4 consecutive features, the MFMA operand layout.  Both the staging stores
+// and the transposed reads are free of bank conflicts.  (The 2D keys are
+// token-major already and are staged row by row.)
+template <int AXIS, int KS, bool PH>  // AXIS 0: keys, 1: values; KS = ceil(r / 16)
 __global__ __launch_bounds__(kThreads) void recon2d_kernel(Prefill2dArgs a) {
   constexpr int R = KS * 16;
-  constexpr int CS = R + 8;  // LDS row stride (bf16): 16-byte reads of 16 rows hit distinct banks
-  __shared__ __attribute__((aligned(16))) bf16_t s_c[kRTok * CS];
+  constexpr int TOK = PH ? kPage : kRTok;  // tokens per workgroup
+  constexpr bool FM = PH || AXIS == 1;     // the latents arrive as feature-major pages
+  constexpr int CS = R + 8;  // token-major LDS row stride (bf16): 16-byte reads of 16 rows hit distinct banks
+  constexpr int LDS = FM ? (TOK / kPage) * R * kPage : TOK * CS;
+  __shared__ __attribute__((aligned(16))) bf16_t s_c[LDS];
 
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int col = lane & 31, g = lane >> 5;
-  const int b = blockIdx.y, n0 = blockIdx.x * kRTok;
+  const int b = PH ? blockIdx.y / a.H : blockIdx.y, n0 = blockIdx.x * TOK;
   const int nvalid = a.p0 + a.M;  // tokens that hold latents; the rest are rebuilt as 0
   const int H = a.H;
+  const int rr = PH ? (AXIS == 0 ? a.rk : a.rv) : R;  // the cache's rank (row pitch of its pages)
 
-  // ---- latent tile, token-major, zero past nvalid ----
-  if (AXIS == 0) {
+  // ---- latent tile, zero past nvalid (and past rr) ----
+  if constexpr (!FM) {
     const bf16_t* src = static_cast<const bf16_t*>(a.ck) + (size_t)b * a.n_max * R;
     constexpr int C8 = R / 8;
-    for (int e = tid; e < kRTok * C8; e += kThreads) {
+    for (int e = tid; e < TOK * C8; e += kThreads) {
       const int n = e / C8, c8 = e - n * C8;
       const uint4 v = n0 + n < nvalid ? ld16(src + (size_t)(n0 + n) * R + 8 * c8) : make_uint4(0, 0, 0, 0);
       *reinterpret_cast<uint4*>(&s_c[n * CS + 8 * c8]) = v;
     }
   } else {
-    // values: pages [R][64] feature-major; chunk = 8 tokens of one feature,
-    // transposed into the token-major tile with 2-byte stores
-    const bf16_t* src = static_cast<const bf16_t*>(a.cv) + (size_t)b * a.n_max * R;
-    for (int e = tid; e < kRTok / kPage * R * 8; e += kThreads) {
-      const int pg = e / (R * 8), rem = e - pg * (R * 8), j = rem >> 3, t8 = rem & 7;
-      const int nb = n0 + pg * kPage + 8 * t8;  // first token of the chunk
+    // chunk e: page pg, feature row j, 8-token chunk c (consecutive e are
+    // consecutive 16 bytes of the cache)
+    const size_t cache = PH ? (size_t)blockIdx.y : (size_t)b;
+    const bf16_t* src = static_cast<const bf16_t*>(AXIS == 0 ? a.ck : a.cv) + cache * a.n_max * rr;
+    for (int e = tid; e < TOK / kPage * R * 8; e += kThreads) {
+      const int pg = e / (R * 8), rem = e - pg * (R * 8), j = rem >> 3, c = rem & 7;
+      const int nb = n0 + pg * kPage + 8 * c;  // first token of the chunk
       uint4 v = make_uint4(0, 0, 0, 0);
-      if (nb < nvalid) {
-        v = ld16(src + (size_t)(n0 / kPage + pg) * kPage * R + (size_t)j * kPage + 8 * t8);
+      if (nb < nvalid && j < rr) {
+        v = ld16(src + (size_t)(n0 / kPage + pg) * kPage * rr + (size_t)j * kPage + 8 * c);
         const int nv = nvalid - nb;  // tokens of the chunk that hold latents
         if (nv < 8) {
           auto keep = [nv](int i) { return nv > 2 * i + 1 ? 0xffffffffu : nv > 2 * i ? 0x0000ffffu : 0u; };
@@ -136,21 +161,35 @@ __global__ __launch_bounds__(kThreads) void recon2d_kernel(Prefill2dArgs a) {
           v.w &= keep(3);
         }
       }
-      const bf16_t* h8 = reinterpret_cast<const bf16_t*>(&v);
-      bf16_t* dst = &s_c[(pg * kPage + 8 * t8) * CS + j];
-#pragma unroll
-      for (int e2 = 0; e2 < 8; ++e2) dst[e2 * CS] = h8[e2];
+      *reinterpret_cast<uint4*>(&s_c[(pg * R + j) * kPage + ((c ^ (((j >> 1) & 1) << 2)) << 3)]) = v;
     }
   }
   __syncthreads();
 
+  // The latent operand of K-step s for 32-token tile nt: lane (col, g) gets
+  // features 16 s + 8 g .. + 7 of token 32 nt + col.  Transposed reads: lane
+  // (x16, th) of a 16-lane group addresses feature row 16 s + 8 g + x16 / 4
+  // (+ 4 for the second read) and tokens 16 th + 4 (x16 % 4) .. + 3 of its tile.
+  const int x16 = lane & 15, th = (lane >> 4) & 1, sw1 = (x16 >> 3) & 1;
+  const int troff = (8 * g + (x16 >> 2)) * kPage + ((2 * th + ((x16 & 3) >> 1)) << 3) + 4 * (x16 & 1);
+  auto lat_op = [&](int nt, int s) -> bf16x8 {
+    if constexpr (!FM) {
+      return as_bf16x8(*reinterpret_cast<const uint4*>(&s_c[(32 * nt + col) * CS + 16 * s + 8 * g]));
+    } else {
+      const bf16_t* p = s_c + (nt >> 1) * R * kPage + troff + ((4 * ((nt & 1) ^ sw1)) << 3) + 16 * s * kPage;
+      const uint2 r0 = lds_tr16(p), r1 = lds_tr16(p + 4 * kPage);
+      return as_bf16x8(make_uint4(r0.x, r0.y, r1.x, r1.y));
+    }
+  };
+
   const bf16_t* U = static_cast<const bf16_t*>(AXIS == 0 ? a.uk : a.uv);
-  const int ntile = min(kRTok, a.nk - n0) / 32;  // 32-token tiles of this workgroup inside nk
-  // up-projection rows 32 wave + col of head h as K-step operands
+  const int ntile = min(TOK, a.nk - n0) / 32;  // 32-token tiles of this workgroup inside nk
+  // up-projection rows 32 wave + col of head h as K-step operands (features
+  // past the rank rr are zero)
   auto load_u = [&](int h, uint4 (&u)[KS]) {
-    const bf16_t* row = U + ((size_t)h * kD + 32 * wave + col) * R + 8 * g;
+    const bf16_t* row = U + ((size_t)h * kD + 32 * wave + col) * rr + 8 * g;
 #pragma unroll
-    for (int s = 0; s < KS; ++s) u[s] = ld16(row + 16 * s);
+    for (int s = 0; s < KS; ++s) u[s] = (!PH || 16 * s + 8 * g < rr) ? ld16(row + 16 * s) : make_uint4(0, 0, 0, 0);
   };
   uint4 ua[KS];
   // NT = the workgroup's token tiles, a compile-time count so the product loop
@@ -165,7 +204,7 @@ __global__ __launch_bounds__(kThreads) void recon2d_kernel(Prefill2dArgs a) {
     for (int s = 0; s < KS; ++s) {
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
-        const bf16x8 c = as_bf16x8(*reinterpret_cast<const uint4*>(&s_c[(32 * nt + col) * CS + 16 * s + 8 * g]));
+        const bf16x8 c = lat_op(nt, s);
         acc[nt] = AXIS == 0 ? mfma(as_bf16x8(u[s]), c, acc[nt]) : mfma(c, as_bf16x8(u[s]), acc[nt]);
       }
     }
@@ -198,14 +237,16 @@ __global__ __launch_bounds__(kThreads) void recon2d_kernel(Prefill2dArgs a) {
   };
   // every operand load of a head is issued before its first product, so the
   // products of the early K-steps overlap the later loads
-  for (int h = 0; h < H; ++h) {
+  for (int h = PH ? (int)blockIdx.y % H : 0; h < (PH ? (int)blockIdx.y % H + 1 : H); ++h) {
     load_u(h, ua);
-    switch (ntile) {  // uniform; 2 or 4 (the key count is a multiple of 64)
-      case 4: head(h, ua, IntC<4>{}); break;
-      case 3: head(h, ua, IntC<3>{}); break;
-      case 2: head(h, ua, IntC<2>{}); break;
-      case 1: head(h, ua, IntC<1>{}); break;
-      default: break;
+    if constexpr (TOK == 4 * 32) {
+      switch (ntile) {  // uniform; 2 or 4 (the key count is a multiple of 64)
+        case 4: head(h, ua, IntC<4>{}); break;
+        case 2: head(h, ua, IntC<2>{}); break;
+        default: break;
+      }
+    } else {
+      head(h, ua, IntC<2>{});  // one page: always two tiles
     }
   }
 }
@@ -434,18 +475,20 @@ void flash2d_kernel(Prefill2dArgs a) {
   }
 }
 
-template <int AXIS, int KS>
+template <int AXIS, int KS, bool PH>
 hipError_t launch_recon(const Prefill2dArgs& a, hipStream_t stream) {
-  const dim3 grid((a.nk + kRTok - 1) / kRTok, a.B);
-  hipLaunchKernelGGL((recon2d_kernel<AXIS, KS>), grid, dim3(kThreads), 0, stream, a);
+  constexpr int TOK = PH ? kPage : kRTok;
+  const dim3 grid((a.nk + TOK - 1) / TOK, PH ? a.B * a.H : a.B);
+  hipLaunchKernelGGL((recon2d_kernel<AXIS, KS, PH>), grid, dim3(kThreads), 0, stream, a);
   return hipGetLastError();
 }
 
-template <int AXIS>
+// r: the rank rounded up to a multiple of 16
+template <int AXIS, bool PH>
 hipError_t launch_recon_r(const Prefill2dArgs& a, int r, hipStream_t stream) {
   switch (r / 16) {
 #define LLA_R(ks) \
-  case ks: return launch_recon<AXIS, ks>(a, stream);
+  case ks: return launch_recon<AXIS, ks, PH>(a, stream);
     LLA_R(1) LLA_R(2) LLA_R(3) LLA_R(4) LLA_R(5) LLA_R(6) LLA_R(7) LLA_R(8)
     LLA_R(9) LLA_R(10) LLA_R(11) LLA_R(12) LLA_R(13) LLA_R(14) LLA_R(15) LLA_R(16)
     LLA_R(17) LLA_R(18) LLA_R(19) LLA_R(20) LLA_R(21) LLA_R(22) LLA_R(23) LLA_R(24)
@@ -463,9 +506,19 @@ size_t prefill_2d_ws_bytes(int B, int H, int n_keys) {
 }
 
 hipError_t launch_prefill_2d(const Prefill2dArgs& a, hipStream_t stream) {
-  hipError_t e = launch_recon_r<0>(a, a.rk, stream);
+  hipError_t e = launch_recon_r<0, false>(a, a.rk, stream);
   if (e != hipSuccess) return e;
-  e = launch_recon_r<1>(a, a.rv, stream);
+  e = launch_recon_r<1, false>(a, a.rv, stream);
+  if (e != hipSuccess) return e;
+  const dim3 grid(a.B * a.H, (a.M + kQBlock - 1) / kQBlock);
+  hipLaunchKernelGGL(flash2d_kernel, grid, dim3(kFThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_prefill_rebuild(const Prefill2dArgs& a, hipStream_t stream) {
+  hipError_t e = launch_recon_r<0, true>(a, (a.rk + 15) / 16 * 16, stream);
+  if (e != hipSuccess) return e;
+  e = launch_recon_r<1, true>(a, (a.rv + 15) / 16 * 16, stream);
   if (e != hipSuccess) return e;
   const dim3 grid(a.B * a.H, (a.M + kQBlock - 1) / kQBlock);
   hipLaunchKernelGGL(flash2d_kernel, grid, dim3(kFThreads), 0, stream, a);

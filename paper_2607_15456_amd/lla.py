@@ -42,7 +42,8 @@ _SIGS = {
     "lla_decode_splits": (_c_int, [_c_int] * 5 + [ctypes.POINTER(_c_int)]),
     "lla_decode_attn": (_c_int, [_c_int] * 9 + [_c_vp] * 8 + [_c_f, _c_vp, _c_vp, _c_sz, _c_vp]),
     "lla_decode_attn_noalloc": (_c_int, [_c_int] * 9 + [_c_vp] * 8 + [_c_f, _c_vp, _c_vp]),
-    "lla_prefill_attn": (_c_int, [_c_int] * 10 + [_c_vp] * 7 + [_c_f, _c_vp, _c_vp]),
+    "lla_prefill_attn": (_c_int, [_c_int] * 10 + [_c_vp] * 7 + [_c_f, _c_vp, _c_vp, _c_sz, _c_vp]),
+    "lla_prefill_workspace_bytes": (_c_int, [_c_int] * 8 + [ctypes.POINTER(_c_sz)]),
     "lla_rope_write": (_c_int, [_c_int] * 5 + [_c_vp, ctypes.c_double, _c_vp, _c_int, _c_int, _c_vp]),
     "lla_rope_rotate": (_c_int, [_c_int] * 5 + [_c_vp, _c_vp, _c_int, ctypes.c_double, _c_vp, _c_vp]),
     "lla_decode_attn_rope": (_c_int, [_c_int] * 11 + [_c_vp] * 10 + [_c_f, _c_vp, _c_vp, _c_sz, _c_vp]),
@@ -332,12 +333,23 @@ def _rope_shapes(q_rope, r_cache, dtype, dev, B, H, n_max):
     return H_rope, d_rope
 
 
+def prefill_workspace_bytes(dtype: torch.dtype, B: int, H: int, M: int, d_head: int, r_k: int, r_v: int,
+                            p0: int) -> int:
+    """Workspace lla_prefill_attn needs (0: none; bf16 ranks above 95 rebuild K and V)."""
+    out = _c_sz()
+    _check(lib().lla_prefill_workspace_bytes(LLA_BF16 if dtype == torch.bfloat16 else LLA_F32, B, H, M, d_head,
+                                             r_k, r_v, p0, ctypes.byref(out)))
+    return out.value
+
+
 def prefill_attn(q, c_k, c_v, u_k, u_v, *, p0: int, mu_k=None, mu_v=None, scale: float | None = None,
-                 out=None, out_dtype=torch.float32, q_rope=None, r_cache=None):
+                 out=None, out_dtype=torch.float32, q_rope=None, r_cache=None, workspace=None):
     """Causal loop-l prefill of q [B, H, M, d] at positions p0..p0+M-1 over the paged cache.
 
-    With the rotary branch: q_rope [B, H, M, d_rope] rotated at p0 + m
-    (rope_rotate with pos0=p0) and the rotary cache r_cache (rope_write)."""
+    workspace: uint8 device tensor of at least prefill_workspace_bytes(...)
+    bytes when that is nonzero (allocated here if None).  With the rotary
+    branch: q_rope [B, H, M, d_rope] rotated at p0 + m (rope_rotate with
+    pos0=p0) and the rotary cache r_cache (rope_write)."""
     dev = q.device
     B, H, M, d = q.shape
     for t, n in ((q, "q"), (c_k, "c_k"), (c_v, "c_v"), (u_k, "u_k"), (u_v, "u_v")):
@@ -359,9 +371,17 @@ def prefill_attn(q, c_k, c_v, u_k, u_v, *, p0: int, mu_k=None, mu_v=None, scale:
     if q_rope is None:
         if scale is None:
             scale = 1.0 / math.sqrt(d)
+        if workspace is None:
+            need = prefill_workspace_bytes(q.dtype, B, H, M, d, r_k, r_v, p0)
+            if need:
+                workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+        else:
+            _need(workspace, "workspace", None, dev)
+        ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
         _check(lib().lla_prefill_attn(_dt(q), _out_code(out.dtype), B, H, M, d, r_k, r_v, n_max, p0,
                                       _ptr(q), _ptr(c_k), _ptr(c_v), _ptr(u_k), _ptr(u_v), _ptr(mu_k),
-                                      _ptr(mu_v), float(scale), _ptr(out), _stream(q)))
+                                      _ptr(mu_v), float(scale), _ptr(out), _ptr(workspace), ws_bytes,
+                                      _stream(q)))
         return out
     H_rope, d_rope = _rope_shapes(q_rope, r_cache, q.dtype, dev, B, H, n_max)
     if q_rope.shape != (B, H, M, d_rope):

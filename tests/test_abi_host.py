@@ -31,7 +31,8 @@ def test_header_declares_the_boundary():
     assert names == sorted(["lla_status_string", "lla_abi_version", "lla_rho", "lla_cache_bytes",
                             "lla_encode", "lla_decode_workspace_bytes", "lla_decode_splits", "lla_decode_attn",
                             "lla_decode_attn_noalloc",
-                            "lla_prefill_attn", "lla_rope_write", "lla_rope_rotate",
+                            "lla_prefill_attn", "lla_prefill_workspace_bytes", "lla_rope_write",
+                            "lla_rope_rotate",
                             "lla_decode_attn_rope", "lla_prefill_attn_rope", "lla_encode_ring",
                             "lla_rope_write_ring", "lla_encode_2d", "lla_encode_2d_workspace_bytes",
                             "lla_decode_2d_workspace_bytes", "lla_decode_attn_2d",
@@ -43,7 +44,7 @@ def test_library_exports_every_declared_symbol():
     h = ctypes.CDLL(lla.LIB_PATH)
     for name in _declared():
         assert hasattr(h, name), name
-    assert lla.abi_version() == 8
+    assert lla.abi_version() == 9
 
 
 def test_decode_split_choice():
@@ -193,19 +194,43 @@ def test_encode_rejects(kw):
 
 def _prefill(**kw):
     a = dict(dtype=1, out_dtype=0, B=1, H=16, M=64, d=128, rk=18, rv=30, n_max=512, p0=0, q=P, ck=P, cv=P,
-             uk=P, uv=P, muk=None, muv=None, scale=0.088, out=P, stream=None)
+             uk=P, uv=P, muk=None, muv=None, scale=0.088, out=P, ws=None, ws_bytes=0, stream=None)
     a.update(kw)
     return lla.lib().lla_prefill_attn(a["dtype"], a["out_dtype"], a["B"], a["H"], a["M"], a["d"], a["rk"],
                                       a["rv"], a["n_max"], a["p0"], a["q"], a["ck"], a["cv"], a["uk"],
-                                      a["uv"], a["muk"], a["muv"], a["scale"], a["out"], a["stream"])
+                                      a["uv"], a["muk"], a["muv"], a["scale"], a["out"], a["ws"],
+                                      a["ws_bytes"], a["stream"])
+
+
+REBUILD = dict(rk=96, rv=160)  # the 4x tier: bf16 takes the rebuild path, which needs a workspace
+REBUILD_WS = 4 * 1 * 16 * 128 * 64  # B * H * d_head * (p0 + M rounded up to 64) * 2 tensors * 2 bytes
 
 
 @pytest.mark.parametrize("kw,code", [
     (dict(M=0), 1), (dict(p0=-1), 1), (dict(p0=449), 1), (dict(d=40), 1), (dict(q=MIS), 1),
     (dict(scale=-1.0), 1), (dict(rk=96), 2), (dict(rv=96), 2), (dict(d=256), 2),
+    (dict(REBUILD), 3), (dict(REBUILD, ws=P, ws_bytes=REBUILD_WS - 16), 3), (dict(REBUILD, ws=MIS, ws_bytes=1 << 30), 3),
+    (dict(REBUILD, ws=P, ws_bytes=0), 3), (dict(rk=100, rv=160, ws=P, ws_bytes=1 << 30), 2),
+    (dict(REBUILD, d=64, ws=P, ws_bytes=1 << 30), 2), (dict(ws=None, ws_bytes=16), 3),
 ])
 def test_prefill_rejects(kw, code):
     assert _prefill(**kw) == code
+
+
+def test_prefill_workspace_bytes():
+    assert lla.prefill_workspace_bytes(torch_bf16(), 1, 16, 64, 128, 96, 160, 0) == REBUILD_WS
+    assert lla.prefill_workspace_bytes(torch_bf16(), 4, 16, 8192, 128, 288, 480, 0) == 4 * 4 * 16 * 128 * 8192
+    assert lla.prefill_workspace_bytes(torch_bf16(), 2, 3, 100, 128, 96, 160, 5) == 4 * 2 * 3 * 128 * 128
+    assert lla.prefill_workspace_bytes(torch_bf16(), 4, 16, 8192, 128, 18, 30, 0) == 0   # absorbed kernel
+    import torch
+    assert lla.prefill_workspace_bytes(torch.float32, 1, 16, 64, 128, 96, 160, 0) == 0   # fp32 scan
+    with pytest.raises(lla.LLAError):
+        lla.prefill_workspace_bytes(torch_bf16(), 1, 16, 0, 128, 96, 160, 0)
+
+
+def torch_bf16():
+    import torch
+    return torch.bfloat16
 
 
 # ---- the decoupled rotary branch ----

@@ -145,3 +145,89 @@ def test_full_prefill_write():
             plain = np.stack([oracle.decode_attn(q64[b, h, i], lat_k[b, h, :rows[i] + 1], lat_v[b, h, :rows[i] + 1],
                                                  uk64[h], uv64[h]) for i in idx])
             assert_close(o[b, h, idx], plain, torch.bfloat16, f"loop {loop} unit ({b},{h}) plain definition")
+
+
+# ---------------------------------------------------------------------------
+# bf16 at the paper's per-head rank tiers (tab:tier4, ranks above the absorbed
+# kernel's 95): each head's K_l and V_l are rebuilt (Eq. 3) into the
+# workspace, then attended.  Rows are checked against the absorbed oracle
+# (App. J; pinned against the plain definition), and a sample against the
+# plain definition (K and V rebuilt once, the teacher's attention per row).
+# ---------------------------------------------------------------------------
+
+def _rows_absorbed(q, ck, cv, uk, uv, muk, muv, p0, scale=None, rows=None):
+    q64, k64, v64, uk64, uv64 = f64(q), f64(ck), f64(cv), f64(uk), f64(uv)
+    mk = None if muk is None else f64(muk)
+    mv = None if muv is None else f64(muv)
+    B, H, M, _ = q64.shape
+    rows = range(M) if rows is None else rows
+    return np.stack([np.stack([np.stack([
+        oracle.decode_attn_absorbed(q64[b, h, m], k64[b, h, :p0 + m + 1], v64[b, h, :p0 + m + 1], uk64[h], uv64[h],
+                                    None if mk is None else mk[h], None if mv is None else mv[h], scale)
+        for m in rows]) for h in range(H)]) for b in range(B)])
+
+
+TIERS = [(96, 160), (120, 200), (144, 240), (192, 320), (240, 400), (288, 480)]
+
+
+@pytest.mark.parametrize("r_k,r_v", TIERS + [(512, 512), (8, 504), (128, 96)])
+@pytest.mark.parametrize("M,p0", [(1, 0), (37, 0), (130, 5), (300, 64), (257, 200)])
+def test_bf16_prefill_tier_ranks(r_k, r_v, M, p0):
+    log(f"prefill bf16 rebuild r=({r_k},{r_v}) M={M} p0={p0}")
+    assert lla.prefill_workspace_bytes(torch.bfloat16, 2, SMALL.H, M, 128, r_k, r_v, p0) > 0
+    q, ck, cv, uk, uv, muk, muv, pk, pv = _case(SMALL, r_k, r_v, 2, M, p0, torch.bfloat16)
+    out = lla.prefill_attn(q, pk, pv, uk, uv, p0=p0, mu_k=muk, mu_v=muv)
+    torch.cuda.synchronize()
+    assert_close(f64(out), _rows_absorbed(q, ck, cv, uk, uv, muk, muv, p0), torch.bfloat16, "prefill rebuild")
+
+
+def test_bf16_prefill_tier_plain_definition_bf16_out_and_scale():
+    r_k, r_v, M, p0 = 192, 320, 200, 33
+    q, ck, cv, uk, uv, muk, muv, pk, pv = _case(SMALL, r_k, r_v, 2, M, p0, torch.bfloat16, means=False)
+    ws = torch.empty(lla.prefill_workspace_bytes(torch.bfloat16, 2, SMALL.H, M, 128, r_k, r_v, p0),
+                     dtype=torch.uint8, device=DEV)
+    for scale, out_dtype in ((None, torch.float32), (0.2, torch.bfloat16)):
+        out = lla.prefill_attn(q, pk, pv, uk, uv, p0=p0, scale=scale, out_dtype=out_dtype, workspace=ws)
+        torch.cuda.synchronize()
+        ref = np.stack([oracle.prefill_attn_2d(f64(q)[b, h:h + 1], f64(ck)[b, h], f64(cv)[b, h], f64(uk)[h:h + 1],
+                                               f64(uv)[h:h + 1], scale=scale, p0=p0)[0]
+                        for b in range(2) for h in range(SMALL.H)]).reshape(2, SMALL.H, M, 128)
+        assert_close(f64(out), ref, torch.bfloat16, f"plain definition scale={scale}",
+                     out_bf16=out_dtype == torch.bfloat16)
+
+
+@pytest.mark.parametrize("qmul,kramp", [(4.0, 0.0), (1.0, 6.0)])
+def test_bf16_prefill_tier_peaked_and_rising(qmul, kramp):
+    q, ck, cv, uk, uv, muk, muv, pk, pv = _case(SMALL, 96, 160, 2, 600, 0, torch.bfloat16, qmul=qmul, kramp=kramp)
+    out = lla.prefill_attn(q, pk, pv, uk, uv, p0=0, mu_k=muk, mu_v=muv)
+    torch.cuda.synchronize()
+    assert_close(f64(out), _rows_absorbed(q, ck, cv, uk, uv, muk, muv, 0), torch.bfloat16,
+                 f"q x{qmul} ramp {kramp}")
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("r_k,r_v", [(96, 160), (288, 480)])
+def test_full_prefill_tier(r_k, r_v):
+    """4 x 8192 new tokens, 16 heads, at the 4x and 1.33x tiers: every (b, h) at
+    the first and last row of every 256-query block."""
+    wl = W.WORKLOADS["prefill_write"]
+    B, M, H = wl.B, wl.N, wl.H
+    log(f"full-size rebuild prefill r=({r_k},{r_v})")
+    ck = lla.to_paged(W.latents(wl, r_k, "k", 0, device=DEV), M)
+    cv = lla.to_paged(W.latents(wl, r_v, "v", 0, device=DEV), M)
+    q = W.queries(wl, 0, 1, M=M, device=DEV)
+    uk, uv, _, _ = W.codec_loop(wl, r_k, r_v, 0, 1, DEV)
+    out = lla.prefill_attn(q, ck, cv, uk, uv, p0=0)
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(out).all())
+    rows = sorted({256 * qb + e for qb in range(M // 256) for e in (0, 255)})
+    o = f64_dev(out[:, :, rows])
+    q64, uk64, uv64 = f64_dev(q[:, :, rows]), f64(uk), f64(uv)
+    ref = np.empty_like(o)
+    for b in range(B):
+        k64 = f64_dev(lla.from_paged(ck[b:b + 1]))[0]
+        v64 = f64_dev(lla.from_paged(cv[b:b + 1]))[0]
+        for h in range(H):
+            for i, m in enumerate(rows):
+                ref[b, h, i] = oracle.decode_attn_absorbed(q64[b, h, i], k64[h, :m + 1], v64[h, :m + 1], uk64[h], uv64[h])
+    assert_units_close(o, ref, f"every (b, h) at {len(rows)} rows")
