@@ -43,6 +43,7 @@ FETCH_SCALE, WRITE_SCALE = 2.000, 1.000
 MEASURED_TRAFFIC = {
     ("ouro14b_decode", 192, 320, "absorbed"): {"fetch_kib": 1057151.66, "write_kib": 256.0},
     ("ouro14b_decode", 192, 320, "fullrope"): {"fetch_kib": 1079769.56, "write_kib": 256.0},
+    ("ouro26b_long", 36, 60, "absorbed"): {"fetch_kib": 788406.95, "write_kib": 128.0},
 }
 
 
@@ -105,6 +106,18 @@ class KernelTimer:
 
     def mean_ms(self):
         return sum(a.elapsed_time(b) for a, b in self.pairs) / max(1, len(self.pairs))
+
+
+def cpu_model():
+    """The host CPU's model name (/proc/cpuinfo), for the CPU baseline record."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def cpu_threads():
@@ -301,7 +314,7 @@ def cpu_baseline_decode(wl, r_k, r_v, caches, loops, torch, budget_s=15.0, fullr
         units += 1
     per_unit = t / units
     step_s = per_unit * wl.B * wl.H * wl.T * wl.layers
-    return dict(value=wl.B / step_s, unit="tokens/s", cores=cpu_threads(), kind="oracle",
+    return dict(value=wl.B / step_s, unit="tokens/s", cores=cpu_threads(), cpu_model=cpu_model(), kind="oracle",
                 sample=(f"oracle.{'decode_attn_fullrope' if fullrope else 'decode_attn'} (float64, "
                         f"reconstruct-then-attend) on the first {units} "
                         f"(loop, layer, b, h) units of the step, {t:.1f} s of CPU time; per-unit time "
@@ -352,7 +365,7 @@ def cpu_baseline_prefill(wl, r_k, r_v, tensors, torch, budget_s=15.0):
     oracle.encode_batched(xv64, None, wv64)
     enc_t = time.perf_counter() - t0
     step_s = rows_t / nrows * B * H * M * T + enc_t / toks * B * M
-    return dict(value=B * M / step_s, unit="tokens/s", cores=cpu_threads(), kind="oracle",
+    return dict(value=B * M / step_s, unit="tokens/s", cores=cpu_threads(), cpu_model=cpu_model(), kind="oracle",
                 sample=(f"oracle.prefill_attn (float64, plain definition per row) on {nrows} query rows "
                         f"of the first {nunits} (loop, b, h) units, each unit's rows in random order, "
                         f"{rows_t:.1f} s; mean row time "
@@ -686,7 +699,7 @@ def cpu_baseline_prefill_2d(wl, r_k, r_v, ck, cv, loops, torch, budget_s=15.0):
         spent += time.perf_counter() - t0
         nrows += 1
     step_s = spent / nrows * B * M * T
-    return dict(value=B * M / step_s, unit="tokens/s", cores=cpu_threads(), kind="oracle",
+    return dict(value=B * M / step_s, unit="tokens/s", cores=cpu_threads(), cpu_model=cpu_model(), kind="oracle",
                 sample=(f"oracle.prefill_attn_2d (float64, plain definition) on {nrows} query rows of "
                         f"sequence 0 at loop 0 (all {wl.H} heads, rows at random positions), "
                         f"{spent:.1f} s of CPU time; per-row time x {B * M} rows x {T} loops; the 2D encode "
