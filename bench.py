@@ -42,7 +42,7 @@ BF16_PEAK_TFLOPS = 2516.6  # 256 CU x 2.4 GHz x 4096 flop/clk, dense
 FETCH_SCALE, WRITE_SCALE = 2.000, 1.000
 MEASURED_TRAFFIC = {
     ("ouro14b_decode", 192, 320, "absorbed"): {"fetch_kib": 1057151.66, "write_kib": 256.0},
-    ("ouro14b_decode", 192, 320, "fullrope"): {"fetch_kib": 1079769.56, "write_kib": 256.0},
+    ("ouro14b_decode", 192, 320, "fullrope"): {"fetch_kib": 1057024.41, "write_kib": 256.0},
     ("ouro26b_long", 36, 60, "absorbed"): {"fetch_kib": 788406.95, "write_kib": 128.0},
 }
 

@@ -217,12 +217,18 @@ void fullrope_mfma_kernel(FullRopeArgs a) {
   // needed before the next page's loads are issued.
   // Every lane issues every load (instructions wholly past r_k re-read the
   // last rows), so the compiler's waits count loads exactly.
+  // A prefetch of a page past the range (p >= pe, uniform) takes a vector
+  // offset at the end of the (b, h) buffer: the raw buffer load is out of
+  // range, returns zeros and reads no memory, and still counts as a load for
+  // the wait counters.  Those registers are never consumed.
+  const int k_oob = a.n_max * rk * 2, v_oob = a.n_max * rv * 2;
   auto kload = [&](uint4 (&kr)[KD], int p) {
+    const bool past = p >= pe;
 #pragma unroll
     for (int u = 0; u < KD; ++u) {
       const int k8 = min(8 * (wave + kFrWaves * u), (rk - 1) & ~7);  // first row of the instruction
       const int voff = (min(k8 + krow, rk - 1) - k8) * (kPage * 2) + (lane & 7) * 16;
-      kr[u] = buf_ld16(ksrc, voff, p * kpage + k8 * kPage * 2);
+      kr[u] = buf_ld16(ksrc, past ? k_oob : voff, past ? 0 : p * kpage + k8 * kPage * 2);
     }
   };
   auto kstore = [&](const uint4 (&kr)[KD], int slot) {
@@ -238,11 +244,12 @@ void fullrope_mfma_kernel(FullRopeArgs a) {
   // A lane whose row is past r_v reads row r_v - 1 (never used); every lane
   // issues every load, as for the keys.
   auto vload = [&](uint4 (&vr)[VR], int p) {
+    const bool past = p >= pe;
 #pragma unroll
     for (int k = 0; k < VR; ++k) {
       const int j0 = min(vrow0 + 8 * k, rv - 1);
       const int voff = (min(vrow0 + 8 * k + hi, rv - 1) - j0) * (kPage * 2) + lo * 16;
-      vr[k] = buf_ld16(vsrc, voff, p * vpage + j0 * kPage * 2);
+      vr[k] = buf_ld16(vsrc, past ? v_oob : voff, past ? 0 : p * vpage + j0 * kPage * 2);
     }
   };
 
@@ -296,13 +303,14 @@ void fullrope_mfma_kernel(FullRopeArgs a) {
   // page p + 3's are requested, the values are multiplied and page p + 1's
   // requested -- all before this page's products, so two pages of keys and of
   // values stay in flight while the wavefront computes.  Past the last page
-  // the loads re-read it: every load is issued, so the waits count exactly.
+  // the loads are issued out of range (zeros, no memory read): every load is
+  // issued, so the waits count exactly.
   auto body = [&](int i, uint4 (&kr)[KD], uint4 (&vr)[VR]) {
     const int p = pb + i, slot = i & 1;
     kstore(kr, slot ^ 1);
-    kload(kr, min(p + 3, pe - 1));
+    kload(kr, p + 3);
     if (i > 0) vconsume(vr, p - 1);
-    vload(vr, min(p + 1, pe - 1));
+    vload(vr, p + 1);
     // ---- rotated query of this wavefront's token tile ----
     {
       float c, sn;
@@ -396,7 +404,7 @@ void fullrope_mfma_kernel(FullRopeArgs a) {
   // staged, so their latency overlaps the staging.
   if (pb < pe) {
     kload(kA, pb);
-    kload(kB, min(pb + 1, pe - 1));
+    kload(kB, pb + 1);
     vload(vA, pb);
   }
   // ---- U_k of head h into LDS (rows = features of K, columns past r_k zero) ----
@@ -433,7 +441,7 @@ void fullrope_mfma_kernel(FullRopeArgs a) {
   }
   if (pb < pe) {
     kstore(kA, 0);
-    kload(kA, min(pb + 2, pe - 1));
+    kload(kA, pb + 2);
   }
   __syncthreads();
   const int npg = pe - pb;
