@@ -641,8 +641,10 @@ hipError_t launch_encode(const EncodeArgs& a, hipStream_t stream) {
         hipLaunchKernelGGL((encode_stream_kernel<8>), grid, dim3(256), 0, stream, a, bpw);
       return hipGetLastError();
     }
-    if (TT >= kGTok && a.K >= 2048 && a.K % kGKC == 0) {
-      // prefill-sized write over a long stack (the LLA-2D down-projection): a compute-bound GEMM
+    if (TT >= kGTok && a.K % kGKC == 0 && (a.K >= 2048 || rmax > 64)) {
+      // prefill-sized write over a long stack (the LLA-2D down-projection), or
+      // at ranks above the streaming kernel's (the per-head tiers): a GEMM
+      // tiled for the MFMAs, x re-read from L2 per row block
       const int ntb = (TT + kGTok - 1) / kGTok, ntb8 = (ntb + 7) / 8 * 8;
       const int nrb_k = (a.r[0] + kGRow - 1) / kGRow, nrb = nrb_k + (a.r[1] + kGRow - 1) / kGRow;
       hipLaunchKernelGGL(encode_gemm_kernel, dim3(nrb * ntb8, a.H), dim3(kGThreads), 0, stream, a, nrb_k, nrb, ntb);

@@ -134,3 +134,20 @@ def test_encode_many_tokens(r_k, r_v, T, d, B, M, pos0):
     log(f"encode many tokens r=({r_k},{r_v}) K={T * d} B={B} M={M} pos0={pos0}")
     inputs, ck, cv = _run(wl, r_k, r_v, B, M, pos0, n_max, True, torch.bfloat16)
     _check(wl, inputs, ck, cv, pos0, M, torch.bfloat16, f"M={M}")
+
+
+@pytest.mark.parametrize("r_k,r_v,T,d,B,M,pos0", [
+    (96, 160, 4, 128, 2, 300, 5),      # the 4x tier, K = 512, ragged token block
+    (288, 480, 4, 128, 1, 1000, 64),   # the 1.33x tier
+    (120, 200, 4, 128, 3, 257, 0),     # row blocks of 96 with ragged ends
+    (96, 160, 2, 128, 1, 513, 7),      # K = 256
+    (200, 8, 4, 96, 2, 400, 0),        # K = 384, one rank above 64
+])
+@pytest.mark.parametrize("means", [False, True])
+def test_encode_many_tokens_tier_ranks(r_k, r_v, T, d, B, M, pos0, means):
+    """Prompt-sized writes at the paper's per-head rank tiers: the MFMA GEMM path."""
+    wl = W.Workload(f"enc_tier_{T}_{d}", 1, 4, d, T, B, 0, ((r_k, r_v),), torch.bfloat16)
+    n_max = ((pos0 + M + 63) // 64) * 64 + 64
+    log(f"encode tier ranks r=({r_k},{r_v}) K={T * d} B={B} M={M} pos0={pos0} means={means}")
+    inputs, ck, cv = _run(wl, r_k, r_v, B, M, pos0, n_max, means, torch.bfloat16)
+    _check(wl, inputs, ck, cv, pos0, M, torch.bfloat16, f"M={M}")
