@@ -480,7 +480,8 @@ def run_prefill(args, torch, lla, W):
                      "kernel": ("recon2d_kernel (K, V rebuilt per head) + flash2d_kernel (lla_prefill_attn, "
                                 "rebuild path; flops counted as rebuild + 4 d per causal pair)" if rebuild
                                 else "prefill_bf16_kernel (lla_prefill_attn)"), "flops_per_launch": fl,
-                     "avg_launch_ms": round(pre_ms, 5)},
+                     "avg_launch_ms": round(pre_ms, 5),
+                     "target_frac": 0.5, "target_met": tflops / BF16_PEAK_TFLOPS >= 0.5},
         "encode": {"bound": "hbm", "achieved": round(eb / (enc_ms * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS,
                    "unit": "GB/s", "frac": round(eb / (enc_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                    "bytes_per_launch": eb, "avg_launch_ms": round(enc_ms, 5)},
@@ -871,6 +872,7 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "target_frac": 0.7, "target_met": achieved / HBM_PEAK_GBS >= 0.7,
             "traffic": traffic,
             "traffic_unit": "HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, calibrated)",
             "kernel": ("fullrope_mfma_kernel (lla_decode_attn_fullrope)" if args.fullrope

@@ -801,8 +801,8 @@ lla_status lla_prefill_attn_2d(int dtype, int out_dtype, int B, int H, int M, in
       !std::isfinite(scale) || !(scale > 0.f))
     return LLA_ERR_INVALID_ARG;
   // launch limits: the rebuild grid's y dimension is B, the attention grid's
-  // y dimension the number of 128-query blocks
-  if ((int64_t)B * H * M > (1 << 30) || B > 65535 || (M + 127) / 128 > 65535) return LLA_ERR_INVALID_ARG;
+  // y dimension the number of 256-query blocks
+  if ((int64_t)B * H * M > (1 << 30) || B > 65535 || (M + 255) / 256 > 65535) return LLA_ERR_INVALID_ARG;
   if (!ptr_ok(q) || !ptr_ok(c_k) || !ptr_ok(c_v) || !ptr_ok(u_k) || !ptr_ok(u_v) || !ptr_ok(out) ||
       !opt_ptr_ok(mu_k) || !opt_ptr_ok(mu_v))
     return LLA_ERR_INVALID_ARG;
