@@ -199,6 +199,50 @@ def test_split_k_long_context(dtype, N, splits):
 
 
 # ---------------------------------------------------------------------------
+# Properties of the launch shape: the same sequences give the same outputs
+# (up to the order of the fp32 sums) whether their contexts are split across
+# workgroups of 8 wavefronts or scanned whole by workgroups of 4; other head
+# widths.
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_independent_of_split_count_and_workgroup_size(dtype):
+    H, N = 16, 8192
+    r_k, r_v = (96, 160) if dtype == torch.float32 else (36, 60)
+    wl = W.Workload("shape_prop", 1, H, 128, 4, 2, N, ((r_k, r_v),), dtype)
+    ck, cv, q, uk, uv, muk, muv, pk, pv = _case(wl, r_k, r_v, 2, N, N, 0, 3, True, dtype)
+    big_b = 64  # 1024 (b, h) units: every compute unit busy without splitting
+    assert lla.decode_splits(dtype, 2, H, N) > 1 and lla.decode_splits(dtype, big_b, H, N) == 1
+    pk_big = torch.zeros((big_b,) + tuple(pk.shape[1:]), dtype=dtype, device=DEV)
+    pv_big = torch.zeros((big_b,) + tuple(pv.shape[1:]), dtype=dtype, device=DEV)
+    q_big = torch.zeros((big_b,) + tuple(q.shape[1:]), dtype=dtype, device=DEV)
+    pk_big[:2], pv_big[:2], q_big[:2] = pk, pv, q
+    small = lla.decode_attn(q, pk, pv, uk, uv, n_ctx=N, mu_k=muk, mu_v=muv, workspace=lla.new_workspace(2, H, r_v, N))
+    big = lla.decode_attn(q_big, pk_big, pv_big, uk, uv, n_ctx=N, mu_k=muk, mu_v=muv,
+                          workspace=lla.new_workspace(big_b, H, r_v, N))
+    unsplit = lla.decode_attn(q, pk, pv, uk, uv, n_ctx=N, mu_k=muk, mu_v=muv)  # no workspace: one workgroup per (b, h)
+    torch.cuda.synchronize()
+    a, b, c = f64(small), f64(big[:2]), f64(unsplit)
+    for other, what in ((b, "4-wave workgroups, not split"), (c, "8-wave workgroups, not split")):
+        rel = np.linalg.norm(a - other) / np.linalg.norm(a)
+        log(f"  split vs {what}: rel diff {rel:.2e}")
+        assert rel < 1e-6  # measured about 2e-8
+    assert_close(a, _oracle(q, ck, cv, uk, uv, muk, muv), dtype, "split")
+
+
+@pytest.mark.parametrize("d", [32, 64, 96, 256])
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_other_head_widths(d, dtype):
+    wl = W.Workload(f"dec_d{d}", 1, 4, d, 4, 3, 0, ((36, 60),), dtype)
+    N = 700
+    ck, cv, q, uk, uv, muk, muv, pk, pv = _case(wl, 36, 60, 3, N, 768, 0, 1, True, dtype)
+    for w in (None, lla.new_workspace(3, 4, 60, N)):
+        out = lla.decode_attn(q, pk, pv, uk, uv, n_ctx=N, mu_k=muk, mu_v=muv, workspace=w)
+        torch.cuda.synchronize()
+        assert_close(f64(out), _oracle(q, ck, cv, uk, uv, muk, muv), dtype, f"d_head={d}")
+
+
+# ---------------------------------------------------------------------------
 # Full-size workloads, in the launch configuration the benchmark times
 # (default split heuristic with a workspace).  Every (b, h) unit is checked
 # against the absorbed oracle (App. J; pinned against the plain definition

@@ -231,3 +231,12 @@ def test_full_prefill_tier(r_k, r_v):
             for i, m in enumerate(rows):
                 ref[b, h, i] = oracle.decode_attn_absorbed(q64[b, h, i], k64[h, :m + 1], v64[h, :m + 1], uk64[h], uv64[h])
     assert_units_close(o, ref, f"every (b, h) at {len(rows)} rows")
+
+
+@pytest.mark.parametrize("d", [32, 64, 96])
+def test_bf16_prefill_other_head_widths(d):
+    wl = W.Workload(f"pf_d{d}", 1, 3, d, 4, 2, 0, ((18, 30),), torch.bfloat16)
+    q, ck, cv, uk, uv, muk, muv, pk, pv = _case(wl, 18, 30, 2, 150, 7, torch.bfloat16)
+    out = lla.prefill_attn(q, pk, pv, uk, uv, p0=7, mu_k=muk, mu_v=muv)
+    torch.cuda.synchronize()
+    assert_close(f64(out), _oracle(q, ck, cv, uk, uv, muk, muv, 7), torch.bfloat16, f"d_head={d}")
