@@ -104,22 +104,17 @@ struct IntC {
   static constexpr int value = N;
 };
 
-// PH selects the per-head cache (one latent per (b, h); both axes paged
-// feature-major, rank r any multiple of 8, padded to KS*16 with zeros): the
-// workgroup rebuilds the one head h of its (b, h) from one 64-token page of
-// that head's latents.
-//
-// Feature-major pages (per-head caches, and the 2D values) are staged as they
-// are, 16-byte chunks of 8 tokens of one feature, with the chunk index of rows
-// 4k+2, 4k+3 XORed with 4; ds_read_b64_tr_b16 then hands each lane one token's
-// 4 consecutive features, the MFMA operand layout.  Both the staging stores
-// and the transposed reads are free of bank conflicts.  (The 2D keys are
+// Feature-major pages (the values; the per-head caches below) are staged as
+// they are, 16-byte chunks of 8 tokens of one feature, with the chunk index of
+// rows 4k+2, 4k+3 XORed with 4; ds_read_b64_tr_b16 then hands each lane one
+// token's 4 consecutive features, the MFMA operand layout.  Both the staging
+// stores and the transposed reads are free of bank conflicts.  (The keys are
 // token-major already and are staged row by row.)
-template <int AXIS, int KS, bool PH>  // AXIS 0: keys, 1: values; KS = ceil(r / 16)
+template <int AXIS, int KS>  // AXIS 0: keys, 1: values; KS = r / 16
 __global__ __launch_bounds__(kThreads) void recon2d_kernel(Prefill2dArgs a) {
   constexpr int R = KS * 16;
-  constexpr int TOK = PH ? kPage : kRTok;  // tokens per workgroup
-  constexpr bool FM = PH || AXIS == 1;     // the latents arrive as feature-major pages
+  constexpr int TOK = kRTok;           // tokens per workgroup
+  constexpr bool FM = AXIS == 1;       // the latents arrive as feature-major pages
   constexpr int CS = R + 8;  // token-major LDS row stride (bf16): 16-byte reads of 16 rows hit distinct banks
   constexpr int LDS = FM ? (TOK / kPage) * R * kPage : TOK * CS;
   __shared__ __attribute__((aligned(16))) bf16_t s_c[LDS];
@@ -127,10 +122,10 @@ __global__ __launch_bounds__(kThreads) void recon2d_kernel(Prefill2dArgs a) {
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int col = lane & 31, g = lane >> 5;
-  const int b = PH ? blockIdx.y / a.H : blockIdx.y, n0 = blockIdx.x * TOK;
+  const int b = blockIdx.y, n0 = blockIdx.x * TOK;
   const int nvalid = a.p0 + a.M;  // tokens that hold latents; the rest are rebuilt as 0
   const int H = a.H;
-  const int rr = PH ? (AXIS == 0 ? a.rk : a.rv) : R;  // the cache's rank (row pitch of its pages)
+  constexpr int rr = R;  // the cache's rank (row pitch of its pages)
 
   // ---- latent tile, zero past nvalid (and past rr) ----
   if constexpr (!FM) {
@@ -144,8 +139,7 @@ __global__ __launch_bounds__(kThreads) void recon2d_kernel(Prefill2dArgs a) {
   } else {
     // chunk e: page pg, feature row j, 8-token chunk c (consecutive e are
     // consecutive 16 bytes of the cache)
-    const size_t cache = PH ? (size_t)blockIdx.y : (size_t)b;
-    const bf16_t* src = static_cast<const bf16_t*>(AXIS == 0 ? a.ck : a.cv) + cache * a.n_max * rr;
+    const bf16_t* src = static_cast<const bf16_t*>(a.cv) + (size_t)b * a.n_max * rr;
     for (int e = tid; e < TOK / kPage * R * 8; e += kThreads) {
       const int pg = e / (R * 8), rem = e - pg * (R * 8), j = rem >> 3, c = rem & 7;
       const int nb = n0 + pg * kPage + 8 * c;  // first token of the chunk
@@ -184,12 +178,11 @@ __global__ __launch_bounds__(kThreads) void recon2d_kernel(Prefill2dArgs a) {
 
   const bf16_t* U = static_cast<const bf16_t*>(AXIS == 0 ? a.uk : a.uv);
   const int ntile = min(TOK, a.nk - n0) / 32;  // 32-token tiles of this workgroup inside nk
-  // up-projection rows 32 wave + col of head h as K-step operands (features
-  // past the rank rr are zero)
+  // up-projection rows 32 wave + col of head h as K-step operands
   auto load_u = [&](int h, uint4 (&u)[KS]) {
-    const bf16_t* row = U + ((size_t)h * kD + 32 * wave + col) * rr + 8 * g;
+    const bf16_t* row = U + ((size_t)h * kD + 32 * wave + col) * R + 8 * g;
 #pragma unroll
-    for (int s = 0; s < KS; ++s) u[s] = (!PH || 16 * s + 8 * g < rr) ? ld16(row + 16 * s) : make_uint4(0, 0, 0, 0);
+    for (int s = 0; s < KS; ++s) u[s] = ld16(row + 16 * s);
   };
   uint4 ua[KS];
   // NT = the workgroup's token tiles, a compile-time count so the product loop
@@ -237,17 +230,123 @@ __global__ __launch_bounds__(kThreads) void recon2d_kernel(Prefill2dArgs a) {
   };
   // every operand load of a head is issued before its first product, so the
   // products of the early K-steps overlap the later loads
-  for (int h = PH ? (int)blockIdx.y % H : 0; h < (PH ? (int)blockIdx.y % H + 1 : H); ++h) {
+  for (int h = 0; h < H; ++h) {
     load_u(h, ua);
-    if constexpr (TOK == 4 * 32) {
-      switch (ntile) {  // uniform; 2 or 4 (the key count is a multiple of 64)
-        case 4: head(h, ua, IntC<4>{}); break;
-        case 2: head(h, ua, IntC<2>{}); break;
-        default: break;
-      }
-    } else {
-      head(h, ua, IntC<2>{});  // one page: always two tiles
+    switch (ntile) {  // uniform; 2 or 4 (the key count is a multiple of 64)
+      case 4: head(h, ua, IntC<4>{}); break;
+      case 2: head(h, ua, IntC<2>{}); break;
+      default: break;
     }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Per-head rebuild over a run of pages.  One workgroup = one (b, h) and up to
+// `ppw` consecutive 64-token pages: the head's up-projection rows are loaded
+// into registers once, and while one page's products run from LDS the next
+// page's latents are already in flight into registers.  Staging, operand
+// reads (ds_read_b64_tr_b16) and outputs are those of the per-head
+// recon2d_kernel above.
+// ---------------------------------------------------------------------------
+template <int AXIS, int KS>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
+void recon_ph_kernel(Prefill2dArgs a, int ppw) {
+  constexpr int R = KS * 16;
+  constexpr int CPT = (R * 8 + kThreads - 1) / kThreads;  // 16-byte chunks of a page per thread
+  __shared__ __attribute__((aligned(16))) bf16_t s_c[R * kPage];
+
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int col = lane & 31, g = lane >> 5;
+  const int bh = blockIdx.y, h = bh % a.H;
+  const int nvalid = a.p0 + a.M;
+  const int rr = AXIS == 0 ? a.rk : a.rv;
+  const int pg0 = blockIdx.x * ppw, pg1 = min(pg0 + ppw, a.nk / kPage);
+  const bf16_t* src = static_cast<const bf16_t*>(AXIS == 0 ? a.ck : a.cv) + (size_t)bh * a.n_max * rr;
+
+  // this thread's chunks of a page: chunk e = tid + 256 i is feature row e / 8,
+  // tokens 8 (e % 8) .. + 7
+  uint4 stg[CPT];
+  auto gload = [&](int pg) {
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int e = tid + i * kThreads, j = e >> 3, c = e & 7;
+      const int nb = pg * kPage + 8 * c;
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (e < R * 8 && j < rr && nb < nvalid) {
+        v = ld16(src + (size_t)pg * kPage * rr + (size_t)j * kPage + 8 * c);
+        const int nv = nvalid - nb;
+        if (nv < 8) {
+          auto keep = [nv](int q) { return nv > 2 * q + 1 ? 0xffffffffu : nv > 2 * q ? 0x0000ffffu : 0u; };
+          v.x &= keep(0);
+          v.y &= keep(1);
+          v.z &= keep(2);
+          v.w &= keep(3);
+        }
+      }
+      stg[i] = v;
+    }
+  };
+  auto lstore = [&]() {
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int e = tid + i * kThreads, j = e >> 3, c = e & 7;
+      if (e < R * 8) *reinterpret_cast<uint4*>(&s_c[j * kPage + ((c ^ (((j >> 1) & 1) << 2)) << 3)]) = stg[i];
+    }
+  };
+  const int x16 = lane & 15, th = (lane >> 4) & 1, sw1 = (x16 >> 3) & 1;
+  const int troff = (8 * g + (x16 >> 2)) * kPage + ((2 * th + ((x16 & 3) >> 1)) << 3) + 4 * (x16 & 1);
+  auto lat_op = [&](int nt, int s) -> bf16x8 {  // token tile nt (0, 1) of the staged page
+    const bf16_t* p = s_c + troff + ((4 * (nt ^ sw1)) << 3) + 16 * s * kPage;
+    const uint2 r0 = lds_tr16(p), r1 = lds_tr16(p + 4 * kPage);
+    return as_bf16x8(make_uint4(r0.x, r0.y, r1.x, r1.y));
+  };
+  // up-projection rows 32 wave + col of head h (features past rr are zero)
+  uint4 ua[KS];
+  {
+    const bf16_t* row = static_cast<const bf16_t*>(AXIS == 0 ? a.uk : a.uv) + ((size_t)h * kD + 32 * wave + col) * rr + 8 * g;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) ua[s] = 16 * s + 8 * g < rr ? ld16(row + 16 * s) : make_uint4(0, 0, 0, 0);
+  }
+  if (pg0 < pg1) gload(pg0);
+  for (int pg = pg0; pg < pg1; ++pg) {
+    lstore();
+    __syncthreads();
+    if (pg + 1 < pg1) gload(pg + 1);  // in flight during this page's products
+    f32x16 acc[2] = {f32x16{0.f}, f32x16{0.f}};
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt) {
+        const bf16x8 c = lat_op(nt, s);
+        acc[nt] = AXIS == 0 ? mfma(as_bf16x8(ua[s]), c, acc[nt]) : mfma(c, as_bf16x8(ua[s]), acc[nt]);
+      }
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) {
+      const int tok0 = pg * kPage + 32 * nt;
+      if (AXIS == 0) {
+        // lane (token col, half g), register r: feature 32 wave + 8 (r/4) + 4 g + r%4
+        uint16_t* dst = static_cast<uint16_t*>(a.kh) + ((size_t)bh * a.nk + tok0 + col) * kD + 32 * wave + 4 * g;
+#pragma unroll
+        for (int c4 = 0; c4 < 4; ++c4)
+          *reinterpret_cast<uint2*>(dst + 8 * c4) =
+              make_uint2(pack2h(acc[nt][4 * c4], acc[nt][4 * c4 + 1]), pack2h(acc[nt][4 * c4 + 2], acc[nt][4 * c4 + 3]));
+      } else {
+        // lane (feature col, half g), registers 8 blk .. + 7: tokens at permuted
+        // positions 16 blk + 8 g .. + 7 of the tile
+        uint16_t* dst = static_cast<uint16_t*>(a.vt) +
+                        (((size_t)bh * (a.nk / kPage) + pg) * kD + 32 * wave + col) * kPage + 32 * nt + 8 * g;
+#pragma unroll
+        for (int blk = 0; blk < 2; ++blk) {
+          const f32x16& x = acc[nt];
+          const int r0 = 8 * blk;
+          *reinterpret_cast<uint4*>(dst + 16 * blk) =
+              make_uint4(pack2h(x[r0], x[r0 + 1]), pack2h(x[r0 + 2], x[r0 + 3]), pack2h(x[r0 + 4], x[r0 + 5]),
+                         pack2h(x[r0 + 6], x[r0 + 7]));
+        }
+      }
+    }
+    __syncthreads();  // the page's LDS tile is read by every wavefront before the next is stored
   }
 }
 
@@ -475,20 +574,18 @@ void flash2d_kernel(Prefill2dArgs a) {
   }
 }
 
-template <int AXIS, int KS, bool PH>
+template <int AXIS, int KS>
 hipError_t launch_recon(const Prefill2dArgs& a, hipStream_t stream) {
-  constexpr int TOK = PH ? kPage : kRTok;
-  const dim3 grid((a.nk + TOK - 1) / TOK, PH ? a.B * a.H : a.B);
-  hipLaunchKernelGGL((recon2d_kernel<AXIS, KS, PH>), grid, dim3(kThreads), 0, stream, a);
+  const dim3 grid((a.nk + kRTok - 1) / kRTok, a.B);
+  hipLaunchKernelGGL((recon2d_kernel<AXIS, KS>), grid, dim3(kThreads), 0, stream, a);
   return hipGetLastError();
 }
 
-// r: the rank rounded up to a multiple of 16
-template <int AXIS, bool PH>
+template <int AXIS>
 hipError_t launch_recon_r(const Prefill2dArgs& a, int r, hipStream_t stream) {
   switch (r / 16) {
 #define LLA_R(ks) \
-  case ks: return launch_recon<AXIS, ks, PH>(a, stream);
+  case ks: return launch_recon<AXIS, ks>(a, stream);
     LLA_R(1) LLA_R(2) LLA_R(3) LLA_R(4) LLA_R(5) LLA_R(6) LLA_R(7) LLA_R(8)
     LLA_R(9) LLA_R(10) LLA_R(11) LLA_R(12) LLA_R(13) LLA_R(14) LLA_R(15) LLA_R(16)
     LLA_R(17) LLA_R(18) LLA_R(19) LLA_R(20) LLA_R(21) LLA_R(22) LLA_R(23) LLA_R(24)
@@ -506,19 +603,40 @@ size_t prefill_2d_ws_bytes(int B, int H, int n_keys) {
 }
 
 hipError_t launch_prefill_2d(const Prefill2dArgs& a, hipStream_t stream) {
-  hipError_t e = launch_recon_r<0, false>(a, a.rk, stream);
+  hipError_t e = launch_recon_r<0>(a, a.rk, stream);
   if (e != hipSuccess) return e;
-  e = launch_recon_r<1, false>(a, a.rv, stream);
+  e = launch_recon_r<1>(a, a.rv, stream);
   if (e != hipSuccess) return e;
   const dim3 grid(a.B * a.H, (a.M + kQBlock - 1) / kQBlock);
   hipLaunchKernelGGL(flash2d_kernel, grid, dim3(kFThreads), 0, stream, a);
   return hipGetLastError();
 }
 
+template <int AXIS>
+hipError_t launch_recon_ph(const Prefill2dArgs& a, int r, hipStream_t stream) {
+  // pages per workgroup: about 2048 workgroups over the (b, h) pages, 1 to 8 pages each
+  const int pages = a.nk / kPage;
+  const long total = (long)pages * a.B * a.H;
+  int ppw = (int)(total / 2048);
+  ppw = ppw < 1 ? 1 : ppw > 8 ? 8 : ppw;
+  const dim3 grid((pages + ppw - 1) / ppw, a.B * a.H);
+  switch ((r + 15) / 16) {
+#define LLA_R(ks) \
+  case ks: hipLaunchKernelGGL((recon_ph_kernel<AXIS, ks>), grid, dim3(kThreads), 0, stream, a, ppw); break;
+    LLA_R(1) LLA_R(2) LLA_R(3) LLA_R(4) LLA_R(5) LLA_R(6) LLA_R(7) LLA_R(8)
+    LLA_R(9) LLA_R(10) LLA_R(11) LLA_R(12) LLA_R(13) LLA_R(14) LLA_R(15) LLA_R(16)
+    LLA_R(17) LLA_R(18) LLA_R(19) LLA_R(20) LLA_R(21) LLA_R(22) LLA_R(23) LLA_R(24)
+    LLA_R(25) LLA_R(26) LLA_R(27) LLA_R(28) LLA_R(29) LLA_R(30) LLA_R(31) LLA_R(32)
+#undef LLA_R
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_prefill_rebuild(const Prefill2dArgs& a, hipStream_t stream) {
-  hipError_t e = launch_recon_r<0, true>(a, (a.rk + 15) / 16 * 16, stream);
+  hipError_t e = launch_recon_ph<0>(a, a.rk, stream);
   if (e != hipSuccess) return e;
-  e = launch_recon_r<1, true>(a, (a.rv + 15) / 16 * 16, stream);
+  e = launch_recon_ph<1>(a, a.rv, stream);
   if (e != hipSuccess) return e;
   const dim3 grid(a.B * a.H, (a.M + kQBlock - 1) / kQBlock);
   hipLaunchKernelGGL(flash2d_kernel, grid, dim3(kFThreads), 0, stream, a);
