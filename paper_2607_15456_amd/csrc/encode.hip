@@ -485,29 +485,57 @@ __device__ __forceinline__ void encode_gemm_body(const EncodeArgs& a, int tb, in
     const int t = t0 + 32 * wave + col;
     if (t < TT) {
       const int b = t / a.M, pos = ring_slot(a.pos0 + (t - b * a.M), a.sink, a.window);
+      const bool tm = a.k_token_major != 0;
 #pragma unroll
       for (int rt = 0; rt < 3; ++rt)
 #pragma unroll
-        for (int q = 0; q < 16; ++q) {
-          const int rl = 32 * rt + 8 * (q / 4) + 4 * g + q % 4, row = row0 + rl;
-          if (row < r)
-            cout[cache_index(b, h, H, a.n_max, r, pos, row, a.k_token_major != 0)] =
-                f32_to_bf16(acc[rt][q] - (mu ? s_mu[rl] : 0.f));
+        for (int i = 0; i < 4; ++i) {
+          const int rl = 32 * rt + 8 * i + 4 * g, row = row0 + rl;  // first of 4 consecutive rows
+          if (tm && row + 3 < r) {
+            // token-major cache: the 4 rows are contiguous, 8-byte aligned (r_k % 32 == 0)
+            const uint32_t lo = uint32_t(f32_to_bf16(acc[rt][4 * i] - (mu ? s_mu[rl] : 0.f))) |
+                                (uint32_t(f32_to_bf16(acc[rt][4 * i + 1] - (mu ? s_mu[rl + 1] : 0.f))) << 16);
+            const uint32_t hi = uint32_t(f32_to_bf16(acc[rt][4 * i + 2] - (mu ? s_mu[rl + 2] : 0.f))) |
+                                (uint32_t(f32_to_bf16(acc[rt][4 * i + 3] - (mu ? s_mu[rl + 3] : 0.f))) << 16);
+            *reinterpret_cast<uint2*>(&cout[cache_index(b, h, H, a.n_max, r, pos, row, true)]) = make_uint2(lo, hi);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (row + e < r)
+                cout[cache_index(b, h, H, a.n_max, r, pos, row + e, tm)] =
+                    f32_to_bf16(acc[rt][4 * i + e] - (mu ? s_mu[rl + e] : 0.f));
+          }
         }
     }
   } else {
-    // lane (row col of tile rt, half g), register q: token 32 wave + 8(q/4) + 4g + q%4
+    // lane (row col of tile rt, half g), register q: token 32 wave + 8(q/4) + 4g + q%4,
+    // so registers 4i .. 4i + 3 are 4 consecutive tokens of one feature row.
+    // When their slots are 4 consecutive positions of one page (one sequence,
+    // no ring, position a multiple of 4) they are one 8-byte store.
 #pragma unroll
     for (int rt = 0; rt < 3; ++rt) {
       const int rl = 32 * rt + col, row = row0 + rl;
       if (row >= r) continue;
       const float m = mu ? s_mu[rl] : 0.f;
 #pragma unroll
-      for (int q = 0; q < 16; ++q) {
-        const int t = t0 + 32 * wave + 8 * (q / 4) + 4 * g + q % 4;
-        if (t < TT) {
-          const int b = t / a.M, pos = ring_slot(a.pos0 + (t - b * a.M), a.sink, a.window);
-          cout[cache_index(b, h, H, a.n_max, r, pos, row)] = f32_to_bf16(acc[rt][q] - m);
+      for (int i = 0; i < 4; ++i) {
+        const int t = t0 + 32 * wave + 8 * i + 4 * g;  // first token of the run
+        const int b = t / a.M, m0 = t - b * a.M, p = a.pos0 + m0;
+        if (a.window == 0 && t + 3 < TT && m0 + 3 < a.M && (p & 3) == 0) {
+          const uint32_t lo = uint32_t(f32_to_bf16(acc[rt][4 * i] - m)) |
+                              (uint32_t(f32_to_bf16(acc[rt][4 * i + 1] - m)) << 16);
+          const uint32_t hi = uint32_t(f32_to_bf16(acc[rt][4 * i + 2] - m)) |
+                              (uint32_t(f32_to_bf16(acc[rt][4 * i + 3] - m)) << 16);
+          *reinterpret_cast<uint2*>(&cout[cache_index(b, h, H, a.n_max, r, p, row)]) = make_uint2(lo, hi);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int te = t + e;
+            if (te < TT) {
+              const int be = te / a.M, pos = ring_slot(a.pos0 + (te - be * a.M), a.sink, a.window);
+              cout[cache_index(be, h, H, a.n_max, r, pos, row)] = f32_to_bf16(acc[rt][4 * i + e] - m);
+            }
+          }
         }
       }
     }
