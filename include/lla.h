@@ -34,6 +34,10 @@
  * - dtype arguments take lla_dtype values.  "dtype" is the element type of
  *   every input tensor of the call (queries, latents, projections, means);
  *   accumulation is always fp32.
+ * - The attention calls address one latent region with 32-bit byte offsets:
+ *   n_max * r * (element bytes) must be below 2^31 for every cache they read
+ *   (r = r_k, r_v or d_rope; one region is one (b, h) of a per-head cache,
+ *   one sequence of an LLA-2D cache), else LLA_ERR_UNSUPPORTED.
  * - Calls are stateless and reentrant.  Calls that share a workspace or write
  *   the same cache region must be ordered by the caller (same stream).
  *

@@ -19,6 +19,11 @@
 //     (rg, ts) owns feature rows j = k*8 + rg and token slice ts of each page:
 //     zacc[k] += sum over its 8 tokens of p_n c_v[j][n]; the reduction over
 //     token slices is deferred to the end of the scan.
+// Short contexts (HALF): with fewer 8-page groups than wavefronts, the K phase
+// takes groups of 4 pages and each wave-wide load covers two feature rows
+// (lanes 32..63 take the odd row); one lane swap then sums the two halves of
+// every score.  All wavefronts stream with full 16-byte loads, and a group's K
+// phase has half as many dependent load batches.
 // The waves of a workgroup interleave groups and merge their (m, l, z) in LDS.
 // When the context is split over several workgroups (split-K), each writes its
 // merged partial to the workspace and the last to arrive (an agent-scope
@@ -137,6 +142,11 @@ __device__ __forceinline__ uint4 buf_ld16(BufRsrc r, int voff, int soff) {
   return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, kCpolNT));
 }
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+// x[lane] + x[lane ^ 32]
+__device__ __forceinline__ float sum_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
 
 template <typename T>
 __device__ __forceinline__ int vec_width(int r) {
@@ -146,8 +156,9 @@ __device__ __forceinline__ int vec_width(int r) {
 
 // DEEP: at most two wavefronts per SIMD; the doubled register budget holds a
 // second batch of loads in flight (software pipelining).  Otherwise four per
-// SIMD, one batch at a time.
-template <typename TIn, int GV, int kWaves, bool DEEP>
+// SIMD, one batch at a time.  HALF: K groups of PPG / 2 pages, two feature rows
+// per wave-wide load (short contexts).
+template <typename TIn, int GV, int kWaves, bool DEEP, bool HALF>
 __global__ __launch_bounds__(kWaves * kWave) __attribute__((amdgpu_waves_per_eu(DEEP ? 2 : 4)))
 void decode_kernel(DecodeArgs a) {
   constexpr int kThreads = kWaves * kWave;
@@ -156,12 +167,16 @@ void decode_kernel(DecodeArgs a) {
   constexpr int EPL = Elem<TIn>::kPer16B;  // tokens covered by one 16-byte load
   constexpr int LPR = kPage / EPL;         // lanes per 64-token feature row
   constexpr int PPG = kWave / LPR;         // pages per group (K phase) = rows per load (V phase)
+  constexpr int KRL = HALF ? 2 : 1;        // feature rows per wave-wide K load
+  constexpr int KPG = PPG / KRL;           // pages per K group
+  constexpr int KRB = KB * KRL;            // feature rows per K batch
 
   // s_work holds the prologue's row-block partials, then (after the prologue's
   // last barrier) the per-wave probability buffers and latent partials.
   constexpr int kPWave = PPG * kPage;
   __shared__ float s_q[kMaxHead];
-  __shared__ __attribute__((aligned(16))) float s_qt[kMaxRank];
+  // content rows padded to KRB, then the rotary rows padded to KRB
+  __shared__ __attribute__((aligned(16))) float s_qt[kMaxRank + (HALF ? 16 : 0)];
   __shared__ __attribute__((aligned(16))) float s_work[kWaves * (kPWave + kMaxRank)];
   static_assert(kWaves * (kPWave + kMaxRank) >= kThreads * 8, "prologue partials do not fit");
   float* const s_part = s_work;
@@ -195,7 +210,10 @@ void decode_kernel(DecodeArgs a) {
   const size_t bh = (size_t)b * a.H + h;
   const size_t unit = bh * a.M + m;  // (b, h, m)
   const int rk = a.rk, rv = a.rv;
-  const int rq0 = (rk + 7) & ~7;  // s_qt slot of the first rotary row
+  // s_qt slot of the first rotary row; rotary rows padded to whole batches
+  // (dr is a multiple of 8)
+  const int rq0 = HALF ? (rk + KRB - 1) / KRB * KRB : (rk + 7) & ~7;
+  const int drp = HALF ? (a.dr + KRB - 1) / KRB * KRB : a.dr;
 
   // ---- prologue: absorbed query q~ = U_k^T q, with scale * log2(e) folded in ----
   {
@@ -209,18 +227,22 @@ void decode_kernel(DecodeArgs a) {
       case 2: absorb_query<TIn, 2, kThreads>(uk, a.d, rk, a.qscale, s_q, s_part, s_qt); break;
       default: absorb_query<TIn, 1, kThreads>(uk, a.d, rk, a.qscale, s_q, s_part, s_qt); break;
     }
-    // the last content batch is padded to 8 rows with zero weights; the rotary
-    // branch: the (already rotated) query part joins q~ as extra rows, from the
-    // 16-byte aligned slot past the padded content rows
+    // the last content batch is padded to whole batches with zero weights; the
+    // rotary branch: the (already rotated) query part joins q~ as extra rows,
+    // from the 16-byte aligned slot past the padded content rows
     for (int j = rk + tid; j < rq0; j += kThreads) s_qt[j] = 0.f;
     if (a.dr) {
       const TIn* qr = static_cast<const TIn*>(a.qr) + unit * a.dr;
       for (int i = tid; i < a.dr; i += kThreads) s_qt[rq0 + i] = a.qscale * Elem<TIn>::get(qr, i);
+      if constexpr (HALF)
+        for (int i = a.dr + tid; i < drp; i += kThreads) s_qt[rq0 + i] = 0.f;
     }
     __syncthreads();
   }
 
   const int hi = lane / LPR, lo = lane - hi * LPR;
+  const int kpg = HALF ? hi % KPG : hi;  // K phase: page of the group
+  const int krw = HALF ? hi / KPG : 0;   // K phase (HALF): which row of each load's pair
   float zacc[GV];
 #pragma unroll
   for (int k = 0; k < GV; ++k) zacc[k] = 0.f;
@@ -234,14 +256,18 @@ void decode_kernel(DecodeArgs a) {
   const BufRsrc rv_src = make_rsrc(static_cast<const TIn*>(a.cv) + bh * (size_t)a.n_max * rv,
                                    (size_t)a.n_max * rv * ES);
   const int kpage_bytes = kPage * rk * ES, vpage_bytes = kPage * rv * ES;
-  const int vk_lane = hi * kpage_bytes + lo * 16;   // K phase: page hi of the group, slice lo
+  // K phase: page kpg of the group, slice lo (HALF: and the odd row for krw = 1)
+  const int vk_lane = kpg * kpage_bytes + krw * kPage * ES + lo * 16;
   // rotary keys of this (b, h): the same paging with dr feature rows
   const size_t bhr = (size_t)b * a.Hr + (a.Hr == 1 ? 0 : h);
   const BufRsrc rr_src = make_rsrc(a.dr ? static_cast<const TIn*>(a.rc) + bhr * (size_t)a.n_max * a.dr
                                         : static_cast<const TIn*>(a.ck),
                                    (size_t)a.n_max * a.dr * ES);
   const int rpage_bytes = kPage * a.dr * ES;
-  const int vr_lane = hi * rpage_bytes + lo * 16;
+  const int vr_lane = kpg * rpage_bytes + krw * kPage * ES + lo * 16;
+  // HALF: offsets past each region's size (rows beyond r_k or dr) read as zero
+  // and touch no memory
+  const int k_oob = a.n_max * rk * ES, r_oob = a.n_max * a.dr * ES;
   const int vv_lane = hi * kPage * ES + lo * 16;    // V phase: row hi of the row group, slice lo
   const int vg_full = rv / PPG, vg_part = rv % PPG;  // full row groups, rows of the partial one
   float* sp = s_p[wave];
@@ -252,15 +278,34 @@ void decode_kernel(DecodeArgs a) {
   // between two register sets, and V batches prefetch across row groups and
   // pages, so the FMAs of one batch overlap the memory latency of the next.
   constexpr bool PIPE = DEEP;
-  const int nkb = (rk + KB - 1) / KB;                       // K batches (the last padded, zero weights)
-  const int ntb = nkb + a.dr / KB;                          // plus the rotary rows (dr % 8 == 0)
+  const int nkb = (rk + KRB - 1) / KRB;                     // K batches (the last padded, zero weights)
+  const int ntb = nkb + drp / KRB;                          // plus the rotary rows
   const int nvb = (vg_full + (vg_part ? 1 : 0) + VB - 1) / VB;  // V batches per page
   constexpr int NKC = (GV + VB - 1) / VB;
 
-  // batch jb < nkb: content rows jb*KB.. of c_k (rows past r_k re-read row
+  // batch jb < nkb: content rows jb*KRB.. of c_k (rows past r_k re-read row
   // r_k - 1, weighted by zero); later batches: rotary rows.  Every batch issues
   // all its loads, so the compiler's waits count loads exactly.
   auto kload = [&](uint4 (&r)[KB], int g0p, int jb) {
+    if constexpr (HALF) {
+      // load u reads rows r0 = 2u (lanes krw = 0) and r0 + 1 (krw = 1) of the
+      // batch's content or rotary rows, page g0p + kpg; the pair's offset is
+      // uniform, and a lane whose row is past the range reads out of the region
+      // (zero, no memory access)
+      const bool rot = jb >= nkb;
+      const BufRsrc src = rot ? rr_src : rk_src;
+      const int lim = rot ? a.dr : rk, oob = rot ? r_oob : k_oob;
+      const int lbase = rot ? vr_lane : vk_lane;
+      const int pbase = g0p * (rot ? rpage_bytes : kpage_bytes);
+      const int rb = (rot ? jb - nkb : jb) * KRB;
+#pragma unroll
+      for (int u = 0; u < KB; ++u) {
+        const int r0 = rb + 2 * u;
+        const int so = r0 < lim ? pbase + r0 * kPage * ES : 0;
+        r[u] = buf_ld16(src, r0 + krw < lim ? lbase : oob, so);
+      }
+      return;
+    }
     if (jb < nkb) {
 #pragma unroll
       for (int u = 0; u < KB; ++u)
@@ -273,14 +318,19 @@ void decode_kernel(DecodeArgs a) {
   };
   auto kfma = [&](const uint4 (&r)[KB], int jb, float (&acc)[EPL]) {
     float qj[KB];
-    const int q0 = jb < nkb ? jb * KB : rq0 + (jb - nkb) * KB;
+    const int q0 = jb < nkb ? jb * KRB : rq0 + (jb - nkb) * KRB;
+    if constexpr (HALF) {
 #pragma unroll
-    for (int u = 0; u < KB; u += 4) {
-      const float4 qa = *reinterpret_cast<const float4*>(&s_qt[q0 + u]);
-      qj[u] = qa.x;
-      qj[u + 1] = qa.y;
-      qj[u + 2] = qa.z;
-      qj[u + 3] = qa.w;
+      for (int u = 0; u < KB; ++u) qj[u] = s_qt[q0 + 2 * u + krw];
+    } else {
+#pragma unroll
+      for (int u = 0; u < KB; u += 4) {
+        const float4 qa = *reinterpret_cast<const float4*>(&s_qt[q0 + u]);
+        qj[u] = qa.x;
+        qj[u + 1] = qa.y;
+        qj[u + 2] = qa.z;
+        qj[u + 3] = qa.w;
+      }
     }
 #pragma unroll
     for (int u = 0; u < KB; ++u) {
@@ -300,12 +350,12 @@ void decode_kernel(DecodeArgs a) {
     }
   };
 
-  for (int g0 = pb + wave * PPG; g0 < pe; g0 += kWaves * PPG) {
-    const int np = min(PPG, pe - g0);
+  for (int g0 = pb + wave * KPG; g0 < pe; g0 += kWaves * KPG) {
+    const int np = min(KPG, pe - g0);
     float acc[EPL];
 #pragma unroll
     for (int e = 0; e < EPL; ++e) acc[e] = 0.f;
-    if (hi < np) {
+    if (kpg < np) {
       if constexpr (PIPE) {
         uint4 ka[KB], kb2[KB];
         if (ntb > 0) kload(ka, g0, 0);
@@ -323,15 +373,19 @@ void decode_kernel(DecodeArgs a) {
         }
       }
     }
+    if constexpr (HALF) {  // each half of the wave holds half of every score's rows
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) acc[e] = sum_halves(acc[e]);
+    }
     uint4 vcur[VB];
     if constexpr (PIPE) vload(vcur, g0, 0);  // first V batch in flight during the softmax
 
     // scores of invalid pages / tokens beyond N are -inf
-    const int n0 = (g0 + hi) * kPage + lo * EPL;
+    const int n0 = (g0 + kpg) * kPage + lo * EPL;
     float mb = neg_inf();
 #pragma unroll
     for (int e = 0; e < EPL; ++e) {
-      if (hi >= np || n0 + e >= N) acc[e] = neg_inf();
+      if (kpg >= np || n0 + e >= N) acc[e] = neg_inf();
       mb = fmaxf(mb, acc[e]);
     }
 #pragma unroll
@@ -347,12 +401,14 @@ void decode_kernel(DecodeArgs a) {
 #pragma unroll
     for (int e = 0; e < EPL; ++e) {
       pr[e] = fast_exp2(acc[e] - m_run);
-      l_lane += pr[e];
+      if (krw == 0) l_lane += pr[e];  // HALF: the upper half holds the same probabilities
     }
+    if (krw == 0) {
 #pragma unroll
-    for (int e = 0; e < EPL; e += 4)
-      *reinterpret_cast<float4*>(&sp[hi * kPage + lo * EPL + e]) =
-          make_float4(pr[e], pr[e + 1], pr[e + 2], pr[e + 3]);
+      for (int e = 0; e < EPL; e += 4)
+        *reinterpret_cast<float4*>(&sp[kpg * kPage + lo * EPL + e]) =
+            make_float4(pr[e], pr[e + 1], pr[e + 2], pr[e + 3]);
+    }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -523,16 +579,25 @@ void decode_kernel(DecodeArgs a) {
 template <typename TIn, int GV>
 hipError_t launch_t(const DecodeArgs& a, hipStream_t stream) {
   dim3 grid(a.B * a.M * a.splits, a.H);
+  if (a.half) {  // short contexts: bf16, 4 wavefronts, pipelined
+    if constexpr (sizeof(TIn) == 2) {
+      if (a.waves != 4 || !a.deep) return hipErrorInvalidValue;
+      hipLaunchKernelGGL((decode_kernel<TIn, GV, 4, true, true>), grid, dim3(4 * kWave), 0, stream, a);
+      return hipGetLastError();
+    } else {
+      return hipErrorInvalidValue;
+    }
+  }
   if (a.waves == 8) {
     if (a.deep)
-      hipLaunchKernelGGL((decode_kernel<TIn, GV, 8, true>), grid, dim3(8 * kWave), 0, stream, a);
+      hipLaunchKernelGGL((decode_kernel<TIn, GV, 8, true, false>), grid, dim3(8 * kWave), 0, stream, a);
     else
-      hipLaunchKernelGGL((decode_kernel<TIn, GV, 8, false>), grid, dim3(8 * kWave), 0, stream, a);
+      hipLaunchKernelGGL((decode_kernel<TIn, GV, 8, false, false>), grid, dim3(8 * kWave), 0, stream, a);
   } else {
     if (a.deep)
-      hipLaunchKernelGGL((decode_kernel<TIn, GV, 4, true>), grid, dim3(4 * kWave), 0, stream, a);
+      hipLaunchKernelGGL((decode_kernel<TIn, GV, 4, true, false>), grid, dim3(4 * kWave), 0, stream, a);
     else
-      hipLaunchKernelGGL((decode_kernel<TIn, GV, 4, false>), grid, dim3(4 * kWave), 0, stream, a);
+      hipLaunchKernelGGL((decode_kernel<TIn, GV, 4, false, false>), grid, dim3(4 * kWave), 0, stream, a);
   }
   return hipGetLastError();
 }

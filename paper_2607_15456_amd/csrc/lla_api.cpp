@@ -25,6 +25,15 @@ bool head_ok(int d) { return d >= 32 && d <= 256 && d % 32 == 0; }
 bool rank_ok(int r) { return r >= 1 && r <= LLA_MAX_RANK; }
 bool cap_ok(int n_max) { return n_max >= LLA_PAGE_TOKENS && n_max % LLA_PAGE_TOKENS == 0; }
 bool rope_ok(int d_rope) { return d_rope >= 8 && d_rope <= LLA_MAX_ROPE && d_rope % 8 == 0; }
+// The attention kernels address one latent region (n_max slots of r features:
+// per (b, h) for the per-head cache, per sequence for the LLA-2D cache) with
+// 32-bit byte offsets.
+bool region_ok(int n_max, int r, int dtype) {
+  return (int64_t)n_max * r * (dtype == LLA_F32 ? 4 : 2) < ((int64_t)1 << 31);
+}
+bool regions_ok(int n_max, int r_k, int r_v, int d_rope, int dtype) {
+  return region_ok(n_max, r_k, dtype) && region_ok(n_max, r_v, dtype) && region_ok(n_max, d_rope, dtype);
+}
 
 int64_t gcd64(int64_t a, int64_t b) {
   while (b) {
@@ -58,10 +67,11 @@ size_t workspace_bytes(int B, int H, int r_v, int n_ctx) {
 // wavefronts (4-wave workgroups when (b, h) units alone reach that, 8-wave
 // ones otherwise); only smaller batches split the context (split-K), up to 8
 // wavefronts per compute unit, with every wavefront keeping at least one
-// 8-page group.  LLA_DECODE_WAVES / LLA_DECODE_SPLITS / LLA_DECODE_DEEP
-// override the choice (for tuning sweeps).
+// 8-page group.  Short bf16 contexts (fewer 8-page groups per workgroup than
+// wavefronts) use the 4-page K groups.  LLA_DECODE_WAVES / LLA_DECODE_SPLITS /
+// LLA_DECODE_DEEP / LLA_DECODE_HALF override the choice (for tuning sweeps).
 struct DecodeShape {
-  int waves, splits, deep;
+  int waves, splits, deep, half;
 };
 
 int env_int(const char* name) {
@@ -73,13 +83,14 @@ DecodeShape choose_shape(int units, int n_ctx, bool allow_split, bool bf16) {
   static const int forced_waves = env_int("LLA_DECODE_WAVES");
   static const int forced_splits = env_int("LLA_DECODE_SPLITS");
   static const int forced_deep = env_int("LLA_DECODE_DEEP");
+  static const int forced_half = env_int("LLA_DECODE_HALF");
   const int pages = (n_ctx + LLA_PAGE_TOKENS - 1) / LLA_PAGE_TOKENS;
   const int groups = (pages + 7) / 8;
   const long target = 8L * lla::device_cu_count();  // resident wavefronts wanted
   // bf16: the software-pipelined variant (two batches of loads in flight per
   // wavefront, at most 2 wavefronts per SIMD) measured as fast or faster on
   // every decode workload; fp32 keeps the 4-per-SIMD variant.
-  DecodeShape sh{4, 1, bf16 ? 1 : 0};
+  DecodeShape sh{4, 1, bf16 ? 1 : 0, 0};
   if ((long)units * 4 < target && groups >= 8) sh.waves = 8;
   if (allow_split && (long)units * sh.waves < target) {
     long s = (target + (long)units * sh.waves - 1) / ((long)units * sh.waves);
@@ -92,6 +103,13 @@ DecodeShape choose_shape(int units, int n_ctx, bool allow_split, bool bf16) {
   if (sh.splits > max_splits(n_ctx)) sh.splits = max_splits(n_ctx);
   if (sh.splits < 1) sh.splits = 1;
   if (forced_deep) sh.deep = forced_deep > 0 ? 1 : 0;
+  // short contexts: fewer 8-page groups per workgroup than wavefronts -> K
+  // groups of 4 pages with two feature rows per load, so every wavefront streams
+  if (bf16 && sh.deep && sh.waves == 4) {
+    const int per = (pages + sh.splits - 1) / sh.splits;
+    sh.half = (per + 7) / 8 < sh.waves ? 1 : 0;
+    if (forced_half) sh.half = forced_half > 0 ? 1 : 0;
+  }
   return sh;
 }
 
@@ -320,6 +338,7 @@ lla_status decode_impl(int dtype, int out_dtype, int B, int H, int d_head, int r
   if (d_rope && (!rope_ok(d_rope) || !(H_rope == 1 || H_rope == H) || !ptr_ok(q_rope) ||
                  !ptr_ok(r_cache) || ((r_k + 7) / 8) * 8 + d_rope > LLA_MAX_RANK))
     return LLA_ERR_INVALID_ARG;
+  if (!regions_ok(n_max, r_k, r_v, d_rope, dtype)) return LLA_ERR_UNSUPPORTED;
   if (!static_scratch) {
     if ((workspace == nullptr) != (ws_bytes == 0)) return LLA_ERR_WORKSPACE;
     if (workspace && (!aligned16(workspace) || ws_bytes < workspace_bytes(B, H, r_v, n_ctx)))
@@ -358,6 +377,7 @@ lla_status decode_impl(int dtype, int out_dtype, int B, int H, int d_head, int r
   a.waves = sh.waves;
   a.splits = sh.splits;
   a.deep = sh.deep;
+  a.half = sh.half;
   const hipStream_t st = static_cast<hipStream_t>(stream);
   if (static_scratch) {
     // partials of exactly the chosen split count, in the device's static array
@@ -437,6 +457,7 @@ lla_status lla_decode_attn_fullrope(int dtype, int out_dtype, int B, int H, int 
       (ctx_len && (reinterpret_cast<uintptr_t>(ctx_len) & 3u)) ||
       (q_pos && (reinterpret_cast<uintptr_t>(q_pos) & 3u)))
     return LLA_ERR_INVALID_ARG;
+  if (!regions_ok(n_max, r_k, r_v, 0, dtype)) return LLA_ERR_UNSUPPORTED;
   if ((workspace == nullptr) != (ws_bytes == 0)) return LLA_ERR_WORKSPACE;
   if (workspace && (!aligned16(workspace) || ws_bytes < workspace_bytes(B, H, r_v, n_ctx)))
     return LLA_ERR_WORKSPACE;
@@ -517,6 +538,7 @@ lla_status prefill_impl(int dtype, int out_dtype, int B, int H, int M, int d_hea
   if (d_rope && (!rope_ok(d_rope) || !(H_rope == 1 || H_rope == H) || !ptr_ok(q_rope) ||
                  !ptr_ok(r_cache) || ((r_k + 7) / 8) * 8 + d_rope > LLA_MAX_RANK))
     return LLA_ERR_INVALID_ARG;
+  if (!regions_ok(n_max, r_k, r_v, d_rope, dtype)) return LLA_ERR_UNSUPPORTED;
   (void)mu_k;  // q . mu_k is constant over the keys of a query: it cancels in the softmax
   const float qscale = (float)((double)scale * kLog2e);
   if ((workspace == nullptr) != (ws_bytes == 0)) return LLA_ERR_WORKSPACE;
@@ -755,7 +777,8 @@ lla_status lla_decode_attn_2d(int dtype, int out_dtype, int B, int H, int d_head
       !opt_ptr_ok(mu_k) || !opt_ptr_ok(mu_v) ||
       (ctx_len && (reinterpret_cast<uintptr_t>(ctx_len) & 3u)))
     return LLA_ERR_INVALID_ARG;
-  if (dtype != LLA_BF16 || H != 16 || !rank2d_ok(r_k, r_v)) return LLA_ERR_UNSUPPORTED;
+  if (dtype != LLA_BF16 || H != 16 || !rank2d_ok(r_k, r_v) || !regions_ok(n_max, r_k, r_v, 0, dtype))
+    return LLA_ERR_UNSUPPORTED;
   if (!workspace || !aligned16(workspace) || ws_bytes < ws2d_bytes(B, H, r_k, r_v, n_ctx))
     return LLA_ERR_WORKSPACE;
   (void)mu_k;  // q . mu_k is constant over the context: it cancels in the softmax
@@ -806,7 +829,8 @@ lla_status lla_prefill_attn_2d(int dtype, int out_dtype, int B, int H, int M, in
   if (!ptr_ok(q) || !ptr_ok(c_k) || !ptr_ok(c_v) || !ptr_ok(u_k) || !ptr_ok(u_v) || !ptr_ok(out) ||
       !opt_ptr_ok(mu_k) || !opt_ptr_ok(mu_v))
     return LLA_ERR_INVALID_ARG;
-  if (dtype != LLA_BF16 || d_head != 128 || r_k % 16 || r_v % 16 || r_k > 512 || r_v > 512)
+  if (dtype != LLA_BF16 || d_head != 128 || r_k % 16 || r_v % 16 || r_k > 512 || r_v > 512 ||
+      !regions_ok(n_max, r_k, r_v, 0, dtype))
     return LLA_ERR_UNSUPPORTED;
   size_t need = 0;
   lla_prefill_2d_workspace_bytes(B, H, d_head, p0 + M, &need);

@@ -151,6 +151,8 @@ def _decode(**kw):
     (dict(ctx_len=P + 2), 1),
     (dict(ws=P, ws_bytes=0), 3), (dict(ws=None, ws_bytes=64), 3), (dict(ws=P, ws_bytes=64), 3),
     (dict(ws=MIS, ws_bytes=1 << 30), 3),
+    # one (b, h) region of n_max * r elements must stay below 2 GiB (32-bit offsets)
+    (dict(n_max=1 << 23), 2), (dict(dtype=0, n_max=1 << 22), 2),
 ])
 def test_decode_rejects(kw, code):
     assert _decode(**kw) == code
@@ -212,6 +214,7 @@ REBUILD_WS = 4 * 1 * 16 * 128 * 64  # B * H * d_head * (p0 + M rounded up to 64)
     (dict(REBUILD), 3), (dict(REBUILD, ws=P, ws_bytes=REBUILD_WS - 16), 3), (dict(REBUILD, ws=MIS, ws_bytes=1 << 30), 3),
     (dict(REBUILD, ws=P, ws_bytes=0), 3), (dict(rk=100, rv=160, ws=P, ws_bytes=1 << 30), 2),
     (dict(REBUILD, d=64, ws=P, ws_bytes=1 << 30), 2), (dict(ws=None, ws_bytes=16), 3),
+    (dict(n_max=1 << 26), 2),
 ])
 def test_prefill_rejects(kw, code):
     assert _prefill(**kw) == code
@@ -250,7 +253,7 @@ def _decode_rope(**kw):
 @pytest.mark.parametrize("kw,code", [
     (dict(dr=0), 1), (dict(dr=12), 1), (dict(dr=264), 1), (dict(Hr=2), 1), (dict(Hr=0), 1),
     (dict(qr=None), 1), (dict(rc=None), 1), (dict(qr=MIS), 1), (dict(rk=500, dr=16), 1),
-    (dict(B=0), 1), (dict(ws=P, ws_bytes=0), 3),
+    (dict(B=0), 1), (dict(ws=P, ws_bytes=0), 3), (dict(rk=8, rv=8, dr=256, n_max=1 << 22), 2),
 ])
 def test_decode_rope_rejects(kw, code):
     assert _decode_rope(**kw) == code
@@ -356,7 +359,7 @@ def _decode_2d(**kw):
     (dict(B=0), 1), (dict(d=40), 1), (dict(n_ctx=0), 1), (dict(n_ctx=600), 1), (dict(q=None), 1),
     (dict(ck=MIS), 1), (dict(scale=0.0), 1), (dict(dtype=0), 2), (dict(H=8), 2), (dict(rk=300), 2),
     (dict(rv=490), 2), (dict(rk=1056), 2), (dict(ws=None, ws_bytes=0), 3), (dict(ws_bytes=64), 3),
-    (dict(ws=MIS), 3),
+    (dict(ws=MIS), 3), (dict(n_max=1 << 22), 2),
 ])
 def test_decode_2d_rejects(kw, code):
     assert _decode_2d(**kw) == code
@@ -412,6 +415,7 @@ def _decode_fullrope(**kw):
     (dict(base=1.0), 1), (dict(base=float("inf")), 1), (dict(q=None), 1), (dict(ck=MIS), 1),
     (dict(muk=MIS), 1), (dict(q_pos=P + 2), 1), (dict(ctx_len=P + 1), 1),
     (dict(ws=P, ws_bytes=0), 3), (dict(ws=P, ws_bytes=64), 3), (dict(ws=MIS, ws_bytes=1 << 30), 3),
+    (dict(n_max=1 << 22), 2),
 ])
 def test_decode_fullrope_rejects(kw, code):
     assert _decode_fullrope(**kw) == code
@@ -442,6 +446,7 @@ def _prefill_2d(**kw):
     (dict(q=None), 1), (dict(cv=MIS), 1), (dict(muv=MIS), 1), (dict(B=65536, H=1, M=1), 1),
     (dict(dtype=0), 2), (dict(d=64), 2), (dict(rk=40), 2), (dict(rv=520), 2),
     (dict(ws=None), 3), (dict(ws_bytes=4 * 2 * 16 * 128 * 128 - 1), 3), (dict(ws=MIS), 3),
+    (dict(n_max=1 << 22), 2),
 ])
 def test_prefill_2d_rejects(kw, code):
     assert _prefill_2d(**kw) == code

@@ -85,6 +85,29 @@ def test_decode_rope(dtype, r_k, r_v, dr, Hr, N):
     assert_close(f64(out), ref, dtype, "decode rope")
 
 
+@pytest.mark.parametrize("r_k,r_v,dr,Hr", [(17, 30, 8, 1), (33, 160, 24, 4), (95, 9, 40, 1), (1, 1, 8, 4)])
+def test_decode_rope_short_context_row_pairs(r_k, r_v, dr, Hr):
+    """bf16 contexts of fewer than 25 pages are scanned in K groups of 4 pages,
+    each wave-wide load covering two feature rows: an odd r_k, or a rotary
+    width that is not a multiple of 16, leaves the last pair half past its
+    range.  The per-sequence lengths give groups of 1 to 4 pages and ragged
+    last pages."""
+    wl, B, N, n_max = SMALL, 3, 1500, 1536
+    dtype = torch.bfloat16
+    log(f"decode rope short context r=({r_k},{r_v}) dr={dr} Hr={Hr}")
+    ck, cv, kr, q, qr, uk, uv, muk, muv, rc = _decode_case(wl, r_k, r_v, dr, Hr, B, N, n_max, dtype, True)
+    lens = torch.tensor([1500, 700, 65], dtype=torch.int32, device=DEV)
+    qr_rot = lla.rope_rotate(qr, pos=lens - 1)
+    out = lla.decode_attn(q, lla.to_paged(ck, n_max), lla.to_paged(cv, n_max), uk, uv, n_ctx=N, ctx_len=lens,
+                          mu_k=muk, mu_v=muv, q_rope=qr_rot, r_cache=rc)
+    torch.cuda.synchronize()
+    ref = np.stack([oracle.decode_attn_rope_batched(f64(q)[b:b + 1], f64(qr)[b:b + 1], f64(ck)[b:b + 1],
+                                                    f64(cv)[b:b + 1], f64(kr).transpose(0, 2, 1, 3)[b:b + 1],
+                                                    f64(uk), f64(uv), f64(muk), f64(muv), ctx_len=int(lens[b]))[0]
+                    for b in range(B)])
+    assert_close(f64(out), ref, dtype, "decode rope, short contexts")
+
+
 @pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
 def test_decode_rope_ragged_lengths_and_split(dtype):
     """Per-sequence lengths (each query rotated at its own newest position) and
