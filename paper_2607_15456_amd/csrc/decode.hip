@@ -576,9 +576,303 @@ void decode_kernel(DecodeArgs a) {
   }
 }
 
+// Short contexts (at most a few 8-page groups per (b, h)), bf16: the four
+// wavefronts of a workgroup split the feature rows of each 8-page group
+// instead of its pages, so a group's loads are spread over every wavefront
+// whatever the page count.
+//   * K phase -- wave w takes the 8-row blocks w, w + 4, ... of the content
+//     rows and then of the rotary rows; lane (pg, ts) owns tokens ts*8.. of
+//     page pg, so one wave-wide load reads one feature row of all 8 pages.
+//     The four partial scores of a token are summed through LDS (double
+//     buffered over groups, one barrier per group), in the same order in
+//     every wavefront, so all four hold identical scores and softmax
+//     statistics.
+//   * V phase -- wave w takes the 8-row groups w, w + 4, ... of the value
+//     latents, each over all pages of the group (lane (rg, ts): row rg of the
+//     group, token slice ts); its z rows are its own, so no merge follows.
+// Slots that are not read (pages past the context, rows past r_k, r_v or dr)
+// are requested out of the region: they read as zero and touch no memory.
+template <int GV>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
+void decode_short_kernel(DecodeArgs a) {
+  typedef bf16_t TIn;
+  constexpr int kWaves = 4, kThreads = kWaves * kWave;
+  constexpr int KB = 8;                       // loads per K batch
+  constexpr int EPL = 8;                      // tokens per 16-byte load
+  constexpr int PPG = 8;                      // pages per group
+  constexpr int VH = PPG / 2;                 // pages per V half-batch
+  constexpr int GVW = (GV + kWaves - 1) / kWaves;  // value row groups per wavefront
+  constexpr int ES = 2;
+  __shared__ float s_q[kMaxHead];
+  __shared__ __attribute__((aligned(16))) float s_qt[kMaxRank];
+  // partial scores [buffer][wave][page*64 + token]; the prologue's row-block
+  // partials use the same memory before the first group
+  __shared__ __attribute__((aligned(16))) float s_ps[2][kWaves][PPG * kPage];
+  __shared__ __attribute__((aligned(16))) float s_p[kWaves][PPG * kPage];  // per-wave probabilities
+  __shared__ float s_zn[kMaxRank];
+  static_assert(2 * kWaves * PPG * kPage >= kThreads * 8, "prologue partials do not fit");
+  float* const s_part = &s_ps[0][0][0];
+
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int b = blockIdx.x, h = blockIdx.y;
+  const int N = a.ctx_len ? a.ctx_len[b] : a.n_ctx;
+  const bool bad = (N < 1) || (N > a.n_ctx);
+  const int pages = bad ? 0 : (N + kPage - 1) / kPage;
+  const size_t unit = (size_t)b * a.H + h;
+  const int rk = a.rk, rv = a.rv, dr = a.dr;
+  const int rq0 = (rk + 7) & ~7;  // s_qt slot of the first rotary row
+
+  const int hi = lane >> 3, lo = lane & 7;  // K: page hi, slice lo; V: row hi of the group, slice lo
+  const BufRsrc rk_src = make_rsrc(static_cast<const TIn*>(a.ck) + unit * (size_t)a.n_max * rk,
+                                   (size_t)a.n_max * rk * ES);
+  const BufRsrc rv_src = make_rsrc(static_cast<const TIn*>(a.cv) + unit * (size_t)a.n_max * rv,
+                                   (size_t)a.n_max * rv * ES);
+  const size_t bhr = (size_t)b * a.Hr + (a.Hr == 1 ? 0 : h);
+  const BufRsrc rr_src = make_rsrc(dr ? static_cast<const TIn*>(a.rc) + bhr * (size_t)a.n_max * dr
+                                      : static_cast<const TIn*>(a.ck),
+                                   (size_t)a.n_max * dr * ES);
+  const int kpage_bytes = kPage * rk * ES, vpage_bytes = kPage * rv * ES, rpage_bytes = kPage * dr * ES;
+  const int k_oob = a.n_max * rk * ES, v_oob = a.n_max * rv * ES, r_oob = a.n_max * dr * ES;
+  const int k_lane = hi * kpage_bytes + lo * 16, r_lane = hi * rpage_bytes + lo * 16;
+  const int v_lane = hi * kPage * ES + lo * 16;
+  const int nkb = (rk + 7) / 8, ntb = nkb + dr / 8;  // 8-row K blocks (content, then rotary)
+  const int nmk = ntb > wave ? (ntb - 1 - wave) / kWaves + 1 : 0;  // this wave's K blocks
+  const int nvg = (rv + 7) / 8;                                    // 8-row value groups
+  const int nmv = nvg > wave ? (nvg - 1 - wave) / kWaves + 1 : 0;  // this wave's value groups
+
+  // K block i of this wave over the group at page g0 (np pages): 8 rows, all
+  // 8 loads issued by every lane
+  auto kload = [&](uint4 (&r)[KB], int i, int g0, int np) {
+    const int blk = wave + i * kWaves;
+    const bool rot = blk >= nkb;
+    const BufRsrc src = rot ? rr_src : rk_src;
+    const int lim = rot ? dr : rk, oob = rot ? r_oob : k_oob;
+    const int base = hi < np ? (rot ? r_lane : k_lane) : oob;
+    const int pbase = g0 * (rot ? rpage_bytes : kpage_bytes);
+    const int r0 = (rot ? blk - nkb : blk) * 8;
+#pragma unroll
+    for (int u = 0; u < KB; ++u) {
+      const int row = r0 + u;
+      const bool ok = row < lim;
+      r[u] = buf_ld16(src, ok ? base : oob, ok ? pbase + row * kPage * ES : 0);
+    }
+  };
+  auto kfma = [&](const uint4 (&r)[KB], int i, float (&acc)[EPL]) {
+    const int blk = wave + i * kWaves;
+    const int q0 = blk < nkb ? blk * 8 : rq0 + (blk - nkb) * 8;
+    float qj[KB];
+#pragma unroll
+    for (int u = 0; u < KB; u += 4) {
+      const float4 qa = *reinterpret_cast<const float4*>(&s_qt[q0 + u]);
+      qj[u] = qa.x;
+      qj[u + 1] = qa.y;
+      qj[u + 2] = qa.z;
+      qj[u + 3] = qa.w;
+    }
+#pragma unroll
+    for (int u = 0; u < KB; ++u) {
+      float v[EPL];
+      Elem<TIn>::unpack(r[u], v);
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) acc[e] = fmaf(qj[u], v[e], acc[e]);
+    }
+  };
+  // half pg0 / VH of value row group k of this wave over the group at page g0
+  auto vload = [&](uint4 (&r)[VH], int k, int pg0, int g0, int np) {
+    const int row0 = (wave + k * kWaves) * 8;
+    const bool ok = row0 + hi < rv;
+#pragma unroll
+    for (int u = 0; u < VH; ++u) {
+      const bool pok = pg0 + u < np;
+      r[u] = buf_ld16(rv_src, ok && pok ? v_lane : v_oob,
+                      pok ? (g0 + pg0 + u) * vpage_bytes + row0 * kPage * ES : 0);
+    }
+  };
+
+  uint4 ka[KB], kb2[KB], va[VH], vb[VH];
+
+  // ---- prologue: q~ = U_k^T q (scale * log2 e folded in), then the rotary query ----
+  {
+    const TIn* qp = static_cast<const TIn*>(a.q) + unit * a.d;
+    for (int i = tid; i < a.d; i += kThreads) s_q[i] = Elem<TIn>::get(qp, i);
+    __syncthreads();
+    const TIn* uk = static_cast<const TIn*>(a.uk) + (size_t)h * a.d * rk;
+    switch (vec_width<TIn>(rk)) {
+      case 8: absorb_query<TIn, 8, kThreads>(uk, a.d, rk, a.qscale, s_q, s_part, s_qt); break;
+      case 4: absorb_query<TIn, 4, kThreads>(uk, a.d, rk, a.qscale, s_q, s_part, s_qt); break;
+      case 2: absorb_query<TIn, 2, kThreads>(uk, a.d, rk, a.qscale, s_q, s_part, s_qt); break;
+      default: absorb_query<TIn, 1, kThreads>(uk, a.d, rk, a.qscale, s_q, s_part, s_qt); break;
+    }
+    for (int j = rk + tid; j < rq0; j += kThreads) s_qt[j] = 0.f;
+    if (dr) {
+      const TIn* qr = static_cast<const TIn*>(a.qr) + unit * dr;
+      for (int i = tid; i < dr; i += kThreads) s_qt[rq0 + i] = a.qscale * Elem<TIn>::get(qr, i);
+    }
+    __syncthreads();
+  }
+
+  float zacc[GVW];
+#pragma unroll
+  for (int k = 0; k < GVW; ++k) zacc[k] = 0.f;
+  float m_run = neg_inf(), l_lane = 0.f;
+
+  int buf = 0;
+  for (int g0 = 0; g0 < pages; g0 += PPG, buf ^= 1) {
+    const int np = min(PPG, pages - g0);
+
+    // ---- K phase: this wave's row blocks over all pages of the group ----
+    float acc[EPL];
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) acc[e] = 0.f;
+    if (nmk > 0) kload(ka, 0, g0, np);
+    for (int i = 0; i < nmk; i += 2) {
+      if (i + 1 < nmk) kload(kb2, i + 1, g0, np);
+      kfma(ka, i, acc);
+      if (i + 2 < nmk) kload(ka, i + 2, g0, np);
+      if (i + 1 < nmk) kfma(kb2, i + 1, acc);
+    }
+    float* ps = &s_ps[buf][0][0];
+#pragma unroll
+    for (int e = 0; e < EPL; e += 4)
+      *reinterpret_cast<float4*>(&ps[wave * PPG * kPage + hi * kPage + lo * EPL + e]) =
+          make_float4(acc[e], acc[e + 1], acc[e + 2], acc[e + 3]);
+    __syncthreads();
+    // the four partials, summed in wave order (identical in every wavefront)
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) acc[e] = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+#pragma unroll
+      for (int e = 0; e < EPL; e += 4) {
+        const float4 t = *reinterpret_cast<const float4*>(&ps[w * PPG * kPage + hi * kPage + lo * EPL + e]);
+        acc[e] += t.x;
+        acc[e + 1] += t.y;
+        acc[e + 2] += t.z;
+        acc[e + 3] += t.w;
+      }
+    }
+
+    // ---- softmax over the group (pages past the context and tokens past N: -inf) ----
+    const int n0 = (g0 + hi) * kPage + lo * EPL;
+    float mb = neg_inf();
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) {
+      if (hi >= np || n0 + e >= N) acc[e] = neg_inf();
+      mb = fmaxf(mb, acc[e]);
+    }
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) mb = fmaxf(mb, xor_shfl(mb, off));
+    if (mb > m_run) {
+      const float alpha = fast_exp2(m_run - mb);
+      l_lane *= alpha;
+#pragma unroll
+      for (int k = 0; k < GVW; ++k) zacc[k] *= alpha;
+      m_run = mb;
+    }
+    float* sp = s_p[wave];
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) {
+      acc[e] = fast_exp2(acc[e] - m_run);
+      l_lane += acc[e];
+    }
+#pragma unroll
+    for (int e = 0; e < EPL; e += 4)
+      *reinterpret_cast<float4*>(&sp[hi * kPage + lo * EPL + e]) =
+          make_float4(acc[e], acc[e + 1], acc[e + 2], acc[e + 3]);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+    // ---- V phase: this wave's value row groups over all pages of the group ----
+    // The probabilities of lane (rg, ts) are those of token slice ts of every
+    // page: 64 registers, read once per group.  Each row group is loaded in two
+    // halves of 4 pages, one half always in flight.
+    float p8[PPG][EPL];
+#pragma unroll
+    for (int pg = 0; pg < PPG; ++pg) {
+#pragma unroll
+      for (int e = 0; e < EPL; e += 4) {
+        const float4 t = *reinterpret_cast<const float4*>(&sp[pg * kPage + lo * EPL + e]);
+        p8[pg][e] = t.x;
+        p8[pg][e + 1] = t.y;
+        p8[pg][e + 2] = t.z;
+        p8[pg][e + 3] = t.w;
+      }
+    }
+    // value slots past N may hold anything: their weight is 0 and their value
+    // is zeroed (an attended NaN still propagates)
+    const int tail_pg = (N - 1) / kPage - g0;  // page of the group holding position N - 1
+    auto vfma = [&](const uint4 (&r)[VH], auto pg0c, float& t) {
+      constexpr int pg0 = decltype(pg0c)::value;
+#pragma unroll
+      for (int u = 0; u < VH; ++u) {
+        float v[EPL];
+        Elem<TIn>::unpack(r[u], v);
+        if (pg0 + u == tail_pg) {
+          const int nv0 = (g0 + pg0 + u) * kPage + lo * EPL;
+#pragma unroll
+          for (int e = 0; e < EPL; ++e)
+            if (nv0 + e >= N) v[e] = 0.f;
+        }
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) t = fmaf(p8[pg0 + u][e], v[e], t);
+      }
+    };
+    if (nmv > 0) vload(va, 0, 0, g0, np);
+    for (int k = 0; k < nmv; ++k) {
+      float t = 0.f;
+      vload(vb, k, VH, g0, np);
+      vfma(va, std::integral_constant<int, 0>{}, t);
+      if (k + 1 < nmv) vload(va, k + 1, 0, g0, np);
+      vfma(vb, std::integral_constant<int, VH>{}, t);
+#pragma unroll
+      for (int kk = 0; kk < GVW; ++kk)
+        if (kk == k) zacc[kk] += t;
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+
+  // ---- this wave's z rows: reduce over the token slices, normalise ----
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) l_lane += xor_shfl(l_lane, off);
+#pragma unroll
+  for (int off = 1; off < 8; off <<= 1)
+#pragma unroll
+    for (int k = 0; k < GVW; ++k) zacc[k] += xor_shfl(zacc[k], off);
+  if (lo == 0) {
+#pragma unroll
+    for (int k = 0; k < GVW; ++k) {
+      const int j = (wave + k * kWaves) * 8 + hi;
+      if (k < nmv && j < rv) s_zn[j] = zacc[k] / l_lane;
+    }
+  }
+  __syncthreads();
+
+  // ---- value epilogue: out = U_v z + mu_v ----
+  const TIn* uv = static_cast<const TIn*>(a.uv) + (size_t)h * a.d * rv;
+  const TIn* muv = a.muv ? static_cast<const TIn*>(a.muv) + (size_t)h * a.d : nullptr;
+  const size_t obase = unit * a.d;
+  switch (vec_width<TIn>(rv)) {
+    case 8: value_epilogue<TIn, 8, kThreads>(uv, muv, a.d, rv, s_zn, bad, a.out_dtype, a.out, obase); break;
+    case 4: value_epilogue<TIn, 4, kThreads>(uv, muv, a.d, rv, s_zn, bad, a.out_dtype, a.out, obase); break;
+    case 2: value_epilogue<TIn, 2, kThreads>(uv, muv, a.d, rv, s_zn, bad, a.out_dtype, a.out, obase); break;
+    default: value_epilogue<TIn, 1, kThreads>(uv, muv, a.d, rv, s_zn, bad, a.out_dtype, a.out, obase); break;
+  }
+}
+
 template <typename TIn, int GV>
 hipError_t launch_t(const DecodeArgs& a, hipStream_t stream) {
   dim3 grid(a.B * a.M * a.splits, a.H);
+  if (a.shortk) {  // short contexts, rows split over the wavefronts: bf16, decode, not split
+    if constexpr (sizeof(TIn) == 2) {
+      if (a.splits != 1 || a.causal || a.M != 1) return hipErrorInvalidValue;
+      hipLaunchKernelGGL((decode_short_kernel<GV>), grid, dim3(4 * kWave), 0, stream, a);
+      return hipGetLastError();
+    } else {
+      return hipErrorInvalidValue;
+    }
+  }
   if (a.half) {  // short contexts: bf16, 4 wavefronts, pipelined
     if constexpr (sizeof(TIn) == 2) {
       if (a.waves != 4 || !a.deep) return hipErrorInvalidValue;

@@ -71,7 +71,7 @@ size_t workspace_bytes(int B, int H, int r_v, int n_ctx) {
 // wavefronts) use the 4-page K groups.  LLA_DECODE_WAVES / LLA_DECODE_SPLITS /
 // LLA_DECODE_DEEP / LLA_DECODE_HALF override the choice (for tuning sweeps).
 struct DecodeShape {
-  int waves, splits, deep, half;
+  int waves, splits, deep, half, shortk;
 };
 
 int env_int(const char* name) {
@@ -79,18 +79,21 @@ int env_int(const char* name) {
   return e ? std::atoi(e) : 0;
 }
 
+constexpr int kShortPages = 16;
+
 DecodeShape choose_shape(int units, int n_ctx, bool allow_split, bool bf16) {
   static const int forced_waves = env_int("LLA_DECODE_WAVES");
   static const int forced_splits = env_int("LLA_DECODE_SPLITS");
   static const int forced_deep = env_int("LLA_DECODE_DEEP");
   static const int forced_half = env_int("LLA_DECODE_HALF");
+  static const int forced_short = env_int("LLA_DECODE_SHORT");
   const int pages = (n_ctx + LLA_PAGE_TOKENS - 1) / LLA_PAGE_TOKENS;
   const int groups = (pages + 7) / 8;
   const long target = 8L * lla::device_cu_count();  // resident wavefronts wanted
   // bf16: the software-pipelined variant (two batches of loads in flight per
   // wavefront, at most 2 wavefronts per SIMD) measured as fast or faster on
   // every decode workload; fp32 keeps the 4-per-SIMD variant.
-  DecodeShape sh{4, 1, bf16 ? 1 : 0, 0};
+  DecodeShape sh{4, 1, bf16 ? 1 : 0, 0, 0};
   if ((long)units * 4 < target && groups >= 8) sh.waves = 8;
   if (allow_split && (long)units * sh.waves < target) {
     long s = (target + (long)units * sh.waves - 1) / ((long)units * sh.waves);
@@ -109,6 +112,12 @@ DecodeShape choose_shape(int units, int n_ctx, bool allow_split, bool bf16) {
     const int per = (pages + sh.splits - 1) / sh.splits;
     sh.half = (per + 7) / 8 < sh.waves ? 1 : 0;
     if (forced_half) sh.half = forced_half > 0 ? 1 : 0;
+  }
+  // at most kShortPages pages: the wavefronts split the feature rows of each
+  // 8-page group (one workgroup per (b, h), not split)
+  if (bf16 && sh.waves == 4 && sh.splits == 1) {
+    sh.shortk = pages <= kShortPages ? 1 : 0;
+    if (forced_short) sh.shortk = forced_short > 0 ? 1 : 0;
   }
   return sh;
 }
@@ -378,6 +387,7 @@ lla_status decode_impl(int dtype, int out_dtype, int B, int H, int d_head, int r
   a.splits = sh.splits;
   a.deep = sh.deep;
   a.half = sh.half;
+  a.shortk = sh.shortk;
   const hipStream_t st = static_cast<hipStream_t>(stream);
   if (static_scratch) {
     // partials of exactly the chosen split count, in the device's static array

@@ -19,6 +19,7 @@ struct DecodeArgs {
   int waves;   // wavefronts per workgroup (4 or 8)
   int deep;    // 1: at most 2 wavefronts per SIMD, 16-row load batches
   int half;    // 1 (bf16, 4 waves, deep): K groups of 4 pages, two feature rows per load
+  int shortk;  // 1 (bf16 decode, not split): wavefronts split the rows of each 8-page group
   const int32_t* ctx_len;
   const void* q;
   const void* ck;

@@ -36,8 +36,10 @@ __device__ __forceinline__ void rope_cs(int p, double inv_freq, float& c, float&
   sincosf((float)r, &s, &c);
 }
 
-// One thread per (b, m, pair i): the angle is shared by the G heads of the
-// row, so cos and sin are formed once and applied G times.
+// One thread per (row, pair i): every head's row is its own thread, so the
+// loads of a call are all in flight at once (a loop over the heads would wait
+// on each head's load in turn, since the output may alias the input); the
+// angle is recomputed per head, bit for bit the same.
 // Write: row (b, m, g) of x [B][M][G][dr] is rotated at position pos0 + m and
 // lands in that position's slot of the paged cache of (b, g).
 template <typename T>
@@ -46,22 +48,21 @@ __global__ __launch_bounds__(256) void rope_write_kernel(RopeArgs a) {
   inv_freq_table(s_inv, a.dr, a.base);
   const int half = a.dr / 2;
   const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (size_t)a.B * a.M * half) return;
-  const size_t bm = idx / half;
-  const int i = (int)(idx - bm * half);
+  if (idx >= (size_t)a.B * a.M * a.G * half) return;
+  const size_t row = idx / half;  // (b, m, g)
+  const int i = (int)(idx - row * half);
+  const int g = (int)(row % a.G);
+  const size_t bm = row / a.G;
   const int m = (int)(bm % a.M), b = (int)(bm / a.M);
   const int pos = a.pos0 + m;
   const int slot = ring_slot(pos, a.sink, a.window);  // rotated at its true position, stored at its slot
   float c, s;
   rope_cs(pos, s_inv[i], c, s);
+  const float x1 = load_elem<T>(a.x, row * a.dr + i), x2 = load_elem<T>(a.x, row * a.dr + i + half);
   T* y = static_cast<T*>(a.y);
-  for (int g = 0; g < a.G; ++g) {
-    const size_t row = bm * a.G + g;
-    const float x1 = load_elem<T>(a.x, row * a.dr + i), x2 = load_elem<T>(a.x, row * a.dr + i + half);
-    const size_t page = ((size_t)(b * a.G + g) * a.n_max + (size_t)(slot / kPage) * kPage) * a.dr;
-    store_out(y, page + (size_t)i * kPage + slot % kPage, x1 * c - x2 * s);
-    store_out(y, page + (size_t)(i + half) * kPage + slot % kPage, x2 * c + x1 * s);
-  }
+  const size_t page = ((size_t)(b * a.G + g) * a.n_max + (size_t)(slot / kPage) * kPage) * a.dr;
+  store_out(y, page + (size_t)i * kPage + slot % kPage, x1 * c - x2 * s);
+  store_out(y, page + (size_t)(i + half) * kPage + slot % kPage, x2 * c + x1 * s);
 }
 
 // Rotate: row (b, g, m) of x [B][G][M][dr] at position (pos ? pos[b] : pos0) + m.
@@ -71,24 +72,21 @@ __global__ __launch_bounds__(256) void rope_rotate_kernel(RopeArgs a) {
   inv_freq_table(s_inv, a.dr, a.base);
   const int half = a.dr / 2;
   const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (size_t)a.B * a.M * half) return;
-  const size_t bm = idx / half;
-  const int i = (int)(idx - bm * half);
-  const int m = (int)(bm % a.M), b = (int)(bm / a.M);
+  if (idx >= (size_t)a.B * a.G * a.M * half) return;
+  const size_t row = idx / half;  // (b, g, m)
+  const int i = (int)(idx - row * half);
+  const int m = (int)(row % a.M), b = (int)(row / ((size_t)a.G * a.M));
   const int pos = (a.pos ? a.pos[b] : a.pos0) + m;
   float c, s;
   rope_cs(pos, s_inv[i], c, s);
+  const float x1 = load_elem<T>(a.x, row * a.dr + i), x2 = load_elem<T>(a.x, row * a.dr + i + half);
   T* y = static_cast<T*>(a.y);
-  for (int g = 0; g < a.G; ++g) {
-    const size_t row = ((size_t)b * a.G + g) * a.M + m;
-    const float x1 = load_elem<T>(a.x, row * a.dr + i), x2 = load_elem<T>(a.x, row * a.dr + i + half);
-    store_out(y, row * a.dr + i, x1 * c - x2 * s);
-    store_out(y, row * a.dr + i + half, x2 * c + x1 * s);
-  }
+  store_out(y, row * a.dr + i, x1 * c - x2 * s);
+  store_out(y, row * a.dr + i + half, x2 * c + x1 * s);
 }
 
 dim3 grid_for(const RopeArgs& a) {
-  const size_t n = (size_t)a.B * a.M * (a.dr / 2);
+  const size_t n = (size_t)a.B * a.M * a.G * (a.dr / 2);
   return dim3((unsigned)((n + 255) / 256));
 }
 

@@ -85,18 +85,23 @@ def test_decode_rope(dtype, r_k, r_v, dr, Hr, N):
     assert_close(f64(out), ref, dtype, "decode rope")
 
 
-@pytest.mark.parametrize("r_k,r_v,dr,Hr", [(17, 30, 8, 1), (33, 160, 24, 4), (95, 9, 40, 1), (1, 1, 8, 4)])
-def test_decode_rope_short_context_row_pairs(r_k, r_v, dr, Hr):
-    """bf16 contexts of fewer than 25 pages are scanned in K groups of 4 pages,
-    each wave-wide load covering two feature rows: an odd r_k, or a rotary
-    width that is not a multiple of 16, leaves the last pair half past its
-    range.  The per-sequence lengths give groups of 1 to 4 pages and ragged
-    last pages."""
-    wl, B, N, n_max = SMALL, 3, 1500, 1536
+@pytest.mark.parametrize("r_k,r_v,dr,Hr", [(17, 30, 8, 1), (33, 160, 24, 4), (95, 9, 40, 1), (1, 1, 8, 4),
+                                           (7, 300, 64, 1)])
+@pytest.mark.parametrize("N,lens", [(1500, [1500, 700, 65]), (1000, [1000, 513, 1])])
+def test_decode_rope_short_context(r_k, r_v, dr, Hr, N, lens):
+    """Short bf16 contexts.  At 17 to 24 pages the K phase takes groups of 4
+    pages, each wave-wide load covering two feature rows: an odd r_k, or a
+    rotary width that is not a multiple of 16, leaves the last pair half past
+    its range.  At up to 16 pages the wavefronts split the feature rows of
+    each 8-page group (8-row blocks of content and rotary rows, 8-row value
+    groups): ranks that are not multiples of 8 or 32 leave blocks and groups
+    partly past their range.  The per-sequence lengths give partial groups,
+    ragged last pages and a one-token context."""
+    wl, B, n_max = SMALL, 3, 1536
     dtype = torch.bfloat16
-    log(f"decode rope short context r=({r_k},{r_v}) dr={dr} Hr={Hr}")
+    log(f"decode rope short context N={N} r=({r_k},{r_v}) dr={dr} Hr={Hr}")
     ck, cv, kr, q, qr, uk, uv, muk, muv, rc = _decode_case(wl, r_k, r_v, dr, Hr, B, N, n_max, dtype, True)
-    lens = torch.tensor([1500, 700, 65], dtype=torch.int32, device=DEV)
+    lens = torch.tensor(lens, dtype=torch.int32, device=DEV)
     qr_rot = lla.rope_rotate(qr, pos=lens - 1)
     out = lla.decode_attn(q, lla.to_paged(ck, n_max), lla.to_paged(cv, n_max), uk, uv, n_ctx=N, ctx_len=lens,
                           mu_k=muk, mu_v=muv, q_rope=qr_rot, r_cache=rc)
