@@ -97,6 +97,38 @@ __device__ void absorb_query(const T* uk, int d, int rk, float qscale, const flo
   __syncthreads();
 }
 
+// q~[j] = qscale * sum_i U_k[i][j] q[i], with each thread reading the q
+// entries of its rows straight from memory (no wait between the q and U_k
+// loads) and at most 8 row blocks, so the final fixed-order sum is short.
+template <typename T, int VW, int kThreads>
+__device__ void absorb_query_direct(const T* uk, const T* qp, int d, int rk, float qscale,
+                                    float* s_part, float* s_qt) {
+  const int nch = rk / VW;
+  const int rb = nch >= kThreads / 8 ? max(1, kThreads / nch) : 8;
+  for (int f = threadIdx.x; f < nch * rb; f += kThreads) {
+    const int jc = f % nch, ib = f / nch;
+    float acc[VW];
+#pragma unroll
+    for (int e = 0; e < VW; ++e) acc[e] = 0.f;
+#pragma unroll 8
+    for (int i = ib; i < d; i += rb) {
+      float u[VW];
+      load_vec<T, VW>(uk + (size_t)i * rk + jc * VW, u);
+      const float qi = Elem<T>::get(qp, i);
+#pragma unroll
+      for (int e = 0; e < VW; ++e) acc[e] = fmaf(u[e], qi, acc[e]);
+    }
+#pragma unroll
+    for (int e = 0; e < VW; ++e) s_part[ib * rk + jc * VW + e] = acc[e];
+  }
+  __syncthreads();
+  for (int j = threadIdx.x; j < rk; j += kThreads) {
+    float s = 0.f;
+    for (int ib = 0; ib < rb; ++ib) s += s_part[ib * rk + j];
+    s_qt[j] = s * qscale;
+  }
+}
+
 // out[i] = sum_j U_v[i][j] zn[j] (+ mu_v[i]).  P consecutive threads share a
 // row and split its column chunks; their partials combine by xor shuffles.
 template <typename T, int VW, int kThreads>
@@ -603,7 +635,6 @@ void decode_short_kernel(DecodeArgs a) {
   constexpr int VH = PPG / 2;                 // pages per V half-batch
   constexpr int GVW = (GV + kWaves - 1) / kWaves;  // value row groups per wavefront
   constexpr int ES = 2;
-  __shared__ float s_q[kMaxHead];
   __shared__ __attribute__((aligned(16))) float s_qt[kMaxRank];
   // partial scores [buffer][wave][page*64 + token]; the prologue's row-block
   // partials use the same memory before the first group
@@ -695,14 +726,12 @@ void decode_short_kernel(DecodeArgs a) {
   // ---- prologue: q~ = U_k^T q (scale * log2 e folded in), then the rotary query ----
   {
     const TIn* qp = static_cast<const TIn*>(a.q) + unit * a.d;
-    for (int i = tid; i < a.d; i += kThreads) s_q[i] = Elem<TIn>::get(qp, i);
-    __syncthreads();
     const TIn* uk = static_cast<const TIn*>(a.uk) + (size_t)h * a.d * rk;
     switch (vec_width<TIn>(rk)) {
-      case 8: absorb_query<TIn, 8, kThreads>(uk, a.d, rk, a.qscale, s_q, s_part, s_qt); break;
-      case 4: absorb_query<TIn, 4, kThreads>(uk, a.d, rk, a.qscale, s_q, s_part, s_qt); break;
-      case 2: absorb_query<TIn, 2, kThreads>(uk, a.d, rk, a.qscale, s_q, s_part, s_qt); break;
-      default: absorb_query<TIn, 1, kThreads>(uk, a.d, rk, a.qscale, s_q, s_part, s_qt); break;
+      case 8: absorb_query_direct<TIn, 8, kThreads>(uk, qp, a.d, rk, a.qscale, s_part, s_qt); break;
+      case 4: absorb_query_direct<TIn, 4, kThreads>(uk, qp, a.d, rk, a.qscale, s_part, s_qt); break;
+      case 2: absorb_query_direct<TIn, 2, kThreads>(uk, qp, a.d, rk, a.qscale, s_part, s_qt); break;
+      default: absorb_query_direct<TIn, 1, kThreads>(uk, qp, a.d, rk, a.qscale, s_part, s_qt); break;
     }
     for (int j = rk + tid; j < rq0; j += kThreads) s_qt[j] = 0.f;
     if (dr) {
