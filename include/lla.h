@@ -339,7 +339,7 @@ lla_status lla_decode_attn_fullrope(int dtype, int out_dtype, int B, int H, int 
  *   r_cache paged rotary cache (layout above), dtype, capacity n_max
  *   base    the RoPE base (e.g. 10000), > 1
  *
- * Requires 0 <= pos0, pos0 + M <= n_max.  Writes exactly the slots
+ * Requires 0 <= pos0, pos0 + M <= n_max, H_rope <= 65535.  Writes exactly the slots
  * [pos0, pos0 + M) of every (b, g); angles are formed in double precision and
  * the result rounded to dtype (RNE for bf16).
  * Errors: LLA_ERR_INVALID_ARG, LLA_ERR_HIP.
@@ -352,7 +352,7 @@ lla_status lla_rope_write(int dtype, int B, int M, int H_rope, int d_rope, const
  *   x, y  [B][G][M][d_rope] of dtype (y may not alias x)
  * Row (b, g, m) is rotated at position (pos ? pos[b] : pos0) + m, where pos is
  * an optional device int32 [B] (for decode: each sequence's newest position,
- * N_b - 1; for prefill: pos0 = p0 with M the new tokens).
+ * N_b - 1; for prefill: pos0 = p0 with M the new tokens).  G <= 65535.
  * Errors: LLA_ERR_INVALID_ARG, LLA_ERR_HIP.
  */
 lla_status lla_rope_rotate(int dtype, int B, int G, int M, int d_rope, const void* x,

@@ -241,7 +241,7 @@ lla_status encode_impl(int dtype, int B, int M, int H, int T, int d_head, int r_
 lla_status rope_write_impl(int dtype, int B, int M, int H_rope, int d_rope, const void* k_rope,
                            double base, void* r_cache, int n_max, int pos0, int sink, int window,
                            void* stream) {
-  if (!dtype_ok(dtype) || B < 1 || M < 1 || H_rope < 1 || !rope_ok(d_rope) || !cap_ok(n_max) ||
+  if (!dtype_ok(dtype) || B < 1 || M < 1 || H_rope < 1 || H_rope > 65535 || !rope_ok(d_rope) || !cap_ok(n_max) ||
       !slots_ok(M, n_max, pos0, sink, window) || !std::isfinite(base) || !(base > 1.0))
     return LLA_ERR_INVALID_ARG;
   if ((int64_t)B * M * H_rope * d_rope > (1LL << 34) || !ptr_ok(k_rope) || !ptr_ok(r_cache))
@@ -687,7 +687,7 @@ lla_status lla_rope_write_ring(int dtype, int B, int M, int H_rope, int d_rope, 
 
 lla_status lla_rope_rotate(int dtype, int B, int G, int M, int d_rope, const void* x,
                            const int32_t* pos, int pos0, double base, void* y, void* stream) {
-  if (!dtype_ok(dtype) || B < 1 || G < 1 || M < 1 || !rope_ok(d_rope) || pos0 < 0 ||
+  if (!dtype_ok(dtype) || B < 1 || G < 1 || G > 65535 || M < 1 || !rope_ok(d_rope) || pos0 < 0 ||
       !std::isfinite(base) || !(base > 1.0))
     return LLA_ERR_INVALID_ARG;
   if ((int64_t)B * G * M * d_rope > (1LL << 34) || !ptr_ok(x) || !ptr_ok(y) ||

@@ -287,6 +287,7 @@ def _rope_write(**kw):
 @pytest.mark.parametrize("kw", [
     dict(dtype=2), dict(B=0), dict(M=0), dict(Hr=0), dict(dr=6), dict(dr=0), dict(x=None), dict(rc=MIS),
     dict(n_max=100), dict(pos0=-1), dict(pos0=505), dict(base=1.0), dict(base=float("nan")),
+    dict(Hr=65536, M=1, B=1),
 ])
 def test_rope_write_rejects(kw):
     assert _rope_write(**kw) == lla.LLA_ERR_INVALID_ARG
@@ -301,7 +302,7 @@ def _rope_rotate(**kw):
 
 @pytest.mark.parametrize("kw", [
     dict(dtype=5), dict(B=0), dict(G=0), dict(M=0), dict(dr=10), dict(x=None), dict(y=MIS),
-    dict(pos=P + 2), dict(pos0=-3), dict(base=0.5),
+    dict(pos=P + 2), dict(pos0=-3), dict(base=0.5), dict(G=65536),
 ])
 def test_rope_rotate_rejects(kw):
     assert _rope_rotate(**kw) == lla.LLA_ERR_INVALID_ARG
