@@ -641,6 +641,12 @@ void decode_short_kernel(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) float s_ps[2][kWaves][PPG * kPage];
   __shared__ __attribute__((aligned(16))) float s_p[kWaves][PPG * kPage];  // per-wave probabilities
   __shared__ float s_zn[kMaxRank];
+  // U_v of this head when it fits (d_head * r_v * 2 bytes, r_v <= 64 at d_head 128): requested
+  // before the query absorption and written to LDS after it (its loads return before the
+  // absorption's own), so the epilogue pays no memory latency
+  constexpr bool kUvPre = GV <= 8;
+  constexpr int kUvBytes = kUvPre ? 16384 : 16;
+  __shared__ __attribute__((aligned(16))) bf16_t s_uv[kUvBytes / 2];
   static_assert(2 * kWaves * PPG * kPage >= kThreads * 8, "prologue partials do not fit");
   float* const s_part = &s_ps[0][0][0];
 
@@ -722,6 +728,18 @@ void decode_short_kernel(DecodeArgs a) {
   };
 
   uint4 ka[KB], kb2[KB], va[VH], vb[VH];
+  const TIn* uv_g = static_cast<const TIn*>(a.uv) + (size_t)h * a.d * rv;
+  const bool uv_pre = kUvPre && a.d * rv * 2 <= kUvBytes;  // uniform
+  const int n_uv16 = a.d * rv * 2 / 16;                     // d_head is a multiple of 32: whole 16-byte pieces
+  constexpr int kUvPer = kUvBytes / 16 / kThreads > 0 ? kUvBytes / 16 / kThreads : 1;
+  uint4 uvr[kUvPer];
+  if (uv_pre) {
+#pragma unroll
+    for (int k = 0; k < kUvPer; ++k) {
+      const int e = tid + k * kThreads;
+      uvr[k] = e < n_uv16 ? reinterpret_cast<const uint4*>(uv_g)[e] : uint4{0, 0, 0, 0};
+    }
+  }
 
   // ---- prologue: q~ = U_k^T q (scale * log2 e folded in), then the rotary query ----
   {
@@ -739,6 +757,13 @@ void decode_short_kernel(DecodeArgs a) {
       for (int i = tid; i < dr; i += kThreads) s_qt[rq0 + i] = a.qscale * Elem<TIn>::get(qr, i);
     }
     __syncthreads();
+  }
+  if (uv_pre) {  // read by the epilogue, after the final barrier
+#pragma unroll
+    for (int k = 0; k < kUvPer; ++k) {
+      const int e = tid + k * kThreads;
+      if (e < n_uv16) reinterpret_cast<uint4*>(s_uv)[e] = uvr[k];
+    }
   }
 
   float zacc[GVW];
@@ -879,7 +904,7 @@ void decode_short_kernel(DecodeArgs a) {
   __syncthreads();
 
   // ---- value epilogue: out = U_v z + mu_v ----
-  const TIn* uv = static_cast<const TIn*>(a.uv) + (size_t)h * a.d * rv;
+  const TIn* uv = uv_pre ? s_uv : uv_g;
   const TIn* muv = a.muv ? static_cast<const TIn*>(a.muv) + (size_t)h * a.d : nullptr;
   const size_t obase = unit * a.d;
   switch (vec_width<TIn>(rv)) {
