@@ -377,34 +377,42 @@ __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
-template <int AXIS>
-__device__ __forceinline__ void encode_gemm_body(const EncodeArgs& a, int tb, int rb, bf16_t (*s_x)[kGTok * kGS],
-                                                 bf16_t (*s_w)[kGRow * kGS], float* s_mu) {
+// AXIS: 0 keys, 1 values.  TM: the output cache is token-major (the LLA-2D key
+// cache); the products then hold rows in a lane's registers (one token per
+// lane), else 4 consecutive tokens of one row, which feature-major pages store
+// as 8 bytes.
+template <int AXIS, bool TM>
+__device__ __forceinline__ void encode_gemm_body(const EncodeArgs& a, int tb, int rb, int h0, int nh,
+                                                 bf16_t (*s_x)[kGTok * kGS], bf16_t (*s_w)[kGRow * kGS],
+                                                 float* s_mu) {
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int col = lane & 31, g = lane >> 5;
   constexpr int axis = AXIS;
   const int row0 = rb * kGRow;
-  const int r = pick(a.r, axis), K = a.K, H = a.H, h = blockIdx.y;
+  const int r = pick(a.r, axis), K = a.K, H = a.H;
   const int TT = a.B * a.M, t0 = tb * kGTok;
   const bf16_t* xg = static_cast<const bf16_t*>(pick(a.x, axis));
-  const bf16_t* wg = static_cast<const bf16_t*>(pick(a.wdt, axis)) + (size_t)h * r * K;
-  const int nkc = K / kGKC;
+  const bf16_t* wg = static_cast<const bf16_t*>(pick(a.wdt, axis));
+  // The workgroup walks heads h0 .. h0 + nh - 1 as one stream of K-chunks
+  // (chunk q: head h0 + q / nkc, K offset (q % nkc) * kGKC), so the loads of a
+  // head's first chunks are in flight while the previous head finishes.
+  const int nkc = K / kGKC, total = nh * nkc;
 
   // staging: x chunk = 256 tokens x 64 (4 chunks of 16 bytes per thread),
   // W chunk = 96 rows x 64 (768 chunks: threads 0 .. 255 take two)
   uint4 sxa[4], swa[2], sxb[4], swb[2];  // two register sets, named at compile time
-  auto load = [&](int kc, uint4 (&sx)[4], uint4 (&sw)[2]) {
-    const int k0 = kc * kGKC;
+  auto load = [&](int q, uint4 (&sx)[4], uint4 (&sw)[2]) {
+    const int hq = q / nkc, hh = h0 + hq, k0 = (q - hq * nkc) * kGKC;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int c = tid + i * kGThreads, tok = c >> 3, part = c & 7, t = t0 + tok;
-      sx[i] = ld16(xg + ((size_t)(t < TT ? t : TT - 1) * H + h) * K + k0 + 8 * part);
+      sx[i] = ld16(xg + ((size_t)(t < TT ? t : TT - 1) * H + hh) * K + k0 + 8 * part);
     }
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int c = tid + i * kGThreads, row = row0 + (c >> 3), part = c & 7;
-      sw[i] = ld16(wg + (size_t)(row < r ? row : r - 1) * K + k0 + 8 * part);
+      sw[i] = ld16(wg + ((size_t)hh * r + (row < r ? row : r - 1)) * K + k0 + 8 * part);
     }
   };
   auto store = [&](const uint4 (&sx)[4], const uint4 (&sw)[2], int buf) {
@@ -425,9 +433,9 @@ __device__ __forceinline__ void encode_gemm_body(const EncodeArgs& a, int tb, in
 #pragma unroll
   for (int rt = 0; rt < 3; ++rt) acc[rt] = f32x16{0.f};
   const bool mu = pick(a.mu, axis) != nullptr;  // uniform
-  const bf16_t* mug = mu ? static_cast<const bf16_t*>(pick(a.mu, axis)) + (size_t)h * K + 8 * g : nullptr;
+  const bf16_t* mug = mu ? static_cast<const bf16_t*>(pick(a.mu, axis)) + 8 * g : nullptr;
 
-  auto chunk = [&](int kc, int buf) {
+  auto chunk = [&](int q, int buf) {
     const bf16_t* xs = &s_x[buf][(32 * wave + col) * kGS + 8 * g];
     const bf16_t* ws = &s_w[buf][col * kGS + 8 * g];
 #pragma unroll
@@ -436,7 +444,7 @@ __device__ __forceinline__ void encode_gemm_body(const EncodeArgs& a, int tb, in
 #pragma unroll
       for (int rt = 0; rt < 3; ++rt) {
         const bf16x8 wo = as_bf16x8(*reinterpret_cast<const uint4*>(ws + 32 * rt * kGS + 16 * s));
-        acc[rt] = axis == 0 ? mfma32(wo, xo, acc[rt]) : mfma32(xo, wo, acc[rt]);
+        acc[rt] = TM ? mfma32(wo, xo, acc[rt]) : mfma32(xo, wo, acc[rt]);
       }
     }
     // the mean's products in one block after the chunk's (a guard inside the
@@ -446,99 +454,119 @@ __device__ __forceinline__ void encode_gemm_body(const EncodeArgs& a, int tb, in
 #pragma unroll
       for (int s = 0; s < kGKC / 16; ++s) {
         wm[s] = *reinterpret_cast<const uint4*>(ws + 32 * wave * kGS + 16 * s);
-        mo[s] = ld16(mug + kc * kGKC + 16 * s);
+        mo[s] = ld16(mug + (size_t)(h0 + q / nkc) * K + (q % nkc) * kGKC + 16 * s);
       }
 #pragma unroll
       for (int s = 0; s < kGKC / 16; ++s) accm = mfma32(as_bf16x8(wm[s]), as_bf16x8(mo[s]), accm);
     }
   };
 
-  // set a holds even chunks, set b odd ones; chunk kc is in LDS buffer kc % 2
-  load(0, sxa, swa);
-  load(nkc > 1 ? 1 : 0, sxb, swb);
-  store(sxa, swa, 0);
-  __syncthreads();
-  for (int kc = 0; kc < nkc; kc += 2) {
-    load(min(kc + 2, nkc - 1), sxa, swa);
-    chunk(kc, 0);
-    if (kc + 1 < nkc) store(sxb, swb, 1);
-    __syncthreads();
-    if (kc + 1 < nkc) {
-      load(min(kc + 3, nkc - 1), sxb, swb);
-      chunk(kc + 1, 1);
-      if (kc + 2 < nkc) store(sxa, swa, 0);
+  // head hh done: the mean's products to LDS, the tile to the cache, then the
+  // accumulators cleared for the next head
+  auto finish = [&](int hh_) {
+    // Opaque copies: the epilogue's row and token bookkeeping is then formed
+    // here, per head, instead of being hoisted out of the head loop, where it
+    // would hold registers across every chunk.
+    int hh = hh_, r = pick(a.r, axis), row0 = rb * kGRow, t0 = tb * kGTok;
+    asm volatile("" : "+s"(hh), "+s"(r), "+s"(row0), "+s"(t0));
+    if (mu) {
+      // accm (M = row of tile `wave`, N = any column): rows 8(q/4) + 4g + q%4
+      if (wave < 3 && col == 0) {
+#pragma unroll
+        for (int q = 0; q < 16; ++q) s_mu[32 * wave + 8 * (q / 4) + 4 * g + q % 4] = accm[q];
+      }
       __syncthreads();
     }
-  }
-  if (mu) {
-    // accm (M = row of tile `wave`, N = any column): rows 8(q/4) + 4g + q%4
-    if (wave < 3 && col == 0) {
-#pragma unroll
-      for (int q = 0; q < 16; ++q) s_mu[32 * wave + 8 * (q / 4) + 4 * g + q % 4] = accm[q];
-    }
-    __syncthreads();
-  }
 
-  bf16_t* cout = static_cast<bf16_t*>(pick(a.c, axis));
-  if (axis == 0) {
-    // lane (token col, half g), register q of row tile rt: row 32 rt + 8(q/4) + 4g + q%4
-    const int t = t0 + 32 * wave + col;
-    if (t < TT) {
-      const int b = t / a.M, pos = ring_slot(a.pos0 + (t - b * a.M), a.sink, a.window);
-      const bool tm = a.k_token_major != 0;
+    bf16_t* cout = static_cast<bf16_t*>(pick(a.c, axis));
+    if constexpr (TM) {
+      // lane (token col, half g), register q of row tile rt: row 32 rt + 8(q/4) + 4g + q%4
+      const int t = t0 + 32 * wave + col;
+      if (t < TT) {
+        const int b = t / a.M, pos = ring_slot(a.pos0 + (t - b * a.M), a.sink, a.window);
 #pragma unroll
-      for (int rt = 0; rt < 3; ++rt)
+        for (int rt = 0; rt < 3; ++rt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int rl = 32 * rt + 8 * i + 4 * g, row = row0 + rl;  // first of 4 consecutive rows
+            if (row + 3 < r) {
+              // token-major cache: the 4 rows are contiguous, 8-byte aligned (r_k % 32 == 0)
+              const uint32_t lo = uint32_t(f32_to_bf16(acc[rt][4 * i] - (mu ? s_mu[rl] : 0.f))) |
+                                  (uint32_t(f32_to_bf16(acc[rt][4 * i + 1] - (mu ? s_mu[rl + 1] : 0.f))) << 16);
+              const uint32_t hi = uint32_t(f32_to_bf16(acc[rt][4 * i + 2] - (mu ? s_mu[rl + 2] : 0.f))) |
+                                  (uint32_t(f32_to_bf16(acc[rt][4 * i + 3] - (mu ? s_mu[rl + 3] : 0.f))) << 16);
+              *reinterpret_cast<uint2*>(&cout[cache_index(b, hh, H, a.n_max, r, pos, row, true)]) = make_uint2(lo, hi);
+            } else {
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                if (row + e < r)
+                  cout[cache_index(b, hh, H, a.n_max, r, pos, row + e, true)] =
+                      f32_to_bf16(acc[rt][4 * i + e] - (mu ? s_mu[rl + e] : 0.f));
+            }
+          }
+      }
+    } else {
+      // lane (row col of tile rt, half g), register q: token 32 wave + 8(q/4) + 4g + q%4,
+      // so registers 4i .. 4i + 3 are 4 consecutive tokens of one feature row.
+      // When their slots are 4 consecutive positions of one page (one sequence,
+      // no ring, position a multiple of 4) they are one 8-byte store.
+#pragma unroll
+      for (int rt = 0; rt < 3; ++rt) {
+        const int rl = 32 * rt + col, row = row0 + rl;
+        if (row >= r) continue;
+        const float m = mu ? s_mu[rl] : 0.f;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int rl = 32 * rt + 8 * i + 4 * g, row = row0 + rl;  // first of 4 consecutive rows
-          if (tm && row + 3 < r) {
-            // token-major cache: the 4 rows are contiguous, 8-byte aligned (r_k % 32 == 0)
-            const uint32_t lo = uint32_t(f32_to_bf16(acc[rt][4 * i] - (mu ? s_mu[rl] : 0.f))) |
-                                (uint32_t(f32_to_bf16(acc[rt][4 * i + 1] - (mu ? s_mu[rl + 1] : 0.f))) << 16);
-            const uint32_t hi = uint32_t(f32_to_bf16(acc[rt][4 * i + 2] - (mu ? s_mu[rl + 2] : 0.f))) |
-                                (uint32_t(f32_to_bf16(acc[rt][4 * i + 3] - (mu ? s_mu[rl + 3] : 0.f))) << 16);
-            *reinterpret_cast<uint2*>(&cout[cache_index(b, h, H, a.n_max, r, pos, row, true)]) = make_uint2(lo, hi);
+          const int t = t0 + 32 * wave + 8 * i + 4 * g;  // first token of the run
+          const int b = t / a.M, m0 = t - b * a.M, p = a.pos0 + m0;
+          if (a.window == 0 && t + 3 < TT && m0 + 3 < a.M && (p & 3) == 0) {
+            const uint32_t lo = uint32_t(f32_to_bf16(acc[rt][4 * i] - m)) |
+                                (uint32_t(f32_to_bf16(acc[rt][4 * i + 1] - m)) << 16);
+            const uint32_t hi = uint32_t(f32_to_bf16(acc[rt][4 * i + 2] - m)) |
+                                (uint32_t(f32_to_bf16(acc[rt][4 * i + 3] - m)) << 16);
+            *reinterpret_cast<uint2*>(&cout[cache_index(b, hh, H, a.n_max, r, p, row)]) = make_uint2(lo, hi);
           } else {
 #pragma unroll
-            for (int e = 0; e < 4; ++e)
-              if (row + e < r)
-                cout[cache_index(b, h, H, a.n_max, r, pos, row + e, tm)] =
-                    f32_to_bf16(acc[rt][4 * i + e] - (mu ? s_mu[rl + e] : 0.f));
-          }
-        }
-    }
-  } else {
-    // lane (row col of tile rt, half g), register q: token 32 wave + 8(q/4) + 4g + q%4,
-    // so registers 4i .. 4i + 3 are 4 consecutive tokens of one feature row.
-    // When their slots are 4 consecutive positions of one page (one sequence,
-    // no ring, position a multiple of 4) they are one 8-byte store.
-#pragma unroll
-    for (int rt = 0; rt < 3; ++rt) {
-      const int rl = 32 * rt + col, row = row0 + rl;
-      if (row >= r) continue;
-      const float m = mu ? s_mu[rl] : 0.f;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int t = t0 + 32 * wave + 8 * i + 4 * g;  // first token of the run
-        const int b = t / a.M, m0 = t - b * a.M, p = a.pos0 + m0;
-        if (a.window == 0 && t + 3 < TT && m0 + 3 < a.M && (p & 3) == 0) {
-          const uint32_t lo = uint32_t(f32_to_bf16(acc[rt][4 * i] - m)) |
-                              (uint32_t(f32_to_bf16(acc[rt][4 * i + 1] - m)) << 16);
-          const uint32_t hi = uint32_t(f32_to_bf16(acc[rt][4 * i + 2] - m)) |
-                              (uint32_t(f32_to_bf16(acc[rt][4 * i + 3] - m)) << 16);
-          *reinterpret_cast<uint2*>(&cout[cache_index(b, h, H, a.n_max, r, p, row)]) = make_uint2(lo, hi);
-        } else {
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int te = t + e;
-            if (te < TT) {
-              const int be = te / a.M, pos = ring_slot(a.pos0 + (te - be * a.M), a.sink, a.window);
-              cout[cache_index(be, h, H, a.n_max, r, pos, row)] = f32_to_bf16(acc[rt][4 * i + e] - m);
+            for (int e = 0; e < 4; ++e) {
+              const int te = t + e;
+              if (te < TT) {
+                const int be = te / a.M, pos = ring_slot(a.pos0 + (te - be * a.M), a.sink, a.window);
+                cout[cache_index(be, hh, H, a.n_max, r, pos, row)] = f32_to_bf16(acc[rt][4 * i + e] - m);
+              }
             }
           }
         }
       }
     }
+#pragma unroll
+    for (int rt = 0; rt < 3; ++rt) acc[rt] = f32x16{0.f};
+    accm = f32x16{0.f};
+  };
+
+  // set a holds even chunks, set b odd ones; chunk q is in LDS buffer q % 2
+  // (nkc is even whenever a workgroup takes more than one head, so every head
+  // starts on set a).  Each head's last chunk is followed, after the barrier,
+  // by its epilogue; the barriers of the next head's chunks order its use of
+  // LDS against the next epilogue.
+  load(0, sxa, swa);
+  load(total > 1 ? 1 : 0, sxb, swb);
+  store(sxa, swa, 0);
+  __syncthreads();
+  for (int hq = 0; hq < nh; ++hq) {
+    const int qe = (hq + 1) * nkc;  // end of this head's chunks
+    for (int q = hq * nkc; q < qe; q += 2) {
+      load(min(q + 2, total - 1), sxa, swa);
+      chunk(q, 0);
+      if (q + 1 < total) store(sxb, swb, 1);
+      __syncthreads();
+      if (q + 1 < qe) {
+        load(min(q + 3, total - 1), sxb, swb);
+        chunk(q + 1, 1);
+        if (q + 2 < total) store(sxa, swa, 0);
+        __syncthreads();
+      }
+    }
+    finish(h0 + hq);
   }
 }
 
@@ -547,17 +575,20 @@ __device__ __forceinline__ void encode_gemm_body(const EncodeArgs& a, int tb, in
 // j-th workgroup of XCD x takes token block x + 8 (j / nrb) and row block
 // j % nrb (the row blocks of axis k, then those of axis v).
 __global__ __launch_bounds__(kGThreads) __attribute__((amdgpu_waves_per_eu(2)))
-void encode_gemm_kernel(EncodeArgs a, int nrb_k, int nrb, int ntb) {
+void encode_gemm_kernel(EncodeArgs a, int nrb_k, int nrb, int ntb, int hpw) {
   __shared__ __attribute__((aligned(16))) bf16_t s_x[2][kGTok * kGS];
   __shared__ __attribute__((aligned(16))) bf16_t s_w[2][kGRow * kGS];
   __shared__ float s_mu[kGRow];
   const int xcd = blockIdx.x % 8, j = blockIdx.x / 8;
   const int tb = xcd + 8 * (j / nrb), rb = j % nrb;
   if (tb >= ntb) return;  // padding of the grid to whole rounds of 8 token blocks
-  if (rb < nrb_k)
-    encode_gemm_body<0>(a, tb, rb, s_x, s_w, s_mu);
+  const int h0 = blockIdx.y * hpw, nh = min(hpw, a.H - h0);  // a run of heads
+  if (rb >= nrb_k)
+    encode_gemm_body<1, false>(a, tb, rb - nrb_k, h0, nh, s_x, s_w, s_mu);
+  else if (a.k_token_major)
+    encode_gemm_body<0, true>(a, tb, rb, h0, nh, s_x, s_w, s_mu);
   else
-    encode_gemm_body<1>(a, tb, rb - nrb_k, s_x, s_w, s_mu);
+    encode_gemm_body<0, false>(a, tb, rb, h0, nh, s_x, s_w, s_mu);
 }
 
 // Second launch of a split write: tile unit (grid x, y, z as the split launch
@@ -627,6 +658,12 @@ __global__ __launch_bounds__(256) void encode_f32_kernel(EncodeArgs a) {
 
 }  // namespace
 
+static int gemm_heads_per_wg(int H, int blocks, int nkc) {
+  if (nkc % 2) return 1;  // a run of heads needs every head to start on the same register set
+  const int hpw = (int)((int64_t)H * blocks / 1024);
+  return hpw < 1 ? 1 : hpw > H ? H : hpw;
+}
+
 int encode_ksplit(int TT, int K) {
   if (TT > 64 || K < 2048) return 1;
   const int s = K / 512;  // 16 K-steps (one round of loads) per split
@@ -675,7 +712,12 @@ hipError_t launch_encode(const EncodeArgs& a, hipStream_t stream) {
       // tiled for the MFMAs, x re-read from L2 per row block
       const int ntb = (TT + kGTok - 1) / kGTok, ntb8 = (ntb + 7) / 8 * 8;
       const int nrb_k = (a.r[0] + kGRow - 1) / kGRow, nrb = nrb_k + (a.r[1] + kGRow - 1) / kGRow;
-      hipLaunchKernelGGL(encode_gemm_kernel, dim3(nrb * ntb8, a.H), dim3(kGThreads), 0, stream, a, nrb_k, nrb, ntb);
+      // heads per workgroup: as many as keep at least 1024 workgroups (four
+      // rounds of the machine), so short stacks (per-head writes) do not pay
+      // the pipeline fill and the epilogue per head on their own
+      const int hpw = gemm_heads_per_wg(a.H, nrb * ntb8, a.K / kGKC);
+      hipLaunchKernelGGL(encode_gemm_kernel, dim3(nrb * ntb8, (a.H + hpw - 1) / hpw), dim3(kGThreads), 0, stream, a,
+                         nrb_k, nrb, ntb, hpw);
       return hipGetLastError();
     }
     const int heads_per_wg = blocks >= 256 ? a.H : 1;
