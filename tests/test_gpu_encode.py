@@ -151,3 +151,27 @@ def test_encode_many_tokens_tier_ranks(r_k, r_v, T, d, B, M, pos0, means):
     log(f"encode tier ranks r=({r_k},{r_v}) K={T * d} B={B} M={M} pos0={pos0} means={means}")
     inputs, ck, cv = _run(wl, r_k, r_v, B, M, pos0, n_max, means, torch.bfloat16)
     _check(wl, inputs, ck, cv, pos0, M, torch.bfloat16, f"M={M}")
+
+
+@pytest.mark.parametrize("r_k,r_v,T,d,H,B,M,pos0,runs", [
+    # 3 row blocks x 48 token blocks x 15 heads: 2 heads per workgroup, the last group 1
+    (96, 160, 4, 128, 15, 2, 6000, 5, 2),
+    # 8 row blocks x 24 token blocks x 16 heads: 3 heads per workgroup, the last group 1
+    (288, 480, 4, 128, 16, 1, 4100, 64, 3),
+    # K = 192: an odd chunk count per head, so one head per workgroup
+    (96, 160, 3, 64, 16, 1, 12000, 0, 1),
+])
+@pytest.mark.parametrize("means", [False, True])
+def test_encode_gemm_head_runs(r_k, r_v, T, d, H, B, M, pos0, runs, means):
+    """Prompt-sized per-head writes where a GEMM workgroup walks a run of heads
+    (as many as keep 1024 workgroups), including a last run shorter than the
+    others; every latent is checked against the oracle."""
+    ntb = (B * M + 255) // 256
+    blocks = ((r_k + 95) // 96 + (r_v + 95) // 96) * ((ntb + 7) // 8 * 8)
+    nkc = T * d // 64
+    assert runs == (1 if nkc % 2 else max(1, min(H, H * blocks // 1024))), "case no longer takes the intended runs"
+    wl = W.Workload(f"enc_runs_{T}_{d}_{H}", 1, H, d, T, B, 0, ((r_k, r_v),), torch.bfloat16)
+    n_max = ((pos0 + M + 63) // 64) * 64 + 64
+    log(f"encode head runs r=({r_k},{r_v}) K={T * d} H={H} B={B} M={M} pos0={pos0} runs={runs} means={means}")
+    inputs, ck, cv = _run(wl, r_k, r_v, B, M, pos0, n_max, means, torch.bfloat16)
+    _check(wl, inputs, ck, cv, pos0, M, torch.bfloat16, f"H={H} M={M}")
