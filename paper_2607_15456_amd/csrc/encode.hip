@@ -371,6 +371,7 @@ __global__ __launch_bounds__(256) void encode_few_kernel(EncodeArgs a, int nrc_k
 // after the first read.  With a mean, wavefronts 0 .. 2 also form W_down^T mu
 // for one 32-row tile each (mu as a broadcast operand), shared through LDS.
 constexpr int kGTok = 256, kGRow = 96, kGKC = 64, kGS = kGKC + 8;
+constexpr int kGTS = kGTok + 8;  // row stride (bf16) of the epilogue's output tile in LDS
 constexpr int kGThreads = 512;
 
 __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
@@ -384,7 +385,7 @@ __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
 template <int AXIS, bool TM>
 __device__ __forceinline__ void encode_gemm_body(const EncodeArgs& a, int tb, int rb, int h0, int nh,
                                                  bf16_t (*s_x)[kGTok * kGS], bf16_t (*s_w)[kGRow * kGS],
-                                                 float* s_mu) {
+                                                 float* s_mu, bf16_t* s_t) {
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int col = lane & 31, g = lane >> 5;
@@ -508,31 +509,43 @@ __device__ __forceinline__ void encode_gemm_body(const EncodeArgs& a, int tb, in
     } else {
       // lane (row col of tile rt, half g), register q: token 32 wave + 8(q/4) + 4g + q%4,
       // so registers 4i .. 4i + 3 are 4 consecutive tokens of one feature row.
-      // When their slots are 4 consecutive positions of one page (one sequence,
-      // no ring, position a multiple of 4) they are one 8-byte store.
+      // The tile goes through LDS as [row][token] bf16, then runs of 8 threads
+      // store a row's 64 tokens of one page as 128 contiguous bytes (16 bytes
+      // each) when the slots are 8 consecutive positions of one sequence (no
+      // ring, a position a multiple of 8), else one element at a time.
 #pragma unroll
       for (int rt = 0; rt < 3; ++rt) {
-        const int rl = 32 * rt + col, row = row0 + rl;
-        if (row >= r) continue;
+        const int rl = 32 * rt + col;
         const float m = mu ? s_mu[rl] : 0.f;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int t = t0 + 32 * wave + 8 * i + 4 * g;  // first token of the run
-          const int b = t / a.M, m0 = t - b * a.M, p = a.pos0 + m0;
-          if (a.window == 0 && t + 3 < TT && m0 + 3 < a.M && (p & 3) == 0) {
-            const uint32_t lo = uint32_t(f32_to_bf16(acc[rt][4 * i] - m)) |
-                                (uint32_t(f32_to_bf16(acc[rt][4 * i + 1] - m)) << 16);
-            const uint32_t hi = uint32_t(f32_to_bf16(acc[rt][4 * i + 2] - m)) |
-                                (uint32_t(f32_to_bf16(acc[rt][4 * i + 3] - m)) << 16);
-            *reinterpret_cast<uint2*>(&cout[cache_index(b, hh, H, a.n_max, r, p, row)]) = make_uint2(lo, hi);
-          } else {
+          const uint32_t lo = uint32_t(f32_to_bf16(acc[rt][4 * i] - m)) |
+                              (uint32_t(f32_to_bf16(acc[rt][4 * i + 1] - m)) << 16);
+          const uint32_t hi = uint32_t(f32_to_bf16(acc[rt][4 * i + 2] - m)) |
+                              (uint32_t(f32_to_bf16(acc[rt][4 * i + 3] - m)) << 16);
+          *reinterpret_cast<uint2*>(&s_t[rl * kGTS + 32 * wave + 8 * i + 4 * g]) = make_uint2(lo, hi);
+        }
+      }
+      __syncthreads();
+      constexpr int kItems = kGRow * (kGTok / 8) / kGThreads;  // 16-byte pieces per thread
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const int te = t + e;
-              if (te < TT) {
-                const int be = te / a.M, pos = ring_slot(a.pos0 + (te - be * a.M), a.sink, a.window);
-                cout[cache_index(be, hh, H, a.n_max, r, pos, row)] = f32_to_bf16(acc[rt][4 * i + e] - m);
-              }
+      for (int k = 0; k < kItems; ++k) {
+        const int item = tid + k * kGThreads, rl = item / (kGTok / 8), grp = item % (kGTok / 8);
+        const int row = row0 + rl;
+        if (row >= r) continue;
+        const uint4 v = *reinterpret_cast<const uint4*>(&s_t[rl * kGTS + 8 * grp]);
+        const int t = t0 + 8 * grp;  // first token of the piece
+        const int b = t / a.M, m0 = t - b * a.M, p = a.pos0 + m0;
+        if (a.window == 0 && t + 7 < TT && m0 + 7 < a.M && (p & 7) == 0) {
+          *reinterpret_cast<uint4*>(&cout[cache_index(b, hh, H, a.n_max, r, p, row)]) = v;
+        } else {
+          const bf16_t* e8 = reinterpret_cast<const bf16_t*>(&v);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int te = t + e;
+            if (te < TT) {
+              const int be = te / a.M, pos = ring_slot(a.pos0 + (te - be * a.M), a.sink, a.window);
+              cout[cache_index(be, hh, H, a.n_max, r, pos, row)] = e8[e];
             }
           }
         }
@@ -579,16 +592,17 @@ void encode_gemm_kernel(EncodeArgs a, int nrb_k, int nrb, int ntb, int hpw) {
   __shared__ __attribute__((aligned(16))) bf16_t s_x[2][kGTok * kGS];
   __shared__ __attribute__((aligned(16))) bf16_t s_w[2][kGRow * kGS];
   __shared__ float s_mu[kGRow];
+  __shared__ __attribute__((aligned(16))) bf16_t s_t[kGRow * kGTS];  // epilogue tile (feature-major outputs)
   const int xcd = blockIdx.x % 8, j = blockIdx.x / 8;
   const int tb = xcd + 8 * (j / nrb), rb = j % nrb;
   if (tb >= ntb) return;  // padding of the grid to whole rounds of 8 token blocks
   const int h0 = blockIdx.y * hpw, nh = min(hpw, a.H - h0);  // a run of heads
   if (rb >= nrb_k)
-    encode_gemm_body<1, false>(a, tb, rb - nrb_k, h0, nh, s_x, s_w, s_mu);
+    encode_gemm_body<1, false>(a, tb, rb - nrb_k, h0, nh, s_x, s_w, s_mu, s_t);
   else if (a.k_token_major)
-    encode_gemm_body<0, true>(a, tb, rb, h0, nh, s_x, s_w, s_mu);
+    encode_gemm_body<0, true>(a, tb, rb, h0, nh, s_x, s_w, s_mu, s_t);
   else
-    encode_gemm_body<0, false>(a, tb, rb, h0, nh, s_x, s_w, s_mu);
+    encode_gemm_body<0, false>(a, tb, rb, h0, nh, s_x, s_w, s_mu, s_t);
 }
 
 // Second launch of a split write: tile unit (grid x, y, z as the split launch
