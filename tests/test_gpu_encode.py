@@ -175,3 +175,37 @@ def test_encode_gemm_head_runs(r_k, r_v, T, d, H, B, M, pos0, runs, means):
     log(f"encode head runs r=({r_k},{r_v}) K={T * d} H={H} B={B} M={M} pos0={pos0} runs={runs} means={means}")
     inputs, ck, cv = _run(wl, r_k, r_v, B, M, pos0, n_max, means, torch.bfloat16)
     _check(wl, inputs, ck, cv, pos0, M, torch.bfloat16, f"H={H} M={M}")
+
+
+@pytest.mark.parametrize("r_k,r_v,means", [(96, 160, False), (200, 8, True)])
+def test_encode_gemm_ring_slots(r_k, r_v, means):
+    """Prompt-sized chunks at ranks above 64 (the GEMM write) streamed into a
+    sink + window ring cache whose positions wrap: every kept position's slot
+    holds the oracle's latent of that token (later tokens overwrite earlier ones)."""
+    sink, window, chunks = 4, 512, [300, 500, 260]  # at most `window` tokens per call
+    wl = W.Workload("enc_ring_gemm", 1, 4, 128, 4, 2, 0, ((r_k, r_v),), torch.bfloat16)
+    B, H, K = wl.B, wl.H, wl.T * wl.d
+    n_max = ((sink + window + 63) // 64) * 64
+    wk = W.down_projection(wl, r_k, "k", 0, DEV, torch.bfloat16)
+    wv = W.down_projection(wl, r_v, "v", 0, DEV, torch.bfloat16)
+    muk = W.stacked_mean(wl, "k", 0, DEV, torch.bfloat16) if means else None
+    muv = W.stacked_mean(wl, "v", 0, DEV, torch.bfloat16) if means else None
+    ck = lla.alloc_cache(B, H, n_max, r_k, device=DEV)
+    cv = lla.alloc_cache(B, H, n_max, r_v, device=DEV)
+    refs_k, refs_v, pos = [], [], 0
+    for i, M in enumerate(chunks):
+        xk = W.normal((B, M, H, K), ("enc_ring_gemm", "x_k", i), 1.0, torch.bfloat16, DEV)
+        xv = W.normal((B, M, H, K), ("enc_ring_gemm", "x_v", i), 1.0, torch.bfloat16, DEV)
+        log(f"ring GEMM write r=({r_k},{r_v}) chunk {i}: M={M} pos0={pos} means={means}")
+        lla.encode(xk, xv, wk, wv, ck, cv, T=wl.T, pos0=pos, mu_k=muk, mu_v=muv, evict=(sink, window))
+        refs_k.append(oracle.encode_batched(f64(xk), None if muk is None else f64(muk), f64(wk)))
+        refs_v.append(oracle.encode_batched(f64(xv), None if muv is None else f64(muv), f64(wv)))
+        pos += M
+    torch.cuda.synchronize()
+    keep = oracle.kept_positions(pos, sink, window)
+    slots = [oracle.ring_slot(p, sink, window) for p in keep]
+    assert sorted(slots) == list(range(sink + window)), "kept positions must fill every slot once"
+    for refs, c, name in ((refs_k, ck, "K"), (refs_v, cv, "V")):
+        ref = np.concatenate(refs, axis=2)[:, :, keep]          # [B, H, kept, r]
+        got = f64(lla.from_paged(c))[:, :, slots]
+        assert_close(got, ref, torch.bfloat16, f"ring GEMM write {name}")
