@@ -380,8 +380,9 @@ __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
 
 // AXIS: 0 keys, 1 values.  TM: the output cache is token-major (the LLA-2D key
 // cache); the products then hold rows in a lane's registers (one token per
-// lane), else 4 consecutive tokens of one row, which feature-major pages store
-// as 8 bytes.
+// lane), stored as 8 bytes of 4 consecutive features.  Otherwise a lane's
+// register groups hold 4 consecutive tokens of one row, and the tile reaches
+// the feature-major pages through LDS as whole 128-byte page rows.
 template <int AXIS, bool TM>
 __device__ __forceinline__ void encode_gemm_body(const EncodeArgs& a, int tb, int rb, int h0, int nh,
                                                  bf16_t (*s_x)[kGTok * kGS], bf16_t (*s_w)[kGRow * kGS],
