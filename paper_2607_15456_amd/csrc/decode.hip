@@ -560,12 +560,12 @@ void decode_kernel(DecodeArgs a) {
       part[0] = mg;
       part[1] = lg;
     }
-    // Every wavefront releases its own partial stores at agent scope (a
-    // workgroup barrier alone does not carry them to other compute units);
-    // thread 0's counter update then publishes the arrival, and the last
+    // Every wavefront's partial stores reach L2 before the barrier; thread
+    // 0's counter update is then the workgroup's one agent-scope release (one
+    // L2 write-back covering them all) and publishes the arrival, and the last
     // arrival's acquire (by thread 0, then the barrier) makes every split's
     // partial visible to the whole workgroup.
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    wait_stores_in_l2();
     __syncthreads();
     if (tid == 0) {
       const uint32_t prev =

@@ -486,9 +486,11 @@ void fullrope_mfma_kernel(FullRopeArgs a) {
       part[0] = s_ml[0];
       part[1] = s_ml[1];
     }
-    // each wavefront releases its partial stores at agent scope; the last
-    // arrival's acquire makes every split's partial visible
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    // every wavefront's partial stores reach L2 before the barrier; thread
+    // 0's counter update is the workgroup's one agent-scope release (one L2
+    // write-back), and the last arrival's acquire makes every split's partial
+    // visible
+    wait_stores_in_l2();
     __syncthreads();
     if (tid == 0) {
       const uint32_t prev =

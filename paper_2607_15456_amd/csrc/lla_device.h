@@ -64,6 +64,15 @@ __device__ __forceinline__ uint4 ld16_nt(const void* p) {
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 
+// Waits until this wavefront's earlier global stores are acknowledged by L2.
+// Split-K partials: every wavefront waits this way, then after a workgroup
+// barrier one thread's agent-scope release (a single L2 write-back) publishes
+// the whole workgroup's stores.  A workgroup-scope release alone does not wait
+// for outstanding stores (all wavefronts of a workgroup share one compute
+// unit), so without it a wavefront's stores could still be in flight when that
+// write-back runs.
+__device__ __forceinline__ void wait_stores_in_l2() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
 // ---- cross-lane ----------------------------------------------------------
 
 __device__ __forceinline__ float xor_shfl(float v, int mask) { return __shfl_xor(v, mask, kWave); }
