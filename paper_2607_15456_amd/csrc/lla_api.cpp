@@ -67,8 +67,9 @@ size_t workspace_bytes(int B, int H, int r_v, int n_ctx) {
 // wavefronts (4-wave workgroups when (b, h) units alone reach that, 8-wave
 // ones otherwise); only smaller batches split the context (split-K), up to 8
 // wavefronts per compute unit, with every wavefront keeping at least one
-// 8-page group.  Short bf16 contexts (fewer 8-page groups per workgroup than
-// wavefronts) use the 4-page K groups.  LLA_DECODE_WAVES / LLA_DECODE_SPLITS /
+// 8-page group (bf16: one 4-page group, in 4-wavefront workgroups, when 8-page
+// groups would fill less than half the machine).  Short bf16 contexts (fewer
+// 8-page groups per workgroup than wavefronts) use the 4-page K groups.  LLA_DECODE_WAVES / LLA_DECODE_SPLITS /
 // LLA_DECODE_DEEP / LLA_DECODE_HALF override the choice (for tuning sweeps).
 struct DecodeShape {
   int waves, splits, deep, half, shortk;
@@ -99,6 +100,18 @@ DecodeShape choose_shape(int units, int n_ctx, bool allow_split, bool bf16) {
     long s = (target + (long)units * sh.waves - 1) / ((long)units * sh.waves);
     const long cap = groups / sh.waves > 0 ? groups / sh.waves : 1;
     if (s > cap) s = cap;
+    // bf16: when whole 8-page groups per wavefront leave the machine under half
+    // full, 4-wavefront workgroups with one 4-page group per wavefront (the
+    // two-rows-per-load K phase) reach further
+    if (bf16 && (long)units * sh.waves * s < target / 2) {
+      const long cap4 = pages / 16 > 0 ? pages / 16 : 1;
+      long s4 = (target + (long)units * 4 - 1) / ((long)units * 4);
+      if (s4 > cap4) s4 = cap4;
+      if (4 * s4 > (long)sh.waves * s) {
+        sh.waves = 4;
+        s = s4;
+      }
+    }
     sh.splits = (int)s;
   }
   if (forced_waves == 4 || forced_waves == 8) sh.waves = forced_waves;
