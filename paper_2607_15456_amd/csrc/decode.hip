@@ -927,10 +927,13 @@ hipError_t launch_t(const DecodeArgs& a, hipStream_t stream) {
       return hipErrorInvalidValue;
     }
   }
-  if (a.half) {  // short contexts: bf16, 4 wavefronts, pipelined
+  if (a.half) {  // 4-page K groups: bf16, pipelined, 4 or 8 wavefronts
     if constexpr (sizeof(TIn) == 2) {
-      if (a.waves != 4 || !a.deep) return hipErrorInvalidValue;
-      hipLaunchKernelGGL((decode_kernel<TIn, GV, 4, true, true>), grid, dim3(4 * kWave), 0, stream, a);
+      if (!a.deep || (a.waves != 4 && a.waves != 8)) return hipErrorInvalidValue;
+      if (a.waves == 8)
+        hipLaunchKernelGGL((decode_kernel<TIn, GV, 8, true, true>), grid, dim3(8 * kWave), 0, stream, a);
+      else
+        hipLaunchKernelGGL((decode_kernel<TIn, GV, 4, true, true>), grid, dim3(4 * kWave), 0, stream, a);
       return hipGetLastError();
     } else {
       return hipErrorInvalidValue;

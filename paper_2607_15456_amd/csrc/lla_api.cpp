@@ -67,9 +67,9 @@ size_t workspace_bytes(int B, int H, int r_v, int n_ctx) {
 // wavefronts (4-wave workgroups when (b, h) units alone reach that, 8-wave
 // ones otherwise); only smaller batches split the context (split-K), up to 8
 // wavefronts per compute unit, with every wavefront keeping at least one
-// 8-page group (bf16: one 4-page group, in 4-wavefront workgroups, when 8-page
-// groups would fill less than half the machine).  Short bf16 contexts (fewer
-// 8-page groups per workgroup than wavefronts) use the 4-page K groups.  LLA_DECODE_WAVES / LLA_DECODE_SPLITS /
+// 8-page group (bf16: one 4-page group when that fills more of the machine).
+// bf16 workgroups with fewer 8-page groups than wavefronts use the 4-page K
+// groups.  LLA_DECODE_WAVES / LLA_DECODE_SPLITS /
 // LLA_DECODE_DEEP / LLA_DECODE_HALF override the choice (for tuning sweeps).
 struct DecodeShape {
   int waves, splits, deep, half, shortk;
@@ -97,19 +97,26 @@ DecodeShape choose_shape(int units, int n_ctx, bool allow_split, bool bf16) {
   DecodeShape sh{4, 1, bf16 ? 1 : 0, 0, 0};
   if ((long)units * 4 < target && groups >= 8) sh.waves = 8;
   if (allow_split && (long)units * sh.waves < target) {
-    long s = (target + (long)units * sh.waves - 1) / ((long)units * sh.waves);
-    const long cap = groups / sh.waves > 0 ? groups / sh.waves : 1;
-    if (s > cap) s = cap;
-    // bf16: when whole 8-page groups per wavefront leave the machine under half
-    // full, 4-wavefront workgroups with one 4-page group per wavefront (the
-    // two-rows-per-load K phase) reach further
-    if (bf16 && (long)units * sh.waves * s < target / 2) {
-      const long cap4 = pages / 16 > 0 ? pages / 16 : 1;
-      long s4 = (target + (long)units * 4 - 1) / ((long)units * 4);
-      if (s4 > cap4) s4 = cap4;
-      if (4 * s4 > (long)sh.waves * s) {
-        sh.waves = 4;
-        s = s4;
+    // splits that bring units * waves * splits to the target, each wavefront
+    // keeping at least `cap`'s share of pages
+    auto fill = [&](int w, long cap) {
+      const long s = (target + (long)units * w - 1) / ((long)units * w);
+      return s < cap ? s : (cap > 0 ? cap : 1L);
+    };
+    long s = fill(sh.waves, groups / sh.waves);
+    // bf16: when whole 8-page groups per wavefront leave the machine short of
+    // the target, one 4-page group per wavefront (the two-rows-per-load K
+    // phase) reaches further: the same workgroup size first, then 4
+    // wavefronts; ties keep the fewer splits
+    if (bf16) {
+      long best = (long)units * sh.waves * s;
+      for (const int w : {sh.waves, 4}) {
+        const long s4 = fill(w, pages / (4 * w));
+        if ((long)units * w * s4 > best) {
+          best = (long)units * w * s4;
+          sh.waves = w;
+          s = s4;
+        }
       }
     }
     sh.splits = (int)s;
@@ -121,7 +128,7 @@ DecodeShape choose_shape(int units, int n_ctx, bool allow_split, bool bf16) {
   if (forced_deep) sh.deep = forced_deep > 0 ? 1 : 0;
   // short contexts: fewer 8-page groups per workgroup than wavefronts -> K
   // groups of 4 pages with two feature rows per load, so every wavefront streams
-  if (bf16 && sh.deep && sh.waves == 4) {
+  if (bf16 && sh.deep) {
     const int per = (pages + sh.splits - 1) / sh.splits;
     sh.half = (per + 7) / 8 < sh.waves ? 1 : 0;
     if (forced_half) sh.half = forced_half > 0 ? 1 : 0;

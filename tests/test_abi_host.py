@@ -56,13 +56,13 @@ def test_decode_split_choice():
     assert lla.decode_splits(bf, 32, 16, 4096) == 1          # the Ouro-1.4B decode step
     assert lla.decode_splits(bf, 16, 16, 32768) == 1         # the Ouro-2.6B long-context step
     assert lla.decode_splits(bf, 64, 16, 8192) == 1          # the rank sweep
-    # one sequence over 8192 tokens: fp32 keeps a whole 8-page group per wavefront
-    # (2 splits of 8-wavefront workgroups); bf16 then fills more of the machine
-    # with 4-wavefront workgroups on 4-page groups (8 splits)
+    # one sequence: fp32 keeps a whole 8-page group per wavefront; bf16 fills
+    # more of the machine with one 4-page group per wavefront (twice the splits)
     assert lla.decode_splits(f32, 1, 16, 8192) == 2
-    assert lla.decode_splits(bf, 1, 16, 8192) == 8
+    assert lla.decode_splits(bf, 1, 16, 8192) == 4
+    assert lla.decode_splits(f32, 1, 16, 32768) == 8
+    assert lla.decode_splits(bf, 1, 16, 32768) == 16
     for dt in (bf, f32):
-        assert lla.decode_splits(dt, 1, 16, 32768) == 8
         assert lla.decode_splits(dt, 2, 16, 32768) == 8
         assert lla.decode_splits(dt, 1, 16, 32768, with_workspace=False) == 1
         assert lla.decode_splits(dt, 1, 16, 512) == 1
