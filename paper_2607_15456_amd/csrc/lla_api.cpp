@@ -104,12 +104,13 @@ DecodeShape choose_shape(int units, int n_ctx, bool allow_split, bool bf16) {
       return s < cap ? s : (cap > 0 ? cap : 1L);
     };
     long s = fill(sh.waves, groups / sh.waves);
-    // bf16: when whole 8-page groups per wavefront leave the machine short of
-    // the target, one 4-page group per wavefront (the two-rows-per-load K
-    // phase) reaches further: the same workgroup size first, then 4
-    // wavefronts; ties keep the fewer splits
-    if (bf16) {
-      long best = (long)units * sh.waves * s;
+    // bf16: when whole 8-page groups per wavefront fill at most half the
+    // target, one 4-page group per wavefront (the two-rows-per-load K phase)
+    // reaches further: the same workgroup size first, then 4 wavefronts; ties
+    // keep the fewer splits (a batch that nearly fills the machine is not
+    // split for a few more resident wavefronts)
+    long best = (long)units * sh.waves * s;
+    if (bf16 && 2 * best <= target) {
       for (const int w : {sh.waves, 4}) {
         const long s4 = fill(w, pages / (4 * w));
         if ((long)units * w * s4 > best) {
