@@ -61,7 +61,7 @@ def parse():
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--workload", default="ouro14b_decode",
                    choices=["ouro14b_decode", "ouro26b_long", "rank_sweep", "prefill_write", "ouro14b_2d",
-                            "prefill_2d", "absorbed_latency"])
+                            "prefill_2d", "absorbed_latency", "split_k"])
     p.add_argument("--batch", type=int, default=1, help="absorbed_latency: sequences per call")
     p.add_argument("--tier", type=int, default=None, help="rank_sweep: run only this tier index")
     p.add_argument("--evict", default=None,
@@ -791,6 +791,65 @@ def run_absorbed_latency(args, torch, lla, W):
 
 
 # ---------------------------------------------------------------------------
+# split-K decode: few sequences over long contexts (split_k)
+# ---------------------------------------------------------------------------
+
+SPLIT_K_SHAPES = ((1, 32768), (2, 8192), (4, 16384))  # (sequences, context)
+
+
+def run_split_k(args, torch, lla, W):
+    """One loop-l decode call per shape where the (b, h) units alone leave the
+    machine idle, so the launch splits every context over workgroups and merges
+    the partial softmax states: Ouro-1.4B geometry, 16 heads, d_head 128,
+    (192, 320), bf16, with a workspace; HIP events around each call."""
+    H, d, r_k, r_v = 16, 128, 192, 320
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    rows = []
+    for B, N in SPLIT_K_SHAPES:
+        print(f"[bench] split_k B={B} N={N}", file=sys.stderr, flush=True)
+        wl = W.Workload("split_k", 1, H, d, 4, B, N, ((r_k, r_v),), torch.bfloat16)
+        ck = W.normal((B, H, N // 64, r_k, 64), (wl.name, "c_k", B, N), 1.0, wl.dtype, dev)
+        cv = W.normal((B, H, N // 64, r_v, 64), (wl.name, "c_v", B, N), 1.0, wl.dtype, dev)
+        q = W.queries(wl, 0, 1, device=dev)
+        uk, uv, _, _ = W.codec_loop(wl, r_k, r_v, 0, 1, dev)
+        out = torch.empty((B, H, d), dtype=torch.float32, device=dev)
+        ws = lla.new_workspace(B, H, r_v, N, dev)
+        timer = KernelTimer(torch, stream)
+        for _ in range(args.warmup):
+            lla.decode_attn(q, ck, cv, uk, uv, n_ctx=N, out=out, workspace=ws)
+        for _ in range(args.steps):
+            e = timer.start()
+            lla.decode_attn(q, ck, cv, uk, uv, n_ctx=N, out=out, workspace=ws)
+            timer.stop(e)
+        torch.cuda.synchronize()
+        ms = timer.mean_ms()
+        nb = decode_bytes(B, H, d, N, r_k, r_v)
+        rows.append({"batch": B, "context": N, "splits": lla.decode_splits(torch.bfloat16, B, H, N),
+                     "call_ms": round(ms, 5), "gbs": round(nb / (ms * 1e-3) / 1e9, 1),
+                     "frac": round(nb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4), "bytes_per_launch": nb})
+        print(f"[bench] {json.dumps(rows[-1])}", file=sys.stderr, flush=True)
+        del ck, cv, ws
+        torch.cuda.empty_cache()
+    head = rows[0]
+    return {
+        "metric": "split-K decode call: tokens/sec and achieved HBM GB/s (% of peak) for few sequences over long contexts",
+        "value": round(head["batch"] / (head["call_ms"] * 1e-3), 1), "unit": "tokens/s (one call, first shape)",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": head["call_ms"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "one loop-l decode call, Ouro-1.4B geometry, 16 heads, d_head 128, (192, 320), "
+                               "split over workgroups", "shapes": [list(x) for x in SPLIT_K_SHAPES],
+                   "parallelism": "single GPU"},
+        "shapes": rows,
+        "roofline": {"bound": "hbm", "achieved": head["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": head["frac"], "traffic": None,
+                     "kernel": f"decode_kernel (lla_decode_attn), {head['batch']} x {head['context']} tokens",
+                     "bytes_per_launch": head["bytes_per_launch"], "avg_launch_ms": head["call_ms"]},
+        "cpu_baseline": None,
+    }
+
+
+# ---------------------------------------------------------------------------
 # main
 # ---------------------------------------------------------------------------
 
@@ -829,6 +888,9 @@ def main():
         return
     if args.workload == "absorbed_latency":
         print(json.dumps(run_absorbed_latency(args, torch, lla, W)), flush=True)
+        return
+    if args.workload == "split_k":
+        print(json.dumps(run_split_k(args, torch, lla, W)), flush=True)
         return
 
     wl, results = run_decode(args, torch, lla, W)
