@@ -19,16 +19,18 @@
 //     (rg, ts) owns feature rows j = k*8 + rg and token slice ts of each page:
 //     zacc[k] += sum over its 8 tokens of p_n c_v[j][n]; the reduction over
 //     token slices is deferred to the end of the scan.
-// Short contexts (HALF): with fewer 8-page groups than wavefronts, the K phase
-// takes groups of 4 pages and each wave-wide load covers two feature rows
-// (lanes 32..63 take the odd row); one lane swap then sums the two halves of
-// every score.  All wavefronts stream with full 16-byte loads, and a group's K
-// phase has half as many dependent load batches.
+// Fewer 8-page groups than wavefronts (HALF: short contexts, and contexts
+// split over many workgroups): the K phase takes groups of 4 pages and each
+// wave-wide load covers two feature rows (lanes 32..63 take the odd row); one
+// lane swap then sums the two halves of every score.  All wavefronts stream
+// with full 16-byte loads, and a group's K phase has half as many dependent
+// load batches.
 // The waves of a workgroup interleave groups and merge their (m, l, z) in LDS.
 // When the context is split over several workgroups (split-K), each writes its
 // merged partial to the workspace and the last to arrive (an agent-scope
-// atomic counter) merges all partials and runs the value epilogue
-// out = U_v (z / l) + mu_v; the counter is left at zero.
+// atomic counter, one L2 write-back per workgroup) merges all partials and
+// runs the value epilogue out = U_v (z / l) + mu_v; the counter is left at
+// zero.
 //
 // With the decoupled rotary branch (App. J: a small explicit rotary key per
 // token, shared across loops), the rotated query part joins q~ and the rotary
