@@ -655,15 +655,19 @@ void decode_short_kernel(DecodeArgs a) {
   constexpr bool kUvPre = GV <= 8;
   constexpr int kUvBytes = kUvPre ? 16384 : 16;
   __shared__ __attribute__((aligned(16))) bf16_t s_uv[kUvBytes / 2];
+  __shared__ int s_last;
   static_assert(2 * kWaves * PPG * kPage >= kThreads * 8, "prologue partials do not fit");
   float* const s_part = &s_ps[0][0][0];
 
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
-  const int b = blockIdx.x, h = blockIdx.y;
+  const int b = blockIdx.x / a.splits, split = blockIdx.x - b * a.splits, h = blockIdx.y;
   const int N = a.ctx_len ? a.ctx_len[b] : a.n_ctx;
   const bool bad = (N < 1) || (N > a.n_ctx);
   const int pages = bad ? 0 : (N + kPage - 1) / kPage;
+  // this split's pages [pb, pe) (split-K: one sequence's pages over several workgroups)
+  const int per = (pages + a.splits - 1) / a.splits;
+  const int pb = min(pages, split * per), pe = min(pages, pb + per);
   const size_t unit = (size_t)b * a.H + h;
   const int rk = a.rk, rv = a.rv, dr = a.dr;
   const int rq0 = (rk + 7) & ~7;  // s_qt slot of the first rotary row
@@ -780,8 +784,8 @@ void decode_short_kernel(DecodeArgs a) {
   float m_run = neg_inf(), l_lane = 0.f;
 
   int buf = 0;
-  for (int g0 = 0; g0 < pages; g0 += PPG, buf ^= 1) {
-    const int np = min(PPG, pages - g0);
+  for (int g0 = pb; g0 < pe; g0 += PPG, buf ^= 1) {
+    const int np = min(PPG, pe - g0);
 
     // ---- K phase: this wave's row blocks over all pages of the group ----
     float acc[EPL];
@@ -902,12 +906,61 @@ void decode_short_kernel(DecodeArgs a) {
   for (int off = 1; off < 8; off <<= 1)
 #pragma unroll
     for (int k = 0; k < GVW; ++k) zacc[k] += xor_shfl(zacc[k], off);
-  if (lo == 0) {
+  if (a.splits == 1) {
+    if (lo == 0) {
 #pragma unroll
-    for (int k = 0; k < GVW; ++k) {
-      const int j = (wave + k * kWaves) * 8 + hi;
-      if (k < nmv && j < rv) s_zn[j] = zacc[k] / l_lane;
+      for (int k = 0; k < GVW; ++k) {
+        const int j = (wave + k * kWaves) * 8 + hi;
+        if (k < nmv && j < rv) s_zn[j] = zacc[k] / l_lane;
+      }
     }
+  } else {
+    // ---- split-K: publish (m, l, z) of this split's pages; the last arrival merges ----
+    // (every wavefront holds the same m and l; each holds its own z rows)
+    const int stride = rv + 2;
+    float* part = a.part + (unit * a.splits + split) * stride;
+    if (lo == 0) {
+#pragma unroll
+      for (int k = 0; k < GVW; ++k) {
+        const int j = (wave + k * kWaves) * 8 + hi;
+        if (k < nmv && j < rv) part[2 + j] = zacc[k];
+      }
+    }
+    if (tid == 0) {
+      part[0] = m_run;
+      part[1] = l_lane;
+    }
+    // every wavefront's stores reach L2 before the barrier; thread 0's counter
+    // update is the workgroup's one agent-scope release and the last arrival's
+    // acquire makes every split's partial visible
+    wait_stores_in_l2();
+    __syncthreads();
+    if (tid == 0) {
+      const uint32_t prev =
+          __hip_atomic_fetch_add(a.cnt + unit, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+      s_last = (prev == (uint32_t)(a.splits - 1));
+    }
+    __syncthreads();
+    if (!s_last) return;
+    const float* P = a.part + unit * a.splits * stride;
+    float ma = neg_inf();
+    for (int s = 0; s < a.splits; ++s) ma = fmaxf(ma, P[(size_t)s * stride]);
+    float la = 0.f;
+    for (int s = 0; s < a.splits; ++s) {
+      const float ms = P[(size_t)s * stride];
+      const float ws = (ms == neg_inf()) ? 0.f : fast_exp2(ms - ma);
+      la = fmaf(ws, P[(size_t)s * stride + 1], la);
+    }
+    for (int j = tid; j < rv; j += kThreads) {
+      float z = 0.f;
+      for (int s = 0; s < a.splits; ++s) {
+        const float ms = P[(size_t)s * stride];
+        const float ws = (ms == neg_inf()) ? 0.f : fast_exp2(ms - ma);
+        z = fmaf(ws, P[(size_t)s * stride + 2 + j], z);
+      }
+      s_zn[j] = z / la;
+    }
+    if (tid == 0) __hip_atomic_store(a.cnt + unit, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   __syncthreads();
 
@@ -926,9 +979,9 @@ void decode_short_kernel(DecodeArgs a) {
 template <typename TIn, int GV>
 hipError_t launch_t(const DecodeArgs& a, hipStream_t stream) {
   dim3 grid(a.B * a.M * a.splits, a.H);
-  if (a.shortk) {  // short contexts, rows split over the wavefronts: bf16, decode, not split
+  if (a.shortk) {  // at most 16 pages per workgroup, rows split over the wavefronts: bf16, decode
     if constexpr (sizeof(TIn) == 2) {
-      if (a.splits != 1 || a.causal || a.M != 1) return hipErrorInvalidValue;
+      if (a.causal || a.M != 1) return hipErrorInvalidValue;
       hipLaunchKernelGGL((decode_short_kernel<GV>), grid, dim3(4 * kWave), 0, stream, a);
       return hipGetLastError();
     } else {

@@ -140,6 +140,18 @@ DecodeShape choose_shape(int units, int n_ctx, bool allow_split, bool bf16) {
     sh.shortk = pages <= kShortPages ? 1 : 0;
     if (forced_short) sh.shortk = forced_short > 0 ? 1 : 0;
   }
+  // Few (b, h) units over a longer context (bf16, split-K allowed): the same
+  // row-split kernel over 8-page slices of every context, each slice its own
+  // workgroup, when that stays within one workgroup per compute unit.  Every
+  // wavefront then walks a quarter of the rows of one group, so the chain of
+  // dependent load batches per call stays short.  (Two workgroups per unit, or
+  // 16-page slices, measured no faster than the general kernel's shapes.)
+  if (bf16 && allow_split && 2L * units * 4 <= target && pages > 8 && forced_short >= 0 &&
+      !forced_waves && !forced_splits && !forced_half) {
+    const long s8 = (pages + 7) / 8;
+    if ((long)units * s8 <= lla::device_cu_count() && s8 <= max_splits(n_ctx))
+      sh = DecodeShape{4, (int)s8, 1, 0, 1};
+  }
   return sh;
 }
 

@@ -56,12 +56,15 @@ def test_decode_split_choice():
     assert lla.decode_splits(bf, 32, 16, 4096) == 1          # the Ouro-1.4B decode step
     assert lla.decode_splits(bf, 16, 16, 32768) == 1         # the Ouro-2.6B long-context step
     assert lla.decode_splits(bf, 64, 16, 8192) == 1          # the rank sweep
-    # one sequence: fp32 keeps a whole 8-page group per wavefront; bf16 fills
-    # more of the machine with one 4-page group per wavefront (twice the splits)
+    # one sequence: fp32 keeps a whole 8-page group per wavefront; bf16 takes the
+    # row-split kernel over 8-page slices up to one workgroup per compute unit
+    # (8192 tokens), beyond that one 4-page group per wavefront
     assert lla.decode_splits(f32, 1, 16, 8192) == 2
-    assert lla.decode_splits(bf, 1, 16, 8192) == 4
+    assert lla.decode_splits(bf, 1, 16, 8192) == 16
     assert lla.decode_splits(f32, 1, 16, 32768) == 8
     assert lla.decode_splits(bf, 1, 16, 32768) == 16
+    assert lla.decode_splits(bf, 1, 16, 1024) == 2
+    assert lla.decode_splits(bf, 4, 16, 16384) == 4          # 64 units: 8-page groups, 4 splits
     for dt in (bf, f32):
         assert lla.decode_splits(dt, 2, 16, 32768) == 8
         assert lla.decode_splits(dt, 1, 16, 32768, with_workspace=False) == 1

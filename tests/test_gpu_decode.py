@@ -155,10 +155,10 @@ def test_mu_k_cancels():
 # ---------------------------------------------------------------------------
 
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
-@pytest.mark.parametrize("N,splits_f32,splits_bf16", [(8192, 2, 4), (32768, 8, 8)])
+@pytest.mark.parametrize("N,splits_f32,splits_bf16", [(4096, 1, 8), (8192, 2, 4), (32768, 8, 8)])
 def test_split_k_long_context(dtype, N, splits_f32, splits_bf16):
     B, H = 2, 16
-    splits = splits_bf16 if dtype == torch.bfloat16 else splits_f32  # bf16 at 8192: 4-page groups
+    splits = splits_bf16 if dtype == torch.bfloat16 else splits_f32  # bf16 at 4096: row-split slices
     r_k, r_v = (96, 160) if dtype == torch.float32 else (36, 60)
     wl = W.Workload("split_k", 1, H, 128, 4, B, N, ((r_k, r_v),), dtype)
     assert lla.decode_splits(dtype, B, H, N) == splits

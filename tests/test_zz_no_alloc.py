@@ -56,14 +56,14 @@ def _check(dtype, B, H, N, r_k, r_v, seed, lens=None):
 @pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
 def test_noalloc_matches_workspace_decode_twice_smaller_second(dtype):
     r_k, r_v = (36, 60) if dtype == torch.bfloat16 else (96, 160)
-    # first call: 32768 tokens (8 splits in fp32; 16 in bf16, on 4-page
-    # groups); second, smaller: 8192 tokens (2 splits in fp32, 4 in bf16)
+    # first call: 32768 tokens (8 splits in fp32, 16 in bf16); second, smaller:
+    # 8192 tokens (2 splits in fp32; 16 row-split slices of 8 pages in bf16)
     bf = dtype == torch.bfloat16
     assert _check(dtype, 1, 16, 32768, r_k, r_v, 1) == (16 if bf else 8)
-    assert _check(dtype, 1, 16, 8192, r_k, r_v, 2) == (4 if bf else 2)
+    assert _check(dtype, 1, 16, 8192, r_k, r_v, 2) == (16 if bf else 2)
     # a batch that does not split (no scratch used), then split again with
     # ragged and out-of-range lengths (the counters must start at zero)
-    assert _check(dtype, 8, 16, 1024, r_k, r_v, 3) == 1
+    assert _check(dtype, 32, 16, 1024, r_k, r_v, 3) == 1
     assert _check(dtype, 2, 16, 16384, r_k, r_v, 4, lens=[16384, 0]) > 1
     assert _check(dtype, 2, 16, 16384, r_k, r_v, 5, lens=[5000, 16383]) > 1
 
