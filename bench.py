@@ -794,7 +794,7 @@ def run_absorbed_latency(args, torch, lla, W):
 # split-K decode: few sequences over long contexts (split_k)
 # ---------------------------------------------------------------------------
 
-SPLIT_K_SHAPES = ((1, 32768), (2, 8192), (4, 16384))  # (sequences, context)
+SPLIT_K_SHAPES = ((1, 32768), (1, 8192), (1, 4096), (2, 8192), (4, 16384))  # (sequences, context)
 
 
 def run_split_k(args, torch, lla, W):
