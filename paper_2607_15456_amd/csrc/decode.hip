@@ -632,7 +632,7 @@ void decode_kernel(DecodeArgs a) {
 //     group, token slice ts); its z rows are its own, so no merge follows.
 // Slots that are not read (pages past the context, rows past r_k, r_v or dr)
 // are requested out of the region: they read as zero and touch no memory.
-template <int GV>
+template <int GV, bool SPLIT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
 void decode_short_kernel(DecodeArgs a) {
   typedef bf16_t TIn;
@@ -661,13 +661,15 @@ void decode_short_kernel(DecodeArgs a) {
 
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
-  const int b = blockIdx.x / a.splits, split = blockIdx.x - b * a.splits, h = blockIdx.y;
+  // SPLIT: the workgroup takes one slice of its (b, h) context (split-K)
+  const int b = SPLIT ? blockIdx.x / a.splits : blockIdx.x, h = blockIdx.y;
+  const int split = SPLIT ? blockIdx.x - b * a.splits : 0;
   const int N = a.ctx_len ? a.ctx_len[b] : a.n_ctx;
   const bool bad = (N < 1) || (N > a.n_ctx);
   const int pages = bad ? 0 : (N + kPage - 1) / kPage;
-  // this split's pages [pb, pe) (split-K: one sequence's pages over several workgroups)
-  const int per = (pages + a.splits - 1) / a.splits;
-  const int pb = min(pages, split * per), pe = min(pages, pb + per);
+  // this slice's pages [pb, pe)
+  const int per = SPLIT ? (pages + a.splits - 1) / a.splits : pages;
+  const int pb = SPLIT ? min(pages, split * per) : 0, pe = SPLIT ? min(pages, pb + per) : pages;
   const size_t unit = (size_t)b * a.H + h;
   const int rk = a.rk, rv = a.rv, dr = a.dr;
   const int rq0 = (rk + 7) & ~7;  // s_qt slot of the first rotary row
@@ -906,7 +908,7 @@ void decode_short_kernel(DecodeArgs a) {
   for (int off = 1; off < 8; off <<= 1)
 #pragma unroll
     for (int k = 0; k < GVW; ++k) zacc[k] += xor_shfl(zacc[k], off);
-  if (a.splits == 1) {
+  if constexpr (!SPLIT) {
     if (lo == 0) {
 #pragma unroll
       for (int k = 0; k < GVW; ++k) {
@@ -982,7 +984,10 @@ hipError_t launch_t(const DecodeArgs& a, hipStream_t stream) {
   if (a.shortk) {  // at most 16 pages per workgroup, rows split over the wavefronts: bf16, decode
     if constexpr (sizeof(TIn) == 2) {
       if (a.causal || a.M != 1) return hipErrorInvalidValue;
-      hipLaunchKernelGGL((decode_short_kernel<GV>), grid, dim3(4 * kWave), 0, stream, a);
+      if (a.splits > 1)
+        hipLaunchKernelGGL((decode_short_kernel<GV, true>), grid, dim3(4 * kWave), 0, stream, a);
+      else
+        hipLaunchKernelGGL((decode_short_kernel<GV, false>), grid, dim3(4 * kWave), 0, stream, a);
       return hipGetLastError();
     } else {
       return hipErrorInvalidValue;
