@@ -9,7 +9,7 @@ import torch
 
 import oracle
 from paper_2607_15456_amd import lla, workloads as W
-from tests.helpers import assert_close, f64, log
+from tests.helpers import assert_close, f64, f64_dev, log
 
 pytestmark = pytest.mark.gpu
 
@@ -157,3 +157,31 @@ def test_prefill_rope(dtype, r_k, r_v, dr, Hr, M, p0):
     ref = oracle.prefill_attn_rope_batched(f64(q), f64(qr), f64(ck), f64(cv), f64(kr).transpose(0, 2, 1, 3),
                                            f64(uk), f64(uv), f64(muk), f64(muv), p0=p0)
     assert_close(f64(out), ref, dtype, "prefill rope")
+
+
+@pytest.mark.parametrize("N,r_k,r_v,Hr", [(32768, 96, 160, 1), (32768, 192, 320, 16), (131072, 96, 160, 1)])
+def test_decode_rope_split_k(N, r_k, r_v, Hr):
+    """One sequence of 16 heads over a long context with the rotary branch,
+    the shape of the absorbed-against-rebuilt latency comparison (App. J):
+    the launch splits each (b, h) context over 16 workgroups of 8 wavefronts
+    (4-page K groups at 32,768 tokens, 8-page groups at 131,072) and merges
+    their partial states.  Full and ragged lengths, every head checked."""
+    B, H, dr, dtype = 1, 16, 64, torch.bfloat16
+    assert lla.decode_splits(dtype, B, H, N) == 16
+    wl = W.Workload("rope_split", 1, H, 128, 4, B, N, ((r_k, r_v),), dtype)
+    log(f"decode rope split-K N={N} r=({r_k},{r_v}) Hr={Hr}")
+    ck, cv, kr, q, qr, uk, uv, muk, muv, rc = _decode_case(wl, r_k, r_v, dr, Hr, B, N, N, dtype, True)
+    pk, pv = lla.to_paged(ck, N), lla.to_paged(cv, N)
+    ws = lla.new_workspace(B, H, r_v, N)
+    q64, qr64, ck64, cv64 = f64(q), f64(qr), f64_dev(ck), f64_dev(cv)
+    kr64, uk64, uv64, muk64, muv64 = f64(kr).transpose(0, 2, 1, 3), f64(uk), f64(uv), f64(muk), f64(muv)
+    del ck, cv
+    for n in (N, N - 777):
+        lens = torch.tensor([n], dtype=torch.int32, device=DEV)
+        qr_rot = lla.rope_rotate(qr, pos=lens - 1)
+        out = lla.decode_attn(q, pk, pv, uk, uv, n_ctx=N, ctx_len=lens, mu_k=muk, mu_v=muv,
+                              q_rope=qr_rot, r_cache=rc, workspace=ws)
+        torch.cuda.synchronize()
+        ref = oracle.decode_attn_rope_batched(q64, qr64, ck64, cv64, kr64, uk64, uv64, muk64, muv64, ctx_len=n)
+        assert_close(f64(out), ref, dtype, f"decode rope split-K n={n}")
+    assert int(ws[:4 * B * H].view(torch.int32).abs().sum()) == 0
