@@ -22,7 +22,7 @@ Attention itself is the teacher's, unchanged (Sec. 1, caption of the
 architecture figure: reconstruction happens before attention, which is left
 unchanged): s_n = scale * <q, k_n>, a = softmax(s), o = sum_n a_n v_n.
 
-Readings where the paper is silent (all listed in the design doc):
+Readings where the paper is silent:
 * the softmax scale is a parameter; the teacher's 1/sqrt(d_head) is the default;
 * no RoPE on the content path (the NoPE content path of App. J, where
   absorption is exact); the decoupled rotary branch of App. J is a separate
