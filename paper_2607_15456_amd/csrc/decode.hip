@@ -616,27 +616,29 @@ void decode_kernel(DecodeArgs a) {
   }
 }
 
-// Short contexts (at most a few 8-page groups per (b, h)), bf16: the four
-// wavefronts of a workgroup split the feature rows of each 8-page group
+// Short contexts (at most a few 8-page groups per (b, h)), bf16: the W = 4
+// or 8 wavefronts of a workgroup split the feature rows of each 8-page group
 // instead of its pages, so a group's loads are spread over every wavefront
 // whatever the page count.
-//   * K phase -- wave w takes the 8-row blocks w, w + 4, ... of the content
+//   * K phase -- wave w takes the 8-row blocks w, w + W, ... of the content
 //     rows and then of the rotary rows; lane (pg, ts) owns tokens ts*8.. of
 //     page pg, so one wave-wide load reads one feature row of all 8 pages.
-//     The four partial scores of a token are summed through LDS (double
+//     The W partial scores of a token are summed through LDS (double
 //     buffered over groups, one barrier per group), in the same order in
-//     every wavefront, so all four hold identical scores and softmax
+//     every wavefront, so all of them hold identical scores and softmax
 //     statistics.
-//   * V phase -- wave w takes the 8-row groups w, w + 4, ... of the value
+//   * V phase -- wave w takes the 8-row groups w, w + W, ... of the value
 //     latents, each over all pages of the group (lane (rg, ts): row rg of the
 //     group, token slice ts); its z rows are its own, so no merge follows.
+// Eight wavefronts halve each one's chain of dependent row loads; they are
+// used when the workgroups fill at most half the compute units.
 // Slots that are not read (pages past the context, rows past r_k, r_v or dr)
 // are requested out of the region: they read as zero and touch no memory.
-template <int GV, bool SPLIT>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
+template <int GV, bool SPLIT, int WAVES>
+__global__ __launch_bounds__(WAVES * kWave) __attribute__((amdgpu_waves_per_eu(2)))
 void decode_short_kernel(DecodeArgs a) {
   typedef bf16_t TIn;
-  constexpr int kWaves = 4, kThreads = kWaves * kWave;
+  constexpr int kWaves = WAVES, kThreads = kWaves * kWave;
   constexpr int KB = 8;                       // loads per K batch
   constexpr int EPL = 8;                      // tokens per 16-byte load
   constexpr int PPG = 8;                      // pages per group
@@ -806,7 +808,7 @@ void decode_short_kernel(DecodeArgs a) {
       *reinterpret_cast<float4*>(&ps[wave * PPG * kPage + hi * kPage + lo * EPL + e]) =
           make_float4(acc[e], acc[e + 1], acc[e + 2], acc[e + 3]);
     __syncthreads();
-    // the four partials, summed in wave order (identical in every wavefront)
+    // the wavefronts' partials, summed in wave order (identical in every wavefront)
 #pragma unroll
     for (int e = 0; e < EPL; ++e) acc[e] = 0.f;
 #pragma unroll
@@ -984,10 +986,17 @@ hipError_t launch_t(const DecodeArgs& a, hipStream_t stream) {
   if (a.shortk) {  // at most 16 pages per workgroup, rows split over the wavefronts: bf16, decode
     if constexpr (sizeof(TIn) == 2) {
       if (a.causal || a.M != 1) return hipErrorInvalidValue;
-      if (a.splits > 1)
-        hipLaunchKernelGGL((decode_short_kernel<GV, true>), grid, dim3(4 * kWave), 0, stream, a);
-      else
-        hipLaunchKernelGGL((decode_short_kernel<GV, false>), grid, dim3(4 * kWave), 0, stream, a);
+      if (a.waves != 4 && a.waves != 8) return hipErrorInvalidValue;
+      if (a.waves == 8) {
+        if (a.splits > 1)
+          hipLaunchKernelGGL((decode_short_kernel<GV, true, 8>), grid, dim3(8 * kWave), 0, stream, a);
+        else
+          hipLaunchKernelGGL((decode_short_kernel<GV, false, 8>), grid, dim3(8 * kWave), 0, stream, a);
+      } else if (a.splits > 1) {
+        hipLaunchKernelGGL((decode_short_kernel<GV, true, 4>), grid, dim3(4 * kWave), 0, stream, a);
+      } else {
+        hipLaunchKernelGGL((decode_short_kernel<GV, false, 4>), grid, dim3(4 * kWave), 0, stream, a);
+      }
       return hipGetLastError();
     } else {
       return hipErrorInvalidValue;

@@ -4,6 +4,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <cstdlib>
@@ -70,7 +71,8 @@ size_t workspace_bytes(int B, int H, int r_v, int n_ctx) {
 // 8-page group (bf16: one 4-page group when that fills more of the machine).
 // bf16 workgroups with fewer 8-page groups than wavefronts use the 4-page K
 // groups.  LLA_DECODE_WAVES / LLA_DECODE_SPLITS /
-// LLA_DECODE_DEEP / LLA_DECODE_HALF override the choice (for tuning sweeps).
+// LLA_DECODE_DEEP / LLA_DECODE_HALF / LLA_DECODE_SHORT / LLA_DECODE_SHORT_WAVES
+// override the choice (for tuning sweeps).
 struct DecodeShape {
   int waves, splits, deep, half, shortk;
 };
@@ -82,12 +84,16 @@ int env_int(const char* name) {
 
 constexpr int kShortPages = 16;
 
-DecodeShape choose_shape(int units, int n_ctx, bool allow_split, bool bf16) {
+// row_blocks: the larger of the 8-row key blocks (content and rotary) and the
+// 8-row value groups a (b, h) walks per 8-page group (0: not known; the split
+// count does not depend on it)
+DecodeShape choose_shape(int units, int n_ctx, bool allow_split, bool bf16, int row_blocks = 0) {
   static const int forced_waves = env_int("LLA_DECODE_WAVES");
   static const int forced_splits = env_int("LLA_DECODE_SPLITS");
   static const int forced_deep = env_int("LLA_DECODE_DEEP");
   static const int forced_half = env_int("LLA_DECODE_HALF");
   static const int forced_short = env_int("LLA_DECODE_SHORT");
+  static const int forced_short_waves = env_int("LLA_DECODE_SHORT_WAVES");
   const int pages = (n_ctx + LLA_PAGE_TOKENS - 1) / LLA_PAGE_TOKENS;
   const int groups = (pages + 7) / 8;
   const long target = 8L * lla::device_cu_count();  // resident wavefronts wanted
@@ -140,6 +146,14 @@ DecodeShape choose_shape(int units, int n_ctx, bool allow_split, bool bf16) {
     sh.shortk = pages <= kShortPages ? 1 : 0;
     if (forced_short) sh.shortk = forced_short > 0 ? 1 : 0;
   }
+  // the row-split kernel takes 8 wavefronts (each walking half as many rows)
+  // when its workgroups fill at most half the compute units and there are
+  // more row blocks than 4 wavefronts take in one pass
+  auto short_waves = [&](long workgroups) {
+    if (forced_short_waves == 4 || forced_short_waves == 8) return forced_short_waves;
+    return 2 * workgroups <= lla::device_cu_count() && row_blocks > 4 ? 8 : 4;
+  };
+  if (sh.shortk && !forced_waves) sh.waves = short_waves(units);
   // Few (b, h) units over a longer context (bf16, split-K allowed): the same
   // row-split kernel over 8-page slices of every context, each slice its own
   // workgroup, when that stays within one workgroup per compute unit.  Every
@@ -150,7 +164,7 @@ DecodeShape choose_shape(int units, int n_ctx, bool allow_split, bool bf16) {
       !forced_waves && !forced_splits && !forced_half) {
     const long s8 = (pages + 7) / 8;
     if ((long)units * s8 <= lla::device_cu_count() && s8 <= max_splits(n_ctx))
-      sh = DecodeShape{4, (int)s8, 1, 0, 1};
+      sh = DecodeShape{short_waves((long)units * s8), (int)s8, 1, 0, 1};
   }
   return sh;
 }
@@ -414,8 +428,9 @@ lla_status decode_impl(int dtype, int out_dtype, int B, int H, int d_head, int r
   a.Hr = H_rope;
   a.qr = q_rope;
   a.rc = r_cache;
+  const int row_blocks = std::max((r_k + 7) / 8 + d_rope / 8, (r_v + 7) / 8);
   const DecodeShape sh = choose_shape(B * H, n_ctx, static_scratch || workspace != nullptr,
-                                      dtype == LLA_BF16);
+                                      dtype == LLA_BF16, row_blocks);
   a.waves = sh.waves;
   a.splits = sh.splits;
   a.deep = sh.deep;

@@ -199,16 +199,19 @@ def test_split_k_long_context(dtype, N, splits_f32, splits_bf16):
     assert_close(f64(out), ref([N, N]), dtype, "after the NaN calls")
 
 
-# Split-K slices of the row-split bf16 kernel (two sequences of 16 heads over
-# 4096 tokens: 8 slices of 8 pages per (b, h)) at every bucket of value rows
-# per wavefront: the partial states (running max, denominator, value rows)
-# each slice publishes and the last arrival merges depend on the rank.
+# Split-K slices of the row-split bf16 kernel (16 heads over 4096 tokens: 8
+# slices of 8 pages per (b, h)) at every bucket of value rows per wavefront:
+# the partial states (running max, denominator, value rows) each slice
+# publishes and the last arrival merges depend on the rank.  One sequence
+# gives 128 workgroups (8 wavefronts each, half as many rows per wavefront),
+# two sequences 256 (4 wavefronts each).
+@pytest.mark.parametrize("B", [1, 2])
 @pytest.mark.parametrize("r_k,r_v", [(18, 30), (64, 128), (96, 160), (120, 250), (192, 320),
                                      (250, 380), (300, 440), (288, 480), (512, 512)])
-def test_split_k_row_split_every_rank_bucket(r_k, r_v):
-    B, H, N, dtype = 2, 16, 4096, torch.bfloat16
+def test_split_k_row_split_every_rank_bucket(r_k, r_v, B):
+    H, N, dtype = 16, 4096, torch.bfloat16
     assert lla.decode_splits(dtype, B, H, N) == 8
-    log(f"row-split slices r=({r_k},{r_v})")
+    log(f"row-split slices B={B} r=({r_k},{r_v})")
     wl = W.Workload("split_rows", 1, H, 128, 4, B, N, ((r_k, r_v),), dtype)
     ck, cv, q, uk, uv, muk, muv, pk, pv = _case(wl, r_k, r_v, B, N, N, 0, 2, True, dtype)
     ws = lla.new_workspace(B, H, r_v, N)
@@ -220,8 +223,8 @@ def test_split_k_row_split_every_rank_bucket(r_k, r_v):
                                                                uk64[h], uv64[h], muk64[h], muv64[h])
                                    for h in range(H)]) for b in range(B)])
 
-    # full contexts; a ragged pair whose short sequence leaves most slices empty
-    for lens in ([N, N], [64 * 37 + 5, 1]):
+    # full contexts; ragged lengths whose short sequence leaves most slices empty
+    for lens in ([N, N][:B], [64 * 37 + 5, 1][:B], [1, 64 * 37 + 5][:B]):
         ctx = torch.tensor(lens, dtype=torch.int32, device=DEV)
         out = lla.decode_attn(q, pk, pv, uk, uv, n_ctx=N, ctx_len=ctx, mu_k=muk, mu_v=muv, workspace=ws)
         torch.cuda.synchronize()
