@@ -631,7 +631,7 @@ void decode_kernel(DecodeArgs a) {
 //     latents, each over all pages of the group (lane (rg, ts): row rg of the
 //     group, token slice ts); its z rows are its own, so no merge follows.
 // Eight wavefronts halve each one's chain of dependent row loads; they are
-// used when the workgroups fill at most half the compute units.
+// used when every workgroup fits at one per compute unit.
 // Slots that are not read (pages past the context, rows past r_k, r_v or dr)
 // are requested out of the region: they read as zero and touch no memory.
 template <int GV, bool SPLIT, int WAVES>

@@ -147,11 +147,12 @@ DecodeShape choose_shape(int units, int n_ctx, bool allow_split, bool bf16, int 
     if (forced_short) sh.shortk = forced_short > 0 ? 1 : 0;
   }
   // the row-split kernel takes 8 wavefronts (each walking half as many rows)
-  // when its workgroups fill at most half the compute units and there are
-  // more row blocks than 4 wavefronts take in one pass
+  // when its workgroups all fit at one per compute unit (8 wavefronts each
+  // fill a unit at 2 per SIMD) and there are more row blocks than 4
+  // wavefronts take in one pass
   auto short_waves = [&](long workgroups) {
     if (forced_short_waves == 4 || forced_short_waves == 8) return forced_short_waves;
-    return 2 * workgroups <= lla::device_cu_count() && row_blocks > 4 ? 8 : 4;
+    return workgroups <= lla::device_cu_count() && row_blocks > 4 ? 8 : 4;
   };
   if (sh.shortk && !forced_waves) sh.waves = short_waves(units);
   // Few (b, h) units over a longer context (bf16, split-K allowed): the same
