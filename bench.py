@@ -766,7 +766,7 @@ def run_absorbed_latency(args, torch, lla, W):
                      "fullrope_over_absorbed": round(f_ms / a_ms, 3),
                      "absorbed_gbs": round(ab / (a_ms * 1e-3) / 1e9, 1),
                      "fullrope_gbs": round(fb / (f_ms * 1e-3) / 1e9, 1),
-                     "splits": lla.decode_splits(torch.bfloat16, B, H, N),
+                     "splits": lla.decode_splits(torch.bfloat16, B, H, N, r_k, r_v, dr),
                      "paper_speedup_other_gpu": PAPER_ABSORBED_SPEEDUP[N]})
         print(f"[bench] {json.dumps(rows[-1])}", file=sys.stderr, flush=True)
         del ck, cv, rc, ws
@@ -825,7 +825,7 @@ def run_split_k(args, torch, lla, W):
         torch.cuda.synchronize()
         ms = timer.mean_ms()
         nb = decode_bytes(B, H, d, N, r_k, r_v)
-        rows.append({"batch": B, "context": N, "splits": lla.decode_splits(torch.bfloat16, B, H, N),
+        rows.append({"batch": B, "context": N, "splits": lla.decode_splits(torch.bfloat16, B, H, N, r_k, r_v),
                      "call_ms": round(ms, 5), "gbs": round(nb / (ms * 1e-3) / 1e9, 1),
                      "frac": round(nb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4), "bytes_per_launch": nb})
         print(f"[bench] {json.dumps(rows[-1])}", file=sys.stderr, flush=True)

@@ -155,10 +155,14 @@ lla_status lla_decode_workspace_bytes(int B, int H, int r_v, int n_ctx, size_t* 
  * is chosen only when the (b, h) units alone leave compute units without 8
  * resident wavefronts (small batches, long contexts); the partial softmax
  * states (m, l, z) of the splits are merged as in the split-K step of the
- * decode (the softmax over a union of disjoint key ranges).  Host only.
- * Errors: LLA_ERR_INVALID_ARG.
+ * decode (the softmax over a union of disjoint key ranges).  The ranks r_k,
+ * r_v and the rotary width d_rope (0 without the rotary branch) are those of
+ * the call: at large ranks bf16 contexts are split into longer slices.
+ * Host only.  Errors: LLA_ERR_INVALID_ARG (also for ranks outside
+ * [1, LLA_MAX_RANK] or d_rope outside [0, LLA_MAX_ROPE]).
  */
-lla_status lla_decode_splits(int dtype, int B, int H, int n_ctx, int with_workspace, int* splits);
+lla_status lla_decode_splits(int dtype, int B, int H, int n_ctx, int r_k, int r_v, int d_rope,
+                             int with_workspace, int* splits);
 
 /*
  * Loop-l decode attention over the latent cache, absorbed form (App. J):

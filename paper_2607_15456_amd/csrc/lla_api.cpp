@@ -84,16 +84,20 @@ int env_int(const char* name) {
 
 constexpr int kShortPages = 16;
 
-// row_blocks: the larger of the 8-row key blocks (content and rotary) and the
-// 8-row value groups a (b, h) walks per 8-page group (0: not known; the split
-// count does not depend on it)
-DecodeShape choose_shape(int units, int n_ctx, bool allow_split, bool bf16, int row_blocks = 0) {
+// The larger of the 8-row key blocks (content and rotary) and the 8-row value
+// groups a (b, h) walks per 8-page group.
+int row_blocks_of(int r_k, int r_v, int d_rope) {
+  return std::max((r_k + 7) / 8 + d_rope / 8, (r_v + 7) / 8);
+}
+
+DecodeShape choose_shape(int units, int n_ctx, bool allow_split, bool bf16, int row_blocks) {
   static const int forced_waves = env_int("LLA_DECODE_WAVES");
   static const int forced_splits = env_int("LLA_DECODE_SPLITS");
   static const int forced_deep = env_int("LLA_DECODE_DEEP");
   static const int forced_half = env_int("LLA_DECODE_HALF");
   static const int forced_short = env_int("LLA_DECODE_SHORT");
   static const int forced_short_waves = env_int("LLA_DECODE_SHORT_WAVES");
+  static const int forced_short_groups = env_int("LLA_DECODE_SHORT_GROUPS");
   const int pages = (n_ctx + LLA_PAGE_TOKENS - 1) / LLA_PAGE_TOKENS;
   const int groups = (pages + 7) / 8;
   const long target = 8L * lla::device_cu_count();  // resident wavefronts wanted
@@ -156,16 +160,24 @@ DecodeShape choose_shape(int units, int n_ctx, bool allow_split, bool bf16, int 
   };
   if (sh.shortk && !forced_waves) sh.waves = short_waves(units);
   // Few (b, h) units over a longer context (bf16, split-K allowed): the same
-  // row-split kernel over 8-page slices of every context, each slice its own
+  // row-split kernel over slices of every context, each slice its own
   // workgroup, when that stays within one workgroup per compute unit.  Every
-  // wavefront then walks a quarter of the rows of one group, so the chain of
-  // dependent load batches per call stays short.  (Two workgroups per unit, or
-  // 16-page slices, measured no faster than the general kernel's shapes.)
+  // wavefront then walks an eighth or a quarter of the rows of each group, so
+  // the chain of dependent load batches per call stays short.  (Two workgroups
+  // per unit measured slower than the general kernel's shapes.)
   if (bf16 && allow_split && 2L * units * 4 <= target && pages > 8 && forced_short >= 0 &&
       !forced_waves && !forced_splits && !forced_half) {
-    const long s8 = (pages + 7) / 8;
-    if ((long)units * s8 <= lla::device_cu_count() && s8 <= max_splits(n_ctx))
-      sh = DecodeShape{short_waves((long)units * s8), (int)s8, 1, 0, 1};
+    // slices of k 8-page groups, the shortest that fits; 16-page slices only
+    // at ranks with more than 16 row blocks (measured faster than the general
+    // kernel's shapes there, slower at smaller ranks)
+    const int max_groups = forced_short_groups > 0 ? forced_short_groups : row_blocks > 16 ? 2 : 1;
+    for (int k = 1; k <= max_groups; ++k) {
+      const long s = (pages + 8L * k - 1) / (8L * k);
+      if (s > 1 && (long)units * s <= lla::device_cu_count() && s <= max_splits(n_ctx)) {
+        sh = DecodeShape{short_waves((long)units * s), (int)s, 1, 0, 1};
+        break;
+      }
+    }
   }
   return sh;
 }
@@ -334,10 +346,13 @@ lla_status lla_decode_workspace_bytes(int B, int H, int r_v, int n_ctx, size_t* 
   return LLA_OK;
 }
 
-lla_status lla_decode_splits(int dtype, int B, int H, int n_ctx, int with_workspace, int* splits) {
-  if (!dtype_ok(dtype) || B < 1 || H < 1 || n_ctx < 1 || !splits || (int64_t)B * H > (1 << 24))
+lla_status lla_decode_splits(int dtype, int B, int H, int n_ctx, int r_k, int r_v, int d_rope,
+                             int with_workspace, int* splits) {
+  if (!dtype_ok(dtype) || B < 1 || H < 1 || n_ctx < 1 || !splits || (int64_t)B * H > (1 << 24) ||
+      !rank_ok(r_k) || !rank_ok(r_v) || d_rope < 0 || d_rope > LLA_MAX_ROPE)
     return LLA_ERR_INVALID_ARG;
-  *splits = choose_shape(B * H, n_ctx, with_workspace != 0, dtype == LLA_BF16).splits;
+  *splits = choose_shape(B * H, n_ctx, with_workspace != 0, dtype == LLA_BF16,
+                         row_blocks_of(r_k, r_v, d_rope)).splits;
   return LLA_OK;
 }
 
@@ -429,9 +444,8 @@ lla_status decode_impl(int dtype, int out_dtype, int B, int H, int d_head, int r
   a.Hr = H_rope;
   a.qr = q_rope;
   a.rc = r_cache;
-  const int row_blocks = std::max((r_k + 7) / 8 + d_rope / 8, (r_v + 7) / 8);
   const DecodeShape sh = choose_shape(B * H, n_ctx, static_scratch || workspace != nullptr,
-                                      dtype == LLA_BF16, row_blocks);
+                                      dtype == LLA_BF16, row_blocks_of(r_k, r_v, d_rope));
   a.waves = sh.waves;
   a.splits = sh.splits;
   a.deep = sh.deep;

@@ -39,7 +39,7 @@ _SIGS = {
     "lla_cache_bytes": (_c_int, [_c_i64] * 8 + [_c_int, ctypes.POINTER(_c_i64)]),
     "lla_encode": (_c_int, [_c_int] * 8 + [_c_vp] * 8 + [_c_int, _c_int, _c_vp]),
     "lla_decode_workspace_bytes": (_c_int, [_c_int] * 4 + [ctypes.POINTER(_c_sz)]),
-    "lla_decode_splits": (_c_int, [_c_int] * 5 + [ctypes.POINTER(_c_int)]),
+    "lla_decode_splits": (_c_int, [_c_int] * 8 + [ctypes.POINTER(_c_int)]),
     "lla_decode_attn": (_c_int, [_c_int] * 9 + [_c_vp] * 8 + [_c_f, _c_vp, _c_vp, _c_sz, _c_vp]),
     "lla_decode_attn_noalloc": (_c_int, [_c_int] * 9 + [_c_vp] * 8 + [_c_f, _c_vp, _c_vp]),
     "lla_prefill_attn": (_c_int, [_c_int] * 10 + [_c_vp] * 7 + [_c_f, _c_vp, _c_vp, _c_sz, _c_vp]),
@@ -152,11 +152,12 @@ def decode_workspace_bytes(B: int, H: int, r_v: int, n_ctx: int) -> int:
     return out.value
 
 
-def decode_splits(dtype: torch.dtype, B: int, H: int, n_ctx: int, with_workspace: bool = True) -> int:
+def decode_splits(dtype: torch.dtype, B: int, H: int, n_ctx: int, r_k: int, r_v: int, d_rope: int = 0,
+                  with_workspace: bool = True) -> int:
     """Workgroups lla_decode_attn splits each (b, h) context over (lla_decode_splits)."""
     out = _c_int()
     _check(lib().lla_decode_splits(LLA_BF16 if dtype == torch.bfloat16 else LLA_F32, B, H, n_ctx,
-                                   1 if with_workspace else 0, ctypes.byref(out)))
+                                   r_k, r_v, d_rope, 1 if with_workspace else 0, ctypes.byref(out)))
     return out.value
 
 

@@ -53,24 +53,39 @@ def test_decode_split_choice():
     sequence of 16 heads over a long context is, in proportion to its pages."""
     import torch
     bf, f32 = torch.bfloat16, torch.float32
-    assert lla.decode_splits(bf, 32, 16, 4096) == 1          # the Ouro-1.4B decode step
-    assert lla.decode_splits(bf, 16, 16, 32768) == 1         # the Ouro-2.6B long-context step
-    assert lla.decode_splits(bf, 64, 16, 8192) == 1          # the rank sweep
+    r2 = (192, 320)  # the Ouro-1.4B ranks
+    assert lla.decode_splits(bf, 32, 16, 4096, *r2) == 1          # the Ouro-1.4B decode step
+    assert lla.decode_splits(bf, 16, 16, 32768, 36, 60) == 1      # the Ouro-2.6B long-context step
+    assert lla.decode_splits(bf, 64, 16, 8192, 96, 160) == 1      # the rank sweep
     # one sequence: fp32 keeps a whole 8-page group per wavefront; bf16 takes the
     # row-split kernel over 8-page slices up to one workgroup per compute unit
     # (8192 tokens), beyond that one 4-page group per wavefront
-    assert lla.decode_splits(f32, 1, 16, 8192) == 2
-    assert lla.decode_splits(bf, 1, 16, 8192) == 16
-    assert lla.decode_splits(f32, 1, 16, 32768) == 8
-    assert lla.decode_splits(bf, 1, 16, 32768) == 16
-    assert lla.decode_splits(bf, 1, 16, 1024) == 2
-    assert lla.decode_splits(bf, 4, 16, 16384) == 4          # 64 units: 8-page groups, 4 splits
+    assert lla.decode_splits(f32, 1, 16, 8192, *r2) == 2
+    assert lla.decode_splits(bf, 1, 16, 8192, *r2) == 16
+    assert lla.decode_splits(f32, 1, 16, 32768, *r2) == 8
+    assert lla.decode_splits(bf, 1, 16, 32768, *r2) == 16
+    assert lla.decode_splits(bf, 1, 16, 1024, *r2) == 2
+    assert lla.decode_splits(bf, 4, 16, 16384, *r2) == 4          # 64 units: 8-page groups, 4 splits
     for dt in (bf, f32):
-        assert lla.decode_splits(dt, 2, 16, 32768) == 8
-        assert lla.decode_splits(dt, 1, 16, 32768, with_workspace=False) == 1
-        assert lla.decode_splits(dt, 1, 16, 512) == 1
+        assert lla.decode_splits(dt, 2, 16, 32768, *r2) == 8
+        assert lla.decode_splits(dt, 1, 16, 32768, *r2, with_workspace=False) == 1
+        assert lla.decode_splits(dt, 1, 16, 512, *r2) == 1
+    # more than 16 row blocks (8-row key blocks with the rotary rows, or value
+    # groups): 16-page slices where 8-page ones would need two workgroups per
+    # compute unit; smaller ranks keep the general kernel's shapes
+    assert lla.decode_splits(bf, 1, 16, 16384, *r2) == 16
+    assert lla.decode_splits(bf, 1, 16, 16384, 36, 60) == 8
+    assert lla.decode_splits(bf, 2, 16, 8192, 288, 480) == 8
+    assert lla.decode_splits(bf, 2, 16, 8192, 36, 60) == 4
+    assert lla.decode_splits(bf, 2, 16, 8192, 64, 128) == 4       # 16 row blocks
+    assert lla.decode_splits(bf, 2, 16, 8192, 64, 64, 72) == 8    # 8 + 9 key blocks
+    assert lla.decode_splits(f32, 1, 16, 16384, *r2) == 4
     with pytest.raises(lla.LLAError):
-        lla.decode_splits(bf, 0, 16, 4096)
+        lla.decode_splits(bf, 0, 16, 4096, *r2)
+    with pytest.raises(lla.LLAError):
+        lla.decode_splits(bf, 1, 16, 4096, 0, 320)
+    with pytest.raises(lla.LLAError):
+        lla.decode_splits(bf, 1, 16, 4096, 192, 320, -8)
 
 
 def test_status_strings():

@@ -161,7 +161,7 @@ def test_split_k_long_context(dtype, N, splits_f32, splits_bf16):
     splits = splits_bf16 if dtype == torch.bfloat16 else splits_f32  # bf16 at 4096: row-split slices
     r_k, r_v = (96, 160) if dtype == torch.float32 else (36, 60)
     wl = W.Workload("split_k", 1, H, 128, 4, B, N, ((r_k, r_v),), dtype)
-    assert lla.decode_splits(dtype, B, H, N) == splits
+    assert lla.decode_splits(dtype, B, H, N, r_k, r_v) == splits
     log(f"split-K {dtype} N={N} splits={splits}")
     ck, cv, q, uk, uv, muk, muv, pk, pv = _case(wl, r_k, r_v, B, N, N, 0, 1, True, dtype)
     ws = lla.new_workspace(B, H, r_v, N)
@@ -210,7 +210,7 @@ def test_split_k_long_context(dtype, N, splits_f32, splits_bf16):
                                      (250, 380), (300, 440), (288, 480), (512, 512)])
 def test_split_k_row_split_every_rank_bucket(r_k, r_v, B):
     H, N, dtype = 16, 4096, torch.bfloat16
-    assert lla.decode_splits(dtype, B, H, N) == 8
+    assert lla.decode_splits(dtype, B, H, N, r_k, r_v) == 8
     log(f"row-split slices B={B} r=({r_k},{r_v})")
     wl = W.Workload("split_rows", 1, H, 128, 4, B, N, ((r_k, r_v),), dtype)
     ck, cv, q, uk, uv, muk, muv, pk, pv = _case(wl, r_k, r_v, B, N, N, 0, 2, True, dtype)
@@ -233,6 +233,38 @@ def test_split_k_row_split_every_rank_bucket(r_k, r_v, B):
     assert int(counters.abs().sum()) == 0
 
 
+# 16-page slices of the row-split kernel (each slice two 8-page groups, walked
+# one after the other): ranks with more than 16 row blocks, where 8-page slices
+# would need more than one workgroup per compute unit.
+@pytest.mark.parametrize("B,N,r_k,r_v", [(1, 16384, 192, 320), (1, 16384, 512, 512), (2, 8192, 288, 480),
+                                         (2, 8192, 96, 160), (4, 4096, 130, 250)])
+def test_split_k_row_split_long_slices(B, N, r_k, r_v):
+    H, dtype = 16, torch.bfloat16
+    pages = N // 64
+    splits = lla.decode_splits(dtype, B, H, N, r_k, r_v)
+    assert splits == (pages + 15) // 16 and B * H * splits <= 256
+    log(f"row-split 16-page slices B={B} N={N} r=({r_k},{r_v}) splits={splits}")
+    wl = W.Workload("split_long", 1, H, 128, 4, B, N, ((r_k, r_v),), dtype)
+    ck, cv, q, uk, uv, muk, muv, pk, pv = _case(wl, r_k, r_v, B, N, N, 0, 3, True, dtype)
+    ws = lla.new_workspace(B, H, r_v, N)
+    ck64, cv64 = f64_dev(ck), f64_dev(cv)
+    q64, uk64, uv64, muk64, muv64 = f64(q), f64(uk), f64(uv), f64(muk), f64(muv)
+    del ck, cv
+
+    def ref(lens):
+        return np.stack([np.stack([oracle.decode_attn_absorbed(q64[b, h], ck64[b, h, :lens[b]], cv64[b, h, :lens[b]],
+                                                               uk64[h], uv64[h], muk64[h], muv64[h])
+                                   for h in range(H)]) for b in range(B)])
+
+    # full; a slice boundary inside a group (1100 tokens: 17.2 pages); one token
+    for lens in ([N] * B, [N - 1100] + [1100] * (B - 1), [1] + [N - 5] * (B - 1)):
+        ctx = torch.tensor(lens, dtype=torch.int32, device=DEV)
+        out = lla.decode_attn(q, pk, pv, uk, uv, n_ctx=N, ctx_len=ctx, mu_k=muk, mu_v=muv, workspace=ws)
+        torch.cuda.synchronize()
+        assert_close(f64(out), ref(lens), dtype, f"lens={lens}")
+    assert int(ws[:4 * B * H].view(torch.int32).abs().sum()) == 0
+
+
 # ---------------------------------------------------------------------------
 # Properties of the launch shape: the same sequences give the same outputs
 # (up to the order of the fp32 sums) whether their contexts are split across
@@ -247,7 +279,7 @@ def test_independent_of_split_count_and_workgroup_size(dtype):
     wl = W.Workload("shape_prop", 1, H, 128, 4, 2, N, ((r_k, r_v),), dtype)
     ck, cv, q, uk, uv, muk, muv, pk, pv = _case(wl, r_k, r_v, 2, N, N, 0, 3, True, dtype)
     big_b = 64  # 1024 (b, h) units: every compute unit busy without splitting
-    assert lla.decode_splits(dtype, 2, H, N) > 1 and lla.decode_splits(dtype, big_b, H, N) == 1
+    assert lla.decode_splits(dtype, 2, H, N, r_k, r_v) > 1 and lla.decode_splits(dtype, big_b, H, N, r_k, r_v) == 1
     pk_big = torch.zeros((big_b,) + tuple(pk.shape[1:]), dtype=dtype, device=DEV)
     pv_big = torch.zeros((big_b,) + tuple(pv.shape[1:]), dtype=dtype, device=DEV)
     q_big = torch.zeros((big_b,) + tuple(q.shape[1:]), dtype=dtype, device=DEV)

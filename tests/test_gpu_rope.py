@@ -159,15 +159,18 @@ def test_prefill_rope(dtype, r_k, r_v, dr, Hr, M, p0):
     assert_close(f64(out), ref, dtype, "prefill rope")
 
 
-@pytest.mark.parametrize("N,r_k,r_v,Hr", [(32768, 96, 160, 1), (32768, 192, 320, 16), (131072, 96, 160, 1)])
+@pytest.mark.parametrize("N,r_k,r_v,Hr", [(32768, 96, 160, 1), (32768, 192, 320, 16), (131072, 96, 160, 1),
+                                           (16384, 96, 160, 1), (16384, 192, 320, 16)])
 def test_decode_rope_split_k(N, r_k, r_v, Hr):
     """One sequence of 16 heads over a long context with the rotary branch,
     the shape of the absorbed-against-rebuilt latency comparison (App. J):
     the launch splits each (b, h) context over 16 workgroups of 8 wavefronts
-    (4-page K groups at 32,768 tokens, 8-page groups at 131,072) and merges
-    their partial states.  Full and ragged lengths, every head checked."""
+    (4-page K groups at 32,768 tokens, 8-page groups at 131,072, the row-split
+    kernel's 16-page slices at 16,384) and merges their partial states.  Full
+    and ragged lengths, every head checked."""
     B, H, dr, dtype = 1, 16, 64, torch.bfloat16
-    assert lla.decode_splits(dtype, B, H, N) == 16
+    # (16,384 tokens: the row-split kernel over 16-page slices, 20 or more row blocks)
+    assert lla.decode_splits(dtype, B, H, N, r_k, r_v, dr) == 16
     wl = W.Workload("rope_split", 1, H, 128, 4, B, N, ((r_k, r_v),), dtype)
     log(f"decode rope split-K N={N} r=({r_k},{r_v}) Hr={Hr}")
     ck, cv, kr, q, qr, uk, uv, muk, muv, rc = _decode_case(wl, r_k, r_v, dr, Hr, B, N, N, dtype, True)

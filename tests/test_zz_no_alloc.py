@@ -28,7 +28,7 @@ def _case(dtype, B, H, N, r_k, r_v, seed):
 
 def _check(dtype, B, H, N, r_k, r_v, seed, lens=None):
     q, ck, cv, uk, uv, muk, muv, pk, pv = _case(dtype, B, H, N, r_k, r_v, seed)
-    splits = lla.decode_splits(dtype, B, H, N)
+    splits = lla.decode_splits(dtype, B, H, N, r_k, r_v)
     log(f"noalloc {dtype} B={B} H={H} N={N} r=({r_k},{r_v}) splits={splits} lens={lens}")
     ctx = None if lens is None else torch.tensor(lens, dtype=torch.int32, device=DEV)
     out = torch.full((B, H, 128), 123.0, dtype=torch.float32, device=DEV)
