@@ -66,7 +66,7 @@
 extern "C" {
 #endif
 
-#define LLA_ABI_VERSION 9
+#define LLA_ABI_VERSION 10
 #define LLA_PAGE_TOKENS 64
 #define LLA_MAX_RANK 512
 #define LLA_MAX_ROPE 256

@@ -28,6 +28,7 @@ LLA_OK, LLA_ERR_INVALID_ARG, LLA_ERR_UNSUPPORTED, LLA_ERR_WORKSPACE, LLA_ERR_HIP
 LLA_F32, LLA_BF16 = 0, 1
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblla.so")
+ABI_VERSION = 10  # LLA_ABI_VERSION of include/lla.h this binding follows
 
 _c_int, _c_i64, _c_vp, _c_f, _c_sz = (ctypes.c_int, ctypes.c_int64, ctypes.c_void_p,
                                       ctypes.c_float, ctypes.c_size_t)
@@ -74,6 +75,9 @@ def lib() -> ctypes.CDLL:
             fn = getattr(h, name)
             fn.restype = res
             fn.argtypes = args
+        if h.lla_abi_version() != ABI_VERSION:  # argument lists differ between versions
+            raise RuntimeError(f"{LIB_PATH} has ABI version {h.lla_abi_version()}, this binding "
+                               f"needs {ABI_VERSION}; rebuild it")
         _lib = h
     return _lib
 

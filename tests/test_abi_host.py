@@ -44,7 +44,7 @@ def test_library_exports_every_declared_symbol():
     h = ctypes.CDLL(lla.LIB_PATH)
     for name in _declared():
         assert hasattr(h, name), name
-    assert lla.abi_version() == 9
+    assert lla.abi_version() == 10
 
 
 def test_decode_split_choice():
