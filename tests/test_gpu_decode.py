@@ -233,17 +233,19 @@ def test_split_k_row_split_every_rank_bucket(r_k, r_v, B):
     assert int(counters.abs().sum()) == 0
 
 
-# 16-page slices of the row-split kernel (each slice two 8-page groups, walked
-# one after the other): ranks with more than 16 row blocks, where 8-page slices
-# would need more than one workgroup per compute unit.
-@pytest.mark.parametrize("B,N,r_k,r_v", [(1, 16384, 192, 320), (1, 16384, 512, 512), (2, 8192, 288, 480),
-                                         (2, 8192, 96, 160), (4, 4096, 130, 250)])
-def test_split_k_row_split_long_slices(B, N, r_k, r_v):
+# Longer slices of the row-split kernel (two or four 8-page groups, walked one
+# after the other): ranks with more than 16 (40) row blocks, where shorter
+# slices would need more than one workgroup per compute unit.
+@pytest.mark.parametrize("B,N,r_k,r_v,slice_pages", [(1, 16384, 192, 320, 16), (1, 16384, 512, 512, 16),
+                                                     (2, 8192, 288, 480, 16), (2, 8192, 96, 160, 16),
+                                                     (4, 4096, 130, 250, 16), (3, 8192, 288, 480, 32),
+                                                     (8, 4096, 400, 330, 32)])
+def test_split_k_row_split_long_slices(B, N, r_k, r_v, slice_pages):
     H, dtype = 16, torch.bfloat16
     pages = N // 64
     splits = lla.decode_splits(dtype, B, H, N, r_k, r_v)
-    assert splits == (pages + 15) // 16 and B * H * splits <= 256
-    log(f"row-split 16-page slices B={B} N={N} r=({r_k},{r_v}) splits={splits}")
+    assert splits == (pages + slice_pages - 1) // slice_pages and B * H * splits <= 256
+    log(f"row-split {slice_pages}-page slices B={B} N={N} r=({r_k},{r_v}) splits={splits}")
     wl = W.Workload("split_long", 1, H, 128, 4, B, N, ((r_k, r_v),), dtype)
     ck, cv, q, uk, uv, muk, muv, pk, pv = _case(wl, r_k, r_v, B, N, N, 0, 3, True, dtype)
     ws = lla.new_workspace(B, H, r_v, N)
