@@ -168,10 +168,11 @@ DecodeShape choose_shape(int units, int n_ctx, bool allow_split, bool bf16, int 
   if (bf16 && allow_split && 2L * units * 4 <= target && pages > 8 && forced_short >= 0 &&
       !forced_waves && !forced_splits && !forced_half) {
     // slices of k 8-page groups, the shortest that fits; longer slices only at
-    // larger ranks (16-page slices above 16 row blocks, 32-page ones above 40:
-    // measured faster than the general kernel's shapes there, slower below)
+    // larger ranks (16-page slices above 16 row blocks, up to 64-page ones
+    // above 40: measured faster than the general kernel's shapes there,
+    // slower below)
     const int max_groups = forced_short_groups > 0 ? forced_short_groups
-                           : row_blocks > 40       ? 4
+                           : row_blocks > 40       ? 8
                            : row_blocks > 16       ? 2
                                                    : 1;
     for (int k = 1; k <= max_groups; ++k) {

@@ -233,13 +233,13 @@ def test_split_k_row_split_every_rank_bucket(r_k, r_v, B):
     assert int(counters.abs().sum()) == 0
 
 
-# Longer slices of the row-split kernel (two or four 8-page groups, walked one
-# after the other): ranks with more than 16 (40) row blocks, where shorter
+# Longer slices of the row-split kernel (2, 4 or 8 groups of 8 pages, walked
+# one after the other): ranks with more than 16 (40) row blocks, where shorter
 # slices would need more than one workgroup per compute unit.
 @pytest.mark.parametrize("B,N,r_k,r_v,slice_pages", [(1, 16384, 192, 320, 16), (1, 16384, 512, 512, 16),
                                                      (2, 8192, 288, 480, 16), (2, 8192, 96, 160, 16),
                                                      (4, 4096, 130, 250, 16), (3, 8192, 288, 480, 32),
-                                                     (8, 4096, 400, 330, 32)])
+                                                     (8, 4096, 400, 330, 32), (4, 16384, 288, 480, 64)])
 def test_split_k_row_split_long_slices(B, N, r_k, r_v, slice_pages):
     H, dtype = 16, torch.bfloat16
     pages = N // 64
