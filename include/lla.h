@@ -218,7 +218,8 @@ lla_status lla_decode_attn(int dtype, int out_dtype, int B, int H, int d_head, i
  * Errors: as lla_decode_attn, and LLA_ERR_SCRATCH when the split the launch
  * heuristic chooses needs more than LLA_NOALLOC_SCRATCH_BYTES (4 bytes per
  * (b, h) unit rounded up to 256, plus 4 * (r_v + 2) bytes per unit and split;
- * on a 256-CU MI355X the default heuristic stays below 1.1 MiB).
+ * on a 256-CU MI355X the default heuristic splits at most 768 unit-slices, so
+ * it stays below 1.6 MiB at r_v = 512).
  */
 lla_status lla_decode_attn_noalloc(int dtype, int out_dtype, int B, int H, int d_head, int r_k,
                                    int r_v, int n_max, int n_ctx, const int32_t* ctx_len,

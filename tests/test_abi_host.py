@@ -473,3 +473,28 @@ def _prefill_2d(**kw):
 ])
 def test_prefill_2d_rejects(kw, code):
     assert _prefill_2d(**kw) == code
+
+
+def test_noalloc_scratch_bound_over_shapes():
+    """The non-allocating decode needs (4 bytes per (b, h) rounded up to 256)
+    plus 4 (r_v + 2) bytes per unit and split when the launch splits.  On a
+    256-CU MI355X the shape heuristic splits only below 512 units, and takes
+    at most 768 unit-slices (the bf16 4-page shapes below 256 units), so that
+    stays below 1.6 MiB at r_v = 512, inside LLA_NOALLOC_SCRATCH_BYTES (4 MiB).
+    Checked for every unit count that can split and page counts up to 4096."""
+    import ctypes
+    f, out = lla.lib().lla_decode_splits, ctypes.c_int()
+    pages_set = list(range(1, 65)) + list(range(72, 4097, 8))
+    worst, worst_slices = 0, 0
+    for dt in (lla.LLA_BF16, lla.LLA_F32):
+        for r_k, r_v in ((18, 30), (192, 320), (512, 512)):
+            for units in range(1, 520):
+                for p in pages_set:
+                    assert f(dt, units, 1, p * 64, r_k, r_v, 0, 1, ctypes.byref(out)) == 0
+                    s = out.value
+                    if s > 1:
+                        assert units < 512
+                        worst_slices = max(worst_slices, units * s)
+                        worst = max(worst, (units * 4 + 255) // 256 * 256 + units * s * (r_v + 2) * 4)
+    assert worst_slices <= 768, worst_slices
+    assert worst <= int(1.6 * 2**20) and worst <= 4 << 20, worst
