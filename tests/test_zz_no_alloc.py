@@ -68,6 +68,14 @@ def test_noalloc_matches_workspace_decode_twice_smaller_second(dtype):
     assert _check(dtype, 2, 16, 16384, r_k, r_v, 5, lens=[5000, 16383]) > 1
 
 
+def test_noalloc_largest_scratch_shape():
+    """The shape that needs the most static scratch under the launch heuristic
+    (255 (b, h) units over 48 pages at r_v = 512, bf16: 3 splits, 1.50 MiB of
+    the array), then a smaller split call over the same array."""
+    assert _check(torch.bfloat16, 255, 1, 3072, 512, 512, 7) == 3
+    assert _check(torch.bfloat16, 4, 1, 3072, 512, 512, 8, lens=[3000, 1, 2999, 64]) > 1
+
+
 def test_noalloc_rejects_bad_arguments_before_launch():
     q, ck, cv, uk, uv, muk, muv, pk, pv = _case(torch.bfloat16, 1, 16, 1024, 36, 60, 6)
     out = torch.zeros((1, 16, 128), device=DEV)
