@@ -267,6 +267,26 @@ def test_split_k_row_split_long_slices(B, N, r_k, r_v, slice_pages):
     assert int(ws[:4 * B * H].view(torch.int32).abs().sum()) == 0
 
 
+# Batches of 129-256 (b, h) units over up to 128 pages at 17-60 row blocks:
+# the row-split kernel with 8 wavefronts, one workgroup per (b, h) walking
+# every 8-page group of its context in turn (not split).
+@pytest.mark.parametrize("B,N,r_k,r_v", [(16, 2048, 288, 480), (16, 4096, 192, 320), (9, 8192, 96, 160)])
+def test_row_split_whole_contexts(B, N, r_k, r_v):
+    H, dtype = 16, torch.bfloat16
+    assert lla.decode_splits(dtype, B, H, N, r_k, r_v) == 1
+    log(f"row-split whole contexts B={B} N={N} r=({r_k},{r_v})")
+    wl = W.Workload("rows_whole", 1, H, 128, 4, B, N, ((r_k, r_v),), dtype)
+    ck, cv, q, uk, uv, muk, muv, pk, pv = _case(wl, r_k, r_v, B, N, N, 0, 1, True, dtype)
+    lens = [N, 1, N - 777, 64 * 17 + 9] + [N - 64 * b for b in range(B - 4)]
+    ref = _oracle(q, ck, cv, uk, uv, muk, muv, ctx_len=lens)
+    del ck, cv
+    ctx = torch.tensor(lens, dtype=torch.int32, device=DEV)
+    for w in (None, lla.new_workspace(B, H, r_v, N)):
+        out = lla.decode_attn(q, pk, pv, uk, uv, n_ctx=N, ctx_len=ctx, mu_k=muk, mu_v=muv, workspace=w)
+        torch.cuda.synchronize()
+        assert_units_close(f64(out), ref, f"every (b, h), ws={'yes' if w is not None else 'no'}")
+
+
 # ---------------------------------------------------------------------------
 # Properties of the launch shape: the same sequences give the same outputs
 # (up to the order of the fp32 sums) whether their contexts are split across
