@@ -70,9 +70,9 @@ size_t workspace_bytes(int B, int H, int r_v, int n_ctx) {
 // wavefronts per compute unit, with every wavefront keeping at least one
 // 8-page group (bf16: one 4-page group when that fills more of the machine).
 // bf16 workgroups with fewer 8-page groups than wavefronts use the 4-page K
-// groups.  LLA_DECODE_WAVES / LLA_DECODE_SPLITS /
-// LLA_DECODE_DEEP / LLA_DECODE_HALF / LLA_DECODE_SHORT / LLA_DECODE_SHORT_WAVES
-// override the choice (for tuning sweeps).
+// groups.  LLA_DECODE_WAVES / LLA_DECODE_SPLITS / LLA_DECODE_DEEP /
+// LLA_DECODE_HALF / LLA_DECODE_SHORT / LLA_DECODE_SHORT_WAVES /
+// LLA_DECODE_SHORT_GROUPS override the choice (for tuning sweeps).
 struct DecodeShape {
   int waves, splits, deep, half, shortk;
 };
