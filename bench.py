@@ -795,18 +795,24 @@ def run_absorbed_latency(args, torch, lla, W):
 # ---------------------------------------------------------------------------
 
 SPLIT_K_SHAPES = ((1, 32768), (1, 8192), (1, 4096), (2, 8192), (4, 16384))  # (sequences, context)
+# batches of 9-16 sequences (129-256 (b, h) units) over short contexts, which the
+# row-split kernel takes whole at ranks of 17-60 row blocks
+FEW_UNIT_SHAPES = ((16, 2048), (16, 4096), (12, 8192))
 
 
 def run_split_k(args, torch, lla, W):
     """One loop-l decode call per shape where the (b, h) units alone leave the
     machine idle, so the launch splits every context over workgroups and merges
-    the partial softmax states: Ouro-1.4B geometry, 16 heads, d_head 128,
-    (192, 320), bf16, with a workspace; HIP events around each call."""
+    the partial softmax states, then the few-unit batches: Ouro-1.4B geometry,
+    16 heads, d_head 128, (192, 320) unless --ranks says otherwise, bf16, with a
+    workspace; HIP events around each call."""
     H, d, r_k, r_v = 16, 128, 192, 320
+    if args.ranks:
+        r_k, r_v = (int(v) for v in args.ranks.split(","))
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream(dev)
     rows = []
-    for B, N in SPLIT_K_SHAPES:
+    for B, N in SPLIT_K_SHAPES + FEW_UNIT_SHAPES:
         print(f"[bench] split_k B={B} N={N}", file=sys.stderr, flush=True)
         wl = W.Workload("split_k", 1, H, d, 4, B, N, ((r_k, r_v),), torch.bfloat16)
         ck = W.normal((B, H, N // 64, r_k, 64), (wl.name, "c_k", B, N), 1.0, wl.dtype, dev)
@@ -837,8 +843,9 @@ def run_split_k(args, torch, lla, W):
         "value": round(head["batch"] / (head["call_ms"] * 1e-3), 1), "unit": "tokens/s (one call, first shape)",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": head["call_ms"],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": "one loop-l decode call, Ouro-1.4B geometry, 16 heads, d_head 128, (192, 320), "
-                               "split over workgroups", "shapes": [list(x) for x in SPLIT_K_SHAPES],
+        "config": {"workload": f"one loop-l decode call, Ouro-1.4B geometry, 16 heads, d_head 128, ({r_k}, {r_v}), "
+                               "split over workgroups, then batches of 129-256 (b, h) units",
+                   "shapes": [list(x) for x in SPLIT_K_SHAPES + FEW_UNIT_SHAPES], "r_k": r_k, "r_v": r_v,
                    "parallelism": "single GPU"},
         "shapes": rows,
         "roofline": {"bound": "hbm", "achieved": head["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
