@@ -184,13 +184,13 @@ DecodeShape choose_shape(int units, int n_ctx, bool allow_split, bool bf16, int 
     }
   }
   // Between half and all of the compute units' worth of (b, h) units over up
-  // to 128 pages, at ranks of 17 to 60 row blocks: the row-split kernel with 8
-  // wavefronts, one workgroup per (b, h) walking all its groups, measured
-  // faster than the general kernel's shapes (which split these contexts or
-  // give each wavefront whole 8-page groups).
+  // to 128 pages at 16 to 60 row blocks, or up to 32 pages at any rank: the
+  // row-split kernel with 8 wavefronts, one workgroup per (b, h) walking all
+  // its groups, measured faster than the general kernel's shapes (which split
+  // these contexts or give each wavefront whole 8-page groups).
   if (bf16 && !sh.shortk && forced_short >= 0 && !forced_waves && !forced_splits && !forced_half &&
-      2L * units > lla::device_cu_count() && units <= lla::device_cu_count() && row_blocks > 16 &&
-      row_blocks <= 60 && pages <= 128)
+      2L * units > lla::device_cu_count() && units <= lla::device_cu_count() && row_blocks <= 60 &&
+      pages <= 128 && (row_blocks >= 16 || pages <= 32))
     sh = DecodeShape{short_waves(units), 1, 1, 0, 1};
   return sh;
 }

@@ -80,10 +80,13 @@ def test_decode_split_choice():
     assert lla.decode_splits(bf, 2, 16, 8192, 64, 128) == 4       # 16 row blocks
     assert lla.decode_splits(bf, 2, 16, 8192, 64, 64, 72) == 8    # 8 + 9 key blocks
     assert lla.decode_splits(f32, 1, 16, 16384, *r2) == 4
-    # 129-256 units over at most 128 pages at 17-60 row blocks: one row-split
-    # workgroup per (b, h), not split; smaller ranks keep the general kernel's 2
+    # 129-256 units over at most 128 pages at 16-60 row blocks (or at most 32
+    # pages at any rank): one row-split workgroup per (b, h), not split;
+    # smaller ranks over longer contexts keep the general kernel's 2
     assert lla.decode_splits(bf, 16, 16, 2048, 288, 480) == 1
-    assert lla.decode_splits(bf, 16, 16, 2048, 36, 60) == 2
+    assert lla.decode_splits(bf, 16, 16, 2048, 36, 60) == 1
+    assert lla.decode_splits(bf, 12, 16, 8192, 64, 128) == 1
+    assert lla.decode_splits(bf, 12, 16, 8192, 36, 60) == 2
     with pytest.raises(lla.LLAError):
         lla.decode_splits(bf, 0, 16, 4096, *r2)
     with pytest.raises(lla.LLAError):

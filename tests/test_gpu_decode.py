@@ -267,10 +267,12 @@ def test_split_k_row_split_long_slices(B, N, r_k, r_v, slice_pages):
     assert int(ws[:4 * B * H].view(torch.int32).abs().sum()) == 0
 
 
-# Batches of 129-256 (b, h) units over up to 128 pages at 17-60 row blocks:
-# the row-split kernel with 8 wavefronts, one workgroup per (b, h) walking
-# every 8-page group of its context in turn (not split).
-@pytest.mark.parametrize("B,N,r_k,r_v", [(16, 2048, 288, 480), (16, 4096, 192, 320), (9, 8192, 96, 160)])
+# Batches of 129-256 (b, h) units over up to 128 pages at 16-60 row blocks
+# (or up to 32 pages at any rank): the row-split kernel with 8 wavefronts, one
+# workgroup per (b, h) walking every 8-page group of its context in turn (not
+# split).
+@pytest.mark.parametrize("B,N,r_k,r_v", [(16, 2048, 288, 480), (16, 4096, 192, 320), (9, 8192, 96, 160),
+                                         (12, 8192, 64, 128), (16, 2048, 36, 60), (10, 1984, 18, 30)])
 def test_row_split_whole_contexts(B, N, r_k, r_v):
     H, dtype = 16, torch.bfloat16
     assert lla.decode_splits(dtype, B, H, N, r_k, r_v) == 1
