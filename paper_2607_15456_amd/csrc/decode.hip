@@ -616,10 +616,13 @@ void decode_kernel(DecodeArgs a) {
   }
 }
 
-// Short contexts (at most a few 8-page groups per (b, h)), bf16: the W = 4
-// or 8 wavefronts of a workgroup split the feature rows of each 8-page group
-// instead of its pages, so a group's loads are spread over every wavefront
-// whatever the page count.
+// Row-split decode, bf16: the W = 4 or 8 wavefronts of a workgroup split the
+// feature rows of each 8-page group instead of its pages, so a group's loads
+// are spread over every wavefront whatever the page count.  A workgroup walks
+// the groups of its (b, h) context, or of one slice of it (SPLIT), in turn;
+// the launch heuristic uses it for short contexts, for slices of 8 to 64
+// pages when few (b, h) units split their contexts, and for whole contexts of
+// up to 128 pages in batches of one compute unit's worth of (b, h) or less.
 //   * K phase -- wave w takes the 8-row blocks w, w + W, ... of the content
 //     rows and then of the rotary rows; lane (pg, ts) owns tokens ts*8.. of
 //     page pg, so one wave-wide load reads one feature row of all 8 pages.
@@ -983,7 +986,7 @@ void decode_short_kernel(DecodeArgs a) {
 template <typename TIn, int GV>
 hipError_t launch_t(const DecodeArgs& a, hipStream_t stream) {
   dim3 grid(a.B * a.M * a.splits, a.H);
-  if (a.shortk) {  // at most 16 pages per workgroup, rows split over the wavefronts: bf16, decode
+  if (a.shortk) {  // row-split kernel (rows of each 8-page group split over the wavefronts): bf16, decode
     if constexpr (sizeof(TIn) == 2) {
       if (a.causal || a.M != 1) return hipErrorInvalidValue;
       if (a.waves != 4 && a.waves != 8) return hipErrorInvalidValue;
