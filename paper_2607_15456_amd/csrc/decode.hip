@@ -230,6 +230,8 @@ void decode_kernel(DecodeArgs a) {
   // row offsets of the buffer loads in scalar registers
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  // (launch order: the XCD head order below measured 0.8% slower for this
+  // kernel on the Ouro-1.4B step)
   const int bm = blockIdx.x / a.splits, split = blockIdx.x - bm * a.splits, h = blockIdx.y;
   int b, m, N;
   if (a.causal) {
@@ -667,8 +669,10 @@ void decode_short_kernel(DecodeArgs a) {
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   // SPLIT: the workgroup takes one slice of its (b, h) context (split-K)
-  const int b = SPLIT ? blockIdx.x / a.splits : blockIdx.x, h = blockIdx.y;
-  const int split = SPLIT ? blockIdx.x - b * a.splits : 0;
+  int bx, h;
+  xcd_head_order(bx, h, !(a.dr > 0 && a.Hr == 1));  // a shared rotary key keeps a sequence's heads together
+  const int b = SPLIT ? bx / a.splits : bx;
+  const int split = SPLIT ? bx - b * a.splits : 0;
   const int N = a.ctx_len ? a.ctx_len[b] : a.n_ctx;
   const bool bad = (N < 1) || (N > a.n_ctx);
   const int pages = bad ? 0 : (N + kPage - 1) / kPage;

@@ -73,6 +73,26 @@ __device__ __forceinline__ uint4 ld16_nt(const void* p) {
 // write-back runs.
 __device__ __forceinline__ void wait_stores_in_l2() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
+// Workgroup coordinates (x, y = head) renumbered so that every workgroup of a
+// head runs on one XCD: the linear workgroup i = x + gridDim.x * y is
+// dispatched to XCD i % 8, so when the head count is a multiple of 8, XCD c
+// takes heads c, c + 8, ... and its L2 holds only their up-projections
+// (otherwise every XCD fetches every head's).  A bijection on the grid; other
+// head counts, and on = false, keep the launch order (in which all heads of a
+// sequence share one XCD: what a rotary key shared by the heads wants).
+__device__ __forceinline__ void xcd_head_order(int& x, int& y, bool on) {
+  const int gy = gridDim.y;
+  if (!on || gy % 8) {
+    x = blockIdx.x;
+    y = blockIdx.y;
+    return;
+  }
+  const int i = blockIdx.x + gridDim.x * blockIdx.y;
+  const int j = i >> 3, hp = gy >> 3;
+  y = (i & 7) + 8 * (j % hp);
+  x = j / hp;
+}
+
 // ---- cross-lane ----------------------------------------------------------
 
 __device__ __forceinline__ float xor_shfl(float v, int mask) { return __shfl_xor(v, mask, kWave); }
