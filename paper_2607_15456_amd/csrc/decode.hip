@@ -230,9 +230,13 @@ void decode_kernel(DecodeArgs a) {
   // row offsets of the buffer loads in scalar registers
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
-  // (launch order: the XCD head order below measured 0.8% slower for this
-  // kernel on the Ouro-1.4B step)
-  const int bm = blockIdx.x / a.splits, split = blockIdx.x - bm * a.splits, h = blockIdx.y;
+  // XCD head order only in the 4-page-group variant, which serves split
+  // launches of few (b, h) units (in the 8-page variant it measured 0.8%
+  // slower on the unsplit Ouro-1.4B step)
+  int bx, h;
+  xcd_head_order(bx, h, HALF && a.splits > 1 && !(a.dr > 0 && a.Hr == 1));
+  const unsigned ubx = bx;  // a workgroup index: unsigned division, as on blockIdx
+  const int bm = ubx / a.splits, split = ubx - bm * a.splits;
   int b, m, N;
   if (a.causal) {
     b = bm / a.M;
@@ -671,8 +675,9 @@ void decode_short_kernel(DecodeArgs a) {
   // SPLIT: the workgroup takes one slice of its (b, h) context (split-K)
   int bx, h;
   xcd_head_order(bx, h, !(a.dr > 0 && a.Hr == 1));  // a shared rotary key keeps a sequence's heads together
-  const int b = SPLIT ? bx / a.splits : bx;
-  const int split = SPLIT ? bx - b * a.splits : 0;
+  const unsigned ubx = bx;  // a workgroup index: unsigned division, as on blockIdx
+  const int b = SPLIT ? ubx / a.splits : ubx;
+  const int split = SPLIT ? ubx - b * a.splits : 0;
   const int N = a.ctx_len ? a.ctx_len[b] : a.n_ctx;
   const bool bad = (N < 1) || (N > a.n_ctx);
   const int pages = bad ? 0 : (N + kPage - 1) / kPage;
